@@ -1,0 +1,376 @@
+/*
+ * CPU oracle of the MAPS scheduler core.  TEST INFRASTRUCTURE ONLY: the tests,
+ * the smoke check and the benchmark's CPU-baseline leg may load it; the product
+ * path never does.  It shares no code, header or table with the GPU library.
+ *
+ * Plain, slow and direct: every quantity is computed from its definition in
+ * the paper, in 64-bit integers, one decoding step at a time.
+ *
+ *   calibration  Sec. 3.2, Eqs. (2)-(4): one-sided nonconformity score, the
+ *                conformal rank ceil((1-alpha)(n+1)), the calibrated bound;
+ *                applied per length bucket of the prediction.
+ *   occupancy    Sec. 3.3 and App. A, Eqs. (8) and (10): the KV footprint of a
+ *                request grows one token per decoding step ("token by token",
+ *                Sec. 3.3) until its bound runs out.
+ *   placement    Algorithm 1 / App. C: feasible decoders, minimum-queue choice,
+ *                maximum-capacity fallback, round-robin when no bound exists
+ *                (Eq. (9)), with the static block test replaced by the
+ *                projected peak of the decoder's occupancy plus the arrival.
+ *   local order  Sec. 3.3, Eq. (7): argsort of the queue by the bound, with
+ *                starvation promotion, and the App. A admission rule (10)
+ *                applied to the reordered queue.
+ *
+ * Readings of points the paper leaves open (all listed in the design doc):
+ *   - alpha is an integer in parts per million; the rank is an exact integer
+ *     ceiling.  A rank above the bucket size gives an infinite quantile, and
+ *     the bound is then the cap u_max.  Bounds are capped at u_max.
+ *   - a request is bucketed by its prediction: #{edges <= pred}.
+ *   - a resident with prompt p, generated g and bound U holds p+g+t tokens at
+ *     future step t while t <= R = max(U-g, 0); an arrival with bound U holds
+ *     p+t while t <= U.  Step 0 is the present.
+ *   - feasible means peak <= capacity; ties go to the lowest decoder index.
+ *   - a negative prediction means "no prediction": the bound is -1, and a
+ *     negative bound routes the arrival round-robin.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_Q_INF INT32_MAX
+#define ORACLE_POLICY_MQ 0
+#define ORACLE_POLICY_MC 1
+
+static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+static int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+
+/* ------------------------------------------------------------------------ */
+/* Calibration (Sec. 3.2)                                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Length bucket of a prediction: the number of edges not above it. */
+int32_t oracle_bucket(int32_t pred, const int32_t* edges, int32_t nb)
+{
+    int32_t b = 0;
+    for (int32_t j = 0; j < nb - 1; ++j)
+        if (edges[j] <= pred) b += 1;
+    return b;
+}
+
+/* Eq. (3): k = ceil((1 - alpha) * (n + 1)), alpha = alpha_ppm / 10^6. */
+int64_t oracle_conformal_rank(int64_t n, int32_t alpha_ppm)
+{
+    int64_t num = (int64_t)(1000000 - alpha_ppm) * (n + 1);
+    return (num + 999999) / 1000000;
+}
+
+static int cmp_i64(const void* a, const void* b)
+{
+    int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+    return (x > y) - (x < y);
+}
+
+/* Eqs. (2)-(3) per bucket: q[b] is the k-th smallest score of bucket b
+ * (1-indexed, multiset), or ORACLE_Q_INF when k exceeds the bucket size. */
+int oracle_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
+                     const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                     int32_t* q_out, int32_t* count_out)
+{
+    if (nb < 1 || alpha_ppm <= 0 || alpha_ppm >= 1000000 || n < 0) return -1;
+    int64_t* count = (int64_t*)calloc((size_t)nb, sizeof(int64_t));
+    int64_t* start = (int64_t*)calloc((size_t)nb + 1, sizeof(int64_t));
+    int64_t* fill = (int64_t*)calloc((size_t)nb, sizeof(int64_t));
+    int64_t* scores = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    if (!count || !start || !fill || !scores) return -2;
+
+    for (int64_t i = 0; i < n; ++i) count[oracle_bucket(pred[i], edges, nb)] += 1;
+    for (int32_t b = 0; b < nb; ++b) start[b + 1] = start[b] + count[b];
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t b = oracle_bucket(pred[i], edges, nb);
+        /* Eq. (2): s = (L - L_hat)_+ */
+        int64_t s = max64(0, (int64_t)truth[i] - (int64_t)pred[i]);
+        scores[start[b] + fill[b]] = s;
+        fill[b] += 1;
+    }
+    for (int32_t b = 0; b < nb; ++b) {
+        int64_t nb_b = count[b];
+        qsort(scores + start[b], (size_t)nb_b, sizeof(int64_t), cmp_i64);
+        int64_t k = oracle_conformal_rank(nb_b, alpha_ppm);
+        q_out[b] = (k <= nb_b) ? (int32_t)scores[start[b] + k - 1] : ORACLE_Q_INF;
+        count_out[b] = (int32_t)nb_b;
+    }
+    free(count); free(start); free(fill); free(scores);
+    return 0;
+}
+
+/* Eq. (4): U = L_hat + q of the prediction's bucket, capped at u_max; an
+ * infinite quantile gives u_max and a missing prediction (< 0) gives -1. */
+void oracle_apply_bounds(const int32_t* pred, int64_t m, const int32_t* edges, int32_t nb,
+                         const int32_t* q, int32_t u_max, int32_t* U_out)
+{
+    for (int64_t i = 0; i < m; ++i) {
+        if (pred[i] < 0) { U_out[i] = -1; continue; }
+        int32_t qb = q[oracle_bucket(pred[i], edges, nb)];
+        if (qb == ORACLE_Q_INF) U_out[i] = u_max;
+        else U_out[i] = (int32_t)min64((int64_t)pred[i] + qb, u_max);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Occupancy, one decoding step at a time (Sec. 3.3, App. A)                 */
+/* ------------------------------------------------------------------------ */
+
+static int64_t remaining(int32_t U, int32_t g) { return max64((int64_t)U - g, 0); }
+
+/* O[t], t = 0..T: total KV tokens held at step t by the residents still
+ * decoding.  Each resident holds p+g+t and leaves after step R. */
+int oracle_occupancy(const int32_t* p, const int32_t* g, const int32_t* U, int64_t n,
+                     int64_t T, int64_t* O)
+{
+    int64_t* leave_cnt = (int64_t*)calloc((size_t)T + 1, sizeof(int64_t));
+    int64_t* leave_tok = (int64_t*)calloc((size_t)T + 1, sizeof(int64_t));
+    if (!leave_cnt || !leave_tok) return -2;
+    int64_t active = 0, held = 0;   /* requests decoding, and their p+g */
+    for (int64_t r = 0; r < n; ++r) {
+        if (p[r] < 0 || g[r] < 0 || U[r] < 0) { free(leave_cnt); free(leave_tok); return -1; }
+        int64_t R = remaining(U[r], g[r]);
+        if (R > T) { free(leave_cnt); free(leave_tok); return -3; }
+        active += 1;
+        held += (int64_t)p[r] + g[r];
+        leave_cnt[R] += 1;
+        leave_tok[R] += (int64_t)p[r] + g[r];
+    }
+    for (int64_t t = 0; t <= T; ++t) {
+        O[t] = held + t * active;      /* every active request holds p+g+t */
+        active -= leave_cnt[t];        /* those whose last step is t leave */
+        held -= leave_tok[t];
+    }
+    free(leave_cnt); free(leave_tok);
+    return 0;
+}
+
+static int64_t max_remaining(const int32_t* g, const int32_t* U, int64_t lo, int64_t hi)
+{
+    int64_t T = 0;
+    for (int64_t r = lo; r < hi; ++r) T = max64(T, remaining(U[r], g[r]));
+    return T;
+}
+
+/* Peak of the projected occupancy of each decoder on its own. */
+int oracle_project(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                   const int32_t* U, int64_t* base_peak)
+{
+    for (int32_t d = 0; d < D; ++d) {
+        int64_t lo = seg_off[d], hi = seg_off[d + 1];
+        int64_t T = max_remaining(g, U, lo, hi);
+        int64_t* O = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        if (!O) return -2;
+        int rc = oracle_occupancy(p + lo, g + lo, U + lo, hi - lo, T, O);
+        if (rc) { free(O); return rc; }
+        int64_t peak = 0;
+        for (int64_t t = 0; t <= T; ++t) peak = max64(peak, O[t]);
+        base_peak[d] = peak;
+        free(O);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Placement (Algorithm 1 with the projected peak as the feasibility test)   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For every arrival a and decoder d:
+ *   peak(a, d) = max_t [ O_d[t] + (t <= U_a ? p_a + t : 0) ]
+ * taken over the dense step axis.  The maximum splits at U_a into the steps the
+ * arrival is present (t <= U_a, where it adds p_a + t) and the later ones, so
+ *   peak = max( p_a + max_{t<=U_a} (O[t] + t),  max_{t>U_a} O[t] ).
+ * slack = C_d - peak.  Choice (policy MQ): among decoders with slack >= 0 the
+ * smallest queue length Q_d; when there is none, the largest slack.  Policy MC:
+ * the largest slack.  Ties go to the lowest index.  A negative bound routes
+ * the arrival round-robin: d = (rr_offset + i) mod D, i its arrival index.
+ *
+ * pair_peak (nullable) is decoder-major [D][A]; -1 for round-robin arrivals.
+ * a_index (nullable) gives each arrival's index for the round-robin rule.
+ */
+int oracle_place(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                 const int32_t* U, const int32_t* capacity, const int32_t* queue_len,
+                 int64_t A, const int32_t* a_p, const int32_t* a_U, const int64_t* a_index,
+                 int32_t policy, int64_t rr_offset,
+                 int32_t* choice, int64_t* chosen_peak, int64_t* chosen_overflow,
+                 uint8_t* flags, int64_t* pair_peak, int64_t* base_peak)
+{
+    if (D < 1 || A < 0 || (policy != ORACLE_POLICY_MQ && policy != ORACLE_POLICY_MC)) return -1;
+    int64_t maxU = 0;
+    for (int64_t a = 0; a < A; ++a) maxU = max64(maxU, a_U[a]);
+
+    int32_t* feas_d = (int32_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int32_t));
+    int64_t* feas_peak = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    int32_t* fb_d = (int32_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int32_t));
+    int64_t* fb_slack = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    int64_t* fb_peak = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    if (!feas_d || !feas_peak || !fb_d || !fb_slack || !fb_peak) return -2;
+    for (int64_t a = 0; a < A; ++a) { feas_d[a] = -1; fb_d[a] = -1; }
+
+    for (int32_t d = 0; d < D; ++d) {
+        int64_t lo = seg_off[d], hi = seg_off[d + 1];
+        int64_t T = max64(max_remaining(g, U, lo, hi), maxU);
+        int64_t* O = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        int64_t* present = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        int64_t* after = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        if (!O || !present || !after) return -2;
+        int rc = oracle_occupancy(p + lo, g + lo, U + lo, hi - lo, T, O);
+        if (rc) return rc;
+        int64_t peak0 = 0;
+        for (int64_t t = 0; t <= T; ++t) peak0 = max64(peak0, O[t]);
+        if (base_peak) base_peak[d] = peak0;
+        /* present[u] = max_{t<=u} (O[t] + t);  after[u] = max_{t>u} O[t] */
+        for (int64_t t = 0; t <= T; ++t)
+            present[t] = (t == 0) ? O[0] : max64(present[t - 1], O[t] + t);
+        after[T] = 0;                      /* O[t] = 0 beyond T */
+        for (int64_t t = T - 1; t >= 0; --t) after[t] = max64(after[t + 1], O[t + 1]);
+
+        for (int64_t a = 0; a < A; ++a) {
+            if (a_U[a] < 0) {
+                if (pair_peak) pair_peak[(int64_t)d * A + a] = -1;
+                continue;
+            }
+            int64_t peak = max64((int64_t)a_p[a] + present[a_U[a]], after[a_U[a]]);
+            int64_t slack = (int64_t)capacity[d] - peak;
+            if (pair_peak) pair_peak[(int64_t)d * A + a] = peak;
+            if (policy == ORACLE_POLICY_MQ && slack >= 0) {
+                if (feas_d[a] < 0 || queue_len[d] < queue_len[feas_d[a]]) {
+                    feas_d[a] = d;
+                    feas_peak[a] = peak;
+                }
+            }
+            if (fb_d[a] < 0 || slack > fb_slack[a]) {
+                fb_d[a] = d;
+                fb_slack[a] = slack;
+                fb_peak[a] = peak;
+            }
+        }
+        free(O); free(present); free(after);
+    }
+
+    for (int64_t a = 0; a < A; ++a) {
+        if (a_U[a] < 0) {
+            int64_t i = a_index ? a_index[a] : a;
+            choice[a] = (int32_t)((rr_offset + i) % D);
+            chosen_peak[a] = -1;
+            chosen_overflow[a] = 0;
+            flags[a] = 2;
+        } else if (policy == ORACLE_POLICY_MQ && feas_d[a] >= 0) {
+            choice[a] = feas_d[a];
+            chosen_peak[a] = feas_peak[a];
+            chosen_overflow[a] = 0;
+            flags[a] = 1;
+        } else {
+            int64_t c = capacity[fb_d[a]];
+            choice[a] = fb_d[a];
+            chosen_peak[a] = fb_peak[a];
+            chosen_overflow[a] = max64(0, fb_peak[a] - c);
+            flags[a] = (fb_peak[a] <= c) ? 1 : 0;
+        }
+    }
+    free(feas_d); free(feas_peak); free(fb_d); free(fb_slack); free(fb_peak);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Local order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10))           */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t cls;    /* 0: promoted past the maximum wait, 1: otherwise */
+    int64_t val;    /* promoted: queue index (FCFS); otherwise the bound */
+    int64_t idx;    /* queue index, the final tie-break */
+} order_key;
+
+static int cmp_key(const void* a, const void* b)
+{
+    const order_key* x = (const order_key*)a;
+    const order_key* y = (const order_key*)b;
+    if (x->cls != y->cls) return x->cls < y->cls ? -1 : 1;
+    if (x->val != y->val) return x->val < y->val ? -1 : 1;
+    if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;
+    return 0;
+}
+
+/*
+ * Per decoder: order the pending queue by its bounds (Eq. (7)); requests that
+ * waited at least max_wait_ms go first, in arrival order; equal bounds keep
+ * arrival order.  A missing bound (< 0) counts as u_max.  Then admit requests
+ * in that order while the projected peak of the residents plus the admitted
+ * requests (each starting now, g = 0) stays within the capacity: admitted[d]
+ * is the length of that prefix.  order holds queue-local indices.
+ */
+int oracle_local_order(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                       const int32_t* U, const int32_t* capacity, const int64_t* q_off,
+                       const int32_t* q_p, const int32_t* q_U, const int32_t* q_wait,
+                       int32_t max_wait_ms, int32_t u_max, int32_t* order, int32_t* admitted)
+{
+    for (int32_t d = 0; d < D; ++d) {
+        int64_t qlo = q_off[d], nq = q_off[d + 1] - q_off[d];
+        order_key* keys = (order_key*)malloc((size_t)(nq > 0 ? nq : 1) * sizeof(order_key));
+        if (!keys) return -2;
+        int64_t maxU = 0;
+        for (int64_t i = 0; i < nq; ++i) {
+            int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];
+            int promoted = q_wait != NULL && q_wait[qlo + i] >= max_wait_ms;
+            keys[i].cls = promoted ? 0 : 1;
+            keys[i].val = promoted ? i : Ui;
+            keys[i].idx = i;
+            maxU = max64(maxU, Ui);
+        }
+        qsort(keys, (size_t)nq, sizeof(order_key), cmp_key);
+        for (int64_t i = 0; i < nq; ++i) order[qlo + i] = (int32_t)keys[i].idx;
+
+        int64_t lo = seg_off[d], hi = seg_off[d + 1];
+        int64_t T = max64(max_remaining(g, U, lo, hi), maxU);
+        int64_t* G = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        if (!G) return -2;
+        int rc = oracle_occupancy(p + lo, g + lo, U + lo, hi - lo, T, G);
+        if (rc) return rc;
+        int64_t peak = 0;
+        for (int64_t t = 0; t <= T; ++t) peak = max64(peak, G[t]);
+        int64_t k = 0;
+        if (peak <= capacity[d]) {
+            for (; k < nq; ++k) {
+                int64_t i = keys[k].idx;
+                int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];
+                for (int64_t t = 0; t <= Ui; ++t) {
+                    G[t] += (int64_t)q_p[qlo + i] + t;
+                    peak = max64(peak, G[t]);
+                }
+                if (peak > capacity[d]) break;
+            }
+        }
+        admitted[d] = (int32_t)k;
+        free(G); free(keys);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Brute force (tiny inputs only)                                            */
+/* ------------------------------------------------------------------------ */
+
+/* max over t of  sum_r [t <= R_r] (p_r + g_r + t)  +  sum_k [t <= V_k] (q_k + t),
+ * evaluated term by term at every step t up to the last one anything is held. */
+int64_t oracle_bruteforce_peak(int64_t n, const int32_t* p, const int32_t* g, const int32_t* U,
+                               int64_t m, const int32_t* q, const int32_t* V)
+{
+    int64_t T = 0;
+    for (int64_t r = 0; r < n; ++r) T = max64(T, remaining(U[r], g[r]));
+    for (int64_t k = 0; k < m; ++k) T = max64(T, V[k]);
+    int64_t best = 0;
+    for (int64_t t = 0; t <= T; ++t) {
+        int64_t occ = 0;
+        for (int64_t r = 0; r < n; ++r)
+            if (t <= remaining(U[r], g[r])) occ += (int64_t)p[r] + g[r] + t;
+        for (int64_t k = 0; k < m; ++k)
+            if (t <= V[k]) occ += (int64_t)q[k] + t;
+        best = max64(best, occ);
+    }
+    return best;
+}

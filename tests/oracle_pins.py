@@ -1,0 +1,411 @@
+"""Pins of the CPU oracle to facts fixed outside the oracle itself.
+
+Each ``pin_*`` function takes an :class:`oracle.Oracle` and raises
+AssertionError when the oracle disagrees with
+  * a worked example computed by hand from the paper's definitions
+    (``tests/golden/*.json``, each citing its passage),
+  * a closed form or a special case that reduces to a textbook rule
+    (Algorithm 1's static block test, order statistics),
+  * an invariant of the definitions (coverage, monotonicity, peak bounds),
+  * or a brute force written here in pure Python on tiny inputs.
+The same functions run against deliberately broken builds of the oracle in
+``test_oracle_mutants.py``, which shows each plausible mistake fails a pin.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import workload
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+Q_INF = np.iinfo(np.int32).max
+
+
+def golden(name: str) -> dict:
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------------------
+# pure-Python brute force (tiny inputs)
+# ---------------------------------------------------------------------------
+
+def py_remaining(U, g):
+    return max(int(U) - int(g), 0)
+
+
+def py_occupancy(p, g, U, t):
+    """Tokens held at step t by the residents (p+g+t while t <= R)."""
+    return sum(int(pi) + int(gi) + t for pi, gi, Ui in zip(p, g, U) if t <= py_remaining(Ui, gi))
+
+
+def py_peak(p, g, U, extra=()):
+    """max over steps of residents plus extra (q, V) requests holding q+t for t <= V."""
+    T = max([py_remaining(Ui, gi) for gi, Ui in zip(g, U)] + [V for _, V in extra] + [0])
+    best = 0
+    for t in range(T + 1):
+        occ = py_occupancy(p, g, U, t) + sum(q + t for q, V in extra if t <= V)
+        best = max(best, occ)
+    return best
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _tiny_decoders(rng, D, nmax, umax, pmax):
+    counts = rng.integers(0, nmax + 1, size=D)
+    seg = np.zeros(D + 1, np.int64)
+    seg[1:] = np.cumsum(counts)
+    n = int(seg[-1])
+    p = rng.integers(0, pmax + 1, size=n).astype(np.int32)
+    U = rng.integers(0, umax + 1, size=n).astype(np.int32)
+    g = rng.integers(0, umax + 3, size=n).astype(np.int32)     # g may exceed U
+    return seg, p, g, U
+
+
+# ---------------------------------------------------------------------------
+# calibration (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def pin_calibrate_golden(o):
+    gd = golden("calibrate_hand.json")
+    for case in gd["cases"]:
+        q, cnt = o.calibrate(gd["pred"], gd["truth"], gd["edges"], case["alpha_ppm"])
+        want = [Q_INF if v == "inf" else v for v in case["q"]]
+        assert q.tolist() == want, (case, q)
+        assert cnt.tolist() == case["count"], (case, cnt)
+        for n_b, k in zip(case["count"], case["k"]):
+            assert o.conformal_rank(n_b, case["alpha_ppm"]) == k
+    ap = gd["apply"]
+    q, _ = o.calibrate(gd["pred"], gd["truth"], gd["edges"], ap["alpha_ppm"])
+    U = o.apply_bounds(ap["pred"], gd["edges"], q, gd["u_max"])
+    assert U.tolist() == ap["U"], U
+    ai = gd["apply_inf"]
+    q, _ = o.calibrate(gd["pred"], gd["truth"], gd["edges"], ai["alpha_ppm"])
+    U = o.apply_bounds(ai["pred"], gd["edges"], q, gd["u_max"])
+    assert U.tolist() == ai["U"], U
+    rt = gd["rank_threshold"]
+    for n, k in zip(rt["n"], rt["k"]):
+        assert o.conformal_rank(n, rt["alpha_ppm"]) == k, (n, k)
+
+
+def pin_rank_is_ceiling(o):
+    """k is the least integer with k >= (1 - alpha)(n + 1) (exact rationals)."""
+    rng = _rng(11)
+    alphas = [1, 50000, 100000, 250000, 333333, 500000, 999999] + list(rng.integers(1, 10**6, 20))
+    ns = [0, 1, 2, 3, 8, 9, 10, 19, 99, 500, 3999999, 4000000] + list(rng.integers(0, 10**7, 20))
+    for a in alphas:
+        for n in ns:
+            k = o.conformal_rank(int(n), int(a))
+            x = (1 - Fraction(int(a), 10**6)) * (int(n) + 1)
+            assert k >= x and k - 1 < x, (a, n, k)
+
+
+def pin_quantile_order_statistic(o):
+    """q_b is the k-th smallest score: #{s <= q} >= k and #{s < q} < k."""
+    rng = _rng(12)
+    for trial in range(30):
+        n = int(rng.integers(0, 300))
+        pred = rng.integers(0, 60, size=n).astype(np.int32)
+        truth = rng.integers(0, 90, size=n).astype(np.int32)
+        nb = int(rng.integers(1, 6))
+        edges = np.sort(rng.integers(0, 60, size=nb - 1)).astype(np.int32)
+        alpha = int(rng.choice([50000, 100000, 200000, 500000]))
+        q, cnt = o.calibrate(pred, truth, edges, alpha)
+        b = np.array([int(np.sum(edges <= v)) for v in pred], dtype=np.int64)
+        s = np.maximum(0, truth.astype(np.int64) - pred.astype(np.int64))
+        for j in range(nb):
+            sj = s[b == j]
+            assert cnt[j] == sj.size
+            k = math.ceil((1 - Fraction(alpha, 10**6)) * (sj.size + 1))
+            if k > sj.size:
+                assert q[j] == Q_INF
+            else:
+                assert np.sum(sj <= q[j]) >= k and np.sum(sj < q[j]) < k, (trial, j)
+
+
+def pin_quantile_special_cases(o):
+    # every score zero: the quantile is 0 and the bound is the prediction itself
+    pred = np.arange(1, 21, dtype=np.int32) * 10
+    q, _ = o.calibrate(pred, pred - 5, [100], 100000)
+    assert q.tolist() == [0, 0]
+    U = o.apply_bounds(pred, [100], q, 10**6)
+    assert U.tolist() == pred.tolist()
+    # one bucket (no edges): the paper's single global quantile
+    truth = pred + np.arange(20, dtype=np.int32)
+    q, cnt = o.calibrate(pred, truth, [], 100000)
+    assert cnt.tolist() == [20] and q.tolist() == [18]      # k = ceil(0.9*21) = 19 -> 19th smallest of 0..19
+    # a duplicated edge leaves an empty bucket: infinite quantile, bound u_max
+    q, cnt = o.calibrate(pred, truth, [100, 100], 100000)
+    assert cnt[1] == 0 and q[1] == Q_INF
+    # bucket boundaries: an edge equal to the prediction sends it up
+    assert o.bucket(99, [100, 200]) == 0
+    assert o.bucket(100, [100, 200]) == 1
+    assert o.bucket(10**6, [100, 200]) == 2
+
+
+def pin_quantile_monotone_in_alpha(o):
+    b = workload.make("small")
+    q05, _ = o.calibrate(b.cal_pred, b.cal_truth, b.edges, 50000)
+    q10, _ = o.calibrate(b.cal_pred, b.cal_truth, b.edges, 100000)
+    assert np.all(q05.astype(np.int64) >= q10.astype(np.int64))
+    assert np.any(q05 != q10)
+    pred = b.apply_pred()
+    U05 = o.apply_bounds(pred, b.edges, q05, b.u_max)
+    U10 = o.apply_bounds(pred, b.edges, q10, b.u_max)
+    assert np.all(U05 >= U10)
+
+
+def pin_coverage(o):
+    """Eq. (5): held-out coverage P(L <= U) >= 1 - alpha within sampling error,
+    and calibration-set coverage of every finite bucket quantile >= 1 - alpha."""
+    for name, alpha in (("small", 50000), ("small", 100000), ("medium", 100000)):
+        b = workload.make(name)
+        q, cnt = o.calibrate(b.cal_pred, b.cal_truth, b.edges, alpha)
+        pred, truth = workload.heldout(name, 200000, seed=5)
+        U = o.apply_bounds(pred, b.edges, q, b.u_max)
+        a = alpha / 1e6
+        cov = float(np.mean(truth <= U))
+        assert cov >= 1 - a - 3 * math.sqrt(a * (1 - a) / truth.size), (name, alpha, cov)
+        assert cov <= 1 - a + 0.03, (name, alpha, cov)       # calibrated, not vacuous
+        s = np.maximum(0, b.cal_truth.astype(np.int64) - b.cal_pred)
+        bk = np.searchsorted(b.edges, b.cal_pred, side="right")
+        for j in range(b.edges.size + 1):
+            if q[j] != Q_INF:
+                assert np.mean(s[bk == j] <= q[j]) >= 1 - a
+
+
+# ---------------------------------------------------------------------------
+# occupancy and placement (Sec. 3.3, App. A, Algorithm 1)
+# ---------------------------------------------------------------------------
+
+def pin_place_golden(o):
+    gd = golden("place_hand.json")
+    seg = np.array(gd["seg_off"], np.int64)
+    p, g, U = gd["prompt"], gd["generated"], gd["upper"]
+    for d in range(seg.size - 1):
+        lo, hi = seg[d], seg[d + 1]
+        occ = o.occupancy(p[lo:hi], g[lo:hi], U[lo:hi], len(gd["occupancy"][d]) - 1)
+        assert occ.tolist() == gd["occupancy"][d], (d, occ)
+    assert o.project(seg, p, g, U).tolist() == gd["base_peak"]
+    for policy, key in ((0, "mq"), (1, "mc")):
+        r = o.place(seg, p, g, U, gd["capacity"], gd["queue_len"], gd["a_prompt"], gd["a_upper"],
+                    policy=policy, rr_offset=gd["rr_offset"])
+        assert r.pair_peak.tolist() == gd["pair_peak"], r.pair_peak
+        assert r.base_peak.tolist() == gd["base_peak"]
+        for f in ("choice", "chosen_peak", "chosen_overflow", "flags"):
+            assert getattr(r, f).tolist() == gd[key][f], (key, f, getattr(r, f))
+
+
+def pin_occupancy_bruteforce(o):
+    rng = _rng(21)
+    for trial in range(40):
+        seg, p, g, U = _tiny_decoders(rng, 1, 9, 15, 30)
+        T = max([py_remaining(u, gg) for u, gg in zip(U, g)] + [0]) + 3
+        occ = o.occupancy(p, g, U, T)
+        want = [py_occupancy(p, g, U, t) for t in range(T + 1)]
+        assert occ.tolist() == want, trial
+        assert occ[-1] == 0 and occ[0] == int(np.sum(p.astype(np.int64) + g))
+
+
+def pin_place_bruteforce(o):
+    """Every pair peak equals the step-by-step maximum (Python), every choice
+    the rule of Algorithm 1 applied to those peaks."""
+    rng = _rng(22)
+    for trial in range(25):
+        D = int(rng.integers(1, 5))
+        seg, p, g, U = _tiny_decoders(rng, D, 6, 12, 20)
+        A = int(rng.integers(1, 12))
+        ap = rng.integers(0, 20, size=A).astype(np.int32)
+        aU = rng.integers(-1, 15, size=A).astype(np.int32)
+        cap = rng.integers(0, 150, size=D).astype(np.int32)
+        Q = rng.integers(0, 3, size=D).astype(np.int32)
+        rr = int(rng.integers(0, 7))
+        for policy in (0, 1):
+            r = o.place(seg, p, g, U, cap, Q, ap, aU, policy=policy, rr_offset=rr)
+            for d in range(D):
+                lo, hi = seg[d], seg[d + 1]
+                assert r.base_peak[d] == py_peak(p[lo:hi], g[lo:hi], U[lo:hi])
+            for a in range(A):
+                if aU[a] < 0:
+                    assert all(r.pair_peak[d, a] == -1 for d in range(D))
+                    assert r.choice[a] == (rr + a) % D and r.flags[a] == 2
+                    assert r.chosen_peak[a] == -1 and r.chosen_overflow[a] == 0
+                    continue
+                peaks = []
+                for d in range(D):
+                    lo, hi = seg[d], seg[d + 1]
+                    pk = py_peak(p[lo:hi], g[lo:hi], U[lo:hi], [(int(ap[a]), int(aU[a]))])
+                    assert r.pair_peak[d, a] == pk, (trial, d, a)
+                    peaks.append(pk)
+                slack = [int(cap[d]) - peaks[d] for d in range(D)]
+                feas = [d for d in range(D) if slack[d] >= 0]
+                if policy == 0 and feas:
+                    want = min(feas, key=lambda d: (int(Q[d]), d))
+                else:
+                    want = max(range(D), key=lambda d: (slack[d], -d))
+                assert r.choice[a] == want, (trial, policy, a)
+                assert r.chosen_peak[a] == peaks[want]
+                assert r.chosen_overflow[a] == max(0, -slack[want])
+                assert r.flags[a] == (1 if slack[want] >= 0 else 0)
+
+
+def pin_place_closed_forms(o):
+    # empty decoder: peak = p_a + U_a
+    seg = np.array([0, 0], np.int64)
+    z = np.zeros(0, np.int32)
+    ap = np.array([0, 5, 7, 100], np.int32)
+    aU = np.array([0, 3, 0, 250], np.int32)
+    r = o.place(seg, z, z, z, [10**6], [0], ap, aU)
+    assert r.pair_peak[0].tolist() == (ap + aU).tolist()
+    # one resident (P = p+g, R): U_a >= R -> max(P+R + p_a+R, p_a+U_a); else max(P+R, P+U_a + p_a+U_a)
+    rng = _rng(23)
+    for _ in range(200):
+        pr, gr, Ur = (int(x) for x in rng.integers(0, 50, size=3))
+        pa, Ua = (int(x) for x in rng.integers(0, 60, size=2))
+        P, R = pr + gr, max(Ur - gr, 0)
+        want = max(P + R + pa + R, pa + Ua) if Ua >= R else max(P + R, P + Ua + pa + Ua)
+        r = o.place(np.array([0, 1], np.int64), [pr], [gr], [Ur], [10**6], [0], [pa], [Ua])
+        assert r.pair_peak[0, 0] == want, (pr, gr, Ur, pa, Ua)
+
+
+def pin_place_invariants(o):
+    b = workload.make("tiny")
+    rng = _rng(24)
+    seg = b.seg_off
+    p, g = b.res_prompt, b.res_gen
+    U = np.minimum(b.res_pred + rng.integers(0, 200, size=b.res_pred.size), b.u_max).astype(np.int32)
+    ap = b.arr_prompt
+    aU = np.minimum(b.arr_pred + 50, b.u_max).astype(np.int32)
+    r = o.place(seg, p, g, U, b.capacity, b.queue_len, ap, aU)
+    base = r.base_peak[:, None]
+    pp = r.pair_peak
+    assert np.all(pp >= base)                                # the arrival never lowers the peak
+    assert np.all(pp >= (ap + aU)[None, :])                  # the arrival's own footprint
+    assert np.all(pp <= base + (ap + aU)[None, :])
+    static = np.array([np.sum(p[seg[d]:seg[d + 1]].astype(np.int64) + g[seg[d]:seg[d + 1]]
+                              + np.maximum(U[seg[d]:seg[d + 1]].astype(np.int64) - g[seg[d]:seg[d + 1]], 0))
+                       for d in range(seg.size - 1)])
+    assert np.all(pp <= static[:, None] + (ap + aU)[None, :])   # static reservation bound
+    r1 = o.place(seg, p, g, U, b.capacity, b.queue_len, ap + 1, aU)
+    r2 = o.place(seg, p, g, U, b.capacity, b.queue_len, ap, aU + 1)
+    assert np.all(r1.pair_peak >= pp) and np.all(r2.pair_peak >= pp)
+    for d in range(seg.size - 1):
+        lo, hi = seg[d], seg[d + 1]
+        T = int(np.max(np.maximum(U[lo:hi].astype(np.int64) - g[lo:hi], 0)))
+        occ = o.occupancy(p[lo:hi], g[lo:hi], U[lo:hi], T + 5)
+        assert np.all(occ[T + 1:] == 0) and occ[T] > 0         # empty once every bound has run out
+        assert r.base_peak[d] == occ.max()
+
+
+def pin_place_reduces_to_algorithm1(o):
+    """When every resident and the arrival have the same remaining length, the
+    projected test is Algorithm 1's block test at S = 1: B_need = p_a + U_a,
+    B_eff = C - sum(p_r + U_r); MQ among feasible, else argmax B_eff."""
+    rng = _rng(25)
+    for trial in range(40):
+        D = int(rng.integers(1, 6))
+        T = int(rng.integers(0, 30))
+        counts = rng.integers(0, 5, size=D)
+        seg = np.zeros(D + 1, np.int64)
+        seg[1:] = np.cumsum(counts)
+        n = int(seg[-1])
+        p = rng.integers(0, 40, size=n).astype(np.int32)
+        g = rng.integers(0, 20, size=n).astype(np.int32)
+        U = (g + T).astype(np.int32)                          # R = T for everyone
+        A = int(rng.integers(1, 8))
+        ap = rng.integers(0, 40, size=A).astype(np.int32)
+        aU = np.full(A, T, np.int32)
+        cap = rng.integers(0, 400, size=D).astype(np.int32)
+        Q = rng.integers(0, 4, size=D).astype(np.int32)
+        r = o.place(seg, p, g, U, cap, Q, ap, aU)
+        B_res = np.array([int(np.sum(p[seg[d]:seg[d + 1]].astype(np.int64) + U[seg[d]:seg[d + 1]]))
+                          for d in range(D)])
+        B_eff = cap.astype(np.int64) - B_res
+        for a in range(A):
+            need = int(ap[a]) + int(aU[a])                    # ceil((L_prom + L_up) / S), S = 1
+            feas = [d for d in range(D) if need <= B_eff[d]]
+            if feas:
+                want = min(feas, key=lambda d: (int(Q[d]), d))
+            else:
+                want = max(range(D), key=lambda d: (int(B_eff[d]), -d))
+            assert r.choice[a] == want, (trial, a)
+            assert r.chosen_peak[a] == B_res[want] + need
+
+
+def pin_round_robin_and_ties(o):
+    seg = np.array([0, 1, 2, 3, 4], np.int64)
+    one = np.array([5, 5, 5, 5], np.int32)
+    r = o.place(seg, one, np.zeros(4, np.int32), one, [100] * 4, [2, 2, 2, 2],
+                [1] * 6, [-1, 3, -5, 3, -1, -1], rr_offset=6)
+    assert r.choice.tolist() == [(6 + 0) % 4, 0, (6 + 2) % 4, 0, (6 + 4) % 4, (6 + 5) % 4]
+    r = o.place(seg, one, np.zeros(4, np.int32), one, [0] * 4, [2, 1, 1, 2], [1], [3], policy=0)
+    assert r.choice.tolist() == [0] and r.flags.tolist() == [0]          # all infeasible, equal slack
+    r = o.place(seg, one, np.zeros(4, np.int32), one, [100] * 4, [2, 1, 1, 2], [1], [3], policy=0)
+    assert r.choice.tolist() == [1] and r.flags.tolist() == [1]          # min queue, lowest index
+    r = o.place(seg, one, np.zeros(4, np.int32), one, [100, 101, 101, 100], [0] * 4, [1], [3], policy=1)
+    assert r.choice.tolist() == [1]                                      # max slack, lowest index
+    # every pair peak is 12 (5+t resident and 1+t arrival up to t=3); a peak equal to the
+    # capacity is feasible (B_need <= B_eff in Algorithm 1, K+M <= C in Eq. (10))
+    r = o.place(seg, one, np.zeros(4, np.int32), one, [11, 12, 13, 13], [0, 1, 5, 5], [1], [3], policy=0)
+    assert r.pair_peak[:, 0].tolist() == [12] * 4
+    assert r.choice.tolist() == [1] and r.flags.tolist() == [1] and r.chosen_overflow.tolist() == [0]
+
+
+# ---------------------------------------------------------------------------
+# local order and admission (Sec. 3.3 Eq. (7), App. A Eq. (10))
+# ---------------------------------------------------------------------------
+
+def pin_local_order_golden(o):
+    gd = golden("local_order_hand.json")
+    for key, wait in (("with_wait", gd["q_wait_ms"]), ("without_wait", None)):
+        order, adm = o.local_order(gd["seg_off"], gd["prompt"], gd["generated"], gd["upper"],
+                                   gd["capacity"], gd["q_off"], gd["q_prompt"], gd["q_upper"],
+                                   wait, gd["max_wait_ms"], gd["u_max"])
+        assert order.tolist() == gd[key]["order"], (key, order)
+        assert adm.tolist() == gd[key]["admitted"], (key, adm)
+
+
+def pin_local_order_bruteforce(o):
+    rng = _rng(31)
+    for trial in range(25):
+        D = int(rng.integers(1, 4))
+        seg, p, g, U = _tiny_decoders(rng, D, 4, 10, 15)
+        qc = rng.integers(0, 7, size=D)
+        qoff = np.zeros(D + 1, np.int64)
+        qoff[1:] = np.cumsum(qc)
+        nq = int(qoff[-1])
+        qp = rng.integers(0, 12, size=nq).astype(np.int32)
+        qU = rng.integers(-1, 9, size=nq).astype(np.int32)
+        qw = rng.integers(0, 2000, size=nq).astype(np.int32)
+        u_max, max_wait = 9, 1000
+        cap = rng.integers(0, 160, size=D).astype(np.int32)
+        for wait in (qw, None):
+            order, adm = o.local_order(seg, p, g, U, cap, qoff, qp, qU, wait, max_wait, u_max)
+            for d in range(D):
+                lo, hi = int(qoff[d]), int(qoff[d + 1])
+                Ue = [u_max if int(x) < 0 else int(x) for x in qU[lo:hi]]
+                prom = [wait is not None and int(wait[lo + i]) >= max_wait for i in range(hi - lo)]
+                want = sorted(range(hi - lo), key=lambda i: (0, i) if prom[i] else (1, Ue[i]))
+                assert order[lo:hi].tolist() == want, (trial, d)
+                rp, rg, rU = p[seg[d]:seg[d + 1]], g[seg[d]:seg[d + 1]], U[seg[d]:seg[d + 1]]
+                peaks = [py_peak(rp, rg, rU, [(int(qp[lo + i]), Ue[i]) for i in want[:k]])
+                         for k in range(hi - lo + 1)]
+                assert all(x <= y for x, y in zip(peaks, peaks[1:]))   # adding never lowers the peak
+                k_ok = [k for k in range(hi - lo + 1) if peaks[k] <= cap[d]]
+                assert adm[d] == (max(k_ok) if k_ok else 0), (trial, d, peaks, cap[d])
+
+
+ALL_PINS = [
+    pin_calibrate_golden, pin_rank_is_ceiling, pin_quantile_order_statistic,
+    pin_quantile_special_cases, pin_quantile_monotone_in_alpha, pin_coverage,
+    pin_place_golden, pin_occupancy_bruteforce, pin_place_bruteforce, pin_place_closed_forms,
+    pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
+    pin_local_order_golden, pin_local_order_bruteforce,
+]

@@ -1,0 +1,94 @@
+"""Each plausible mistake planted in the oracle (on the CPU, in a throw-away
+copy of its source) must fail at least one pin: the pins are strong enough to
+catch a dropped term, a wrong sign, an off-by-one or a wrong tie-break."""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+import oracle
+from tests import oracle_pins as pins
+
+# (name, text in maps_oracle.c, replacement)
+MUTANTS = [
+    ("score_sign", "(int64_t)truth[i] - (int64_t)pred[i]", "(int64_t)pred[i] - (int64_t)truth[i]"),
+    ("score_not_one_sided", "max64(0, (int64_t)truth[i] - (int64_t)pred[i])",
+     "((int64_t)truth[i] - (int64_t)pred[i])"),
+    ("rank_n_not_n_plus_1", "* (n + 1);", "* (n);"),
+    ("rank_floor_not_ceil", "(num + 999999) / 1000000", "num / 1000000"),
+    ("bucket_strict_edge", "if (edges[j] <= pred) b += 1;", "if (edges[j] < pred) b += 1;"),
+    ("bound_minus_q", "(int64_t)pred[i] + qb", "(int64_t)pred[i] - qb"),
+    ("bound_not_capped", "U_out[i] = (int32_t)min64((int64_t)pred[i] + qb, u_max);",
+     "U_out[i] = (int32_t)((int64_t)pred[i] + qb);"),
+    ("inf_quantile_gives_pred", "if (qb == ORACLE_Q_INF) U_out[i] = u_max;",
+     "if (qb == ORACLE_Q_INF) U_out[i] = pred[i];"),
+    ("missing_pred_gets_umax", "if (pred[i] < 0) { U_out[i] = -1; continue; }",
+     "if (pred[i] < 0) { U_out[i] = u_max; continue; }"),
+    ("occupancy_no_growth", "O[t] = held + t * active;", "O[t] = held;"),
+    ("occupancy_leaves_early", "        O[t] = held + t * active;      /* every active request holds p+g+t */\n"
+     "        active -= leave_cnt[t];        /* those whose last step is t leave */\n"
+     "        held -= leave_tok[t];",
+     "        active -= leave_cnt[t];\n        held -= leave_tok[t];\n        O[t] = held + t * active;"),
+    ("remaining_plus_g", "return max64((int64_t)U - g, 0);", "return max64((int64_t)U - g + 1, 0);"),
+    ("present_without_t", "max64(present[t - 1], O[t] + t)", "max64(present[t - 1], O[t])"),
+    ("after_includes_u", "after[t] = max64(after[t + 1], O[t + 1]);", "after[t] = max64(after[t + 1], O[t]);"),
+    ("peak_without_prompt", "max64((int64_t)a_p[a] + present[a_U[a]], after[a_U[a]])",
+     "max64(present[a_U[a]], after[a_U[a]])"),
+    ("feasible_strict", "if (policy == ORACLE_POLICY_MQ && slack >= 0) {",
+     "if (policy == ORACLE_POLICY_MQ && slack > 0) {"),
+    ("mq_ties_highest", "queue_len[d] < queue_len[feas_d[a]]", "queue_len[d] <= queue_len[feas_d[a]]"),
+    ("fallback_ties_highest", "if (fb_d[a] < 0 || slack > fb_slack[a]) {",
+     "if (fb_d[a] < 0 || slack >= fb_slack[a]) {"),
+    ("fallback_min_slack", "if (fb_d[a] < 0 || slack > fb_slack[a]) {",
+     "if (fb_d[a] < 0 || slack < fb_slack[a]) {"),
+    ("rr_shifted", "choice[a] = (int32_t)((rr_offset + i) % D);", "choice[a] = (int32_t)((rr_offset + i + 1) % D);"),
+    ("promotion_last", "keys[i].cls = promoted ? 0 : 1;", "keys[i].cls = promoted ? 1 : 0;"),
+    ("promoted_by_bound", "keys[i].val = promoted ? i : Ui;", "keys[i].val = Ui;"),
+    ("sjf_descending", "if (x->val != y->val) return x->val < y->val ? -1 : 1;",
+     "if (x->val != y->val) return x->val > y->val ? -1 : 1;"),
+    ("admission_no_growth", "G[t] += (int64_t)q_p[qlo + i] + t;", "G[t] += (int64_t)q_p[qlo + i];"),
+    ("admission_strict", "if (peak > capacity[d]) break;", "if (peak >= capacity[d]) break;"),
+    ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
+     "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
+]
+
+
+def _build_mutant(tmp, name, old, new):
+    with open(oracle.SOURCE) as f:
+        src = f.read()
+    assert old in src, f"mutation {name} does not apply"
+    src = src.replace(old, new)
+    path = os.path.join(tmp, f"{name}.c")
+    with open(path, "w") as f:
+        f.write(src)
+    return oracle.build(path, os.path.join(tmp, f"lib{name}.so"), strict=False)
+
+
+@pytest.fixture(scope="module")
+def tmpdir_mutants():
+    d = tempfile.mkdtemp(prefix="oracle_mutants_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_fails_a_pin(tmpdir_mutants, name, old, new):
+    lib = oracle.load(_build_mutant(tmpdir_mutants, name, old, new))
+    o = oracle.Oracle(lib)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(o)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"planted mistake {name} passed every pin"
+
+
+def test_unmutated_copy_passes(tmpdir_mutants):
+    path = os.path.join(tmpdir_mutants, "liboriginal.so")
+    o = oracle.Oracle(oracle.load(oracle.build(oracle.SOURCE, path)))
+    for pin in pins.ALL_PINS:
+        pin(o)
