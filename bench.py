@@ -1,0 +1,182 @@
+"""Benchmark of the MAPS scheduler core on one MI355X.
+
+One step = the whole hot path over one batch already resident in HBM:
+calibrate (per-bucket conformal quantiles and the bound of every resident,
+arrival and queued request) -> project (occupancy snapshot of every decoder)
+-> place (every arrival x decoder peak, with the per-pair peak matrix written,
+and the choice per arrival) -> local order (queue order and admitted prefix).
+
+Prints one JSON line: arrival x decoder placement evaluations per second over
+the whole step, the placement pass against the HBM roofline (algorithmic
+bytes / its HIP-event time), and the CPU oracle timed on the host as a
+baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+DEFAULT_WORKLOAD = "large"     # 256 decoders x 4096 residents, 262,144 arrivals
+
+
+def placement_bytes(D: int, A: int, W: int, events) -> int:
+    """Algorithmic bytes of one placement pass: every input read once and
+    every output written once.  Pair matrix 4 B/pair; arrivals 8 B in and
+    13 B out (choice, peak, overflow, flags); per decoder its rank words
+    (8 B each), its E+1 records (16 B each), header, capacity and queue length."""
+    snap = sum(8 * W + 16 * (int(e) + 1) + 32 + 8 for e in events)
+    return 4 * D * A + (8 + 13) * A + snap
+
+
+def cpu_baseline(batch, budget_s: float = 20.0):
+    import oracle
+    o = oracle.Oracle()
+    t0 = time.perf_counter()
+    runs = 0
+    while True:
+        oracle.step(batch, o, want_pairs=True)
+        runs += 1
+        if time.perf_counter() - t0 > budget_s / 2 or runs >= 5:
+            break
+    dt = (time.perf_counter() - t0) / runs
+    pairs = batch.decoders * batch.arrivals
+    return {"value": pairs / dt, "unit": "pair-evaluations/s", "cores": 1, "kind": "oracle",
+            "sample": f"the full workload, {runs} step(s) of the single-threaded C oracle "
+                      f"(calibrate, bound, project, place with pair matrix, local order), "
+                      f"{dt * 1e3:.1f} ms per step"}
+
+
+def copy_probe(nbytes: int):
+    """A plain device copy of known size (for scaling HBM byte counters)."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, help="run only a plain copy of this many bytes")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (--gpus {args.gpus} requested); "
+              "the multi-GPU split is described in DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    import numpy as np
+    import torch
+
+    import workload
+    import paper_2609_15359_amd as maps
+    from paper_2609_15359_amd import pipeline
+
+    b = workload.make(args.workload)
+    D, A = b.decoders, b.arrivals
+    db = pipeline.to_device(b)
+    ws = pipeline.Workspaces(db, want_pairs=True)
+    stream = torch.cuda.current_stream()
+
+    def one_step(ev=None):
+        err = ws.dev_err
+        if ev:
+            ev[0].record(stream)
+        q, cnt, U, _ = maps.calibrate(db.cal_pred, db.cal_truth, db.edges, db.alpha_ppm, db.apply_pred,
+                                      db.u_max, dev_err=err, workspace=ws.cal, out=ws.out)
+        if ev:
+            ev[1].record(stream)
+        nr, na = db.n_res, db.n_arr
+        snap, base, _ = maps.project(db.seg_off, db.res_prompt, db.res_gen, U[:nr], db.u_max,
+                                     snapshot=ws.snapshot, dev_err=err, base_peak=ws.base_peak)
+        if ev:
+            ev[2].record(stream)
+        maps.place(snap, db.capacity, db.queue_len, db.arr_prompt, U[nr:nr + na],
+                   workspace=ws.place, out=ws.placement)
+        if ev:
+            ev[3].record(stream)
+        maps.local_order(snap, db.capacity, db.q_off, db.q_prompt, U[nr + na:], db.q_wait_ms,
+                         db.max_wait_ms, dev_err=err, order=ws.order, admitted=ws.admitted)
+        if ev:
+            ev[4].record(stream)
+        return snap
+
+    ws.dev_err.zero_()
+    for _ in range(args.warmup):
+        snap = one_step()
+    torch.cuda.synchronize()
+    bits = int(ws.dev_err.item()) & 0xFFFFFFFF
+    if bits:
+        raise SystemExit(f"device value errors: {maps.error_names(bits)}")
+
+    # timed region: exactly K steps, bracketed by synchronization
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    parts = {name: statistics.median(ev[i].elapsed_time(ev[i + 1]) for ev in events)
+             for i, name in enumerate(("calibrate", "project", "place", "local_order"))}
+    place_ms = statistics.mean(ev[2].elapsed_time(ev[3]) for ev in events)
+
+    # algorithmic bytes of the placement pass, from the snapshot's own event counts
+    hdr = ws.snapshot[256:256 + 32 * D].view(torch.int32).view(D, 8).cpu().numpy()
+    events_per_decoder = hdr[:, 4]
+    W = (((db.u_max + 1) // 32 + 1) + 1) & ~1
+    nbytes = placement_bytes(D, A, W, events_per_decoder)
+    achieved = nbytes / (place_ms * 1e-3) / 1e9
+    feasible = float(np.mean(ws.placement.flags.cpu().numpy() & 1))
+
+    result = {
+        "metric": "arrival x decoder peak-KV placement evals/sec",
+        "value": D * A / (ms_per_step * 1e-3),
+        "unit": "pair-evaluations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": f"{b.workload.name}: {workload.describe(b.workload)}; "
+                               f"capacities {list(b.workload.capacities)} tokens, alpha_ppm {b.alpha_ppm}, "
+                               f"u_max {b.u_max}; per-pair peak matrix written",
+                   "decoders": D, "arrivals": A, "pairs": D * A},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "maps_place (place_pairs + place_reduce)",
+                     "algorithmic_bytes": nbytes, "place_ms": place_ms},
+        "breakdown_ms": parts,
+        "mean_events_per_decoder": float(np.mean(events_per_decoder)),
+        "feasible_fraction": feasible,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(b)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,203 @@
+/*
+ * maps.h -- C ABI of the MAPS scheduler core for AMD Instinct MI355X (gfx950).
+ *
+ * MAPS (Memory-Aware Predictive Scheduling) turns speculative output-length
+ * predictions into calibrated upper bounds, projects each decoder's future
+ * KV-cache occupancy from its resident requests, places arriving requests on
+ * decoders, and orders each decoder's local queue.  This library computes
+ * those four steps for whole batches on one GPU.
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers unless the comment says otherwise.
+ *     All arrays are dense, C-contiguous and owned by the caller; the library
+ *     keeps no pointer after a call returns.
+ *   - Lengths are int32 token counts (one KV-cache block per token: block
+ *     size S = 1).  Offsets of decoder-major segments are int64.
+ *   - Work is enqueued on `stream` (NULL = the null stream) and completes
+ *     asynchronously; outputs are valid once the stream is synchronized.
+ *   - The library never allocates or frees device memory.  Scratch memory is
+ *     the caller's `workspace` of at least the matching *_workspace_size()
+ *     bytes (any alignment of 256 bytes or more; NULL is allowed when the size
+ *     is 0).  A workspace may be reused once the call that used it finished.
+ *   - Argument errors detectable on the host are returned synchronously as a
+ *     negative maps_status and nothing is enqueued.  Errors in the VALUES of
+ *     device arrays are reported by OR-ing MAPS_ERR_* bits into the device
+ *     word *dev_err (never cleared by the library; the caller zeroes it).  When
+ *     a bit is set the outputs of that call are unspecified, but every kernel
+ *     still stays within the bounds of the buffers it was given.
+ *   - Results are deterministic: the same inputs give bit-identical outputs.
+ *   - Calls on different streams may run concurrently if they share no
+ *     output, snapshot or workspace buffer.
+ */
+#ifndef MAPS_H
+#define MAPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t maps_status;
+
+enum {
+    MAPS_OK = 0,
+    MAPS_E_NULL = -1,        /* a required pointer is NULL */
+    MAPS_E_SIZE = -2,        /* a count or size is out of range */
+    MAPS_E_ALPHA = -3,       /* alpha_ppm is not in (0, 1000000) */
+    MAPS_E_WORKSPACE = -4,   /* workspace smaller than the size query */
+    MAPS_E_HIP = -5,         /* a HIP runtime call or kernel launch failed */
+    MAPS_E_POLICY = -6,      /* unknown placement policy */
+    MAPS_E_BUFFER = -7       /* snapshot buffer smaller than maps_snapshot_bytes() */
+};
+
+/* Quantile of a bucket whose conformal rank exceeds its size (infinite). */
+#define MAPS_Q_INF INT32_MAX
+
+/* Bits OR-ed into *dev_err. */
+enum {
+    MAPS_ERR_NEG_LEN = 1u,          /* a length, capacity or queue length < 0 where
+                                       one is required */
+    MAPS_ERR_EDGES_UNSORTED = 2u,   /* bucket edges not non-decreasing */
+    MAPS_ERR_INT32_RANGE = 4u,      /* a projected occupancy could exceed INT32_MAX */
+    MAPS_ERR_SEG_OFFSETS = 8u,      /* segment offsets not non-decreasing in [0, total] */
+    MAPS_ERR_BOUND_RANGE = 16u,     /* a remaining length max(U-g,0) exceeds u_max */
+    MAPS_ERR_SNAPSHOT = 32u,        /* snapshot was not built for this (D, u_max) */
+    MAPS_ERR_QUEUE_TOO_LONG = 64u   /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
+};
+
+/* Longest pending queue of one decoder that maps_local_order accepts. */
+#define MAPS_MAX_LOCAL_QUEUE 2048
+
+/* Placement policies: minimum queue among feasible decoders with the largest
+ * slack as fallback (Sec. 3.3 and Algorithm 1), or largest slack alone (the
+ * maximum-capacity ablation of Sec. 4). */
+enum { MAPS_POLICY_MQ = 0, MAPS_POLICY_MC = 1 };
+
+/* ------------------------------------------------------------------------ */
+/* 1. Uncertainty-aware calibration (Sec. 3.2, Eqs. (2)-(4))                */
+/* ------------------------------------------------------------------------ */
+/*
+ * Calibration set of n completed requests: pred[i] (prediction L_hat) and
+ * truth[i] (observed output length L), both >= 0.  Request i belongs to length
+ * bucket b(i) = #{j : edges[j] <= pred[i]}, edges[0..nb-2] non-decreasing.
+ * Per bucket b with n_b members, scores s_i = max(0, truth - pred) (Eq. (2)):
+ *   k_b = ceil((1 - alpha)(n_b + 1)),  alpha = alpha_ppm / 10^6  (exact integer)
+ *   q_out[b] = the k_b-th smallest score of the bucket (1-indexed; Eq. (3)),
+ *              or MAPS_Q_INF when k_b > n_b;  count_out[b] = n_b.
+ * Then, for m predictions apply_pred[0..m-1] (m may be 0; apply_pred and
+ * U_out may then be NULL), the bound of Eq. (4) in the prediction's bucket:
+ *   U_out[i] = -1                          if apply_pred[i] < 0 (no prediction)
+ *            = u_max                       if q of its bucket is MAPS_Q_INF
+ *            = min(apply_pred[i] + q, u_max) otherwise.
+ * dev_err bits: NEG_LEN (pred or truth < 0), EDGES_UNSORTED.
+ * Host errors: NULL, SIZE (n < 0, m < 0, nb < 1 or nb > 65536, u_max < 0),
+ * ALPHA, WORKSPACE, HIP.
+ */
+size_t maps_calibrate_workspace_size(int64_t n, int32_t nb);
+maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
+                           const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                           int32_t* q_out, int32_t* count_out,
+                           const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
+                           uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 2. Projection of KV occupancy per decoder (Sec. 3.3; App. A, Eq. (8))    */
+/* ------------------------------------------------------------------------ */
+/*
+ * D decoders; the residents of decoder d are indices [seg_off[d], seg_off[d+1])
+ * of prompt/generated/upper (n_total = seg_off[D] entries, all >= 0).  A
+ * resident with prompt p, g generated tokens and bound U holds p+g+t KV tokens
+ * at future decoding step t while t <= R = max(U-g, 0), then frees them.
+ * The occupancy O_d(t) is the sum over residents.  The call writes
+ *   base_peak[d] = max_t O_d(t)   (0 for a decoder without residents)
+ * and an opaque snapshot (caller-allocated, maps_snapshot_bytes(D, n_total,
+ * u_max) bytes) that maps_place and maps_local_order read; it stays valid
+ * until the caller overwrites it and describes the residents at call time.
+ * Requires every R <= u_max.
+ * dev_err bits: NEG_LEN, SEG_OFFSETS, BOUND_RANGE, INT32_RANGE (when
+ * sum_r (p+g+R) + u_max > INT32_MAX for a decoder).
+ * Host errors: NULL, SIZE (D < 1, n_total < 0, u_max < 0 or u_max >= 2^24),
+ * BUFFER, WORKSPACE, HIP.
+ */
+size_t maps_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max);
+size_t maps_project_workspace_size(int32_t D, int64_t n_total, int32_t u_max);
+maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n_total,
+                         const int32_t* prompt, const int32_t* generated, const int32_t* upper,
+                         int32_t u_max, void* snapshot, size_t snapshot_bytes, int32_t* base_peak,
+                         uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 3. Global placement (Sec. 3.3 and Algorithm 1, App. C)                   */
+/* ------------------------------------------------------------------------ */
+/*
+ * A arriving requests a = (a_prompt[a], a_upper[a]); an arrival holds p+t KV
+ * tokens at step t while t <= U.  For every decoder d (snapshot of
+ * maps_project with the same D and u_max):
+ *   peak(a,d) = max_t [ O_d(t) + (t <= U ? p + t : 0) ],   slack = capacity[d] - peak.
+ * Decoder d is feasible for a when slack >= 0.  Choice:
+ *   MAPS_POLICY_MQ: the feasible decoder with the smallest queue_len[d] (Q_k);
+ *                   if none is feasible, the largest slack;
+ *   MAPS_POLICY_MC: the largest slack;
+ *   ties go to the lowest decoder index.  An arrival with a_upper < 0 has no
+ *   bound and is routed round-robin (App. A, Eq. (9)):
+ *   choice = (rr_offset + a) mod D.
+ * Outputs per arrival: choice[a]; chosen_peak[a] = peak(a, choice) (-1 for
+ * round-robin); chosen_overflow[a] = max(0, -slack) (0 for round-robin);
+ * flags[a] bit0 = chosen decoder feasible, bit1 = routed round-robin.
+ * pair_peak (optional, NULL to skip): decoder-major [D][A] int32 peak(a,d),
+ * -1 for round-robin arrivals.  Arrivals are evaluated independently against
+ * the same snapshot (no reservation between them).
+ * dev_err bits: NEG_LEN (a_prompt, capacity or queue_len < 0), INT32_RANGE
+ * (an arrival whose p + U could overflow a peak), SNAPSHOT.
+ * Host errors: NULL, SIZE (D < 1, A < 0, rr_offset < 0), POLICY, WORKSPACE, HIP.
+ */
+size_t maps_place_workspace_size(int32_t D, int64_t A, int32_t u_max);
+maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,
+                       const int32_t* capacity, const int32_t* queue_len,
+                       const int32_t* a_prompt, const int32_t* a_upper, int64_t A,
+                       int32_t policy, int64_t rr_offset,
+                       int32_t* choice, int32_t* chosen_peak, int32_t* chosen_overflow,
+                       uint8_t* flags, int32_t* pair_peak,
+                       uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 4. Local order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10))       */
+/* ------------------------------------------------------------------------ */
+/*
+ * Pending queue of decoder d: indices [q_off[d], q_off[d+1]) of q_prompt,
+ * q_upper and q_wait_ms (total = q_off[D] entries); q_upper < 0 means "no
+ * bound" and counts as u_max.  Requests that waited at least max_wait_ms go
+ * first in queue order (starvation guard); the rest follow sorted by bound,
+ * equal bounds in queue order (Eq. (7)).  q_wait_ms may be NULL (no request
+ * is promoted).  order[q_off[d] + i] is the queue-local index of the i-th
+ * request of the new order.  admitted[d] is the largest k such that the
+ * residents of the snapshot plus the first k reordered requests (each
+ * starting now, holding p+t while t <= U) keep the projected peak <= capacity[d]
+ * (0 when the residents alone exceed it).
+ * dev_err bits: NEG_LEN, SEG_OFFSETS, QUEUE_TOO_LONG, SNAPSHOT.
+ * Host errors: NULL, SIZE (D < 1, total < 0), WORKSPACE, HIP.
+ */
+size_t maps_local_order_workspace_size(int32_t D, int64_t total);
+maps_status maps_local_order(const void* snapshot, int32_t D, int32_t u_max,
+                             const int32_t* capacity, const int64_t* q_off, int64_t total,
+                             const int32_t* q_prompt, const int32_t* q_upper,
+                             const int32_t* q_wait_ms, int32_t max_wait_ms,
+                             int32_t* order, int32_t* admitted,
+                             uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Static description of a status code (host). */
+const char* maps_status_string(maps_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAPS_H */

@@ -1,0 +1,277 @@
+"""Python binding of the MAPS scheduler core for MI355X (gfx950).
+
+Thin ctypes front end of ``libmaps.so`` (C ABI in ``include/maps.h``): every
+function below marshals torch device tensors into the library call of the same
+name and enqueues it on the current HIP stream.  All computation happens in
+the library's HIP kernels; there is no CPU path.  PyTorch only supplies device
+memory and the stream.
+
+Steps (paper sections): calibrate -- Sec. 3.2 (uncertainty-aware calibration);
+project -- Sec. 3.3 / App. A (KV occupancy projection); place -- Sec. 3.3,
+Algorithm 1 (global memory-aware placement); local_order -- Sec. 3.3, Eq. (7)
+(local SJF order with starvation promotion and admission).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(HERE, "libmaps.so")
+
+Q_INF = 2**31 - 1
+POLICY_MQ, POLICY_MC = 0, 1
+MAX_LOCAL_QUEUE = 2048
+ERR_BITS = {
+    1: "NEG_LEN", 2: "EDGES_UNSORTED", 4: "INT32_RANGE", 8: "SEG_OFFSETS",
+    16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG",
+}
+
+
+class MapsError(RuntimeError):
+    """A library call returned a negative status or flagged a value error."""
+
+
+_c = ctypes
+_vp, _i32, _i64, _sz = _c.c_void_p, _c.c_int32, _c.c_int64, _c.c_size_t
+_SIGNATURES = {
+    "maps_calibrate_workspace_size": (_sz, [_i64, _i32]),
+    "maps_calibrate": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp,
+                              _vp, _vp, _sz, _vp]),
+    "maps_snapshot_bytes": (_sz, [_i32, _i64, _i32]),
+    "maps_project_workspace_size": (_sz, [_i32, _i64, _i32]),
+    "maps_project": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp, _vp, _sz, _vp]),
+    "maps_place_workspace_size": (_sz, [_i32, _i64, _i32]),
+    "maps_place": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp,
+                          _vp, _vp, _vp, _sz, _vp]),
+    "maps_local_order_workspace_size": (_sz, [_i32, _i64]),
+    "maps_local_order": (_i32, [_vp, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
+                                _vp, _sz, _vp]),
+    "maps_status_string": (_c.c_char_p, [_i32]),
+}
+EXPORTS = tuple(_SIGNATURES)
+
+_LIB = None
+
+
+def library():
+    """The loaded ``libmaps.so``; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIBRARY):
+            raise MapsError(f"{LIBRARY} is not built: run paper_2609_15359_amd.build.build() "
+                            "(hipcc for gfx950); there is no fallback path")
+        lib = ctypes.CDLL(LIBRARY)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return library().maps_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise MapsError(f"{what}: {status_string(status)} ({status})")
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise MapsError(f"{name} must be a device tensor (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise MapsError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes: int, device, given=None):
+    if given is not None and given.numel() >= nbytes:
+        return given
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def new_error_word(device=None) -> torch.Tensor:
+    """A zeroed device word for the MAPS_ERR_* bits (int32 storage of a uint32)."""
+    return torch.zeros(1, dtype=torch.int32, device=device or "cuda")
+
+
+def error_names(bits: int) -> list[str]:
+    return [name for b, name in ERR_BITS.items() if bits & b]
+
+
+def check_errors(dev_err: torch.Tensor):
+    """Synchronizes and raises MapsError if any value-error bit is set."""
+    bits = int(dev_err.item()) & 0xFFFFFFFF
+    if bits:
+        raise MapsError("device value error: " + ", ".join(error_names(bits)))
+
+
+def capacity_tokens(capacity_bytes: torch.Tensor, bytes_per_token: int) -> torch.Tensor:
+    """KV capacity in bytes -> tokens (App. A: tokens map to bytes by model
+    constants).  floor(C / b) is exact for the test peak * b <= C."""
+    return torch.div(capacity_bytes, int(bytes_per_token), rounding_mode="floor").to(torch.int32)
+
+
+# ---------------------------------------------------------------------------
+# 1. calibration (Sec. 3.2)
+# ---------------------------------------------------------------------------
+
+def calibrate(pred, truth, edges, alpha_ppm: int, apply_pred=None, u_max: int = 0,
+              dev_err=None, workspace=None, out=None):
+    """Per-bucket conformal quantiles q[nb], bucket sizes, and bounds for apply_pred."""
+    pred = _dev(pred, torch.int32, "pred")
+    dev = pred.device
+    truth = _dev(truth, torch.int32, "truth")
+    edges = _dev(edges, torch.int32, "edges")
+    nb = edges.numel() + 1
+    n = pred.numel()
+    if truth.numel() != n:
+        raise MapsError("pred and truth differ in length")
+    m = 0 if apply_pred is None else _dev(apply_pred, torch.int32, "apply_pred").numel()
+    q = torch.empty(nb, dtype=torch.int32, device=dev) if out is None else out["q"]
+    cnt = torch.empty(nb, dtype=torch.int32, device=dev) if out is None else out["count"]
+    U = (torch.empty(m, dtype=torch.int32, device=dev) if out is None else out["U"]) if m else None
+    err = new_error_word(dev) if dev_err is None else dev_err
+    lib = library()
+    ws_bytes = lib.maps_calibrate_workspace_size(n, nb)
+    ws = _workspace(ws_bytes, dev, workspace)
+    st = lib.maps_calibrate(_ptr(pred), _ptr(truth), n, _ptr(edges) if nb > 1 else None, nb,
+                            int(alpha_ppm), _ptr(q), _ptr(cnt), _ptr(apply_pred) if m else None, m,
+                            int(u_max), _ptr(U), _ptr(err), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "maps_calibrate")
+    return q, cnt, U, err
+
+
+# ---------------------------------------------------------------------------
+# 2. projection (Sec. 3.3, App. A)
+# ---------------------------------------------------------------------------
+
+def snapshot_bytes(D: int, n_total: int, u_max: int) -> int:
+    return int(library().maps_snapshot_bytes(int(D), int(n_total), int(u_max)))
+
+
+def project(seg_off, prompt, generated, upper, u_max: int, snapshot=None, dev_err=None,
+            base_peak=None):
+    """Occupancy snapshot of D decoders and their base peaks."""
+    seg_off = _dev(seg_off, torch.int64, "seg_off")
+    dev = seg_off.device
+    D = seg_off.numel() - 1
+    n = prompt.numel()
+    for name, t in (("prompt", prompt), ("generated", generated), ("upper", upper)):
+        _dev(t, torch.int32, name)
+        if t.numel() != n:
+            raise MapsError("prompt, generated and upper differ in length")
+    nbytes = snapshot_bytes(D, n, u_max)
+    if nbytes == 0:
+        raise MapsError("invalid snapshot size arguments")
+    snap = snapshot if snapshot is not None else torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    bp = torch.empty(D, dtype=torch.int32, device=dev) if base_peak is None else base_peak
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = library().maps_project(D, _ptr(seg_off), n, _ptr(prompt), _ptr(generated), _ptr(upper),
+                                int(u_max), _ptr(snap), snap.numel(), _ptr(bp), _ptr(err), None, 0,
+                                _stream(dev))
+    _check(st, "maps_project")
+    return Snapshot(data=snap, D=D, n_total=n, u_max=int(u_max)), bp, err
+
+
+@dataclass
+class Snapshot:
+    data: torch.Tensor
+    D: int
+    n_total: int
+    u_max: int
+
+
+# ---------------------------------------------------------------------------
+# 3. placement (Sec. 3.3, Algorithm 1)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Placement:
+    choice: torch.Tensor
+    chosen_peak: torch.Tensor
+    chosen_overflow: torch.Tensor
+    flags: torch.Tensor
+    pair_peak: torch.Tensor | None
+    dev_err: torch.Tensor
+
+
+def place_workspace_bytes(D: int, A: int, u_max: int) -> int:
+    return int(library().maps_place_workspace_size(int(D), int(A), int(u_max)))
+
+
+def place(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, policy: int = POLICY_MQ,
+          rr_offset: int = 0, want_pairs: bool = True, dev_err=None, workspace=None,
+          out: Placement | None = None) -> Placement:
+    """Choice of decoder for every arrival, and optionally every pair's peak."""
+    capacity = _dev(capacity, torch.int32, "capacity")
+    dev = capacity.device
+    queue_len = _dev(queue_len, torch.int32, "queue_len")
+    a_prompt = _dev(a_prompt, torch.int32, "a_prompt")
+    a_upper = _dev(a_upper, torch.int32, "a_upper")
+    D, A = snapshot.D, a_prompt.numel()
+    if capacity.numel() != D or queue_len.numel() != D or a_upper.numel() != A:
+        raise MapsError("capacity/queue_len must have D entries and a_upper A entries")
+    if out is None:
+        out = Placement(
+            choice=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_peak=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_overflow=torch.empty(A, dtype=torch.int32, device=dev),
+            flags=torch.empty(A, dtype=torch.uint8, device=dev),
+            pair_peak=torch.empty((D, A), dtype=torch.int32, device=dev) if want_pairs else None,
+            dev_err=new_error_word(dev) if dev_err is None else dev_err)
+    lib = library()
+    ws = _workspace(lib.maps_place_workspace_size(D, A, snapshot.u_max), dev, workspace)
+    st = lib.maps_place(_ptr(snapshot.data), D, snapshot.u_max, _ptr(capacity), _ptr(queue_len),
+                        _ptr(a_prompt), _ptr(a_upper), A, int(policy), int(rr_offset),
+                        _ptr(out.choice), _ptr(out.chosen_peak), _ptr(out.chosen_overflow),
+                        _ptr(out.flags), _ptr(out.pair_peak), _ptr(out.dev_err), _ptr(ws),
+                        ws.numel(), _stream(dev))
+    _check(st, "maps_place")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# 4. local order (Sec. 3.3, Eq. (7); App. A, Eq. (10))
+# ---------------------------------------------------------------------------
+
+def local_order(snapshot: Snapshot, capacity, q_off, q_prompt, q_upper, q_wait_ms=None,
+                max_wait_ms: int = 2**31 - 1, dev_err=None, order=None, admitted=None):
+    """New order of every decoder's queue and the admitted prefix length."""
+    capacity = _dev(capacity, torch.int32, "capacity")
+    dev = capacity.device
+    q_off = _dev(q_off, torch.int64, "q_off")
+    q_prompt = _dev(q_prompt, torch.int32, "q_prompt")
+    q_upper = _dev(q_upper, torch.int32, "q_upper")
+    if q_wait_ms is not None:
+        _dev(q_wait_ms, torch.int32, "q_wait_ms")
+    D, total = snapshot.D, q_prompt.numel()
+    if q_off.numel() != D + 1 or q_upper.numel() != total:
+        raise MapsError("q_off must have D+1 entries and q_upper as many as q_prompt")
+    order = torch.empty(total, dtype=torch.int32, device=dev) if order is None else order
+    admitted = torch.empty(D, dtype=torch.int32, device=dev) if admitted is None else admitted
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = library().maps_local_order(_ptr(snapshot.data), D, snapshot.u_max, _ptr(capacity),
+                                    _ptr(q_off), total, _ptr(q_prompt), _ptr(q_upper),
+                                    _ptr(q_wait_ms), int(max_wait_ms), _ptr(order), _ptr(admitted),
+                                    _ptr(err), None, 0, _stream(dev))
+    _check(st, "maps_local_order")
+    return order, admitted, err

@@ -1,0 +1,328 @@
+// Uncertainty-aware calibration (Sec. 3.2, Eqs. (2)-(4)) on gfx950.
+//
+// Per length bucket b the conformal quantile is the k_b-th smallest one-sided
+// score s = max(0, L - L_hat).  It is found by a most-significant-digit-first
+// radix select over the 32-bit scores, 8 bits per pass, all buckets at once:
+//   cal_score   scores + bucket ids (binary search of the edges in LDS),
+//               bucket sizes and the largest score;
+//   cal_rank    k_b = ceil((1 - alpha)(n_b + 1)) in integers;
+//   cal_hist    per pass: histogram of the current digit of the scores whose
+//               higher digits equal the bucket's selected prefix (LDS
+//               histograms flushed with atomics; passes above the largest
+//               score's top digit are skipped on the device);
+//   cal_select  per pass: the digit holding the k_b-th element, one wavefront
+//               per bucket (wavefront scan over 256 bins);
+//   cal_finish  q_b, n_b;  cal_apply  U = min(L_hat + q_b, u_max).
+// All reductions are integer additions, so the result is deterministic.
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace {
+
+constexpr int kNT = 256;             // threads of the streaming kernels
+constexpr int kHistNT = 1024;        // threads of the histogram kernel
+constexpr int kLdsEdgesMax = 8192;   // buckets whose edges and sizes fit LDS
+constexpr int kLdsHistBuckets = 128; // buckets whose 256-bin histograms fit LDS
+
+struct CalWorkspace {
+    int32_t* s;        // [n] scores
+    uint16_t* b;       // [n] bucket ids
+    uint32_t* cnt;     // [nb] bucket sizes
+    int32_t* krem;     // [nb] rank still to find inside the prefix, -1 when q is infinite
+    uint32_t* prefix;  // [nb] selected high digits of q
+    uint32_t* hist;    // [nb][256]
+    uint32_t* maxs;    // [1] largest score
+    size_t bytes;
+};
+
+CalWorkspace cal_carve(void* base, int64_t n, int32_t nb) {
+    CalWorkspace w;
+    size_t off = 0;
+    char* p = static_cast<char*>(base);
+    auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
+    w.s = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
+    w.b = reinterpret_cast<uint16_t*>(take(size_t(n) * 2));
+    w.cnt = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
+    w.krem = reinterpret_cast<int32_t*>(take(size_t(nb) * 4));
+    w.prefix = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
+    w.hist = reinterpret_cast<uint32_t*>(take(size_t(nb) * 256 * 4));
+    w.maxs = reinterpret_cast<uint32_t*>(take(4));
+    w.bytes = off;
+    return w;
+}
+
+// Number of edges <= v among edges[0..ne-1] (upper bound of v).
+__device__ inline int bucket_of(const int32_t* edges, int ne, int32_t v) {
+    int lo = 0, hi = ne;
+    while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (edges[mid] <= v) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ void cal_init(int nb, uint32_t* cnt, uint32_t* hist, uint32_t* maxs) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < int64_t(nb) * 256; i += stride) {
+        hist[i] = 0;
+        if (i < nb) cnt[i] = 0;
+        if (i == 0) maxs[0] = 0;
+    }
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(kNT) void cal_score(const int32_t* __restrict__ pred,
+                                                 const int32_t* __restrict__ truth, int64_t n,
+                                                 const int32_t* __restrict__ edges, int nb,
+                                                 int32_t* __restrict__ s_out, uint16_t* __restrict__ b_out,
+                                                 uint32_t* __restrict__ cnt, uint32_t* __restrict__ maxs,
+                                                 uint32_t* dev_err) {
+    extern __shared__ int32_t lds[];
+    const int ne = nb - 1;
+    const int32_t* e = edges;
+    uint32_t* c = cnt;
+    if constexpr (kLds) {
+        int32_t* le = lds;
+        uint32_t* lc = reinterpret_cast<uint32_t*>(lds + ne);
+        for (int i = threadIdx.x; i < ne; i += kNT) le[i] = edges[i];
+        for (int i = threadIdx.x; i < nb; i += kNT) lc[i] = 0;
+        __syncthreads();
+        e = le;
+        c = lc;
+    }
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i + 1 < ne; i += kNT)
+            if (edges[i] > edges[i + 1]) raise_error(dev_err, MAPS_ERR_EDGES_UNSORTED);
+    }
+    uint32_t local_max = 0;
+    bool bad = false;
+    const int64_t stride = int64_t(gridDim.x) * kNT;
+    for (int64_t i = int64_t(blockIdx.x) * kNT + threadIdx.x; i < n; i += stride) {
+        int32_t p = pred[i], t = truth[i];
+        bad |= (p < 0) | (t < 0);
+        int64_t d = int64_t(t) - p;     // Eq. (2): s = max(0, L - L_hat)
+        int32_t s = d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
+        int b = bucket_of(e, ne, p);
+        s_out[i] = s;
+        b_out[i] = uint16_t(b);
+        atomicAdd(&c[b], 1u);
+        local_max = local_max > uint32_t(s) ? local_max : uint32_t(s);
+    }
+    if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
+    local_max = wave_reduce_max(local_max);
+    if (threadIdx.x % kWave == 0 && local_max) atomicMax(maxs, local_max);
+    if constexpr (kLds) {
+        __syncthreads();
+        for (int i = threadIdx.x; i < nb; i += kNT)
+            if (c[i]) atomicAdd(&cnt[i], c[i]);
+    }
+}
+
+__global__ void cal_rank(int nb, int32_t alpha_ppm, const uint32_t* cnt, int32_t* krem, uint32_t* prefix) {
+    int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nb) return;
+    int64_t nbk = cnt[b];
+    int64_t k = ((int64_t(1000000 - alpha_ppm)) * (nbk + 1) + 999999) / 1000000;  // Eq. (3)
+    krem[b] = (k <= nbk) ? int32_t(k) : -1;
+    prefix[b] = 0;
+}
+
+__device__ inline bool pass_skipped(const uint32_t* maxs, int shift) {
+    return shift > 0 && (maxs[0] >> shift) == 0u;
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(kHistNT) void cal_hist(const int32_t* __restrict__ s, const uint16_t* __restrict__ bk,
+                                                    int64_t n, int nb, int shift,
+                                                    const int32_t* __restrict__ krem,
+                                                    const uint32_t* __restrict__ prefix,
+                                                    uint32_t* __restrict__ hist, const uint32_t* maxs) {
+    if (pass_skipped(maxs, shift)) return;
+    extern __shared__ uint32_t lh[];
+    uint32_t* h = hist;
+    int32_t* lk = nullptr;
+    uint32_t* lp = nullptr;
+    if constexpr (kLds) {
+        h = lh;
+        lk = reinterpret_cast<int32_t*>(lh + nb * 256);
+        lp = lh + nb * 256 + nb;
+        for (int i = threadIdx.x; i < nb * 256; i += kHistNT) lh[i] = 0;
+        for (int i = threadIdx.x; i < nb; i += kHistNT) { lk[i] = krem[i]; lp[i] = prefix[i]; }
+        __syncthreads();
+    }
+    const int64_t stride = int64_t(gridDim.x) * kHistNT;
+    for (int64_t i = int64_t(blockIdx.x) * kHistNT + threadIdx.x; i < n; i += stride) {
+        int b = bk[i];
+        int32_t k = kLds ? lk[b] : krem[b];
+        if (k < 0) continue;
+        uint32_t v = uint32_t(s[i]);
+        uint32_t pre = kLds ? lp[b] : prefix[b];
+        if (uint32_t(uint64_t(v) >> (shift + 8)) != pre) continue;
+        atomicAdd(&h[b * 256 + ((v >> shift) & 255u)], 1u);
+    }
+    if constexpr (kLds) {
+        __syncthreads();
+        for (int i = threadIdx.x; i < nb * 256; i += kHistNT)
+            if (lh[i]) atomicAdd(&hist[i], lh[i]);
+    }
+}
+
+// One wavefront per bucket: the digit whose cumulative count reaches k.
+__global__ __launch_bounds__(kNT) void cal_select(int nb, int shift, uint32_t* __restrict__ hist,
+                                                  int32_t* __restrict__ krem, uint32_t* __restrict__ prefix,
+                                                  const uint32_t* maxs) {
+    if (pass_skipped(maxs, shift)) return;
+    const int lane = threadIdx.x % kWave;
+    const int b = blockIdx.x * (kNT / kWave) + threadIdx.x / kWave;
+    if (b >= nb) return;
+    uint32_t* row = hist + size_t(b) * 256;
+    const int32_t k = krem[b];
+    uint32_t h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { h[j] = row[lane * 4 + j]; row[lane * 4 + j] = 0; }
+    if (k < 0) return;
+    uint32_t mine = h[0] + h[1] + h[2] + h[3];
+    uint32_t incl = wave_incl_scan_add(mine);
+    uint32_t c = incl - mine;
+    int digit = -1;
+    uint32_t newk = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (digit < 0 && c < uint32_t(k) && c + h[j] >= uint32_t(k)) { digit = lane * 4 + j; newk = uint32_t(k) - c; }
+        c += h[j];
+    }
+    uint64_t hit = __ballot(digit >= 0);
+    if (hit == 0) return;  // cannot happen on consistent input
+    int src = __ffsll((unsigned long long)hit) - 1;
+    digit = __shfl(digit, src, kWave);
+    newk = __shfl(newk, src, kWave);
+    if (lane == 0) {
+        prefix[b] = (prefix[b] << 8) | uint32_t(digit);
+        krem[b] = int32_t(newk);
+    }
+}
+
+__global__ void cal_finish(int nb, const int32_t* krem, const uint32_t* prefix, const uint32_t* cnt,
+                           int32_t* q_out, int32_t* count_out) {
+    int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nb) return;
+    q_out[b] = krem[b] < 0 ? MAPS_Q_INF : int32_t(prefix[b]);
+    count_out[b] = int32_t(cnt[b]);
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pred, int64_t m,
+                                                 const int32_t* __restrict__ edges, int nb,
+                                                 const int32_t* __restrict__ q, int32_t u_max,
+                                                 int32_t* __restrict__ U) {
+    extern __shared__ int32_t lds[];
+    const int ne = nb - 1;
+    const int32_t* e = edges;
+    const int32_t* qq = q;
+    if constexpr (kLds) {
+        int32_t* le = lds;
+        int32_t* lq = lds + ne;
+        for (int i = threadIdx.x; i < ne; i += kNT) le[i] = edges[i];
+        for (int i = threadIdx.x; i < nb; i += kNT) lq[i] = q[i];
+        __syncthreads();
+        e = le;
+        qq = lq;
+    }
+    const int64_t stride = int64_t(gridDim.x) * kNT;
+    for (int64_t i = int64_t(blockIdx.x) * kNT + threadIdx.x; i < m; i += stride) {
+        int32_t p = pred[i];
+        int32_t out;
+        if (p < 0) {
+            out = -1;  // no prediction: no bound
+        } else {
+            int32_t qb = qq[bucket_of(e, ne, p)];
+            int64_t v = int64_t(p) + qb;  // Eq. (4)
+            out = (qb == MAPS_Q_INF || v > u_max) ? u_max : int32_t(v);
+        }
+        U[i] = out;
+    }
+}
+
+int grid_for(int64_t n, int nt, int per_thread, int cap) {
+    int64_t g = (n + int64_t(nt) * per_thread - 1) / (int64_t(nt) * per_thread);
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return int(g);
+}
+
+}  // namespace
+}  // namespace maps
+
+using namespace maps;
+
+extern "C" size_t maps_calibrate_workspace_size(int64_t n, int32_t nb) {
+    if (n < 0 || nb < 1) return 0;
+    return cal_carve(nullptr, n, nb).bytes;
+}
+
+extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
+                                      const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                                      int32_t* q_out, int32_t* count_out,
+                                      const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
+                                      uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+    if (n < 0 || m < 0 || nb < 1 || nb > 65536 || u_max < 0) return MAPS_E_SIZE;
+    if (alpha_ppm <= 0 || alpha_ppm >= 1000000) return MAPS_E_ALPHA;
+    if (!q_out || !count_out || !dev_err || (n > 0 && (!pred || !truth)) || (nb > 1 && !edges) ||
+        (m > 0 && (!apply_pred || !U_out)) || !workspace)
+        return MAPS_E_NULL;
+    CalWorkspace w = cal_carve(workspace, n, nb);
+    if (workspace_bytes < w.bytes) return MAPS_E_WORKSPACE;
+
+    const bool lds_edges = nb <= kLdsEdgesMax;
+    const bool lds_hist = nb <= kLdsHistBuckets;
+    const int ne = nb - 1;
+
+    hipLaunchKernelGGL(cal_init, dim3(grid_for(int64_t(nb) * 256, kNT, 1, 1024)), dim3(kNT), 0, stream,
+                       nb, w.cnt, w.hist, w.maxs);
+    MAPS_CHECK_LAUNCH();
+    if (n > 0) {
+        const int g = grid_for(n, kNT, 16, 2048);
+        if (lds_edges)
+            hipLaunchKernelGGL(cal_score<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
+                               pred, truth, n, edges, nb, w.s, w.b, w.cnt, w.maxs, dev_err);
+        else
+            hipLaunchKernelGGL(cal_score<false>, dim3(g), dim3(kNT), 0, stream,
+                               pred, truth, n, edges, nb, w.s, w.b, w.cnt, w.maxs, dev_err);
+        MAPS_CHECK_LAUNCH();
+    }
+    hipLaunchKernelGGL(cal_rank, dim3((nb + kNT - 1) / kNT), dim3(kNT), 0, stream,
+                       nb, alpha_ppm, w.cnt, w.krem, w.prefix);
+    MAPS_CHECK_LAUNCH();
+    if (n > 0) {
+        const int gh = grid_for(n, kHistNT, 16, 256);
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            if (lds_hist) {
+                allow_dynamic_lds(cal_hist<true>, size_t(nb) * (256 + 2) * 4);
+                hipLaunchKernelGGL(cal_hist<true>, dim3(gh), dim3(kHistNT), size_t(nb) * (256 + 2) * 4, stream,
+                                   w.s, w.b, n, nb, shift, w.krem, w.prefix, w.hist, w.maxs);
+            } else {
+                hipLaunchKernelGGL(cal_hist<false>, dim3(gh), dim3(kHistNT), 0, stream,
+                                   w.s, w.b, n, nb, shift, w.krem, w.prefix, w.hist, w.maxs);
+            }
+            MAPS_CHECK_LAUNCH();
+            hipLaunchKernelGGL(cal_select, dim3((nb + kNT / kWave - 1) / (kNT / kWave)), dim3(kNT), 0, stream,
+                               nb, shift, w.hist, w.krem, w.prefix, w.maxs);
+            MAPS_CHECK_LAUNCH();
+        }
+    }
+    hipLaunchKernelGGL(cal_finish, dim3((nb + kNT - 1) / kNT), dim3(kNT), 0, stream,
+                       nb, w.krem, w.prefix, w.cnt, q_out, count_out);
+    MAPS_CHECK_LAUNCH();
+    if (m > 0) {
+        const int g = grid_for(m, kNT, 8, 4096);
+        if (lds_edges)
+            hipLaunchKernelGGL(cal_apply<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
+                               apply_pred, m, edges, nb, q_out, u_max, U_out);
+        else
+            hipLaunchKernelGGL(cal_apply<false>, dim3(g), dim3(kNT), 0, stream,
+                               apply_pred, m, edges, nb, q_out, u_max, U_out);
+        MAPS_CHECK_LAUNCH();
+    }
+    return MAPS_OK;
+}

@@ -1,0 +1,265 @@
+// Projection of each decoder's KV occupancy (Sec. 3.3; App. A, Eq. (8)) on gfx950.
+//
+// One workgroup per decoder turns the residents' (prompt, generated, bound)
+// triples into the snapshot described in maps_internal.hpp, without sorting:
+//   1. every remaining length R = max(U - g, 0) sets its bit in a bitmap over
+//      the step axis (LDS atomics);
+//   2. an exclusive scan of the words' popcounts ranks the distinct R values:
+//      the event index of R is the number of set bits below it;
+//   3. residents add 1 and p + g to their event's counters (integer atomics,
+//      so the sums are deterministic);
+//   4. reverse scans give N_e and S_e, a forward max-scan the prefix maxima
+//      PMX_e, a max-reduction the base peak.
+// Small decoders keep every array in LDS; decoders that do not fit run the
+// same steps on their own slice of the snapshot in HBM.
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace {
+
+constexpr int kNT = 1024;
+constexpr size_t kLdsBudget = 150 * 1024;
+
+// Arrays of one decoder: bitmap words, events before each word, and per event
+// the count, the p+g sum, the time and the prefix maximum.
+struct LdsArrays {
+    uint32_t *bits, *wpre, *cnt, *wsum, *tau, *pmx;
+    __device__ uint32_t& B(int64_t w) { return bits[w]; }
+    __device__ uint32_t& P(int64_t w) { return wpre[w]; }
+    __device__ uint32_t& C(int64_t e) { return cnt[e]; }
+    __device__ uint32_t& S(int64_t e) { return wsum[e]; }
+    __device__ uint32_t& T(int64_t e) { return tau[e]; }
+    __device__ uint32_t& M(int64_t e) { return pmx[e]; }
+};
+
+// The same arrays laid directly over the decoder's slice of the snapshot:
+// rank word {bits, before} and record {PMX, S, N, tau}.
+struct HbmArrays {
+    uint32_t* rank;  // 2 words per rank entry
+    uint32_t* rec;   // 4 words per record
+    __device__ uint32_t& B(int64_t w) { return rank[2 * w]; }
+    __device__ uint32_t& P(int64_t w) { return rank[2 * w + 1]; }
+    __device__ uint32_t& C(int64_t e) { return rec[4 * e + 2]; }
+    __device__ uint32_t& S(int64_t e) { return rec[4 * e + 1]; }
+    __device__ uint32_t& T(int64_t e) { return rec[4 * e + 3]; }
+    __device__ uint32_t& M(int64_t e) { return rec[4 * e + 0]; }
+};
+
+__device__ inline int64_t remaining(int32_t U, int32_t g) {
+    int64_t R = int64_t(U) - g;
+    return R > 0 ? R : 0;
+}
+
+// Phase boundary: every thread's writes of the previous phase are visible to
+// the whole workgroup.  For arrays in HBM the vector L1 is also invalidated,
+// since values produced by L2 atomics or by other waves may be cached stale.
+template <bool kInLds>
+__device__ inline void phase() {
+    __syncthreads();
+    if constexpr (!kInLds) __threadfence();
+}
+
+struct Scratch {
+    int64_t red64[kNT / kWave];
+    uint32_t red32[kNT / kWave];
+};
+
+template <bool kInLds, typename Arr>
+__device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int32_t* __restrict__ p,
+                            const int32_t* __restrict__ g, const int32_t* __restrict__ U, int32_t u_max, int32_t W,
+                            SnapView V, int64_t rec_off, int32_t* __restrict__ base_peak, uint32_t* dev_err,
+                            Scratch& sc) {
+    const int tid = threadIdx.x;
+    for (int64_t w = tid; w < W; w += kNT) a.B(w) = 0u;
+    phase<kInLds>();
+
+    // 1. event bitmap and total demand sum_r (p + g + R)
+    int64_t tot = 0;
+    bool neg = false, range = false;
+    for (int64_t r = lo + tid; r < hi; r += kNT) {
+        int32_t pr = p[r], gr = g[r], ur = U[r];
+        neg |= (pr < 0) | (gr < 0) | (ur < 0);
+        pr = pr < 0 ? 0 : pr;
+        gr = gr < 0 ? 0 : gr;
+        int64_t R = remaining(ur < 0 ? 0 : ur, gr);
+        if (R > u_max) { range = true; R = u_max; }
+        atomicOr(&a.B(R >> 5), 1u << (R & 31));
+        tot += int64_t(pr) + gr + R;
+    }
+    if (neg) raise_error(dev_err, MAPS_ERR_NEG_LEN);
+    if (range) raise_error(dev_err, MAPS_ERR_BOUND_RANGE);
+    tot = block_reduce_add<kNT>(tot, sc.red64);
+    if (tid == 0 && tot + u_max > int64_t(INT32_MAX)) raise_error(dev_err, MAPS_ERR_INT32_RANGE);
+    phase<kInLds>();
+
+    // 2. events before each bitmap word
+    const uint32_t E = block_scan<kNT, false, false, true, uint32_t>(
+        W, 0u, [&](int64_t w) { return uint32_t(__popc(a.B(w))); },
+        [&](int64_t w, uint32_t v) { a.P(w) = v; }, sc.red32);
+    phase<kInLds>();
+
+    // 3. per-event counters
+    for (int64_t e = tid; e < E; e += kNT) { a.C(e) = 0u; a.S(e) = 0u; }
+    for (int64_t w = tid; w < W; w += kNT) {       // event times, in rank order
+        uint32_t bits = a.B(w), e = a.P(w);
+        while (bits) {
+            a.T(e++) = uint32_t(w * 32 + (__ffs(bits) - 1));
+            bits &= bits - 1u;
+        }
+    }
+    phase<kInLds>();
+    for (int64_t r = lo + tid; r < hi; r += kNT) {
+        int32_t pr = p[r], gr = g[r], ur = U[r];
+        pr = pr < 0 ? 0 : pr;
+        gr = gr < 0 ? 0 : gr;
+        int64_t R = remaining(ur < 0 ? 0 : ur, gr);
+        if (R > u_max) R = u_max;
+        uint32_t word = a.B(R >> 5);
+        uint32_t e = a.P(R >> 5) + __popc(word & ((1u << (R & 31)) - 1u));
+        atomicAdd(&a.C(e), 1u);
+        atomicAdd(&a.S(e), uint32_t(pr) + uint32_t(gr));
+    }
+    phase<kInLds>();
+
+    // 4. N_e and S_e: suffix sums over the events
+    block_scan<kNT, false, true, false, uint32_t>(
+        E, 0u, [&](int64_t e) { return a.C(e); }, [&](int64_t e, uint32_t v) { a.C(e) = v; }, sc.red32);
+    block_scan<kNT, false, true, false, uint32_t>(
+        E, 0u, [&](int64_t e) { return a.S(e); }, [&](int64_t e, uint32_t v) { a.S(e) = v; }, sc.red32);
+    phase<kInLds>();
+    // PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1))
+    const int32_t pmx_end = block_scan<kNT, true, false, true, int32_t>(
+        E, 0,
+        [&](int64_t e) { return int32_t(a.S(e) + a.T(e) * (a.C(e) + 1u)); },
+        [&](int64_t e, int32_t v) { a.M(e) = uint32_t(v); }, reinterpret_cast<int32_t*>(sc.red32));
+    phase<kInLds>();
+    // base peak = max(0, max_e S_e + tau_e N_e)
+    int32_t bmax = 0;
+    for (int64_t e = tid; e < E; e += kNT) {
+        int32_t o = int32_t(a.S(e) + a.T(e) * a.C(e));
+        bmax = bmax > o ? bmax : o;
+    }
+    const int32_t base = block_reduce_max<kNT>(bmax, reinterpret_cast<int32_t*>(sc.red32));
+
+    // 5. write the snapshot slice
+    int4* rec = V.rec + rec_off;
+    uint2* rank = V.rank + int64_t(d) * W;
+    if constexpr (kInLds) {
+        for (int64_t e = tid; e < E; e += kNT)
+            rec[e] = make_int4(int32_t(a.M(e)), int32_t(a.S(e)), int32_t(a.C(e) + 1u), int32_t(a.T(e)));
+        for (int64_t w = tid; w < W; w += kNT) rank[w] = make_uint2(a.B(w), a.P(w));
+    } else {
+        for (int64_t e = tid; e < E; e += kNT) a.C(e) += 1u;
+    }
+    if (tid == 0) {
+        rec[E] = make_int4(pmx_end, 0, 1, INT32_MAX);
+        DecHeader h;
+        h.rec_off = rec_off;
+        h.tot = tot;
+        h.E = int32_t(E);
+        h.base_peak = base;
+        h.pad[0] = h.pad[1] = 0;
+        V.dec[d] = h;
+        base_peak[d] = base;
+    }
+}
+
+__global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t* __restrict__ seg_off,
+                                                        int64_t n_total, const int32_t* __restrict__ p,
+                                                        const int32_t* __restrict__ g,
+                                                        const int32_t* __restrict__ U, int32_t u_max,
+                                                        SnapLayout L, void* snap, int32_t* __restrict__ base_peak,
+                                                        int64_t lds_cap, uint32_t* dev_err) {
+    extern __shared__ uint32_t lds[];
+    __shared__ Scratch sc;
+    const int32_t d = blockIdx.x;
+    const int32_t W = L.W;
+    SnapView V = snap_view(snap, L);
+    int64_t lo = seg_off[d], hi = seg_off[d + 1];
+    if (!(0 <= lo && lo <= hi && hi <= n_total)) {
+        if (threadIdx.x == 0) raise_error(dev_err, MAPS_ERR_SEG_OFFSETS);
+        lo = lo < 0 ? 0 : (lo > n_total ? n_total : lo);
+        hi = lo;
+    }
+    const int64_t rec_off = lo + d;   // decoder d owns records [lo + d, hi + d]
+    if (lds_cap > 0 && hi - lo <= lds_cap) {
+        LdsArrays a;
+        a.bits = lds;
+        a.wpre = lds + W;
+        a.cnt = lds + 2 * W;
+        a.wsum = a.cnt + lds_cap;
+        a.tau = a.wsum + lds_cap;
+        a.pmx = a.tau + lds_cap;
+        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, V, rec_off, base_peak, dev_err, sc);
+    } else {
+        HbmArrays a;
+        a.rank = reinterpret_cast<uint32_t*>(V.rank + int64_t(d) * W);
+        a.rec = reinterpret_cast<uint32_t*>(V.rec + rec_off);
+        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, V, rec_off, base_peak, dev_err, sc);
+    }
+}
+
+__global__ __launch_bounds__(kNT) void project_finish(int32_t D, int64_t n_total, SnapLayout L, void* snap) {
+    __shared__ int64_t red64[kNT / kWave];
+    __shared__ int32_t red32[kNT / kWave];
+    SnapView V = snap_view(snap, L);
+    int64_t mt = 0;
+    int32_t me = 0;
+    for (int d = threadIdx.x; d < D; d += kNT) {
+        DecHeader h = V.dec[d];
+        mt = mt > h.tot ? mt : h.tot;
+        me = me > h.E + 1 ? me : h.E + 1;
+    }
+    mt = block_reduce_max<kNT>(mt, red64);
+    me = block_reduce_max<kNT>(me, red32);
+    if (threadIdx.x == 0) {
+        SnapHeader h;
+        h.D = D;
+        h.u_max = L.u_max;
+        h.W = L.W;
+        h.n_total = n_total;
+        h.max_tot = mt;
+        h.max_records = me;
+        for (int i = 0; i < 7; ++i) h.pad[i] = 0;
+        h.magic = kSnapMagic;
+        *V.hdr = h;
+    }
+}
+
+}  // namespace
+}  // namespace maps
+
+using namespace maps;
+
+extern "C" size_t maps_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max) {
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max >= (1 << 24)) return 0;
+    return snap_layout(D, n_total, u_max).bytes;
+}
+
+extern "C" size_t maps_project_workspace_size(int32_t, int64_t, int32_t) { return 0; }
+
+extern "C" maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n_total,
+                                    const int32_t* prompt, const int32_t* generated, const int32_t* upper,
+                                    int32_t u_max, void* snapshot, size_t snapshot_bytes, int32_t* base_peak,
+                                    uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max >= (1 << 24)) return MAPS_E_SIZE;
+    if (!seg_off || !snapshot || !base_peak || !dev_err ||
+        (n_total > 0 && (!prompt || !generated || !upper)))
+        return MAPS_E_NULL;
+    const SnapLayout L = snap_layout(D, n_total, u_max);
+    if (snapshot_bytes < L.bytes) return MAPS_E_BUFFER;
+    const size_t fixed = size_t(2) * L.W * 4;
+    int64_t cap = fixed < kLdsBudget ? int64_t((kLdsBudget - fixed) / 16) : 0;
+    if (cap > 8192) cap = 8192;
+    const size_t lds = cap > 0 ? fixed + size_t(cap) * 16 : 0;
+    allow_dynamic_lds(project_decoders, lds);
+    hipLaunchKernelGGL(project_decoders, dim3(D), dim3(kNT), lds, stream, D, seg_off, n_total, prompt, generated,
+                       upper, u_max, L, snapshot, base_peak, cap, dev_err);
+    MAPS_CHECK_LAUNCH();
+    hipLaunchKernelGGL(project_finish, dim3(1), dim3(kNT), 0, stream, D, n_total, L, snapshot);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}

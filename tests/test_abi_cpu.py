@@ -1,0 +1,103 @@
+"""The C-ABI library builds for gfx950, loads, and exports every entry point
+that include/maps.h declares; its host-side argument checks answer without a
+GPU (no kernel is launched on any of these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_15359_amd as maps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "maps.h")
+
+
+def declared():
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(maps_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(maps.LIBRARY):
+        pytest.fail("libmaps.so is not built; run __graft_entry__.build()")
+    return maps.library()
+
+
+def test_header_declares_the_four_steps():
+    names = declared()
+    for n in ("maps_calibrate", "maps_project", "maps_place", "maps_local_order"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    raw = ctypes.CDLL(maps.LIBRARY)
+    for name in declared():
+        assert hasattr(raw, name), name
+    assert sorted(maps.EXPORTS) == declared()
+
+
+def test_library_is_built_for_gfx950():
+    with open(maps.LIBRARY, "rb") as f:
+        blob = f.read()
+    assert b"gfx950" in blob
+
+
+def test_size_queries(lib):
+    # header 256 B + D decoder headers + D*W rank words + (n + D) records
+    D, n, u_max = 4, 100, 8192
+    W = (((u_max + 1) // 32 + 1) + 1) & ~1
+    want = 256 + ((D * 32 + 255) // 256) * 256 + ((D * W * 8 + 255) // 256) * 256 + (n + D) * 16
+    assert lib.maps_snapshot_bytes(D, n, u_max) == want
+    assert lib.maps_snapshot_bytes(0, n, u_max) == 0
+    assert lib.maps_snapshot_bytes(D, n, 1 << 24) == 0
+    assert lib.maps_calibrate_workspace_size(1000, 4) >= 1000 * 6
+    assert lib.maps_place_workspace_size(256, 262144, 32768) >= 262144 * 12
+    assert lib.maps_project_workspace_size(4, 100, 8192) == 0
+    assert lib.maps_local_order_workspace_size(4, 100) == 0
+
+
+def test_status_strings(lib):
+    assert maps.status_string(0) == "ok"
+    assert "alpha" in maps.status_string(-3)
+    assert maps.status_string(-99) == "unknown status"
+
+
+def _v(x):
+    return ctypes.c_void_p(x)
+
+
+def test_host_argument_errors_without_gpu(lib):
+    """Invalid sizes, alpha, policy, NULL pointers and short buffers are refused
+    synchronously, before anything is enqueued."""
+    fake = _v(0x1000)  # never dereferenced: every call below fails its host checks
+    # calibrate: alpha outside (0, 1e6), nb < 1, n < 0, NULL outputs
+    assert lib.maps_calibrate(fake, fake, 10, fake, 2, 0, fake, fake, None, 0, 10, None, fake, fake, 1 << 20, None) == -3
+    assert lib.maps_calibrate(fake, fake, 10, fake, 2, 1000000, fake, fake, None, 0, 10, None, fake, fake, 1 << 20, None) == -3
+    assert lib.maps_calibrate(fake, fake, 10, fake, 0, 100000, fake, fake, None, 0, 10, None, fake, fake, 1 << 20, None) == -2
+    assert lib.maps_calibrate(fake, fake, -1, fake, 2, 100000, fake, fake, None, 0, 10, None, fake, fake, 1 << 20, None) == -2
+    assert lib.maps_calibrate(fake, fake, 10, fake, 2, 100000, None, fake, None, 0, 10, None, fake, fake, 1 << 20, None) == -1
+    assert lib.maps_calibrate(fake, fake, 10, fake, 2, 100000, fake, fake, None, 0, 10, None, fake, fake, 8, None) == -4
+    # project: D < 1, u_max too large, short snapshot buffer
+    assert lib.maps_project(0, fake, 0, fake, fake, fake, 10, fake, 1 << 20, fake, fake, None, 0, None) == -2
+    assert lib.maps_project(1, fake, 0, fake, fake, fake, 1 << 24, fake, 1 << 20, fake, fake, None, 0, None) == -2
+    assert lib.maps_project(4, fake, 100, fake, fake, fake, 8192, fake, 64, fake, fake, None, 0, None) == -7
+    assert lib.maps_project(4, None, 100, fake, fake, fake, 8192, fake, 1 << 20, fake, fake, None, 0, None) == -1
+    # place: policy, negative rr_offset, NULL outputs
+    args = [fake, 4, 8192, fake, fake, fake, fake, 10]
+    assert lib.maps_place(*args, 7, 0, fake, fake, fake, fake, None, fake, fake, 1 << 20, None) == -6
+    assert lib.maps_place(*args, 0, -1, fake, fake, fake, fake, None, fake, fake, 1 << 20, None) == -2
+    assert lib.maps_place(*args, 0, 0, None, fake, fake, fake, None, fake, fake, 1 << 20, None) == -1
+    # local order: D < 1, NULL queue offsets
+    assert lib.maps_local_order(fake, 0, 10, fake, fake, 0, fake, fake, None, 0, fake, fake, fake, None, 0, None) == -2
+    assert lib.maps_local_order(fake, 2, 10, fake, None, 0, fake, fake, None, 0, fake, fake, fake, None, 0, None) == -1
+
+
+def test_binding_refuses_host_tensors(lib):
+    import torch
+    x = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(maps.MapsError):
+        maps.calibrate(x, x, torch.zeros(1, dtype=torch.int32), 100000)
