@@ -26,6 +26,30 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
 DEFAULT_WORKLOAD = "large"     # 256 decoders x 4096 residents, 262,144 arrivals
+PLACEMENT_SOURCES = ("paper_2609_15359_amd/csrc/place.hip", "paper_2609_15359_amd/csrc/maps_internal.hpp")
+
+
+def placement_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in PLACEMENT_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload_name: str):
+    """HBM bytes of one placement pass from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy of known size), or None
+    when there is none for this workload or the placement code changed since."""
+    path = os.path.join(ROOT, "profiles", f"place_traffic_{workload_name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != placement_source_hash():
+        return None
+    return rec.get("placement_bytes")
 
 
 def placement_bytes(D: int, A: int, W: int, events) -> int:
@@ -166,7 +190,7 @@ def main():
                                f"u_max {b.u_max}; per-pair peak matrix written",
                    "decoders": D, "arrivals": A, "pairs": D * A},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
                      "kernel": "maps_place (place_pairs + place_reduce)",
                      "algorithmic_bytes": nbytes, "place_ms": place_ms},
         "breakdown_ms": parts,

@@ -66,8 +66,14 @@ enum {
     MAPS_ERR_SEG_OFFSETS = 8u,      /* segment offsets not non-decreasing in [0, total] */
     MAPS_ERR_BOUND_RANGE = 16u,     /* a remaining length max(U-g,0) exceeds u_max */
     MAPS_ERR_SNAPSHOT = 32u,        /* snapshot was not built for this (D, u_max) */
-    MAPS_ERR_QUEUE_TOO_LONG = 64u   /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
+    MAPS_ERR_QUEUE_TOO_LONG = 64u,  /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
+    MAPS_ERR_TOO_MANY = 128u        /* a decoder with MAPS_MAX_RESIDENTS or more residents */
 };
+
+/* Largest u_max (cap on bounds and remaining lengths) the snapshot accepts,
+ * and the resident count per decoder it supports: 24-bit operands. */
+#define MAPS_MAX_U_MAX ((1 << 24) - 64)
+#define MAPS_MAX_RESIDENTS ((1 << 24) - 1)
 
 /* Longest pending queue of one decoder that maps_local_order accepts. */
 #define MAPS_MAX_LOCAL_QUEUE 2048
@@ -120,8 +126,8 @@ maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
  * until the caller overwrites it and describes the residents at call time.
  * Requires every R <= u_max.
  * dev_err bits: NEG_LEN, SEG_OFFSETS, BOUND_RANGE, INT32_RANGE (when
- * sum_r (p+g+R) + u_max > INT32_MAX for a decoder).
- * Host errors: NULL, SIZE (D < 1, n_total < 0, u_max < 0 or u_max >= 2^24),
+ * sum_r (p+g+R) + u_max > INT32_MAX for a decoder), TOO_MANY.
+ * Host errors: NULL, SIZE (D < 1, n_total < 0, u_max < 0 or u_max > MAPS_MAX_U_MAX),
  * BUFFER, WORKSPACE, HIP.
  */
 size_t maps_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max);

@@ -208,7 +208,7 @@ extern "C" maps_status maps_local_order(const void* snapshot, int32_t D, int32_t
                                         size_t workspace_bytes, hipStream_t stream) {
     (void)workspace;
     (void)workspace_bytes;
-    if (D < 1 || total < 0 || u_max < 0 || u_max >= (1 << 24)) return MAPS_E_SIZE;
+    if (D < 1 || total < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
     if (!snapshot || !capacity || !q_off || !admitted || !dev_err ||
         (total > 0 && (!q_prompt || !q_upper || !order)))
         return MAPS_E_NULL;

@@ -79,7 +79,9 @@ __host__ __device__ inline SnapLayout snap_layout(int32_t D, int64_t n_total, in
     L.off_dec = align256(sizeof(SnapHeader));
     L.off_rank = L.off_dec + align256(size_t(D) * sizeof(DecHeader));
     L.off_rec = L.off_rank + align256(size_t(D) * size_t(L.W) * sizeof(uint2));
-    L.bytes = L.off_rec + size_t(n_total + D) * sizeof(int4);
+    // 64 spare records at the end: placement copies records in transfers of
+    // 64, so it reads up to 63 records past a decoder's last one
+    L.bytes = L.off_rec + size_t(n_total + D + 64) * sizeof(int4);
     return L;
 }
 

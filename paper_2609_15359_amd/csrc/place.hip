@@ -24,7 +24,7 @@
 namespace maps {
 namespace {
 
-constexpr int kNT = 1024;
+constexpr int kNT = 512;          // 8 waves per CU: 256 VGPRs per lane for the arrivals
 constexpr size_t kLdsBytes = 160 * 1024;
 constexpr int kMaxGroups = 8;
 
@@ -55,135 +55,220 @@ __device__ inline bool snapshot_ok(const SnapHeader* h, const SnapLayout& L) {
     return h->magic == kSnapMagic && h->D == L.D && h->u_max == L.u_max && h->W == L.W;
 }
 
-__device__ inline bool decoder_ok(const DecHeader& h, int64_t n_total, int32_t D) {
-    return h.E >= 0 && h.rec_off >= 0 && h.rec_off + h.E + 1 <= n_total + D && h.base_peak >= 0;
-}
-
-template <int kPolicy>
-__device__ inline uint32_t select_key(int32_t peak, int32_t C, int32_t Q) {
-    if constexpr (kPolicy == MAPS_POLICY_MQ)
-        return peak <= C ? uint32_t(Q) : (0x80000000u | uint32_t(peak - C));
-    else
-        return uint32_t(peak - C) ^ 0x80000000u;
-}
-
 __device__ inline int32_t imax(int32_t a, int32_t b) { return a > b ? a : b; }
 
-template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
-__global__ __launch_bounds__(kNT) void place_pairs(PlaceArgs g) {
-    extern __shared__ int4 lds[];
+// Per-thread state of kAPT arrivals: prompt, bound, bound clamped for the
+// rank lookup, index of its rank word and the mask of the bits below it, and
+// the best (key, decoder) seen so far.
+template <int kAPT>
+struct Arrivals {
+    int32_t p[kAPT], U[kAPT], Ucl[kAPT];
+    uint32_t wi[kAPT], mask[kAPT];
+    uint32_t best_key[kAPT];
+    int32_t best_d[kAPT];
+};
+
+// Projected peak of one arrival on one decoder, reading the snapshot in HBM.
+__device__ __forceinline__ int32_t peak_from_hbm(const SnapView& V, int32_t W, int32_t d, int32_t p, int32_t U,
+                                                 int32_t Ucl, uint32_t wi, uint32_t mask) {
+    const DecHeader h = V.dec[d];
+    const uint2 w = V.rank[int64_t(d) * W + wi];
+    uint32_t e = w.y + __popc(w.x & mask);
+    e = e < uint32_t(h.E) ? e : uint32_t(h.E);
+    const int4 r = V.rec[h.rec_off + e];
+    const int32_t lin = r.y + int32_t(__umul24(uint32_t(Ucl), uint32_t(r.z)));
+    const int32_t pf = max(max(r.x, lin), U);
+    return p + pf > h.base_peak ? p + pf : h.base_peak;
+}
+
+// Evaluate every arrival of the thread against one decoder whose rank words
+// and records are at rank/rec (LDS or HBM), write the pair-peak row and keep
+// the best choice.  `kFull`: every arrival of the tile exists.
+// Selection key (smaller is better), with u = peak - C + 2^31:
+//   MQ: u when infeasible (u > 2^31), else Q_d;   MC: u.
+template <int kAPT, bool kFull, bool kPairs, int kPolicy>
+__device__ __forceinline__ void eval_decoder(Arrivals<kAPT>& s, const uint2* rank, const int4* rec, int32_t E,
+                                             int32_t base, int32_t C, int32_t Q, int32_t d, bool first,
+                                             int32_t* prow, int64_t a0, int64_t A) {
+    constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
+    const uint32_t kC = 0x80000000u - uint32_t(C);
+#pragma unroll
+    for (int c = 0; c < kAPT; c += kChunk) {
+        uint2 w[kChunk];
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) w[i] = rank[s.wi[c + i]];
+        int4 r[kChunk];
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            uint32_t e = w[i].y + __popc(w[i].x & s.mask[c + i]);
+            e = e < uint32_t(E) ? e : uint32_t(E);   // stays inside the decoder's records
+            r[i] = rec[e];
+        }
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            const int k = c + i;
+            // PF(U) = max(PMX_e, S_e + U (N_e + 1)), U itself when beyond the last event
+            const int32_t lin = r[i].y + int32_t(__umul24(uint32_t(s.Ucl[k]), uint32_t(r[i].z)));
+            const int32_t pf = max(max(r[i].x, lin), s.U[k]);
+            const int32_t peak = imax(s.p[k] + pf, base);
+            if constexpr (kPairs) {
+                // uniform row base per k, lane offset in a VGPR: no per-arrival 64-bit address
+                int32_t* row = prow + a0 + int64_t(k) * kNT;
+                if (kFull || a0 + int64_t(k) * kNT + threadIdx.x < A)
+                    __builtin_nontemporal_store(s.U[k] < 0 ? -1 : peak, row + threadIdx.x);
+            }
+            const uint32_t u = uint32_t(peak) + kC;
+            uint32_t key;
+            if constexpr (kPolicy == MAPS_POLICY_MQ) key = u > 0x80000000u ? u : uint32_t(Q);
+            else key = u;
+            const bool take = first || key < s.best_key[k];
+            s.best_key[k] = take ? key : s.best_key[k];
+            s.best_d[k] = take ? d : s.best_d[k];
+        }
+    }
+}
+
+// A 16-byte unit as a native vector (kept in registers when staged).
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
+
+// 16-byte unit u of decoder d's snapshot slice: its rank words, then its records.
+__device__ __forceinline__ const int4* snapshot_unit(const SnapView& V, int32_t W, int32_t d, const DecHeader& h,
+                                                     int64_t u) {
+    const int64_t half_w = W / 2;
+    return u < half_w ? reinterpret_cast<const int4*>(V.rank + int64_t(d) * W) + u : V.rec + h.rec_off + (u - half_w);
+}
+
+// Load this thread's first kPF units of decoder d into registers (units past
+// the end re-read the last one, so every lane issues the same loads).
+template <int kPF>
+__device__ __forceinline__ void stage_units(v4i (&stage)[kPF], const SnapView& V, int32_t W, int32_t d,
+                                            const DecHeader& h) {
+    const int64_t last = int64_t(W / 2) + h.E;
+#pragma unroll
+    for (int j = 0; j < kPF; ++j) {
+        const int64_t u = threadIdx.x + int64_t(j) * kNT;
+        stage[j] = *reinterpret_cast<const v4i*>(snapshot_unit(V, W, d, h, u < last ? u : last));
+    }
+}
+
+template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy>
+__device__ __forceinline__ void place_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
+                                           int64_t a0) {
+    constexpr int kPF = 7;   // 16-byte units per thread staged in registers ahead of use
     const SnapLayout& L = g.L;
     const int32_t W = L.W;
-    const SnapView V = snap_view(const_cast<void*>(g.snap), L);
-    if (!snapshot_ok(V.hdr, L)) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-        return;
-    }
-    const int32_t grp = blockIdx.x % g.G;
-    const int64_t tile = blockIdx.x / g.G;
+    const int32_t half_w = W / 2;              // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
     const int32_t d_end = d_begin + g.Dg < L.D ? d_begin + g.Dg : L.D;
-    const int64_t a0 = tile * int64_t(kNT * kAPT);
     const int64_t max_tot = V.hdr->max_tot;
     const int64_t n_total = V.hdr->n_total;
-    const int32_t ucl_max = 32 * W - 1;   // ranks above every event
+    const int32_t ucl_max = 32 * W - 1;        // ranks above every event
+    const int64_t lds_units = g.rec_cap > 0 ? half_w + g.rec_cap : 0;
 
-    uint2* lrank = reinterpret_cast<uint2*>(lds);
-    int4* lrec = lds + W / 2;
-
-    int32_t p[kAPT], U[kAPT], Ucl[kAPT], wi[kAPT], best_d[kAPT], best_peak[kAPT];
-    uint32_t mask[kAPT], best_key[kAPT];
+    Arrivals<kAPT> s;
     bool neg = false, range = false;
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        p[k] = 0;
-        U[k] = -1;
-        if (a < g.A) { p[k] = g.ap[a]; U[k] = g.aU[a]; }
-        neg |= p[k] < 0;
-        if (U[k] >= 0 && int64_t(p[k]) + U[k] + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
-        p[k] = p[k] < 0 ? 0 : p[k];
-        Ucl[k] = U[k] < ucl_max ? U[k] : ucl_max;
-        const int32_t uc = Ucl[k] < 0 ? 0 : Ucl[k];
-        wi[k] = uc >> 5;
-        mask[k] = (1u << (uc & 31)) - 1u;
-        best_key[k] = 0xFFFFFFFFu;
-        best_d[k] = d_begin;
-        best_peak[k] = 0;
+        int32_t p = 0, U = -1;
+        if (kFull || a < g.A) { p = g.ap[a]; U = g.aU[a]; }
+        neg |= p < 0;
+        if (U >= 0 && int64_t(p) + U + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
+        s.p[k] = p < 0 ? 0 : p;
+        s.U[k] = U;
+        const int32_t uc = U < 0 ? 0 : (U < ucl_max ? U : ucl_max);
+        s.Ucl[k] = uc;
+        s.wi[k] = uint32_t(uc >> 5);
+        s.mask[k] = (1u << (uc & 31)) - 1u;
+        s.best_key[k] = 0xFFFFFFFFu;
+        s.best_d[k] = d_begin;
     }
     if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
     if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
 
+    auto fits = [&](const DecHeader& h) { return h.E >= 0 && int64_t(half_w) + h.E + 1 <= lds_units; };
+    auto ok = [&](const DecHeader& h) {
+        return h.E >= 0 && h.rec_off >= 0 && h.rec_off + h.E + 1 <= n_total + L.D && h.base_peak >= 0;
+    };
+
+    v4i stage[kPF];
+    DecHeader h = V.dec[d_begin < d_end ? d_begin : 0];
+    if (d_begin < d_end && ok(h) && fits(h)) stage_units<kPF>(stage, V, W, d_begin, h);
     for (int32_t d = d_begin; d < d_end; ++d) {
-        const DecHeader h = V.dec[d];
         const int32_t C = g.cap[d], Q = g.qlen[d];
         if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-        if (!decoder_ok(h, n_total, L.D)) {
-            if (threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-            continue;
-        }
-        const uint2* rank = V.rank + int64_t(d) * W;
-        const int4* rec = V.rec + h.rec_off;
-        const bool in_lds = g.rec_cap > 0 && h.E + 1 <= g.rec_cap;
+        const bool valid = ok(h);
+        const bool in_lds = valid && fits(h);
+        if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         if (in_lds) {
-            __syncthreads();   // the previous decoder is no longer read
-            const uint4* src = reinterpret_cast<const uint4*>(rank);
-            uint4* dst = reinterpret_cast<uint4*>(lrank);
-            for (int i = threadIdx.x; i < W / 2; i += kNT) dst[i] = src[i];
-            for (int i = threadIdx.x; i <= h.E; i += kNT) lrec[i] = rec[i];
+            __syncthreads();   // every wave finished reading the previous decoder
+            const int64_t units = int64_t(half_w) + h.E + 1;
+#pragma unroll
+            for (int j = 0; j < kPF; ++j) {   // lanes past the end write the spare unit
+                const int64_t u = threadIdx.x + int64_t(j) * kNT;
+                reinterpret_cast<v4i*>(lds)[u < units ? u : lds_units] = stage[j];
+            }
+            for (int64_t u = threadIdx.x + int64_t(kPF) * kNT; u < units; u += kNT) lds[u] = *snapshot_unit(V, W, d, h, u);
             __syncthreads();
         }
-        const uint2* rk = in_lds ? lrank : rank;
-        const int4* rc = in_lds ? lrec : rec;
-        int32_t* prow = kPairs ? g.pair + int64_t(d) * g.A : nullptr;
-#pragma unroll
-        for (int k = 0; k < kAPT; ++k) {
-            const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-            if (a >= g.A) continue;
-            if (U[k] < 0) {
-                if constexpr (kPairs) prow[a] = -1;
-                continue;
-            }
-            const uint2 w = rk[wi[k]];
-            uint32_t e = w.y + __popc(w.x & mask[k]);
-            e = e < uint32_t(h.E) ? e : uint32_t(h.E);   // stays inside the decoder's records
-            const int4 r = rc[e];
-            const int32_t pf = imax(imax(r.x, r.y + Ucl[k] * r.z), U[k]);
-            const int32_t peak = imax(p[k] + pf, h.base_peak);
-            if constexpr (kPairs) prow[a] = peak;
-            const uint32_t key = select_key<kPolicy>(peak, C, Q);
-            if (key < best_key[k] || d == d_begin) {
-                best_key[k] = key;
-                best_d[k] = d;
-                best_peak[k] = peak;
-            }
+        const DecHeader cur = h;
+        if (d + 1 < d_end) {
+            h = V.dec[d + 1];
+            if (ok(h) && fits(h)) stage_units<kPF>(stage, V, W, d + 1, h);   // overlaps the evaluation below
         }
+        if (!valid) continue;
+        int32_t* prow = kPairs ? g.pair + int64_t(d) * g.A : nullptr;
+        if (in_lds)
+            eval_decoder<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const uint2*>(lds), lds + half_w, cur.E,
+                                                        cur.base_peak, C, Q, d, d == d_begin, prow, a0, g.A);
+        else
+            eval_decoder<kAPT, kFull, kPairs, kPolicy>(s, V.rank + int64_t(d) * W, V.rec + cur.rec_off, cur.E,
+                                                        cur.base_peak, C, Q, d, d == d_begin, prow, a0, g.A);
     }
 
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        if (a >= g.A) continue;
+        if (!kFull && a >= g.A) continue;
+        // the chosen pair's peak, evaluated once more from the snapshot in HBM
+        const bool has = d_begin < d_end && s.U[k] >= 0 && ok(V.dec[s.best_d[k]]);
+        const int32_t peak = has ? peak_from_hbm(V, W, s.best_d[k], s.p[k], s.U[k], s.Ucl[k], s.wi[k], s.mask[k]) : 0;
         if constexpr (kFinal) {
-            if (U[k] < 0) {
+            if (s.U[k] < 0) {
                 g.choice[a] = int32_t((g.rr_offset + a) % L.D);
                 g.chosen_peak[a] = -1;
                 g.chosen_over[a] = 0;
                 g.flags[a] = 2;
             } else {
-                const int32_t C = g.cap[best_d[k]];
-                g.choice[a] = best_d[k];
-                g.chosen_peak[a] = best_peak[k];
-                g.chosen_over[a] = best_peak[k] > C ? best_peak[k] - C : 0;
-                g.flags[a] = best_peak[k] <= C ? 1 : 0;
+                const int32_t C = g.cap[s.best_d[k]];
+                g.choice[a] = s.best_d[k];
+                g.chosen_peak[a] = peak;
+                g.chosen_over[a] = peak > C ? peak - C : 0;
+                g.flags[a] = peak <= C ? 1 : 0;
             }
         } else {
             const int64_t o = int64_t(grp) * g.A + a;
-            g.pkey[o] = d_begin < d_end ? best_key[k] : 0xFFFFFFFFu;
-            g.pdec[o] = best_d[k] < L.D ? best_d[k] : 0;
-            g.ppeak[o] = best_peak[k];
+            g.pkey[o] = d_begin < d_end ? s.best_key[k] : 0xFFFFFFFFu;
+            g.pdec[o] = s.best_d[k] < L.D ? s.best_d[k] : 0;
+            g.ppeak[o] = peak;
         }
     }
+}
+
+template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+__global__ __launch_bounds__(kNT) void place_pairs(PlaceArgs g) {
+    extern __shared__ int4 lds[];
+    const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
+    if (!snapshot_ok(V.hdr, g.L)) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    const int32_t grp = blockIdx.x % g.G;
+    const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
+    if (a0 + kNT * kAPT <= g.A)
+        place_tile<kAPT, true, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+    else
+        place_tile<kAPT, false, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
 }
 
 __global__ __launch_bounds__(256) void place_reduce(PlaceArgs g) {
@@ -297,7 +382,7 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
                                   int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
                                   int32_t* pair_peak, uint32_t* dev_err, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream) {
-    if (D < 1 || A < 0 || rr_offset < 0 || u_max < 0 || u_max >= (1 << 24)) return MAPS_E_SIZE;
+    if (D < 1 || A < 0 || rr_offset < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
     if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
     if (!snapshot || !capacity || !queue_len || !dev_err ||
         (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags)))
@@ -335,7 +420,8 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
     // depend on the number of residents; records are addressed through the
     // decoder headers and bound-checked against the snapshot's own count.
     const size_t rank_bytes = size_t(a.L.W) * 8;
-    a.rec_cap = rank_bytes + 64 * 16 <= kLdsBytes ? int64_t((kLdsBytes - rank_bytes) / 16) : 0;
+    // LDS: rank words, records, and one spare 16-byte unit
+    a.rec_cap = rank_bytes + 64 * 16 <= kLdsBytes ? int64_t((kLdsBytes - rank_bytes) / 16) - 1 : 0;
     const size_t lds = a.rec_cap > 0 ? kLdsBytes : 0;
     const int64_t tiles = (A + int64_t(kNT) * apt - 1) / (int64_t(kNT) * apt);
     const dim3 grid(unsigned(tiles * G));

@@ -181,6 +181,10 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
         lo = lo < 0 ? 0 : (lo > n_total ? n_total : lo);
         hi = lo;
     }
+    if (hi - lo >= MAPS_MAX_RESIDENTS) {
+        if (threadIdx.x == 0) raise_error(dev_err, MAPS_ERR_TOO_MANY);
+        hi = lo;
+    }
     const int64_t rec_off = lo + d;   // decoder d owns records [lo + d, hi + d]
     if (lds_cap > 0 && hi - lo <= lds_cap) {
         LdsArrays a;
@@ -232,7 +236,7 @@ __global__ __launch_bounds__(kNT) void project_finish(int32_t D, int64_t n_total
 using namespace maps;
 
 extern "C" size_t maps_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max) {
-    if (D < 1 || n_total < 0 || u_max < 0 || u_max >= (1 << 24)) return 0;
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return 0;
     return snap_layout(D, n_total, u_max).bytes;
 }
 
@@ -245,7 +249,7 @@ extern "C" maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n
                                     hipStream_t stream) {
     (void)workspace;
     (void)workspace_bytes;
-    if (D < 1 || n_total < 0 || u_max < 0 || u_max >= (1 << 24)) return MAPS_E_SIZE;
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
     if (!seg_off || !snapshot || !base_peak || !dev_err ||
         (n_total > 0 && (!prompt || !generated || !upper)))
         return MAPS_E_NULL;

@@ -47,13 +47,14 @@ def test_library_is_built_for_gfx950():
 
 
 def test_size_queries(lib):
-    # header 256 B + D decoder headers + D*W rank words + (n + D) records
+    # header 256 B + D decoder headers + D*W rank words + (n + D) records + 64 spare records
     D, n, u_max = 4, 100, 8192
     W = (((u_max + 1) // 32 + 1) + 1) & ~1
-    want = 256 + ((D * 32 + 255) // 256) * 256 + ((D * W * 8 + 255) // 256) * 256 + (n + D) * 16
+    want = 256 + ((D * 32 + 255) // 256) * 256 + ((D * W * 8 + 255) // 256) * 256 + (n + D + 64) * 16
     assert lib.maps_snapshot_bytes(D, n, u_max) == want
     assert lib.maps_snapshot_bytes(0, n, u_max) == 0
-    assert lib.maps_snapshot_bytes(D, n, 1 << 24) == 0
+    assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 63) == 0
+    assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 64) > 0
     assert lib.maps_calibrate_workspace_size(1000, 4) >= 1000 * 6
     assert lib.maps_place_workspace_size(256, 262144, 32768) >= 262144 * 12
     assert lib.maps_project_workspace_size(4, 100, 8192) == 0
