@@ -52,12 +52,18 @@ def recorded_traffic(workload_name: str):
     return rec.get("placement_bytes")
 
 
-def placement_bytes(D: int, A: int, W: int, events) -> int:
+def placement_bytes(D: int, A: int, u_max: int, W: int, events) -> int:
     """Algorithmic bytes of one placement pass: every input read once and
     every output written once.  Pair matrix 4 B/pair; arrivals 8 B in and
-    13 B out (choice, peak, overflow, flags); per decoder its rank words
-    (8 B each), its E+1 records (16 B each), header, capacity and queue length."""
-    snap = sum(8 * W + 16 * (int(e) + 1) + 32 + 8 for e in events)
+    13 B out (choice, peak, overflow, flags); per decoder its header, capacity
+    and queue length, and its dense profile (4 B per entry, u_max + 1 entries
+    rounded up to 4) or, for bounds too long for a profile, its rank words
+    (8 B each) and its E+1 records (16 B each)."""
+    P = (u_max + 4) & ~3 if u_max + 1 <= 16384 else 0
+    if P:
+        snap = D * (4 * P + 32 + 8)
+    else:
+        snap = sum(8 * W + 16 * (int(e) + 1) + 32 + 8 for e in events)
     return 4 * D * A + (8 + 13) * A + snap
 
 
@@ -168,7 +174,7 @@ def main():
     hdr = ws.snapshot[256:256 + 32 * D].view(torch.int32).view(D, 8).cpu().numpy()
     events_per_decoder = hdr[:, 4]
     W = (((db.u_max + 1) // 32 + 1) + 1) & ~1
-    nbytes = placement_bytes(D, A, W, events_per_decoder)
+    nbytes = placement_bytes(D, A, db.u_max, W, events_per_decoder)
     achieved = nbytes / (place_ms * 1e-3) / 1e9
     feasible = float(np.mean(ws.placement.flags.cpu().numpy() & 1))
 
@@ -191,7 +197,7 @@ def main():
                    "decoders": D, "arrivals": A, "pairs": D * A},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
-                     "kernel": "maps_place (place_pairs + place_reduce)",
+                     "kernel": "maps_place (place_records + place_reduce)",
                      "algorithmic_bytes": nbytes, "place_ms": place_ms},
         "breakdown_ms": parts,
         "mean_events_per_decoder": float(np.mean(events_per_decoder)),

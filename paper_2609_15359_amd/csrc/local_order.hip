@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kNT) void local_order_kernel(LocalArgs g) {
         return;
     }
     const DecHeader h = V.dec[d];
-    if (!(h.E >= 0 && h.rec_off >= 0 && h.rec_off + h.E + 1 <= hdr.n_total + L.D)) {
+    if (!slice_ok(h, hdr.n_total, L)) {
         if (threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         return;
     }
@@ -180,8 +180,8 @@ __global__ __launch_bounds__(kNT) void local_order_kernel(LocalArgs g) {
         [&](int64_t i, int32_t v) { s.grp[i] = v; }, s.red32);
 
     // 3. admission: largest k with peak(k) <= C
-    const uint2* rank = V.rank + int64_t(d) * L.W;
-    const int4* rec = V.rec + h.rec_off;
+    const uint2* rank = slice_rank(V, h);
+    const int4* rec = slice_rec(V, h, L);
     int lo = 0;
     if (h.base_peak <= C) {
         int hi = n;

@@ -37,7 +37,16 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // {PMX_E, 0, 1, INT32_MAX}.  The rank e = #{events < U} comes from a bitmap
 // over the step axis: word w holds bit j for event time 32w + j, next to the
 // number of events before word w.  W words cover [0, 32 W) with 32 W - 1 > u_max,
-// so a bound clamped to 32 W - 1 ranks above every event.
+// so a bound clamped to 32 W - 1 ranks above every event.  Each decoder's rank
+// words and records form one contiguous slice of 16-byte units (W/2 units of
+// rank words, then the records), so a consumer copies it in one pass.
+//
+// Since PF depends on the arrival only through U, a decoder whose bounds are
+// short enough also gets a dense profile F(u) = max(PF(u), u) for u = 0..u_max
+// (P >= u_max + 1 entries, the tail padded with the same formula).  For any
+// U >= 0, F(min(U, u_max)) and U give PF exactly: F(u) >= u, and beyond u_max
+// no event remains, so PF(U) = max(F(u_max), U).  Placement then needs one
+// table read per pair:  peak(p, U) = max(p + max(F(min(U, u_max)), U), base).
 // ---------------------------------------------------------------------------
 struct SnapHeader {       // at offset 0, 64 bytes
     uint32_t magic;
@@ -47,12 +56,13 @@ struct SnapHeader {       // at offset 0, 64 bytes
     int64_t n_total;      // residents
     int64_t max_tot;      // max over decoders of sum_r (p + g + R)
     int32_t max_records;  // max over decoders of E + 1
-    int32_t pad[7];
+    int32_t P;            // profile entries per decoder (0: no profile)
+    int32_t pad[6];
 };
 static_assert(sizeof(SnapHeader) == 64, "header size");
 
 struct DecHeader {        // one per decoder, 32 bytes
-    int64_t rec_off;      // index of record 0 of this decoder
+    int64_t slice_off;    // first 16-byte unit of this decoder's slice
     int64_t tot;          // sum_r (p + g + R)
     int32_t E;            // number of events
     int32_t base_peak;    // max_t O(t)
@@ -64,38 +74,66 @@ static_assert(sizeof(DecHeader) == 32, "decoder header size");
 // decoder's slice starts on a 16-byte boundary.
 __host__ __device__ inline int32_t rank_words(int32_t u_max) { return (((u_max + 1) / 32 + 1) + 1) & ~1; }
 
+// Profile entries per decoder: u_max + 1 rounded up to a multiple of 4 (whole
+// 16-byte units), or 0 when the table would exceed kProfileMaxEntries.  The
+// rank words cover every padded entry: 32 W >= round_up(u_max + 1, 32) >= P.
+constexpr int32_t kProfileMaxEntries = 16384;
+__host__ __device__ inline int32_t profile_entries(int32_t u_max) {
+    return u_max + 1 <= kProfileMaxEntries ? (u_max + 4) & ~3 : 0;
+}
+
 struct SnapLayout {
-    int32_t D, u_max, W;
+    int32_t D, u_max, W, P;
     int64_t n_total;
-    size_t off_dec, off_rank, off_rec, bytes;
+    size_t off_dec, off_prof, off_slice, bytes;
 };
+
+// Units of the slice region: (n_total + 1) records and W/2 rank units per decoder.
+__host__ __device__ inline int64_t slice_units(const SnapLayout& L) {
+    return L.n_total + int64_t(L.D) * (1 + L.W / 2);
+}
 
 __host__ __device__ inline SnapLayout snap_layout(int32_t D, int64_t n_total, int32_t u_max) {
     SnapLayout L;
     L.D = D;
     L.u_max = u_max;
     L.W = rank_words(u_max);
+    L.P = profile_entries(u_max);
     L.n_total = n_total;
     L.off_dec = align256(sizeof(SnapHeader));
-    L.off_rank = L.off_dec + align256(size_t(D) * sizeof(DecHeader));
-    L.off_rec = L.off_rank + align256(size_t(D) * size_t(L.W) * sizeof(uint2));
-    // 64 spare records at the end: placement copies records in transfers of
-    // 64, so it reads up to 63 records past a decoder's last one
-    L.bytes = L.off_rec + size_t(n_total + D + 64) * sizeof(int4);
+    L.off_prof = L.off_dec + align256(size_t(D) * sizeof(DecHeader));
+    L.off_slice = L.off_prof + align256(size_t(D) * size_t(L.P) * sizeof(int32_t));
+    // decoder d with residents [lo, hi) owns the units [lo + d (1 + W/2), hi + (d + 1)(1 + W/2)):
+    // its W/2 units of rank words and up to hi - lo + 1 records; 64 spare units at the end
+    L.bytes = L.off_slice + size_t(slice_units(L) + 64) * sizeof(int4);
     return L;
 }
 
 struct SnapView {
     SnapHeader* hdr;
     DecHeader* dec;
-    uint2* rank;   // [D][W] {bits, events before the word}
-    int4* rec;     // records {PMX, S, N+1, tau}
+    int4* slices;   // per decoder: W/2 units of rank words {bits, events before the word}, then
+                    // records {PMX, S, N+1, tau}
+    int32_t* prof;  // [D][P] profile F(u)
 };
 
 __host__ __device__ inline SnapView snap_view(void* base, const SnapLayout& L) {
     char* b = static_cast<char*>(base);
     return SnapView{reinterpret_cast<SnapHeader*>(b), reinterpret_cast<DecHeader*>(b + L.off_dec),
-                    reinterpret_cast<uint2*>(b + L.off_rank), reinterpret_cast<int4*>(b + L.off_rec)};
+                    reinterpret_cast<int4*>(b + L.off_slice), reinterpret_cast<int32_t*>(b + L.off_prof)};
+}
+
+// Whether a decoder header describes a slice inside the snapshot (n_total
+// from the snapshot's own header).
+__host__ __device__ inline bool slice_ok(const DecHeader& h, int64_t n_total, const SnapLayout& L) {
+    return h.E >= 0 && h.slice_off >= 0 && h.base_peak >= 0 &&
+           h.slice_off + L.W / 2 + h.E + 1 <= n_total + int64_t(L.D) * (1 + L.W / 2);
+}
+__host__ __device__ inline const uint2* slice_rank(const SnapView& V, const DecHeader& h) {
+    return reinterpret_cast<const uint2*>(V.slices + h.slice_off);
+}
+__host__ __device__ inline const int4* slice_rec(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
+    return V.slices + h.slice_off + L.W / 2;
 }
 
 // ---------------------------------------------------------------------------

@@ -1,24 +1,28 @@
 // Global placement (Sec. 3.3 and Algorithm 1, App. C) on gfx950.
 //
 // Every arrival is evaluated against every decoder's snapshot.  With the
-// snapshot of maps_internal.hpp the projected peak of one pair is
+// snapshot of maps_internal.hpp the projected peak of one pair is either
 //   e    = bits_before(word) + popcount(word & below(U))     (rank of U)
 //   peak = max(p + max(PMX_e, S_e + U (N_e + 1), U), base)
-// i.e. one 8-byte and one 16-byte LDS read and a handful of integer ops.
+// (record path: one 8-byte and one 12-byte LDS read), or, when the snapshot
+// carries dense profiles,
+//   peak = max(p + max(F[min(U, u_max)], U), base)
+// (profile path: one 4-byte LDS read).
 //
 // Work decomposition: the decoders are split into G groups and the arrivals
 // into tiles.  Workgroup b handles group b % G -- so with G dividing 8 all
 // workgroups of a group run on the same XCDs and share their L2 -- and tile
 // b / G.  Each thread keeps its arrivals in registers; the workgroup walks its
-// decoders in order, stages each decoder's rank words and records in LDS, and
-// evaluates all its arrivals against it, writing the decoder-major pair-peak
-// row segment with coalesced stores and keeping the running best choice per
-// arrival.  Ties keep the earlier (lower) decoder.  With G > 1 each group
-// writes its best (key, decoder, peak) per arrival and place_reduce picks the
-// best group in group order; with G = 1 the outputs are written directly.
+// decoders in order, stages their snapshot data in LDS, and evaluates all its
+// arrivals against each, writing the decoder-major pair-peak row segment with
+// coalesced stores and keeping the running best choice per arrival.  Ties
+// keep the earlier (lower) decoder.  With G > 1 each group writes its best
+// (key, decoder, peak) per arrival and place_reduce picks the best group in
+// group order; with G = 1 the outputs are written directly.
 //
-// Selection key (smaller is better): policy MQ uses Q_d for a feasible pair
-// and 2^31 | (peak - C_d) otherwise; policy MC uses (peak - C_d) + 2^31.
+// Selection (smaller key is better, see select_key): policy MQ prefers any
+// feasible decoder, by queue length, then the smallest overflow; policy MC
+// the largest slack.
 #include "maps_internal.hpp"
 
 namespace maps {
@@ -42,130 +46,164 @@ struct PlaceArgs {
     int32_t* chosen_over;
     uint8_t* flags;
     int32_t* pair;
-    uint32_t* pkey;   // [G][A] partial best keys
-    int32_t* pdec;    // [G][A] partial best decoders
-    int32_t* ppeak;   // [G][A] partial best peaks
+    int32_t* pkey;     // [G][A] partial best keys
+    int32_t* pdec;     // [G][A] partial best decoders
+    int32_t* ppeak;    // [G][A] partial best peaks
     int32_t G;
-    int32_t Dg;       // decoders per group
-    int64_t rec_cap;  // records that fit LDS next to the rank words (0: rank words do not fit)
+    int32_t Dg;        // decoders per group
+    int32_t buf_units; // record path: 16-byte units per LDS buffer (0: slices stay in HBM)
+    int32_t nb;        // profile path: profiles per LDS batch
     uint32_t* dev_err;
 };
 
+// Read-only values every lane needs alike (capacities, queue lengths, snapshot
+// headers), loaded through the scalar cache into scalar registers: vector
+// loads would make their first use wait for every store issued before them.
+template <typename T>
+__device__ __forceinline__ T load_uniform(const T* p) {
+    return *(const __attribute__((address_space(4))) T*)(p);
+}
+__device__ __forceinline__ DecHeader load_dec(const DecHeader* p) {
+    DecHeader h;
+    h.slice_off = load_uniform(&p->slice_off);
+    h.tot = load_uniform(&p->tot);
+    h.E = load_uniform(&p->E);
+    h.base_peak = load_uniform(&p->base_peak);
+    h.pad[0] = h.pad[1] = 0;
+    return h;
+}
+
 __device__ inline bool snapshot_ok(const SnapHeader* h, const SnapLayout& L) {
-    return h->magic == kSnapMagic && h->D == L.D && h->u_max == L.u_max && h->W == L.W;
+    return load_uniform(&h->magic) == kSnapMagic && load_uniform(&h->D) == L.D &&
+           load_uniform(&h->u_max) == L.u_max && load_uniform(&h->W) == L.W && load_uniform(&h->P) == L.P;
 }
 
 __device__ inline int32_t imax(int32_t a, int32_t b) { return a > b ? a : b; }
 
-// Per-thread state of kAPT arrivals: prompt, bound, bound clamped for the
-// rank lookup, index of its rank word and the mask of the bits below it, and
-// the best (key, decoder) seen so far.
-template <int kAPT>
-struct Arrivals {
-    int32_t p[kAPT], U[kAPT], Ucl[kAPT];
-    uint32_t wi[kAPT], mask[kAPT];
-    uint32_t best_key[kAPT];
-    int32_t best_d[kAPT];
-};
+// A 16-byte unit as a native vector (kept in registers when staged).
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
-// Projected peak of one arrival on one decoder, reading the snapshot in HBM.
-__device__ __forceinline__ int32_t peak_from_hbm(const SnapView& V, int32_t W, int32_t d, int32_t p, int32_t U,
-                                                 int32_t Ucl, uint32_t wi, uint32_t mask) {
-    const DecHeader h = V.dec[d];
-    const uint2 w = V.rank[int64_t(d) * W + wi];
-    uint32_t e = w.y + __popc(w.x & mask);
-    e = e < uint32_t(h.E) ? e : uint32_t(h.E);
-    const int4 r = V.rec[h.rec_off + e];
-    const int32_t lin = r.y + int32_t(__umul24(uint32_t(Ucl), uint32_t(r.z)));
-    const int32_t pf = max(max(r.x, lin), U);
-    return p + pf > h.base_peak ? p + pf : h.base_peak;
+// Selection key of a pair as a signed value (smaller is better), with the
+// overflow v = peak - C_d (|v| < 2^31):
+//   MQ: v when infeasible (v > 0), else Q_d - 2^31 (every feasible pair ranks
+//       first, by queue length);   MC: v (largest slack first).
+// Qm is Q_d - 2^31.
+template <int kPolicy>
+__device__ __forceinline__ int32_t select_key(int32_t peak, int32_t C, int32_t Qm) {
+    const int32_t v = peak - C;
+    if constexpr (kPolicy == MAPS_POLICY_MQ) return v > 0 ? v : Qm;
+    else return v;
 }
 
-// Evaluate every arrival of the thread against one decoder whose rank words
-// and records are at rank/rec (LDS or HBM), write the pair-peak row and keep
-// the best choice.  `kFull`: every arrival of the tile exists.
-// Selection key (smaller is better), with u = peak - C + 2^31:
-//   MQ: u when infeasible (u > 2^31), else Q_d;   MC: u.
+// Raw buffer resources (gfx9 descriptor, 32-bit data format): accesses whose
+// VGPR offset (plus immediate) reaches past `bytes` read 0 and write nothing.
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kNonTemporal = 2;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kBufferWord3);
+}
+
+// Pair-peak store of arrival k of the thread into a tile row.  In a full tile
+// the arrival's place in the row is a uniform offset; in a partial tile the
+// whole offset goes through the range check, which drops the missing arrivals.
+template <bool kFull>
+__device__ __forceinline__ void store_pair(__amdgpu_buffer_rsrc_t row, int k, int32_t v) {
+    if constexpr (kFull)
+        __builtin_amdgcn_raw_buffer_store_b32(v, row, int(threadIdx.x) * 4, k * kNT * 4, kNonTemporal);
+    else
+        __builtin_amdgcn_raw_buffer_store_b32(v, row, int(threadIdx.x) * 4 + k * kNT * 4, 0, kNonTemporal);
+}
+
+// ---------------------------------------------------------------------------
+// Record path.
+//
+// Each thread holds kAPT arrivals: prompt, bound, -1/0 for a missing bound,
+// the byte offset of the bound's rank word in a slice and the mask of the
+// bits below it (bound clamped to [0, 32 W - 1]), and the running best.
+// The workgroup walks its decoders with two LDS buffers: while decoder d is
+// evaluated from one buffer, the slice of decoder d+1 is already on its way
+// into registers, and it is written to the other buffer before the single
+// barrier of the next step.  A slice too large for a buffer is read from HBM.
+//
+// For a bound at or above 32 W the rank lands on record E (N + 1 = 1, S = 0),
+// where S + U (N + 1) <= U; so the product may use U itself (its low 24 bits,
+// all of it whenever a record before E is hit, since events are <= u_max).
+// ---------------------------------------------------------------------------
+constexpr int kStage = 10;  // 16-byte units per thread staged in registers: a whole LDS buffer
+
+template <int kAPT>
+struct RecArrivals {
+    int32_t p[kAPT], U[kAPT], neg[kAPT];
+    uint32_t roff[kAPT], mask[kAPT];
+    int32_t best_key[kAPT], best_d[kAPT];
+};
+
+__device__ __forceinline__ int32_t record_peak(const int4& r, int32_t p, int32_t U, int32_t base) {
+    const int32_t lin = r.y + int32_t(__umul24(uint32_t(U), uint32_t(r.z)));
+    const int32_t pf = max(max(r.x, lin), U);
+    return imax(p + pf, base);
+}
+
+// Evaluate the thread's arrivals against one decoder whose rank words start
+// at `rank` and records at `rec` (both in LDS, or both in HBM).
 template <int kAPT, bool kFull, bool kPairs, int kPolicy>
-__device__ __forceinline__ void eval_decoder(Arrivals<kAPT>& s, const uint2* rank, const int4* rec, int32_t E,
-                                             int32_t base, int32_t C, int32_t Q, int32_t d, bool first,
-                                             int32_t* prow, int64_t a0, int64_t A) {
+__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int4* rec, uint32_t E,
+                                             int32_t base, int32_t C, int32_t Q, int32_t d,
+                                             __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
-    const uint32_t kC = 0x80000000u - uint32_t(C);
+    const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
 #pragma unroll
     for (int c = 0; c < kAPT; c += kChunk) {
         uint2 w[kChunk];
 #pragma unroll
-        for (int i = 0; i < kChunk; ++i) w[i] = rank[s.wi[c + i]];
+        for (int i = 0; i < kChunk; ++i) w[i] = *reinterpret_cast<const uint2*>(rank + s.roff[c + i]);
         int4 r[kChunk];
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             uint32_t e = w[i].y + __popc(w[i].x & s.mask[c + i]);
-            e = e < uint32_t(E) ? e : uint32_t(E);   // stays inside the decoder's records
+            e = e < E ? e : E;   // stays inside the decoder's records
             r[i] = rec[e];
         }
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             const int k = c + i;
-            // PF(U) = max(PMX_e, S_e + U (N_e + 1)), U itself when beyond the last event
-            const int32_t lin = r[i].y + int32_t(__umul24(uint32_t(s.Ucl[k]), uint32_t(r[i].z)));
-            const int32_t pf = max(max(r[i].x, lin), s.U[k]);
-            const int32_t peak = imax(s.p[k] + pf, base);
-            if constexpr (kPairs) {
-                // uniform row base per k, lane offset in a VGPR: no per-arrival 64-bit address
-                int32_t* row = prow + a0 + int64_t(k) * kNT;
-                if (kFull || a0 + int64_t(k) * kNT + threadIdx.x < A)
-                    __builtin_nontemporal_store(s.U[k] < 0 ? -1 : peak, row + threadIdx.x);
-            }
-            const uint32_t u = uint32_t(peak) + kC;
-            uint32_t key;
-            if constexpr (kPolicy == MAPS_POLICY_MQ) key = u > 0x80000000u ? u : uint32_t(Q);
-            else key = u;
-            const bool take = first || key < s.best_key[k];
+            const int32_t peak = record_peak(r[i], s.p[k], s.U[k], base);
+            if constexpr (kPairs) store_pair<kFull>(row, k, peak | s.neg[k]);
+            const int32_t key = select_key<kPolicy>(peak, C, Qm);
+            const bool take = key < s.best_key[k];
             s.best_key[k] = take ? key : s.best_key[k];
             s.best_d[k] = take ? d : s.best_d[k];
         }
     }
 }
 
-// A 16-byte unit as a native vector (kept in registers when staged).
-typedef int32_t v4i __attribute__((ext_vector_type(4)));
-
-// 16-byte unit u of decoder d's snapshot slice: its rank words, then its records.
-__device__ __forceinline__ const int4* snapshot_unit(const SnapView& V, int32_t W, int32_t d, const DecHeader& h,
-                                                     int64_t u) {
-    const int64_t half_w = W / 2;
-    return u < half_w ? reinterpret_cast<const int4*>(V.rank + int64_t(d) * W) + u : V.rec + h.rec_off + (u - half_w);
-}
-
-// Load this thread's first kPF units of decoder d into registers (units past
-// the end re-read the last one, so every lane issues the same loads).
-template <int kPF>
-__device__ __forceinline__ void stage_units(v4i (&stage)[kPF], const SnapView& V, int32_t W, int32_t d,
-                                            const DecHeader& h) {
-    const int64_t last = int64_t(W / 2) + h.E;
+// Load this thread's first kStage units of a slice of `units` units into
+// registers (units past the end read as 0).
+__device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* src, int32_t units) {
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, uint32_t(units) * 16u);
 #pragma unroll
-    for (int j = 0; j < kPF; ++j) {
-        const int64_t u = threadIdx.x + int64_t(j) * kNT;
-        stage[j] = *reinterpret_cast<const v4i*>(snapshot_unit(V, W, d, h, u < last ? u : last));
-    }
+    for (int j = 0; j < kStage; ++j)
+        stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                               rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
 }
 
-template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy>
-__device__ __forceinline__ void place_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
-                                           int64_t a0) {
-    constexpr int kPF = 7;   // 16-byte units per thread staged in registers ahead of use
+// One arrival tile against the decoders of group grp.  kMixed: some slices
+// may exceed an LDS buffer and are then read from HBM; otherwise every slice
+// fits (a header claiming more is reported and skipped).
+template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy, bool kMixed>
+__device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
+                                             int64_t a0) {
     const SnapLayout& L = g.L;
-    const int32_t W = L.W;
-    const int32_t half_w = W / 2;              // rank words in 16-byte units
+    const int32_t half_w = L.W / 2;                // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
     const int32_t d_end = d_begin + g.Dg < L.D ? d_begin + g.Dg : L.D;
-    const int64_t max_tot = V.hdr->max_tot;
-    const int64_t n_total = V.hdr->n_total;
-    const int32_t ucl_max = 32 * W - 1;        // ranks above every event
-    const int64_t lds_units = g.rec_cap > 0 ? half_w + g.rec_cap : 0;
+    const int64_t max_tot = load_uniform(&V.hdr->max_tot);
+    const int64_t n_total = load_uniform(&V.hdr->n_total);
+    const int32_t ucl_max = 32 * L.W - 1;          // ranks above every event
+    const int32_t buf_units = g.buf_units;
+    const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
-    Arrivals<kAPT> s;
+    RecArrivals<kAPT> s;
     bool neg = false, range = false;
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
@@ -176,54 +214,55 @@ __device__ __forceinline__ void place_tile(const PlaceArgs& g, const SnapView& V
         if (U >= 0 && int64_t(p) + U + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
         s.p[k] = p < 0 ? 0 : p;
         s.U[k] = U;
+        s.neg[k] = U < 0 ? -1 : 0;
         const int32_t uc = U < 0 ? 0 : (U < ucl_max ? U : ucl_max);
-        s.Ucl[k] = uc;
-        s.wi[k] = uint32_t(uc >> 5);
+        s.roff[k] = uint32_t(uc >> 5) * 8u;
         s.mask[k] = (1u << (uc & 31)) - 1u;
-        s.best_key[k] = 0xFFFFFFFFu;
+        s.best_key[k] = INT32_MAX;
         s.best_d[k] = d_begin;
     }
     if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
     if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
 
-    auto fits = [&](const DecHeader& h) { return h.E >= 0 && int64_t(half_w) + h.E + 1 <= lds_units; };
-    auto ok = [&](const DecHeader& h) {
-        return h.E >= 0 && h.rec_off >= 0 && h.rec_off + h.E + 1 <= n_total + L.D && h.base_peak >= 0;
-    };
+    auto fits = [&](const DecHeader& h) { return half_w + h.E + 1 <= buf_units; };
 
-    v4i stage[kPF];
-    DecHeader h = V.dec[d_begin < d_end ? d_begin : 0];
-    if (d_begin < d_end && ok(h) && fits(h)) stage_units<kPF>(stage, V, W, d_begin, h);
+    v4i stage[kStage];
+    DecHeader h = load_dec(V.dec + (d_begin < d_end ? d_begin : 0));
+    bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
+    if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);
     for (int32_t d = d_begin; d < d_end; ++d) {
-        const int32_t C = g.cap[d], Q = g.qlen[d];
-        if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-        const bool valid = ok(h);
-        const bool in_lds = valid && fits(h);
-        if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-        if (in_lds) {
-            __syncthreads();   // every wave finished reading the previous decoder
-            const int64_t units = int64_t(half_w) + h.E + 1;
-#pragma unroll
-            for (int j = 0; j < kPF; ++j) {   // lanes past the end write the spare unit
-                const int64_t u = threadIdx.x + int64_t(j) * kNT;
-                reinterpret_cast<v4i*>(lds)[u < units ? u : lds_units] = stage[j];
-            }
-            for (int64_t u = threadIdx.x + int64_t(kPF) * kNT; u < units; u += kNT) lds[u] = *snapshot_unit(V, W, d, h, u);
-            __syncthreads();
-        }
         const DecHeader cur = h;
-        if (d + 1 < d_end) {
-            h = V.dec[d + 1];
-            if (ok(h) && fits(h)) stage_units<kPF>(stage, V, W, d + 1, h);   // overlaps the evaluation below
+        const bool valid = h_ok;
+        const bool in_lds = valid && (!kMixed || fits(cur));
+        const int32_t buf = (d - d_begin) & 1;
+        const int32_t C = load_uniform(g.cap + d), Q = load_uniform(g.qlen + d);
+        if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+        if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+        int4* slice = lds + buf * buf_units;
+        if (in_lds) {
+            // Buffer `buf` was last read for decoder d-2, which every wave
+            // finished before passing the barrier of decoder d-1.  The staged
+            // units cover the whole buffer; those past the slice's end are 0.
+#pragma unroll
+            for (int j = 0; j < kStage; ++j)
+                reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
         }
+        if (d + 1 < d_end) {
+            h = load_dec(V.dec + d + 1);
+            h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
+            if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);   // overlaps the evaluation
+        }
+        __syncthreads();
         if (!valid) continue;
-        int32_t* prow = kPairs ? g.pair + int64_t(d) * g.A : nullptr;
-        if (in_lds)
-            eval_decoder<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const uint2*>(lds), lds + half_w, cur.E,
-                                                        cur.base_peak, C, Q, d, d == d_begin, prow, a0, g.A);
-        else
-            eval_decoder<kAPT, kFull, kPairs, kPolicy>(s, V.rank + int64_t(d) * W, V.rec + cur.rec_off, cur.E,
-                                                        cur.base_peak, C, Q, d, d == d_begin, prow, a0, g.A);
+        const __amdgpu_buffer_rsrc_t row =
+            buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
+        if (!kMixed || in_lds)
+            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice), slice + half_w,
+                                                       uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+        else if constexpr (kMixed)
+            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
+                                                       slice_rec(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
+                                                       d, row);
     }
 
 #pragma unroll
@@ -231,8 +270,17 @@ __device__ __forceinline__ void place_tile(const PlaceArgs& g, const SnapView& V
         const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
         if (!kFull && a >= g.A) continue;
         // the chosen pair's peak, evaluated once more from the snapshot in HBM
-        const bool has = d_begin < d_end && s.U[k] >= 0 && ok(V.dec[s.best_d[k]]);
-        const int32_t peak = has ? peak_from_hbm(V, W, s.best_d[k], s.p[k], s.U[k], s.Ucl[k], s.wi[k], s.mask[k]) : 0;
+        int32_t peak = 0;
+        if (d_begin < d_end && s.U[k] >= 0) {
+            const DecHeader hb = V.dec[s.best_d[k]];
+            if (slice_ok(hb, n_total, L)) {
+                const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(slice_rank(V, hb)) +
+                                                                s.roff[k]);
+                uint32_t e = w.y + __popc(w.x & s.mask[k]);
+                e = e < uint32_t(hb.E) ? e : uint32_t(hb.E);
+                peak = record_peak(slice_rec(V, hb, L)[e], s.p[k], s.U[k], hb.base_peak);
+            }
+        }
         if constexpr (kFinal) {
             if (s.U[k] < 0) {
                 g.choice[a] = int32_t((g.rr_offset + a) % L.D);
@@ -248,15 +296,18 @@ __device__ __forceinline__ void place_tile(const PlaceArgs& g, const SnapView& V
             }
         } else {
             const int64_t o = int64_t(grp) * g.A + a;
-            g.pkey[o] = d_begin < d_end ? s.best_key[k] : 0xFFFFFFFFu;
-            g.pdec[o] = s.best_d[k] < L.D ? s.best_d[k] : 0;
+            g.pkey[o] = s.best_key[k];
+            g.pdec[o] = s.best_d[k];
             g.ppeak[o] = peak;
         }
     }
 }
 
+// When every slice fits an LDS buffer (the snapshot's largest record count
+// says so) the tile runs in one pass; otherwise it is split into sub-tiles of
+// at most 4 arrivals per thread that read the large slices from HBM.
 template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
-__global__ __launch_bounds__(kNT) void place_pairs(PlaceArgs g) {
+__global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     extern __shared__ int4 lds[];
     const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
     if (!snapshot_ok(V.hdr, g.L)) {
@@ -265,10 +316,19 @@ __global__ __launch_bounds__(kNT) void place_pairs(PlaceArgs g) {
     }
     const int32_t grp = blockIdx.x % g.G;
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
-    if (a0 + kNT * kAPT <= g.A)
-        place_tile<kAPT, true, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
-    else
-        place_tile<kAPT, false, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+    const int32_t max_records = load_uniform(&V.hdr->max_records);
+    if (g.L.W / 2 + max_records <= g.buf_units) {
+        if (a0 + kNT * kAPT <= g.A)
+            records_tile<kAPT, true, kPairs, kFinal, kPolicy, false>(g, V, lds, grp, a0);
+        else
+            records_tile<kAPT, false, kPairs, kFinal, kPolicy, false>(g, V, lds, grp, a0);
+    } else {
+        constexpr int kSub = kAPT < 4 ? kAPT : 4;
+        for (int t = 0; t < kAPT / kSub; ++t) {
+            const int64_t b0 = a0 + int64_t(t) * kNT * kSub;
+            if (b0 < g.A) records_tile<kSub, false, kPairs, kFinal, kPolicy, true>(g, V, lds, grp, b0);
+        }
+    }
 }
 
 __global__ __launch_bounds__(256) void place_reduce(PlaceArgs g) {
@@ -284,11 +344,11 @@ __global__ __launch_bounds__(256) void place_reduce(PlaceArgs g) {
             g.flags[a] = 2;
             continue;
         }
-        uint32_t key = g.pkey[a];
+        int32_t key = g.pkey[a];
         int32_t d = g.pdec[a], peak = g.ppeak[a];
         for (int32_t gi = 1; gi < g.G; ++gi) {
             const int64_t o = int64_t(gi) * g.A + a;
-            const uint32_t k2 = g.pkey[o];
+            const int32_t k2 = g.pkey[o];
             if (k2 < key) { key = k2; d = g.pdec[o]; peak = g.ppeak[o]; }
         }
         d = d < 0 || d >= L.D ? 0 : d;
@@ -300,34 +360,196 @@ __global__ __launch_bounds__(256) void place_reduce(PlaceArgs g) {
     }
 }
 
-template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
-void launch_one(dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
-    auto fn = place_pairs<kAPT, kPairs, kFinal, kPolicy>;
-    allow_dynamic_lds(fn, kLdsBytes);
-    hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
-}
-
-template <int kAPT, bool kPairs, bool kFinal>
-void launch_policy(int32_t policy, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
-    if (policy == MAPS_POLICY_MQ) launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MQ>(grid, lds, s, a);
-    else launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MC>(grid, lds, s, a);
-}
+// ---------------------------------------------------------------------------
+// Placement from the dense profiles (snapshots with P > 0).
+//
+// The profile F of a decoder answers a pair with one 4-byte LDS read:
+//   peak = max(p + max(F[min(U, u_max)], U), base).
+// Workgroup b takes decoder group b % G and arrival tile b / G (kAPT arrivals
+// per thread, kept in registers with their running best).  The group's
+// profiles go through LDS nb decoders at a time; while one batch is evaluated
+// the next one is already on its way into registers (kProfPF units of 16
+// bytes per thread, the remainder loaded after the barrier).
+// ---------------------------------------------------------------------------
+constexpr int kProfPF = 16;
 
 template <int kAPT>
-void launch_apt(bool pairs, bool final_, int32_t policy, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
-    if (pairs) {
-        if (final_) launch_policy<kAPT, true, true>(policy, grid, lds, s, a);
-        else launch_policy<kAPT, true, false>(policy, grid, lds, s, a);
-    } else {
-        if (final_) launch_policy<kAPT, false, true>(policy, grid, lds, s, a);
-        else launch_policy<kAPT, false, false>(policy, grid, lds, s, a);
+struct ProfArrivals {
+    int32_t p[kAPT], U[kAPT], neg[kAPT];
+    uint32_t off[kAPT];   // byte offset of F[min(U, u_max)] in a profile
+    int32_t best_key[kAPT], best_d[kAPT];
+};
+
+// Load this thread's kProfPF units of the batch starting at decoder db, which
+// cover the whole batch (units past its end read as 0).
+__device__ __forceinline__ void stage_profile(v4i (&stage)[kProfPF], const int32_t* prof, int32_t P, int32_t db,
+                                              int32_t units) {
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(prof + int64_t(db) * P, uint32_t(units) * 16u);
+#pragma unroll
+    for (int j = 0; j < kProfPF; ++j)
+        stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                               rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
+}
+
+template <int kAPT, bool kFull, bool kPairs, int kPolicy>
+__device__ __forceinline__ void prof_decoder(ProfArrivals<kAPT>& s, const char* table, int32_t base, int32_t C,
+                                             int32_t Q, int32_t d, __amdgpu_buffer_rsrc_t row) {
+    const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int32_t f = *reinterpret_cast<const int32_t*>(table + s.off[k]);
+        const int32_t peak = imax(s.p[k] + (f > s.U[k] ? f : s.U[k]), base);
+        if constexpr (kPairs) store_pair<kFull>(row, k, peak | s.neg[k]);
+        const int32_t key = select_key<kPolicy>(peak, C, Qm);
+        const bool take = key < s.best_key[k];
+        s.best_key[k] = take ? key : s.best_key[k];
+        s.best_d[k] = take ? d : s.best_d[k];
     }
 }
 
-// Arrivals per thread and decoder groups: the largest arrival tile that still
-// gives at least one workgroup per compute unit.
-void plan(int32_t D, int64_t A, int cus, int* apt, int* groups) {
-    for (int t : {8, 4, 2, 1}) {
+template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy>
+__device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
+                                          int64_t a0) {
+    const SnapLayout& L = g.L;
+    const int32_t P = L.P;
+    const int32_t d_begin = grp * g.Dg;
+    const int32_t d_end = d_begin + g.Dg < L.D ? d_begin + g.Dg : L.D;
+    const int64_t max_tot = load_uniform(&V.hdr->max_tot);
+    const int32_t nb = g.nb;   // nb * P / 4 <= kProfPF * kNT
+    const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
+
+    ProfArrivals<kAPT> s;
+    bool neg = false, range = false;
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
+        int32_t p = 0, U = -1;
+        if (kFull || a < g.A) { p = g.ap[a]; U = g.aU[a]; }
+        neg |= p < 0;
+        if (U >= 0 && int64_t(p) + U + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
+        s.p[k] = p < 0 ? 0 : p;
+        s.U[k] = U;
+        s.neg[k] = U < 0 ? -1 : 0;
+        s.off[k] = 4u * uint32_t(U < 0 ? 0 : (U < L.u_max ? U : L.u_max));
+        s.best_key[k] = INT32_MAX;
+        s.best_d[k] = d_begin;
+    }
+    if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+    if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
+
+    v4i stage[kProfPF];
+    if (d_begin < d_end) {
+        const int32_t n0 = d_end - d_begin < nb ? d_end - d_begin : nb;
+        stage_profile(stage, V.prof, P, d_begin, n0 * (P / 4));
+    }
+    for (int32_t db = d_begin; db < d_end; db += nb) {
+        const int32_t n = d_end - db < nb ? d_end - db : nb;
+        __syncthreads();   // every wave finished reading the previous batch
+#pragma unroll
+        for (int j = 0; j < kProfPF; ++j) reinterpret_cast<v4i*>(lds)[int(threadIdx.x) + j * kNT] = stage[j];
+        __syncthreads();
+        if (db + nb < d_end) {
+            const int32_t n1 = d_end - (db + nb) < nb ? d_end - (db + nb) : nb;
+            stage_profile(stage, V.prof, P, db + nb, n1 * (P / 4));   // overlaps the evaluation below
+        }
+        for (int32_t i = 0; i < n; ++i) {
+            const int32_t d = db + i;
+            const int32_t base = load_uniform(&V.dec[d].base_peak);
+            const int32_t C = load_uniform(g.cap + d), Q = load_uniform(g.qlen + d);
+            if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+            if (threadIdx.x == 0 && base < 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+            const char* table = reinterpret_cast<const char*>(lds) + size_t(i) * P * 4;
+            const __amdgpu_buffer_rsrc_t row = buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr,
+                                                           kPairs ? uint32_t(tile_n) * 4u : 0u);
+            prof_decoder<kAPT, kFull, kPairs, kPolicy>(s, table, base, C, Q, d, row);
+        }
+    }
+
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
+        if (!kFull && a >= g.A) continue;
+        // the chosen pair's peak, read once more from the profile in HBM
+        int32_t peak = 0;
+        if (d_begin < d_end && s.U[k] >= 0) {
+            const int32_t bd = s.best_d[k];
+            const int32_t f = V.prof[int64_t(bd) * P + (s.off[k] >> 2)];
+            peak = imax(s.p[k] + (f > s.U[k] ? f : s.U[k]), V.dec[bd].base_peak);
+        }
+        if constexpr (kFinal) {
+            if (s.U[k] < 0) {
+                g.choice[a] = int32_t((g.rr_offset + a) % L.D);
+                g.chosen_peak[a] = -1;
+                g.chosen_over[a] = 0;
+                g.flags[a] = 2;
+            } else {
+                const int32_t C = g.cap[s.best_d[k]];
+                g.choice[a] = s.best_d[k];
+                g.chosen_peak[a] = peak;
+                g.chosen_over[a] = peak > C ? peak - C : 0;
+                g.flags[a] = peak <= C ? 1 : 0;
+            }
+        } else {
+            const int64_t o = int64_t(grp) * g.A + a;
+            g.pkey[o] = s.best_key[k];
+            g.pdec[o] = s.best_d[k];
+            g.ppeak[o] = peak;
+        }
+    }
+}
+
+template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+__global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
+    extern __shared__ int4 lds[];
+    const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
+    if (!snapshot_ok(V.hdr, g.L)) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    const int32_t grp = blockIdx.x % g.G;
+    const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
+    if (a0 + kNT * kAPT <= g.A)
+        prof_tile<kAPT, true, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+    else
+        prof_tile<kAPT, false, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+}
+
+template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+void launch_one(bool prof, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
+    if (prof) {
+        auto fn = place_prof<kAPT, kPairs, kFinal, kPolicy>;
+        allow_dynamic_lds(fn, kLdsBytes);
+        hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
+    } else {
+        auto fn = place_records<kAPT, kPairs, kFinal, kPolicy>;
+        allow_dynamic_lds(fn, kLdsBytes);
+        hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
+    }
+}
+
+template <int kAPT, bool kPairs, bool kFinal>
+void launch_policy(bool prof, int32_t policy, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
+    if (policy == MAPS_POLICY_MQ) launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MQ>(prof, grid, lds, s, a);
+    else launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MC>(prof, grid, lds, s, a);
+}
+
+template <int kAPT>
+void launch_apt(bool prof, bool pairs, bool final_, int32_t policy, dim3 grid, size_t lds, hipStream_t s,
+                const PlaceArgs& a) {
+    if (pairs) {
+        if (final_) launch_policy<kAPT, true, true>(prof, policy, grid, lds, s, a);
+        else launch_policy<kAPT, true, false>(prof, policy, grid, lds, s, a);
+    } else {
+        if (final_) launch_policy<kAPT, false, true>(prof, policy, grid, lds, s, a);
+        else launch_policy<kAPT, false, false>(prof, policy, grid, lds, s, a);
+    }
+}
+
+// Arrivals per thread and decoder groups: the largest arrival tile (up to
+// max_apt per thread) that still gives at least one workgroup per compute unit.
+void plan(int32_t D, int64_t A, int cus, int max_apt, int* apt, int* groups) {
+    for (int t : {16, 8, 4, 2, 1}) {
+        if (t > max_apt) continue;
         const int64_t tiles = (A + int64_t(kNT) * t - 1) / (int64_t(kNT) * t);
         int G = 1;
         while (G < kMaxGroups && G < D && tiles * G < cus) G *= 2;
@@ -339,7 +561,7 @@ void plan(int32_t D, int64_t A, int cus, int* apt, int* groups) {
 }
 
 struct PlaceWorkspace {
-    uint32_t* key;
+    int32_t* key;
     int32_t* dec;
     int32_t* peak;
     size_t bytes;
@@ -350,7 +572,7 @@ PlaceWorkspace place_carve(void* base, int64_t A) {
     char* p = static_cast<char*>(base);
     size_t off = 0;
     auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
-    w.key = reinterpret_cast<uint32_t*>(take(size_t(kMaxGroups) * A * 4));
+    w.key = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
     w.dec = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
     w.peak = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
     w.bytes = off;
@@ -388,16 +610,18 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
         (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags)))
         return MAPS_E_NULL;
     if (A == 0) return MAPS_OK;
+    const SnapLayout L = snap_layout(D, 0, u_max);   // region offsets do not depend on the resident count
+    const bool prof = L.P > 0;
     int apt = 8, G = 1;
-    plan(D, A, compute_units(), &apt, &G);
+    plan(D, A, compute_units(), prof ? 8 : 16, &apt, &G);   // the profile path stages 64 VGPRs
     PlaceWorkspace w{};
     if (G > 1) {
         if (!workspace) return MAPS_E_NULL;
         w = place_carve(workspace, A);
         if (workspace_bytes < w.bytes) return MAPS_E_WORKSPACE;
     }
-    PlaceArgs a;
-    a.L = snap_layout(D, 0, u_max);
+    PlaceArgs a{};
+    a.L = L;
     a.snap = snapshot;
     a.cap = capacity;
     a.qlen = queue_len;
@@ -416,21 +640,28 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
     a.G = G;
     a.Dg = (D + G - 1) / G;
     a.dev_err = dev_err;
-    // The record region starts after the rank words, whose offset does not
-    // depend on the number of residents; records are addressed through the
-    // decoder headers and bound-checked against the snapshot's own count.
-    const size_t rank_bytes = size_t(a.L.W) * 8;
-    // LDS: rank words, records, and one spare 16-byte unit
-    a.rec_cap = rank_bytes + 64 * 16 <= kLdsBytes ? int64_t((kLdsBytes - rank_bytes) / 16) - 1 : 0;
-    const size_t lds = a.rec_cap > 0 ? kLdsBytes : 0;
+    // Slices are addressed through the decoder headers and bound-checked
+    // against the snapshot's own resident count.
+    // Record path LDS: two buffers of buf_units 16-byte units, each at least
+    // as large as the staged part of a slice.
+    const int32_t buf_units = int32_t(kLdsBytes / 16 / 2);
+    a.buf_units = L.W / 2 + 64 <= buf_units && kStage * kNT <= buf_units ? buf_units : 0;
+    size_t lds = size_t(2 * a.buf_units) * 16;
+    if (prof) {
+        // LDS: the staged units of one batch of nb profiles
+        const int64_t nb = int64_t(kProfPF) * kNT * 4 / L.P;
+        a.nb = int32_t(nb < 8 ? nb : 8);
+        lds = size_t(kProfPF) * kNT * 16;
+    }
     const int64_t tiles = (A + int64_t(kNT) * apt - 1) / (int64_t(kNT) * apt);
     const dim3 grid(unsigned(tiles * G));
     const bool pairs = pair_peak != nullptr, final_ = G == 1;
     switch (apt) {
-        case 8: launch_apt<8>(pairs, final_, policy, grid, lds, stream, a); break;
-        case 4: launch_apt<4>(pairs, final_, policy, grid, lds, stream, a); break;
-        case 2: launch_apt<2>(pairs, final_, policy, grid, lds, stream, a); break;
-        default: launch_apt<1>(pairs, final_, policy, grid, lds, stream, a); break;
+        case 16: launch_apt<16>(prof, pairs, final_, policy, grid, lds, stream, a); break;
+        case 8: launch_apt<8>(prof, pairs, final_, policy, grid, lds, stream, a); break;
+        case 4: launch_apt<4>(prof, pairs, final_, policy, grid, lds, stream, a); break;
+        case 2: launch_apt<2>(prof, pairs, final_, policy, grid, lds, stream, a); break;
+        default: launch_apt<1>(prof, pairs, final_, policy, grid, lds, stream, a); break;
     }
     MAPS_CHECK_LAUNCH();
     if (!final_) {

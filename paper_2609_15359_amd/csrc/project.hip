@@ -9,7 +9,8 @@
 //   3. residents add 1 and p + g to their event's counters (integer atomics,
 //      so the sums are deterministic);
 //   4. reverse scans give N_e and S_e, a forward max-scan the prefix maxima
-//      PMX_e, a max-reduction the base peak.
+//      PMX_e, a max-reduction the base peak;
+//   5. when u_max is small enough, the dense profile F(u) for every u.
 // Small decoders keep every array in LDS; decoders that do not fit run the
 // same steps on their own slice of the snapshot in HBM.
 #include "maps_internal.hpp"
@@ -67,7 +68,7 @@ struct Scratch {
 template <bool kInLds, typename Arr>
 __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int32_t* __restrict__ p,
                             const int32_t* __restrict__ g, const int32_t* __restrict__ U, int32_t u_max, int32_t W,
-                            SnapView V, int64_t rec_off, int32_t* __restrict__ base_peak, uint32_t* dev_err,
+                            int32_t P, SnapView V, int64_t slice_off, int32_t* __restrict__ base_peak, uint32_t* dev_err,
                             Scratch& sc) {
     const int tid = threadIdx.x;
     for (int64_t w = tid; w < W; w += kNT) a.B(w) = 0u;
@@ -141,9 +142,26 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     }
     const int32_t base = block_reduce_max<kNT>(bmax, reinterpret_cast<int32_t*>(sc.red32));
 
-    // 5. write the snapshot slice
-    int4* rec = V.rec + rec_off;
-    uint2* rank = V.rank + int64_t(d) * W;
+    // 5. dense profile F(u) = max(PMX_e, S_e + u (N_e + 1), u), e = #{events < u}
+    if (P > 0) {
+        int32_t* prof = V.prof + int64_t(d) * P;
+        for (int64_t u = tid; u < P; u += kNT) {
+            const uint32_t word = a.B(u >> 5);
+            const uint32_t e = a.P(u >> 5) + __popc(word & ((1u << (u & 31)) - 1u));
+            int32_t pmx = pmx_end, lin = int32_t(u);
+            if (e < E) {
+                pmx = int32_t(a.M(e));
+                lin = int32_t(a.S(e) + uint32_t(u) * (a.C(e) + 1u));
+            }
+            const int32_t f = pmx > lin ? pmx : lin;
+            prof[u] = f > int32_t(u) ? f : int32_t(u);
+        }
+        phase<kInLds>();   // the HBM arrays are updated in place below
+    }
+
+    // 6. write the snapshot slice
+    uint2* rank = reinterpret_cast<uint2*>(V.slices + slice_off);
+    int4* rec = V.slices + slice_off + W / 2;
     if constexpr (kInLds) {
         for (int64_t e = tid; e < E; e += kNT)
             rec[e] = make_int4(int32_t(a.M(e)), int32_t(a.S(e)), int32_t(a.C(e) + 1u), int32_t(a.T(e)));
@@ -154,7 +172,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     if (tid == 0) {
         rec[E] = make_int4(pmx_end, 0, 1, INT32_MAX);
         DecHeader h;
-        h.rec_off = rec_off;
+        h.slice_off = slice_off;
         h.tot = tot;
         h.E = int32_t(E);
         h.base_peak = base;
@@ -185,7 +203,8 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
         if (threadIdx.x == 0) raise_error(dev_err, MAPS_ERR_TOO_MANY);
         hi = lo;
     }
-    const int64_t rec_off = lo + d;   // decoder d owns records [lo + d, hi + d]
+    // decoder d's slice: W/2 units of rank words, then records [0, hi - lo]
+    const int64_t slice_off = lo + int64_t(d) * (1 + W / 2);
     if (lds_cap > 0 && hi - lo <= lds_cap) {
         LdsArrays a;
         a.bits = lds;
@@ -194,12 +213,12 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
         a.wsum = a.cnt + lds_cap;
         a.tau = a.wsum + lds_cap;
         a.pmx = a.tau + lds_cap;
-        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, V, rec_off, base_peak, dev_err, sc);
+        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
     } else {
         HbmArrays a;
-        a.rank = reinterpret_cast<uint32_t*>(V.rank + int64_t(d) * W);
-        a.rec = reinterpret_cast<uint32_t*>(V.rec + rec_off);
-        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, V, rec_off, base_peak, dev_err, sc);
+        a.rank = reinterpret_cast<uint32_t*>(V.slices + slice_off);
+        a.rec = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
+        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
     }
 }
 
@@ -224,7 +243,8 @@ __global__ __launch_bounds__(kNT) void project_finish(int32_t D, int64_t n_total
         h.n_total = n_total;
         h.max_tot = mt;
         h.max_records = me;
-        for (int i = 0; i < 7; ++i) h.pad[i] = 0;
+        h.P = L.P;
+        for (int i = 0; i < 6; ++i) h.pad[i] = 0;
         h.magic = kSnapMagic;
         *V.hdr = h;
     }

@@ -47,11 +47,17 @@ def test_library_is_built_for_gfx950():
 
 
 def test_size_queries(lib):
-    # header 256 B + D decoder headers + D*W rank words + (n + D) records + 64 spare records
-    D, n, u_max = 4, 100, 8192
-    W = (((u_max + 1) // 32 + 1) + 1) & ~1
-    want = 256 + ((D * 32 + 255) // 256) * 256 + ((D * W * 8 + 255) // 256) * 256 + (n + D + 64) * 16
-    assert lib.maps_snapshot_bytes(D, n, u_max) == want
+    # header 256 B + D decoder headers + D*P profile entries + per decoder a
+    # slice of W/2 16-byte units of rank words and up to n_d + 1 records
+    # + 64 spare units; P = 0 once u_max + 1 > 16384
+    def want(D, n, u_max):
+        W = (((u_max + 1) // 32 + 1) + 1) & ~1
+        P = (u_max + 4) & ~3 if u_max + 1 <= 16384 else 0
+        a = lambda x: (x + 255) // 256 * 256
+        return 256 + a(D * 32) + a(D * P * 4) + (n + D * (1 + W // 2) + 64) * 16
+    D, n = 4, 100
+    for u_max in (0, 1, 8192, 16383, 16384, 65535):
+        assert lib.maps_snapshot_bytes(D, n, u_max) == want(D, n, u_max), u_max
     assert lib.maps_snapshot_bytes(0, n, u_max) == 0
     assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 63) == 0
     assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 64) > 0

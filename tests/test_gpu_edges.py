@@ -130,6 +130,29 @@ def test_ragged_shapes(orc, D, nmax, A, qmax, policy):
         compare_all(gg, o)
 
 
+@pytest.mark.parametrize("want_pairs", [False, True])
+@pytest.mark.parametrize("policy", [0, 1])
+def test_record_path(orc, policy, want_pairs):
+    """u_max above the dense-profile limit (16,384 entries): placement answers
+    every pair from the rank words and event records instead."""
+    rng = np.random.default_rng(77 + 2 * policy + want_pairs)
+    D, nmax, A, qmax, u_max = 9, 300, 5000, 20, 20000
+    seg, p, g, pred = _decoders(rng, D, nmax, u_max)
+    arr_pred = rng.integers(-2, u_max + 500, size=A).astype(np.int32)
+    qoff, qp, qpred, qw = _queues(rng, D, qmax, u_max)
+    b = custom_batch(cal_pred=np.arange(1, 41), cal_truth=np.arange(1, 41) + 7, edges=[20], alpha_ppm=100000,
+                     u_max=u_max, seg_off=seg, res_prompt=p, res_gen=g, res_pred=pred,
+                     arr_prompt=rng.integers(0, 3000, size=A), arr_pred=arr_pred,
+                     capacity=rng.integers(0, 400000, size=D), queue_len=rng.integers(0, 4, size=D),
+                     q_off=qoff, q_prompt=qp, q_pred=qpred, q_wait_ms=qw)
+    o0 = oracle_step(b, o=orc, want_pairs=False)
+    cap = (o0["base_peak"] + rng.integers(0, 30000, size=D)).astype(np.int32)
+    o = oracle_step(b, capacity=cap, policy=policy, want_pairs=want_pairs, o=orc)
+    gg = gpu_step(b, capacity=cap, policy=policy, want_pairs=want_pairs)
+    assert gg["err"] == 0, gg["errors"]
+    compare_all(gg, o, pairs=want_pairs)
+
+
 def test_capacity_boundary_and_ties(orc):
     """A peak equal to the capacity is feasible; equal queues and equal slacks
     go to the lowest decoder; all-infeasible arrivals take the largest slack."""
