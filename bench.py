@@ -197,7 +197,7 @@ def main():
                    "decoders": D, "arrivals": A, "pairs": D * A},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
-                     "kernel": "maps_place (place_records + place_reduce)",
+                     "kernel": "maps_place (place_records + place_finish)",
                      "algorithmic_bytes": nbytes, "place_ms": place_ms},
         "breakdown_ms": parts,
         "mean_events_per_decoder": float(np.mean(events_per_decoder)),

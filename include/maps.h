@@ -159,9 +159,13 @@ maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n_total,
  * pair_peak (optional, NULL to skip): decoder-major [D][A] int32 peak(a,d),
  * -1 for round-robin arrivals.  Arrivals are evaluated independently against
  * the same snapshot (no reservation between them).
+ * workspace: device memory of maps_place_workspace_size(D, A, u_max) bytes
+ * (per-group partial choices), required when A > 0; the caller owns it and
+ * it must not be shared by calls in flight at the same time.
  * dev_err bits: NEG_LEN (a_prompt, capacity or queue_len < 0), INT32_RANGE
  * (an arrival whose p + U could overflow a peak), SNAPSHOT.
- * Host errors: NULL, SIZE (D < 1, A < 0, rr_offset < 0), POLICY, WORKSPACE, HIP.
+ * Host errors: NULL (also a NULL workspace with A > 0), SIZE (D < 1, A < 0,
+ * rr_offset < 0), POLICY, WORKSPACE (workspace_bytes too small), HIP.
  */
 size_t maps_place_workspace_size(int32_t D, int64_t A, int32_t u_max);
 maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,

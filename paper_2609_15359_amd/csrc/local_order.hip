@@ -67,7 +67,7 @@ __device__ void bitonic_sort(uint64_t* keys, int n2) {
 }
 
 // Largest projected peak of the residents plus the first k requests of the new order.
-__device__ int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, const int4* rec, int32_t E,
+__device__ int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, const int2* cold, int32_t E,
                                int32_t W) {
     block_scan<kNT, false, true, false, int32_t>(
         n, 0, [&](int64_t i) { return int32_t(s.pos[s.uidx[i]] < k); },
@@ -78,17 +78,22 @@ __device__ int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, con
     if (threadIdx.x == 0) { s.csuf[n] = 0; s.psuf[n] = 0; }
     __syncthreads();
     int64_t best = 0;
-    // resident event times
-    for (int e = threadIdx.x; e < E; e += kNT) {
-        const int4 r = rec[e];
-        const int64_t tau = r.w;
-        int lo = 0, hi = n;   // first bound-sorted position with bound >= tau
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (s.ue[s.uidx[mid]] < tau) lo = mid + 1; else hi = mid;
+    // resident event times: the set bits of the rank words, event e the
+    // (before + j)-th of them
+    for (int w = threadIdx.x; w < W; w += kNT) {
+        const uint2 rw = rank[w];
+        uint32_t bits = rw.x, e = rw.y;
+        for (; bits != 0u && e < uint32_t(E); bits &= bits - 1u, ++e) {
+            const int64_t tau = int64_t(w) * 32 + (__ffs(bits) - 1);
+            const int2 r = cold[e];
+            int lo = 0, hi = n;   // first bound-sorted position with bound >= tau
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s.ue[s.uidx[mid]] < tau) lo = mid + 1; else hi = mid;
+            }
+            const int64_t v = int64_t(r.x) + tau * (r.y - 1) + s.psuf[lo] + tau * s.csuf[lo];
+            best = best > v ? best : v;
         }
-        const int64_t v = int64_t(r.y) + tau * (r.z - 1) + s.psuf[lo] + tau * s.csuf[lo];
-        best = best > v ? best : v;
     }
     // bounds of the admitted requests
     const int32_t ucl_max = 32 * W - 1;
@@ -100,8 +105,8 @@ __device__ int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, con
         const uint2 w = rank[tc >> 5];
         uint32_t e = w.y + __popc(w.x & ((1u << (tc & 31)) - 1u));
         e = e < uint32_t(E) ? e : uint32_t(E);
-        const int4 r = rec[e];
-        const int64_t occ = e < uint32_t(E) ? int64_t(r.y) + t * (r.z - 1) : 0;
+        const int2 r = cold[e];
+        const int64_t occ = e < uint32_t(E) ? int64_t(r.x) + t * (r.y - 1) : 0;
         const int g0 = s.grp[i];
         const int64_t v = occ + s.psuf[g0] + t * s.csuf[g0];
         best = best > v ? best : v;
@@ -181,13 +186,13 @@ __global__ __launch_bounds__(kNT) void local_order_kernel(LocalArgs g) {
 
     // 3. admission: largest k with peak(k) <= C
     const uint2* rank = slice_rank(V, h);
-    const int4* rec = slice_rec(V, h, L);
+    const int2* cold = slice_cold(V, h, L);
     int lo = 0;
     if (h.base_peak <= C) {
         int hi = n;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
-            const int64_t pk = prefix_peak(s, n, mid, rank, rec, h.E, L.W);
+            const int64_t pk = prefix_peak(s, n, mid, rank, cold, h.E, L.W);
             if (pk <= C) lo = mid; else hi = mid - 1;
         }
     }

@@ -33,13 +33,18 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // PF(U) >= base already.  Hence the projected peak with the arrival is
 //   peak(p, U) = max(p + PF(U), base).
 //
-// Record e (0 <= e <= E) stores {PMX_e, S_e, N_e + 1, tau_e}; record E is
-// {PMX_E, 0, 1, INT32_MAX}.  The rank e = #{events < U} comes from a bitmap
+// Each event e (0 <= e <= E, with S_E = N_E = 0) has two 8-byte records:
+//   hot  {PMX_e, T_e}     T_e = the smallest U with S_e + U (N_e + 1) > PMX_e
+//                         (0 when S_e > PMX_e; capped at INT32_MAX),
+//   cold {S_e, N_e + 1}.
+// For U < T_e, PF(U) = PMX_e and the cold record is not needed; for U >= T_e,
+// PF(U) = S_e + U (N_e + 1).  The rank e = #{events < U} comes from a bitmap
 // over the step axis: word w holds bit j for event time 32w + j, next to the
 // number of events before word w.  W words cover [0, 32 W) with 32 W - 1 > u_max,
 // so a bound clamped to 32 W - 1 ranks above every event.  Each decoder's rank
 // words and records form one contiguous slice of 16-byte units (W/2 units of
-// rank words, then the records), so a consumer copies it in one pass.
+// rank words, then the E + 1 hot records, then the E + 1 cold records), so a
+// consumer copies it in one pass.
 //
 // Since PF depends on the arrival only through U, a decoder whose bounds are
 // short enough also gets a dense profile F(u) = max(PF(u), u) for u = 0..u_max
@@ -132,8 +137,18 @@ __host__ __device__ inline bool slice_ok(const DecHeader& h, int64_t n_total, co
 __host__ __device__ inline const uint2* slice_rank(const SnapView& V, const DecHeader& h) {
     return reinterpret_cast<const uint2*>(V.slices + h.slice_off);
 }
-__host__ __device__ inline const int4* slice_rec(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
-    return V.slices + h.slice_off + L.W / 2;
+__host__ __device__ inline const int2* slice_hot(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
+    return reinterpret_cast<const int2*>(V.slices + h.slice_off + L.W / 2);
+}
+__host__ __device__ inline const int2* slice_cold(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
+    return slice_hot(V, h, L) + h.E + 1;
+}
+
+// Threshold T of an event: the smallest U >= 0 with S + U n1 > pmx.
+__host__ __device__ inline int32_t event_threshold(int32_t pmx, int32_t S, uint32_t n1) {
+    if (S > pmx) return 0;
+    const int64_t t = int64_t(pmx - S) / int64_t(n1) + 1;
+    return t < int64_t(INT32_MAX) ? int32_t(t) : INT32_MAX;
 }
 
 // ---------------------------------------------------------------------------

@@ -4,7 +4,8 @@
 // snapshot of maps_internal.hpp the projected peak of one pair is either
 //   e    = bits_before(word) + popcount(word & below(U))     (rank of U)
 //   peak = max(p + max(PMX_e, S_e + U (N_e + 1), U), base)
-// (record path: one 8-byte and one 12-byte LDS read), or, when the snapshot
+// (record path: an 8-byte rank word and an 8-byte record, plus a second 8-byte
+// record only past the event's threshold, all in LDS), or, when the snapshot
 // carries dense profiles,
 //   peak = max(p + max(F[min(U, u_max)], U), base)
 // (profile path: one 4-byte LDS read).
@@ -15,10 +16,10 @@
 // b / G.  Each thread keeps its arrivals in registers; the workgroup walks its
 // decoders in order, stages their snapshot data in LDS, and evaluates all its
 // arrivals against each, writing the decoder-major pair-peak row segment with
-// coalesced stores and keeping the running best choice per arrival.  Ties
-// keep the earlier (lower) decoder.  With G > 1 each group writes its best
-// (key, decoder, peak) per arrival and place_reduce picks the best group in
-// group order; with G = 1 the outputs are written directly.
+// coalesced stores and keeping the running best choice per arrival (ties keep
+// the earlier, lower decoder).  Each group writes its best (key, decoder) per
+// arrival; place_finish picks the best group in group order, evaluates the
+// chosen pair's peak once more from the snapshot and writes the outputs.
 //
 // Selection (smaller key is better, see select_key): policy MQ prefers any
 // feasible decoder, by queue length, then the smallest overflow; policy MC
@@ -46,9 +47,8 @@ struct PlaceArgs {
     int32_t* chosen_over;
     uint8_t* flags;
     int32_t* pair;
-    int32_t* pkey;     // [G][A] partial best keys
-    int32_t* pdec;     // [G][A] partial best decoders
-    int32_t* ppeak;    // [G][A] partial best peaks
+    int32_t* pkey;     // [G][A] best key of each group
+    int32_t* pdec;     // [G][A] best decoder of each group
     int32_t G;
     int32_t Dg;        // decoders per group
     int32_t buf_units; // record path: 16-byte units per LDS buffer (0: slices stay in HBM)
@@ -56,21 +56,10 @@ struct PlaceArgs {
     uint32_t* dev_err;
 };
 
-// Read-only values every lane needs alike (capacities, queue lengths, snapshot
-// headers), loaded through the scalar cache into scalar registers: vector
-// loads would make their first use wait for every store issued before them.
+// Read-only values every lane needs alike, loaded through the scalar cache.
 template <typename T>
 __device__ __forceinline__ T load_uniform(const T* p) {
     return *(const __attribute__((address_space(4))) T*)(p);
-}
-__device__ __forceinline__ DecHeader load_dec(const DecHeader* p) {
-    DecHeader h;
-    h.slice_off = load_uniform(&p->slice_off);
-    h.tot = load_uniform(&p->tot);
-    h.E = load_uniform(&p->E);
-    h.base_peak = load_uniform(&p->base_peak);
-    h.pad[0] = h.pad[1] = 0;
-    return h;
 }
 
 __device__ inline bool snapshot_ok(const SnapHeader* h, const SnapLayout& L) {
@@ -95,6 +84,43 @@ __device__ __forceinline__ int32_t select_key(int32_t peak, int32_t C, int32_t Q
     else return v;
 }
 
+// Per-decoder values of up to 64 consecutive decoders, lane j of every wave
+// holding decoder d0 + j.  One vector load per field serves 64 decoders, and
+// each decoder's values are then read out of the lanes into scalar registers:
+// no load latency per decoder, and no wait on a fresh load (which would also
+// wait for every store issued before it) inside the decoder loop.
+struct DecLanes {
+    int32_t off_lo, off_hi, E, base, C, Q;
+};
+
+__device__ __forceinline__ DecLanes load_lanes(const PlaceArgs& g, const SnapView& V, int32_t d0, int32_t d_end) {
+    const int32_t d = d0 + int32_t(threadIdx.x % kWave);
+    DecLanes l{0, 0, -1, -1, 0, 0};
+    if (d < d_end) {
+        const DecHeader h = V.dec[d];
+        l.off_lo = int32_t(uint64_t(h.slice_off));
+        l.off_hi = int32_t(uint64_t(h.slice_off) >> 32);
+        l.E = h.E;
+        l.base = h.base_peak;
+        l.C = g.cap[d];
+        l.Q = g.qlen[d];
+    }
+    return l;
+}
+
+__device__ __forceinline__ int32_t lane_value(int32_t v, int32_t lane) { return __builtin_amdgcn_readlane(v, lane); }
+
+__device__ __forceinline__ DecHeader lane_header(const DecLanes& l, int32_t lane) {
+    DecHeader h;
+    h.slice_off = int64_t(uint64_t(uint32_t(lane_value(l.off_lo, lane))) |
+                          (uint64_t(uint32_t(lane_value(l.off_hi, lane))) << 32));
+    h.tot = 0;
+    h.E = lane_value(l.E, lane);
+    h.base_peak = lane_value(l.base, lane);
+    h.pad[0] = h.pad[1] = 0;
+    return h;
+}
+
 // Raw buffer resources (gfx9 descriptor, 32-bit data format): accesses whose
 // VGPR offset (plus immediate) reaches past `bytes` read 0 and write nothing.
 constexpr int kBufferWord3 = 0x00020000;
@@ -114,6 +140,57 @@ __device__ __forceinline__ void store_pair(__amdgpu_buffer_rsrc_t row, int k, in
         __builtin_amdgcn_raw_buffer_store_b32(v, row, int(threadIdx.x) * 4 + k * kNT * 4, 0, kNonTemporal);
 }
 
+// Projected peak of (p, U) from the records of event e (see maps_internal.hpp):
+// PF(U) = PMX_e below the event's threshold, else S_e + U (N_e + 1).  For a
+// bound at or above 32 W the rank lands on event E (N + 1 = 1, S = 0), where
+// S + U (N + 1) = U; so the product may use U itself (its low 24 bits, all of
+// it whenever an event before E is hit, since events are <= u_max), and the
+// final max with U restores it.
+__device__ __forceinline__ int32_t event_peak(const int2* hot, const int2* cold, uint32_t e, int32_t p, int32_t U,
+                                              int32_t base) {
+    const int2 h = hot[e];
+    int32_t pf = max(h.x, U);
+    if (U >= h.y) {
+        const int2 c = cold[e];
+        pf = max(c.x + int32_t(__umul24(uint32_t(U), uint32_t(c.y))), U);
+    }
+    return imax(p + pf, base);
+}
+
+// Arrival k of the thread's tile with its prompt clamped at 0, reporting the
+// error bits of the tile's arrivals.
+template <int kAPT, bool kFull>
+__device__ __forceinline__ void load_arrivals(const PlaceArgs& g, int64_t a0, int64_t max_tot, int32_t (&p)[kAPT],
+                                              int32_t (&U)[kAPT]) {
+    bool neg = false, range = false;
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
+        int32_t pk = 0, Uk = -1;
+        if (kFull || a < g.A) { pk = g.ap[a]; Uk = g.aU[a]; }
+        neg |= pk < 0;
+        if (Uk >= 0 && int64_t(pk) + Uk + max_tot + g.L.u_max > int64_t(INT32_MAX)) range = true;
+        p[k] = pk < 0 ? 0 : pk;
+        U[k] = Uk;
+    }
+    if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+    if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
+}
+
+// The group's best (key, decoder) of each arrival of the tile.
+template <int kAPT, bool kFull>
+__device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, int64_t a0,
+                                               const int32_t (&key)[kAPT], const int32_t (&dec)[kAPT]) {
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
+        if (!kFull && a >= g.A) continue;
+        const int64_t o = int64_t(grp) * g.A + a;
+        g.pkey[o] = key[k];
+        g.pdec[o] = dec[k] < g.L.D ? dec[k] : 0;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Record path.
 //
@@ -124,10 +201,6 @@ __device__ __forceinline__ void store_pair(__amdgpu_buffer_rsrc_t row, int k, in
 // evaluated from one buffer, the slice of decoder d+1 is already on its way
 // into registers, and it is written to the other buffer before the single
 // barrier of the next step.  A slice too large for a buffer is read from HBM.
-//
-// For a bound at or above 32 W the rank lands on record E (N + 1 = 1, S = 0),
-// where S + U (N + 1) <= U; so the product may use U itself (its low 24 bits,
-// all of it whenever a record before E is hit, since events are <= u_max).
 // ---------------------------------------------------------------------------
 constexpr int kStage = 10;  // 16-byte units per thread staged in registers: a whole LDS buffer
 
@@ -138,36 +211,51 @@ struct RecArrivals {
     int32_t best_key[kAPT], best_d[kAPT];
 };
 
-__device__ __forceinline__ int32_t record_peak(const int4& r, int32_t p, int32_t U, int32_t base) {
-    const int32_t lin = r.y + int32_t(__umul24(uint32_t(U), uint32_t(r.z)));
-    const int32_t pf = max(max(r.x, lin), U);
-    return imax(p + pf, base);
-}
-
 // Evaluate the thread's arrivals against one decoder whose rank words start
-// at `rank` and records at `rec` (both in LDS, or both in HBM).
+// at `rank` and hot records at `hot`, the cold ones following them (all in
+// LDS, or all in HBM).  Only lanes whose bound reaches an event's threshold
+// read its cold record.
 template <int kAPT, bool kFull, bool kPairs, int kPolicy>
-__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int4* rec, uint32_t E,
+__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int2* hot, uint32_t E,
                                              int32_t base, int32_t C, int32_t Q, int32_t d,
                                              __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
+    const int2* cold = hot + E + 1;
     const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
 #pragma unroll
     for (int c = 0; c < kAPT; c += kChunk) {
         uint2 w[kChunk];
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) w[i] = *reinterpret_cast<const uint2*>(rank + s.roff[c + i]);
-        int4 r[kChunk];
+        uint32_t e[kChunk];
+        int2 h[kChunk];
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
-            uint32_t e = w[i].y + __popc(w[i].x & s.mask[c + i]);
-            e = e < E ? e : E;   // stays inside the decoder's records
-            r[i] = rec[e];
+            e[i] = w[i].y + __popc(w[i].x & s.mask[c + i]);
+            e[i] = e[i] < E ? e[i] : E;   // stays inside the decoder's records
+            h[i] = hot[e[i]];
+        }
+        int32_t pf[kChunk];
+        bool line = false;
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            pf[i] = max(h[i].x, s.U[c + i]);
+            line |= s.U[c + i] >= h[i].y;
+        }
+        if (__builtin_amdgcn_ballot_w64(line) != 0) {   // a lane of the wave reached a threshold
+#pragma unroll
+            for (int i = 0; i < kChunk; ++i) {
+                const int32_t U = s.U[c + i];
+                if (U >= h[i].y) {
+                    const int2 cr = cold[e[i]];
+                    pf[i] = max(cr.x + int32_t(__umul24(uint32_t(U), uint32_t(cr.y))), U);
+                }
+            }
         }
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             const int k = c + i;
-            const int32_t peak = record_peak(r[i], s.p[k], s.U[k], base);
+            const int32_t peak = imax(s.p[k] + pf[i], base);
             if constexpr (kPairs) store_pair<kFull>(row, k, peak | s.neg[k]);
             const int32_t key = select_key<kPolicy>(peak, C, Qm);
             const bool take = key < s.best_key[k];
@@ -177,43 +265,38 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
     }
 }
 
-// Load this thread's first kStage units of a slice of `units` units into
-// registers (units past the end read as 0).
+// Load this thread's units of a slice of `units` units into registers: rows
+// j of kNT units that hold part of the slice (a uniform test), with the units
+// past the end of the last one read as 0.
 __device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* src, int32_t units) {
     const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, uint32_t(units) * 16u);
 #pragma unroll
     for (int j = 0; j < kStage; ++j)
-        stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
-                                               rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
+        if (j * kNT < units)
+            stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                                   rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
 }
 
 // One arrival tile against the decoders of group grp.  kMixed: some slices
 // may exceed an LDS buffer and are then read from HBM; otherwise every slice
 // fits (a header claiming more is reported and skipped).
-template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy, bool kMixed>
+template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kMixed>
 __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
                                              int64_t a0) {
     const SnapLayout& L = g.L;
     const int32_t half_w = L.W / 2;                // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
     const int32_t d_end = d_begin + g.Dg < L.D ? d_begin + g.Dg : L.D;
-    const int64_t max_tot = load_uniform(&V.hdr->max_tot);
     const int64_t n_total = load_uniform(&V.hdr->n_total);
     const int32_t ucl_max = 32 * L.W - 1;          // ranks above every event
     const int32_t buf_units = g.buf_units;
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     RecArrivals<kAPT> s;
-    bool neg = false, range = false;
+    load_arrivals<kAPT, kFull>(g, a0, load_uniform(&V.hdr->max_tot), s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
-        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        int32_t p = 0, U = -1;
-        if (kFull || a < g.A) { p = g.ap[a]; U = g.aU[a]; }
-        neg |= p < 0;
-        if (U >= 0 && int64_t(p) + U + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
-        s.p[k] = p < 0 ? 0 : p;
-        s.U[k] = U;
+        const int32_t U = s.U[k];
         s.neg[k] = U < 0 ? -1 : 0;
         const int32_t uc = U < 0 ? 0 : (U < ucl_max ? U : ucl_max);
         s.roff[k] = uint32_t(uc >> 5) * 8u;
@@ -221,13 +304,13 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         s.best_key[k] = INT32_MAX;
         s.best_d[k] = d_begin;
     }
-    if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-    if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
 
     auto fits = [&](const DecHeader& h) { return half_w + h.E + 1 <= buf_units; };
 
+    DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+    int32_t lanes0 = d_begin;
     v4i stage[kStage];
-    DecHeader h = load_dec(V.dec + (d_begin < d_end ? d_begin : 0));
+    DecHeader h = lane_header(lanes, 0);
     bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
     if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);
     for (int32_t d = d_begin; d < d_end; ++d) {
@@ -235,20 +318,26 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         const bool valid = h_ok;
         const bool in_lds = valid && (!kMixed || fits(cur));
         const int32_t buf = (d - d_begin) & 1;
-        const int32_t C = load_uniform(g.cap + d), Q = load_uniform(g.qlen + d);
+        const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
         if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
         if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         int4* slice = lds + buf * buf_units;
         if (in_lds) {
             // Buffer `buf` was last read for decoder d-2, which every wave
-            // finished before passing the barrier of decoder d-1.  The staged
-            // units cover the whole buffer; those past the slice's end are 0.
+            // finished before passing the barrier of decoder d-1.  Staged units
+            // past the slice's end (0) stay inside the buffer: kStage * kNT
+            // units fit it.
+            const int32_t units = half_w + cur.E + 1;
 #pragma unroll
             for (int j = 0; j < kStage; ++j)
-                reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
+                if (j * kNT < units) reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
         }
         if (d + 1 < d_end) {
-            h = load_dec(V.dec + d + 1);
+            if (d + 1 - lanes0 == kWave) {
+                lanes = load_lanes(g, V, d + 1, d_end);
+                lanes0 = d + 1;
+            }
+            h = lane_header(lanes, d + 1 - lanes0);
             h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
             if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);   // overlaps the evaluation
         }
@@ -257,56 +346,21 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         const __amdgpu_buffer_rsrc_t row =
             buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
         if (!kMixed || in_lds)
-            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice), slice + half_w,
+            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice),
+                                                       reinterpret_cast<const int2*>(slice + half_w),
                                                        uint32_t(cur.E), cur.base_peak, C, Q, d, row);
         else if constexpr (kMixed)
             eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
-                                                       slice_rec(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
+                                                       slice_hot(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
                                                        d, row);
     }
-
-#pragma unroll
-    for (int k = 0; k < kAPT; ++k) {
-        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        if (!kFull && a >= g.A) continue;
-        // the chosen pair's peak, evaluated once more from the snapshot in HBM
-        int32_t peak = 0;
-        if (d_begin < d_end && s.U[k] >= 0) {
-            const DecHeader hb = V.dec[s.best_d[k]];
-            if (slice_ok(hb, n_total, L)) {
-                const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(slice_rank(V, hb)) +
-                                                                s.roff[k]);
-                uint32_t e = w.y + __popc(w.x & s.mask[k]);
-                e = e < uint32_t(hb.E) ? e : uint32_t(hb.E);
-                peak = record_peak(slice_rec(V, hb, L)[e], s.p[k], s.U[k], hb.base_peak);
-            }
-        }
-        if constexpr (kFinal) {
-            if (s.U[k] < 0) {
-                g.choice[a] = int32_t((g.rr_offset + a) % L.D);
-                g.chosen_peak[a] = -1;
-                g.chosen_over[a] = 0;
-                g.flags[a] = 2;
-            } else {
-                const int32_t C = g.cap[s.best_d[k]];
-                g.choice[a] = s.best_d[k];
-                g.chosen_peak[a] = peak;
-                g.chosen_over[a] = peak > C ? peak - C : 0;
-                g.flags[a] = peak <= C ? 1 : 0;
-            }
-        } else {
-            const int64_t o = int64_t(grp) * g.A + a;
-            g.pkey[o] = s.best_key[k];
-            g.pdec[o] = s.best_d[k];
-            g.ppeak[o] = peak;
-        }
-    }
+    write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }
 
 // When every slice fits an LDS buffer (the snapshot's largest record count
 // says so) the tile runs in one pass; otherwise it is split into sub-tiles of
 // at most 4 arrivals per thread that read the large slices from HBM.
-template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+template <int kAPT, bool kPairs, int kPolicy>
 __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     extern __shared__ int4 lds[];
     const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
@@ -319,57 +373,25 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     const int32_t max_records = load_uniform(&V.hdr->max_records);
     if (g.L.W / 2 + max_records <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
-            records_tile<kAPT, true, kPairs, kFinal, kPolicy, false>(g, V, lds, grp, a0);
+            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0);
         else
-            records_tile<kAPT, false, kPairs, kFinal, kPolicy, false>(g, V, lds, grp, a0);
+            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0);
     } else {
         constexpr int kSub = kAPT < 4 ? kAPT : 4;
         for (int t = 0; t < kAPT / kSub; ++t) {
             const int64_t b0 = a0 + int64_t(t) * kNT * kSub;
-            if (b0 < g.A) records_tile<kSub, false, kPairs, kFinal, kPolicy, true>(g, V, lds, grp, b0);
+            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0);
         }
-    }
-}
-
-__global__ __launch_bounds__(256) void place_reduce(PlaceArgs g) {
-    const SnapLayout& L = g.L;
-    const SnapView V = snap_view(const_cast<void*>(g.snap), L);
-    if (!snapshot_ok(V.hdr, L)) return;
-    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    for (int64_t a = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; a < g.A; a += stride) {
-        if (g.aU[a] < 0) {
-            g.choice[a] = int32_t((g.rr_offset + a) % L.D);
-            g.chosen_peak[a] = -1;
-            g.chosen_over[a] = 0;
-            g.flags[a] = 2;
-            continue;
-        }
-        int32_t key = g.pkey[a];
-        int32_t d = g.pdec[a], peak = g.ppeak[a];
-        for (int32_t gi = 1; gi < g.G; ++gi) {
-            const int64_t o = int64_t(gi) * g.A + a;
-            const int32_t k2 = g.pkey[o];
-            if (k2 < key) { key = k2; d = g.pdec[o]; peak = g.ppeak[o]; }
-        }
-        d = d < 0 || d >= L.D ? 0 : d;
-        const int32_t C = g.cap[d];
-        g.choice[a] = d;
-        g.chosen_peak[a] = peak;
-        g.chosen_over[a] = peak > C ? peak - C : 0;
-        g.flags[a] = peak <= C ? 1 : 0;
     }
 }
 
 // ---------------------------------------------------------------------------
-// Placement from the dense profiles (snapshots with P > 0).
+// Profile path (snapshots with P > 0).
 //
 // The profile F of a decoder answers a pair with one 4-byte LDS read:
 //   peak = max(p + max(F[min(U, u_max)], U), base).
-// Workgroup b takes decoder group b % G and arrival tile b / G (kAPT arrivals
-// per thread, kept in registers with their running best).  The group's
-// profiles go through LDS nb decoders at a time; while one batch is evaluated
-// the next one is already on its way into registers (kProfPF units of 16
-// bytes per thread, the remainder loaded after the barrier).
+// The group's profiles go through LDS nb decoders at a time; while one batch
+// is evaluated the next one is already on its way into registers.
 // ---------------------------------------------------------------------------
 constexpr int kProfPF = 16;
 
@@ -380,15 +402,16 @@ struct ProfArrivals {
     int32_t best_key[kAPT], best_d[kAPT];
 };
 
-// Load this thread's kProfPF units of the batch starting at decoder db, which
-// cover the whole batch (units past its end read as 0).
+// Load this thread's units of the batch starting at decoder db (rows j of kNT
+// units that hold part of it; units past its end read as 0).
 __device__ __forceinline__ void stage_profile(v4i (&stage)[kProfPF], const int32_t* prof, int32_t P, int32_t db,
                                               int32_t units) {
     const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(prof + int64_t(db) * P, uint32_t(units) * 16u);
 #pragma unroll
     for (int j = 0; j < kProfPF; ++j)
-        stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
-                                               rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
+        if (j * kNT < units)
+            stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                                   rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
 }
 
 template <int kAPT, bool kFull, bool kPairs, int kPolicy>
@@ -407,36 +430,29 @@ __device__ __forceinline__ void prof_decoder(ProfArrivals<kAPT>& s, const char* 
     }
 }
 
-template <int kAPT, bool kFull, bool kPairs, bool kFinal, int kPolicy>
+template <int kAPT, bool kFull, bool kPairs, int kPolicy>
 __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
                                           int64_t a0) {
     const SnapLayout& L = g.L;
     const int32_t P = L.P;
     const int32_t d_begin = grp * g.Dg;
     const int32_t d_end = d_begin + g.Dg < L.D ? d_begin + g.Dg : L.D;
-    const int64_t max_tot = load_uniform(&V.hdr->max_tot);
     const int32_t nb = g.nb;   // nb * P / 4 <= kProfPF * kNT
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     ProfArrivals<kAPT> s;
-    bool neg = false, range = false;
+    load_arrivals<kAPT, kFull>(g, a0, load_uniform(&V.hdr->max_tot), s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
-        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        int32_t p = 0, U = -1;
-        if (kFull || a < g.A) { p = g.ap[a]; U = g.aU[a]; }
-        neg |= p < 0;
-        if (U >= 0 && int64_t(p) + U + max_tot + L.u_max > int64_t(INT32_MAX)) range = true;
-        s.p[k] = p < 0 ? 0 : p;
-        s.U[k] = U;
+        const int32_t U = s.U[k];
         s.neg[k] = U < 0 ? -1 : 0;
         s.off[k] = 4u * uint32_t(U < 0 ? 0 : (U < L.u_max ? U : L.u_max));
         s.best_key[k] = INT32_MAX;
         s.best_d[k] = d_begin;
     }
-    if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-    if (range) raise_error(g.dev_err, MAPS_ERR_INT32_RANGE);
 
+    DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+    int32_t lanes0 = d_begin;
     v4i stage[kProfPF];
     if (d_begin < d_end) {
         const int32_t n0 = d_end - d_begin < nb ? d_end - d_begin : nb;
@@ -444,9 +460,11 @@ __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V,
     }
     for (int32_t db = d_begin; db < d_end; db += nb) {
         const int32_t n = d_end - db < nb ? d_end - db : nb;
+        const int32_t units = n * (P / 4);
         __syncthreads();   // every wave finished reading the previous batch
 #pragma unroll
-        for (int j = 0; j < kProfPF; ++j) reinterpret_cast<v4i*>(lds)[int(threadIdx.x) + j * kNT] = stage[j];
+        for (int j = 0; j < kProfPF; ++j)
+            if (j * kNT < units) reinterpret_cast<v4i*>(lds)[int(threadIdx.x) + j * kNT] = stage[j];
         __syncthreads();
         if (db + nb < d_end) {
             const int32_t n1 = d_end - (db + nb) < nb ? d_end - (db + nb) : nb;
@@ -454,8 +472,12 @@ __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V,
         }
         for (int32_t i = 0; i < n; ++i) {
             const int32_t d = db + i;
-            const int32_t base = load_uniform(&V.dec[d].base_peak);
-            const int32_t C = load_uniform(g.cap + d), Q = load_uniform(g.qlen + d);
+            if (d - lanes0 == kWave) {
+                lanes = load_lanes(g, V, d, d_end);
+                lanes0 = d;
+            }
+            const int32_t base = lane_value(lanes.base, d - lanes0);
+            const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
             if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
             if (threadIdx.x == 0 && base < 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
             const char* table = reinterpret_cast<const char*>(lds) + size_t(i) * P * 4;
@@ -464,41 +486,10 @@ __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V,
             prof_decoder<kAPT, kFull, kPairs, kPolicy>(s, table, base, C, Q, d, row);
         }
     }
-
-#pragma unroll
-    for (int k = 0; k < kAPT; ++k) {
-        const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        if (!kFull && a >= g.A) continue;
-        // the chosen pair's peak, read once more from the profile in HBM
-        int32_t peak = 0;
-        if (d_begin < d_end && s.U[k] >= 0) {
-            const int32_t bd = s.best_d[k];
-            const int32_t f = V.prof[int64_t(bd) * P + (s.off[k] >> 2)];
-            peak = imax(s.p[k] + (f > s.U[k] ? f : s.U[k]), V.dec[bd].base_peak);
-        }
-        if constexpr (kFinal) {
-            if (s.U[k] < 0) {
-                g.choice[a] = int32_t((g.rr_offset + a) % L.D);
-                g.chosen_peak[a] = -1;
-                g.chosen_over[a] = 0;
-                g.flags[a] = 2;
-            } else {
-                const int32_t C = g.cap[s.best_d[k]];
-                g.choice[a] = s.best_d[k];
-                g.chosen_peak[a] = peak;
-                g.chosen_over[a] = peak > C ? peak - C : 0;
-                g.flags[a] = peak <= C ? 1 : 0;
-            }
-        } else {
-            const int64_t o = int64_t(grp) * g.A + a;
-            g.pkey[o] = s.best_key[k];
-            g.pdec[o] = s.best_d[k];
-            g.ppeak[o] = peak;
-        }
-    }
+    write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }
 
-template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+template <int kAPT, bool kPairs, int kPolicy>
 __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
     extern __shared__ int4 lds[];
     const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
@@ -509,39 +500,84 @@ __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
     const int32_t grp = blockIdx.x % g.G;
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
     if (a0 + kNT * kAPT <= g.A)
-        prof_tile<kAPT, true, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+        prof_tile<kAPT, true, kPairs, kPolicy>(g, V, lds, grp, a0);
     else
-        prof_tile<kAPT, false, kPairs, kFinal, kPolicy>(g, V, lds, grp, a0);
+        prof_tile<kAPT, false, kPairs, kPolicy>(g, V, lds, grp, a0);
 }
 
-template <int kAPT, bool kPairs, bool kFinal, int kPolicy>
+// ---------------------------------------------------------------------------
+// Final choice per arrival: the best group in group order (strictly smaller
+// key wins, so ties keep the lower decoder), the chosen pair's peak evaluated
+// once more from the snapshot's records, and the outputs; an arrival without
+// a bound goes round-robin.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
+    const SnapLayout& L = g.L;
+    const SnapView V = snap_view(const_cast<void*>(g.snap), L);
+    if (!snapshot_ok(V.hdr, L)) return;
+    const int64_t n_total = load_uniform(&V.hdr->n_total);
+    const int32_t ucl_max = 32 * L.W - 1;
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t a = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; a < g.A; a += stride) {
+        const int32_t U = g.aU[a];
+        if (U < 0) {
+            g.choice[a] = int32_t((g.rr_offset + a) % L.D);
+            g.chosen_peak[a] = -1;
+            g.chosen_over[a] = 0;
+            g.flags[a] = 2;
+            continue;
+        }
+        int32_t key = g.pkey[a], d = g.pdec[a];
+        for (int32_t gi = 1; gi < g.G; ++gi) {
+            const int64_t o = int64_t(gi) * g.A + a;
+            const int32_t k2 = g.pkey[o];
+            if (k2 < key) { key = k2; d = g.pdec[o]; }
+        }
+        d = d < 0 || d >= L.D ? 0 : d;
+        const int32_t p = g.ap[a] < 0 ? 0 : g.ap[a];
+        const DecHeader h = V.dec[d];
+        int32_t peak = 0;
+        if (slice_ok(h, n_total, L)) {
+            const int32_t uc = U < ucl_max ? U : ucl_max;
+            const uint2 w = slice_rank(V, h)[uc >> 5];
+            uint32_t e = w.y + __popc(w.x & ((1u << (uc & 31)) - 1u));
+            e = e < uint32_t(h.E) ? e : uint32_t(h.E);
+            peak = event_peak(slice_hot(V, h, L), slice_cold(V, h, L), e, p, U, h.base_peak);
+        }
+        const int32_t C = g.cap[d];
+        g.choice[a] = d;
+        g.chosen_peak[a] = peak;
+        g.chosen_over[a] = peak > C ? peak - C : 0;
+        g.flags[a] = peak <= C ? 1 : 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launch
+// ---------------------------------------------------------------------------
+template <int kAPT, bool kPairs, int kPolicy>
 void launch_one(bool prof, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
     if (prof) {
-        auto fn = place_prof<kAPT, kPairs, kFinal, kPolicy>;
-        allow_dynamic_lds(fn, kLdsBytes);
-        hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
+        if constexpr (kAPT <= 8) {   // the profile path stages 64 VGPRs per thread
+            auto fn = place_prof<kAPT, kPairs, kPolicy>;
+            allow_dynamic_lds(fn, kLdsBytes);
+            hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
+        }
     } else {
-        auto fn = place_records<kAPT, kPairs, kFinal, kPolicy>;
+        auto fn = place_records<kAPT, kPairs, kPolicy>;
         allow_dynamic_lds(fn, kLdsBytes);
         hipLaunchKernelGGL(fn, grid, dim3(kNT), lds, s, a);
     }
 }
 
-template <int kAPT, bool kPairs, bool kFinal>
-void launch_policy(bool prof, int32_t policy, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
-    if (policy == MAPS_POLICY_MQ) launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MQ>(prof, grid, lds, s, a);
-    else launch_one<kAPT, kPairs, kFinal, MAPS_POLICY_MC>(prof, grid, lds, s, a);
-}
-
 template <int kAPT>
-void launch_apt(bool prof, bool pairs, bool final_, int32_t policy, dim3 grid, size_t lds, hipStream_t s,
-                const PlaceArgs& a) {
+void launch_apt(bool prof, bool pairs, int32_t policy, dim3 grid, size_t lds, hipStream_t s, const PlaceArgs& a) {
     if (pairs) {
-        if (final_) launch_policy<kAPT, true, true>(prof, policy, grid, lds, s, a);
-        else launch_policy<kAPT, true, false>(prof, policy, grid, lds, s, a);
+        if (policy == MAPS_POLICY_MQ) launch_one<kAPT, true, MAPS_POLICY_MQ>(prof, grid, lds, s, a);
+        else launch_one<kAPT, true, MAPS_POLICY_MC>(prof, grid, lds, s, a);
     } else {
-        if (final_) launch_policy<kAPT, false, true>(prof, policy, grid, lds, s, a);
-        else launch_policy<kAPT, false, false>(prof, policy, grid, lds, s, a);
+        if (policy == MAPS_POLICY_MQ) launch_one<kAPT, false, MAPS_POLICY_MQ>(prof, grid, lds, s, a);
+        else launch_one<kAPT, false, MAPS_POLICY_MC>(prof, grid, lds, s, a);
     }
 }
 
@@ -563,7 +599,6 @@ void plan(int32_t D, int64_t A, int cus, int max_apt, int* apt, int* groups) {
 struct PlaceWorkspace {
     int32_t* key;
     int32_t* dec;
-    int32_t* peak;
     size_t bytes;
 };
 
@@ -574,7 +609,6 @@ PlaceWorkspace place_carve(void* base, int64_t A) {
     auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
     w.key = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
     w.dec = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
-    w.peak = reinterpret_cast<int32_t*>(take(size_t(kMaxGroups) * A * 4));
     w.bytes = off;
     return w;
 }
@@ -610,16 +644,13 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
         (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags)))
         return MAPS_E_NULL;
     if (A == 0) return MAPS_OK;
+    if (!workspace) return MAPS_E_NULL;
+    const PlaceWorkspace w = place_carve(workspace, A);
+    if (workspace_bytes < w.bytes) return MAPS_E_WORKSPACE;
     const SnapLayout L = snap_layout(D, 0, u_max);   // region offsets do not depend on the resident count
     const bool prof = L.P > 0;
     int apt = 8, G = 1;
-    plan(D, A, compute_units(), prof ? 8 : 16, &apt, &G);   // the profile path stages 64 VGPRs
-    PlaceWorkspace w{};
-    if (G > 1) {
-        if (!workspace) return MAPS_E_NULL;
-        w = place_carve(workspace, A);
-        if (workspace_bytes < w.bytes) return MAPS_E_WORKSPACE;
-    }
+    plan(D, A, compute_units(), prof ? 8 : 16, &apt, &G);
     PlaceArgs a{};
     a.L = L;
     a.snap = snapshot;
@@ -636,38 +667,37 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
     a.pair = pair_peak;
     a.pkey = w.key;
     a.pdec = w.dec;
-    a.ppeak = w.peak;
     a.G = G;
     a.Dg = (D + G - 1) / G;
     a.dev_err = dev_err;
     // Slices are addressed through the decoder headers and bound-checked
     // against the snapshot's own resident count.
-    // Record path LDS: two buffers of buf_units 16-byte units, each at least
-    // as large as the staged part of a slice.
-    const int32_t buf_units = int32_t(kLdsBytes / 16 / 2);
-    a.buf_units = L.W / 2 + 64 <= buf_units && kStage * kNT <= buf_units ? buf_units : 0;
-    size_t lds = size_t(2 * a.buf_units) * 16;
+    size_t lds = 0;
     if (prof) {
         // LDS: the staged units of one batch of nb profiles
         const int64_t nb = int64_t(kProfPF) * kNT * 4 / L.P;
         a.nb = int32_t(nb < 8 ? nb : 8);
         lds = size_t(kProfPF) * kNT * 16;
+    } else {
+        // two buffers of buf_units 16-byte units, each at least as large as
+        // the staged part of a slice
+        const int32_t buf_units = int32_t(kLdsBytes / 16 / 2);
+        a.buf_units = L.W / 2 + 64 <= buf_units && kStage * kNT <= buf_units ? buf_units : 0;
+        lds = size_t(2 * a.buf_units) * 16;
     }
     const int64_t tiles = (A + int64_t(kNT) * apt - 1) / (int64_t(kNT) * apt);
     const dim3 grid(unsigned(tiles * G));
-    const bool pairs = pair_peak != nullptr, final_ = G == 1;
+    const bool pairs = pair_peak != nullptr;
     switch (apt) {
-        case 16: launch_apt<16>(prof, pairs, final_, policy, grid, lds, stream, a); break;
-        case 8: launch_apt<8>(prof, pairs, final_, policy, grid, lds, stream, a); break;
-        case 4: launch_apt<4>(prof, pairs, final_, policy, grid, lds, stream, a); break;
-        case 2: launch_apt<2>(prof, pairs, final_, policy, grid, lds, stream, a); break;
-        default: launch_apt<1>(prof, pairs, final_, policy, grid, lds, stream, a); break;
+        case 16: launch_apt<16>(prof, pairs, policy, grid, lds, stream, a); break;
+        case 8: launch_apt<8>(prof, pairs, policy, grid, lds, stream, a); break;
+        case 4: launch_apt<4>(prof, pairs, policy, grid, lds, stream, a); break;
+        case 2: launch_apt<2>(prof, pairs, policy, grid, lds, stream, a); break;
+        default: launch_apt<1>(prof, pairs, policy, grid, lds, stream, a); break;
     }
     MAPS_CHECK_LAUNCH();
-    if (!final_) {
-        const int64_t blocks = (A + 255) / 256;
-        hipLaunchKernelGGL(place_reduce, dim3(unsigned(blocks < 4096 ? blocks : 4096)), dim3(256), 0, stream, a);
-        MAPS_CHECK_LAUNCH();
-    }
+    const int64_t blocks = (A + 255) / 256;
+    hipLaunchKernelGGL(place_finish, dim3(unsigned(blocks < 4096 ? blocks : 4096)), dim3(256), 0, stream, a);
+    MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

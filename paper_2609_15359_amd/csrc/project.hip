@@ -31,19 +31,23 @@ struct LdsArrays {
     __device__ uint32_t& S(int64_t e) { return wsum[e]; }
     __device__ uint32_t& T(int64_t e) { return tau[e]; }
     __device__ uint32_t& M(int64_t e) { return pmx[e]; }
+    __device__ void events(uint32_t) {}
 };
 
 // The same arrays laid directly over the decoder's slice of the snapshot:
-// rank word {bits, before} and record {PMX, S, N, tau}.
+// rank word {bits, before}, hot record {PMX, tau -> T} and cold record {S, N}
+// (the cold records start once the event count is known).
 struct HbmArrays {
     uint32_t* rank;  // 2 words per rank entry
-    uint32_t* rec;   // 4 words per record
+    uint32_t* hot;   // 2 words per hot record
+    uint32_t* cold;  // 2 words per cold record
     __device__ uint32_t& B(int64_t w) { return rank[2 * w]; }
     __device__ uint32_t& P(int64_t w) { return rank[2 * w + 1]; }
-    __device__ uint32_t& C(int64_t e) { return rec[4 * e + 2]; }
-    __device__ uint32_t& S(int64_t e) { return rec[4 * e + 1]; }
-    __device__ uint32_t& T(int64_t e) { return rec[4 * e + 3]; }
-    __device__ uint32_t& M(int64_t e) { return rec[4 * e + 0]; }
+    __device__ uint32_t& M(int64_t e) { return hot[2 * e]; }
+    __device__ uint32_t& T(int64_t e) { return hot[2 * e + 1]; }
+    __device__ uint32_t& S(int64_t e) { return cold[2 * e]; }
+    __device__ uint32_t& C(int64_t e) { return cold[2 * e + 1]; }
+    __device__ void events(uint32_t E) { cold = hot + 2 * (int64_t(E) + 1); }
 };
 
 __device__ inline int64_t remaining(int32_t U, int32_t g) {
@@ -97,6 +101,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     const uint32_t E = block_scan<kNT, false, false, true, uint32_t>(
         W, 0u, [&](int64_t w) { return uint32_t(__popc(a.B(w))); },
         [&](int64_t w, uint32_t v) { a.P(w) = v; }, sc.red32);
+    a.events(E);
     phase<kInLds>();
 
     // 3. per-event counters
@@ -159,18 +164,28 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         phase<kInLds>();   // the HBM arrays are updated in place below
     }
 
-    // 6. write the snapshot slice
+    // 6. write the snapshot slice: hot records {PMX_e, T_e}, cold {S_e, N_e + 1}
     uint2* rank = reinterpret_cast<uint2*>(V.slices + slice_off);
-    int4* rec = V.slices + slice_off + W / 2;
+    int2* hot = reinterpret_cast<int2*>(V.slices + slice_off + W / 2);
+    int2* cold = hot + E + 1;
     if constexpr (kInLds) {
-        for (int64_t e = tid; e < E; e += kNT)
-            rec[e] = make_int4(int32_t(a.M(e)), int32_t(a.S(e)), int32_t(a.C(e) + 1u), int32_t(a.T(e)));
+        for (int64_t e = tid; e < E; e += kNT) {
+            const int32_t m = int32_t(a.M(e)), sv = int32_t(a.S(e));
+            const uint32_t n1 = a.C(e) + 1u;
+            hot[e] = make_int2(m, event_threshold(m, sv, n1));
+            cold[e] = make_int2(sv, int32_t(n1));
+        }
         for (int64_t w = tid; w < W; w += kNT) rank[w] = make_uint2(a.B(w), a.P(w));
     } else {
-        for (int64_t e = tid; e < E; e += kNT) a.C(e) += 1u;
+        for (int64_t e = tid; e < E; e += kNT) {   // in place: each thread owns its events
+            const uint32_t n1 = a.C(e) + 1u;
+            a.T(e) = uint32_t(event_threshold(int32_t(a.M(e)), int32_t(a.S(e)), n1));
+            a.C(e) = n1;
+        }
     }
     if (tid == 0) {
-        rec[E] = make_int4(pmx_end, 0, 1, INT32_MAX);
+        hot[E] = make_int2(pmx_end, event_threshold(pmx_end, 0, 1u));
+        cold[E] = make_int2(0, 1);
         DecHeader h;
         h.slice_off = slice_off;
         h.tot = tot;
@@ -217,7 +232,8 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
     } else {
         HbmArrays a;
         a.rank = reinterpret_cast<uint32_t*>(V.slices + slice_off);
-        a.rec = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
+        a.hot = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
+        a.cold = nullptr;
         project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
     }
 }
