@@ -1,18 +1,23 @@
 // Uncertainty-aware calibration (Sec. 3.2, Eqs. (2)-(4)) on gfx950.
 //
 // Per length bucket b the conformal quantile is the k_b-th smallest one-sided
-// score s = max(0, L - L_hat).  It is found by a most-significant-digit-first
-// radix select over the 32-bit scores, 8 bits per pass, all buckets at once:
-//   cal_score   scores + bucket ids (binary search of the edges in LDS),
-//               bucket sizes and the largest score;
-//   cal_rank    k_b = ceil((1 - alpha)(n_b + 1)) in integers;
-//   cal_hist    per pass: histogram of the current digit of the scores whose
-//               higher digits equal the bucket's selected prefix (LDS
-//               histograms flushed with atomics; passes above the largest
-//               score's top digit are skipped on the device);
-//   cal_select  per pass: the digit holding the k_b-th element, one wavefront
-//               per bucket (wavefront scan over 256 bins);
-//   cal_finish  q_b, n_b;  cal_apply  U = min(L_hat + q_b, u_max).
+// score s = max(0, L - L_hat), k_b = ceil((1 - alpha)(n_b + 1)) (infinite when
+// k_b > n_b); every bound is then U = min(L_hat + q_b, u_max).
+//
+// Up to 1,024 buckets: a counting sort by bucket, then one workgroup per
+// bucket selects in LDS.
+//   cal_count         scores' buckets (binary search of the edges in LDS):
+//                     per-workgroup bucket sizes and the largest score;
+//   cal_offsets       per bucket: exclusive scan of the workgroups' sizes, the
+//                     bucket size n_b, k_b, the largest score;
+//   cal_scatter       every score to its bucket's run, bucket-major;
+//   cal_bucket_select per bucket: most-significant-digit-first radix select
+//                     of the k_b-th score over its run, 8 bits a pass from the
+//                     top digit of the largest score, histograms in LDS;
+//   cal_apply         U = min(L_hat + q_b, u_max).
+// More buckets: the same select over all buckets at once, one histogram
+// pass and one selection kernel per 8-bit digit (cal_score, cal_rank,
+// cal_hist, cal_select, cal_finish), histograms in LDS for up to 128 buckets.
 // All reductions are integer additions, so the result is deterministic.
 #include "maps_internal.hpp"
 
@@ -243,6 +248,202 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
     }
 }
 
+// ---------------------------------------------------------------------------
+// Counting-sort path (nb <= kFastBuckets)
+// ---------------------------------------------------------------------------
+constexpr int kFastBuckets = 1024;
+constexpr int kSortNT = 256;
+constexpr int64_t kSortPerBlockMin = 2048;
+constexpr int64_t kSortMaxBlocks = 4096;
+constexpr int kSelNT = 1024;
+
+// Elements per workgroup of cal_count / cal_scatter (both cover the same
+// ranges) and the number of workgroups.
+struct SortPlan {
+    int64_t per_block;
+    int64_t blocks;
+};
+
+SortPlan sort_plan(int64_t n) {
+    SortPlan sp;
+    int64_t per = (n + kSortMaxBlocks - 1) / kSortMaxBlocks;
+    per = per < kSortPerBlockMin ? kSortPerBlockMin : per;
+    sp.per_block = (per + kSortNT - 1) / kSortNT * kSortNT;
+    sp.blocks = (n + sp.per_block - 1) / sp.per_block;
+    return sp;
+}
+
+struct FastWorkspace {
+    uint32_t* cnt_part;   // [blocks][nb] bucket sizes of each workgroup
+    uint32_t* off_part;   // [blocks][nb] where each workgroup's run starts inside the bucket
+    uint32_t* max_part;   // [blocks] largest score of each workgroup
+    uint32_t* bcount;     // [nb] bucket sizes
+    uint32_t* bmax;       // [nb] largest score (the same for every bucket)
+    int32_t* krank;       // [nb] k_b, -1 when the quantile is infinite
+    int32_t* sorted;      // [n] scores, bucket-major
+    size_t bytes;
+};
+
+FastWorkspace fast_carve(void* base, int64_t n, int32_t nb) {
+    const SortPlan sp = sort_plan(n);
+    FastWorkspace w;
+    size_t off = 0;
+    char* p = static_cast<char*>(base);
+    auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
+    w.cnt_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * nb * 4));
+    w.off_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * nb * 4));
+    w.max_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * 4));
+    w.bcount = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
+    w.bmax = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
+    w.krank = reinterpret_cast<int32_t*>(take(size_t(nb) * 4));
+    w.sorted = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
+    w.bytes = off;
+    return w;
+}
+
+// Score of one residual (Eq. (2)): max(0, L - L_hat), saturated at INT32_MAX.
+__device__ inline int32_t score_of(int32_t p, int32_t t) {
+    const int64_t d = int64_t(t) - p;
+    return d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
+}
+
+__global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__ pred,
+                                                     const int32_t* __restrict__ truth, int64_t n,
+                                                     const int32_t* __restrict__ edges, int nb, int64_t per_block,
+                                                     uint32_t* __restrict__ cnt_part, uint32_t* __restrict__ max_part,
+                                                     uint32_t* dev_err) {
+    extern __shared__ int32_t lds[];
+    __shared__ uint32_t red[kSortNT / kWave];
+    const int ne = nb - 1;
+    int32_t* le = lds;
+    uint32_t* lc = reinterpret_cast<uint32_t*>(lds + ne);
+    for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
+    for (int i = threadIdx.x; i < nb; i += kSortNT) lc[i] = 0;
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i + 1 < ne; i += kSortNT)
+            if (edges[i] > edges[i + 1]) raise_error(dev_err, MAPS_ERR_EDGES_UNSORTED);
+    __syncthreads();
+    const int64_t lo = int64_t(blockIdx.x) * per_block;
+    const int64_t hi = lo + per_block < n ? lo + per_block : n;
+    uint32_t mx = 0;
+    bool bad = false;
+#pragma unroll 4
+    for (int64_t i = lo + threadIdx.x; i < hi; i += kSortNT) {
+        const int32_t p = pred[i], t = truth[i];
+        bad |= (p < 0) | (t < 0);
+        const int32_t sc = score_of(p, t);
+        atomicAdd(&lc[bucket_of(le, ne, p)], 1u);
+        mx = mx > uint32_t(sc) ? mx : uint32_t(sc);
+    }
+    if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
+    mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the counts are complete
+    for (int b = threadIdx.x; b < nb; b += kSortNT) cnt_part[int64_t(blockIdx.x) * nb + b] = lc[b];
+    if (threadIdx.x == 0) max_part[blockIdx.x] = mx;
+}
+
+__global__ __launch_bounds__(kSortNT) void cal_offsets(int nb, int64_t blocks, int32_t alpha_ppm,
+                                                       const uint32_t* __restrict__ cnt_part,
+                                                       const uint32_t* __restrict__ max_part,
+                                                       uint32_t* __restrict__ off_part, uint32_t* __restrict__ bcount,
+                                                       uint32_t* __restrict__ bmax, int32_t* __restrict__ krank) {
+    __shared__ uint32_t tmp[kSortNT / kWave];
+    const int b = blockIdx.x;
+    const uint32_t total = block_scan<kSortNT, false, false, true, uint32_t>(
+        blocks, 0u, [&](int64_t i) { return cnt_part[i * nb + b]; },
+        [&](int64_t i, uint32_t v) { off_part[i * nb + b] = v; }, tmp);
+    uint32_t mx = 0;
+    for (int64_t i = threadIdx.x; i < blocks; i += kSortNT) mx = mx > max_part[i] ? mx : max_part[i];
+    mx = block_reduce_max<kSortNT>(mx, tmp);
+    if (threadIdx.x == 0) {
+        const int64_t nbk = total;
+        const int64_t k = (int64_t(1000000 - alpha_ppm) * (nbk + 1) + 999999) / 1000000;  // Eq. (3)
+        bcount[b] = total;
+        bmax[b] = mx;
+        krank[b] = k <= nbk ? int32_t(k) : -1;
+    }
+}
+
+__global__ __launch_bounds__(kSortNT) void cal_scatter(const int32_t* __restrict__ pred,
+                                                       const int32_t* __restrict__ truth, int64_t n,
+                                                       const int32_t* __restrict__ edges, int nb, int64_t per_block,
+                                                       const uint32_t* __restrict__ bcount,
+                                                       const uint32_t* __restrict__ off_part,
+                                                       int32_t* __restrict__ sorted) {
+    extern __shared__ int32_t lds[];
+    __shared__ uint32_t tmp[kSortNT / kWave];
+    const int ne = nb - 1;
+    int32_t* le = lds;
+    uint32_t* next = reinterpret_cast<uint32_t*>(lds + ne);
+    for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
+    // start of each bucket's run, then of this workgroup's part of it
+    block_scan<kSortNT, false, false, true, uint32_t>(
+        nb, 0u, [&](int64_t i) { return bcount[i]; }, [&](int64_t i, uint32_t v) { next[i] = v; }, tmp);
+    for (int b = threadIdx.x; b < nb; b += kSortNT) next[b] += off_part[int64_t(blockIdx.x) * nb + b];
+    __syncthreads();
+    const int64_t lo = int64_t(blockIdx.x) * per_block;
+    const int64_t hi = lo + per_block < n ? lo + per_block : n;
+#pragma unroll 4
+    for (int64_t i = lo + threadIdx.x; i < hi; i += kSortNT) {
+        const int32_t p = pred[i], t = truth[i];
+        const uint32_t pos = atomicAdd(&next[bucket_of(le, ne, p)], 1u);
+        if (pos < uint64_t(n)) sorted[pos] = score_of(p, t);   // always: the runs partition [0, n)
+    }
+}
+
+// One workgroup per bucket: the k_b-th smallest score of its run.
+__global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, const int32_t* __restrict__ sorted,
+                                                            const uint32_t* __restrict__ bcount,
+                                                            const uint32_t* __restrict__ bmax,
+                                                            const int32_t* __restrict__ krank,
+                                                            int32_t* __restrict__ q_out,
+                                                            int32_t* __restrict__ count_out) {
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t red[kSelNT / kWave];
+    __shared__ uint32_t pick[2];
+    const int b = blockIdx.x;
+    uint32_t before = 0;
+    for (int i = threadIdx.x; i < b; i += kSelNT) before += bcount[i];
+    const uint32_t base = block_reduce_add<kSelNT>(before, red);
+    const uint32_t nbk = bcount[b];
+    int32_t k = krank[b];
+    if (threadIdx.x == 0) count_out[b] = int32_t(nbk);
+    if (k < 0) {
+        if (threadIdx.x == 0) q_out[b] = MAPS_Q_INF;
+        return;
+    }
+    const uint32_t mx = bmax[b];
+    const int top = mx >> 24 ? 24 : (mx >> 16 ? 16 : (mx >> 8 ? 8 : 0));
+    const int32_t* v = sorted + base;
+    uint32_t prefix = 0;
+    for (int shift = top; shift >= 0; shift -= 8) {
+        if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+        __syncthreads();
+        for (uint32_t i = threadIdx.x; i < nbk; i += kSelNT) {
+            const uint32_t x = uint32_t(v[i]) >> shift;
+            if ((x >> 8) == prefix) atomicAdd(&hist[x & 255u], 1u);
+        }
+        __syncthreads();
+        if (threadIdx.x < kWave) {   // the digit holding the k-th element
+            const int lane = threadIdx.x;
+            uint32_t h[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) h[j] = hist[lane * 4 + j];
+            const uint32_t mine = h[0] + h[1] + h[2] + h[3];
+            uint32_t c = wave_incl_scan_add(mine) - mine;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (c < uint32_t(k) && c + h[j] >= uint32_t(k)) { pick[0] = uint32_t(lane * 4 + j); pick[1] = uint32_t(k) - c; }
+                c += h[j];
+            }
+        }
+        __syncthreads();
+        prefix = (prefix << 8) | pick[0];
+        k = int32_t(pick[1]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) q_out[b] = int32_t(prefix);
+}
+
 int grid_for(int64_t n, int nt, int per_thread, int cap) {
     int64_t g = (n + int64_t(nt) * per_thread - 1) / (int64_t(nt) * per_thread);
     if (g < 1) g = 1;
@@ -257,22 +458,46 @@ using namespace maps;
 
 extern "C" size_t maps_calibrate_workspace_size(int64_t n, int32_t nb) {
     if (n < 0 || nb < 1) return 0;
-    return cal_carve(nullptr, n, nb).bytes;
+    return nb <= kFastBuckets ? fast_carve(nullptr, n, nb).bytes : cal_carve(nullptr, n, nb).bytes;
 }
 
-extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
-                                      const int32_t* edges, int32_t nb, int32_t alpha_ppm,
-                                      int32_t* q_out, int32_t* count_out,
-                                      const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
-                                      uint32_t* dev_err, void* workspace, size_t workspace_bytes,
-                                      hipStream_t stream) {
-    if (n < 0 || m < 0 || nb < 1 || nb > 65536 || u_max < 0) return MAPS_E_SIZE;
-    if (alpha_ppm <= 0 || alpha_ppm >= 1000000) return MAPS_E_ALPHA;
-    if (!q_out || !count_out || !dev_err || (n > 0 && (!pred || !truth)) || (nb > 1 && !edges) ||
-        (m > 0 && (!apply_pred || !U_out)) || !workspace)
-        return MAPS_E_NULL;
+namespace {
+
+// Calibration for up to kFastBuckets buckets (counting sort, then one
+// workgroup per bucket).
+maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges, int32_t nb,
+                           int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
+                           void* workspace, hipStream_t stream) {
+    const FastWorkspace w = fast_carve(workspace, n, nb);
+    const SortPlan sp = sort_plan(n);
+    const size_t lds = size_t(2 * nb) * 4;   // edges and per-bucket counters
+    if (n > 0) {
+        hipLaunchKernelGGL(cal_count, dim3(unsigned(sp.blocks)), dim3(kSortNT), lds, stream, pred, truth, n, edges,
+                           nb, sp.per_block, w.cnt_part, w.max_part, dev_err);
+        MAPS_CHECK_LAUNCH();
+    }
+    hipLaunchKernelGGL(cal_offsets, dim3(unsigned(nb)), dim3(kSortNT), 0, stream, nb, sp.blocks, alpha_ppm,
+                       w.cnt_part, w.max_part, w.off_part, w.bcount, w.bmax, w.krank);
+    MAPS_CHECK_LAUNCH();
+    if (n > 0) {
+        hipLaunchKernelGGL(cal_scatter, dim3(unsigned(sp.blocks)), dim3(kSortNT), lds, stream, pred, truth, n,
+                           edges, nb, sp.per_block, w.bcount, w.off_part, w.sorted);
+        MAPS_CHECK_LAUNCH();
+    }
+    hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), 0, stream, nb, w.sorted, w.bcount,
+                       w.bmax, w.krank, q_out, count_out);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+}  // namespace
+
+namespace {
+
+maps_status calibrate_general(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges,
+                              int32_t nb, int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
+                              void* workspace, hipStream_t stream) {
     CalWorkspace w = cal_carve(workspace, n, nb);
-    if (workspace_bytes < w.bytes) return MAPS_E_WORKSPACE;
 
     const bool lds_edges = nb <= kLdsEdgesMax;
     const bool lds_hist = nb <= kLdsHistBuckets;
@@ -314,7 +539,35 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     hipLaunchKernelGGL(cal_finish, dim3((nb + kNT - 1) / kNT), dim3(kNT), 0, stream,
                        nb, w.krem, w.prefix, w.cnt, q_out, count_out);
     MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+}  // namespace
+
+extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
+                                      const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                                      int32_t* q_out, int32_t* count_out,
+                                      const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
+                                      uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+    if (n < 0 || m < 0 || nb < 1 || nb > 65536 || u_max < 0) return MAPS_E_SIZE;
+    if (alpha_ppm <= 0 || alpha_ppm >= 1000000) return MAPS_E_ALPHA;
+    if (!q_out || !count_out || !dev_err || (n > 0 && (!pred || !truth)) || (nb > 1 && !edges) ||
+        (m > 0 && (!apply_pred || !U_out)) || !workspace)
+        return MAPS_E_NULL;
+    if (workspace_bytes < maps_calibrate_workspace_size(n, nb)) return MAPS_E_WORKSPACE;
+    const int ne = nb - 1;
+    if (nb <= kFastBuckets) {
+        const maps_status st =
+            calibrate_fast(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, dev_err, workspace, stream);
+        if (st != MAPS_OK) return st;
+    } else {
+        const maps_status st =
+            calibrate_general(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, dev_err, workspace, stream);
+        if (st != MAPS_OK) return st;
+    }
     if (m > 0) {
+        const bool lds_edges = nb <= kLdsEdgesMax;
         const int g = grid_for(m, kNT, 8, 4096);
         if (lds_edges)
             hipLaunchKernelGGL(cal_apply<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
@@ -326,3 +579,5 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     }
     return MAPS_OK;
 }
+
+

@@ -61,7 +61,10 @@ def test_size_queries(lib):
     assert lib.maps_snapshot_bytes(0, n, u_max) == 0
     assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 63) == 0
     assert lib.maps_snapshot_bytes(D, n, (1 << 24) - 64) > 0
-    assert lib.maps_calibrate_workspace_size(1000, 4) >= 1000 * 6
+    # scores in bucket order (4 B per residual) up to 1,024 buckets, scores and
+    # bucket ids (6 B per residual) beyond
+    assert lib.maps_calibrate_workspace_size(1000, 4) >= 1000 * 4
+    assert lib.maps_calibrate_workspace_size(1000, 2000) >= 1000 * 6
     assert lib.maps_place_workspace_size(256, 262144, 32768) >= 262144 * 12
     assert lib.maps_project_workspace_size(4, 100, 8192) == 0
     assert lib.maps_local_order_workspace_size(4, 100) == 0
