@@ -104,6 +104,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, help="run only a plain copy of this many bytes")
+    ap.add_argument("--graph", action="store_true", help="replay one HIP graph per phase instead of "
+                                                         "launching every kernel from the host")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (--gpus {args.gpus} requested); "
@@ -124,41 +126,35 @@ def main():
     D, A = b.decoders, b.arrivals
     db = pipeline.to_device(b)
     ws = pipeline.Workspaces(db, want_pairs=True)
-    stream = torch.cuda.current_stream()
-
-    def one_step(ev=None):
-        err = ws.dev_err
-        if ev:
-            ev[0].record(stream)
-        q, cnt, U, _ = maps.calibrate(db.cal_pred, db.cal_truth, db.edges, db.alpha_ppm, db.apply_pred,
-                                      db.u_max, dev_err=err, workspace=ws.cal, out=ws.out)
-        if ev:
-            ev[1].record(stream)
-        nr, na = db.n_res, db.n_arr
-        snap, base, _ = maps.project(db.seg_off, db.res_prompt, db.res_gen, U[:nr], db.u_max,
-                                     snapshot=ws.snapshot, dev_err=err, base_peak=ws.base_peak)
-        if ev:
-            ev[2].record(stream)
-        maps.place(snap, db.capacity, db.queue_len, db.arr_prompt, U[nr:nr + na],
-                   workspace=ws.place, out=ws.placement)
-        if ev:
-            ev[3].record(stream)
-        maps.local_order(snap, db.capacity, db.q_off, db.q_prompt, U[nr + na:], db.q_wait_ms,
-                         db.max_wait_ms, dev_err=err, order=ws.order, admitted=ws.admitted)
-        if ev:
-            ev[4].record(stream)
-        return snap
+    phases = pipeline.step_phases(db, ws)
 
     ws.dev_err.zero_()
+    for fn in phases:   # one eager step: the reference for the replayed graphs
+        fn()
+    eager = (ws.placement.choice.clone(), ws.placement.pair_peak.sum(dtype=torch.int64), ws.order.clone())
+    graphs = pipeline.StepGraphs(db, ws) if args.graph else None
+
+    def one_step(ev=None):
+        if graphs is not None:
+            graphs.replay(ev)
+            return
+        for i, fn in enumerate(phases):
+            if ev:
+                ev[i].record()
+            fn()
+        if ev:
+            ev[-1].record()
+
     for _ in range(args.warmup):
-        snap = one_step()
+        one_step()
     torch.cuda.synchronize()
     bits = int(ws.dev_err.item()) & 0xFFFFFFFF
     if bits:
         raise SystemExit(f"device value errors: {maps.error_names(bits)}")
 
     # timed region: exactly K steps, bracketed by synchronization
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(pipeline.PHASES) + 1)]
+              for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -166,8 +162,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
+    if not (torch.equal(eager[0], ws.placement.choice) and torch.equal(eager[2], ws.order)
+            and int(eager[1]) == int(ws.placement.pair_peak.sum(dtype=torch.int64))):
+        raise SystemExit("replayed steps differ from the eager step")
     parts = {name: statistics.median(ev[i].elapsed_time(ev[i + 1]) for ev in events)
-             for i, name in enumerate(("calibrate", "project", "place", "local_order"))}
+             for i, name in enumerate(pipeline.PHASES)}
     place_ms = statistics.mean(ev[2].elapsed_time(ev[3]) for ev in events)
 
     # algorithmic bytes of the placement pass, from the snapshot's own event counts

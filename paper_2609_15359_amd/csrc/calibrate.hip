@@ -66,6 +66,23 @@ __device__ inline int bucket_of(const int32_t* edges, int ne, int32_t v) {
     return lo;
 }
 
+// bucket_of for kJ values at once, the searches interleaved (binary lifting
+// over the sorted edges: the same count of edges <= v).
+template <int kJ>
+__device__ inline void buckets_of(const int32_t* edges, int ne, const int32_t (&v)[kJ], int (&b)[kJ]) {
+    int step = 1;
+    while (step * 2 <= ne) step *= 2;
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) b[j] = 0;
+    for (; step > 0; step >>= 1) {
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            const int np = b[j] + step;
+            if (np <= ne && edges[np - 1] <= v[j]) b[j] = np;
+        }
+    }
+}
+
 __global__ void cal_init(int nb, uint32_t* cnt, uint32_t* hist, uint32_t* maxs) {
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < int64_t(nb) * 256; i += stride) {
@@ -233,18 +250,29 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
         e = le;
         qq = lq;
     }
-    const int64_t stride = int64_t(gridDim.x) * kNT;
-    for (int64_t i = int64_t(blockIdx.x) * kNT + threadIdx.x; i < m; i += stride) {
-        int32_t p = pred[i];
-        int32_t out;
-        if (p < 0) {
-            out = -1;  // no prediction: no bound
-        } else {
-            int32_t qb = qq[bucket_of(e, ne, p)];
-            int64_t v = int64_t(p) + qb;  // Eq. (4)
-            out = (qb == MAPS_Q_INF || v > u_max) ? u_max : int32_t(v);
+    constexpr int kA = 8;   // predictions per thread in flight
+    const int64_t stride = int64_t(gridDim.x) * kNT * kA;
+    for (int64_t c0 = int64_t(blockIdx.x) * kNT * kA; c0 < m; c0 += stride) {
+        int32_t p[kA];
+        int b[kA];
+#pragma unroll
+        for (int j = 0; j < kA; ++j) {
+            const int64_t i = c0 + int64_t(j) * kNT + threadIdx.x;
+            p[j] = i < m ? pred[i] : -1;
         }
-        U[i] = out;
+        buckets_of<kA>(e, ne, p, b);
+#pragma unroll
+        for (int j = 0; j < kA; ++j) {
+            const int64_t i = c0 + int64_t(j) * kNT + threadIdx.x;
+            if (i >= m) continue;
+            int32_t out = -1;   // no prediction: no bound
+            if (p[j] >= 0) {
+                const int32_t qb = qq[b[j]];
+                const int64_t v = int64_t(p[j]) + qb;   // Eq. (4)
+                out = (qb == MAPS_Q_INF || v > u_max) ? u_max : int32_t(v);
+            }
+            U[i] = out;
+        }
     }
 }
 
@@ -307,6 +335,8 @@ __device__ inline int32_t score_of(int32_t p, int32_t t) {
     return d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
 }
 
+constexpr int kJ = 8;   // residuals per thread in flight
+
 __global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__ pred,
                                                      const int32_t* __restrict__ truth, int64_t n,
                                                      const int32_t* __restrict__ edges, int nb, int64_t per_block,
@@ -327,13 +357,24 @@ __global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__
     const int64_t hi = lo + per_block < n ? lo + per_block : n;
     uint32_t mx = 0;
     bool bad = false;
-#pragma unroll 4
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kSortNT) {
-        const int32_t p = pred[i], t = truth[i];
-        bad |= (p < 0) | (t < 0);
-        const int32_t sc = score_of(p, t);
-        atomicAdd(&lc[bucket_of(le, ne, p)], 1u);
-        mx = mx > uint32_t(sc) ? mx : uint32_t(sc);
+    for (int64_t c0 = lo; c0 < hi; c0 += int64_t(kSortNT) * kJ) {
+        int32_t p[kJ], t[kJ];
+        int b[kJ];
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            const int64_t i = c0 + int64_t(j) * kSortNT + threadIdx.x;
+            p[j] = i < hi ? pred[i] : 0;
+            t[j] = i < hi ? truth[i] : 0;
+        }
+        buckets_of<kJ>(le, ne, p, b);
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            if (c0 + int64_t(j) * kSortNT + threadIdx.x >= hi) continue;
+            bad |= (p[j] < 0) | (t[j] < 0);
+            atomicAdd(&lc[b[j]], 1u);
+            const uint32_t sc = uint32_t(score_of(p[j], t[j]));
+            mx = mx > sc ? mx : sc;
+        }
     }
     if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
     mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the counts are complete
@@ -382,11 +423,22 @@ __global__ __launch_bounds__(kSortNT) void cal_scatter(const int32_t* __restrict
     __syncthreads();
     const int64_t lo = int64_t(blockIdx.x) * per_block;
     const int64_t hi = lo + per_block < n ? lo + per_block : n;
-#pragma unroll 4
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kSortNT) {
-        const int32_t p = pred[i], t = truth[i];
-        const uint32_t pos = atomicAdd(&next[bucket_of(le, ne, p)], 1u);
-        if (pos < uint64_t(n)) sorted[pos] = score_of(p, t);   // always: the runs partition [0, n)
+    for (int64_t c0 = lo; c0 < hi; c0 += int64_t(kSortNT) * kJ) {
+        int32_t p[kJ], t[kJ];
+        int b[kJ];
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            const int64_t i = c0 + int64_t(j) * kSortNT + threadIdx.x;
+            p[j] = i < hi ? pred[i] : 0;
+            t[j] = i < hi ? truth[i] : 0;
+        }
+        buckets_of<kJ>(le, ne, p, b);
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            if (c0 + int64_t(j) * kSortNT + threadIdx.x >= hi) continue;
+            const uint32_t pos = atomicAdd(&next[b[j]], 1u);
+            if (pos < uint64_t(n)) sorted[pos] = score_of(p[j], t[j]);   // always: the runs partition [0, n)
+        }
     }
 }
 
@@ -415,12 +467,29 @@ __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, const int32_
     const int top = mx >> 24 ? 24 : (mx >> 16 ? 16 : (mx >> 8 ? 8 : 0));
     const int32_t* v = sorted + base;
     uint32_t prefix = 0;
+    const int lane = threadIdx.x % kWave;
     for (int shift = top; shift >= 0; shift -= 8) {
         if (threadIdx.x < 256) hist[threadIdx.x] = 0;
         __syncthreads();
-        for (uint32_t i = threadIdx.x; i < nbk; i += kSelNT) {
-            const uint32_t x = uint32_t(v[i]) >> shift;
-            if ((x >> 8) == prefix) atomicAdd(&hist[x & 255u], 1u);
+        for (uint32_t c0 = 0; c0 < nbk; c0 += kSelNT * kJ) {
+            uint32_t x[kJ];
+#pragma unroll
+            for (int j = 0; j < kJ; ++j) {
+                const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
+                x[j] = i < nbk ? uint32_t(v[i]) >> shift : 0xFFFFFFFFu;
+            }
+#pragma unroll
+            for (int j = 0; j < kJ; ++j) {
+                const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
+                if (i < nbk && (x[j] >> 8) == prefix) {
+                    // lanes holding the first such lane's digit add it with one atomic
+                    const uint32_t digit = x[j] & 255u;
+                    const uint32_t lead = __builtin_amdgcn_readfirstlane(digit);
+                    const uint64_t same = __ballot(digit == lead);
+                    if (digit != lead) atomicAdd(&hist[digit], 1u);
+                    else if (lane == __ffsll((unsigned long long)same) - 1) atomicAdd(&hist[lead], uint32_t(__popcll(same)));
+                }
+            }
         }
         __syncthreads();
         if (threadIdx.x < kWave) {   // the digit holding the k-th element
@@ -568,7 +637,7 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     }
     if (m > 0) {
         const bool lds_edges = nb <= kLdsEdgesMax;
-        const int g = grid_for(m, kNT, 8, 4096);
+        const int g = grid_for(m, kNT, 8, 8192);
         if (lds_edges)
             hipLaunchKernelGGL(cal_apply<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
                                apply_pred, m, edges, nb, q_out, u_max, U_out);

@@ -271,11 +271,16 @@ __device__ inline T block_scan(int64_t len, T identity, Get get, Put put, T* tmp
 }
 
 // Host: let a kernel use `bytes` of dynamic LDS (gfx950 has 160 KB per CU).
+// Each kernel's attribute is set once per process, so that calls made while
+// a stream is being captured into a graph issue no attribute change.
+void allow_dynamic_lds_fn(const void* fn, size_t bytes);
 template <typename Kernel>
 inline void allow_dynamic_lds(Kernel* fn, size_t bytes) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              int(bytes));
+    allow_dynamic_lds_fn(reinterpret_cast<const void*>(fn), bytes);
 }
+
+// Host: compute units of the current device, queried once per device.
+int device_compute_units();
 
 }  // namespace maps
 

@@ -613,15 +613,6 @@ PlaceWorkspace place_carve(void* base, int64_t A) {
     return w;
 }
 
-int compute_units() {
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
-    }
-    return cus;
-}
-
 }  // namespace
 }  // namespace maps
 
@@ -650,7 +641,7 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
     const SnapLayout L = snap_layout(D, 0, u_max);   // region offsets do not depend on the resident count
     const bool prof = L.P > 0;
     int apt = 8, G = 1;
-    plan(D, A, compute_units(), prof ? 8 : 16, &apt, &G);
+    plan(D, A, device_compute_units(), prof ? 8 : 16, &apt, &G);
     PlaceArgs a{};
     a.L = L;
     a.snap = snapshot;

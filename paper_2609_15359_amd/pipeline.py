@@ -104,20 +104,80 @@ class Workspaces:
         self.admitted = torch.empty(D, dtype=torch.int32, device=dev)
 
 
+PHASES = ("calibrate", "project", "place", "local_order")
+
+
+def step_phases(db: DeviceBatch, ws: Workspaces, want_pairs: bool = True, capacity=None,
+                policy: int = POLICY_MQ, rr_offset: int = 0):
+    """The step as one callable per phase (PHASES order).  Each enqueues its
+    library calls on the current stream and writes only into `ws`, so a phase
+    can also be captured into a graph and replayed."""
+    cap = db.capacity if capacity is None else capacity
+    err = ws.dev_err
+    nr, na = db.n_res, db.n_arr
+    U = ws.out["U"]
+    snap = Snapshot(data=ws.snapshot, D=db.decoders, n_total=nr, u_max=db.u_max)
+
+    def cal():
+        calibrate(db.cal_pred, db.cal_truth, db.edges, db.alpha_ppm, db.apply_pred, db.u_max,
+                  dev_err=err, workspace=ws.cal, out=ws.out)
+
+    def proj():
+        project(db.seg_off, db.res_prompt, db.res_gen, U[:nr], db.u_max, snapshot=ws.snapshot, dev_err=err,
+                base_peak=ws.base_peak)
+
+    def pla():
+        place(snap, cap, db.queue_len, db.arr_prompt, U[nr:nr + na], policy=policy, rr_offset=rr_offset,
+              want_pairs=want_pairs, workspace=ws.place, out=ws.placement)
+
+    def loc():
+        local_order(snap, cap, db.q_off, db.q_prompt, U[nr + na:], db.q_wait_ms, db.max_wait_ms, dev_err=err,
+                    order=ws.order, admitted=ws.admitted)
+
+    return [cal, proj, pla, loc]
+
+
+def outputs(db: DeviceBatch, ws: Workspaces) -> StepOutputs:
+    """The step's results as they stand in `ws`."""
+    return StepOutputs(q=ws.out["q"], count=ws.out["count"], U=ws.out["U"],
+                       snapshot=Snapshot(data=ws.snapshot, D=db.decoders, n_total=db.n_res, u_max=db.u_max),
+                       base_peak=ws.base_peak, placement=ws.placement, order=ws.order, admitted=ws.admitted,
+                       dev_err=ws.dev_err)
+
+
 def step(db: DeviceBatch, ws: Workspaces | None = None, want_pairs: bool = True, capacity=None,
          policy: int = POLICY_MQ, rr_offset: int = 0) -> StepOutputs:
     """Enqueue the whole hot path for one batch on the current stream."""
     ws = ws or Workspaces(db, want_pairs)
-    cap = db.capacity if capacity is None else capacity
-    err = ws.dev_err
-    q, cnt, U, _ = calibrate(db.cal_pred, db.cal_truth, db.edges, db.alpha_ppm, db.apply_pred, db.u_max,
-                             dev_err=err, workspace=ws.cal, out=ws.out)
-    nr, na = db.n_res, db.n_arr
-    snap, base, _ = project(db.seg_off, db.res_prompt, db.res_gen, U[:nr], db.u_max,
-                            snapshot=ws.snapshot, dev_err=err, base_peak=ws.base_peak)
-    pl = place(snap, cap, db.queue_len, db.arr_prompt, U[nr:nr + na], policy=policy, rr_offset=rr_offset,
-               want_pairs=want_pairs, workspace=ws.place, out=ws.placement)
-    order, admitted, _ = local_order(snap, cap, db.q_off, db.q_prompt, U[nr + na:], db.q_wait_ms,
-                                     db.max_wait_ms, dev_err=err, order=ws.order, admitted=ws.admitted)
-    return StepOutputs(q=q, count=cnt, U=U, snapshot=snap, base_peak=base, placement=pl, order=order,
-                       admitted=admitted, dev_err=err)
+    for fn in step_phases(db, ws, want_pairs, capacity, policy, rr_offset):
+        fn()
+    return outputs(db, ws)
+
+
+class StepGraphs:
+    """The step captured as one HIP graph per phase, then replayed on the
+    current stream.  The phases run once eagerly first, so that every kernel
+    attribute is set before capture; all buffers live in `ws`."""
+
+    def __init__(self, db: DeviceBatch, ws: Workspaces, **kw):
+        phases = step_phases(db, ws, **kw)
+        for fn in phases:
+            fn()
+        torch.cuda.synchronize()
+        self.graphs = []
+        for fn in phases:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                fn()
+            self.graphs.append(g)
+        torch.cuda.synchronize()
+
+    def replay(self, events=None):
+        """One step; with events (len(PHASES) + 1 of them), the phase
+        boundaries are recorded on the current stream."""
+        for i, g in enumerate(self.graphs):
+            if events is not None:
+                events[i].record()
+            g.replay()
+        if events is not None:
+            events[-1].record()
