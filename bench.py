@@ -193,7 +193,8 @@ def main():
         "config": {"workload": f"{b.workload.name}: {workload.describe(b.workload)}; "
                                f"capacities {list(b.workload.capacities)} tokens, alpha_ppm {b.alpha_ppm}, "
                                f"u_max {b.u_max}; per-pair peak matrix written",
-                   "decoders": D, "arrivals": A, "pairs": D * A},
+                   "decoders": D, "arrivals": A, "pairs": D * A,
+                   "launch": "one HIP graph per phase" if args.graph else "host launches"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
                      "kernel": "maps_place (place_records + place_finish)",
