@@ -44,6 +44,9 @@ CAL_CASES = {
     "wide_scores_4_passes": dict(n=20000, nb=16, alpha=100000, wide=True),
     "many_buckets_global_hist": dict(n=50000, nb=200, alpha=100000),
     "very_many_buckets_global_edges": dict(n=60000, nb=9000, alpha=200000),
+    "buckets_1024_sorted_path": dict(n=40000, nb=1024, alpha=100000),
+    "buckets_1025_all_bucket_path": dict(n=40000, nb=1025, alpha=100000),
+    "one_bucket_holds_most": dict(n=120000, nb=8, alpha=50000, skew=True),
     "alpha_1ppm": dict(n=4000, nb=4, alpha=1),
     "alpha_999999ppm": dict(n=4000, nb=4, alpha=999999),
     "duplicate_edges": dict(n=4000, nb=6, alpha=100000, dup=True),
@@ -66,6 +69,8 @@ def test_calibrate_cases(orc, case):
     edges = np.sort(rng.integers(0, 5000, size=nb - 1)).astype(np.int32)
     if c.get("dup"):
         edges = np.array([100, 100, 100, 2000, 9000][: nb - 1], np.int32)
+    if c.get("skew"):
+        edges = np.array([4000, 4100, 4200, 4300, 4400, 4500, 4600], np.int32)[: nb - 1]
     u_max = 65536
     ap = np.concatenate([rng.integers(-3, 10**6, size=3000), [-1, 0, 1, 2**31 - 1]]).astype(np.int32)
     say(f"[edge] calibrate {case}: n={n} nb={nb}")
@@ -151,6 +156,32 @@ def test_record_path(orc, policy, want_pairs):
     gg = gpu_step(b, capacity=cap, policy=policy, want_pairs=want_pairs)
     assert gg["err"] == 0, gg["errors"]
     compare_all(gg, o, pairs=want_pairs)
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_record_path_growing_occupancy(orc, policy):
+    """Residents with long remaining lengths and small prompts: the occupancy
+    grows until the first event, so for short bounds the line S + U (N + 1)
+    exceeds the running maximum and placement must read the cold records."""
+    rng = np.random.default_rng(91 + policy)
+    D, u_max, A = 5, 20000, 4000
+    counts = [3, 40, 1, 200, 0]
+    seg = np.zeros(D + 1, np.int64)
+    seg[1:] = np.cumsum(counts)
+    n = int(seg[-1])
+    p = rng.integers(0, 20, size=n).astype(np.int32)
+    g = rng.integers(0, 5, size=n).astype(np.int32)
+    pred = rng.integers(5000, u_max, size=n).astype(np.int32)
+    arr = rng.integers(-1, 9000, size=A).astype(np.int32)
+    b = custom_batch(cal_pred=[5], cal_truth=[5], edges=[], alpha_ppm=100000, u_max=u_max, seg_off=seg,
+                     res_prompt=p, res_gen=g, res_pred=pred, arr_prompt=rng.integers(0, 500, size=A),
+                     arr_pred=arr, capacity=rng.integers(0, 60000, size=D), queue_len=[2, 0, 1, 3, 0])
+    b.cal_pred = np.arange(1, 21, dtype=np.int32)
+    b.cal_truth = b.cal_pred.copy()
+    o = oracle_step(b, policy=policy, o=orc)
+    gg = gpu_step(b, policy=policy)
+    assert gg["err"] == 0, gg["errors"]
+    compare_all(gg, o)
 
 
 def test_capacity_boundary_and_ties(orc):
