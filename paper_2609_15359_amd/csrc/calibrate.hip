@@ -4,16 +4,18 @@
 // score s = max(0, L - L_hat), k_b = ceil((1 - alpha)(n_b + 1)) (infinite when
 // k_b > n_b); every bound is then U = min(L_hat + q_b, u_max).
 //
-// Up to 1,024 buckets: a counting sort by bucket, then one workgroup per
-// bucket selects in LDS.
+// Up to 1,024 buckets (and 8.4M residuals): a counting sort by bucket, then
+// one workgroup per bucket selects.
 //   cal_count         scores' buckets (binary search of the edges in LDS):
 //                     per-workgroup bucket sizes and the largest score;
 //   cal_offsets       per bucket: exclusive scan of the workgroups' sizes, the
 //                     bucket size n_b, k_b, the largest score;
-//   cal_scatter       every score to its bucket's run, bucket-major;
+//   cal_scatter       each workgroup sorts its scores by bucket in LDS and
+//                     writes every run to its place, bucket-major;
 //   cal_bucket_select per bucket: most-significant-digit-first radix select
-//                     of the k_b-th score over its run, 8 bits a pass from the
-//                     top digit of the largest score, histograms in LDS;
+//                     of the k_b-th score over its run (kept in registers),
+//                     8 bits a pass from the top digit of the largest score,
+//                     histograms in LDS;
 //   cal_apply         U = min(L_hat + q_b, u_max).
 // More buckets: the same select over all buckets at once, one histogram
 // pass and one selection kernel per 8-bit digit (cal_score, cal_rank,
@@ -281,29 +283,17 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
 // ---------------------------------------------------------------------------
 constexpr int kFastBuckets = 1024;
 constexpr int kSortNT = 256;
-constexpr int64_t kSortPerBlockMin = 2048;
-constexpr int64_t kSortMaxBlocks = 4096;
+constexpr int kJ = 8;                                   // residuals per thread
+constexpr int64_t kPerBlock = int64_t(kSortNT) * kJ;    // residuals per workgroup of cal_count / cal_scatter
+constexpr int64_t kSortMaxBlocks = 4096;                // larger sets take the all-bucket path
 constexpr int kSelNT = 1024;
+constexpr int kKeep = 24;   // scores per thread the bucket select keeps in registers across passes
 
-// Elements per workgroup of cal_count / cal_scatter (both cover the same
-// ranges) and the number of workgroups.
-struct SortPlan {
-    int64_t per_block;
-    int64_t blocks;
-};
-
-SortPlan sort_plan(int64_t n) {
-    SortPlan sp;
-    int64_t per = (n + kSortMaxBlocks - 1) / kSortMaxBlocks;
-    per = per < kSortPerBlockMin ? kSortPerBlockMin : per;
-    sp.per_block = (per + kSortNT - 1) / kSortNT * kSortNT;
-    sp.blocks = (n + sp.per_block - 1) / sp.per_block;
-    return sp;
-}
+int64_t sort_blocks(int64_t n) { return (n + kPerBlock - 1) / kPerBlock; }
 
 struct FastWorkspace {
-    uint32_t* cnt_part;   // [blocks][nb] bucket sizes of each workgroup
-    uint32_t* off_part;   // [blocks][nb] where each workgroup's run starts inside the bucket
+    uint32_t* cnt_part;   // [nb][blocks] bucket sizes of each workgroup
+    uint32_t* off_part;   // [nb][blocks] where each workgroup's run starts inside the bucket
     uint32_t* max_part;   // [blocks] largest score of each workgroup
     uint32_t* bcount;     // [nb] bucket sizes
     uint32_t* bmax;       // [nb] largest score (the same for every bucket)
@@ -313,14 +303,14 @@ struct FastWorkspace {
 };
 
 FastWorkspace fast_carve(void* base, int64_t n, int32_t nb) {
-    const SortPlan sp = sort_plan(n);
+    const int64_t blocks = sort_blocks(n);
     FastWorkspace w;
     size_t off = 0;
     char* p = static_cast<char*>(base);
     auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
-    w.cnt_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * nb * 4));
-    w.off_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * nb * 4));
-    w.max_part = reinterpret_cast<uint32_t*>(take(size_t(sp.blocks) * 4));
+    w.cnt_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * nb * 4));
+    w.off_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * nb * 4));
+    w.max_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * 4));
     w.bcount = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
     w.bmax = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
     w.krank = reinterpret_cast<int32_t*>(take(size_t(nb) * 4));
@@ -329,17 +319,44 @@ FastWorkspace fast_carve(void* base, int64_t n, int32_t nb) {
     return w;
 }
 
+bool fast_path(int64_t n, int32_t nb) { return nb <= kFastBuckets && sort_blocks(n) <= kSortMaxBlocks; }
+
 // Score of one residual (Eq. (2)): max(0, L - L_hat), saturated at INT32_MAX.
 __device__ inline int32_t score_of(int32_t p, int32_t t) {
     const int64_t d = int64_t(t) - p;
     return d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
 }
 
-constexpr int kJ = 8;   // residuals per thread in flight
+// The kJ residuals of this thread in workgroup blockIdx.x: prompt
+// prediction, score, bucket; `valid` masks the ones past n.
+struct Residuals {
+    int32_t p[kJ], s[kJ];
+    int b[kJ];
+    bool valid[kJ];
+};
+
+__device__ inline void load_residuals(const int32_t* __restrict__ pred, const int32_t* __restrict__ truth, int64_t n,
+                                      const int32_t* le, int ne, Residuals& r, bool& bad) {
+    const int64_t lo = int64_t(blockIdx.x) * kPerBlock;
+    int32_t t[kJ];
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) {
+        const int64_t i = lo + int64_t(j) * kSortNT + threadIdx.x;
+        r.valid[j] = i < n;
+        r.p[j] = r.valid[j] ? pred[i] : 0;
+        t[j] = r.valid[j] ? truth[i] : 0;
+    }
+    buckets_of<kJ>(le, ne, r.p, r.b);
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) {
+        bad |= r.valid[j] & ((r.p[j] < 0) | (t[j] < 0));
+        r.s[j] = score_of(r.p[j], t[j]);
+    }
+}
 
 __global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__ pred,
                                                      const int32_t* __restrict__ truth, int64_t n,
-                                                     const int32_t* __restrict__ edges, int nb, int64_t per_block,
+                                                     const int32_t* __restrict__ edges, int nb, int64_t blocks,
                                                      uint32_t* __restrict__ cnt_part, uint32_t* __restrict__ max_part,
                                                      uint32_t* dev_err) {
     extern __shared__ int32_t lds[];
@@ -353,32 +370,19 @@ __global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__
         for (int i = threadIdx.x; i + 1 < ne; i += kSortNT)
             if (edges[i] > edges[i + 1]) raise_error(dev_err, MAPS_ERR_EDGES_UNSORTED);
     __syncthreads();
-    const int64_t lo = int64_t(blockIdx.x) * per_block;
-    const int64_t hi = lo + per_block < n ? lo + per_block : n;
-    uint32_t mx = 0;
+    Residuals r;
     bool bad = false;
-    for (int64_t c0 = lo; c0 < hi; c0 += int64_t(kSortNT) * kJ) {
-        int32_t p[kJ], t[kJ];
-        int b[kJ];
+    load_residuals(pred, truth, n, le, ne, r, bad);
+    uint32_t mx = 0;
 #pragma unroll
-        for (int j = 0; j < kJ; ++j) {
-            const int64_t i = c0 + int64_t(j) * kSortNT + threadIdx.x;
-            p[j] = i < hi ? pred[i] : 0;
-            t[j] = i < hi ? truth[i] : 0;
-        }
-        buckets_of<kJ>(le, ne, p, b);
-#pragma unroll
-        for (int j = 0; j < kJ; ++j) {
-            if (c0 + int64_t(j) * kSortNT + threadIdx.x >= hi) continue;
-            bad |= (p[j] < 0) | (t[j] < 0);
-            atomicAdd(&lc[b[j]], 1u);
-            const uint32_t sc = uint32_t(score_of(p[j], t[j]));
-            mx = mx > sc ? mx : sc;
-        }
+    for (int j = 0; j < kJ; ++j) {
+        if (!r.valid[j]) continue;
+        atomicAdd(&lc[r.b[j]], 1u);
+        mx = mx > uint32_t(r.s[j]) ? mx : uint32_t(r.s[j]);
     }
     if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
     mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the counts are complete
-    for (int b = threadIdx.x; b < nb; b += kSortNT) cnt_part[int64_t(blockIdx.x) * nb + b] = lc[b];
+    for (int b = threadIdx.x; b < nb; b += kSortNT) cnt_part[int64_t(b) * blocks + blockIdx.x] = lc[b];
     if (threadIdx.x == 0) max_part[blockIdx.x] = mx;
 }
 
@@ -389,9 +393,10 @@ __global__ __launch_bounds__(kSortNT) void cal_offsets(int nb, int64_t blocks, i
                                                        uint32_t* __restrict__ bmax, int32_t* __restrict__ krank) {
     __shared__ uint32_t tmp[kSortNT / kWave];
     const int b = blockIdx.x;
+    const uint32_t* col = cnt_part + int64_t(b) * blocks;
+    uint32_t* ocol = off_part + int64_t(b) * blocks;
     const uint32_t total = block_scan<kSortNT, false, false, true, uint32_t>(
-        blocks, 0u, [&](int64_t i) { return cnt_part[i * nb + b]; },
-        [&](int64_t i, uint32_t v) { off_part[i * nb + b] = v; }, tmp);
+        blocks, 0u, [&](int64_t i) { return col[i]; }, [&](int64_t i, uint32_t v) { ocol[i] = v; }, tmp);
     uint32_t mx = 0;
     for (int64_t i = threadIdx.x; i < blocks; i += kSortNT) mx = mx > max_part[i] ? mx : max_part[i];
     mx = block_reduce_max<kSortNT>(mx, tmp);
@@ -404,45 +409,83 @@ __global__ __launch_bounds__(kSortNT) void cal_offsets(int nb, int64_t blocks, i
     }
 }
 
+// Each workgroup sorts its residuals' scores by bucket in LDS, then writes
+// every bucket's run to its place in the bucket-major array (consecutive
+// scores of a run go to consecutive addresses).
 __global__ __launch_bounds__(kSortNT) void cal_scatter(const int32_t* __restrict__ pred,
                                                        const int32_t* __restrict__ truth, int64_t n,
-                                                       const int32_t* __restrict__ edges, int nb, int64_t per_block,
+                                                       const int32_t* __restrict__ edges, int nb, int64_t blocks,
                                                        const uint32_t* __restrict__ bcount,
                                                        const uint32_t* __restrict__ off_part,
                                                        int32_t* __restrict__ sorted) {
     extern __shared__ int32_t lds[];
     __shared__ uint32_t tmp[kSortNT / kWave];
     const int ne = nb - 1;
-    int32_t* le = lds;
-    uint32_t* next = reinterpret_cast<uint32_t*>(lds + ne);
+    int32_t* le = lds;                                              // [ne]
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(le + ne);          // [nb] local sizes, then local starts
+    uint32_t* gdst = lcnt + nb;                                     // [nb] global start of the local run
+    int32_t* lsort = reinterpret_cast<int32_t*>(gdst + nb);         // [kPerBlock] scores by bucket
+    uint16_t* lbkt = reinterpret_cast<uint16_t*>(lsort + kPerBlock);   // [kPerBlock] their buckets
     for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
-    // start of each bucket's run, then of this workgroup's part of it
+    for (int i = threadIdx.x; i < nb; i += kSortNT) lcnt[i] = 0;
+    // start of each bucket's run in the bucket-major array
     block_scan<kSortNT, false, false, true, uint32_t>(
-        nb, 0u, [&](int64_t i) { return bcount[i]; }, [&](int64_t i, uint32_t v) { next[i] = v; }, tmp);
-    for (int b = threadIdx.x; b < nb; b += kSortNT) next[b] += off_part[int64_t(blockIdx.x) * nb + b];
+        nb, 0u, [&](int64_t i) { return bcount[i]; }, [&](int64_t i, uint32_t v) { gdst[i] = v; }, tmp);
+    for (int b = threadIdx.x; b < nb; b += kSortNT) gdst[b] += off_part[int64_t(b) * blocks + blockIdx.x];
+    Residuals r;
+    bool bad = false;
+    load_residuals(pred, truth, n, le, ne, r, bad);
+    uint32_t rank[kJ];
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) rank[j] = r.valid[j] ? atomicAdd(&lcnt[r.b[j]], 1u) : 0u;
     __syncthreads();
-    const int64_t lo = int64_t(blockIdx.x) * per_block;
-    const int64_t hi = lo + per_block < n ? lo + per_block : n;
-    for (int64_t c0 = lo; c0 < hi; c0 += int64_t(kSortNT) * kJ) {
-        int32_t p[kJ], t[kJ];
-        int b[kJ];
+    block_scan<kSortNT, false, false, true, uint32_t>(
+        nb, 0u, [&](int64_t i) { return lcnt[i]; }, [&](int64_t i, uint32_t v) { lcnt[i] = v; }, tmp);
 #pragma unroll
-        for (int j = 0; j < kJ; ++j) {
-            const int64_t i = c0 + int64_t(j) * kSortNT + threadIdx.x;
-            p[j] = i < hi ? pred[i] : 0;
-            t[j] = i < hi ? truth[i] : 0;
-        }
-        buckets_of<kJ>(le, ne, p, b);
-#pragma unroll
-        for (int j = 0; j < kJ; ++j) {
-            if (c0 + int64_t(j) * kSortNT + threadIdx.x >= hi) continue;
-            const uint32_t pos = atomicAdd(&next[b[j]], 1u);
-            if (pos < uint64_t(n)) sorted[pos] = score_of(p[j], t[j]);   // always: the runs partition [0, n)
-        }
+    for (int j = 0; j < kJ; ++j) {
+        if (!r.valid[j]) continue;
+        const uint32_t at = lcnt[r.b[j]] + rank[j];
+        lsort[at] = r.s[j];
+        lbkt[at] = uint16_t(r.b[j]);
+    }
+    __syncthreads();
+    const int64_t lo = int64_t(blockIdx.x) * kPerBlock;
+    const int cnt = int(n - lo < kPerBlock ? n - lo : kPerBlock);
+    for (int i = threadIdx.x; i < cnt; i += kSortNT) {
+        const int b = lbkt[i];
+        const uint32_t pos = gdst[b] + uint32_t(i) - lcnt[b];
+        if (pos < uint64_t(n)) sorted[pos] = lsort[i];   // always: the runs partition [0, n)
     }
 }
 
-// One workgroup per bucket: the k_b-th smallest score of its run.
+// Digit of the k-th element among the 256 bins of hist (one wavefront).
+__device__ inline void pick_digit(const uint32_t* hist, int32_t k, uint32_t* pick) {
+    const int lane = threadIdx.x;
+    uint32_t h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) h[j] = hist[lane * 4 + j];
+    const uint32_t mine = h[0] + h[1] + h[2] + h[3];
+    uint32_t c = wave_incl_scan_add(mine) - mine;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (c < uint32_t(k) && c + h[j] >= uint32_t(k)) { pick[0] = uint32_t(lane * 4 + j); pick[1] = uint32_t(k) - c; }
+        c += h[j];
+    }
+}
+
+// Histogram update of one score's digit; the lanes holding the first active
+// lane's digit add it with one atomic.
+__device__ inline void hist_add(uint32_t* hist, uint32_t digit) {
+    const uint32_t lead = __builtin_amdgcn_readfirstlane(digit);
+    const uint64_t same = __ballot(digit == lead);
+    if (digit != lead) atomicAdd(&hist[digit], 1u);
+    else if (int(threadIdx.x % kWave) == __ffsll((unsigned long long)same) - 1)
+        atomicAdd(&hist[lead], uint32_t(__popcll(same)));
+}
+
+// One workgroup per bucket: the k_b-th smallest score of its run, most
+// significant 8-bit digit first from the top digit of the largest score.  A
+// run of at most kSelNT * kKeep scores stays in registers across passes.
 __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, const int32_t* __restrict__ sorted,
                                                             const uint32_t* __restrict__ bcount,
                                                             const uint32_t* __restrict__ bmax,
@@ -466,45 +509,43 @@ __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, const int32_
     const uint32_t mx = bmax[b];
     const int top = mx >> 24 ? 24 : (mx >> 16 ? 16 : (mx >> 8 ? 8 : 0));
     const int32_t* v = sorted + base;
+    const bool in_regs = nbk <= uint32_t(kSelNT) * kKeep;
+    uint32_t x[kKeep];
+    if (in_regs) {
+#pragma unroll
+        for (int j = 0; j < kKeep; ++j) {
+            const uint32_t i = uint32_t(j) * kSelNT + threadIdx.x;
+            x[j] = i < nbk ? uint32_t(v[i]) : 0u;
+        }
+    }
     uint32_t prefix = 0;
-    const int lane = threadIdx.x % kWave;
     for (int shift = top; shift >= 0; shift -= 8) {
         if (threadIdx.x < 256) hist[threadIdx.x] = 0;
         __syncthreads();
-        for (uint32_t c0 = 0; c0 < nbk; c0 += kSelNT * kJ) {
-            uint32_t x[kJ];
+        if (in_regs) {
 #pragma unroll
-            for (int j = 0; j < kJ; ++j) {
-                const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
-                x[j] = i < nbk ? uint32_t(v[i]) >> shift : 0xFFFFFFFFu;
+            for (int j = 0; j < kKeep; ++j) {
+                const uint32_t i = uint32_t(j) * kSelNT + threadIdx.x;
+                const uint32_t y = x[j] >> shift;
+                if (i < nbk && (y >> 8) == prefix) hist_add(hist, y & 255u);
             }
+        } else {
+            for (uint32_t c0 = 0; c0 < nbk; c0 += kSelNT * kJ) {
+                uint32_t y[kJ];
 #pragma unroll
-            for (int j = 0; j < kJ; ++j) {
-                const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
-                if (i < nbk && (x[j] >> 8) == prefix) {
-                    // lanes holding the first such lane's digit add it with one atomic
-                    const uint32_t digit = x[j] & 255u;
-                    const uint32_t lead = __builtin_amdgcn_readfirstlane(digit);
-                    const uint64_t same = __ballot(digit == lead);
-                    if (digit != lead) atomicAdd(&hist[digit], 1u);
-                    else if (lane == __ffsll((unsigned long long)same) - 1) atomicAdd(&hist[lead], uint32_t(__popcll(same)));
+                for (int j = 0; j < kJ; ++j) {
+                    const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
+                    y[j] = i < nbk ? uint32_t(v[i]) >> shift : 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < kJ; ++j) {
+                    const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
+                    if (i < nbk && (y[j] >> 8) == prefix) hist_add(hist, y[j] & 255u);
                 }
             }
         }
         __syncthreads();
-        if (threadIdx.x < kWave) {   // the digit holding the k-th element
-            const int lane = threadIdx.x;
-            uint32_t h[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) h[j] = hist[lane * 4 + j];
-            const uint32_t mine = h[0] + h[1] + h[2] + h[3];
-            uint32_t c = wave_incl_scan_add(mine) - mine;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (c < uint32_t(k) && c + h[j] >= uint32_t(k)) { pick[0] = uint32_t(lane * 4 + j); pick[1] = uint32_t(k) - c; }
-                c += h[j];
-            }
-        }
+        if (threadIdx.x < kWave) pick_digit(hist, k, pick);
         __syncthreads();
         prefix = (prefix << 8) | pick[0];
         k = int32_t(pick[1]);
@@ -527,30 +568,31 @@ using namespace maps;
 
 extern "C" size_t maps_calibrate_workspace_size(int64_t n, int32_t nb) {
     if (n < 0 || nb < 1) return 0;
-    return nb <= kFastBuckets ? fast_carve(nullptr, n, nb).bytes : cal_carve(nullptr, n, nb).bytes;
+    return fast_path(n, nb) ? fast_carve(nullptr, n, nb).bytes : cal_carve(nullptr, n, nb).bytes;
 }
 
 namespace {
 
-// Calibration for up to kFastBuckets buckets (counting sort, then one
-// workgroup per bucket).
+// Calibration by counting sort (up to kFastBuckets buckets and
+// kSortMaxBlocks * kPerBlock residuals), then one workgroup per bucket.
 maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges, int32_t nb,
                            int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
                            void* workspace, hipStream_t stream) {
     const FastWorkspace w = fast_carve(workspace, n, nb);
-    const SortPlan sp = sort_plan(n);
-    const size_t lds = size_t(2 * nb) * 4;   // edges and per-bucket counters
+    const int64_t blocks = sort_blocks(n);
+    const size_t lds_count = size_t(2 * nb) * 4;   // edges and per-bucket counters
+    const size_t lds_scatter = size_t(3 * nb) * 4 + size_t(kPerBlock) * 6;
     if (n > 0) {
-        hipLaunchKernelGGL(cal_count, dim3(unsigned(sp.blocks)), dim3(kSortNT), lds, stream, pred, truth, n, edges,
-                           nb, sp.per_block, w.cnt_part, w.max_part, dev_err);
+        hipLaunchKernelGGL(cal_count, dim3(unsigned(blocks)), dim3(kSortNT), lds_count, stream, pred, truth, n,
+                           edges, nb, blocks, w.cnt_part, w.max_part, dev_err);
         MAPS_CHECK_LAUNCH();
     }
-    hipLaunchKernelGGL(cal_offsets, dim3(unsigned(nb)), dim3(kSortNT), 0, stream, nb, sp.blocks, alpha_ppm,
+    hipLaunchKernelGGL(cal_offsets, dim3(unsigned(nb)), dim3(kSortNT), 0, stream, nb, blocks, alpha_ppm,
                        w.cnt_part, w.max_part, w.off_part, w.bcount, w.bmax, w.krank);
     MAPS_CHECK_LAUNCH();
     if (n > 0) {
-        hipLaunchKernelGGL(cal_scatter, dim3(unsigned(sp.blocks)), dim3(kSortNT), lds, stream, pred, truth, n,
-                           edges, nb, sp.per_block, w.bcount, w.off_part, w.sorted);
+        hipLaunchKernelGGL(cal_scatter, dim3(unsigned(blocks)), dim3(kSortNT), lds_scatter, stream, pred, truth, n,
+                           edges, nb, blocks, w.bcount, w.off_part, w.sorted);
         MAPS_CHECK_LAUNCH();
     }
     hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), 0, stream, nb, w.sorted, w.bcount,
@@ -558,10 +600,6 @@ maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n,
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }
-
-}  // namespace
-
-namespace {
 
 maps_status calibrate_general(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges,
                               int32_t nb, int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
@@ -626,7 +664,7 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
         return MAPS_E_NULL;
     if (workspace_bytes < maps_calibrate_workspace_size(n, nb)) return MAPS_E_WORKSPACE;
     const int ne = nb - 1;
-    if (nb <= kFastBuckets) {
+    if (fast_path(n, nb)) {
         const maps_status st =
             calibrate_fast(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, dev_err, workspace, stream);
         if (st != MAPS_OK) return st;
@@ -637,7 +675,7 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     }
     if (m > 0) {
         const bool lds_edges = nb <= kLdsEdgesMax;
-        const int g = grid_for(m, kNT, 8, 8192);
+        const int g = grid_for(m, kNT, 4, 8192);
         if (lds_edges)
             hipLaunchKernelGGL(cal_apply<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
                                apply_pred, m, edges, nb, q_out, u_max, U_out);
