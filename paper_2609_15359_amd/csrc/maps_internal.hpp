@@ -59,10 +59,8 @@ struct SnapHeader {       // at offset 0, 64 bytes
     int32_t u_max;
     int32_t W;            // rank words per decoder
     int64_t n_total;      // residents
-    int64_t max_tot;      // max over decoders of sum_r (p + g + R)
-    int32_t max_records;  // max over decoders of E + 1
     int32_t P;            // profile entries per decoder (0: no profile)
-    int32_t pad[6];
+    int32_t pad[9];
 };
 static_assert(sizeof(SnapHeader) == 64, "header size");
 

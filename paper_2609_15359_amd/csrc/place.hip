@@ -121,6 +121,24 @@ __device__ __forceinline__ DecHeader lane_header(const DecLanes& l, int32_t lane
     return h;
 }
 
+// Largest total demand sum_r (p + g + R) and record count E + 1 over the
+// decoders [d0, d1), the same in every lane.
+struct GroupMax {
+    int64_t tot;
+    int32_t records;
+};
+
+__device__ inline GroupMax group_max(const SnapView& V, int32_t d0, int32_t d1) {
+    int64_t t = 0;
+    int32_t r = 0;
+    for (int32_t d = d0 + int32_t(threadIdx.x % kWave); d < d1; d += kWave) {
+        const DecHeader h = V.dec[d];
+        t = t > h.tot ? t : h.tot;
+        r = r > h.E + 1 ? r : h.E + 1;
+    }
+    return GroupMax{wave_reduce_max(t), wave_reduce_max(r)};
+}
+
 // Raw buffer resources (gfx9 descriptor, 32-bit data format): accesses whose
 // VGPR offset (plus immediate) reaches past `bytes` read 0 and write nothing.
 constexpr int kBufferWord3 = 0x00020000;
@@ -282,7 +300,7 @@ __device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* sr
 // fits (a header claiming more is reported and skipped).
 template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kMixed>
 __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
-                                             int64_t a0) {
+                                             int64_t a0, int64_t max_tot) {
     const SnapLayout& L = g.L;
     const int32_t half_w = L.W / 2;                // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
@@ -293,7 +311,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     RecArrivals<kAPT> s;
-    load_arrivals<kAPT, kFull>(g, a0, load_uniform(&V.hdr->max_tot), s.p, s.U);
+    load_arrivals<kAPT, kFull>(g, a0, max_tot, s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int32_t U = s.U[k];
@@ -357,9 +375,9 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }
 
-// When every slice fits an LDS buffer (the snapshot's largest record count
-// says so) the tile runs in one pass; otherwise it is split into sub-tiles of
-// at most 4 arrivals per thread that read the large slices from HBM.
+// When every slice of the group fits an LDS buffer the tile runs in one pass;
+// otherwise it is split into sub-tiles of at most 4 arrivals per thread that
+// read the large slices from HBM.
 template <int kAPT, bool kPairs, int kPolicy>
 __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     extern __shared__ int4 lds[];
@@ -370,17 +388,18 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     }
     const int32_t grp = blockIdx.x % g.G;
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
-    const int32_t max_records = load_uniform(&V.hdr->max_records);
-    if (g.L.W / 2 + max_records <= g.buf_units) {
+    const int32_t d_begin = grp * g.Dg;
+    const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
+    if (g.L.W / 2 + gm.records <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
-            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0);
+            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm.tot);
         else
-            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0);
+            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm.tot);
     } else {
         constexpr int kSub = kAPT < 4 ? kAPT : 4;
         for (int t = 0; t < kAPT / kSub; ++t) {
             const int64_t b0 = a0 + int64_t(t) * kNT * kSub;
-            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0);
+            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0, gm.tot);
         }
     }
 }
@@ -441,7 +460,7 @@ __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V,
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     ProfArrivals<kAPT> s;
-    load_arrivals<kAPT, kFull>(g, a0, load_uniform(&V.hdr->max_tot), s.p, s.U);
+    load_arrivals<kAPT, kFull>(g, a0, group_max(V, d_begin, d_end).tot, s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int32_t U = s.U[k];

@@ -220,6 +220,17 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
     }
     // decoder d's slice: W/2 units of rank words, then records [0, hi - lo]
     const int64_t slice_off = lo + int64_t(d) * (1 + W / 2);
+    if (d == 0 && threadIdx.x == 0) {   // the snapshot header: every field is known before the decoders
+        SnapHeader h;
+        h.D = D;
+        h.u_max = u_max;
+        h.W = W;
+        h.n_total = n_total;
+        h.P = L.P;
+        for (int i = 0; i < 9; ++i) h.pad[i] = 0;
+        h.magic = kSnapMagic;
+        *V.hdr = h;
+    }
     if (lds_cap > 0 && hi - lo <= lds_cap) {
         LdsArrays a;
         a.bits = lds;
@@ -235,34 +246,6 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
         a.hot = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
         a.cold = nullptr;
         project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
-    }
-}
-
-__global__ __launch_bounds__(kNT) void project_finish(int32_t D, int64_t n_total, SnapLayout L, void* snap) {
-    __shared__ int64_t red64[kNT / kWave];
-    __shared__ int32_t red32[kNT / kWave];
-    SnapView V = snap_view(snap, L);
-    int64_t mt = 0;
-    int32_t me = 0;
-    for (int d = threadIdx.x; d < D; d += kNT) {
-        DecHeader h = V.dec[d];
-        mt = mt > h.tot ? mt : h.tot;
-        me = me > h.E + 1 ? me : h.E + 1;
-    }
-    mt = block_reduce_max<kNT>(mt, red64);
-    me = block_reduce_max<kNT>(me, red32);
-    if (threadIdx.x == 0) {
-        SnapHeader h;
-        h.D = D;
-        h.u_max = L.u_max;
-        h.W = L.W;
-        h.n_total = n_total;
-        h.max_tot = mt;
-        h.max_records = me;
-        h.P = L.P;
-        for (int i = 0; i < 6; ++i) h.pad[i] = 0;
-        h.magic = kSnapMagic;
-        *V.hdr = h;
     }
 }
 
@@ -298,8 +281,6 @@ extern "C" maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n
     allow_dynamic_lds(project_decoders, lds);
     hipLaunchKernelGGL(project_decoders, dim3(D), dim3(kNT), lds, stream, D, seg_off, n_total, prompt, generated,
                        upper, u_max, L, snapshot, base_peak, cap, dev_err);
-    MAPS_CHECK_LAUNCH();
-    hipLaunchKernelGGL(project_finish, dim3(1), dim3(kNT), 0, stream, D, n_total, L, snapshot);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }
