@@ -216,11 +216,13 @@ __device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, 
 // the byte offset of the bound's rank word in a slice and the mask of the
 // bits below it (bound clamped to [0, 32 W - 1]), and the running best.
 // The workgroup walks its decoders with two LDS buffers: while decoder d is
-// evaluated from one buffer, the slice of decoder d+1 is already on its way
-// into registers, and it is written to the other buffer before the single
-// barrier of the next step.  A slice too large for a buffer is read from HBM.
+// evaluated from one buffer, the rank words and hot records of decoder d+1
+// are already on their way into registers, and they are written to the other
+// buffer before the single barrier of the next step.  Cold records, needed
+// only past an event's threshold, stay in the snapshot (read through L2).  A
+// slice whose staged part exceeds a buffer is read from HBM altogether.
 // ---------------------------------------------------------------------------
-constexpr int kStage = 10;  // 16-byte units per thread staged in registers: a whole LDS buffer
+constexpr int kStage = 6;   // 16-byte units per thread staged in registers: a whole LDS buffer
 
 template <int kAPT>
 struct RecArrivals {
@@ -230,15 +232,14 @@ struct RecArrivals {
 };
 
 // Evaluate the thread's arrivals against one decoder whose rank words start
-// at `rank` and hot records at `hot`, the cold ones following them (all in
-// LDS, or all in HBM).  Only lanes whose bound reaches an event's threshold
-// read its cold record.
+// at `rank` and hot records at `hot` (both in LDS, or both in HBM), with its
+// cold records at `cold` in HBM.  Only lanes whose bound reaches an event's
+// threshold read its cold record.
 template <int kAPT, bool kFull, bool kPairs, int kPolicy>
-__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int2* hot, uint32_t E,
-                                             int32_t base, int32_t C, int32_t Q, int32_t d,
-                                             __amdgpu_buffer_rsrc_t row) {
+__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int2* hot,
+                                             const int2* cold, uint32_t E, int32_t base, int32_t C, int32_t Q,
+                                             int32_t d, __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
-    const int2* cold = hot + E + 1;
     const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
 #pragma unroll
     for (int c = 0; c < kAPT; c += kChunk) {
@@ -323,14 +324,16 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         s.best_d[k] = d_begin;
     }
 
-    auto fits = [&](const DecHeader& h) { return half_w + h.E + 1 <= buf_units; };
+    // staged units: the rank words and the hot records
+    auto staged = [&](const DecHeader& h) { return half_w + (h.E + 2) / 2; };
+    auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
 
     DecLanes lanes = load_lanes(g, V, d_begin, d_end);
     int32_t lanes0 = d_begin;
     v4i stage[kStage];
     DecHeader h = lane_header(lanes, 0);
     bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
-    if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);
+    if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));
     for (int32_t d = d_begin; d < d_end; ++d) {
         const DecHeader cur = h;
         const bool valid = h_ok;
@@ -345,7 +348,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             // finished before passing the barrier of decoder d-1.  Staged units
             // past the slice's end (0) stay inside the buffer: kStage * kNT
             // units fit it.
-            const int32_t units = half_w + cur.E + 1;
+            const int32_t units = staged(cur);
 #pragma unroll
             for (int j = 0; j < kStage; ++j)
                 if (j * kNT < units) reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
@@ -357,7 +360,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             }
             h = lane_header(lanes, d + 1 - lanes0);
             h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
-            if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, half_w + h.E + 1);   // overlaps the evaluation
+            if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));   // overlaps the evaluation
         }
         __syncthreads();
         if (!valid) continue;
@@ -366,11 +369,12 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         if (!kMixed || in_lds)
             eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice),
                                                        reinterpret_cast<const int2*>(slice + half_w),
-                                                       uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+                                                       slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
+                                                       d, row);
         else if constexpr (kMixed)
             eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
-                                                       slice_hot(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
-                                                       d, row);
+                                                       slice_hot(V, cur, L), slice_cold(V, cur, L), uint32_t(cur.E),
+                                                       cur.base_peak, C, Q, d, row);
     }
     write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }
@@ -390,7 +394,7 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
     const int32_t d_begin = grp * g.Dg;
     const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
-    if (g.L.W / 2 + gm.records <= g.buf_units) {
+    if (g.L.W / 2 + (gm.records + 1) / 2 <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
             records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm.tot);
         else
@@ -689,10 +693,9 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
         a.nb = int32_t(nb < 8 ? nb : 8);
         lds = size_t(kProfPF) * kNT * 16;
     } else {
-        // two buffers of buf_units 16-byte units, each at least as large as
-        // the staged part of a slice
-        const int32_t buf_units = int32_t(kLdsBytes / 16 / 2);
-        a.buf_units = L.W / 2 + 64 <= buf_units && kStage * kNT <= buf_units ? buf_units : 0;
+        // two buffers of kStage * kNT 16-byte units: the staged part of a slice
+        const int32_t buf_units = kStage * kNT;
+        a.buf_units = L.W / 2 + 64 <= buf_units ? buf_units : 0;
         lds = size_t(2 * a.buf_units) * 16;
     }
     const int64_t tiles = (A + int64_t(kNT) * apt - 1) / (int64_t(kNT) * apt);
