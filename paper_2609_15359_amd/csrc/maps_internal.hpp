@@ -38,7 +38,10 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 //                         (0 when S_e > PMX_e; capped at INT32_MAX),
 //   cold {S_e, N_e + 1}.
 // For U < T_e, PF(U) = PMX_e and the cold record is not needed; for U >= T_e,
-// PF(U) = S_e + U (N_e + 1).  The rank e = #{events < U} comes from a bitmap
+// PF(U) = S_e + U (N_e + 1).  A bound lands on event e when tau_{e-1} < U <=
+// tau_e, so the bounds that need a cold record form the ranges
+// [max(T_e, tau_{e-1} + 1), tau_e]; the header's hot window [hot_lo, hot_hi]
+// lies above event 0's range and below every later one.  The rank e = #{events < U} comes from a bitmap
 // over the step axis: word w holds bit j for event time 32w + j, next to the
 // number of events before word w.  W words cover [0, 32 W) with 32 W - 1 > u_max,
 // so a bound clamped to 32 W - 1 ranks above every event.  Each decoder's rank
@@ -69,7 +72,8 @@ struct DecHeader {        // one per decoder, 32 bytes
     int64_t tot;          // sum_r (p + g + R)
     int32_t E;            // number of events
     int32_t base_peak;    // max_t O(t)
-    int32_t pad[2];
+    int32_t hot_lo;       // every bound U in [hot_lo, hot_hi] has PF(U) = max(PMX_e, U):
+    int32_t hot_hi;       //   it stays below the threshold of the event it lands on
 };
 static_assert(sizeof(DecHeader) == 32, "decoder header size");
 

@@ -56,6 +56,11 @@ struct PlaceArgs {
     uint32_t* dev_err;
 };
 
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
+
 // Read-only values every lane needs alike, loaded through the scalar cache.
 template <typename T>
 __device__ __forceinline__ T load_uniform(const T* p) {
@@ -117,26 +122,31 @@ __device__ __forceinline__ DecHeader lane_header(const DecLanes& l, int32_t lane
     h.tot = 0;
     h.E = lane_value(l.E, lane);
     h.base_peak = lane_value(l.base, lane);
-    h.pad[0] = h.pad[1] = 0;
+    h.hot_lo = 1;
+    h.hot_hi = 0;
     return h;
 }
 
 // Largest total demand sum_r (p + g + R) and record count E + 1 over the
-// decoders [d0, d1), the same in every lane.
+// decoders [d0, d1), and the intersection of their hot windows, the same in
+// every lane.
 struct GroupMax {
     int64_t tot;
     int32_t records;
+    int32_t hot_lo, hot_hi;
 };
 
 __device__ inline GroupMax group_max(const SnapView& V, int32_t d0, int32_t d1) {
     int64_t t = 0;
-    int32_t r = 0;
+    int32_t r = 0, lo = 0, hi = INT32_MAX;
     for (int32_t d = d0 + int32_t(threadIdx.x % kWave); d < d1; d += kWave) {
         const DecHeader h = V.dec[d];
         t = t > h.tot ? t : h.tot;
         r = r > h.E + 1 ? r : h.E + 1;
+        lo = lo > h.hot_lo ? lo : h.hot_lo;
+        hi = hi < h.hot_hi ? hi : h.hot_hi;
     }
-    return GroupMax{wave_reduce_max(t), wave_reduce_max(r)};
+    return GroupMax{wave_reduce_max(t), wave_reduce_max(r), wave_reduce_max(lo), -wave_reduce_max(-hi)};
 }
 
 // Raw buffer resources (gfx9 descriptor, 32-bit data format): accesses whose
@@ -234,8 +244,9 @@ struct RecArrivals {
 // Evaluate the thread's arrivals against one decoder whose rank words start
 // at `rank` and hot records at `hot` (both in LDS, or both in HBM), with its
 // cold records at `cold` in HBM.  Only lanes whose bound reaches an event's
-// threshold read its cold record.
-template <int kAPT, bool kFull, bool kPairs, int kPolicy>
+// threshold read its cold record.  kHot: every bound of the tile lies in the
+// decoder's hot window (no threshold test) and every arrival has a bound.
+template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kHot>
 __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int2* hot,
                                              const int2* cold, uint32_t E, int32_t base, int32_t C, int32_t Q,
                                              int32_t d, __amdgpu_buffer_rsrc_t row) {
@@ -259,9 +270,9 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             pf[i] = max(h[i].x, s.U[c + i]);
-            line |= s.U[c + i] >= h[i].y;
+            if constexpr (!kHot) line |= s.U[c + i] >= h[i].y;
         }
-        if (__builtin_amdgcn_ballot_w64(line) != 0) {   // a lane of the wave reached a threshold
+        if (!kHot && __builtin_amdgcn_ballot_w64(line) != 0) {   // a lane of the wave reached a threshold
 #pragma unroll
             for (int i = 0; i < kChunk; ++i) {
                 const int32_t U = s.U[c + i];
@@ -275,7 +286,7 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
         for (int i = 0; i < kChunk; ++i) {
             const int k = c + i;
             const int32_t peak = imax(s.p[k] + pf[i], base);
-            if constexpr (kPairs) store_pair<kFull>(row, k, peak | s.neg[k]);
+            if constexpr (kPairs) store_pair<kFull>(row, k, kHot ? peak : peak | s.neg[k]);
             const int32_t key = select_key<kPolicy>(peak, C, Qm);
             const bool take = key < s.best_key[k];
             s.best_key[k] = take ? key : s.best_key[k];
@@ -301,7 +312,7 @@ __device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* sr
 // fits (a header claiming more is reported and skipped).
 template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kMixed>
 __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
-                                             int64_t a0, int64_t max_tot) {
+                                             int64_t a0, const GroupMax& gm) {
     const SnapLayout& L = g.L;
     const int32_t half_w = L.W / 2;                // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
@@ -312,7 +323,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     RecArrivals<kAPT> s;
-    load_arrivals<kAPT, kFull>(g, a0, max_tot, s.p, s.U);
+    load_arrivals<kAPT, kFull>(g, a0, gm.tot, s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int32_t U = s.U[k];
@@ -323,59 +334,99 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         s.best_key[k] = INT32_MAX;
         s.best_d[k] = d_begin;
     }
+    // smallest and largest bound of the tile, and whether an arrival lacks one
+    __shared__ int32_t red[3][kNT / kWave];
+    int32_t t_lo = INT32_MAX, t_hi = -1, t_neg = 0;
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int32_t U = s.U[k];
+        if (U >= 0) {
+            t_lo = U < t_lo ? U : t_lo;
+            t_hi = U > t_hi ? U : t_hi;
+        } else if (int64_t(k) * kNT + threadIdx.x < tile_n) {
+            t_neg = 1;
+        }
+    }
+    t_lo = -wave_reduce_max(-t_lo);
+    t_hi = wave_reduce_max(t_hi);
+    t_neg = wave_reduce_max(t_neg);
+    if (threadIdx.x % kWave == 0) {
+        red[0][threadIdx.x / kWave] = t_lo;
+        red[1][threadIdx.x / kWave] = t_hi;
+        red[2][threadIdx.x / kWave] = t_neg;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kNT / kWave; ++i) {
+        t_lo = red[0][i] < t_lo ? red[0][i] : t_lo;
+        t_hi = red[1][i] > t_hi ? red[1][i] : t_hi;
+        t_neg |= red[2][i];
+    }
+    t_lo = __builtin_amdgcn_readfirstlane(t_lo);   // the same in every lane: keep the test below scalar
+    t_hi = __builtin_amdgcn_readfirstlane(t_hi);
+    t_neg = __builtin_amdgcn_readfirstlane(t_neg);
+    // the tile skips every threshold test when the hot windows of all the
+    // group's decoders hold all its bounds (and every arrival has a bound)
+    const bool all_hot = !kMixed && t_neg == 0 && t_lo >= gm.hot_lo && t_hi <= gm.hot_hi;
 
     // staged units: the rank words and the hot records
     auto staged = [&](const DecHeader& h) { return half_w + (h.E + 2) / 2; };
     auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
 
-    DecLanes lanes = load_lanes(g, V, d_begin, d_end);
-    int32_t lanes0 = d_begin;
-    v4i stage[kStage];
-    DecHeader h = lane_header(lanes, 0);
-    bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
-    if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));
-    for (int32_t d = d_begin; d < d_end; ++d) {
-        const DecHeader cur = h;
-        const bool valid = h_ok;
-        const bool in_lds = valid && (!kMixed || fits(cur));
-        const int32_t buf = (d - d_begin) & 1;
-        const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
-        if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-        if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-        int4* slice = lds + buf * buf_units;
-        if (in_lds) {
-            // Buffer `buf` was last read for decoder d-2, which every wave
-            // finished before passing the barrier of decoder d-1.  Staged units
-            // past the slice's end (0) stay inside the buffer: kStage * kNT
-            // units fit it.
-            const int32_t units = staged(cur);
-#pragma unroll
-            for (int j = 0; j < kStage; ++j)
-                if (j * kNT < units) reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
-        }
-        if (d + 1 < d_end) {
-            if (d + 1 - lanes0 == kWave) {
-                lanes = load_lanes(g, V, d + 1, d_end);
-                lanes0 = d + 1;
+    // the decoder walk, with or without the threshold tests
+    auto walk = [&](auto hot_tag) {
+        constexpr bool kHot = decltype(hot_tag)::value;
+        DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+        int32_t lanes0 = d_begin;
+        v4i stage[kStage];
+        DecHeader h = lane_header(lanes, 0);
+        bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
+        if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));
+        for (int32_t d = d_begin; d < d_end; ++d) {
+            const DecHeader cur = h;
+            const bool valid = h_ok;
+            const bool in_lds = valid && (!kMixed || fits(cur));
+            const int32_t buf = (d - d_begin) & 1;
+            const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
+            if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+            if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+            int4* slice = lds + buf * buf_units;
+            if (in_lds) {
+                // Buffer `buf` was last read for decoder d-2, which every wave
+                // finished before passing the barrier of decoder d-1.  Staged units
+                // past the slice's end (0) stay inside the buffer: kStage * kNT
+                // units fit it.
+                const int32_t units = staged(cur);
+    #pragma unroll
+                for (int j = 0; j < kStage; ++j)
+                    if (j * kNT < units) reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
             }
-            h = lane_header(lanes, d + 1 - lanes0);
-            h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
-            if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));   // overlaps the evaluation
+            if (d + 1 < d_end) {
+                if (d + 1 - lanes0 == kWave) {
+                    lanes = load_lanes(g, V, d + 1, d_end);
+                    lanes0 = d + 1;
+                }
+                h = lane_header(lanes, d + 1 - lanes0);
+                h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
+                if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));   // overlaps the evaluation
+            }
+            __syncthreads();
+            if (!valid) continue;
+            const __amdgpu_buffer_rsrc_t row =
+                buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
+            if (!kMixed || in_lds)
+                eval_records<kAPT, kFull, kPairs, kPolicy, kHot>(s, reinterpret_cast<const char*>(slice),
+                                                                 reinterpret_cast<const int2*>(slice + half_w),
+                                                                 slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C,
+                                                                 Q, d, row);
+            else if constexpr (kMixed)
+                eval_records<kAPT, kFull, kPairs, kPolicy, false>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
+                                                                  slice_hot(V, cur, L), slice_cold(V, cur, L),
+                                                                  uint32_t(cur.E), cur.base_peak, C, Q, d, row);
         }
-        __syncthreads();
-        if (!valid) continue;
-        const __amdgpu_buffer_rsrc_t row =
-            buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
-        if (!kMixed || in_lds)
-            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice),
-                                                       reinterpret_cast<const int2*>(slice + half_w),
-                                                       slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q,
-                                                       d, row);
-        else if constexpr (kMixed)
-            eval_records<kAPT, kFull, kPairs, kPolicy>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
-                                                       slice_hot(V, cur, L), slice_cold(V, cur, L), uint32_t(cur.E),
-                                                       cur.base_peak, C, Q, d, row);
-    }
+    };
+    if (all_hot) walk(BoolTag<true>{});
+    else walk(BoolTag<false>{});
     write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }
 
@@ -396,14 +447,14 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
     if (g.L.W / 2 + (gm.records + 1) / 2 <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
-            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm.tot);
+            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
         else
-            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm.tot);
+            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
     } else {
         constexpr int kSub = kAPT < 4 ? kAPT : 4;
         for (int t = 0; t < kAPT / kSub; ++t) {
             const int64_t b0 = a0 + int64_t(t) * kNT * kSub;
-            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0, gm.tot);
+            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0, gm);
         }
     }
 }

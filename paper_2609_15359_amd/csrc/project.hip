@@ -147,6 +147,24 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     }
     const int32_t base = block_reduce_max<kNT>(bmax, reinterpret_cast<int32_t*>(sc.red32));
 
+    // hot window: bounds above event 0's cold range and below the first cold
+    // range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] (to infinity
+    // for e = E); with no event at all the window is empty
+    int32_t lo_w = 0, start_min = INT32_MAX;
+    for (int64_t e = tid; e <= E; e += kNT) {
+        const bool last = e == E;
+        const int64_t T = last ? event_threshold(pmx_end, 0, 1u)
+                               : event_threshold(int32_t(a.M(e)), int32_t(a.S(e)), a.C(e) + 1u);
+        const int64_t lo_e = e == 0 ? 0 : int64_t(a.T(e - 1)) + 1;
+        const int64_t hi_e = last ? int64_t(INT32_MAX) + 1 : int64_t(a.T(e));
+        const int64_t start = T > lo_e ? T : lo_e;
+        if (start > hi_e) continue;   // no bound landing on e reaches T_e
+        if (e == 0) lo_w = hi_e >= int64_t(INT32_MAX) ? INT32_MAX : int32_t(hi_e + 1);
+        else if (start < start_min) start_min = int32_t(start);
+    }
+    const int32_t hot_lo = block_reduce_max<kNT>(lo_w, reinterpret_cast<int32_t*>(sc.red32));
+    const int32_t hot_hi = -block_reduce_max<kNT>(-start_min, reinterpret_cast<int32_t*>(sc.red32)) - 1;
+
     // 5. dense profile F(u) = max(PMX_e, S_e + u (N_e + 1), u), e = #{events < u}
     if (P > 0) {
         int32_t* prof = V.prof + int64_t(d) * P;
@@ -191,7 +209,8 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         h.tot = tot;
         h.E = int32_t(E);
         h.base_peak = base;
-        h.pad[0] = h.pad[1] = 0;
+        h.hot_lo = hot_lo;
+        h.hot_hi = hot_hi;
         V.dec[d] = h;
         base_peak[d] = base;
     }
