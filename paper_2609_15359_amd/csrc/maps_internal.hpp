@@ -33,10 +33,10 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // PF(U) >= base already.  Hence the projected peak with the arrival is
 //   peak(p, U) = max(p + PF(U), base).
 //
-// Each event e (0 <= e <= E, with S_E = N_E = 0) has two 8-byte records:
-//   hot  {PMX_e, T_e}     T_e = the smallest U with S_e + U (N_e + 1) > PMX_e
-//                         (0 when S_e > PMX_e; capped at INT32_MAX),
-//   cold {S_e, N_e + 1}.
+// Each event e (0 <= e <= E, with S_E = N_E = 0) has
+//   PMX_e, and T_e = the smallest U with S_e + U (N_e + 1) > PMX_e
+//          (0 when S_e > PMX_e; capped at INT32_MAX), in two int32 arrays,
+//   and the cold record {S_e, N_e + 1}.
 // For U < T_e, PF(U) = PMX_e and the cold record is not needed; for U >= T_e,
 // PF(U) = S_e + U (N_e + 1).  A bound lands on event e when tau_{e-1} < U <=
 // tau_e, so the bounds that need a cold record form the ranges
@@ -45,9 +45,10 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // over the step axis: word w holds bit j for event time 32w + j, next to the
 // number of events before word w.  W words cover [0, 32 W) with 32 W - 1 > u_max,
 // so a bound clamped to 32 W - 1 ranks above every event.  Each decoder's rank
-// words and records form one contiguous slice of 16-byte units (W/2 units of
-// rank words, then the E + 1 hot records, then the E + 1 cold records), so a
-// consumer copies it in one pass.
+// words and event data form one contiguous slice of 16-byte units: W/2 units
+// of rank words, the E + 1 PMX values and the E + 1 thresholds (each array
+// padded to whole units), then the E + 1 cold records; a consumer copies the
+// prefix it needs in one pass.
 //
 // Since PF depends on the arrival only through U, a decoder whose bounds are
 // short enough also gets a dense profile F(u) = max(PF(u), u) for u = 0..u_max
@@ -95,9 +96,19 @@ struct SnapLayout {
     size_t off_dec, off_prof, off_slice, bytes;
 };
 
-// Units of the slice region: (n_total + 1) records and W/2 rank units per decoder.
+// 16-byte units of one int32 array over the events 0..E.
+__host__ __device__ inline int64_t event_units(int64_t E) { return (E + 4) / 4; }
+
+// Units of a decoder's slice with E events: rank words, PMX, T, cold records.
+// With E <= n_d residents this is at most W/2 + n_d + kSliceSpare.
+constexpr int kSliceSpare = 3;
+__host__ __device__ inline int64_t slice_span(int32_t W, int64_t E) {
+    return W / 2 + 2 * event_units(E) + (E + 2) / 2;
+}
+
+// Units of the slice region: n_total, plus W/2 + kSliceSpare per decoder.
 __host__ __device__ inline int64_t slice_units(const SnapLayout& L) {
-    return L.n_total + int64_t(L.D) * (1 + L.W / 2);
+    return L.n_total + int64_t(L.D) * (kSliceSpare + L.W / 2);
 }
 
 __host__ __device__ inline SnapLayout snap_layout(int32_t D, int64_t n_total, int32_t u_max) {
@@ -110,8 +121,8 @@ __host__ __device__ inline SnapLayout snap_layout(int32_t D, int64_t n_total, in
     L.off_dec = align256(sizeof(SnapHeader));
     L.off_prof = L.off_dec + align256(size_t(D) * sizeof(DecHeader));
     L.off_slice = L.off_prof + align256(size_t(D) * size_t(L.P) * sizeof(int32_t));
-    // decoder d with residents [lo, hi) owns the units [lo + d (1 + W/2), hi + (d + 1)(1 + W/2)):
-    // its W/2 units of rank words and up to hi - lo + 1 records; 64 spare units at the end
+    // decoder d with residents [lo, hi) owns the units [lo + d s, hi + (d + 1) s), s = kSliceSpare + W/2;
+    // 64 spare units at the end
     L.bytes = L.off_slice + size_t(slice_units(L) + 64) * sizeof(int4);
     return L;
 }
@@ -120,7 +131,7 @@ struct SnapView {
     SnapHeader* hdr;
     DecHeader* dec;
     int4* slices;   // per decoder: W/2 units of rank words {bits, events before the word}, then
-                    // records {PMX, S, N+1, tau}
+                    // PMX[E + 1], T[E + 1] and the cold records {S, N + 1}[E + 1]
     int32_t* prof;  // [D][P] profile F(u)
 };
 
@@ -134,16 +145,19 @@ __host__ __device__ inline SnapView snap_view(void* base, const SnapLayout& L) {
 // from the snapshot's own header).
 __host__ __device__ inline bool slice_ok(const DecHeader& h, int64_t n_total, const SnapLayout& L) {
     return h.E >= 0 && h.slice_off >= 0 && h.base_peak >= 0 &&
-           h.slice_off + L.W / 2 + h.E + 1 <= n_total + int64_t(L.D) * (1 + L.W / 2);
+           h.slice_off + slice_span(L.W, h.E) <= n_total + int64_t(L.D) * (kSliceSpare + L.W / 2);
 }
 __host__ __device__ inline const uint2* slice_rank(const SnapView& V, const DecHeader& h) {
     return reinterpret_cast<const uint2*>(V.slices + h.slice_off);
 }
-__host__ __device__ inline const int2* slice_hot(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
-    return reinterpret_cast<const int2*>(V.slices + h.slice_off + L.W / 2);
+__host__ __device__ inline const int32_t* slice_pmx(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
+    return reinterpret_cast<const int32_t*>(V.slices + h.slice_off + L.W / 2);
+}
+__host__ __device__ inline const int32_t* slice_thr(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
+    return slice_pmx(V, h, L) + 4 * event_units(h.E);
 }
 __host__ __device__ inline const int2* slice_cold(const SnapView& V, const DecHeader& h, const SnapLayout& L) {
-    return slice_hot(V, h, L) + h.E + 1;
+    return reinterpret_cast<const int2*>(V.slices + h.slice_off + L.W / 2 + 2 * event_units(h.E));
 }
 
 // Threshold T of an event: the smallest U >= 0 with S + U n1 > pmx.

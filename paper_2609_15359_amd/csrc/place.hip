@@ -174,11 +174,10 @@ __device__ __forceinline__ void store_pair(__amdgpu_buffer_rsrc_t row, int k, in
 // S + U (N + 1) = U; so the product may use U itself (its low 24 bits, all of
 // it whenever an event before E is hit, since events are <= u_max), and the
 // final max with U restores it.
-__device__ __forceinline__ int32_t event_peak(const int2* hot, const int2* cold, uint32_t e, int32_t p, int32_t U,
-                                              int32_t base) {
-    const int2 h = hot[e];
-    int32_t pf = max(h.x, U);
-    if (U >= h.y) {
+__device__ __forceinline__ int32_t event_peak(const int32_t* pmx, const int32_t* thr, const int2* cold, uint32_t e,
+                                              int32_t p, int32_t U, int32_t base) {
+    int32_t pf = max(pmx[e], U);
+    if (U >= thr[e]) {
         const int2 c = cold[e];
         pf = max(c.x + int32_t(__umul24(uint32_t(U), uint32_t(c.y))), U);
     }
@@ -226,8 +225,9 @@ __device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, 
 // the byte offset of the bound's rank word in a slice and the mask of the
 // bits below it (bound clamped to [0, 32 W - 1]), and the running best.
 // The workgroup walks its decoders with two LDS buffers: while decoder d is
-// evaluated from one buffer, the rank words and hot records of decoder d+1
-// are already on their way into registers, and they are written to the other
+// evaluated from one buffer, the rank words and PMX values (and thresholds,
+// unless the tile lies in every decoder's hot window) of decoder d+1 are
+// already on their way into registers, and they are written to the other
 // buffer before the single barrier of the next step.  Cold records, needed
 // only past an event's threshold, stay in the snapshot (read through L2).  A
 // slice whose staged part exceeds a buffer is read from HBM altogether.
@@ -242,14 +242,14 @@ struct RecArrivals {
 };
 
 // Evaluate the thread's arrivals against one decoder whose rank words start
-// at `rank` and hot records at `hot` (both in LDS, or both in HBM), with its
-// cold records at `cold` in HBM.  Only lanes whose bound reaches an event's
+// at `rank`, PMX values at `pmx` and thresholds at `thr` (all in LDS, or all
+// in HBM), with its cold records at `cold` in HBM.  Only lanes whose bound reaches an event's
 // threshold read its cold record.  kHot: every bound of the tile lies in the
 // decoder's hot window (no threshold test) and every arrival has a bound.
 template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kHot>
-__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int2* hot,
-                                             const int2* cold, uint32_t E, int32_t base, int32_t C, int32_t Q,
-                                             int32_t d, __amdgpu_buffer_rsrc_t row) {
+__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int32_t* pmx,
+                                             const int32_t* thr, const int2* cold, uint32_t E, int32_t base, int32_t C,
+                                             int32_t Q, int32_t d, __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
     const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
 #pragma unroll
@@ -258,25 +258,26 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) w[i] = *reinterpret_cast<const uint2*>(rank + s.roff[c + i]);
         uint32_t e[kChunk];
-        int2 h[kChunk];
+        int32_t m[kChunk], t[kChunk];
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             e[i] = w[i].y + __popc(w[i].x & s.mask[c + i]);
             e[i] = e[i] < E ? e[i] : E;   // stays inside the decoder's records
-            h[i] = hot[e[i]];
+            m[i] = pmx[e[i]];
+            if constexpr (!kHot) t[i] = thr[e[i]];
         }
         int32_t pf[kChunk];
         bool line = false;
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
-            pf[i] = max(h[i].x, s.U[c + i]);
-            if constexpr (!kHot) line |= s.U[c + i] >= h[i].y;
+            pf[i] = max(m[i], s.U[c + i]);
+            if constexpr (!kHot) line |= s.U[c + i] >= t[i];
         }
         if (!kHot && __builtin_amdgcn_ballot_w64(line) != 0) {   // a lane of the wave reached a threshold
 #pragma unroll
             for (int i = 0; i < kChunk; ++i) {
                 const int32_t U = s.U[c + i];
-                if (U >= h[i].y) {
+                if (U >= t[i]) {
                     const int2 cr = cold[e[i]];
                     pf[i] = max(cr.x + int32_t(__umul24(uint32_t(U), uint32_t(cr.y))), U);
                 }
@@ -369,19 +370,18 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     // group's decoders hold all its bounds (and every arrival has a bound)
     const bool all_hot = !kMixed && t_neg == 0 && t_lo >= gm.hot_lo && t_hi <= gm.hot_hi;
 
-    // staged units: the rank words and the hot records
-    auto staged = [&](const DecHeader& h) { return half_w + (h.E + 2) / 2; };
-    auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
-
-    // the decoder walk, with or without the threshold tests
+    // the decoder walk, with or without the threshold tests: it stages the
+    // rank words and the PMX values, and the thresholds when it tests them
     auto walk = [&](auto hot_tag) {
         constexpr bool kHot = decltype(hot_tag)::value;
+        auto staged = [&](const DecHeader& h) { return int64_t(half_w) + (kHot ? 1 : 2) * event_units(h.E); };
+        auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
         DecLanes lanes = load_lanes(g, V, d_begin, d_end);
         int32_t lanes0 = d_begin;
         v4i stage[kStage];
         DecHeader h = lane_header(lanes, 0);
         bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
-        if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));
+        if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
         for (int32_t d = d_begin; d < d_end; ++d) {
             const DecHeader cur = h;
             const bool valid = h_ok;
@@ -393,11 +393,11 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             int4* slice = lds + buf * buf_units;
             if (in_lds) {
                 // Buffer `buf` was last read for decoder d-2, which every wave
-                // finished before passing the barrier of decoder d-1.  Staged units
-                // past the slice's end (0) stay inside the buffer: kStage * kNT
-                // units fit it.
-                const int32_t units = staged(cur);
-    #pragma unroll
+                // finished before passing the barrier of decoder d-1.  Staged
+                // units past the slice's end (0) stay inside the buffer:
+                // kStage * kNT units fit it.
+                const int32_t units = int32_t(staged(cur));
+#pragma unroll
                 for (int j = 0; j < kStage; ++j)
                     if (j * kNT < units) reinterpret_cast<v4i*>(slice)[int(threadIdx.x) + j * kNT] = stage[j];
             }
@@ -408,21 +408,23 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                 }
                 h = lane_header(lanes, d + 1 - lanes0);
                 h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
-                if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, staged(h));   // overlaps the evaluation
+                if (h_ok && fits(h))   // overlaps the evaluation
+                    stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
             }
             __syncthreads();
             if (!valid) continue;
             const __amdgpu_buffer_rsrc_t row =
                 buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
-            if (!kMixed || in_lds)
-                eval_records<kAPT, kFull, kPairs, kPolicy, kHot>(s, reinterpret_cast<const char*>(slice),
-                                                                 reinterpret_cast<const int2*>(slice + half_w),
-                                                                 slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C,
-                                                                 Q, d, row);
-            else if constexpr (kMixed)
-                eval_records<kAPT, kFull, kPairs, kPolicy, false>(s, reinterpret_cast<const char*>(slice_rank(V, cur)),
-                                                                  slice_hot(V, cur, L), slice_cold(V, cur, L),
-                                                                  uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+            if (!kMixed || in_lds) {
+                const int32_t* pmx = reinterpret_cast<const int32_t*>(slice + half_w);
+                eval_records<kAPT, kFull, kPairs, kPolicy, kHot>(
+                    s, reinterpret_cast<const char*>(slice), pmx, pmx + 4 * event_units(cur.E),
+                    slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+            } else if constexpr (kMixed) {
+                eval_records<kAPT, kFull, kPairs, kPolicy, false>(
+                    s, reinterpret_cast<const char*>(slice_rank(V, cur)), slice_pmx(V, cur, L), slice_thr(V, cur, L),
+                    slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+            }
         }
     };
     if (all_hot) walk(BoolTag<true>{});
@@ -445,7 +447,7 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
     const int32_t d_begin = grp * g.Dg;
     const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
-    if (g.L.W / 2 + (gm.records + 1) / 2 <= g.buf_units) {
+    if (g.L.W / 2 + 2 * ((int64_t(gm.records) + 3) / 4) <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
             records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
         else
@@ -616,7 +618,7 @@ __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
             const uint2 w = slice_rank(V, h)[uc >> 5];
             uint32_t e = w.y + __popc(w.x & ((1u << (uc & 31)) - 1u));
             e = e < uint32_t(h.E) ? e : uint32_t(h.E);
-            peak = event_peak(slice_hot(V, h, L), slice_cold(V, h, L), e, p, U, h.base_peak);
+            peak = event_peak(slice_pmx(V, h, L), slice_thr(V, h, L), slice_cold(V, h, L), e, p, U, h.base_peak);
         }
         const int32_t C = g.cap[d];
         g.choice[a] = d;

@@ -35,19 +35,23 @@ struct LdsArrays {
 };
 
 // The same arrays laid directly over the decoder's slice of the snapshot:
-// rank word {bits, before}, hot record {PMX, tau -> T} and cold record {S, N}
-// (the cold records start once the event count is known).
+// rank word {bits, before}, PMX, tau -> T and the cold record {S, N} (the
+// threshold and cold arrays are placed once the event count is known).
 struct HbmArrays {
     uint32_t* rank;  // 2 words per rank entry
-    uint32_t* hot;   // 2 words per hot record
+    uint32_t* pmx;   // 1 word per event
+    uint32_t* thr;   // 1 word per event
     uint32_t* cold;  // 2 words per cold record
     __device__ uint32_t& B(int64_t w) { return rank[2 * w]; }
     __device__ uint32_t& P(int64_t w) { return rank[2 * w + 1]; }
-    __device__ uint32_t& M(int64_t e) { return hot[2 * e]; }
-    __device__ uint32_t& T(int64_t e) { return hot[2 * e + 1]; }
+    __device__ uint32_t& M(int64_t e) { return pmx[e]; }
+    __device__ uint32_t& T(int64_t e) { return thr[e]; }
     __device__ uint32_t& S(int64_t e) { return cold[2 * e]; }
     __device__ uint32_t& C(int64_t e) { return cold[2 * e + 1]; }
-    __device__ void events(uint32_t E) { cold = hot + 2 * (int64_t(E) + 1); }
+    __device__ void events(uint32_t E) {
+        thr = pmx + 4 * event_units(E);
+        cold = thr + 4 * event_units(E);
+    }
 };
 
 __device__ inline int64_t remaining(int32_t U, int32_t g) {
@@ -182,15 +186,17 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         phase<kInLds>();   // the HBM arrays are updated in place below
     }
 
-    // 6. write the snapshot slice: hot records {PMX_e, T_e}, cold {S_e, N_e + 1}
+    // 6. write the snapshot slice: PMX_e, T_e and the cold records {S_e, N_e + 1}
     uint2* rank = reinterpret_cast<uint2*>(V.slices + slice_off);
-    int2* hot = reinterpret_cast<int2*>(V.slices + slice_off + W / 2);
-    int2* cold = hot + E + 1;
+    int32_t* pmx = reinterpret_cast<int32_t*>(V.slices + slice_off + W / 2);
+    int32_t* thr = pmx + 4 * event_units(E);
+    int2* cold = reinterpret_cast<int2*>(thr + 4 * event_units(E));
     if constexpr (kInLds) {
         for (int64_t e = tid; e < E; e += kNT) {
             const int32_t m = int32_t(a.M(e)), sv = int32_t(a.S(e));
             const uint32_t n1 = a.C(e) + 1u;
-            hot[e] = make_int2(m, event_threshold(m, sv, n1));
+            pmx[e] = m;
+            thr[e] = event_threshold(m, sv, n1);
             cold[e] = make_int2(sv, int32_t(n1));
         }
         for (int64_t w = tid; w < W; w += kNT) rank[w] = make_uint2(a.B(w), a.P(w));
@@ -202,7 +208,8 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         }
     }
     if (tid == 0) {
-        hot[E] = make_int2(pmx_end, event_threshold(pmx_end, 0, 1u));
+        pmx[E] = pmx_end;
+        thr[E] = event_threshold(pmx_end, 0, 1u);
         cold[E] = make_int2(0, 1);
         DecHeader h;
         h.slice_off = slice_off;
@@ -237,8 +244,8 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
         if (threadIdx.x == 0) raise_error(dev_err, MAPS_ERR_TOO_MANY);
         hi = lo;
     }
-    // decoder d's slice: W/2 units of rank words, then records [0, hi - lo]
-    const int64_t slice_off = lo + int64_t(d) * (1 + W / 2);
+    // decoder d's slice: W/2 units of rank words, then the event arrays (at most hi - lo + kSliceSpare units)
+    const int64_t slice_off = lo + int64_t(d) * (kSliceSpare + W / 2);
     if (d == 0 && threadIdx.x == 0) {   // the snapshot header: every field is known before the decoders
         SnapHeader h;
         h.D = D;
@@ -262,7 +269,8 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
     } else {
         HbmArrays a;
         a.rank = reinterpret_cast<uint32_t*>(V.slices + slice_off);
-        a.hot = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
+        a.pmx = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
+        a.thr = nullptr;
         a.cold = nullptr;
         project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
     }
