@@ -50,6 +50,7 @@ struct PlaceArgs {
     int32_t* pkey;     // [G][A] best key of each group
     int32_t* pdec;     // [G][A] best decoder of each group
     int32_t G;
+    int32_t policy;
     int32_t Dg;        // decoders per group
     int32_t buf_units; // record path: 16-byte units per LDS buffer (0: slices stay in HBM)
     int32_t nb;        // profile path: profiles per LDS batch
@@ -583,9 +584,11 @@ __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
 
 // ---------------------------------------------------------------------------
 // Final choice per arrival: the best group in group order (strictly smaller
-// key wins, so ties keep the lower decoder), the chosen pair's peak evaluated
-// once more from the snapshot's records, and the outputs; an arrival without
-// a bound goes round-robin.
+// key wins, so ties keep the lower decoder), the chosen pair's peak, and the
+// outputs; an arrival without a bound goes round-robin.  A key that is the
+// overflow v = peak - C (policy MC, and MQ without a feasible decoder) gives
+// the peak back as v + C; a feasible MQ choice evaluates its pair once more
+// from the snapshot's records.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
     const SnapLayout& L = g.L;
@@ -603,24 +606,30 @@ __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
             g.flags[a] = 2;
             continue;
         }
-        int32_t key = g.pkey[a], d = g.pdec[a];
-        for (int32_t gi = 1; gi < g.G; ++gi) {
-            const int64_t o = int64_t(gi) * g.A + a;
-            const int32_t k2 = g.pkey[o];
-            if (k2 < key) { key = k2; d = g.pdec[o]; }
-        }
+        int32_t keys[kMaxGroups];
+#pragma unroll
+        for (int gi = 0; gi < kMaxGroups; ++gi) keys[gi] = gi < g.G ? g.pkey[int64_t(gi) * g.A + a] : INT32_MAX;
+        int32_t key = keys[0], best = 0;
+#pragma unroll
+        for (int gi = 1; gi < kMaxGroups; ++gi)
+            if (keys[gi] < key) { key = keys[gi]; best = gi; }
+        int32_t d = g.pdec[int64_t(best) * g.A + a];
         d = d < 0 || d >= L.D ? 0 : d;
-        const int32_t p = g.ap[a] < 0 ? 0 : g.ap[a];
-        const DecHeader h = V.dec[d];
-        int32_t peak = 0;
-        if (slice_ok(h, n_total, L)) {
-            const int32_t uc = U < ucl_max ? U : ucl_max;
-            const uint2 w = slice_rank(V, h)[uc >> 5];
-            uint32_t e = w.y + __popc(w.x & ((1u << (uc & 31)) - 1u));
-            e = e < uint32_t(h.E) ? e : uint32_t(h.E);
-            peak = event_peak(slice_pmx(V, h, L), slice_thr(V, h, L), slice_cold(V, h, L), e, p, U, h.base_peak);
-        }
         const int32_t C = g.cap[d];
+        int32_t peak = 0;
+        if (g.policy == MAPS_POLICY_MC || key >= 0) {
+            peak = int32_t(int64_t(key) + C);
+        } else {
+            const DecHeader h = V.dec[d];
+            if (slice_ok(h, n_total, L)) {
+                const int32_t p = g.ap[a] < 0 ? 0 : g.ap[a];
+                const int32_t uc = U < ucl_max ? U : ucl_max;
+                const uint2 w = slice_rank(V, h)[uc >> 5];
+                uint32_t e = w.y + __popc(w.x & ((1u << (uc & 31)) - 1u));
+                e = e < uint32_t(h.E) ? e : uint32_t(h.E);
+                peak = event_peak(slice_pmx(V, h, L), slice_thr(V, h, L), slice_cold(V, h, L), e, p, U, h.base_peak);
+            }
+        }
         g.choice[a] = d;
         g.chosen_peak[a] = peak;
         g.chosen_over[a] = peak > C ? peak - C : 0;
@@ -735,6 +744,7 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
     a.pkey = w.key;
     a.pdec = w.dec;
     a.G = G;
+    a.policy = policy;
     a.Dg = (D + G - 1) / G;
     a.dev_err = dev_err;
     // Slices are addressed through the decoder headers and bound-checked
