@@ -238,6 +238,7 @@ constexpr int kStage = 6;   // 16-byte units per thread staged in registers: a w
 template <int kAPT>
 struct RecArrivals {
     int32_t p[kAPT], U[kAPT], neg[kAPT];
+    int32_t pU[kAPT];   // p + U, set by the walk without threshold tests
     uint32_t roff[kAPT], mask[kAPT];
     int32_t best_key[kAPT], best_d[kAPT];
 };
@@ -263,7 +264,10 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             e[i] = w[i].y + __popc(w[i].x & s.mask[c + i]);
-            e[i] = e[i] < E ? e[i] : E;   // stays inside the decoder's records
+            if constexpr (kHot)   // LDS only: a rank past E (malformed slice) reads other LDS data, or 0
+                asm("" : "+v"(e[i]));   // opaque: the table address stays one shift-add
+            else
+                e[i] = e[i] < E ? e[i] : E;   // stays inside the decoder's records
             m[i] = pmx[e[i]];
             if constexpr (!kHot) t[i] = thr[e[i]];
         }
@@ -287,7 +291,8 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
             const int k = c + i;
-            const int32_t peak = imax(s.p[k] + pf[i], base);
+            // without a threshold test pf = max(PMX, U), and p + pf = max(p + PMX, p + U)
+            const int32_t peak = kHot ? imax(imax(s.p[k] + m[i], s.pU[k]), base) : imax(s.p[k] + pf[i], base);
             if constexpr (kPairs) store_pair<kFull>(row, k, kHot ? peak : peak | s.neg[k]);
             const int32_t key = select_key<kPolicy>(peak, C, Qm);
             const bool take = key < s.best_key[k];
@@ -375,6 +380,13 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     // rank words and the PMX values, and the thresholds when it tests them
     auto walk = [&](auto hot_tag) {
         constexpr bool kHot = decltype(hot_tag)::value;
+        if constexpr (kHot) {
+#pragma unroll
+            for (int k = 0; k < kAPT; ++k) {
+                s.pU[k] = s.p[k] + s.U[k];
+                asm("" : "+v"(s.pU[k]));   // opaque: keeps max(p + PMX, p + U, base) a single three-way max
+            }
+        }
         auto staged = [&](const DecHeader& h) { return int64_t(half_w) + (kHot ? 1 : 2) * event_units(h.E); };
         auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
         DecLanes lanes = load_lanes(g, V, d_begin, d_end);
