@@ -395,17 +395,19 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         DecHeader h = lane_header(lanes, 0);
         bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
         if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
-        for (int32_t d = d_begin; d < d_end; ++d) {
+        // one step per decoder; unrolled by two so that the buffer is a
+        // compile-time offset where every slice is staged in LDS
+        auto step = [&](int32_t d, auto par_tag) {
+            constexpr bool kOdd = decltype(par_tag)::value;
             const DecHeader cur = h;
             const bool valid = h_ok;
             const bool in_lds = valid && (!kMixed || fits(cur));
-            const int32_t buf = (d - d_begin) & 1;
             const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
             if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
             if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-            int4* slice = lds + buf * buf_units;
+            int4* slice = lds + (kOdd ? (kMixed ? buf_units : kStage * kNT) : 0);
             if (in_lds) {
-                // Buffer `buf` was last read for decoder d-2, which every wave
+                // This buffer was last read for decoder d-2, which every wave
                 // finished before passing the barrier of decoder d-1.  Staged
                 // units past the slice's end (0) stay inside the buffer:
                 // kStage * kNT units fit it.
@@ -425,7 +427,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                     stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
             }
             __syncthreads();
-            if (!valid) continue;
+            if (!valid) return;
             const __amdgpu_buffer_rsrc_t row =
                 buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
             if (!kMixed || in_lds) {
@@ -438,6 +440,10 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                     s, reinterpret_cast<const char*>(slice_rank(V, cur)), slice_pmx(V, cur, L), slice_thr(V, cur, L),
                     slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
             }
+        };
+        for (int32_t d = d_begin; d < d_end; d += 2) {
+            step(d, BoolTag<false>{});
+            if (d + 1 < d_end) step(d + 1, BoolTag<true>{});
         }
     };
     if (all_hot) walk(BoolTag<true>{});
