@@ -184,6 +184,95 @@ def test_record_path_growing_occupancy(orc, policy):
     compare_all(gg, o)
 
 
+def hot_windows(b, U):
+    """Each decoder's hot window recomputed on the host from the definitions:
+    events tau_e (distinct remaining lengths), N_e and S_e over R >= tau_e,
+    PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1)), the threshold T_e (the
+    smallest bound with S_e + U (N_e + 1) > PMX_e), and the bounds landing on
+    e, (tau_{e-1}, tau_e], that reach it; the window lies above event 0's such
+    range and below the first one of a later event (S_E = N_E = 0 after the
+    last event)."""
+    big = 2**31 - 1
+    out = []
+    for d in range(b.decoders):
+        lo, hi = int(b.seg_off[d]), int(b.seg_off[d + 1])
+        p = b.res_prompt[lo:hi].astype(np.int64)
+        g = b.res_gen[lo:hi].astype(np.int64)
+        R = np.maximum(U[lo:hi].astype(np.int64) - g, 0)
+        tau = np.unique(R)
+        E = tau.size
+        N = np.array([(R >= t).sum() for t in tau] + [0], np.int64)
+        S = np.array([(p + g)[R >= t].sum() for t in tau] + [0], np.int64)
+        pmx = [0]
+        for e in range(E):
+            pmx.append(max(pmx[-1], int(S[e] + tau[e] * (N[e] + 1))))
+        win_lo, first = 0, None
+        for e in range(E + 1):
+            n1 = int(N[e]) + 1
+            T = 0 if S[e] > pmx[e] else min((pmx[e] - int(S[e])) // n1 + 1, big)
+            lo_e = 0 if e == 0 else int(tau[e - 1]) + 1
+            hi_e = int(tau[e]) if e < E else big + 1
+            start = max(T, lo_e)
+            if start > hi_e:
+                continue
+            if e == 0:
+                win_lo = min(hi_e + 1, big)
+            elif first is None:
+                first = start
+        out.append((win_lo, (big if first is None else first) - 1))
+    return np.array(out, np.int64)
+
+
+def window_batch(seed):
+    """Record-path decoders of four kinds in groups of two: growing occupancy
+    (short prompts, long remaining lengths: cold ranges right above the first
+    event), long prompts (a window far above u_max), a single resident, and no
+    resident; every arrival has a bound, spread over [1, u_max]."""
+    rng = np.random.default_rng(seed)
+    D, u_max, A = 16, 20000, 20000
+    kinds = [0, 1, 1, 1, 2, 1, 0, 0, 3, 1, 1, 2, 0, 3, 1, 0]
+    counts = [[30, 300, 1, 0][k] for k in kinds]
+    seg = np.zeros(D + 1, np.int64)
+    seg[1:] = np.cumsum(counts)
+    p, g, pred = [], [], []
+    for k, c in zip(kinds, counts):
+        if k == 0:
+            p.append(rng.integers(0, 20, c)); g.append(rng.integers(0, 5, c)); pred.append(rng.integers(5000, u_max, c))
+        else:
+            p.append(rng.integers(5000, 100000, c)); g.append(rng.integers(0, 50, c)); pred.append(rng.integers(1, u_max, c))
+    b = custom_batch(cal_pred=np.arange(1, 21), cal_truth=np.arange(1, 21), edges=[], alpha_ppm=100000, u_max=u_max,
+                     seg_off=seg, res_prompt=np.concatenate(p), res_gen=np.concatenate(g),
+                     res_pred=np.concatenate(pred), arr_prompt=rng.integers(0, 500, size=A),
+                     arr_pred=np.sort(rng.integers(1, u_max + 1, size=A)), capacity=rng.integers(0, 3 * 10**6, size=D),
+                     queue_len=rng.integers(0, 4, size=D))
+    return b
+
+
+def test_hot_window_headers(orc):
+    """The projection's hot window of every decoder equals the one recomputed
+    from the definitions (a window too wide would skip a needed cold record)."""
+    b = window_batch(5)
+    o = oracle_step(b, o=orc)
+    gg = gpu_step(b)
+    assert gg["err"] == 0, gg["errors"]
+    want = hot_windows(b, o["U"][: b.res_pred.size])
+    got = gg["dec_hdr"][:, 6:8].astype(np.int64)
+    say("hot windows", got.tolist())
+    assert np.array_equal(got, want), (got, want)
+    assert (want[:, 0] <= want[:, 1]).any() and (want[:, 0] > want[:, 1]).any()
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_hot_walk_mixed_with_full_walk(orc, policy):
+    """Arrival tiles sorted by bound fall inside, across and outside the hot
+    windows of their decoder groups, so both walks run in one launch."""
+    b = window_batch(6 + policy)
+    o = oracle_step(b, policy=policy, o=orc)
+    gg = gpu_step(b, policy=policy)
+    assert gg["err"] == 0, gg["errors"]
+    compare_all(gg, o)
+
+
 def test_capacity_boundary_and_ties(orc):
     """A peak equal to the capacity is feasible; equal queues and equal slacks
     go to the lowest decoder; all-infeasible arrivals take the largest slack."""
