@@ -31,6 +31,7 @@ namespace {
 
 constexpr int kNT = 512;          // 8 waves per CU: 256 VGPRs per lane for the arrivals
 constexpr size_t kLdsBytes = 160 * 1024;
+constexpr size_t kRedBytes = 256;   // record path: the tile's bound reduction, past the two buffers
 constexpr int kMaxGroups = 8;
 
 struct PlaceArgs {
@@ -223,7 +224,7 @@ __device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, 
 // Record path.
 //
 // Each thread holds kAPT arrivals: prompt, bound, -1/0 for a missing bound,
-// the byte offset of the bound's rank word in a slice and the mask of the
+// the LDS address of the bound's rank word in buffer 0 and the mask of the
 // bits below it (bound clamped to [0, 32 W - 1]), and the running best.
 // The workgroup walks its decoders with two LDS buffers: while decoder d is
 // evaluated from one buffer, the rank words and PMX values (and thresholds,
@@ -243,22 +244,31 @@ struct RecArrivals {
     int32_t best_key[kAPT], best_d[kAPT];
 };
 
-// Evaluate the thread's arrivals against one decoder whose rank words start
-// at `rank`, PMX values at `pmx` and thresholds at `thr` (all in LDS, or all
-// in HBM), with its cold records at `cold` in HBM.  Only lanes whose bound reaches an event's
+// Evaluate the thread's arrivals against one decoder whose PMX values are at
+// `pmx` and thresholds at `thr`, with its cold records at `cold` in HBM.  The
+// thread's rank-word offsets are LDS addresses of buffer 0: with kLds the rank
+// words are read at those addresses plus `rank_lds` (the buffer's offset, a
+// constant where the buffer is fixed), otherwise at `rank_g` plus them (the
+// HBM rank words minus buffer 0's LDS address).  Only lanes whose bound reaches an event's
 // threshold read its cold record.  kHot: every bound of the tile lies in the
 // decoder's hot window (no threshold test) and every arrival has a bound.
-template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kHot>
-__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank, const int32_t* pmx,
-                                             const int32_t* thr, const int2* cold, uint32_t E, int32_t base, int32_t C,
-                                             int32_t Q, int32_t d, __amdgpu_buffer_rsrc_t row) {
+template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kHot, bool kLds>
+__device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* rank_g, uint32_t rank_lds,
+                                             const int32_t* pmx, const int32_t* thr, const int2* cold, uint32_t E,
+                                             int32_t base, int32_t C, int32_t Q, int32_t d,
+                                             __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
     const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
 #pragma unroll
     for (int c = 0; c < kAPT; c += kChunk) {
         uint2 w[kChunk];
 #pragma unroll
-        for (int i = 0; i < kChunk; ++i) w[i] = *reinterpret_cast<const uint2*>(rank + s.roff[c + i]);
+        for (int i = 0; i < kChunk; ++i) {
+            if constexpr (kLds)
+                w[i] = *reinterpret_cast<const __attribute__((address_space(3))) uint2*>(size_t(s.roff[c + i] + rank_lds));
+            else
+                w[i] = *reinterpret_cast<const uint2*>(rank_g + s.roff[c + i]);
+        }
         uint32_t e[kChunk];
         int32_t m[kChunk], t[kChunk];
 #pragma unroll
@@ -329,6 +339,8 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     const int32_t buf_units = g.buf_units;
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
+    // LDS address of buffer 0 (where the dynamic LDS starts)
+    const uint32_t lds_off = uint32_t(size_t((__attribute__((address_space(3))) char*)lds));
     RecArrivals<kAPT> s;
     load_arrivals<kAPT, kFull>(g, a0, gm.tot, s.p, s.U);
 #pragma unroll
@@ -336,13 +348,16 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
         const int32_t U = s.U[k];
         s.neg[k] = U < 0 ? -1 : 0;
         const int32_t uc = U < 0 ? 0 : (U < ucl_max ? U : ucl_max);
-        s.roff[k] = uint32_t(uc >> 5) * 8u;
+        s.roff[k] = uint32_t(uc >> 5) * 8u + lds_off;
+        asm("" : "+v"(s.roff[k]));   // opaque: kept whole, so a read adds only an immediate offset
         s.mask[k] = (1u << (uc & 31)) - 1u;
         s.best_key[k] = INT32_MAX;
         s.best_d[k] = d_begin;
     }
     // smallest and largest bound of the tile, and whether an arrival lacks one
-    __shared__ int32_t red[3][kNT / kWave];
+    // (reduced through LDS past the two buffers: with no static LDS the
+    // buffers start at address 0, so their offsets fold into the LDS reads)
+    int32_t (*red)[kNT / kWave] = reinterpret_cast<int32_t (*)[kNT / kWave]>(lds + 2 * buf_units);
     int32_t t_lo = INT32_MAX, t_hi = -1, t_neg = 0;
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
@@ -432,13 +447,14 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                 buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
             if (!kMixed || in_lds) {
                 const int32_t* pmx = reinterpret_cast<const int32_t*>(slice + half_w);
-                eval_records<kAPT, kFull, kPairs, kPolicy, kHot>(
-                    s, reinterpret_cast<const char*>(slice), pmx, pmx + 4 * event_units(cur.E),
-                    slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+                const uint32_t rank_lds = kOdd ? uint32_t(kMixed ? buf_units : kStage * kNT) * 16u : 0u;
+                eval_records<kAPT, kFull, kPairs, kPolicy, kHot, true>(
+                    s, nullptr, rank_lds, pmx, pmx + 4 * event_units(cur.E), slice_cold(V, cur, L), uint32_t(cur.E),
+                    cur.base_peak, C, Q, d, row);
             } else if constexpr (kMixed) {
-                eval_records<kAPT, kFull, kPairs, kPolicy, false>(
-                    s, reinterpret_cast<const char*>(slice_rank(V, cur)), slice_pmx(V, cur, L), slice_thr(V, cur, L),
-                    slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+                eval_records<kAPT, kFull, kPairs, kPolicy, false, false>(
+                    s, reinterpret_cast<const char*>(slice_rank(V, cur)) - lds_off, 0u, slice_pmx(V, cur, L),
+                    slice_thr(V, cur, L), slice_cold(V, cur, L), uint32_t(cur.E), cur.base_peak, C, Q, d, row);
             }
         };
         for (int32_t d = d_begin; d < d_end; d += 2) {
@@ -777,7 +793,7 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
         // two buffers of kStage * kNT 16-byte units: the staged part of a slice
         const int32_t buf_units = kStage * kNT;
         a.buf_units = L.W / 2 + 64 <= buf_units ? buf_units : 0;
-        lds = size_t(2 * a.buf_units) * 16;
+        lds = size_t(2 * a.buf_units) * 16 + kRedBytes;
     }
     const int64_t tiles = (A + int64_t(kNT) * apt - 1) / (int64_t(kNT) * apt);
     const dim3 grid(unsigned(tiles * G));
