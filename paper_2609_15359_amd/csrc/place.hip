@@ -81,14 +81,27 @@ typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
 // Selection key of a pair as a signed value (smaller is better), with the
 // overflow v = peak - C_d (|v| < 2^31):
-//   MQ: v when infeasible (v > 0), else Q_d - 2^31 (every feasible pair ranks
-//       first, by queue length);   MC: v (largest slack first).
-// Qm is Q_d - 2^31.
+//   MQ: v - 1 when infeasible (v > 0), else Q_d - 2^31 (every feasible pair
+//       ranks first, by queue length);   MC: v (largest slack first).
+// Qm is Q_d - 2^31.  The MQ key is a bit-select on the sign of v - 1 (no
+// compare: a select on a fresh compare result costs wait states on gfx950).
 template <int kPolicy>
 __device__ __forceinline__ int32_t select_key(int32_t peak, int32_t C, int32_t Qm) {
-    const int32_t v = peak - C;
-    if constexpr (kPolicy == MAPS_POLICY_MQ) return v > 0 ? v : Qm;
-    else return v;
+    if constexpr (kPolicy == MAPS_POLICY_MQ) {
+        const int32_t t = int32_t(uint32_t(peak) - uint32_t(C) - 1u);   // v - 1, exact: v > -2^31
+        const int32_t m = t >> 31;                                       // all ones when feasible
+        int32_t key;
+        asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(key) : "v"(m), "s"(Qm), "v"(t));   // m ? Qm : t
+        return key;
+    } else {
+        return peak - C;
+    }
+}
+
+// The peak behind a key that is not a feasible MQ key (MQ: key >= 0).
+template <int kPolicy>
+__device__ __forceinline__ int64_t key_peak(int32_t key, int32_t C) {
+    return int64_t(key) + C + (kPolicy == MAPS_POLICY_MQ ? 1 : 0);
 }
 
 // Per-decoder values of up to 64 consecutive decoders, lane j of every wave
@@ -258,15 +271,18 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
                                              int32_t base, int32_t C, int32_t Q, int32_t d,
                                              __amdgpu_buffer_rsrc_t row) {
     constexpr int kChunk = kAPT < 4 ? kAPT : 4;   // arrivals whose lookups are in flight together
-    const int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
+    int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
+    asm("" : "+s"(Qm));   // kept as is in a scalar register: the key select then needs no source modifier
 #pragma unroll
     for (int c = 0; c < kAPT; c += kChunk) {
         uint2 w[kChunk];
 #pragma unroll
         for (int i = 0; i < kChunk; ++i) {
-            if constexpr (kLds)
-                w[i] = *reinterpret_cast<const __attribute__((address_space(3))) uint2*>(size_t(s.roff[c + i] + rank_lds));
-            else
+            if constexpr (kLds) {
+                const uint64_t x =
+                    *reinterpret_cast<const __attribute__((address_space(3))) uint64_t*>(size_t(s.roff[c + i] + rank_lds));
+                w[i] = make_uint2(uint32_t(x), uint32_t(x >> 32));
+            } else
                 w[i] = *reinterpret_cast<const uint2*>(rank_g + s.roff[c + i]);
         }
         uint32_t e[kChunk];
@@ -619,10 +635,10 @@ __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
 // ---------------------------------------------------------------------------
 // Final choice per arrival: the best group in group order (strictly smaller
 // key wins, so ties keep the lower decoder), the chosen pair's peak, and the
-// outputs; an arrival without a bound goes round-robin.  A key that is the
+// outputs; an arrival without a bound goes round-robin.  A key made from the
 // overflow v = peak - C (policy MC, and MQ without a feasible decoder) gives
-// the peak back as v + C; a feasible MQ choice evaluates its pair once more
-// from the snapshot's records.
+// the peak back; a feasible MQ choice evaluates its pair once more from the
+// snapshot's records.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
     const SnapLayout& L = g.L;
@@ -651,8 +667,10 @@ __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
         d = d < 0 || d >= L.D ? 0 : d;
         const int32_t C = g.cap[d];
         int32_t peak = 0;
-        if (g.policy == MAPS_POLICY_MC || key >= 0) {
-            peak = int32_t(int64_t(key) + C);
+        if (g.policy == MAPS_POLICY_MC) {
+            peak = int32_t(key_peak<MAPS_POLICY_MC>(key, C));
+        } else if (key >= 0) {
+            peak = int32_t(key_peak<MAPS_POLICY_MQ>(key, C));
         } else {
             const DecHeader h = V.dec[d];
             if (slice_ok(h, n_total, L)) {
