@@ -170,7 +170,7 @@ def main():
     place_ms = statistics.mean(ev[2].elapsed_time(ev[3]) for ev in events)
 
     # algorithmic bytes of the placement pass, from the snapshot's own event counts
-    hdr = ws.snapshot[256:256 + 32 * D].view(torch.int32).view(D, 8).cpu().numpy()
+    hdr = ws.snapshot[256:256 + 64 * D].view(torch.int32).view(D, 16).cpu().numpy()
     events_per_decoder = hdr[:, 4]
     W = (((db.u_max + 1) // 32 + 1) + 1) & ~1
     nbytes = placement_bytes(D, A, db.u_max, W, events_per_decoder)

@@ -40,8 +40,11 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // For U < T_e, PF(U) = PMX_e and the cold record is not needed; for U >= T_e,
 // PF(U) = S_e + U (N_e + 1).  A bound lands on event e when tau_{e-1} < U <=
 // tau_e, so the bounds that need a cold record form the ranges
-// [max(T_e, tau_{e-1} + 1), tau_e]; the header's hot window [hot_lo, hot_hi]
-// lies above event 0's range and below every later one.  The rank e = #{events < U} comes from a bitmap
+// [max(T_e, tau_{e-1} + 1), tau_e] for e < E (at e = E, S = N = 0 and
+// max(PMX_E, U) is exact); the header's hot window [hot_lo, hot_hi] lies above
+// event 0's range and below every later one.  PMX_e is nondecreasing: once it
+// reaches PMX_E (at event e*), every bound U >= flat_lo = tau_{e*-1} + 1 that
+// lies in the hot window has PF(U) = max(PMX_E, U), with no lookup at all.  The rank e = #{events < U} comes from a bitmap
 // over the step axis: word w holds bit j for event time 32w + j, next to the
 // number of events before word w.  W words cover [0, 32 W) with 32 W - 1 > u_max,
 // so a bound clamped to 32 W - 1 ranks above every event.  Each decoder's rank
@@ -68,15 +71,18 @@ struct SnapHeader {       // at offset 0, 64 bytes
 };
 static_assert(sizeof(SnapHeader) == 64, "header size");
 
-struct DecHeader {        // one per decoder, 32 bytes
+struct DecHeader {        // one per decoder, 64 bytes
     int64_t slice_off;    // first 16-byte unit of this decoder's slice
     int64_t tot;          // sum_r (p + g + R)
     int32_t E;            // number of events
     int32_t base_peak;    // max_t O(t)
     int32_t hot_lo;       // every bound U in [hot_lo, hot_hi] has PF(U) = max(PMX_e, U):
     int32_t hot_hi;       //   it stays below the threshold of the event it lands on
+    int32_t flat_lo;      // every bound U >= flat_lo lands on an event e with PMX_e = PMX_E
+    int32_t pmx_end;      // PMX_E, the largest S_e + tau_e (N_e + 1)
+    int32_t pad[6];
 };
-static_assert(sizeof(DecHeader) == 32, "decoder header size");
+static_assert(sizeof(DecHeader) == 64, "decoder header size");
 
 // Rank words per decoder: 32 W - 1 > u_max, rounded up to an even count so each
 // decoder's slice starts on a 16-byte boundary.

@@ -110,12 +110,12 @@ __device__ __forceinline__ int64_t key_peak(int32_t key, int32_t C) {
 // no load latency per decoder, and no wait on a fresh load (which would also
 // wait for every store issued before it) inside the decoder loop.
 struct DecLanes {
-    int32_t off_lo, off_hi, E, base, C, Q;
+    int32_t off_lo, off_hi, E, base, C, Q, pmx_end;
 };
 
 __device__ __forceinline__ DecLanes load_lanes(const PlaceArgs& g, const SnapView& V, int32_t d0, int32_t d_end) {
     const int32_t d = d0 + int32_t(threadIdx.x % kWave);
-    DecLanes l{0, 0, -1, -1, 0, 0};
+    DecLanes l{0, 0, -1, -1, 0, 0, 0};
     if (d < d_end) {
         const DecHeader h = V.dec[d];
         l.off_lo = int32_t(uint64_t(h.slice_off));
@@ -124,6 +124,7 @@ __device__ __forceinline__ DecLanes load_lanes(const PlaceArgs& g, const SnapVie
         l.base = h.base_peak;
         l.C = g.cap[d];
         l.Q = g.qlen[d];
+        l.pmx_end = h.pmx_end;
     }
     return l;
 }
@@ -139,6 +140,9 @@ __device__ __forceinline__ DecHeader lane_header(const DecLanes& l, int32_t lane
     h.base_peak = lane_value(l.base, lane);
     h.hot_lo = 1;
     h.hot_hi = 0;
+    h.flat_lo = 1;
+    h.pmx_end = lane_value(l.pmx_end, lane);
+    for (int i = 0; i < 6; ++i) h.pad[i] = 0;
     return h;
 }
 
@@ -149,19 +153,23 @@ struct GroupMax {
     int64_t tot;
     int32_t records;
     int32_t hot_lo, hot_hi;
+    int32_t flat_lo;   // largest max(flat_lo, hot_lo)
 };
 
 __device__ inline GroupMax group_max(const SnapView& V, int32_t d0, int32_t d1) {
     int64_t t = 0;
-    int32_t r = 0, lo = 0, hi = INT32_MAX;
+    int32_t r = 0, lo = 0, hi = INT32_MAX, fl = 0;
     for (int32_t d = d0 + int32_t(threadIdx.x % kWave); d < d1; d += kWave) {
         const DecHeader h = V.dec[d];
         t = t > h.tot ? t : h.tot;
         r = r > h.E + 1 ? r : h.E + 1;
         lo = lo > h.hot_lo ? lo : h.hot_lo;
         hi = hi < h.hot_hi ? hi : h.hot_hi;
+        fl = fl > h.flat_lo ? fl : h.flat_lo;
     }
-    return GroupMax{wave_reduce_max(t), wave_reduce_max(r), wave_reduce_max(lo), -wave_reduce_max(-hi)};
+    lo = wave_reduce_max(lo);
+    fl = wave_reduce_max(fl);
+    return GroupMax{wave_reduce_max(t), wave_reduce_max(r), lo, -wave_reduce_max(-hi), fl > lo ? fl : lo};
 }
 
 // Raw buffer resources (gfx9 descriptor, 32-bit data format): accesses whose
@@ -328,6 +336,25 @@ __device__ __forceinline__ void eval_records(RecArrivals<kAPT>& s, const char* r
     }
 }
 
+// Evaluate the thread's arrivals against one decoder whose bounds all lie in
+// its flat region (and hot window): PF(U) = max(PMX_E, U), so the peak is
+// max(p + PMX_E, p + U, base) with no lookup.
+template <int kAPT, bool kFull, bool kPairs, int kPolicy>
+__device__ __forceinline__ void eval_flat(RecArrivals<kAPT>& s, int32_t pmx_end, int32_t base, int32_t C, int32_t Q,
+                                          int32_t d, __amdgpu_buffer_rsrc_t row) {
+    int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
+    asm("" : "+s"(Qm));
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int32_t peak = imax(imax(s.p[k] + pmx_end, s.pU[k]), base);
+        if constexpr (kPairs) store_pair<kFull>(row, k, peak);
+        const int32_t key = select_key<kPolicy>(peak, C, Qm);
+        const bool take = key < s.best_key[k];
+        s.best_key[k] = take ? key : s.best_key[k];
+        s.best_d[k] = take ? d : s.best_d[k];
+    }
+}
+
 // Load this thread's units of a slice of `units` units into registers: rows
 // j of kNT units that hold part of the slice (a uniform test), with the units
 // past the end of the last one read as 0.
@@ -406,6 +433,8 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     // the tile skips every threshold test when the hot windows of all the
     // group's decoders hold all its bounds (and every arrival has a bound)
     const bool all_hot = !kMixed && t_neg == 0 && t_lo >= gm.hot_lo && t_hi <= gm.hot_hi;
+    // ... and needs no lookup at all when they also lie in every flat region
+    const bool all_flat = t_neg == 0 && t_lo >= gm.flat_lo && t_hi <= gm.hot_hi;
 
     // the decoder walk, with or without the threshold tests: it stages the
     // rank words and the PMX values, and the thresholds when it tests them
@@ -478,7 +507,33 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             if (d + 1 < d_end) step(d + 1, BoolTag<true>{});
         }
     };
-    if (all_hot) walk(BoolTag<true>{});
+    // the walk of a tile in every flat region: no slices, no LDS, no barrier
+    auto flat_walk = [&]() {
+#pragma unroll
+        for (int k = 0; k < kAPT; ++k) {
+            s.pU[k] = s.p[k] + s.U[k];
+            asm("" : "+v"(s.pU[k]));   // opaque: keeps max(p + PMX_E, p + U, base) a single three-way max
+        }
+        DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+        int32_t lanes0 = d_begin;
+        for (int32_t d = d_begin; d < d_end; ++d) {
+            if (d - lanes0 == kWave) {
+                lanes = load_lanes(g, V, d, d_end);
+                lanes0 = d;
+            }
+            const DecHeader h = lane_header(lanes, d - lanes0);
+            const int32_t C = lane_value(lanes.C, d - lanes0), Q = lane_value(lanes.Q, d - lanes0);
+            const bool valid = slice_ok(h, n_total, L);
+            if (threadIdx.x == 0 && (C < 0 || Q < 0)) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+            if (!valid && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+            if (!valid) continue;
+            const __amdgpu_buffer_rsrc_t row =
+                buffer_rsrc(kPairs ? g.pair + int64_t(d) * g.A + a0 : nullptr, kPairs ? uint32_t(tile_n) * 4u : 0u);
+            eval_flat<kAPT, kFull, kPairs, kPolicy>(s, h.pmx_end, h.base_peak, C, Q, d, row);
+        }
+    };
+    if (all_flat) flat_walk();
+    else if (all_hot) walk(BoolTag<true>{});
     else walk(BoolTag<false>{});
     write_partials<kAPT, kFull>(g, grp, a0, s.best_key, s.best_d);
 }

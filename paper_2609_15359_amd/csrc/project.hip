@@ -152,22 +152,25 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     const int32_t base = block_reduce_max<kNT>(bmax, reinterpret_cast<int32_t*>(sc.red32));
 
     // hot window: bounds above event 0's cold range and below the first cold
-    // range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] (to infinity
-    // for e = E); with no event at all the window is empty
-    int32_t lo_w = 0, start_min = INT32_MAX;
-    for (int64_t e = tid; e <= E; e += kNT) {
-        const bool last = e == E;
-        const int64_t T = last ? event_threshold(pmx_end, 0, 1u)
-                               : event_threshold(int32_t(a.M(e)), int32_t(a.S(e)), a.C(e) + 1u);
+    // range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] for e < E (the
+    // last event needs no cold record); flat region: bounds past the first
+    // event e* with PMX_e = PMX_E, i.e. U >= tau_{e*-1} + 1
+    int32_t lo_w = 0, start_min = INT32_MAX, estar = int32_t(E);
+    for (int64_t e = tid; e < E; e += kNT) {
+        const int32_t m = int32_t(a.M(e));
+        if (m == pmx_end && int32_t(e) < estar) estar = int32_t(e);
+        const int64_t T = event_threshold(m, int32_t(a.S(e)), a.C(e) + 1u);
         const int64_t lo_e = e == 0 ? 0 : int64_t(a.T(e - 1)) + 1;
-        const int64_t hi_e = last ? int64_t(INT32_MAX) + 1 : int64_t(a.T(e));
+        const int64_t hi_e = int64_t(a.T(e));
         const int64_t start = T > lo_e ? T : lo_e;
         if (start > hi_e) continue;   // no bound landing on e reaches T_e
-        if (e == 0) lo_w = hi_e >= int64_t(INT32_MAX) ? INT32_MAX : int32_t(hi_e + 1);
+        if (e == 0) lo_w = int32_t(hi_e + 1);
         else if (start < start_min) start_min = int32_t(start);
     }
     const int32_t hot_lo = block_reduce_max<kNT>(lo_w, reinterpret_cast<int32_t*>(sc.red32));
     const int32_t hot_hi = -block_reduce_max<kNT>(-start_min, reinterpret_cast<int32_t*>(sc.red32)) - 1;
+    const int32_t e_star = -block_reduce_max<kNT>(-estar, reinterpret_cast<int32_t*>(sc.red32));
+    const int32_t flat_lo = e_star == 0 ? 0 : int32_t(a.T(e_star - 1)) + 1;
 
     // 5. dense profile F(u) = max(PMX_e, S_e + u (N_e + 1), u), e = #{events < u}
     if (P > 0) {
@@ -218,6 +221,9 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         h.base_peak = base;
         h.hot_lo = hot_lo;
         h.hot_hi = hot_hi;
+        h.flat_lo = flat_lo;
+        h.pmx_end = pmx_end;
+        for (int i = 0; i < 6; ++i) h.pad[i] = 0;
         V.dec[d] = h;
         base_peak[d] = base;
     }

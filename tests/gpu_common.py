@@ -37,10 +37,10 @@ def gpu_step(b: Batch, capacity=None, want_pairs=True, policy=0, rr_offset=0):
         chosen_overflow=pl.chosen_overflow.cpu().numpy(), flags=pl.flags.cpu().numpy(),
         pair_peak=None if pl.pair_peak is None else pl.pair_peak.cpu().numpy(),
         order=out.order.cpu().numpy(), admitted=out.admitted.cpu().numpy())
-    # the snapshot's decoder headers (8 int32 each: slice offset lo/hi, total lo/hi, E, base peak,
-    # hot window low, hot window high), behind its 256-byte header
+    # the snapshot's decoder headers (16 int32 each: slice offset lo/hi, total lo/hi, E, base peak,
+    # hot window low, hot window high, flat region start, PMX_E, padding), behind its 256-byte header
     D = b.decoders
-    res["dec_hdr"] = out.snapshot.data[256:256 + 32 * D].view(torch.int32).view(D, 8).cpu().numpy()
+    res["dec_hdr"] = out.snapshot.data[256:256 + 64 * D].view(torch.int32).view(D, 16).cpu().numpy()
     return res
 
 

@@ -54,7 +54,7 @@ def test_size_queries(lib):
         W = (((u_max + 1) // 32 + 1) + 1) & ~1
         P = (u_max + 4) & ~3 if u_max + 1 <= 16384 else 0
         a = lambda x: (x + 255) // 256 * 256
-        return 256 + a(D * 32) + a(D * P * 4) + (n + D * (3 + W // 2) + 64) * 16
+        return 256 + a(D * 64) + a(D * P * 4) + (n + D * (3 + W // 2) + 64) * 16
     D, n = 4, 100
     for u_max in (0, 1, 8192, 16383, 16384, 65535):
         assert lib.maps_snapshot_bytes(D, n, u_max) == want(D, n, u_max), u_max

@@ -185,13 +185,15 @@ def test_record_path_growing_occupancy(orc, policy):
 
 
 def hot_windows(b, U):
-    """Each decoder's hot window recomputed on the host from the definitions:
-    events tau_e (distinct remaining lengths), N_e and S_e over R >= tau_e,
-    PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1)), the threshold T_e (the
-    smallest bound with S_e + U (N_e + 1) > PMX_e), and the bounds landing on
-    e, (tau_{e-1}, tau_e], that reach it; the window lies above event 0's such
-    range and below the first one of a later event (S_E = N_E = 0 after the
-    last event)."""
+    """Each decoder's hot window and flat region recomputed on the host from
+    the definitions: events tau_e (distinct remaining lengths), N_e and S_e
+    over R >= tau_e, PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1)), the
+    threshold T_e (the smallest bound with S_e + U (N_e + 1) > PMX_e), and the
+    bounds landing on e < E, (tau_{e-1}, tau_e], that reach it (after the last
+    event S_E = N_E = 0 and max(PMX_E, U) is exact); the window lies above
+    event 0's such range and below the first one of a later event.  The flat
+    region starts past the first event e* with PMX_e = PMX_E.  Returns rows
+    (hot_lo, hot_hi, flat_lo, PMX_E)."""
     big = 2**31 - 1
     out = []
     for d in range(b.decoders):
@@ -207,19 +209,21 @@ def hot_windows(b, U):
         for e in range(E):
             pmx.append(max(pmx[-1], int(S[e] + tau[e] * (N[e] + 1))))
         win_lo, first = 0, None
-        for e in range(E + 1):
+        for e in range(E):
             n1 = int(N[e]) + 1
             T = 0 if S[e] > pmx[e] else min((pmx[e] - int(S[e])) // n1 + 1, big)
             lo_e = 0 if e == 0 else int(tau[e - 1]) + 1
-            hi_e = int(tau[e]) if e < E else big + 1
+            hi_e = int(tau[e])
             start = max(T, lo_e)
             if start > hi_e:
                 continue
             if e == 0:
-                win_lo = min(hi_e + 1, big)
+                win_lo = hi_e + 1
             elif first is None:
                 first = start
-        out.append((win_lo, (big if first is None else first) - 1))
+        estar = next(e for e in range(E + 1) if pmx[e] == pmx[E])
+        flat_lo = 0 if estar == 0 else int(tau[estar - 1]) + 1
+        out.append((win_lo, (big if first is None else first) - 1, flat_lo, pmx[E]))
     return np.array(out, np.int64)
 
 
@@ -249,17 +253,19 @@ def window_batch(seed):
 
 
 def test_hot_window_headers(orc):
-    """The projection's hot window of every decoder equals the one recomputed
-    from the definitions (a window too wide would skip a needed cold record)."""
+    """The projection's hot window, flat region start and PMX_E of every
+    decoder equal the ones recomputed from the definitions (a window too wide
+    would skip a needed cold record)."""
     b = window_batch(5)
     o = oracle_step(b, o=orc)
     gg = gpu_step(b)
     assert gg["err"] == 0, gg["errors"]
     want = hot_windows(b, o["U"][: b.res_pred.size])
-    got = gg["dec_hdr"][:, 6:8].astype(np.int64)
-    say("hot windows", got.tolist())
+    got = gg["dec_hdr"][:, 6:10].astype(np.int64)
+    say("hot windows and flat regions", got.tolist())
     assert np.array_equal(got, want), (got, want)
-    assert (want[:, 0] <= want[:, 1]).any() and (want[:, 0] > want[:, 1]).any()
+    # some decoders have a usable flat region, others (growing occupancy) not
+    assert (want[:, 2] <= want[:, 1]).any() and (want[:, 2] > want[:, 1]).any()
 
 
 @pytest.mark.parametrize("policy", [0, 1])
