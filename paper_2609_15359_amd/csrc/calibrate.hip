@@ -27,6 +27,7 @@ namespace maps {
 namespace {
 
 constexpr int kNT = 256;             // threads of the streaming kernels
+constexpr int kApplyPer = 4;         // bounds per cal_apply thread (more waves beat more loads in flight)
 constexpr int kHistNT = 1024;        // threads of the histogram kernel
 constexpr int kLdsEdgesMax = 8192;   // buckets whose edges and sizes fit LDS
 constexpr int kLdsHistBuckets = 128; // buckets whose 256-bin histograms fit LDS
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
         e = le;
         qq = lq;
     }
-    constexpr int kA = 8;   // predictions per thread in flight
+    constexpr int kA = kApplyPer;   // predictions per thread in flight
     const int64_t stride = int64_t(gridDim.x) * kNT * kA;
     for (int64_t c0 = int64_t(blockIdx.x) * kNT * kA; c0 < m; c0 += stride) {
         int32_t p[kA];
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
 // ---------------------------------------------------------------------------
 constexpr int kFastBuckets = 1024;
 constexpr int kSortNT = 256;
-constexpr int kJ = 8;                                   // residuals per thread
+constexpr int kJ = 4;                                   // residuals per thread
 constexpr int64_t kPerBlock = int64_t(kSortNT) * kJ;    // residuals per workgroup of cal_count / cal_scatter
 constexpr int64_t kSortMaxBlocks = 4096;                // larger sets take the all-bucket path
 constexpr int kSelNT = 1024;
@@ -675,7 +676,7 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     }
     if (m > 0) {
         const bool lds_edges = nb <= kLdsEdgesMax;
-        const int g = grid_for(m, kNT, 4, 8192);
+        const int g = grid_for(m, kNT, kApplyPer, 8192);
         if (lds_edges)
             hipLaunchKernelGGL(cal_apply<true>, dim3(g), dim3(kNT), size_t(ne + nb) * 4, stream,
                                apply_pred, m, edges, nb, q_out, u_max, U_out);
