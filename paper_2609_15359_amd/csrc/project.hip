@@ -71,7 +71,30 @@ __device__ inline void phase() {
 struct Scratch {
     int64_t red64[kNT / kWave];
     uint32_t red32[kNT / kWave];
+    int4 red4[kNT / kWave];
 };
+
+// Four workgroup-wide maxima at once (one LDS round instead of four).
+__device__ inline int4 block_reduce_max4(int4 v, int4* tmp) {
+    v.x = wave_reduce_max(v.x);
+    v.y = wave_reduce_max(v.y);
+    v.z = wave_reduce_max(v.z);
+    v.w = wave_reduce_max(v.w);
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    __syncthreads();
+    if (lane == 0) tmp[wid] = v;
+    __syncthreads();
+    int4 r = tmp[0];
+#pragma unroll
+    for (int i = 1; i < kNT / kWave; ++i) {
+        const int4 t = tmp[i];
+        r.x = r.x > t.x ? r.x : t.x;
+        r.y = r.y > t.y ? r.y : t.y;
+        r.z = r.z > t.z ? r.z : t.z;
+        r.w = r.w > t.w ? r.w : t.w;
+    }
+    return r;
+}
 
 template <bool kInLds, typename Arr>
 __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int32_t* __restrict__ p,
@@ -131,11 +154,15 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     }
     phase<kInLds>();
 
-    // 4. N_e and S_e: suffix sums over the events
-    block_scan<kNT, false, true, false, uint32_t>(
-        E, 0u, [&](int64_t e) { return a.C(e); }, [&](int64_t e, uint32_t v) { a.C(e) = v; }, sc.red32);
-    block_scan<kNT, false, true, false, uint32_t>(
-        E, 0u, [&](int64_t e) { return a.S(e); }, [&](int64_t e, uint32_t v) { a.S(e) = v; }, sc.red32);
+    // 4. N_e and S_e: suffix sums over the events, as one scan of (N << 32 | S)
+    //    (S stays below 2^32: a larger total demand is reported as out of range)
+    block_scan<kNT, false, true, false, uint64_t>(
+        E, uint64_t(0), [&](int64_t e) { return (uint64_t(a.C(e)) << 32) | a.S(e); },
+        [&](int64_t e, uint64_t v) {
+            a.C(e) = uint32_t(v >> 32);
+            a.S(e) = uint32_t(v);
+        },
+        reinterpret_cast<uint64_t*>(sc.red64));
     phase<kInLds>();
     // PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1))
     const int32_t pmx_end = block_scan<kNT, true, false, true, int32_t>(
@@ -143,20 +170,15 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         [&](int64_t e) { return int32_t(a.S(e) + a.T(e) * (a.C(e) + 1u)); },
         [&](int64_t e, int32_t v) { a.M(e) = uint32_t(v); }, reinterpret_cast<int32_t*>(sc.red32));
     phase<kInLds>();
-    // base peak = max(0, max_e S_e + tau_e N_e)
-    int32_t bmax = 0;
-    for (int64_t e = tid; e < E; e += kNT) {
-        int32_t o = int32_t(a.S(e) + a.T(e) * a.C(e));
-        bmax = bmax > o ? bmax : o;
-    }
-    const int32_t base = block_reduce_max<kNT>(bmax, reinterpret_cast<int32_t*>(sc.red32));
-
+    // base peak = max(0, max_e S_e + tau_e N_e);
     // hot window: bounds above event 0's cold range and below the first cold
     // range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] for e < E (the
     // last event needs no cold record); flat region: bounds past the first
     // event e* with PMX_e = PMX_E, i.e. U >= tau_{e*-1} + 1
-    int32_t lo_w = 0, start_min = INT32_MAX, estar = int32_t(E);
+    int32_t bmax = 0, lo_w = 0, start_min = INT32_MAX, estar = int32_t(E);
     for (int64_t e = tid; e < E; e += kNT) {
+        const int32_t o = int32_t(a.S(e) + a.T(e) * a.C(e));
+        bmax = bmax > o ? bmax : o;
         const int32_t m = int32_t(a.M(e));
         if (m == pmx_end && int32_t(e) < estar) estar = int32_t(e);
         const int64_t T = event_threshold(m, int32_t(a.S(e)), a.C(e) + 1u);
@@ -167,9 +189,8 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         if (e == 0) lo_w = int32_t(hi_e + 1);
         else if (start < start_min) start_min = int32_t(start);
     }
-    const int32_t hot_lo = block_reduce_max<kNT>(lo_w, reinterpret_cast<int32_t*>(sc.red32));
-    const int32_t hot_hi = -block_reduce_max<kNT>(-start_min, reinterpret_cast<int32_t*>(sc.red32)) - 1;
-    const int32_t e_star = -block_reduce_max<kNT>(-estar, reinterpret_cast<int32_t*>(sc.red32));
+    const int4 r = block_reduce_max4(make_int4(bmax, lo_w, -start_min, -estar), sc.red4);
+    const int32_t base = r.x, hot_lo = r.y, hot_hi = -r.z - 1, e_star = -r.w;
     const int32_t flat_lo = e_star == 0 ? 0 : int32_t(a.T(e_star - 1)) + 1;
 
     // 5. dense profile F(u) = max(PMX_e, S_e + u (N_e + 1), u), e = #{events < u}
