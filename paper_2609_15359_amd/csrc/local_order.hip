@@ -5,6 +5,7 @@
 //      bound, index) -- unique keys, so the order is the stable one;
 //   2. a second bitonic sort of (bound, index) gives the queue by bound, with
 //      the start of each run of equal bounds;
+//   (a queue of at most 64 requests is sorted in the lanes of one wavefront);
 //   3. admitted = the largest k whose prefix keeps the projected peak within
 //      the capacity, by binary search over k (the peak never decreases when a
 //      request is added).  For a prefix, residents plus admitted requests form
@@ -64,6 +65,23 @@ __device__ void bitonic_sort(uint64_t* keys, int n2) {
             __syncthreads();
         }
     }
+}
+
+// Ascending sort of one key per lane across a wavefront (bitonic network
+// through lane shuffles: no LDS, no barrier).
+__device__ inline uint64_t wave_bitonic(uint64_t key) {
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const uint64_t other = __shfl_xor(key, j, kWave);
+            const bool ascending = (lane & k) == 0;
+            const bool lower = (lane & j) == 0;
+            key = (lower == ascending) ? (key < other ? key : other) : (key > other ? key : other);
+        }
+    }
+    return key;
 }
 
 // Largest projected peak of the residents plus the first k requests of the new order.
@@ -145,44 +163,81 @@ __global__ __launch_bounds__(kNT) void local_order_kernel(LocalArgs g) {
     int n2 = 1;
     while (n2 < n) n2 <<= 1;
 
-    // 1. the new order (Eq. (7) with promotion)
-    bool neg = false;
-    for (int i = threadIdx.x; i < n2; i += kNT) {
-        if (i < n) {
-            int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
-            neg |= pr < 0;
-            s.pp[i] = pr < 0 ? 0 : pr;
-            const int32_t ue = u < 0 ? L.u_max : u;
-            s.ue[i] = ue;
-            const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
-            const uint64_t cls = promoted ? 0ull : (1ull << 63);
-            const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
-            s.keys[i] = cls | (val << 32) | uint64_t(uint32_t(i));
-        } else {
-            s.keys[i] = ~0ull;
+    if (n2 <= kWave) {
+        // a queue of at most one wavefront: both sorts and the runs of equal
+        // bounds in the lanes of wave 0 (key i in lane i)
+        if (threadIdx.x < kWave) {
+            const int i = threadIdx.x;
+            uint64_t key = ~0ull, key2 = ~0ull;
+            bool neg = false;
+            if (i < n) {
+                const int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
+                neg = pr < 0;
+                s.pp[i] = pr < 0 ? 0 : pr;
+                const int32_t ue = u < 0 ? L.u_max : u;
+                s.ue[i] = ue;
+                const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
+                const uint64_t cls = promoted ? 0ull : (1ull << 63);
+                const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
+                key = cls | (val << 32) | uint64_t(uint32_t(i));
+                key2 = (uint64_t(uint32_t(ue)) << 32) | uint64_t(uint32_t(i));
+            }
+            if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+            key = wave_bitonic(key);
+            key2 = wave_bitonic(key2);
+            if (i < n) {
+                const int idx = int(uint32_t(key));
+                g.order[qlo + i] = idx;
+                s.pos[idx] = i;
+                s.uidx[i] = int(uint32_t(key2));
+            }
+            const uint32_t b = uint32_t(key2 >> 32);
+            const uint32_t prev = __shfl_up(b, 1, kWave);
+            const int32_t start = (i == 0 || prev != b) ? i : 0;
+            const int32_t run = wave_incl_scan_max(start);
+            if (i < n) s.grp[i] = run;
         }
-    }
-    if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-    __syncthreads();
-    bitonic_sort(s.keys, n2);
-    for (int i = threadIdx.x; i < n; i += kNT) {
-        const int idx = int(uint32_t(s.keys[i]));
-        g.order[qlo + i] = idx;
-        s.pos[idx] = i;
-    }
-    __syncthreads();
+        __syncthreads();
+    } else {
+        // 1. the new order (Eq. (7) with promotion)
+        bool neg = false;
+        for (int i = threadIdx.x; i < n2; i += kNT) {
+            if (i < n) {
+                int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
+                neg |= pr < 0;
+                s.pp[i] = pr < 0 ? 0 : pr;
+                const int32_t ue = u < 0 ? L.u_max : u;
+                s.ue[i] = ue;
+                const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
+                const uint64_t cls = promoted ? 0ull : (1ull << 63);
+                const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
+                s.keys[i] = cls | (val << 32) | uint64_t(uint32_t(i));
+            } else {
+                s.keys[i] = ~0ull;
+            }
+        }
+        if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+        __syncthreads();
+        bitonic_sort(s.keys, n2);
+        for (int i = threadIdx.x; i < n; i += kNT) {
+            const int idx = int(uint32_t(s.keys[i]));
+            g.order[qlo + i] = idx;
+            s.pos[idx] = i;
+        }
+        __syncthreads();
 
-    // 2. the queue sorted by bound
-    for (int i = threadIdx.x; i < n2; i += kNT)
-        s.keys[i] = i < n ? ((uint64_t(uint32_t(s.ue[i])) << 32) | uint64_t(uint32_t(i))) : ~0ull;
-    __syncthreads();
-    bitonic_sort(s.keys, n2);
-    for (int i = threadIdx.x; i < n; i += kNT) s.uidx[i] = int(uint32_t(s.keys[i]));
-    __syncthreads();
-    block_scan<kNT, true, false, false, int32_t>(
-        n, 0,
-        [&](int64_t i) { return (i == 0 || s.ue[s.uidx[i - 1]] != s.ue[s.uidx[i]]) ? int32_t(i) : 0; },
-        [&](int64_t i, int32_t v) { s.grp[i] = v; }, s.red32);
+        // 2. the queue sorted by bound
+        for (int i = threadIdx.x; i < n2; i += kNT)
+            s.keys[i] = i < n ? ((uint64_t(uint32_t(s.ue[i])) << 32) | uint64_t(uint32_t(i))) : ~0ull;
+        __syncthreads();
+        bitonic_sort(s.keys, n2);
+        for (int i = threadIdx.x; i < n; i += kNT) s.uidx[i] = int(uint32_t(s.keys[i]));
+        __syncthreads();
+        block_scan<kNT, true, false, false, int32_t>(
+            n, 0,
+            [&](int64_t i) { return (i == 0 || s.ue[s.uidx[i - 1]] != s.ue[s.uidx[i]]) ? int32_t(i) : 0; },
+            [&](int64_t i, int32_t v) { s.grp[i] = v; }, s.red32);
+    }
 
     // 3. admission: largest k with peak(k) <= C
     const uint2* rank = slice_rank(V, h);
