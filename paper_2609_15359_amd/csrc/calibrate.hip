@@ -4,20 +4,20 @@
 // score s = max(0, L - L_hat), k_b = ceil((1 - alpha)(n_b + 1)) (infinite when
 // k_b > n_b); every bound is then U = min(L_hat + q_b, u_max).
 //
-// Up to 1,024 buckets (and 8.4M residuals): a counting sort by bucket, then
-// one workgroup per bucket selects.
-//   cal_count         scores' buckets (binary search of the edges in LDS):
-//                     per-workgroup bucket sizes and the largest score;
-//   cal_offsets       per bucket: exclusive scan of the workgroups' sizes, the
-//                     bucket size n_b, k_b, the largest score;
-//   cal_scatter       each workgroup sorts its scores by bucket in LDS and
-//                     writes every run to its place, bucket-major;
-//   cal_bucket_select per bucket: most-significant-digit-first radix select
-//                     of the k_b-th score over its run (kept in registers),
-//                     8 bits a pass from the top digit of the largest score,
-//                     histograms in LDS;
+// Up to 1,024 buckets (and 4.2M residuals): chunks sorted by bucket, then one
+// workgroup per bucket selects.
+//   cal_chunk_sort    per chunk of 4,096 residuals: scores and buckets (binary
+//                     search of the edges in LDS), a counting sort of the
+//                     chunk by bucket in LDS written back contiguously, the
+//                     size and start of every bucket's run in the chunk, the
+//                     chunk's largest score;
+//   cal_bucket_select per bucket: n_b and k_b from its runs' sizes, its runs
+//                     gathered into LDS and registers, then a most-
+//                     significant-digit-first radix select of the k_b-th
+//                     score, 8 bits a pass from the top digit of the largest
+//                     score, histograms in LDS;
 //   cal_apply         U = min(L_hat + q_b, u_max).
-// More buckets: the same select over all buckets at once, one histogram
+// More buckets or residuals: the same select over all buckets at once, one histogram
 // pass and one selection kernel per 8-bit digit (cal_score, cal_rank,
 // cal_hist, cal_select, cal_finish), histograms in LDS for up to 128 buckets.
 // All reductions are integer additions, so the result is deterministic.
@@ -283,44 +283,43 @@ __global__ __launch_bounds__(kNT) void cal_apply(const int32_t* __restrict__ pre
 // Counting-sort path (nb <= kFastBuckets)
 // ---------------------------------------------------------------------------
 constexpr int kFastBuckets = 1024;
-constexpr int kSortNT = 256;
-constexpr int kJ = 4;                                   // residuals per thread
-constexpr int64_t kPerBlock = int64_t(kSortNT) * kJ;    // residuals per workgroup of cal_count / cal_scatter
-constexpr int64_t kSortMaxBlocks = 4096;                // larger sets take the all-bucket path
+constexpr int kSortNT = 1024;
+constexpr int kJ = 4;                                  // residuals per thread
+constexpr int64_t kChunk = int64_t(kSortNT) * kJ;      // residuals per workgroup of cal_chunk_sort
+constexpr int64_t kSortMaxChunks = 1024;               // larger sets take the all-bucket path
 constexpr int kSelNT = 1024;
-constexpr int kKeep = 24;   // scores per thread the bucket select keeps in registers across passes
+constexpr int kSelWaves = kSelNT / kWave;
+constexpr int kKeep = 24;         // scores per thread the bucket select keeps in registers across passes
+constexpr int kGatherRuns = 16;   // runs a wavefront of the select loads at once
+constexpr size_t kSelStageBytes = size_t(kSelNT) * kKeep * 4;
+static_assert(kSortMaxChunks <= kSelNT, "the select holds one run of its bucket per thread");
+static_assert(kKeep % 4 == 0 && kGatherRuns <= kWave, "select slots come in groups of four");
 
-int64_t sort_blocks(int64_t n) { return (n + kPerBlock - 1) / kPerBlock; }
+int64_t sort_chunks(int64_t n) { return (n + kChunk - 1) / kChunk; }
 
 struct FastWorkspace {
-    uint32_t* cnt_part;   // [nb][blocks] bucket sizes of each workgroup
-    uint32_t* off_part;   // [nb][blocks] where each workgroup's run starts inside the bucket
-    uint32_t* max_part;   // [blocks] largest score of each workgroup
-    uint32_t* bcount;     // [nb] bucket sizes
-    uint32_t* bmax;       // [nb] largest score (the same for every bucket)
-    int32_t* krank;       // [nb] k_b, -1 when the quantile is infinite
-    int32_t* sorted;      // [n] scores, bucket-major
+    uint32_t* run_cnt;     // [nb][chunks] scores of bucket b in chunk c (the run of b in c)
+    uint32_t* run_start;   // [nb][chunks] where that run starts inside its chunk
+    uint32_t* max_part;    // [chunks] largest score of each chunk
+    int32_t* sorted;       // [n] scores, every chunk of kChunk sorted by bucket
     size_t bytes;
 };
 
 FastWorkspace fast_carve(void* base, int64_t n, int32_t nb) {
-    const int64_t blocks = sort_blocks(n);
+    const int64_t chunks = sort_chunks(n);
     FastWorkspace w;
     size_t off = 0;
     char* p = static_cast<char*>(base);
     auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
-    w.cnt_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * nb * 4));
-    w.off_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * nb * 4));
-    w.max_part = reinterpret_cast<uint32_t*>(take(size_t(blocks) * 4));
-    w.bcount = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
-    w.bmax = reinterpret_cast<uint32_t*>(take(size_t(nb) * 4));
-    w.krank = reinterpret_cast<int32_t*>(take(size_t(nb) * 4));
+    w.run_cnt = reinterpret_cast<uint32_t*>(take(size_t(chunks) * nb * 4));
+    w.run_start = reinterpret_cast<uint32_t*>(take(size_t(chunks) * nb * 4));
+    w.max_part = reinterpret_cast<uint32_t*>(take(size_t(chunks) * 4));
     w.sorted = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
     w.bytes = off;
     return w;
 }
 
-bool fast_path(int64_t n, int32_t nb) { return nb <= kFastBuckets && sort_blocks(n) <= kSortMaxBlocks; }
+bool fast_path(int64_t n, int32_t nb) { return nb <= kFastBuckets && sort_chunks(n) <= kSortMaxChunks; }
 
 // Score of one residual (Eq. (2)): max(0, L - L_hat), saturated at INT32_MAX.
 __device__ inline int32_t score_of(int32_t p, int32_t t) {
@@ -328,135 +327,94 @@ __device__ inline int32_t score_of(int32_t p, int32_t t) {
     return d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
 }
 
-// The kJ residuals of this thread in workgroup blockIdx.x: prompt
-// prediction, score, bucket; `valid` masks the ones past n.
+// The kJ residuals of this thread in chunk blockIdx.x: prompt prediction,
+// score, bucket; `valid` masks the ones past n.
 struct Residuals {
     int32_t p[kJ], s[kJ];
     int b[kJ];
     bool valid[kJ];
 };
 
-__device__ inline void load_residuals(const int32_t* __restrict__ pred, const int32_t* __restrict__ truth, int64_t n,
-                                      const int32_t* le, int ne, Residuals& r, bool& bad) {
-    const int64_t lo = int64_t(blockIdx.x) * kPerBlock;
-    int32_t t[kJ];
+// Loads only: issued before the workgroup stages its tables, so that both
+// latencies overlap.
+__device__ inline void fetch_residuals(const int32_t* __restrict__ pred, const int32_t* __restrict__ truth,
+                                       int64_t n, Residuals& r) {
+    const int64_t lo = int64_t(blockIdx.x) * kChunk;
 #pragma unroll
     for (int j = 0; j < kJ; ++j) {
         const int64_t i = lo + int64_t(j) * kSortNT + threadIdx.x;
         r.valid[j] = i < n;
         r.p[j] = r.valid[j] ? pred[i] : 0;
-        t[j] = r.valid[j] ? truth[i] : 0;
-    }
-    buckets_of<kJ>(le, ne, r.p, r.b);
-#pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-        bad |= r.valid[j] & ((r.p[j] < 0) | (t[j] < 0));
-        r.s[j] = score_of(r.p[j], t[j]);
+        r.s[j] = r.valid[j] ? truth[i] : 0;   // the true length until classify_residuals
     }
 }
 
-__global__ __launch_bounds__(kSortNT) void cal_count(const int32_t* __restrict__ pred,
-                                                     const int32_t* __restrict__ truth, int64_t n,
-                                                     const int32_t* __restrict__ edges, int nb, int64_t blocks,
-                                                     uint32_t* __restrict__ cnt_part, uint32_t* __restrict__ max_part,
-                                                     uint32_t* dev_err) {
-    extern __shared__ int32_t lds[];
+__device__ inline void classify_residuals(const int32_t* le, int ne, Residuals& r, bool& bad) {
+    buckets_of<kJ>(le, ne, r.p, r.b);
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) {
+        bad |= r.valid[j] & ((r.p[j] < 0) | (r.s[j] < 0));
+        r.s[j] = score_of(r.p[j], r.s[j]);
+    }
+}
+
+// One workgroup per chunk of kChunk residuals: scores and buckets, then a
+// counting sort of the chunk by bucket in LDS, written back in place of the
+// chunk (one 16-byte store a thread); the size and start of every bucket's
+// run in the chunk, bucket-major; the chunk's largest score.
+__global__ __launch_bounds__(kSortNT) void cal_chunk_sort(const int32_t* __restrict__ pred,
+                                                          const int32_t* __restrict__ truth, int64_t n,
+                                                          const int32_t* __restrict__ edges, int nb, int64_t chunks,
+                                                          uint32_t* __restrict__ run_cnt,
+                                                          uint32_t* __restrict__ run_start,
+                                                          uint32_t* __restrict__ max_part,
+                                                          int32_t* __restrict__ sorted, uint32_t* dev_err) {
+    extern __shared__ __align__(16) int32_t chunk_lds[];
     __shared__ uint32_t red[kSortNT / kWave];
+    Residuals r;
+    fetch_residuals(pred, truth, n, r);
     const int ne = nb - 1;
-    int32_t* le = lds;
-    uint32_t* lc = reinterpret_cast<uint32_t*>(lds + ne);
+    int32_t* lsort = chunk_lds;                                            // [kChunk] scores by bucket
+    int32_t* le = lsort + kChunk;                                    // [ne]
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(le + ne);           // [nb] run sizes, then run starts
     for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
-    for (int i = threadIdx.x; i < nb; i += kSortNT) lc[i] = 0;
+    for (int i = threadIdx.x; i < nb; i += kSortNT) lcnt[i] = 0;
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i + 1 < ne; i += kSortNT)
             if (edges[i] > edges[i + 1]) raise_error(dev_err, MAPS_ERR_EDGES_UNSORTED);
     __syncthreads();
-    Residuals r;
     bool bad = false;
-    load_residuals(pred, truth, n, le, ne, r, bad);
+    classify_residuals(le, ne, r, bad);
+    uint32_t rank[kJ];
     uint32_t mx = 0;
 #pragma unroll
     for (int j = 0; j < kJ; ++j) {
-        if (!r.valid[j]) continue;
-        atomicAdd(&lc[r.b[j]], 1u);
-        mx = mx > uint32_t(r.s[j]) ? mx : uint32_t(r.s[j]);
+        rank[j] = r.valid[j] ? atomicAdd(&lcnt[r.b[j]], 1u) : 0u;
+        if (r.valid[j]) mx = mx > uint32_t(r.s[j]) ? mx : uint32_t(r.s[j]);
     }
     if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
-    mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the counts are complete
-    for (int b = threadIdx.x; b < nb; b += kSortNT) cnt_part[int64_t(b) * blocks + blockIdx.x] = lc[b];
-    if (threadIdx.x == 0) max_part[blockIdx.x] = mx;
-}
-
-__global__ __launch_bounds__(kSortNT) void cal_offsets(int nb, int64_t blocks, int32_t alpha_ppm,
-                                                       const uint32_t* __restrict__ cnt_part,
-                                                       const uint32_t* __restrict__ max_part,
-                                                       uint32_t* __restrict__ off_part, uint32_t* __restrict__ bcount,
-                                                       uint32_t* __restrict__ bmax, int32_t* __restrict__ krank) {
-    __shared__ uint32_t tmp[kSortNT / kWave];
-    const int b = blockIdx.x;
-    const uint32_t* col = cnt_part + int64_t(b) * blocks;
-    uint32_t* ocol = off_part + int64_t(b) * blocks;
-    const uint32_t total = block_scan<kSortNT, false, false, true, uint32_t>(
-        blocks, 0u, [&](int64_t i) { return col[i]; }, [&](int64_t i, uint32_t v) { ocol[i] = v; }, tmp);
-    uint32_t mx = 0;
-    for (int64_t i = threadIdx.x; i < blocks; i += kSortNT) mx = mx > max_part[i] ? mx : max_part[i];
-    mx = block_reduce_max<kSortNT>(mx, tmp);
-    if (threadIdx.x == 0) {
-        const int64_t nbk = total;
-        const int64_t k = (int64_t(1000000 - alpha_ppm) * (nbk + 1) + 999999) / 1000000;  // Eq. (3)
-        bcount[b] = total;
-        bmax[b] = mx;
-        krank[b] = k <= nbk ? int32_t(k) : -1;
-    }
-}
-
-// Each workgroup sorts its residuals' scores by bucket in LDS, then writes
-// every bucket's run to its place in the bucket-major array (consecutive
-// scores of a run go to consecutive addresses).
-__global__ __launch_bounds__(kSortNT) void cal_scatter(const int32_t* __restrict__ pred,
-                                                       const int32_t* __restrict__ truth, int64_t n,
-                                                       const int32_t* __restrict__ edges, int nb, int64_t blocks,
-                                                       const uint32_t* __restrict__ bcount,
-                                                       const uint32_t* __restrict__ off_part,
-                                                       int32_t* __restrict__ sorted) {
-    extern __shared__ int32_t lds[];
-    __shared__ uint32_t tmp[kSortNT / kWave];
-    const int ne = nb - 1;
-    int32_t* le = lds;                                              // [ne]
-    uint32_t* lcnt = reinterpret_cast<uint32_t*>(le + ne);          // [nb] local sizes, then local starts
-    uint32_t* gdst = lcnt + nb;                                     // [nb] global start of the local run
-    int32_t* lsort = reinterpret_cast<int32_t*>(gdst + nb);         // [kPerBlock] scores by bucket
-    uint16_t* lbkt = reinterpret_cast<uint16_t*>(lsort + kPerBlock);   // [kPerBlock] their buckets
-    for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
-    for (int i = threadIdx.x; i < nb; i += kSortNT) lcnt[i] = 0;
-    // start of each bucket's run in the bucket-major array
+    mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the run sizes are complete
+    const int64_t c = blockIdx.x;
     block_scan<kSortNT, false, false, true, uint32_t>(
-        nb, 0u, [&](int64_t i) { return bcount[i]; }, [&](int64_t i, uint32_t v) { gdst[i] = v; }, tmp);
-    for (int b = threadIdx.x; b < nb; b += kSortNT) gdst[b] += off_part[int64_t(b) * blocks + blockIdx.x];
-    Residuals r;
-    bool bad = false;
-    load_residuals(pred, truth, n, le, ne, r, bad);
-    uint32_t rank[kJ];
+        nb, 0u, [&](int64_t i) { return lcnt[i]; },
+        [&](int64_t i, uint32_t v) {
+            run_cnt[i * chunks + c] = lcnt[i];
+            run_start[i * chunks + c] = v;
+            lcnt[i] = v;
+        },
+        red);   // ends with a barrier: the run starts are complete
 #pragma unroll
-    for (int j = 0; j < kJ; ++j) rank[j] = r.valid[j] ? atomicAdd(&lcnt[r.b[j]], 1u) : 0u;
+    for (int j = 0; j < kJ; ++j)
+        if (r.valid[j]) lsort[lcnt[r.b[j]] + rank[j]] = r.s[j];
     __syncthreads();
-    block_scan<kSortNT, false, false, true, uint32_t>(
-        nb, 0u, [&](int64_t i) { return lcnt[i]; }, [&](int64_t i, uint32_t v) { lcnt[i] = v; }, tmp);
-#pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-        if (!r.valid[j]) continue;
-        const uint32_t at = lcnt[r.b[j]] + rank[j];
-        lsort[at] = r.s[j];
-        lbkt[at] = uint16_t(r.b[j]);
+    const int64_t lo = c * kChunk;
+    const int cnt = int(n - lo < kChunk ? n - lo : kChunk);
+    if (cnt == kChunk) {
+        reinterpret_cast<int4*>(sorted + lo)[threadIdx.x] = reinterpret_cast<const int4*>(lsort)[threadIdx.x];
+    } else {
+        for (int i = threadIdx.x; i < cnt; i += kSortNT) sorted[lo + i] = lsort[i];
     }
-    __syncthreads();
-    const int64_t lo = int64_t(blockIdx.x) * kPerBlock;
-    const int cnt = int(n - lo < kPerBlock ? n - lo : kPerBlock);
-    for (int i = threadIdx.x; i < cnt; i += kSortNT) {
-        const int b = lbkt[i];
-        const uint32_t pos = gdst[b] + uint32_t(i) - lcnt[b];
-        if (pos < uint64_t(n)) sorted[pos] = lsort[i];   // always: the runs partition [0, n)
-    }
+    if (threadIdx.x == 0) max_part[c] = mx;
 }
 
 // Digit of the k-th element among the 256 bins of hist (one wavefront).
@@ -474,85 +432,136 @@ __device__ inline void pick_digit(const uint32_t* hist, int32_t k, uint32_t* pic
     }
 }
 
-// Histogram update of one score's digit; the lanes holding the first active
-// lane's digit add it with one atomic.
-__device__ inline void hist_add(uint32_t* hist, uint32_t digit) {
-    const uint32_t lead = __builtin_amdgcn_readfirstlane(digit);
-    const uint64_t same = __ballot(digit == lead);
-    if (digit != lead) atomicAdd(&hist[digit], 1u);
-    else if (int(threadIdx.x % kWave) == __ffsll((unsigned long long)same) - 1)
-        atomicAdd(&hist[lead], uint32_t(__popcll(same)));
+// Histogram update of one score's digit when `take`.  Digit 0 is the common
+// one (every score of zero, and short scores on the top digit): those lanes
+// are counted by a ballot into the wavefront-uniform `zeros`, which the
+// caller adds to bin 0 once; the other lanes add one each.  Called by whole
+// wavefronts.
+__device__ inline void hist_add(uint32_t* hist, bool take, uint32_t digit, uint32_t& zeros) {
+    zeros += uint32_t(__popcll(__ballot(take && digit == 0)));
+    if (take && digit != 0) atomicAdd(&hist[digit], 1u);
 }
 
-// One workgroup per bucket: the k_b-th smallest score of its run, most
-// significant 8-bit digit first from the top digit of the largest score.  A
-// run of at most kSelNT * kKeep scores stays in registers across passes.
-__global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, const int32_t* __restrict__ sorted,
-                                                            const uint32_t* __restrict__ bcount,
-                                                            const uint32_t* __restrict__ bmax,
-                                                            const int32_t* __restrict__ krank,
+__device__ inline void hist_flush_zeros(uint32_t* hist, uint32_t zeros) {
+    if ((threadIdx.x % kWave) == 0 && zeros != 0) atomicAdd(&hist[0], zeros);
+}
+
+// One workgroup per bucket: its size n_b and rank k_b (Eq. (3)) from the
+// run sizes, then the k_b-th smallest score of its runs, most significant
+// 8-bit digit first from the top digit of the largest score.  A bucket of at
+// most kSelNT * kKeep scores is gathered once (runs into LDS, then into
+// registers) and kept across passes; a larger one is read from its runs on
+// every pass.
+__global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, int64_t chunks, int32_t alpha_ppm,
+                                                            const int32_t* __restrict__ sorted,
+                                                            const uint32_t* __restrict__ run_cnt,
+                                                            const uint32_t* __restrict__ run_start,
+                                                            const uint32_t* __restrict__ max_part,
                                                             int32_t* __restrict__ q_out,
                                                             int32_t* __restrict__ count_out) {
+    extern __shared__ __align__(16) uint32_t stage[];   // [kSelNT * kKeep] the bucket's scores
+    __shared__ uint32_t roff[kSortMaxChunks];           // where each run starts among the bucket's scores
+    __shared__ uint32_t rcnt[kSortMaxChunks];           // its size
+    __shared__ uint32_t rsrc[kSortMaxChunks];           // its first score's index in `sorted`
     __shared__ uint32_t hist[256];
-    __shared__ uint32_t red[kSelNT / kWave];
+    __shared__ uint32_t red[kSelWaves];
     __shared__ uint32_t pick[2];
     const int b = blockIdx.x;
-    uint32_t before = 0;
-    for (int i = threadIdx.x; i < b; i += kSelNT) before += bcount[i];
-    const uint32_t base = block_reduce_add<kSelNT>(before, red);
-    const uint32_t nbk = bcount[b];
-    int32_t k = krank[b];
-    if (threadIdx.x == 0) count_out[b] = int32_t(nbk);
-    if (k < 0) {
-        if (threadIdx.x == 0) q_out[b] = MAPS_Q_INF;
+    const int t = threadIdx.x;
+    const int lane = t % kWave, w = t / kWave;
+    uint32_t c = 0, m = 0, src = 0;
+    if (t < chunks) {
+        c = run_cnt[int64_t(b) * chunks + t];
+        src = uint32_t(t * kChunk) + run_start[int64_t(b) * chunks + t];
+        m = max_part[t];
+    }
+    uint32_t nbk;
+    const uint32_t off = block_excl_scan<kSelNT, false>(c, 0u, red, &nbk);
+    if (t < chunks) {
+        roff[t] = off;
+        rcnt[t] = c;
+        rsrc[t] = src;
+    }
+    const uint32_t mx = block_reduce_max<kSelNT>(m, red);   // its barriers publish the run tables
+    const int64_t k64 = (int64_t(1000000 - alpha_ppm) * (int64_t(nbk) + 1) + 999999) / 1000000;   // Eq. (3)
+    if (t == 0) count_out[b] = int32_t(nbk);
+    if (k64 > int64_t(nbk)) {
+        if (t == 0) q_out[b] = MAPS_Q_INF;
         return;
     }
-    const uint32_t mx = bmax[b];
+    int32_t k = int32_t(k64);
     const int top = mx >> 24 ? 24 : (mx >> 16 ? 16 : (mx >> 8 ? 8 : 0));
-    const int32_t* v = sorted + base;
     const bool in_regs = nbk <= uint32_t(kSelNT) * kKeep;
-    uint32_t x[kKeep];
+    // Slot j = 4g + e of thread t holds score g * 4 * kSelNT + 4t + e of the
+    // bucket (16-byte LDS reads); groups past n_b are skipped whole.
+    uint32_t x[kKeep] = {};
+    auto slot = [&](int j) { return uint32_t(j / 4) * (4 * kSelNT) + 4 * uint32_t(t) + uint32_t(j % 4); };
     if (in_regs) {
+        // wavefront w gathers runs w, w + kSelWaves, ...: the first 128
+        // scores of kGatherRuns runs in flight per lane, longer runs' rest
+        // after.  Lane q reads run q's table entry; the wavefront shares it.
+        for (int64_t r0 = w; r0 < chunks; r0 += int64_t(kSelWaves) * kGatherRuns) {
+            const int64_t rq = r0 + int64_t(lane) * kSelWaves;
+            const bool has = lane < kGatherRuns && rq < chunks;
+            const uint32_t tc = has ? rcnt[rq] : 0u, ts = has ? rsrc[rq] : 0u, to = has ? roff[rq] : 0u;
+            uint32_t v0[kGatherRuns], v1[kGatherRuns];
 #pragma unroll
-        for (int j = 0; j < kKeep; ++j) {
-            const uint32_t i = uint32_t(j) * kSelNT + threadIdx.x;
-            x[j] = i < nbk ? uint32_t(v[i]) : 0u;
+            for (int q = 0; q < kGatherRuns; ++q) {
+                const uint32_t cn = __builtin_amdgcn_readlane(tc, q), s0 = __builtin_amdgcn_readlane(ts, q);
+                v0[q] = uint32_t(lane) < cn ? uint32_t(sorted[s0 + lane]) : 0u;
+                v1[q] = uint32_t(lane) + kWave < cn ? uint32_t(sorted[s0 + kWave + lane]) : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < kGatherRuns; ++q) {
+                const uint32_t cn = __builtin_amdgcn_readlane(tc, q), s0 = __builtin_amdgcn_readlane(ts, q);
+                const uint32_t d0 = __builtin_amdgcn_readlane(to, q);
+                if (uint32_t(lane) < cn) stage[d0 + lane] = v0[q];
+                if (uint32_t(lane) + kWave < cn) stage[d0 + kWave + lane] = v1[q];
+                for (uint32_t i = 2 * kWave + lane; i < cn; i += kWave) stage[d0 + i] = uint32_t(sorted[s0 + i]);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int g = 0; g < kKeep / 4; ++g) {
+            if (uint32_t(g) * (4 * kSelNT) >= nbk) break;
+            const uint4 v = reinterpret_cast<const uint4*>(stage)[g * kSelNT + t];
+            x[4 * g] = v.x;
+            x[4 * g + 1] = v.y;
+            x[4 * g + 2] = v.z;
+            x[4 * g + 3] = v.w;
         }
     }
     uint32_t prefix = 0;
     for (int shift = top; shift >= 0; shift -= 8) {
-        if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+        if (t < 256) hist[t] = 0;
         __syncthreads();
+        uint32_t zeros = 0;
         if (in_regs) {
 #pragma unroll
             for (int j = 0; j < kKeep; ++j) {
-                const uint32_t i = uint32_t(j) * kSelNT + threadIdx.x;
+                if (j % 4 == 0 && uint32_t(j / 4) * (4 * kSelNT) >= nbk) break;
                 const uint32_t y = x[j] >> shift;
-                if (i < nbk && (y >> 8) == prefix) hist_add(hist, y & 255u);
+                hist_add(hist, slot(j) < nbk && (y >> 8) == prefix, y & 255u, zeros);
             }
         } else {
-            for (uint32_t c0 = 0; c0 < nbk; c0 += kSelNT * kJ) {
-                uint32_t y[kJ];
-#pragma unroll
-                for (int j = 0; j < kJ; ++j) {
-                    const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
-                    y[j] = i < nbk ? uint32_t(v[i]) >> shift : 0u;
-                }
-#pragma unroll
-                for (int j = 0; j < kJ; ++j) {
-                    const uint32_t i = c0 + uint32_t(j) * kSelNT + threadIdx.x;
-                    if (i < nbk && (y[j] >> 8) == prefix) hist_add(hist, y[j] & 255u);
+            for (int64_t r = w; r < chunks; r += kSelWaves) {
+                const uint32_t cn = rcnt[r], s0 = rsrc[r];
+                for (uint32_t i0 = 0; i0 < cn; i0 += kWave) {   // bounds uniform across the wavefront
+                    const uint32_t i = i0 + lane;
+                    const uint32_t y = i < cn ? uint32_t(sorted[s0 + i]) >> shift : 0u;
+                    hist_add(hist, i < cn && (y >> 8) == prefix, y & 255u, zeros);
                 }
             }
         }
+        hist_flush_zeros(hist, zeros);
         __syncthreads();
-        if (threadIdx.x < kWave) pick_digit(hist, k, pick);
+        if (t < kWave) pick_digit(hist, k, pick);
         __syncthreads();
         prefix = (prefix << 8) | pick[0];
         k = int32_t(pick[1]);
         __syncthreads();
     }
-    if (threadIdx.x == 0) q_out[b] = int32_t(prefix);
+    if (t == 0) q_out[b] = int32_t(prefix);
 }
 
 int grid_for(int64_t n, int nt, int per_thread, int cap) {
@@ -575,29 +584,23 @@ extern "C" size_t maps_calibrate_workspace_size(int64_t n, int32_t nb) {
 namespace {
 
 // Calibration by counting sort (up to kFastBuckets buckets and
-// kSortMaxBlocks * kPerBlock residuals), then one workgroup per bucket.
+// kSortMaxChunks chunks of kChunk residuals): chunks sorted by bucket, then
+// one workgroup per bucket.
 maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges, int32_t nb,
                            int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
                            void* workspace, hipStream_t stream) {
     const FastWorkspace w = fast_carve(workspace, n, nb);
-    const int64_t blocks = sort_blocks(n);
-    const size_t lds_count = size_t(2 * nb) * 4;   // edges and per-bucket counters
-    const size_t lds_scatter = size_t(3 * nb) * 4 + size_t(kPerBlock) * 6;
+    const int64_t chunks = sort_chunks(n);
     if (n > 0) {
-        hipLaunchKernelGGL(cal_count, dim3(unsigned(blocks)), dim3(kSortNT), lds_count, stream, pred, truth, n,
-                           edges, nb, blocks, w.cnt_part, w.max_part, dev_err);
+        const size_t lds_sort = size_t(kChunk) * 4 + size_t(2 * nb - 1) * 4;   // chunk, edges, run sizes
+        allow_dynamic_lds(cal_chunk_sort, lds_sort);
+        hipLaunchKernelGGL(cal_chunk_sort, dim3(unsigned(chunks)), dim3(kSortNT), lds_sort, stream, pred, truth, n,
+                           edges, nb, chunks, w.run_cnt, w.run_start, w.max_part, w.sorted, dev_err);
         MAPS_CHECK_LAUNCH();
     }
-    hipLaunchKernelGGL(cal_offsets, dim3(unsigned(nb)), dim3(kSortNT), 0, stream, nb, blocks, alpha_ppm,
-                       w.cnt_part, w.max_part, w.off_part, w.bcount, w.bmax, w.krank);
-    MAPS_CHECK_LAUNCH();
-    if (n > 0) {
-        hipLaunchKernelGGL(cal_scatter, dim3(unsigned(blocks)), dim3(kSortNT), lds_scatter, stream, pred, truth, n,
-                           edges, nb, blocks, w.bcount, w.off_part, w.sorted);
-        MAPS_CHECK_LAUNCH();
-    }
-    hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), 0, stream, nb, w.sorted, w.bcount,
-                       w.bmax, w.krank, q_out, count_out);
+    allow_dynamic_lds(cal_bucket_select, kSelStageBytes);
+    hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), kSelStageBytes, stream, nb, chunks,
+                       alpha_ppm, w.sorted, w.run_cnt, w.run_start, w.max_part, q_out, count_out);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

@@ -50,6 +50,12 @@ CAL_CASES = {
     "alpha_1ppm": dict(n=4000, nb=4, alpha=1),
     "alpha_999999ppm": dict(n=4000, nb=4, alpha=999999),
     "duplicate_edges": dict(n=4000, nb=6, alpha=100000, dup=True),
+    # residuals in prediction order: each chunk of 4,096 falls in one or two
+    # buckets, so runs are far longer than a wavefront
+    "sorted_pred_long_runs": dict(n=30000, nb=4, alpha=100000, sort=True),
+    "ragged_last_chunk": dict(n=4097, nb=3, alpha=100000),
+    "chunks_at_limit": dict(n=1024 * 4096, nb=128, alpha=100000),
+    "one_past_chunk_limit": dict(n=1024 * 4096 + 1, nb=16, alpha=50000),
 }
 
 
@@ -71,6 +77,9 @@ def test_calibrate_cases(orc, case):
         edges = np.array([100, 100, 100, 2000, 9000][: nb - 1], np.int32)
     if c.get("skew"):
         edges = np.array([4000, 4100, 4200, 4300, 4400, 4500, 4600], np.int32)[: nb - 1]
+    if c.get("sort"):
+        order = np.argsort(pred, kind="stable")
+        pred, truth = pred[order], truth[order]
     u_max = 65536
     ap = np.concatenate([rng.integers(-3, 10**6, size=3000), [-1, 0, 1, 2**31 - 1]]).astype(np.int32)
     say(f"[edge] calibrate {case}: n={n} nb={nb}")
