@@ -173,11 +173,12 @@ class StepGraphs:
         torch.cuda.synchronize()
 
     def replay(self, events=None):
-        """One step; with events (len(PHASES) + 1 of them), the phase
-        boundaries are recorded on the current stream."""
+        """One step; with events (len(PHASES) + 1 of them, None where no
+        event is wanted), the phase boundaries are recorded on the current
+        stream."""
         for i, g in enumerate(self.graphs):
-            if events is not None:
+            if events is not None and events[i] is not None:
                 events[i].record()
             g.replay()
-        if events is not None:
+        if events is not None and events[-1] is not None:
             events[-1].record()
