@@ -376,7 +376,8 @@ __global__ __launch_bounds__(kSortNT) void cal_chunk_sort(const int32_t* __restr
     const int ne = nb - 1;
     int32_t* lsort = chunk_lds;                                            // [kChunk] scores by bucket
     int32_t* le = lsort + kChunk;                                    // [ne]
-    uint32_t* lcnt = reinterpret_cast<uint32_t*>(le + ne);           // [nb] run sizes, then run starts
+    uint32_t* lcnt = reinterpret_cast<uint32_t*>(le + ne);           // [nb] run sizes
+    uint32_t* lstart = lcnt + nb;                                    // [nb] run starts
     for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = edges[i];
     for (int i = threadIdx.x; i < nb; i += kSortNT) lcnt[i] = 0;
     if (blockIdx.x == 0)
@@ -396,17 +397,18 @@ __global__ __launch_bounds__(kSortNT) void cal_chunk_sort(const int32_t* __restr
     mx = block_reduce_max<kSortNT>(mx, red);   // starts with a barrier: the run sizes are complete
     const int64_t c = blockIdx.x;
     block_scan<kSortNT, false, false, true, uint32_t>(
-        nb, 0u, [&](int64_t i) { return lcnt[i]; },
-        [&](int64_t i, uint32_t v) {
-            run_cnt[i * chunks + c] = lcnt[i];
-            run_start[i * chunks + c] = v;
-            lcnt[i] = v;
-        },
+        nb, 0u, [&](int64_t i) { return lcnt[i]; }, [&](int64_t i, uint32_t v) { lstart[i] = v; },
         red);   // ends with a barrier: the run starts are complete
 #pragma unroll
     for (int j = 0; j < kJ; ++j)
-        if (r.valid[j]) lsort[lcnt[r.b[j]] + rank[j]] = r.s[j];
+        if (r.valid[j]) lsort[lstart[r.b[j]] + rank[j]] = r.s[j];
     __syncthreads();
+    // global stores only after the last barrier (a barrier waits for every
+    // store in flight)
+    for (int i = threadIdx.x; i < nb; i += kSortNT) {
+        run_cnt[int64_t(i) * chunks + c] = lcnt[i];
+        run_start[int64_t(i) * chunks + c] = lstart[i];
+    }
     const int64_t lo = c * kChunk;
     const int cnt = int(n - lo < kChunk ? n - lo : kChunk);
     if (cnt == kChunk) {
@@ -592,7 +594,7 @@ maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n,
     const FastWorkspace w = fast_carve(workspace, n, nb);
     const int64_t chunks = sort_chunks(n);
     if (n > 0) {
-        const size_t lds_sort = size_t(kChunk) * 4 + size_t(2 * nb - 1) * 4;   // chunk, edges, run sizes
+        const size_t lds_sort = size_t(kChunk) * 4 + size_t(3 * nb - 1) * 4;   // chunk, edges, run sizes and starts
         allow_dynamic_lds(cal_chunk_sort, lds_sort);
         hipLaunchKernelGGL(cal_chunk_sort, dim3(unsigned(chunks)), dim3(kSortNT), lds_sort, stream, pred, truth, n,
                            edges, nb, chunks, w.run_cnt, w.run_start, w.max_part, w.sorted, dev_err);

@@ -4,6 +4,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <limits>
 #include <stdint.h>
 
 #include "maps.h"
@@ -169,7 +170,12 @@ __host__ __device__ inline const int2* slice_cold(const SnapView& V, const DecHe
 // Threshold T of an event: the smallest U >= 0 with S + U n1 > pmx.
 __host__ __device__ inline int32_t event_threshold(int32_t pmx, int32_t S, uint32_t n1) {
     if (S > pmx) return 0;
-    const int64_t t = int64_t(pmx - S) / int64_t(n1) + 1;
+    const int32_t diff = pmx - S;
+    if (diff >= 0) {   // every valid snapshot: a 32-bit division
+        const uint32_t q = uint32_t(diff) / n1;
+        return q < uint32_t(INT32_MAX - 1) ? int32_t(q + 1) : INT32_MAX;
+    }
+    const int64_t t = int64_t(diff) / int64_t(n1) + 1;
     return t < int64_t(INT32_MAX) ? int32_t(t) : INT32_MAX;
 }
 
@@ -180,41 +186,81 @@ __device__ inline void raise_error(uint32_t* dev_err, uint32_t bits) {
     if (dev_err) atomicOr(dev_err, bits);
 }
 
+// Wavefront scans and reductions through DPP (data-parallel primitives: a
+// lane reads another lane's register as an instruction operand, no LDS
+// round trip).  The inclusive scan is Hillis-Steele within each row of 16
+// lanes (row shifts by 1, 2, 4, 8), then the row broadcasts of gfx9: lane 15
+// of rows 0 and 2 into rows 1 and 3, then lane 31 into rows 2 and 3.  Lanes
+// without a source keep `fill`, the operation's identity.  Called by whole
+// wavefronts.
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppWaveShr1 = 0x138, kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+
+template <int kCtrl, int kRowMask, typename T>
+__device__ inline T dpp_move(T fill, T v) {
+    static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit values");
+    if constexpr (sizeof(T) == 4) {
+        return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                                 __builtin_bit_cast(int, v), kCtrl, kRowMask,
+                                                                 0xf, false));
+    } else {
+        const uint64_t f = __builtin_bit_cast(uint64_t, fill), x = __builtin_bit_cast(uint64_t, v);
+        const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(int(uint32_t(f)), int(uint32_t(x)), kCtrl,
+                                                                 kRowMask, 0xf, false));
+        const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(int(uint32_t(f >> 32)), int(uint32_t(x >> 32)),
+                                                                 kCtrl, kRowMask, 0xf, false));
+        return __builtin_bit_cast(T, (uint64_t(hi) << 32) | lo);
+    }
+}
+
+template <typename T, typename Op>
+__device__ inline T wave_incl_scan(T v, T fill, Op op) {
+    v = op(v, dpp_move<kDppRowShr1, 0xf>(fill, v));
+    v = op(v, dpp_move<kDppRowShr2, 0xf>(fill, v));
+    v = op(v, dpp_move<kDppRowShr4, 0xf>(fill, v));
+    v = op(v, dpp_move<kDppRowShr8, 0xf>(fill, v));
+    v = op(v, dpp_move<kDppRowBcast15, 0xa>(fill, v));
+    v = op(v, dpp_move<kDppRowBcast31, 0xc>(fill, v));
+    return v;
+}
+
+// The value of lane 63, in every lane.
+template <typename T>
+__device__ inline T wave_last(T v) {
+    if constexpr (sizeof(T) == 4) {
+        return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), kWave - 1));
+    } else {
+        const uint64_t x = __builtin_bit_cast(uint64_t, v);
+        const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(x)), kWave - 1));
+        const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(x >> 32)), kWave - 1));
+        return __builtin_bit_cast(T, (uint64_t(hi) << 32) | lo);
+    }
+}
+
+// Lane i gets lane i - 1's value, lane 0 gets `fill`.
+template <typename T>
+__device__ inline T wave_shift_up1(T v, T fill) {
+    return dpp_move<kDppWaveShr1, 0xf>(fill, v);
+}
+
 template <typename T>
 __device__ inline T wave_incl_scan_add(T v) {
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        T o = __shfl_up(v, off, kWave);
-        if (int(threadIdx.x % kWave) >= off) v += o;
-    }
-    return v;
+    return wave_incl_scan(v, T(0), [](T x, T y) { return x + y; });
 }
 
 template <typename T>
 __device__ inline T wave_incl_scan_max(T v) {
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        T o = __shfl_up(v, off, kWave);
-        if (int(threadIdx.x % kWave) >= off) v = v > o ? v : o;
-    }
-    return v;
+    return wave_incl_scan(v, std::numeric_limits<T>::lowest(), [](T x, T y) { return x > y ? x : y; });
 }
 
 template <typename T>
 __device__ inline T wave_reduce_add(T v) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    return wave_last(wave_incl_scan_add(v));
 }
 
 template <typename T>
 __device__ inline T wave_reduce_max(T v) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        T o = __shfl_xor(v, off, kWave);
-        v = v > o ? v : o;
-    }
-    return v;
+    return wave_last(wave_incl_scan_max(v));
 }
 
 // Workgroup-wide reductions over one value per thread; `tmp` holds NT/64 slots.
@@ -260,8 +306,7 @@ __device__ inline T block_excl_scan(T v, T identity, T* tmp, T* total) {
         if (i < wid) wave_prefix = kMax ? (wave_prefix > x ? wave_prefix : x) : wave_prefix + x;
         all = kMax ? (all > x ? all : x) : all + x;
     }
-    T excl_in_wave = __shfl_up(incl, 1, kWave);
-    if (lane == 0) excl_in_wave = identity;
+    const T excl_in_wave = wave_shift_up1(incl, identity);
     *total = all;
     return kMax ? (wave_prefix > excl_in_wave ? wave_prefix : excl_in_wave) : wave_prefix + excl_in_wave;
 }

@@ -20,6 +20,8 @@ namespace {
 
 constexpr int kNT = 1024;
 constexpr size_t kLdsBudget = 150 * 1024;
+constexpr int kResPer = 8;   // residents per thread held in registers (decoders of up to kNT * kResPer)
+constexpr int kEvPer = 8;    // events per thread held in registers when the arrays are in LDS
 
 // Arrays of one decoder: bitmap words, events before each word, and per event
 // the count, the p+g sum, the time and the prefix maximum.
@@ -105,11 +107,15 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     for (int64_t w = tid; w < W; w += kNT) a.B(w) = 0u;
     phase<kInLds>();
 
-    // 1. event bitmap and total demand sum_r (p + g + R)
+    // 1. event bitmap and total demand sum_r (p + g + R).  A decoder of at
+    // most kNT * kResPer residents is read once, every load in flight
+    // together, and keeps R and p + g in registers for step 3.
     int64_t tot = 0;
     bool neg = false, range = false;
-    for (int64_t r = lo + tid; r < hi; r += kNT) {
-        int32_t pr = p[r], gr = g[r], ur = U[r];
+    const int64_t n = hi - lo;
+    const bool in_regs = n <= int64_t(kNT) * kResPer;
+    uint32_t Rk[kResPer], PGk[kResPer];
+    auto resident = [&](int32_t pr, int32_t gr, int32_t ur, uint32_t& Rout, uint32_t& PGout) {
         neg |= (pr < 0) | (gr < 0) | (ur < 0);
         pr = pr < 0 ? 0 : pr;
         gr = gr < 0 ? 0 : gr;
@@ -117,6 +123,29 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         if (R > u_max) { range = true; R = u_max; }
         atomicOr(&a.B(R >> 5), 1u << (R & 31));
         tot += int64_t(pr) + gr + R;
+        Rout = uint32_t(R);
+        PGout = uint32_t(pr) + uint32_t(gr);
+    };
+    if (in_regs) {
+        int32_t pr[kResPer], gr[kResPer], ur[kResPer];
+#pragma unroll
+        for (int j = 0; j < kResPer; ++j) {
+            const int64_t i = int64_t(j) * kNT + tid;
+            pr[j] = i < n ? p[lo + i] : 0;
+            gr[j] = i < n ? g[lo + i] : 0;
+            ur[j] = i < n ? U[lo + i] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < kResPer; ++j) {
+            Rk[j] = 0u;
+            PGk[j] = 0u;
+            if (int64_t(j) * kNT + tid < n) resident(pr[j], gr[j], ur[j], Rk[j], PGk[j]);
+        }
+    } else {
+        for (int64_t r = lo + tid; r < hi; r += kNT) {
+            uint32_t R, PG;
+            resident(p[r], g[r], U[r], R, PG);
+        }
     }
     if (neg) raise_error(dev_err, MAPS_ERR_NEG_LEN);
     if (range) raise_error(dev_err, MAPS_ERR_BOUND_RANGE);
@@ -141,53 +170,135 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         }
     }
     phase<kInLds>();
-    for (int64_t r = lo + tid; r < hi; r += kNT) {
-        int32_t pr = p[r], gr = g[r], ur = U[r];
-        pr = pr < 0 ? 0 : pr;
-        gr = gr < 0 ? 0 : gr;
-        int64_t R = remaining(ur < 0 ? 0 : ur, gr);
-        if (R > u_max) R = u_max;
-        uint32_t word = a.B(R >> 5);
-        uint32_t e = a.P(R >> 5) + __popc(word & ((1u << (R & 31)) - 1u));
+    auto count = [&](uint32_t R, uint32_t PG) {
+        const uint32_t word = a.B(R >> 5);
+        const uint32_t e = a.P(R >> 5) + __popc(word & ((1u << (R & 31)) - 1u));
         atomicAdd(&a.C(e), 1u);
-        atomicAdd(&a.S(e), uint32_t(pr) + uint32_t(gr));
+        atomicAdd(&a.S(e), PG);
+    };
+    if (in_regs) {
+#pragma unroll
+        for (int j = 0; j < kResPer; ++j)
+            if (int64_t(j) * kNT + tid < n) count(Rk[j], PGk[j]);
+    } else {
+        for (int64_t r = lo + tid; r < hi; r += kNT) {
+            int32_t pr = p[r], gr = g[r], ur = U[r];
+            pr = pr < 0 ? 0 : pr;
+            gr = gr < 0 ? 0 : gr;
+            int64_t R = remaining(ur < 0 ? 0 : ur, gr);
+            if (R > u_max) R = u_max;
+            count(uint32_t(R), uint32_t(pr) + uint32_t(gr));
+        }
     }
     phase<kInLds>();
 
-    // 4. N_e and S_e: suffix sums over the events, as one scan of (N << 32 | S)
-    //    (S stays below 2^32: a larger total demand is reported as out of range)
-    block_scan<kNT, false, true, false, uint64_t>(
-        E, uint64_t(0), [&](int64_t e) { return (uint64_t(a.C(e)) << 32) | a.S(e); },
-        [&](int64_t e, uint64_t v) {
-            a.C(e) = uint32_t(v >> 32);
-            a.S(e) = uint32_t(v);
-        },
-        reinterpret_cast<uint64_t*>(sc.red64));
-    phase<kInLds>();
-    // PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1))
-    const int32_t pmx_end = block_scan<kNT, true, false, true, int32_t>(
-        E, 0,
-        [&](int64_t e) { return int32_t(a.S(e) + a.T(e) * (a.C(e) + 1u)); },
-        [&](int64_t e, int32_t v) { a.M(e) = uint32_t(v); }, reinterpret_cast<int32_t*>(sc.red32));
-    phase<kInLds>();
-    // base peak = max(0, max_e S_e + tau_e N_e);
-    // hot window: bounds above event 0's cold range and below the first cold
-    // range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] for e < E (the
-    // last event needs no cold record); flat region: bounds past the first
-    // event e* with PMX_e = PMX_E, i.e. U >= tau_{e*-1} + 1
-    int32_t bmax = 0, lo_w = 0, start_min = INT32_MAX, estar = int32_t(E);
-    for (int64_t e = tid; e < E; e += kNT) {
-        const int32_t o = int32_t(a.S(e) + a.T(e) * a.C(e));
-        bmax = bmax > o ? bmax : o;
-        const int32_t m = int32_t(a.M(e));
-        if (m == pmx_end && int32_t(e) < estar) estar = int32_t(e);
-        const int64_t T = event_threshold(m, int32_t(a.S(e)), a.C(e) + 1u);
-        const int64_t lo_e = e == 0 ? 0 : int64_t(a.T(e - 1)) + 1;
-        const int64_t hi_e = int64_t(a.T(e));
-        const int64_t start = T > lo_e ? T : lo_e;
-        if (start > hi_e) continue;   // no bound landing on e reaches T_e
-        if (e == 0) lo_w = int32_t(hi_e + 1);
-        else if (start < start_min) start_min = int32_t(start);
+    // 4. N_e and S_e: suffix sums over the events (of N << 32 | S: S stays
+    //    below 2^32, a larger total demand is reported as out of range); then
+    //    PMX_e = max(0, max_{i<e} S_i + tau_i (N_i + 1)) by a forward max-scan;
+    //    then the base peak max(0, max_e S_e + tau_e N_e), the thresholds T_e,
+    //    the hot window (bounds above event 0's cold range and below the first
+    //    cold range of a later event, [max(T_e, tau_{e-1} + 1), tau_e] for
+    //    e < E: the last event needs no cold record) and the flat region
+    //    (bounds past the first event e* with PMX_e = PMX_E, i.e.
+    //    U >= tau_{e*-1} + 1).
+    int32_t pmx_end, bmax = 0, lo_w = 0, start_min = INT32_MAX, estar = int32_t(E);
+    // the snapshot slice: rank words, then PMX_e, T_e and the cold records {S_e, N_e + 1}
+    uint2* rank = reinterpret_cast<uint2*>(V.slices + slice_off);
+    int32_t* pmx = reinterpret_cast<int32_t*>(V.slices + slice_off + W / 2);
+    int32_t* thr = pmx + 4 * event_units(E);
+    int2* cold = reinterpret_cast<int2*>(thr + 4 * event_units(E));
+    // register chunks of the LDS path: after the pass below, per event the
+    // suffix count N_e (cN), the suffix sum S_e (cS), the threshold T_e (cT)
+    // and PMX_e (cM)
+    uint32_t cN[kEvPer], cS[kEvPer], cT[kEvPer];
+    int32_t cM[kEvPer];
+    bool ok[kEvPer];
+    const int chunk = int((int64_t(E) + kNT - 1) / kNT);
+    const int e0 = kInLds ? tid * chunk : 0;
+    if constexpr (kInLds) {
+        // E <= residents <= kNT * kEvPer: each thread keeps its contiguous
+        // chunk of events in registers through both scans and the thresholds
+#pragma unroll
+        for (int j = 0; j < kEvPer; ++j) {
+            const int e = e0 + j;
+            ok[j] = j < chunk && e < int(E);
+            cN[j] = ok[j] ? a.C(e) : 0u;
+            cS[j] = ok[j] ? a.S(e) : 0u;
+            cT[j] = ok[j] ? a.T(e) : 0u;
+        }
+        uint64_t loc = 0;
+#pragma unroll
+        for (int j = 0; j < kEvPer; ++j) loc += (uint64_t(cN[j]) << 32) | cS[j];
+        uint64_t all;
+        const uint64_t before =
+            block_excl_scan<kNT, false, uint64_t>(loc, uint64_t(0), reinterpret_cast<uint64_t*>(sc.red64), &all);
+        uint64_t run = all - before - loc;   // the events after this chunk
+        int32_t v[kEvPer];
+        int32_t lmax = 0;
+#pragma unroll
+        for (int j = kEvPer - 1; j >= 0; --j) {
+            run += (uint64_t(cN[j]) << 32) | cS[j];
+            cN[j] = uint32_t(run >> 32);
+            cS[j] = uint32_t(run);
+            v[j] = int32_t(cS[j] + cT[j] * (cN[j] + 1u));
+            if (ok[j]) lmax = lmax > v[j] ? lmax : v[j];
+        }
+        int32_t mall;
+        int32_t m = block_excl_scan<kNT, true, int32_t>(lmax, 0, reinterpret_cast<int32_t*>(sc.red32), &mall);
+        pmx_end = mall;
+        uint32_t prev_tau = e0 >= 1 && e0 - 1 < int(E) ? a.T(e0 - 1) : 0u;
+#pragma unroll
+        for (int j = 0; j < kEvPer; ++j) {
+            cM[j] = m;
+            if (!ok[j]) continue;
+            const int e = e0 + j;
+            const int32_t o = int32_t(cS[j] + cT[j] * cN[j]);
+            bmax = bmax > o ? bmax : o;
+            if (m == pmx_end && e < estar) estar = e;
+            const int32_t T = event_threshold(m, int32_t(cS[j]), cN[j] + 1u);
+            if (P > 0) {   // the dense profile reads the scanned arrays back
+                a.C(e) = cN[j];
+                a.S(e) = cS[j];
+                a.M(e) = uint32_t(m);
+            }
+            const int64_t lo_e = e == 0 ? 0 : int64_t(prev_tau) + 1;
+            const int64_t hi_e = int64_t(cT[j]);
+            const int64_t start = T > lo_e ? T : lo_e;
+            if (start <= hi_e) {   // a bound landing on e reaches T_e
+                if (e == 0) lo_w = int32_t(hi_e + 1);
+                else if (start < start_min) start_min = int32_t(start);
+            }
+            prev_tau = cT[j];
+            cT[j] = uint32_t(T);
+            m = m > v[j] ? m : v[j];
+        }
+    } else {
+        block_scan<kNT, false, true, false, uint64_t>(
+            E, uint64_t(0), [&](int64_t e) { return (uint64_t(a.C(e)) << 32) | a.S(e); },
+            [&](int64_t e, uint64_t v) {
+                a.C(e) = uint32_t(v >> 32);
+                a.S(e) = uint32_t(v);
+            },
+            reinterpret_cast<uint64_t*>(sc.red64));
+        phase<kInLds>();
+        pmx_end = block_scan<kNT, true, false, true, int32_t>(
+            E, 0,
+            [&](int64_t e) { return int32_t(a.S(e) + a.T(e) * (a.C(e) + 1u)); },
+            [&](int64_t e, int32_t v) { a.M(e) = uint32_t(v); }, reinterpret_cast<int32_t*>(sc.red32));
+        phase<kInLds>();
+        for (int64_t e = tid; e < E; e += kNT) {
+            const int32_t o = int32_t(a.S(e) + a.T(e) * a.C(e));
+            bmax = bmax > o ? bmax : o;
+            const int32_t m = int32_t(a.M(e));
+            if (m == pmx_end && int32_t(e) < estar) estar = int32_t(e);
+            const int64_t T = event_threshold(m, int32_t(a.S(e)), a.C(e) + 1u);
+            const int64_t lo_e = e == 0 ? 0 : int64_t(a.T(e - 1)) + 1;
+            const int64_t hi_e = int64_t(a.T(e));
+            const int64_t start = T > lo_e ? T : lo_e;
+            if (start > hi_e) continue;   // no bound landing on e reaches T_e
+            if (e == 0) lo_w = int32_t(hi_e + 1);
+            else if (start < start_min) start_min = int32_t(start);
+        }
     }
     const int4 r = block_reduce_max4(make_int4(bmax, lo_w, -start_min, -estar), sc.red4);
     const int32_t base = r.x, hot_lo = r.y, hot_hi = -r.z - 1, e_star = -r.w;
@@ -199,29 +310,29 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         for (int64_t u = tid; u < P; u += kNT) {
             const uint32_t word = a.B(u >> 5);
             const uint32_t e = a.P(u >> 5) + __popc(word & ((1u << (u & 31)) - 1u));
-            int32_t pmx = pmx_end, lin = int32_t(u);
+            int32_t pm = pmx_end, lin = int32_t(u);
             if (e < E) {
-                pmx = int32_t(a.M(e));
+                pm = int32_t(a.M(e));
                 lin = int32_t(a.S(e) + uint32_t(u) * (a.C(e) + 1u));
             }
-            const int32_t f = pmx > lin ? pmx : lin;
+            const int32_t f = pm > lin ? pm : lin;
             prof[u] = f > int32_t(u) ? f : int32_t(u);
         }
         phase<kInLds>();   // the HBM arrays are updated in place below
     }
 
-    // 6. write the snapshot slice: PMX_e, T_e and the cold records {S_e, N_e + 1}
-    uint2* rank = reinterpret_cast<uint2*>(V.slices + slice_off);
-    int32_t* pmx = reinterpret_cast<int32_t*>(V.slices + slice_off + W / 2);
-    int32_t* thr = pmx + 4 * event_units(E);
-    int2* cold = reinterpret_cast<int2*>(thr + 4 * event_units(E));
+    // 6. the rest of the snapshot slice (arrays in LDS: the rank words; in
+    //    HBM: T_e and N_e + 1 in place)
     if constexpr (kInLds) {
-        for (int64_t e = tid; e < E; e += kNT) {
-            const int32_t m = int32_t(a.M(e)), sv = int32_t(a.S(e));
-            const uint32_t n1 = a.C(e) + 1u;
-            pmx[e] = m;
-            thr[e] = event_threshold(m, sv, n1);
-            cold[e] = make_int2(sv, int32_t(n1));
+        // the event arrays from the registers, after the last barrier (a
+        // barrier waits for every store in flight)
+#pragma unroll
+        for (int j = 0; j < kEvPer; ++j) {
+            if (!ok[j]) continue;
+            const int e = e0 + j;
+            pmx[e] = cM[j];
+            thr[e] = int32_t(cT[j]);
+            cold[e] = make_int2(int32_t(cS[j]), int32_t(cN[j] + 1u));
         }
         for (int64_t w = tid; w < W; w += kNT) rank[w] = make_uint2(a.B(w), a.P(w));
     } else {
@@ -330,7 +441,7 @@ extern "C" maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n
     if (snapshot_bytes < L.bytes) return MAPS_E_BUFFER;
     const size_t fixed = size_t(2) * L.W * 4;
     int64_t cap = fixed < kLdsBudget ? int64_t((kLdsBudget - fixed) / 16) : 0;
-    if (cap > 8192) cap = 8192;
+    if (cap > int64_t(kNT) * kEvPer) cap = int64_t(kNT) * kEvPer;   // the register chunks of the LDS path
     const size_t lds = cap > 0 ? fixed + size_t(cap) * 16 : 0;
     allow_dynamic_lds(project_decoders, lds);
     hipLaunchKernelGGL(project_decoders, dim3(D), dim3(kNT), lds, stream, D, seg_off, n_total, prompt, generated,
