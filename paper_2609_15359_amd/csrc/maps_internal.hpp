@@ -291,12 +291,14 @@ __device__ inline T block_reduce_max(T v, T* tmp) {
 }
 
 // Exclusive scan of one value per thread across the workgroup; returns the
-// thread's exclusive prefix and writes the total to *total.
-template <int NT, bool kMax, typename T>
+// thread's exclusive prefix and writes the total to *total.  Without
+// kGuard the caller guarantees that no thread still reads `tmp` from an
+// earlier use (the leading barrier is skipped).
+template <int NT, bool kMax, typename T, bool kGuard = true>
 __device__ inline T block_excl_scan(T v, T identity, T* tmp, T* total) {
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
     T incl = kMax ? wave_incl_scan_max(v) : wave_incl_scan_add(v);
-    __syncthreads();
+    if constexpr (kGuard) __syncthreads();
     if (lane == kWave - 1) tmp[wid] = incl;
     __syncthreads();
     T wave_prefix = identity, all = identity;

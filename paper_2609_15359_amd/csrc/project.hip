@@ -76,16 +76,30 @@ struct Scratch {
     int4 red4[kNT / kWave];
 };
 
-// Four workgroup-wide maxima at once (one LDS round instead of four).
-__device__ inline int4 block_reduce_max4(int4 v, int4* tmp) {
+// Four workgroup-wide maxima at once (one LDS round instead of four), and a
+// sum when `sum` is given.  Without kGuard the caller guarantees that no
+// thread still reads `tmp` or `tmp_sum` from an earlier use.
+template <bool kGuard = true>
+__device__ inline int4 block_reduce_max4(int4 v, int4* tmp, int64_t* sum = nullptr, int64_t* tmp_sum = nullptr) {
     v.x = wave_reduce_max(v.x);
     v.y = wave_reduce_max(v.y);
     v.z = wave_reduce_max(v.z);
     v.w = wave_reduce_max(v.w);
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    int64_t s = 0;
+    if (sum) s = wave_reduce_add(*sum);
+    if constexpr (kGuard) __syncthreads();
+    if (lane == 0) {
+        tmp[wid] = v;
+        if (sum) tmp_sum[wid] = s;
+    }
     __syncthreads();
-    if (lane == 0) tmp[wid] = v;
-    __syncthreads();
+    if (sum) {
+        s = 0;
+#pragma unroll
+        for (int i = 0; i < kNT / kWave; ++i) s += tmp_sum[i];
+        *sum = s;
+    }
     int4 r = tmp[0];
 #pragma unroll
     for (int i = 1; i < kNT / kWave; ++i) {
@@ -105,6 +119,9 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
                             Scratch& sc) {
     const int tid = threadIdx.x;
     for (int64_t w = tid; w < W; w += kNT) a.B(w) = 0u;
+    if constexpr (kInLds) {   // the event counters too: E <= residents <= the LDS capacity
+        for (int64_t e = tid; e < hi - lo; e += kNT) { a.C(e) = 0u; a.S(e) = 0u; }
+    }
     phase<kInLds>();
 
     // 1. event bitmap and total demand sum_r (p + g + R).  A decoder of at
@@ -149,19 +166,24 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     }
     if (neg) raise_error(dev_err, MAPS_ERR_NEG_LEN);
     if (range) raise_error(dev_err, MAPS_ERR_BOUND_RANGE);
-    tot = block_reduce_add<kNT>(tot, sc.red64);
-    if (tid == 0 && tot + u_max > int64_t(INT32_MAX)) raise_error(dev_err, MAPS_ERR_INT32_RANGE);
+    if constexpr (!kInLds) {   // the LDS path sums the demand with its last reduction
+        tot = block_reduce_add<kNT>(tot, sc.red64);
+        if (tid == 0 && tot + u_max > int64_t(INT32_MAX)) raise_error(dev_err, MAPS_ERR_INT32_RANGE);
+    }
     phase<kInLds>();
 
     // 2. events before each bitmap word
     const uint32_t E = block_scan<kNT, false, false, true, uint32_t>(
         W, 0u, [&](int64_t w) { return uint32_t(__popc(a.B(w))); },
-        [&](int64_t w, uint32_t v) { a.P(w) = v; }, sc.red32);
+        [&](int64_t w, uint32_t v) { a.P(w) = v; }, sc.red32);   // ends with a barrier
     a.events(E);
-    phase<kInLds>();
+    if constexpr (!kInLds) phase<kInLds>();
 
-    // 3. per-event counters
-    for (int64_t e = tid; e < E; e += kNT) { a.C(e) = 0u; a.S(e) = 0u; }
+    // 3. per-event counters (in LDS already zero, and independent of the
+    //    event times: no barrier between the two loops)
+    if constexpr (!kInLds) {
+        for (int64_t e = tid; e < E; e += kNT) { a.C(e) = 0u; a.S(e) = 0u; }
+    }
     for (int64_t w = tid; w < W; w += kNT) {       // event times, in rank order
         uint32_t bits = a.B(w), e = a.P(w);
         while (bits) {
@@ -169,7 +191,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
             bits &= bits - 1u;
         }
     }
-    phase<kInLds>();
+    if constexpr (!kInLds) phase<kInLds>();
     auto count = [&](uint32_t R, uint32_t PG) {
         const uint32_t word = a.B(R >> 5);
         const uint32_t e = a.P(R >> 5) + __popc(word & ((1u << (R & 31)) - 1u));
@@ -231,7 +253,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         for (int j = 0; j < kEvPer; ++j) loc += (uint64_t(cN[j]) << 32) | cS[j];
         uint64_t all;
         const uint64_t before =
-            block_excl_scan<kNT, false, uint64_t>(loc, uint64_t(0), reinterpret_cast<uint64_t*>(sc.red64), &all);
+            block_excl_scan<kNT, false, uint64_t, false>(loc, uint64_t(0), reinterpret_cast<uint64_t*>(sc.red64), &all);
         uint64_t run = all - before - loc;   // the events after this chunk
         int32_t v[kEvPer];
         int32_t lmax = 0;
@@ -244,7 +266,8 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
             if (ok[j]) lmax = lmax > v[j] ? lmax : v[j];
         }
         int32_t mall;
-        int32_t m = block_excl_scan<kNT, true, int32_t>(lmax, 0, reinterpret_cast<int32_t*>(sc.red32), &mall);
+        // red32 was last read before the barriers of the scan above
+        int32_t m = block_excl_scan<kNT, true, int32_t, false>(lmax, 0, reinterpret_cast<int32_t*>(sc.red32), &mall);
         pmx_end = mall;
         uint32_t prev_tau = e0 >= 1 && e0 - 1 < int(E) ? a.T(e0 - 1) : 0u;
 #pragma unroll
@@ -300,7 +323,13 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
             else if (start < start_min) start_min = int32_t(start);
         }
     }
-    const int4 r = block_reduce_max4(make_int4(bmax, lo_w, -start_min, -estar), sc.red4);
+    int4 r;
+    if constexpr (kInLds) {   // red4 unused so far, red64 last read before the barriers of the max-scan
+        r = block_reduce_max4<false>(make_int4(bmax, lo_w, -start_min, -estar), sc.red4, &tot, sc.red64);
+        if (tid == 0 && tot + u_max > int64_t(INT32_MAX)) raise_error(dev_err, MAPS_ERR_INT32_RANGE);
+    } else {
+        r = block_reduce_max4(make_int4(bmax, lo_w, -start_min, -estar), sc.red4);
+    }
     const int32_t base = r.x, hot_lo = r.y, hot_hi = -r.z - 1, e_star = -r.w;
     const int32_t flat_lo = e_star == 0 ? 0 : int32_t(a.T(e_star - 1)) + 1;
 
