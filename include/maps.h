@@ -67,7 +67,10 @@ enum {
     MAPS_ERR_BOUND_RANGE = 16u,     /* a remaining length max(U-g,0) exceeds u_max */
     MAPS_ERR_SNAPSHOT = 32u,        /* snapshot was not built for this (D, u_max) */
     MAPS_ERR_QUEUE_TOO_LONG = 64u,  /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
-    MAPS_ERR_TOO_MANY = 128u        /* a decoder with MAPS_MAX_RESIDENTS or more residents */
+    MAPS_ERR_TOO_MANY = 128u,       /* a decoder with MAPS_MAX_RESIDENTS or more residents */
+    MAPS_ERR_WAIT_TIMEOUT = 256u    /* a workgroup's bounded wait for the other workgroups
+                                       of its launch ran out (the device did not hold
+                                       every workgroup of the launch at once) */
 };
 
 /* Largest u_max (cap on bounds and remaining lengths) the snapshot accepts,
@@ -99,7 +102,7 @@ enum { MAPS_POLICY_MQ = 0, MAPS_POLICY_MC = 1 };
  *   U_out[i] = -1                          if apply_pred[i] < 0 (no prediction)
  *            = u_max                       if q of its bucket is MAPS_Q_INF
  *            = min(apply_pred[i] + q, u_max) otherwise.
- * dev_err bits: NEG_LEN (pred or truth < 0), EDGES_UNSORTED.
+ * dev_err bits: NEG_LEN (pred or truth < 0), EDGES_UNSORTED, WAIT_TIMEOUT.
  * Host errors: NULL, SIZE (n < 0, m < 0, nb < 1 or nb > 65536, u_max < 0),
  * ALPHA, WORKSPACE, HIP.
  */

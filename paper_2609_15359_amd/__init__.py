@@ -27,7 +27,7 @@ POLICY_MQ, POLICY_MC = 0, 1
 MAX_LOCAL_QUEUE = 2048
 ERR_BITS = {
     1: "NEG_LEN", 2: "EDGES_UNSORTED", 4: "INT32_RANGE", 8: "SEG_OFFSETS",
-    16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG", 128: "TOO_MANY",
+    16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG", 128: "TOO_MANY", 256: "WAIT_TIMEOUT",
 }
 MAX_U_MAX = (1 << 24) - 64
 

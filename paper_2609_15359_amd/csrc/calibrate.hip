@@ -302,6 +302,7 @@ struct FastWorkspace {
     uint32_t* run_start;   // [nb][chunks] where that run starts inside its chunk
     uint32_t* max_part;    // [chunks] largest score of each chunk
     int32_t* sorted;       // [n] scores, every chunk of kChunk sorted by bucket
+    uint64_t* qflag;       // [nb] 1 << 32 | q_b once bucket b is selected (the fused apply waits on them)
     size_t bytes;
 };
 
@@ -315,6 +316,7 @@ FastWorkspace fast_carve(void* base, int64_t n, int32_t nb) {
     w.run_start = reinterpret_cast<uint32_t*>(take(size_t(chunks) * nb * 4));
     w.max_part = reinterpret_cast<uint32_t*>(take(size_t(chunks) * 4));
     w.sorted = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
+    w.qflag = reinterpret_cast<uint64_t*>(take(size_t(nb) * 8));
     w.bytes = off;
     return w;
 }
@@ -368,7 +370,8 @@ __global__ __launch_bounds__(kSortNT) void cal_chunk_sort(const int32_t* __restr
                                                           uint32_t* __restrict__ run_cnt,
                                                           uint32_t* __restrict__ run_start,
                                                           uint32_t* __restrict__ max_part,
-                                                          int32_t* __restrict__ sorted, uint32_t* dev_err) {
+                                                          int32_t* __restrict__ sorted, uint64_t* qflag,
+                                                          uint32_t* dev_err) {
     extern __shared__ __align__(16) int32_t chunk_lds[];
     __shared__ uint32_t red[kSortNT / kWave];
     Residuals r;
@@ -417,6 +420,8 @@ __global__ __launch_bounds__(kSortNT) void cal_chunk_sort(const int32_t* __restr
         for (int i = threadIdx.x; i < cnt; i += kSortNT) sorted[lo + i] = lsort[i];
     }
     if (threadIdx.x == 0) max_part[c] = mx;
+    if (c == 0)   // the selection that follows raises them
+        for (int i = threadIdx.x; i < nb; i += kSortNT) qflag[i] = 0u;
 }
 
 // Digit of the k-th element among the 256 bins of hist (one wavefront).
@@ -448,19 +453,41 @@ __device__ inline void hist_flush_zeros(uint32_t* hist, uint32_t zeros) {
     if ((threadIdx.x % kWave) == 0 && zeros != 0) atomicAdd(&hist[0], zeros);
 }
 
-// One workgroup per bucket: its size n_b and rank k_b (Eq. (3)) from the
-// run sizes, then the k_b-th smallest score of its runs, most significant
-// 8-bit digit first from the top digit of the largest score.  A bucket of at
-// most kSelNT * kKeep scores is gathered once (runs into LDS, then into
-// registers) and kept across passes; a larger one is read from its runs on
-// every pass.
-__global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, int64_t chunks, int32_t alpha_ppm,
-                                                            const int32_t* __restrict__ sorted,
-                                                            const uint32_t* __restrict__ run_cnt,
-                                                            const uint32_t* __restrict__ run_start,
-                                                            const uint32_t* __restrict__ max_part,
-                                                            int32_t* __restrict__ q_out,
-                                                            int32_t* __restrict__ count_out) {
+// Thread 0 of a selecting workgroup: bucket b's quantile, published with
+// its ready bit in one device-coherent word (the value is the flag, so no
+// fence orders it against other stores).
+__device__ inline void publish_q(uint64_t* qflag, int b, int32_t q) {
+    if (qflag != nullptr && threadIdx.x == 0)
+        __hip_atomic_store(&qflag[b], (uint64_t(1) << 32) | uint32_t(q), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct SelectArgs {
+    int nb;
+    int64_t chunks;
+    int32_t alpha_ppm;
+    const int32_t* sorted;
+    const uint32_t* run_cnt;
+    const uint32_t* run_start;
+    const uint32_t* max_part;
+    int32_t* q_out;
+    int32_t* count_out;
+    uint64_t* qflag;   // NULL when no apply workgroup waits
+};
+
+// Workgroup b of a selection: bucket b's size n_b and rank k_b (Eq. (3))
+// from the run sizes, then the k_b-th smallest score of its runs, most
+// significant 8-bit digit first from the top digit of the largest score.  A
+// bucket of at most kSelNT * kKeep scores is gathered once (runs into LDS,
+// then into registers) and kept across passes; a larger one is read from its
+// runs on every pass.
+__device__ void select_bucket(const SelectArgs& A, int b) {
+    const int nb = A.nb;
+    const int64_t chunks = A.chunks;
+    const int32_t alpha_ppm = A.alpha_ppm;
+    const int32_t* __restrict__ sorted = A.sorted;
+    int32_t* q_out = A.q_out;
+    int32_t* count_out = A.count_out;
+    (void)nb;
     extern __shared__ __align__(16) uint32_t stage[];   // [kSelNT * kKeep] the bucket's scores
     __shared__ uint32_t roff[kSortMaxChunks];           // where each run starts among the bucket's scores
     __shared__ uint32_t rcnt[kSortMaxChunks];           // its size
@@ -468,14 +495,13 @@ __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, int64_t chun
     __shared__ uint32_t hist[256];
     __shared__ uint32_t red[kSelWaves];
     __shared__ uint32_t pick[2];
-    const int b = blockIdx.x;
     const int t = threadIdx.x;
     const int lane = t % kWave, w = t / kWave;
     uint32_t c = 0, m = 0, src = 0;
     if (t < chunks) {
-        c = run_cnt[int64_t(b) * chunks + t];
-        src = uint32_t(t * kChunk) + run_start[int64_t(b) * chunks + t];
-        m = max_part[t];
+        c = A.run_cnt[int64_t(b) * chunks + t];
+        src = uint32_t(t * kChunk) + A.run_start[int64_t(b) * chunks + t];
+        m = A.max_part[t];
     }
     uint32_t nbk;
     const uint32_t off = block_excl_scan<kSelNT, false>(c, 0u, red, &nbk);
@@ -489,6 +515,7 @@ __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, int64_t chun
     if (t == 0) count_out[b] = int32_t(nbk);
     if (k64 > int64_t(nbk)) {
         if (t == 0) q_out[b] = MAPS_Q_INF;
+        publish_q(A.qflag, b, MAPS_Q_INF);
         return;
     }
     int32_t k = int32_t(k64);
@@ -564,6 +591,98 @@ __global__ __launch_bounds__(kSelNT) void cal_bucket_select(int nb, int64_t chun
         __syncthreads();
     }
     if (t == 0) q_out[b] = int32_t(prefix);
+    publish_q(A.qflag, b, int32_t(prefix));
+}
+
+// The selection alone: one workgroup per bucket.
+__global__ __launch_bounds__(kSelNT) void cal_bucket_select(SelectArgs A) { select_bucket(A, int(blockIdx.x)); }
+
+struct ApplyArgs {
+    const int32_t* edges;
+    const int32_t* pred;
+    int64_t m;
+    int32_t u_max;
+    int32_t* U;
+    uint32_t* dev_err;
+};
+
+constexpr int kApplyFusedPer = 8;              // bounds per thread of a fused apply workgroup
+constexpr uint32_t kMaxSpins = 1u << 17;       // polls of the ready count before giving up (tens of ms)
+static_assert(2 * kSelStageBytes > 160 * 1024, "one workgroup of the fused launch per CU");
+
+// Apply workgroup j of ga in the fused launch (Eq. (4)): its first
+// predictions are loaded and their buckets found while the selection runs;
+// then thread i < nb waits (bounded) for bucket i's published quantile, and
+// the workgroup writes its bounds, then the rest of its share.
+__device__ void apply_after_select(const SelectArgs& S, const ApplyArgs& A, int j, int ga) {
+    extern __shared__ __align__(16) uint32_t stage[];
+    const int nb = S.nb, ne = nb - 1;
+    const int t = threadIdx.x;
+    int32_t* le = reinterpret_cast<int32_t*>(stage);   // [ne] edges
+    int32_t* lq = le + ne;                             // [nb] quantiles
+    constexpr int kA = kApplyFusedPer;
+    const int64_t stride = int64_t(ga) * kSelNT * kA;
+    int32_t p[kA];
+    int bk[kA];
+    auto fetch = [&](int64_t c0) {
+#pragma unroll
+        for (int i = 0; i < kA; ++i) {
+            const int64_t x = c0 + int64_t(i) * kSelNT + t;
+            p[i] = x < A.m ? A.pred[x] : -1;
+        }
+    };
+    auto emit = [&](int64_t c0) {
+#pragma unroll
+        for (int i = 0; i < kA; ++i) {
+            const int64_t x = c0 + int64_t(i) * kSelNT + t;
+            if (x >= A.m) continue;
+            int32_t out = -1;   // no prediction: no bound
+            if (p[i] >= 0) {
+                const int32_t qb = lq[bk[i]];
+                const int64_t v = int64_t(p[i]) + qb;   // Eq. (4)
+                out = (qb == MAPS_Q_INF || v > A.u_max) ? A.u_max : int32_t(v);
+            }
+            A.U[x] = out;
+        }
+    };
+    int64_t c0 = int64_t(j) * kSelNT * kA;
+    fetch(c0);
+    for (int i = t; i < ne; i += kSelNT) le[i] = A.edges[i];
+    __syncthreads();
+    buckets_of<kA>(le, ne, p, bk);
+    for (int i0 = 0; i0 < nb; i0 += kSelNT) {   // uniform across the workgroup
+        const int i = i0 + t;
+        if (i0 + (t & ~(kWave - 1)) >= nb) continue;   // wavefronts past nb: nothing to wait for
+        uint64_t v = 0;
+        uint32_t spins = 0;
+        for (;;) {   // device-coherent polls, no cache invalidation
+            v = i < nb ? __hip_atomic_load(&S.qflag[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                       : (uint64_t(1) << 32);
+            if (__all(int(v >> 32) != 0)) break;
+            if (++spins > kMaxSpins) {
+                if (t % kWave == 0) raise_error(A.dev_err, MAPS_ERR_WAIT_TIMEOUT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(8);
+        }
+        if (i < nb) lq[i] = int32_t(uint32_t(v));
+    }
+    __syncthreads();
+    emit(c0);
+    for (c0 += stride; c0 < A.m; c0 += stride) {
+        fetch(c0);
+        buckets_of<kA>(le, ne, p, bk);
+        emit(c0);
+    }
+}
+
+// Selection and bounds in one launch: workgroups [0, nb) select, the rest
+// apply.  Every workgroup holds more than half of a CU's LDS and the grid is
+// at most the CU count, so all of them are resident at once and the apply
+// workgroups' wait ends.
+__global__ __launch_bounds__(kSelNT) void cal_select_apply(SelectArgs S, ApplyArgs A) {
+    if (int(blockIdx.x) < S.nb) select_bucket(S, int(blockIdx.x));
+    else apply_after_select(S, A, int(blockIdx.x) - S.nb, int(gridDim.x) - S.nb);
 }
 
 int grid_for(int64_t n, int nt, int per_thread, int cap) {
@@ -588,21 +707,38 @@ namespace {
 // Calibration by counting sort (up to kFastBuckets buckets and
 // kSortMaxChunks chunks of kChunk residuals): chunks sorted by bucket, then
 // one workgroup per bucket.
+// When the grid fits the CUs, the bounds are written by extra workgroups of
+// the selection's launch (*applied = true).
 maps_status calibrate_fast(const int32_t* pred, const int32_t* truth, int64_t n, const int32_t* edges, int32_t nb,
-                           int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, uint32_t* dev_err,
-                           void* workspace, hipStream_t stream) {
+                           int32_t alpha_ppm, int32_t* q_out, int32_t* count_out, const ApplyArgs& apply,
+                           uint32_t* dev_err, void* workspace, hipStream_t stream, bool* applied) {
     const FastWorkspace w = fast_carve(workspace, n, nb);
     const int64_t chunks = sort_chunks(n);
+    *applied = false;
     if (n > 0) {
         const size_t lds_sort = size_t(kChunk) * 4 + size_t(3 * nb - 1) * 4;   // chunk, edges, run sizes and starts
         allow_dynamic_lds(cal_chunk_sort, lds_sort);
         hipLaunchKernelGGL(cal_chunk_sort, dim3(unsigned(chunks)), dim3(kSortNT), lds_sort, stream, pred, truth, n,
-                           edges, nb, chunks, w.run_cnt, w.run_start, w.max_part, w.sorted, dev_err);
+                           edges, nb, chunks, w.run_cnt, w.run_start, w.max_part, w.sorted, w.qflag, dev_err);
         MAPS_CHECK_LAUNCH();
     }
+    SelectArgs S{nb, chunks, alpha_ppm, w.sorted, w.run_cnt, w.run_start, w.max_part, q_out, count_out, nullptr};
+    const int cus = device_compute_units();
+    const int64_t per_wg = int64_t(kSelNT) * kApplyFusedPer;
+    // the flags are cleared by the chunk sort, so the fused launch needs n > 0
+    if (n > 0 && apply.m > 0 && int64_t(nb) + 1 <= cus) {
+        const int64_t need = (apply.m + per_wg - 1) / per_wg;
+        const int64_t ga = need < cus - nb ? need : cus - nb;
+        S.qflag = w.qflag;
+        allow_dynamic_lds(cal_select_apply, kSelStageBytes);
+        hipLaunchKernelGGL(cal_select_apply, dim3(unsigned(nb + ga)), dim3(kSelNT), kSelStageBytes, stream, S,
+                           apply);
+        MAPS_CHECK_LAUNCH();
+        *applied = true;
+        return MAPS_OK;
+    }
     allow_dynamic_lds(cal_bucket_select, kSelStageBytes);
-    hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), kSelStageBytes, stream, nb, chunks,
-                       alpha_ppm, w.sorted, w.run_cnt, w.run_start, w.max_part, q_out, count_out);
+    hipLaunchKernelGGL(cal_bucket_select, dim3(unsigned(nb)), dim3(kSelNT), kSelStageBytes, stream, S);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }
@@ -670,16 +806,18 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
         return MAPS_E_NULL;
     if (workspace_bytes < maps_calibrate_workspace_size(n, nb)) return MAPS_E_WORKSPACE;
     const int ne = nb - 1;
+    bool applied = false;
     if (fast_path(n, nb)) {
-        const maps_status st =
-            calibrate_fast(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, dev_err, workspace, stream);
+        const ApplyArgs apply{edges, apply_pred, m, u_max, U_out, dev_err};
+        const maps_status st = calibrate_fast(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, apply, dev_err,
+                                              workspace, stream, &applied);
         if (st != MAPS_OK) return st;
     } else {
         const maps_status st =
             calibrate_general(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, dev_err, workspace, stream);
         if (st != MAPS_OK) return st;
     }
-    if (m > 0) {
+    if (m > 0 && !applied) {
         const bool lds_edges = nb <= kLdsEdgesMax;
         const int g = grid_for(m, kNT, kApplyPer, 8192);
         if (lds_edges)
