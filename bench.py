@@ -28,7 +28,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
 DEFAULT_WORKLOAD = "large"     # 256 decoders x 4096 residents, 262,144 arrivals
 PLACE_SAMPLE = 5               # placement bracketed by timing events on every 5th timed step
 BREAKDOWN_STEPS = 10           # untimed steps with an event at every phase boundary
-PLACEMENT_SOURCES = ("paper_2609_15359_amd/csrc/place.hip", "paper_2609_15359_amd/csrc/maps_internal.hpp")
+PLACEMENT_SOURCES = ("paper_2609_15359_amd/csrc/place.hip", "paper_2609_15359_amd/csrc/maps_internal.hpp",
+                     "paper_2609_15359_amd/csrc/order_core.hpp")
 
 
 def placement_source_hash() -> str:
@@ -165,19 +166,22 @@ def main():
     D, A = b.decoders, b.arrivals
     db = pipeline.to_device(b)
     ws = pipeline.Workspaces(db, want_pairs=True)
-    phases = pipeline.step_phases(db, ws)
+    # placement and local order in one call: the final selection and the
+    # local orders share a launch
+    phases = pipeline.step_phases(db, ws, fused=True)
+    names = pipeline.PHASES_FUSED
 
     ws.dev_err.zero_()
     for fn in phases:   # one eager step: the reference for the replayed graphs
         fn()
     eager = (ws.placement.choice.clone(), ws.placement.pair_peak.sum(dtype=torch.int64), ws.order.clone())
-    graphs = pipeline.StepGraphs(db, ws) if args.graph else None
+    graphs = pipeline.StepGraphs(db, ws, fused=True) if args.graph else None
 
     def one_step(ev=None, place_ev=None):
         """One step; `ev` brackets every phase, `place_ev` only placement.
         Timing events are created without the system-scope fence."""
         if graphs is not None:
-            graphs.replay(ev if ev else ([None, None, place_ev[0], place_ev[1], None] if place_ev else None))
+            graphs.replay(ev if ev else ([None, None, place_ev[0], place_ev[1]] if place_ev else None))
             return
         for i, fn in enumerate(phases):
             if ev:
@@ -215,12 +219,12 @@ def main():
             and int(eager[1]) == int(ws.placement.pair_peak.sum(dtype=torch.int64))):
         raise SystemExit("replayed steps differ from the eager step")
     place_ms = statistics.mean(a.elapsed_time(b) for a, b in place_events.values())
-    events = [[TimingEvent() for _ in range(len(pipeline.PHASES) + 1)] for _ in range(BREAKDOWN_STEPS)]
+    events = [[TimingEvent() for _ in range(len(names) + 1)] for _ in range(BREAKDOWN_STEPS)]
     for ev in events:
         one_step(ev)
     torch.cuda.synchronize()
     parts = {name: statistics.median(ev[i].elapsed_time(ev[i + 1]) for ev in events)
-             for i, name in enumerate(pipeline.PHASES)}
+             for i, name in enumerate(names)}
 
     # algorithmic bytes of the placement pass, from the snapshot's own event counts
     hdr = ws.snapshot[256:256 + 64 * D].view(torch.int32).view(D, 16).cpu().numpy()
@@ -250,7 +254,8 @@ def main():
                    "launch": "one HIP graph per phase" if args.graph else "host launches"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
-                     "kernel": "maps_place (place_records + place_finish)",
+                     "kernel": "maps_place_order (place_records, then place_finish_order: placement's final "
+                               "selection and every local order in one launch)",
                      "algorithmic_bytes": nbytes, "place_ms": place_ms},
         "breakdown_ms": parts,
         "breakdown_note": f"median of {BREAKDOWN_STEPS} untimed steps with a timing event (no system "

@@ -206,6 +206,35 @@ maps_status maps_local_order(const void* snapshot, int32_t D, int32_t u_max,
                              uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/* ------------------------------------------------------------------------ */
+/* 3 + 4. Placement and local order in two launches (Algorithm 1; Sec. 3.3, */
+/*        Eq. (7))                                                           */
+/* ------------------------------------------------------------------------ */
+/*
+ * Exactly maps_place followed by maps_local_order on the same snapshot, D,
+ * u_max and capacity (the arguments keep their meaning, layout and ownership;
+ * q_total is maps_local_order's `total`; one dev_err word and the placement
+ * workspace of maps_place_workspace_size(D, A, u_max) bytes), with the same
+ * outputs bit for bit.  The final selection of placement and every decoder's
+ * local order share one launch, so the order costs no launch of its own and
+ * runs beside the selection.  A may be 0 (then only the orders are computed).
+ * dev_err bits: those of both calls.
+ * Host errors: those of both calls; nothing is enqueued when either argument
+ * set is rejected.
+ */
+maps_status maps_place_order(const void* snapshot, int32_t D, int32_t u_max,
+                             const int32_t* capacity, const int32_t* queue_len,
+                             const int32_t* a_prompt, const int32_t* a_upper, int64_t A,
+                             int32_t policy, int64_t rr_offset,
+                             int32_t* choice, int32_t* chosen_peak, int32_t* chosen_overflow,
+                             uint8_t* flags, int32_t* pair_peak,
+                             const int64_t* q_off, int64_t q_total,
+                             const int32_t* q_prompt, const int32_t* q_upper,
+                             const int32_t* q_wait_ms, int32_t max_wait_ms,
+                             int32_t* order, int32_t* admitted,
+                             uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
 /* Static description of a status code (host). */
 const char* maps_status_string(maps_status status);
 

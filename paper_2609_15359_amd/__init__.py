@@ -51,6 +51,8 @@ _SIGNATURES = {
     "maps_local_order_workspace_size": (_sz, [_i32, _i64]),
     "maps_local_order": (_i32, [_vp, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                 _vp, _sz, _vp]),
+    "maps_place_order": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp,
+                                _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)
@@ -276,3 +278,51 @@ def local_order(snapshot: Snapshot, capacity, q_off, q_prompt, q_upper, q_wait_m
                                     _ptr(err), None, 0, _stream(dev))
     _check(st, "maps_local_order")
     return order, admitted, err
+
+
+# ---------------------------------------------------------------------------
+# 3 + 4. placement and local order in two launches
+# ---------------------------------------------------------------------------
+
+def place_order(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, q_off, q_prompt, q_upper,
+                q_wait_ms=None, max_wait_ms: int = 2**31 - 1, policy: int = POLICY_MQ, rr_offset: int = 0,
+                want_pairs: bool = True, dev_err=None, workspace=None, out: Placement | None = None,
+                order=None, admitted=None):
+    """place() then local_order() on the same snapshot, with the final
+    selection and the local orders in one launch; returns (Placement, order,
+    admitted)."""
+    capacity = _dev(capacity, torch.int32, "capacity")
+    dev = capacity.device
+    queue_len = _dev(queue_len, torch.int32, "queue_len")
+    a_prompt = _dev(a_prompt, torch.int32, "a_prompt")
+    a_upper = _dev(a_upper, torch.int32, "a_upper")
+    q_off = _dev(q_off, torch.int64, "q_off")
+    q_prompt = _dev(q_prompt, torch.int32, "q_prompt")
+    q_upper = _dev(q_upper, torch.int32, "q_upper")
+    if q_wait_ms is not None:
+        _dev(q_wait_ms, torch.int32, "q_wait_ms")
+    D, A, total = snapshot.D, a_prompt.numel(), q_prompt.numel()
+    if capacity.numel() != D or queue_len.numel() != D or a_upper.numel() != A:
+        raise MapsError("capacity/queue_len must have D entries and a_upper A entries")
+    if q_off.numel() != D + 1 or q_upper.numel() != total:
+        raise MapsError("q_off must have D+1 entries and q_upper as many as q_prompt")
+    if out is None:
+        out = Placement(
+            choice=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_peak=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_overflow=torch.empty(A, dtype=torch.int32, device=dev),
+            flags=torch.empty(A, dtype=torch.uint8, device=dev),
+            pair_peak=torch.empty((D, A), dtype=torch.int32, device=dev) if want_pairs else None,
+            dev_err=new_error_word(dev) if dev_err is None else dev_err)
+    order = torch.empty(total, dtype=torch.int32, device=dev) if order is None else order
+    admitted = torch.empty(D, dtype=torch.int32, device=dev) if admitted is None else admitted
+    lib = library()
+    ws = _workspace(lib.maps_place_workspace_size(D, A, snapshot.u_max), dev, workspace)
+    st = lib.maps_place_order(_ptr(snapshot.data), D, snapshot.u_max, _ptr(capacity), _ptr(queue_len),
+                              _ptr(a_prompt), _ptr(a_upper), A, int(policy), int(rr_offset),
+                              _ptr(out.choice), _ptr(out.chosen_peak), _ptr(out.chosen_overflow),
+                              _ptr(out.flags), _ptr(out.pair_peak), _ptr(q_off), total, _ptr(q_prompt),
+                              _ptr(q_upper), _ptr(q_wait_ms), int(max_wait_ms), _ptr(order), _ptr(admitted),
+                              _ptr(out.dev_err), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "maps_place_order")
+    return out, order, admitted

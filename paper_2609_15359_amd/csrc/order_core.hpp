@@ -1,0 +1,265 @@
+#pragma once
+// Local SJF order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10)) on gfx950:
+// the device code, shared by the local-order launch and the launch that ends
+// placement and orders every local queue.
+//
+// One workgroup per decoder:
+//   1. bitonic sort in LDS of the packed keys (promoted?0:1, promoted? index :
+//      bound, index) -- unique keys, so the order is the stable one;
+//   2. a second bitonic sort of (bound, index) gives the queue by bound, with
+//      the start of each run of equal bounds;
+//   (a queue of at most 64 requests is sorted in the lanes of one wavefront);
+//   3. admitted = the largest k whose prefix keeps the projected peak within
+//      the capacity, by binary search over k (the peak never decreases when a
+//      request is added).  For a prefix, residents plus admitted requests form
+//      a curve that increases between breakpoints -- the residents' event
+//      times and the requests' bounds -- so the peak is its maximum over those
+//      points.  At a point t the prefix contributes sum (p_i + t) over members
+//      with bound >= t: masked suffix sums over the bound-sorted queue give it
+//      in O(1) after one scan per k.  Residents' occupancy comes from the
+//      snapshot (record S + t N at the rank of t).
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace order {
+
+constexpr int kOrderNT = 1024;
+constexpr int kMaxQ = MAPS_MAX_LOCAL_QUEUE;
+
+struct LocalArgs {
+    SnapLayout L;
+    const void* snap;
+    const int32_t* cap;
+    const int64_t* q_off;
+    int64_t total;
+    const int32_t* qp;
+    const int32_t* qU;
+    const int32_t* qwait;
+    int32_t max_wait;
+    int32_t* order;
+    int32_t* admitted;
+    uint32_t* dev_err;
+};
+
+struct LocalLds {
+    // the sort keys (steps 1-2) and the prompt suffix sums (step 3) are never
+    // live together: sharing their space leaves room for two workgroups per CU
+    union {
+        uint64_t keys[kMaxQ];
+        int64_t psuf[kMaxQ + 1];  // prompts summed over the members csuf counts
+    };
+    int32_t pos[kMaxQ];       // position of queue entry i in the new order
+    int32_t ue[kMaxQ];        // bound of entry i (missing bound -> u_max)
+    int32_t pp[kMaxQ];        // prompt of entry i
+    int32_t uidx[kMaxQ];      // entries sorted by (bound, index)
+    int32_t grp[kMaxQ];       // first position of the run of equal bounds
+    int32_t csuf[kMaxQ + 1];  // members of the prefix with bound >= that position's bound
+    int64_t red64[kOrderNT / kWave];
+    int32_t red32[kOrderNT / kWave];
+};
+
+__device__ inline void bitonic_sort(uint64_t* keys, int n2) {
+    for (int k = 2; k <= n2; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < n2; i += kOrderNT) {
+                const int ixj = i ^ j;
+                if (ixj > i) {
+                    const uint64_t a = keys[i], b = keys[ixj];
+                    const bool up = (i & k) == 0;
+                    if ((a > b) == up) { keys[i] = b; keys[ixj] = a; }
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Ascending sort of one key per lane across a wavefront (bitonic network
+// through lane shuffles: no LDS, no barrier).
+__device__ inline uint64_t wave_bitonic(uint64_t key) {
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const uint64_t other = __shfl_xor(key, j, kWave);
+            const bool ascending = (lane & k) == 0;
+            const bool lower = (lane & j) == 0;
+            key = (lower == ascending) ? (key < other ? key : other) : (key > other ? key : other);
+        }
+    }
+    return key;
+}
+
+// Largest projected peak of the residents plus the first k requests of the new order.
+__device__ inline int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, const int2* cold, int32_t E,
+                               int32_t W) {
+    block_scan<kOrderNT, false, true, false, int32_t>(
+        n, 0, [&](int64_t i) { return int32_t(s.pos[s.uidx[i]] < k); },
+        [&](int64_t i, int32_t v) { s.csuf[i] = v; }, s.red32);
+    block_scan<kOrderNT, false, true, false, int64_t>(
+        n, int64_t(0), [&](int64_t i) { const int j = s.uidx[i]; return s.pos[j] < k ? int64_t(s.pp[j]) : int64_t(0); },
+        [&](int64_t i, int64_t v) { s.psuf[i] = v; }, s.red64);
+    if (threadIdx.x == 0) { s.csuf[n] = 0; s.psuf[n] = 0; }
+    __syncthreads();
+    int64_t best = 0;
+    // resident event times: the set bits of the rank words, event e the
+    // (before + j)-th of them
+    for (int w = threadIdx.x; w < W; w += kOrderNT) {
+        const uint2 rw = rank[w];
+        uint32_t bits = rw.x, e = rw.y;
+        for (; bits != 0u && e < uint32_t(E); bits &= bits - 1u, ++e) {
+            const int64_t tau = int64_t(w) * 32 + (__ffs(bits) - 1);
+            const int2 r = cold[e];
+            int lo = 0, hi = n;   // first bound-sorted position with bound >= tau
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s.ue[s.uidx[mid]] < tau) lo = mid + 1; else hi = mid;
+            }
+            const int64_t v = int64_t(r.x) + tau * (r.y - 1) + s.psuf[lo] + tau * s.csuf[lo];
+            best = best > v ? best : v;
+        }
+    }
+    // bounds of the admitted requests
+    const int32_t ucl_max = 32 * W - 1;
+    for (int i = threadIdx.x; i < n; i += kOrderNT) {
+        const int j = s.uidx[i];
+        if (s.pos[j] >= k) continue;
+        const int64_t t = s.ue[j];
+        const int32_t tc = t < ucl_max ? int32_t(t) : ucl_max;
+        const uint2 w = rank[tc >> 5];
+        uint32_t e = w.y + __popc(w.x & ((1u << (tc & 31)) - 1u));
+        e = e < uint32_t(E) ? e : uint32_t(E);
+        const int2 r = cold[e];
+        const int64_t occ = e < uint32_t(E) ? int64_t(r.x) + t * (r.y - 1) : 0;
+        const int g0 = s.grp[i];
+        const int64_t v = occ + s.psuf[g0] + t * s.csuf[g0];
+        best = best > v ? best : v;
+    }
+    return block_reduce_max<kOrderNT>(best, s.red64);
+}
+
+// The whole local order of decoder d by one workgroup of kOrderNT threads.
+__device__ inline void order_queue(const LocalArgs& g, int32_t d) {
+    __shared__ LocalLds s;
+    const SnapLayout& L = g.L;
+    const SnapView V = snap_view(const_cast<void*>(g.snap), L);
+    const SnapHeader hdr = *V.hdr;
+    if (!(hdr.magic == kSnapMagic && hdr.D == L.D && hdr.u_max == L.u_max && hdr.W == L.W)) {
+        if (d == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    const DecHeader h = V.dec[d];
+    if (!slice_ok(h, hdr.n_total, L)) {
+        if (threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    int64_t qlo = g.q_off[d], qhi = g.q_off[d + 1];
+    if (!(0 <= qlo && qlo <= qhi && qhi <= g.total)) {
+        if (threadIdx.x == 0) { raise_error(g.dev_err, MAPS_ERR_SEG_OFFSETS); g.admitted[d] = 0; }
+        return;
+    }
+    const int64_t n64 = qhi - qlo;
+    if (n64 > kMaxQ) {
+        if (threadIdx.x == 0) { raise_error(g.dev_err, MAPS_ERR_QUEUE_TOO_LONG); g.admitted[d] = 0; }
+        return;
+    }
+    const int n = int(n64);
+    const int32_t C = g.cap[d];
+    if (threadIdx.x == 0 && C < 0) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+    int n2 = 1;
+    while (n2 < n) n2 <<= 1;
+
+    if (n2 <= kWave) {
+        // a queue of at most one wavefront: both sorts and the runs of equal
+        // bounds in the lanes of wave 0 (key i in lane i)
+        if (threadIdx.x < kWave) {
+            const int i = threadIdx.x;
+            uint64_t key = ~0ull, key2 = ~0ull;
+            bool neg = false;
+            if (i < n) {
+                const int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
+                neg = pr < 0;
+                s.pp[i] = pr < 0 ? 0 : pr;
+                const int32_t ue = u < 0 ? L.u_max : u;
+                s.ue[i] = ue;
+                const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
+                const uint64_t cls = promoted ? 0ull : (1ull << 63);
+                const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
+                key = cls | (val << 32) | uint64_t(uint32_t(i));
+                key2 = (uint64_t(uint32_t(ue)) << 32) | uint64_t(uint32_t(i));
+            }
+            if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+            key = wave_bitonic(key);
+            key2 = wave_bitonic(key2);
+            if (i < n) {
+                const int idx = int(uint32_t(key));
+                g.order[qlo + i] = idx;
+                s.pos[idx] = i;
+                s.uidx[i] = int(uint32_t(key2));
+            }
+            const uint32_t b = uint32_t(key2 >> 32);
+            const uint32_t prev = __shfl_up(b, 1, kWave);
+            const int32_t start = (i == 0 || prev != b) ? i : 0;
+            const int32_t run = wave_incl_scan_max(start);
+            if (i < n) s.grp[i] = run;
+        }
+        __syncthreads();
+    } else {
+        // 1. the new order (Eq. (7) with promotion)
+        bool neg = false;
+        for (int i = threadIdx.x; i < n2; i += kOrderNT) {
+            if (i < n) {
+                int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
+                neg |= pr < 0;
+                s.pp[i] = pr < 0 ? 0 : pr;
+                const int32_t ue = u < 0 ? L.u_max : u;
+                s.ue[i] = ue;
+                const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
+                const uint64_t cls = promoted ? 0ull : (1ull << 63);
+                const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
+                s.keys[i] = cls | (val << 32) | uint64_t(uint32_t(i));
+            } else {
+                s.keys[i] = ~0ull;
+            }
+        }
+        if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+        __syncthreads();
+        bitonic_sort(s.keys, n2);
+        for (int i = threadIdx.x; i < n; i += kOrderNT) {
+            const int idx = int(uint32_t(s.keys[i]));
+            g.order[qlo + i] = idx;
+            s.pos[idx] = i;
+        }
+        __syncthreads();
+
+        // 2. the queue sorted by bound
+        for (int i = threadIdx.x; i < n2; i += kOrderNT)
+            s.keys[i] = i < n ? ((uint64_t(uint32_t(s.ue[i])) << 32) | uint64_t(uint32_t(i))) : ~0ull;
+        __syncthreads();
+        bitonic_sort(s.keys, n2);
+        for (int i = threadIdx.x; i < n; i += kOrderNT) s.uidx[i] = int(uint32_t(s.keys[i]));
+        __syncthreads();
+        block_scan<kOrderNT, true, false, false, int32_t>(
+            n, 0,
+            [&](int64_t i) { return (i == 0 || s.ue[s.uidx[i - 1]] != s.ue[s.uidx[i]]) ? int32_t(i) : 0; },
+            [&](int64_t i, int32_t v) { s.grp[i] = v; }, s.red32);
+    }
+
+    // 3. admission: largest k with peak(k) <= C
+    const uint2* rank = slice_rank(V, h);
+    const int2* cold = slice_cold(V, h, L);
+    int lo = 0;
+    if (h.base_peak <= C) {
+        int hi = n;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            const int64_t pk = prefix_peak(s, n, mid, rank, cold, h.E, L.W);
+            if (pk <= C) lo = mid; else hi = mid - 1;
+        }
+    }
+    if (threadIdx.x == 0) g.admitted[d] = lo;
+}
+
+}  // namespace order
+}  // namespace maps

@@ -25,6 +25,7 @@
 // feasible decoder, by queue length, then the smallest overflow; policy MC
 // the largest slack.
 #include "maps_internal.hpp"
+#include "order_core.hpp"
 
 namespace maps {
 namespace {
@@ -695,14 +696,14 @@ __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
 // the peak back; a feasible MQ choice evaluates its pair once more from the
 // snapshot's records.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
+// The final selection for arrivals first, first + stride, ...
+__device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_t stride) {
     const SnapLayout& L = g.L;
     const SnapView V = snap_view(const_cast<void*>(g.snap), L);
     if (!snapshot_ok(V.hdr, L)) return;
     const int64_t n_total = load_uniform(&V.hdr->n_total);
     const int32_t ucl_max = 32 * L.W - 1;
-    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    for (int64_t a = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; a < g.A; a += stride) {
+    for (int64_t a = first; a < g.A; a += stride) {
         const int32_t U = g.aU[a];
         if (U < 0) {
             g.choice[a] = int32_t((g.rr_offset + a) % L.D);
@@ -742,6 +743,25 @@ __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
         g.chosen_over[a] = peak > C ? peak - C : 0;
         g.flags[a] = peak <= C ? 1 : 0;
     }
+}
+
+__global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
+    finish_arrivals(g, int64_t(blockIdx.x) * blockDim.x + threadIdx.x, int64_t(gridDim.x) * blockDim.x);
+}
+
+// The end of placement and every decoder's local order in one launch:
+// workgroups [0, D) order one local queue each (dispatched first: they are
+// the longer, latency-bound ones), the others make the final selection.  The
+// two read the same snapshot and write disjoint outputs, so the selection
+// runs beside the queue work.
+__global__ __launch_bounds__(order::kOrderNT) void place_finish_order(PlaceArgs g, order::LocalArgs o,
+                                                                      int32_t fin_blocks) {
+    const int32_t D = o.L.D;
+    if (int32_t(blockIdx.x) < D)
+        order::order_queue(o, int32_t(blockIdx.x));
+    else
+        finish_arrivals(g, int64_t(int32_t(blockIdx.x) - D) * order::kOrderNT + threadIdx.x,
+                        int64_t(fin_blocks) * order::kOrderNT);
 }
 
 // ---------------------------------------------------------------------------
@@ -815,12 +835,17 @@ extern "C" size_t maps_place_workspace_size(int32_t D, int64_t A, int32_t u_max)
     return place_carve(nullptr, A).bytes;
 }
 
-extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max, const int32_t* capacity,
+namespace {
+
+// Checks the arguments of a placement and, when A > 0, launches its records
+// pass and fills *out for the final selection (*launched = A > 0).
+maps_status place_records_enqueue(const void* snapshot, int32_t D, int32_t u_max, const int32_t* capacity,
                                   const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
                                   int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
                                   int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
                                   int32_t* pair_peak, uint32_t* dev_err, void* workspace,
-                                  size_t workspace_bytes, hipStream_t stream) {
+                                  size_t workspace_bytes, hipStream_t stream, PlaceArgs* out, bool* launched) {
+    *launched = false;
     if (D < 1 || A < 0 || rr_offset < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
     if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
     if (!snapshot || !capacity || !queue_len || !dev_err ||
@@ -879,8 +904,74 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
         default: launch_apt<1>(prof, pairs, policy, grid, lds, stream, a); break;
     }
     MAPS_CHECK_LAUNCH();
+    *out = a;
+    *launched = true;
+    return MAPS_OK;
+}
+
+}  // namespace
+
+extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max, const int32_t* capacity,
+                                  const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
+                                  int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
+                                  int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
+                                  int32_t* pair_peak, uint32_t* dev_err, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+    PlaceArgs a{};
+    bool launched = false;
+    const maps_status st = place_records_enqueue(snapshot, D, u_max, capacity, queue_len, a_prompt, a_upper, A,
+                                                 policy, rr_offset, choice, chosen_peak, chosen_overflow, flags,
+                                                 pair_peak, dev_err, workspace, workspace_bytes, stream, &a,
+                                                 &launched);
+    if (st != MAPS_OK || !launched) return st;
     const int64_t blocks = (A + 255) / 256;
     hipLaunchKernelGGL(place_finish, dim3(unsigned(blocks < 4096 ? blocks : 4096)), dim3(256), 0, stream, a);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+extern "C" maps_status maps_place_order(const void* snapshot, int32_t D, int32_t u_max, const int32_t* capacity,
+                                        const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
+                                        int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
+                                        int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
+                                        int32_t* pair_peak, const int64_t* q_off, int64_t q_total,
+                                        const int32_t* q_prompt, const int32_t* q_upper, const int32_t* q_wait_ms,
+                                        int32_t max_wait_ms, int32_t* order, int32_t* admitted, uint32_t* dev_err,
+                                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    // the local-order arguments first: nothing is enqueued when either set is wrong
+    if (D < 1 || q_total < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
+    if (!q_off || !admitted || (q_total > 0 && (!q_prompt || !q_upper || !order))) return MAPS_E_NULL;
+    if (D < 1 || A < 0 || rr_offset < 0) return MAPS_E_SIZE;
+    if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
+    if (!snapshot || !capacity || !queue_len || !dev_err ||
+        (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags)) ||
+        (A > 0 && !workspace))
+        return MAPS_E_NULL;
+    if (A > 0 && workspace_bytes < place_carve(nullptr, A).bytes) return MAPS_E_WORKSPACE;
+    PlaceArgs a{};
+    bool launched = false;
+    const maps_status st = place_records_enqueue(snapshot, D, u_max, capacity, queue_len, a_prompt, a_upper, A,
+                                                 policy, rr_offset, choice, chosen_peak, chosen_overflow, flags,
+                                                 pair_peak, dev_err, workspace, workspace_bytes, stream, &a,
+                                                 &launched);
+    if (st != MAPS_OK) return st;
+    order::LocalArgs o;
+    o.L = snap_layout(D, 0, u_max);
+    o.snap = snapshot;
+    o.cap = capacity;
+    o.q_off = q_off;
+    o.total = q_total;
+    o.qp = q_prompt;
+    o.qU = q_upper;
+    o.qwait = q_wait_ms;
+    o.max_wait = max_wait_ms;
+    o.order = order;
+    o.admitted = admitted;
+    o.dev_err = dev_err;
+    int64_t fin = launched ? (A + order::kOrderNT - 1) / order::kOrderNT : 0;
+    fin = fin < 1024 ? fin : 1024;
+    hipLaunchKernelGGL(place_finish_order, dim3(unsigned(fin + D)), dim3(order::kOrderNT), 0, stream, a, o,
+                       int32_t(fin));
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

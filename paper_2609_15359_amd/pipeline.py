@@ -9,7 +9,7 @@ from dataclasses import dataclass
 import numpy as np
 import torch
 
-from . import (POLICY_MQ, Placement, Snapshot, calibrate, local_order, new_error_word, place,
+from . import (POLICY_MQ, Placement, Snapshot, calibrate, local_order, new_error_word, place, place_order,
                place_workspace_bytes, project)
 
 
@@ -105,13 +105,16 @@ class Workspaces:
 
 
 PHASES = ("calibrate", "project", "place", "local_order")
+# with placement and local order in one call (maps_place_order)
+PHASES_FUSED = ("calibrate", "project", "place+local_order")
 
 
 def step_phases(db: DeviceBatch, ws: Workspaces, want_pairs: bool = True, capacity=None,
-                policy: int = POLICY_MQ, rr_offset: int = 0):
-    """The step as one callable per phase (PHASES order).  Each enqueues its
-    library calls on the current stream and writes only into `ws`, so a phase
-    can also be captured into a graph and replayed."""
+                policy: int = POLICY_MQ, rr_offset: int = 0, fused: bool = False):
+    """The step as one callable per phase (PHASES order, or PHASES_FUSED with
+    `fused`).  Each enqueues its library calls on the current stream and
+    writes only into `ws`, so a phase can also be captured into a graph and
+    replayed."""
     cap = db.capacity if capacity is None else capacity
     err = ws.dev_err
     nr, na = db.n_res, db.n_arr
@@ -134,7 +137,12 @@ def step_phases(db: DeviceBatch, ws: Workspaces, want_pairs: bool = True, capaci
         local_order(snap, cap, db.q_off, db.q_prompt, U[nr + na:], db.q_wait_ms, db.max_wait_ms, dev_err=err,
                     order=ws.order, admitted=ws.admitted)
 
-    return [cal, proj, pla, loc]
+    def pla_loc():
+        place_order(snap, cap, db.queue_len, db.arr_prompt, U[nr:nr + na], db.q_off, db.q_prompt, U[nr + na:],
+                    db.q_wait_ms, db.max_wait_ms, policy=policy, rr_offset=rr_offset, want_pairs=want_pairs,
+                    workspace=ws.place, out=ws.placement, order=ws.order, admitted=ws.admitted)
+
+    return [cal, proj, pla_loc] if fused else [cal, proj, pla, loc]
 
 
 def outputs(db: DeviceBatch, ws: Workspaces) -> StepOutputs:
@@ -146,10 +154,10 @@ def outputs(db: DeviceBatch, ws: Workspaces) -> StepOutputs:
 
 
 def step(db: DeviceBatch, ws: Workspaces | None = None, want_pairs: bool = True, capacity=None,
-         policy: int = POLICY_MQ, rr_offset: int = 0) -> StepOutputs:
+         policy: int = POLICY_MQ, rr_offset: int = 0, fused: bool = False) -> StepOutputs:
     """Enqueue the whole hot path for one batch on the current stream."""
     ws = ws or Workspaces(db, want_pairs)
-    for fn in step_phases(db, ws, want_pairs, capacity, policy, rr_offset):
+    for fn in step_phases(db, ws, want_pairs, capacity, policy, rr_offset, fused):
         fn()
     return outputs(db, ws)
 
@@ -161,6 +169,7 @@ class StepGraphs:
 
     def __init__(self, db: DeviceBatch, ws: Workspaces, **kw):
         phases = step_phases(db, ws, **kw)
+        self.n_phases = len(phases)
         for fn in phases:
             fn()
         torch.cuda.synchronize()
@@ -173,7 +182,7 @@ class StepGraphs:
         torch.cuda.synchronize()
 
     def replay(self, events=None):
-        """One step; with events (len(PHASES) + 1 of them, None where no
+        """One step; with events (one per phase plus one, None where no
         event is wanted), the phase boundaries are recorded on the current
         stream."""
         for i, g in enumerate(self.graphs):

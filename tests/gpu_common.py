@@ -18,14 +18,16 @@ def say(*a):
     sys.stdout.flush()
 
 
-def gpu_step(b: Batch, capacity=None, want_pairs=True, policy=0, rr_offset=0):
+def gpu_step(b: Batch, capacity=None, want_pairs=True, policy=0, rr_offset=0, fused=False):
+    """The whole step on the GPU; `fused` makes placement and local order one
+    call (maps_place_order), as the benchmark does."""
     import torch
 
     import paper_2609_15359_amd as maps
     from paper_2609_15359_amd import pipeline
     db = pipeline.to_device(b)
     cap = None if capacity is None else torch.from_numpy(np.ascontiguousarray(capacity, np.int32)).cuda()
-    out = pipeline.step(db, want_pairs=want_pairs, capacity=cap, policy=policy, rr_offset=rr_offset)
+    out = pipeline.step(db, want_pairs=want_pairs, capacity=cap, policy=policy, rr_offset=rr_offset, fused=fused)
     torch.cuda.synchronize()
     bits = int(out.dev_err.item()) & 0xFFFFFFFF
     pl = out.placement

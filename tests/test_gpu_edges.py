@@ -139,9 +139,10 @@ def test_ragged_shapes(orc, D, nmax, A, qmax, policy):
     cap = (o0["base_peak"] + rng.integers(0, 20000, size=D)).astype(np.int32)
     for capacity in (None, cap):
         o = oracle_step(b, capacity=capacity, policy=policy, rr_offset=2**40 + 3, o=orc)
-        gg = gpu_step(b, capacity=capacity, policy=policy, rr_offset=2**40 + 3)
-        assert gg["err"] == 0, gg["errors"]
-        compare_all(gg, o)
+        for fused in (False, True):
+            gg = gpu_step(b, capacity=capacity, policy=policy, rr_offset=2**40 + 3, fused=fused)
+            assert gg["err"] == 0, gg["errors"]
+            compare_all(gg, o)
 
 
 @pytest.mark.parametrize("want_pairs", [False, True])
@@ -435,3 +436,25 @@ def test_empty_arrival_batch():
     pl = maps.place(snap, _cuda([100]), _cuda([0]), _cuda([]), _cuda([]))
     torch.cuda.synchronize()
     assert pl.choice.numel() == 0 and int(pl.dev_err.item()) == 0
+
+
+def test_empty_arrival_batch_with_queues(orc):
+    """maps_place_order with no arrivals still orders and admits every local
+    queue (one empty)."""
+    import torch
+
+    import paper_2609_15359_amd as maps
+    seg, p, g, U = [0, 2, 2, 3], [10, 20, 30], [0, 0, 5], [5, 6, 40]
+    snap, _, _ = _project(seg, p, g, U, 100)
+    qoff = np.array([0, 3, 3, 5], np.int64)
+    qp = np.array([7, 3, 9, 1, 2], np.int32)
+    qU = np.array([50, -1, 4, 9, 9], np.int32)
+    cap = np.array([120, 50, 100], np.int32)
+    pl, order, admitted = maps.place_order(snap, _cuda(cap), _cuda([0, 0, 0]), _cuda([]), _cuda([]),
+                                           _cuda(qoff, np.int64), _cuda(qp), _cuda(qU))
+    torch.cuda.synchronize()
+    assert pl.choice.numel() == 0 and int(pl.dev_err.item()) == 0
+    want_order, want_adm = orc.local_order(np.array(seg, np.int64), np.array(p, np.int32), np.array(g, np.int32),
+                                           np.array(U, np.int32), cap, qoff, qp, qU, None, 2**31 - 1, 100)
+    assert_same("order", order.cpu().numpy(), want_order)
+    assert_same("admitted", admitted.cpu().numpy(), want_adm)

@@ -17,20 +17,21 @@ def _snapshot_all(db, ws):
             "flags": pl.flags, "pair_peak": pl.pair_peak, "order": ws.order, "admitted": ws.admitted}
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", ["small", "medium"])
-def test_graph_replays_match_eager(name):
+def test_graph_replays_match_eager(name, fused):
     import torch
 
     from paper_2609_15359_amd import pipeline
     b = workload.make(name)
     db = pipeline.to_device(b)
     ws = pipeline.Workspaces(db, want_pairs=True)
-    pipeline.step(db, ws)
+    pipeline.step(db, ws, fused=fused)
     torch.cuda.synchronize()
     want = {k: v.cpu().numpy().copy() for k, v in _snapshot_all(db, ws).items()}
     assert int(ws.dev_err.item()) == 0
 
-    graphs = pipeline.StepGraphs(db, ws)
+    graphs = pipeline.StepGraphs(db, ws, fused=fused)
     other = pipeline.Workspaces(db, want_pairs=True)   # eager work between replays
     for r in range(3):
         for t in _snapshot_all(db, ws).values():

@@ -23,7 +23,7 @@ def test_workload_bit_exact(orc, name, alpha):
     b = workload.make(name, alpha_ppm=alpha)
     say(f"[parity] {name} alpha_ppm={b.alpha_ppm} D={b.decoders} A={b.arrivals}")
     o = oracle_step(b, o=orc)
-    g = gpu_step(b)
+    g = gpu_step(b, fused=True)   # the benchmark's launch configuration
     assert g["err"] == 0, g["errors"]
     compare_all(g, o)
     # the literal workloads overload the decoders; the fit variant below takes both branches
