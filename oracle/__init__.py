@@ -60,6 +60,10 @@ def _declare(lib):
     lib.oracle_apply_bounds.argtypes = [_i32p, c.c_int64, _i32p, c.c_int32, _i32p, c.c_int32,
                                         _i32p]
     lib.oracle_apply_bounds.restype = None
+    lib.oracle_calibrate_window.argtypes = [_i32p, _i32p, c.c_int64, _i32p, c.c_int32, c.c_int32,
+                                            c.c_int32, _i32p, _i64p, c.c_int64, c.c_int32, _i32p,
+                                            _i32p]
+    lib.oracle_calibrate_window.restype = c.c_int
     lib.oracle_occupancy.argtypes = [_i32p, _i32p, _i32p, c.c_int64, c.c_int64, _i64p]
     lib.oracle_occupancy.restype = c.c_int
     lib.oracle_project.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i64p]
@@ -124,6 +128,23 @@ class Oracle:
         if rc:
             raise ValueError(f"oracle_calibrate failed ({rc})")
         return q, cnt
+
+    def calibrate_window(self, pred, truth, edges, window: int, alpha_ppm: int, apply_pred, seen,
+                         u_max: int):
+        """Sliding-window calibration (Sec. 3.2, Sec. 4): each request's own set
+        is the `window` most recent completions of its bucket among the first
+        seen[j] log entries.  Returns (q, U) per request."""
+        pred, truth = _i32(pred), _i32(truth)
+        apply_pred, seen = _i32(apply_pred), _i64(seen)
+        e = _i32(edges) if len(edges) else np.zeros(1, np.int32)
+        q = np.zeros(apply_pred.size, np.int32)
+        U = np.zeros(apply_pred.size, np.int32)
+        rc = self.lib.oracle_calibrate_window(pred, truth, pred.size, e, len(edges) + 1, int(window),
+                                              int(alpha_ppm), apply_pred, seen, apply_pred.size,
+                                              int(u_max), q, U)
+        if rc:
+            raise ValueError(f"oracle_calibrate_window failed ({rc})")
+        return q, U
 
     def apply_bounds(self, pred, edges, q, u_max: int):
         pred = _i32(pred)

@@ -8,7 +8,9 @@
  *
  *   calibration  Sec. 3.2, Eqs. (2)-(4): one-sided nonconformity score, the
  *                conformal rank ceil((1-alpha)(n+1)), the calibrated bound;
- *                applied per length bucket of the prediction.
+ *                applied per length bucket of the prediction, on a fixed
+ *                calibration set or on each request's sliding window of the
+ *                most recent completions (Sec. 3.2, Sec. 4).
  *   occupancy    Sec. 3.3 and App. A, Eqs. (8) and (10): the KV footprint of a
  *                request grows one token per decoding step ("token by token",
  *                Sec. 3.3) until its bound runs out.
@@ -113,6 +115,71 @@ void oracle_apply_bounds(const int32_t* pred, int64_t m, const int32_t* edges, i
         if (qb == ORACLE_Q_INF) U_out[i] = u_max;
         else U_out[i] = (int32_t)min64((int64_t)pred[i] + qb, u_max);
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sliding-window calibration (Sec. 3.2: the calibration set holds the most  */
+/* recent completed requests; Sec. 4: a window of the 500 most recent)       */
+/* ------------------------------------------------------------------------ */
+
+/* Bounds for m requests, each calibrated on its own set: the `window` most
+ * recent completions of the request's bucket among the first seen[j] entries
+ * of the completion log (oldest first), or all of them when the bucket has
+ * fewer.  Eqs. (2)-(3) on that set give q_out[j]: the k-th smallest score,
+ * k = ceil((1-alpha)(n_w+1)) for a set of n_w scores, ORACLE_Q_INF when k
+ * exceeds n_w (an empty set included); a request without a prediction gets
+ * q_out = -1 and U_out = -1.  U_out follows Eq. (4) as in oracle_apply_bounds.
+ * Returns -1 on bad arguments, -2 when out of memory, -3 when a seen count
+ * lies outside [0, n], -4 for a negative length in the log. */
+int oracle_calibrate_window(const int32_t* pred, const int32_t* truth, int64_t n,
+                            const int32_t* edges, int32_t nb, int32_t window, int32_t alpha_ppm,
+                            const int32_t* apply_pred, const int64_t* seen, int64_t m,
+                            int32_t u_max, int32_t* q_out, int32_t* U_out)
+{
+    if (nb < 1 || window < 1 || alpha_ppm <= 0 || alpha_ppm >= 1000000 || n < 0 || m < 0) return -1;
+    for (int64_t i = 0; i < n; ++i)
+        if (pred[i] < 0 || truth[i] < 0) return -4;
+    /* where each bucket's completions sit in the log, in log order */
+    int64_t* count = (int64_t*)calloc((size_t)nb, sizeof(int64_t));
+    int64_t* start = (int64_t*)calloc((size_t)nb + 1, sizeof(int64_t));
+    int64_t* fill = (int64_t*)calloc((size_t)nb, sizeof(int64_t));
+    int64_t* pos = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    int64_t* set = (int64_t*)malloc((size_t)window * sizeof(int64_t));
+    if (!count || !start || !fill || !pos || !set) return -2;
+    for (int64_t i = 0; i < n; ++i) count[oracle_bucket(pred[i], edges, nb)] += 1;
+    for (int32_t b = 0; b < nb; ++b) start[b + 1] = start[b] + count[b];
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t b = oracle_bucket(pred[i], edges, nb);
+        pos[start[b] + fill[b]] = i;
+        fill[b] += 1;
+    }
+    int rc = 0;
+    for (int64_t j = 0; j < m; ++j) {
+        if (apply_pred[j] < 0) { q_out[j] = -1; U_out[j] = -1; continue; }
+        if (seen[j] < 0 || seen[j] > n) { rc = -3; break; }
+        int32_t b = oracle_bucket(apply_pred[j], edges, nb);
+        /* c = completions of bucket b logged before entry seen[j] */
+        int64_t lo = 0, hi = count[b];
+        while (lo < hi) {
+            int64_t mid = lo + (hi - lo) / 2;
+            if (pos[start[b] + mid] < seen[j]) lo = mid + 1; else hi = mid;
+        }
+        int64_t c = lo;
+        int64_t nw = min64(c, window);
+        /* the set: the last nw of them; Eq. (2) scores */
+        for (int64_t t = 0; t < nw; ++t) {
+            int64_t i = pos[start[b] + c - nw + t];
+            set[t] = max64(0, (int64_t)truth[i] - (int64_t)pred[i]);
+        }
+        qsort(set, (size_t)nw, sizeof(int64_t), cmp_i64);
+        int64_t k = oracle_conformal_rank(nw, alpha_ppm);
+        int32_t q = (k <= nw) ? (int32_t)set[k - 1] : ORACLE_Q_INF;
+        q_out[j] = q;
+        if (q == ORACLE_Q_INF) U_out[j] = u_max;
+        else U_out[j] = (int32_t)min64((int64_t)apply_pred[j] + q, u_max);
+    }
+    free(count); free(start); free(fill); free(pos); free(set);
+    return rc;
 }
 
 /* ------------------------------------------------------------------------ */

@@ -182,6 +182,116 @@ def pin_coverage(o):
 
 
 # ---------------------------------------------------------------------------
+# sliding-window calibration (Sec. 3.2; Sec. 4: the 500 most recent requests)
+# ---------------------------------------------------------------------------
+
+def py_window_quantile(pred, truth, edges, window, alpha_ppm, p, seen):
+    """Brute force: walk the log back from entry seen-1, keep the scores of the
+    request's bucket until `window` are found, take the k-th smallest."""
+    if p < 0:
+        return -1
+    b = sum(1 for e in edges if e <= p)
+    got = []
+    i = seen - 1
+    while i >= 0 and len(got) < window:
+        if sum(1 for e in edges if e <= pred[i]) == b:
+            got.append(max(0, int(truth[i]) - int(pred[i])))
+        i -= 1
+    k = math.ceil((1 - Fraction(alpha_ppm, 10**6)) * (len(got) + 1))
+    return sorted(got)[k - 1] if k <= len(got) else Q_INF
+
+
+def pin_window_golden(o):
+    gd = golden("calibrate_window_hand.json")
+    r = gd["requests"]
+    for case in gd["cases"]:
+        q, U = o.calibrate_window(gd["pred"], gd["truth"], gd["edges"], case["window"], case["alpha_ppm"],
+                                  r["pred"], r["seen"], gd["u_max"])
+        assert q.tolist() == [Q_INF if v == "inf" else v for v in case["q"]], (case, q)
+        assert U.tolist() == case["U"], (case, U)
+
+
+def pin_window_bruteforce(o):
+    rng = _rng(31)
+    for trial in range(40):
+        n = int(rng.integers(0, 45))
+        pred = rng.integers(0, 50, size=n).astype(np.int32)
+        truth = rng.integers(0, 80, size=n).astype(np.int32)
+        nb = int(rng.integers(1, 4))
+        edges = np.sort(rng.integers(0, 50, size=nb - 1)).astype(np.int32)
+        window = int(rng.choice([1, 2, 5, 9, 60]))
+        alpha = int(rng.choice([50000, 100000, 250000, 500000, 900000]))
+        m = 60
+        ap = rng.integers(-2, 60, size=m).astype(np.int32)
+        seen = rng.integers(0, n + 1, size=m).astype(np.int64)
+        u_max = 70
+        q, U = o.calibrate_window(pred, truth, edges, window, alpha, ap, seen, u_max)
+        for j in range(m):
+            want = py_window_quantile(pred, truth, edges, window, alpha, int(ap[j]), int(seen[j]))
+            assert q[j] == want, (trial, j, q[j], want)
+            if ap[j] < 0:
+                assert U[j] == -1
+            else:
+                assert U[j] == (u_max if want == Q_INF else min(int(ap[j]) + want, u_max)), (trial, j)
+
+
+def pin_window_closed_forms(o):
+    """One bucket.  Scores equal to the log position: the set of a request
+    that saw c completions is positions c-n_w .. c-1, so q = c - n_w + k - 1.
+    Scores n - i (falling): q = n - c + k."""
+    n, window, alpha = 300, 40, 100000
+    i = np.arange(n, dtype=np.int32)
+    pred = np.full(n, 10, np.int32)
+    seen = np.arange(n + 1, dtype=np.int64)
+    ap = np.full(n + 1, 10, np.int32)
+    for truth, form in ((pred + i, lambda c, nw, k: c - nw + k - 1), (pred + (n - i), lambda c, nw, k: n - c + k)):
+        q, _ = o.calibrate_window(pred, truth, [], window, alpha, ap, seen, 10**6)
+        for c in range(n + 1):
+            nw = min(c, window)
+            k = math.ceil((1 - Fraction(alpha, 10**6)) * (nw + 1))
+            assert q[c] == (form(c, nw, k) if k <= nw else Q_INF), (c, q[c])
+
+
+def pin_window_reduces_to_fixed_set(o):
+    """A window at least as long as the log, every request after the last
+    completion: the set is the whole bucket, the quantile of numpy's sort."""
+    b = workload.make("small")
+    n = b.cal_pred.size
+    ap = b.apply_pred()[:2000]
+    q, U = o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, n, b.alpha_ppm, ap,
+                              np.full(ap.size, n, np.int64), b.u_max)
+    s = np.maximum(0, b.cal_truth.astype(np.int64) - b.cal_pred)
+    bk = np.searchsorted(b.edges, b.cal_pred, side="right")
+    qb = []
+    for j in range(b.edges.size + 1):
+        sj = np.sort(s[bk == j])
+        k = math.ceil((1 - Fraction(b.alpha_ppm, 10**6)) * (sj.size + 1))
+        qb.append(int(sj[k - 1]) if k <= sj.size else Q_INF)
+    want = np.where(ap < 0, -1, np.array(qb)[np.searchsorted(b.edges, np.maximum(ap, 0), side="right")])
+    assert np.array_equal(q, want)
+    assert np.array_equal(U, o.apply_bounds(ap, b.edges, np.array(qb, np.int32), b.u_max))
+
+
+def pin_window_coverage(o):
+    """Eq. (5) online: each completion, bounded from the window of the ones
+    before it (500 most recent, Sec. 4), is covered with probability at least
+    1 - alpha; a smaller alpha never gives a smaller bound."""
+    for name, alpha in (("small", 100000), ("small", 50000)):
+        b = workload.make(name)
+        n = b.cal_pred.size
+        seen = np.arange(n, dtype=np.int64)
+        q, U = o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, 500, alpha, b.cal_pred, seen, b.u_max)
+        warm = np.arange(n) >= min(n // 2, 2 * 500 * (b.edges.size + 1))   # windows mostly full
+        a = alpha / 1e6
+        cov = float(np.mean(b.cal_truth[warm] <= U[warm]))
+        m = int(warm.sum())
+        assert cov >= 1 - a - 3 * math.sqrt(a * (1 - a) / m), (name, cov)
+        assert cov <= 1 - a + 0.03, (name, cov)
+        q2, U2 = o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, 500, 2 * alpha, b.cal_pred, seen, b.u_max)
+        assert np.all(q.astype(np.int64) >= q2) and np.all(U >= U2)
+
+
+# ---------------------------------------------------------------------------
 # occupancy and placement (Sec. 3.3, App. A, Algorithm 1)
 # ---------------------------------------------------------------------------
 
@@ -405,6 +515,8 @@ def pin_local_order_bruteforce(o):
 ALL_PINS = [
     pin_calibrate_golden, pin_rank_is_ceiling, pin_quantile_order_statistic,
     pin_quantile_special_cases, pin_quantile_monotone_in_alpha, pin_coverage,
+    pin_window_golden, pin_window_bruteforce, pin_window_closed_forms, pin_window_reduces_to_fixed_set,
+    pin_window_coverage,
     pin_place_golden, pin_occupancy_bruteforce, pin_place_bruteforce, pin_place_closed_forms,
     pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
     pin_local_order_golden, pin_local_order_bruteforce,

@@ -50,6 +50,16 @@ MUTANTS = [
      "if (x->val != y->val) return x->val > y->val ? -1 : 1;"),
     ("admission_no_growth", "G[t] += (int64_t)q_p[qlo + i] + t;", "G[t] += (int64_t)q_p[qlo + i];"),
     ("admission_strict", "if (peak > capacity[d]) break;", "if (peak >= capacity[d]) break;"),
+    ("window_includes_seen", "if (pos[start[b] + mid] < seen[j]) lo = mid + 1;",
+     "if (pos[start[b] + mid] <= seen[j]) lo = mid + 1;"),
+    ("window_oldest_not_newest", "int64_t i = pos[start[b] + c - nw + t];", "int64_t i = pos[start[b] + t];"),
+    ("window_rank_from_length", "int64_t k = oracle_conformal_rank(nw, alpha_ppm);",
+     "int64_t k = oracle_conformal_rank(window, alpha_ppm);"),
+    ("window_ignores_bucket", "int32_t b = oracle_bucket(apply_pred[j], edges, nb);", "int32_t b = 0;"),
+    ("window_two_sided_score", "set[t] = max64(0, (int64_t)truth[i] - (int64_t)pred[i]);",
+     "set[t] = (int64_t)truth[i] - (int64_t)pred[i];"),
+    ("window_one_short", "int64_t nw = min64(c, window);", "int64_t nw = min64(c, window - 1);"),
+    ("window_inf_gives_pred", "if (q == ORACLE_Q_INF) U_out[j] = u_max;", "if (q == ORACLE_Q_INF) U_out[j] = apply_pred[j];"),
     ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
      "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
 ]
@@ -84,6 +94,7 @@ def test_mutant_fails_a_pin(tmpdir_mutants, name, old, new):
             pin(o)
         except (AssertionError, ValueError, IndexError):
             failed.append(pin.__name__)
+            break   # one failing pin is enough
     assert failed, f"planted mistake {name} passed every pin"
 
 

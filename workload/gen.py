@@ -147,6 +147,20 @@ def make(name_or_workload, alpha_ppm: int | None = None, seed: int | None = None
                  q_off=q_off, q_prompt=q_prompt, q_pred=q_pred, q_wait_ms=q_wait)
 
 
+def window_seen(batch: Batch, seed: int | None = None) -> np.ndarray:
+    """For sliding-window calibration: how many entries of the completion log
+    (the calibration pairs, oldest first) each bounded request had seen when
+    its bound was taken, in :meth:`Batch.apply_pred` order.  Residents were
+    bounded at earlier times, uniform over the log; arrivals and queued
+    requests see all of it.  int64."""
+    seed = batch.workload.seed if seed is None else seed
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed, spawn_key=(5,))))
+    n = batch.cal_pred.size
+    res = rng.integers(0, n + 1, size=batch.res_pred.size, dtype=np.int64)
+    rest = np.full(batch.arr_pred.size + batch.q_pred.size, n, dtype=np.int64)
+    return np.concatenate([res, rest])
+
+
 def manifest(batch: Batch) -> dict:
     """SHA-256 of every input array (bytes in native little-endian order)."""
     return {k: hashlib.sha256(np.ascontiguousarray(v).tobytes()).hexdigest()
