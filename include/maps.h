@@ -68,9 +68,11 @@ enum {
     MAPS_ERR_SNAPSHOT = 32u,        /* snapshot was not built for this (D, u_max) */
     MAPS_ERR_QUEUE_TOO_LONG = 64u,  /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
     MAPS_ERR_TOO_MANY = 128u,       /* a decoder with MAPS_MAX_RESIDENTS or more residents */
-    MAPS_ERR_WAIT_TIMEOUT = 256u    /* a workgroup's bounded wait for the other workgroups
+    MAPS_ERR_WAIT_TIMEOUT = 256u,   /* a workgroup's bounded wait for the other workgroups
                                        of its launch ran out (the device did not hold
                                        every workgroup of the launch at once) */
+    MAPS_ERR_SEEN_RANGE = 512u      /* a seen count outside [0, n] (sliding-window
+                                       calibration) */
 };
 
 /* Largest u_max (cap on bounds and remaining lengths) the snapshot accepts,
@@ -80,6 +82,11 @@ enum {
 
 /* Longest pending queue of one decoder that maps_local_order accepts. */
 #define MAPS_MAX_LOCAL_QUEUE 2048
+
+/* Longest calibration window and most length buckets that
+ * maps_calibrate_window accepts. */
+#define MAPS_MAX_WINDOW 4096
+#define MAPS_MAX_WINDOW_BUCKETS 4096
 
 /* Placement policies: minimum queue among feasible decoders with the largest
  * slack as fallback (Sec. 3.3 and Algorithm 1), or largest slack alone (the
@@ -113,6 +120,41 @@ maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
                            const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
                            uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 1b. Sliding-window calibration (Sec. 3.2: the calibration set holds the  */
+/*     most recent completed requests; Sec. 4: a window of the last 500)    */
+/* ------------------------------------------------------------------------ */
+/*
+ * Completion log of n requests, oldest first: pred[i], truth[i] >= 0, bucket
+ * b(i) = #{j : edges[j] <= pred[i]} as for maps_calibrate (edges[0..nb-2]
+ * non-decreasing).  Request j (0 <= j < m) with prediction apply_pred[j] had
+ * seen the first apply_seen[j] log entries (0 <= apply_seen[j] <= n) when its
+ * bound was taken.  Its calibration set is the `window` most recent of those
+ * entries in its bucket (all of them when the bucket had fewer): n_w scores
+ * s = max(0, truth - pred) (Eq. (2)), k = ceil((1 - alpha)(n_w + 1)), and
+ *   q_out[j] = the k-th smallest of them (Eq. (3)), MAPS_Q_INF when k > n_w
+ *              (an empty set included), -1 when apply_pred[j] < 0;
+ *   U_out[j] = -1 when apply_pred[j] < 0, u_max when q is MAPS_Q_INF, else
+ *              min(apply_pred[j] + q, u_max) (Eq. (4)).
+ * With window >= n and every apply_seen[j] = n this is maps_calibrate's
+ * bound.  All arrays are device arrays; q_out may be NULL; apply_seen is
+ * int64.  m may be 0 (nothing is enqueued).
+ * dev_err bits: NEG_LEN (pred or truth < 0 in the log), EDGES_UNSORTED,
+ * SEEN_RANGE.  Outputs are unspecified when *dev_err != 0 (the kernels stay
+ * inside their buffers).
+ * Host errors: NULL, SIZE (n < 0 or n > INT32_MAX, m < 0, nb < 1 or nb >
+ * MAPS_MAX_WINDOW_BUCKETS, window < 1 or window > MAPS_MAX_WINDOW,
+ * u_max < 0), ALPHA, WORKSPACE (smaller than
+ * maps_calibrate_window_workspace_size(n, nb)), HIP.
+ */
+size_t maps_calibrate_window_workspace_size(int64_t n, int32_t nb);
+maps_status maps_calibrate_window(const int32_t* pred, const int32_t* truth, int64_t n,
+                                  const int32_t* edges, int32_t nb, int32_t window, int32_t alpha_ppm,
+                                  const int32_t* apply_pred, const int64_t* apply_seen, int64_t m,
+                                  int32_t u_max, int32_t* q_out, int32_t* U_out,
+                                  uint32_t* dev_err, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 2. Projection of KV occupancy per decoder (Sec. 3.3; App. A, Eq. (8))    */

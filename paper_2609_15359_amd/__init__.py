@@ -28,7 +28,10 @@ MAX_LOCAL_QUEUE = 2048
 ERR_BITS = {
     1: "NEG_LEN", 2: "EDGES_UNSORTED", 4: "INT32_RANGE", 8: "SEG_OFFSETS",
     16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG", 128: "TOO_MANY", 256: "WAIT_TIMEOUT",
+    512: "SEEN_RANGE",
 }
+MAX_WINDOW = 4096
+MAX_WINDOW_BUCKETS = 4096
 MAX_U_MAX = (1 << 24) - 64
 
 
@@ -42,6 +45,9 @@ _SIGNATURES = {
     "maps_calibrate_workspace_size": (_sz, [_i64, _i32]),
     "maps_calibrate": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp,
                               _vp, _vp, _sz, _vp]),
+    "maps_calibrate_window_workspace_size": (_sz, [_i64, _i32]),
+    "maps_calibrate_window": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp,
+                                     _vp, _vp, _sz, _vp]),
     "maps_snapshot_bytes": (_sz, [_i32, _i64, _i32]),
     "maps_project_workspace_size": (_sz, [_i32, _i64, _i32]),
     "maps_project": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp, _vp, _sz, _vp]),
@@ -161,6 +167,38 @@ def calibrate(pred, truth, edges, alpha_ppm: int, apply_pred=None, u_max: int = 
                             int(u_max), _ptr(U), _ptr(err), _ptr(ws), ws.numel(), _stream(dev))
     _check(st, "maps_calibrate")
     return q, cnt, U, err
+
+
+def calibrate_window_workspace_bytes(n: int, nb: int) -> int:
+    return int(library().maps_calibrate_window_workspace_size(int(n), int(nb)))
+
+
+def calibrate_window(pred, truth, edges, window: int, alpha_ppm: int, apply_pred, apply_seen, u_max: int,
+                     dev_err=None, workspace=None, q=None, U=None, want_q: bool = True):
+    """Sliding-window calibration: each request's bound from the `window` most
+    recent completions of its bucket among the first apply_seen[j] entries of
+    the completion log (pred, truth).  Returns (q or None, U, dev_err)."""
+    pred = _dev(pred, torch.int32, "pred")
+    dev = pred.device
+    truth = _dev(truth, torch.int32, "truth")
+    edges = _dev(edges, torch.int32, "edges")
+    apply_pred = _dev(apply_pred, torch.int32, "apply_pred")
+    apply_seen = _dev(apply_seen, torch.int64, "apply_seen")
+    nb, n, m = edges.numel() + 1, pred.numel(), apply_pred.numel()
+    if truth.numel() != n or apply_seen.numel() != m:
+        raise MapsError("pred/truth or apply_pred/apply_seen differ in length")
+    if want_q and q is None:
+        q = torch.empty(m, dtype=torch.int32, device=dev)
+    U = torch.empty(m, dtype=torch.int32, device=dev) if U is None else U
+    err = new_error_word(dev) if dev_err is None else dev_err
+    lib = library()
+    ws = _workspace(lib.maps_calibrate_window_workspace_size(n, nb), dev, workspace)
+    st = lib.maps_calibrate_window(_ptr(pred), _ptr(truth), n, _ptr(edges) if nb > 1 else None, nb, int(window),
+                                   int(alpha_ppm), _ptr(apply_pred), _ptr(apply_seen), m, int(u_max),
+                                   _ptr(q) if want_q else None, _ptr(U), _ptr(err), _ptr(ws), ws.numel(),
+                                   _stream(dev))
+    _check(st, "maps_calibrate_window")
+    return (q if want_q else None), U, err
 
 
 # ---------------------------------------------------------------------------

@@ -104,6 +104,27 @@ def test_host_argument_errors_without_gpu(lib):
     # local order: D < 1, NULL queue offsets
     assert lib.maps_local_order(fake, 0, 10, fake, fake, 0, fake, fake, None, 0, fake, fake, fake, None, 0, None) == -2
     assert lib.maps_local_order(fake, 2, 10, fake, None, 0, fake, fake, None, 0, fake, fake, fake, None, 0, None) == -1
+    # placement with local order: either argument set refused, nothing enqueued
+    po = [fake, 4, 8192, fake, fake, fake, fake, 10]
+    tail = [fake, 5, fake, fake, fake, 1000, fake, fake, fake, fake, 1 << 20, None]
+    assert lib.maps_place_order(*po, 7, 0, fake, fake, fake, fake, None, *tail) == -6
+    assert lib.maps_place_order(*po, 0, 0, fake, fake, fake, fake, None, None, *tail[1:]) == -1
+    assert lib.maps_place_order(*po, 0, 0, fake, fake, fake, fake, None, fake, -1, *tail[2:]) == -2
+    # sliding-window calibration: window and bucket limits, alpha, NULL, short workspace
+    wa = lambda n, nb, w, a, ws: lib.maps_calibrate_window(fake, fake, n, fake, nb, w, a, fake, fake, 10, 100,
+                                                         None, fake, fake, fake, ws, None)
+    assert wa(100, 4, 0, 100000, 1 << 24) == -2
+    assert wa(100, 4, maps.MAX_WINDOW + 1, 100000, 1 << 24) == -2
+    assert wa(100, maps.MAX_WINDOW_BUCKETS + 1, 500, 100000, 1 << 24) == -2
+    assert wa(-1, 4, 500, 100000, 1 << 24) == -2
+    assert wa(2**31, 4, 500, 100000, 1 << 24) == -2
+    assert wa(100, 4, 500, 0, 1 << 24) == -3
+    assert wa(100, 4, 500, 100000, 16) == -4
+    assert lib.maps_calibrate_window(fake, fake, 100, fake, 4, 500, 100000, fake, None, 10, 100, None, fake, fake,
+                                     fake, 1 << 24, None) == -1
+    # the workspace holds the scores three times over (grouped, by bucket, and their
+    # log indices) plus a quantile per position of every bucket
+    assert lib.maps_calibrate_window_workspace_size(100000, 64) >= 100000 * 18
 
 
 def test_binding_refuses_host_tensors(lib):

@@ -1,0 +1,154 @@
+"""Sliding-window calibration on the GPU (maps_calibrate_window) against the
+CPU oracle, bit for bit: each request calibrated on the most recent
+completions of its bucket that it had seen (Sec. 3.2; Sec. 4 uses a window of
+the 500 most recent).  Ragged logs around the 4,096-entry chunks and the
+1,536-position select runs, windows from 1 to the maximum, empty logs and
+buckets, the seeded workloads (sampled requests at the two largest), and the
+device error bits."""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from tests.gpu_common import assert_same, say
+
+pytestmark = pytest.mark.gpu
+Q_INF = 2**31 - 1
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.Oracle()
+
+
+def _cuda(x, dtype=np.int32):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=dtype)).cuda()
+
+
+def _gpu(pred, truth, edges, window, alpha, ap, seen, u_max):
+    import torch
+
+    import paper_2609_15359_amd as maps
+    q, U, err = maps.calibrate_window(_cuda(pred), _cuda(truth), _cuda(edges), window, alpha, _cuda(ap),
+                                      _cuda(seen, np.int64), u_max)
+    torch.cuda.synchronize()
+    return q.cpu().numpy(), U.cpu().numpy(), int(err.item()) & 0xFFFFFFFF
+
+
+def test_hand_worked_example():
+    from tests.oracle_pins import golden
+    gd = golden("calibrate_window_hand.json")
+    r = gd["requests"]
+    for case in gd["cases"]:
+        q, U, err = _gpu(gd["pred"], gd["truth"], gd["edges"], case["window"], case["alpha_ppm"], r["pred"],
+                         r["seen"], gd["u_max"])
+        assert err == 0
+        assert q.tolist() == [Q_INF if v == "inf" else v for v in case["q"]], case
+        assert U.tolist() == case["U"], case
+
+
+# (n, nb, window): chunk and run boundaries, single entries, one bucket, windows 1 .. max
+RAGGED = [(0, 3, 500), (1, 1, 1), (5, 2, 3), (4095, 7, 500), (4096, 7, 500), (4097, 40, 1600), (9000, 2, 1),
+          (20000, 7, 4096), (30001, 64, 500), (70000, 5, 2000)]
+
+
+@pytest.mark.parametrize("n,nb,window", RAGGED, ids=[f"n{r[0]}-nb{r[1]}-w{r[2]}" for r in RAGGED])
+def test_ragged_logs(orc, n, nb, window):
+    rng = np.random.default_rng(7 * n + nb + window)
+    pred = rng.integers(0, 3000, size=n).astype(np.int32)
+    truth = (pred + rng.integers(-800, 2500, size=n)).clip(0).astype(np.int32)
+    edges = np.sort(rng.integers(0, 3000, size=nb - 1)).astype(np.int32)
+    if nb > 3:
+        edges[1] = edges[2]          # a duplicated edge: an empty bucket
+    m = 20000
+    ap = rng.integers(-3, 3500, size=m).astype(np.int32)
+    seen = rng.integers(0, n + 1, size=m).astype(np.int64)
+    seen[:50] = n
+    seen[50:100] = 0
+    for alpha in (100000, 50000):
+        say(f"[window] n={n} nb={nb} W={window} alpha={alpha}")
+        qo, Uo = orc.calibrate_window(pred, truth, edges, window, alpha, ap, seen, 4000)
+        q, U, err = _gpu(pred, truth, edges, window, alpha, ap, seen, 4000)
+        assert err == 0
+        assert_same("q", q, qo)
+        assert_same("U", U, Uo)
+
+
+def test_every_position_of_one_bucket(orc):
+    """One bucket, every seen count from 0 to n: all select runs and the
+    partial windows at the start of the log."""
+    rng = np.random.default_rng(3)
+    n = 5000
+    pred = rng.integers(0, 100, size=n).astype(np.int32)
+    truth = rng.integers(0, 100000, size=n).astype(np.int32)   # 17-bit scores
+    seen = np.arange(n + 1, dtype=np.int64)
+    ap = np.full(n + 1, 50, np.int32)
+    for window in (1, 2, 500, 1537):
+        qo, Uo = orc.calibrate_window(pred, truth, [], window, 100000, ap, seen, 2**30)
+        q, U, err = _gpu(pred, truth, [], window, 100000, ap, seen, 2**30)
+        assert err == 0
+        assert_same(f"q (window {window})", q, qo)
+        assert_same(f"U (window {window})", U, Uo)
+
+
+def test_fixed_set_special_case(orc):
+    """A window as long as the log and every request after the last
+    completion: the fixed-set bound of maps_calibrate."""
+    import paper_2609_15359_amd as maps
+    b = workload.make("small")
+    n = b.cal_pred.size
+    ap = b.apply_pred()
+    seen = np.full(ap.size, n, np.int64)
+    q, U, err = _gpu(b.cal_pred, b.cal_truth, b.edges, maps.MAX_WINDOW, b.alpha_ppm, ap, seen, b.u_max)
+    assert err == 0
+    # each bucket of small holds at most 4,096 completions, so the window covers it
+    assert np.bincount(np.searchsorted(b.edges, b.cal_pred, side="right")).max() <= maps.MAX_WINDOW
+    qb, _ = orc.calibrate(b.cal_pred, b.cal_truth, b.edges, b.alpha_ppm)
+    assert_same("U", U, orc.apply_bounds(ap, b.edges, qb, b.u_max))
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "medium", "large", "xlarge"])
+def test_workload_window_500(orc, name):
+    """The seeded workloads: every bounded request of the step (residents at
+    earlier points of the log, arrivals and queued requests after all of it),
+    window 500 as in Sec. 4.  Full comparison up to medium; at large and
+    xlarge the oracle computes 50,000 sampled requests one by one, and every
+    request's bound is checked against its quantile."""
+    b = workload.make(name)
+    ap = b.apply_pred()
+    seen = workload.window_seen(b)
+    say(f"[window] {name}: log {b.cal_pred.size}, {b.edges.size + 1} buckets, {ap.size} requests")
+    q, U, err = _gpu(b.cal_pred, b.cal_truth, b.edges, 500, b.alpha_ppm, ap, seen, b.u_max)
+    assert err == 0
+    if ap.size <= 200000:
+        idx = np.arange(ap.size)
+    else:
+        rng = np.random.default_rng(11)
+        idx = np.unique(np.concatenate([rng.choice(ap.size, 50000, replace=False), np.arange(200),
+                                        np.arange(ap.size - 200, ap.size)]))
+    qo, Uo = orc.calibrate_window(b.cal_pred, b.cal_truth, b.edges, 500, b.alpha_ppm, ap[idx], seen[idx], b.u_max)
+    assert_same("q", q[idx], qo)
+    assert_same("U", U[idx], Uo)
+    ok = ap >= 0
+    fin = ok & (q != Q_INF)
+    assert np.all(U[~ok] == -1) and np.all(q[~ok] == -1)
+    assert np.all(U[ok & (q == Q_INF)] == b.u_max)
+    assert np.array_equal(U[fin], np.minimum(ap[fin].astype(np.int64) + q[fin], b.u_max))
+
+
+def test_error_bits():
+    import paper_2609_15359_amd as maps
+    pred = np.array([5, 6, 7], np.int32)
+    truth = np.array([9, 9, 9], np.int32)
+    _, _, err = _gpu(pred, truth, [], 10, 100000, [1, 2], [0, 4], 100)
+    assert err & 512, maps.error_names(err)
+    _, _, err = _gpu(pred, truth, [], 10, 100000, [1, 2], [-1, 0], 100)
+    assert err & 512
+    _, _, err = _gpu(np.array([5, -6, 7], np.int32), truth, [], 10, 100000, [1], [3], 100)
+    assert err & 1
+    _, _, err = _gpu(pred, truth, [9, 3], 10, 100000, [1], [3], 100)
+    assert err & 2
+    # no prediction: no bucket, no seen check
+    q, U, err = _gpu(pred, truth, [], 10, 100000, [-1], [99], 100)
+    assert err == 0 and q.tolist() == [-1] and U.tolist() == [-1]
