@@ -88,6 +88,61 @@ def cpu_baseline(batch, budget_s: float = 20.0):
                       f"{dt * 1e3:.1f} ms per step"}
 
 
+WINDOW = 500   # Sec. 4: calibration over a sliding window of the 500 most recent requests
+
+
+def window_calibration(b, cpu: bool, calls: int = 20):
+    """Sliding-window calibration of every bounded request of the batch
+    (maps_calibrate_window, window 500): residents bounded at earlier points of
+    the completion log, arrivals and queued requests after all of it.  Timed
+    with fence-free HIP events around each call, inputs resident in HBM."""
+    import numpy as np
+    import torch
+
+    import workload
+    import paper_2609_15359_amd as maps
+    ap = b.apply_pred()
+    seen = workload.window_seen(b)
+    dev = lambda x, t=torch.int32: torch.from_numpy(np.ascontiguousarray(x)).to(t).cuda()  # noqa: E731
+    pred, truth, edges, apd, sn = dev(b.cal_pred), dev(b.cal_truth), dev(b.edges), dev(ap), dev(seen, torch.int64)
+    n, nb, m = pred.numel(), edges.numel() + 1, apd.numel()
+    ws = torch.empty(maps.calibrate_window_workspace_bytes(n, nb), dtype=torch.uint8, device="cuda")
+    U = torch.empty(m, dtype=torch.int32, device="cuda")
+    err = maps.new_error_word()
+
+    def call():
+        maps.calibrate_window(pred, truth, edges, WINDOW, b.alpha_ppm, apd, sn, b.u_max, dev_err=err,
+                              workspace=ws, U=U, want_q=False)
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    ev = [(TimingEvent(), TimingEvent()) for _ in range(calls)]
+    for e0, e1 in ev:
+        e0.record()
+        call()
+        e1.record()
+    torch.cuda.synchronize()
+    ms = statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
+    if int(err.item()) != 0:
+        raise SystemExit(f"window calibration raised {maps.error_names(int(err.item()))}")
+    nbytes = 8 * n + 16 * m   # log (pred, truth) in; per request pred and seen in, bound out
+    out = {"log": n, "buckets": nb, "window": WINDOW, "requests": m, "ms": ms, "requests_per_s": m / (ms * 1e-3),
+           "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes},
+           "note": "median of per-call HIP events over the five launches of one call"}
+    if cpu:
+        import oracle
+        o = oracle.Oracle()
+        idx = np.arange(0, m, max(1, m // 30000))
+        t0 = time.perf_counter()
+        o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, WINDOW, b.alpha_ppm, ap[idx], seen[idx], b.u_max)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": idx.size / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{idx.size} evenly spaced requests of the same batch, single-threaded C "
+                                         f"oracle (each request's window sorted), {dt:.2f} s"}
+    return out
+
+
 class TimingEvent:
     """A HIP event made only for timing: created with hipEventDisableSystemFence,
     so recording it costs no system-scope cache write-back and invalidation
@@ -144,6 +199,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, help="run only a plain copy of this many bytes")
+    ap.add_argument("--window-only", action="store_true", help="run only the sliding-window calibration leg "
+                                                               "(for profiling its kernels)")
     ap.add_argument("--graph", action="store_true", help="replay one HIP graph per phase instead of "
                                                          "launching every kernel from the host")
     args = ap.parse_args()
@@ -163,6 +220,9 @@ def main():
     from paper_2609_15359_amd import pipeline
 
     b = workload.make(args.workload)
+    if args.window_only:
+        print(json.dumps({"window_calibration": window_calibration(b, cpu=False)}), flush=True)
+        return
     D, A = b.decoders, b.arrivals
     db = pipeline.to_device(b)
     ws = pipeline.Workspaces(db, want_pairs=True)
@@ -266,6 +326,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(b)
+    # the next row on the path: sliding-window calibration of the same batch
+    result["window_calibration"] = window_calibration(b, cpu=not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)
 
 

@@ -86,7 +86,7 @@ enum {
 /* Longest calibration window and most length buckets that
  * maps_calibrate_window accepts. */
 #define MAPS_MAX_WINDOW 4096
-#define MAPS_MAX_WINDOW_BUCKETS 4096
+#define MAPS_MAX_WINDOW_BUCKETS 1024
 
 /* Placement policies: minimum queue among feasible decoders with the largest
  * slack as fallback (Sec. 3.3 and Algorithm 1), or largest slack alone (the

@@ -31,7 +31,7 @@ ERR_BITS = {
     512: "SEEN_RANGE",
 }
 MAX_WINDOW = 4096
-MAX_WINDOW_BUCKETS = 4096
+MAX_WINDOW_BUCKETS = 1024
 MAX_U_MAX = (1 << 24) - 64
 
 

@@ -7,10 +7,13 @@
 // them uses x_{max(0,c-W)} .. x_{c-1}; every position c = 0..n_b of every
 // bucket therefore has one quantile, and each request looks its own up.
 //
-//   win_chunk_sort  per chunk of 4,096 log entries: scores and buckets, a
-//                   bitonic sort in LDS by (bucket, log index), i.e. the
-//                   chunk grouped by bucket with log order inside each group,
-//                   and every group's size and start;
+//   win_chunk_sort  per chunk of 4,096 log entries: scores and buckets, the
+//                   chunk grouped by bucket with log order inside each group
+//                   (a stable counting sort: each wavefront ranks its 64
+//                   entries a round among equal buckets through ballots and
+//                   keeps running counts per bucket in LDS, then per bucket a
+//                   prefix over the wavefronts and over the buckets), and
+//                   every group's size and start;
 //   win_row_scan    per bucket: the prefix over chunks of its group sizes
 //                   (where each chunk's group starts in the bucket sequence);
 //   win_scatter     every score to its place in its bucket's sequence (the
@@ -35,12 +38,14 @@ namespace {
 constexpr int kChunk = 4096;                    // log entries per sort workgroup
 constexpr int kSortNT = 1024;
 constexpr int kSortPer = kChunk / kSortNT;
+constexpr int kSegs = kSortNT / kWave;          // one segment of kSortPer * 64 entries per wavefront
 constexpr int kBucketsMax = MAPS_MAX_WINDOW_BUCKETS;
 constexpr int kSelNT = 512;
 constexpr int kSelPer = 3;                      // positions per select thread
 constexpr int kSelC = kSelNT * kSelPer;         // positions per select workgroup
 constexpr int kLevels = 31;                     // score bits (scores are non-negative int32)
 constexpr int kApplyNT = 256;
+constexpr int kApplyPer = 4;                   // requests per apply thread
 
 struct WinWorkspace {
     int32_t* run_s;     // [n] scores, each chunk grouped by bucket
@@ -111,76 +116,89 @@ struct WinArgs {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSortNT) void win_chunk_sort(WinArgs a) {
     __shared__ int32_t le[kBucketsMax - 1];
-    __shared__ int32_t cnt_l[kBucketsMax];
-    __shared__ uint32_t keys[kChunk];
-    __shared__ int32_t sc[kChunk];
+    __shared__ uint16_t seg[kSegs][kBucketsMax];   // entries of each bucket in each wave's segment
+    __shared__ int32_t grp[kBucketsMax];           // chunk counts, then group starts
     __shared__ int32_t tmp[kSortNT / kWave];
     const int ne = a.nb - 1;
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
     for (int i = threadIdx.x; i < ne; i += kSortNT) le[i] = a.edges[i];
-    for (int i = threadIdx.x; i < a.nb; i += kSortNT) cnt_l[i] = 0;
+    for (int i = threadIdx.x; i < kSegs * a.nb; i += kSortNT) seg[i / a.nb][i % a.nb] = 0;
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i + 1 < ne; i += kSortNT)
             if (a.edges[i] > a.edges[i + 1]) raise_error(a.dev_err, MAPS_ERR_EDGES_UNSORTED);
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kChunk;
+    const int nbits = a.nb > 1 ? 32 - __clz(uint32_t(a.nb - 1)) : 0;
+    const uint64_t below = (uint64_t(1) << lane) - 1u;
+    int32_t s[kSortPer], b[kSortPer], rank[kSortPer];
     bool bad = false;
+    // wave w owns the 256 entries [256 w, 256 w + 256) of the chunk, 64 a round
 #pragma unroll
     for (int r = 0; r < kSortPer; ++r) {
-        const int loc = threadIdx.x + r * kSortNT;
+        const int loc = wid * (kWave * kSortPer) + r * kWave + lane;
         const int64_t i = base + loc;
-        uint32_t key = 0xFFFFFFFFu;   // past the end: sorts last
-        int32_t s = 0;
-        if (i < a.n) {
+        const bool valid = i < a.n;
+        s[r] = 0;
+        b[r] = 0;
+        if (valid) {
             const int32_t p = a.pred[i], t = a.truth[i];
             bad |= (p < 0) | (t < 0);
             const int64_t d = int64_t(t) - p;   // Eq. (2)
-            s = d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
-            const int b = win_bucket(le, ne, p);
-            key = (uint32_t(b) << 12) | uint32_t(loc);
-            atomicAdd(&cnt_l[b], 1);
+            s[r] = d <= 0 ? 0 : (d > INT32_MAX ? INT32_MAX : int32_t(d));
+            b[r] = win_bucket(le, ne, p);
         }
-        keys[loc] = key;
-        sc[loc] = s;
+        // lanes with the same bucket, bit by bit through ballots
+        uint64_t peers = __ballot(valid);
+        for (int bit = 0; bit < nbits; ++bit) {
+            const bool one = (b[r] >> bit) & 1;
+            const uint64_t m = __ballot(one);
+            peers &= one ? m : ~m;
+        }
+        const int before = __popcll(peers & below);
+        rank[r] = 0;
+        if (valid) {
+            // every lane of the group reads the running count before its
+            // first lane adds the group (one wavefront: LDS operations in order)
+            const int run = seg[wid][b[r]];
+            rank[r] = run + before;
+            if (before == 0) seg[wid][b[r]] = uint16_t(run + __popcll(peers));
+        }
     }
     if (bad) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
     __syncthreads();
-    // bitonic sort of the 4,096 keys, two compare-exchanges per thread a stage
-    for (int k = 2; k <= kChunk; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
+    // per bucket: the entries in earlier segments, and the chunk's count
+    for (int bb = threadIdx.x; bb < a.nb; bb += kSortNT) {
+        int acc = 0;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int q = threadIdx.x + h * kSortNT;            // pair index in [0, 2048)
-                const int lo = ((q & ~(j - 1)) << 1) | (q & (j - 1));
-                const int hi = lo | j;
-                const uint32_t x = keys[lo], y = keys[hi];
-                const bool up = (lo & k) == 0;
-                if ((x > y) == up) { keys[lo] = y; keys[hi] = x; }
-            }
-            __syncthreads();
+        for (int w = 0; w < kSegs; ++w) {
+            const int v = seg[w][bb];
+            seg[w][bb] = uint16_t(acc);
+            acc += v;
         }
+        grp[bb] = acc;
     }
-    const int64_t left = a.n - base;
-    const int valid = left < kChunk ? int(left) : kChunk;
-#pragma unroll
-    for (int r = 0; r < kSortPer; ++r) {
-        const int p = threadIdx.x + r * kSortNT;
-        if (p < valid) {
-            const uint32_t key = keys[p];
-            const int loc = int(key & 0xFFFu);
-            a.w.run_s[base + p] = sc[loc];
-            a.w.run_i[base + p] = int32_t(base + loc);
-            a.w.run_b[base + p] = uint16_t(key >> 12);
-        }
-    }
-    // group sizes and starts (every bucket, zero sizes included)
+    __syncthreads();
+    // group starts (exclusive scan over buckets); sizes and starts to the tables
     const int64_t c = blockIdx.x;
     block_scan<kSortNT, false, false, true, int32_t>(
-        a.nb, 0, [&](int64_t b) { return cnt_l[b]; },
-        [&](int64_t b, int32_t v) {
-            a.w.cnt[b * a.nch + c] = cnt_l[b];
-            a.w.rs[b * a.nch + c] = v;
+        a.nb, 0, [&](int64_t bb) { return grp[bb]; },
+        [&](int64_t bb, int32_t v) {
+            a.w.cnt[bb * a.nch + c] = grp[bb];
+            a.w.rs[bb * a.nch + c] = v;
+            grp[bb] = v;
         },
         tmp);
+#pragma unroll
+    for (int r = 0; r < kSortPer; ++r) {
+        const int loc = wid * (kWave * kSortPer) + r * kWave + lane;
+        const int64_t i = base + loc;
+        if (i < a.n) {
+            const int64_t pos = base + grp[b[r]] + seg[wid][b[r]] + rank[r];
+            a.w.run_s[pos] = s[r];
+            a.w.run_i[pos] = int32_t(i);
+            a.w.run_b[pos] = uint16_t(b[r]);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -379,40 +397,71 @@ struct ApplyArgs {
 };
 
 __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
-    extern __shared__ int32_t ledges[];
+    __shared__ int32_t ledges[kBucketsMax - 1];
+    __shared__ int64_t lpbase[kBucketsMax];
     const int ne = a.nb - 1;
     for (int i = threadIdx.x; i < ne; i += kApplyNT) ledges[i] = a.edges[i];
+    for (int i = threadIdx.x; i < a.nb; i += kApplyNT) lpbase[i] = a.w.pbase[i];
     __syncthreads();
     bool bad = false;
-    const int64_t stride = int64_t(gridDim.x) * kApplyNT;
-    for (int64_t j = int64_t(blockIdx.x) * kApplyNT + threadIdx.x; j < r.m; j += stride) {
-        const int32_t p = r.apply_pred[j];
-        const int64_t seen = r.seen[j];
-        int32_t q = -1, U = -1;
-        if (p >= 0 && (seen < 0 || seen > a.n)) {
-            bad = true;
-        } else if (p >= 0) {
-            const int64_t b = win_bucket(ledges, ne, p);
-            const int64_t ch = seen / kChunk;
-            const int32_t* row = a.w.off + b * (a.nch + 1);
-            int64_t c;
-            if (ch >= a.nch) {
-                c = row[a.nch];
-            } else {
-                // entries of bucket b in chunk ch logged before `seen`
-                const int32_t* gi = a.w.run_i + ch * kChunk + a.w.rs[b * a.nch + ch];
-                int lo = 0, hi = a.w.cnt[b * a.nch + ch];
-                while (lo < hi) {
-                    const int mid = (lo + hi) >> 1;
-                    if (gi[mid] < seen) lo = mid + 1; else hi = mid;
+    // kApplyPer requests per thread, their searches interleaved so that their
+    // loads are in flight together
+    for (int64_t j0 = int64_t(blockIdx.x) * (kApplyNT * kApplyPer); j0 < r.m;
+         j0 += int64_t(gridDim.x) * (kApplyNT * kApplyPer)) {
+        int32_t p[kApplyPer], b[kApplyPer], n_g[kApplyPer], pos[kApplyPer];
+        int64_t seen[kApplyPer], c[kApplyPer];
+        const int32_t* gi[kApplyPer];
+        bool live[kApplyPer];
+        int32_t most = 0;
+#pragma unroll
+        for (int k = 0; k < kApplyPer; ++k) {
+            const int64_t j = j0 + threadIdx.x + k * kApplyNT;
+            p[k] = j < r.m ? r.apply_pred[j] : -1;
+            seen[k] = j < r.m ? r.seen[j] : 0;
+            live[k] = p[k] >= 0 && seen[k] >= 0 && seen[k] <= a.n;
+            bad |= p[k] >= 0 && !live[k];
+            b[k] = live[k] ? win_bucket(ledges, ne, p[k]) : 0;
+            const int64_t ch = seen[k] / kChunk;
+            const int32_t* row = a.w.off + int64_t(b[k]) * (a.nch + 1);
+            n_g[k] = 0;
+            gi[k] = a.w.run_i;
+            c[k] = 0;
+            if (live[k]) {
+                if (ch >= a.nch) {
+                    c[k] = row[a.nch];
+                } else {
+                    // entries of bucket b in chunk ch logged before `seen`: a
+                    // search of the group's (ascending) log indices
+                    gi[k] = a.w.run_i + ch * kChunk + a.w.rs[int64_t(b[k]) * a.nch + ch];
+                    n_g[k] = a.w.cnt[int64_t(b[k]) * a.nch + ch];
+                    c[k] = row[ch];
                 }
-                c = row[ch] + lo;
             }
-            q = a.w.qw[a.w.pbase[b] + c];
-            U = q == MAPS_Q_INF ? r.u_max : int32_t(int64_t(p) + q < r.u_max ? int64_t(p) + q : r.u_max);
+            most = most > n_g[k] ? most : n_g[k];
+            pos[k] = 0;
         }
-        if (r.q_out) r.q_out[j] = q;
-        r.U_out[j] = U;
+        int step = 1;
+        while (step * 2 <= most) step *= 2;
+        for (; most > 0 && step > 0; step >>= 1) {
+#pragma unroll
+            for (int k = 0; k < kApplyPer; ++k) {
+                const int np = pos[k] + step;
+                if (np <= n_g[k] && gi[k][np - 1] < seen[k]) pos[k] = np;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kApplyPer; ++k) {
+            const int64_t j = j0 + threadIdx.x + k * kApplyNT;
+            if (j >= r.m) continue;
+            int32_t q = -1, U = -1;
+            if (live[k]) {
+                q = a.w.qw[lpbase[b[k]] + c[k] + pos[k]];
+                U = q == MAPS_Q_INF ? r.u_max
+                                    : int32_t(int64_t(p[k]) + q < r.u_max ? int64_t(p[k]) + q : r.u_max);
+            }
+            if (r.q_out) r.q_out[j] = q;
+            r.U_out[j] = U;
+        }
     }
     if (bad) raise_error(a.dev_err, MAPS_ERR_SEEN_RANGE);
 }
@@ -469,9 +518,9 @@ extern "C" maps_status maps_calibrate_window(const int32_t* pred, const int32_t*
     hipLaunchKernelGGL(win_select, dim3(unsigned(groups)), dim3(kSelNT), S.bytes, stream, a);
     MAPS_CHECK_LAUNCH();
     ApplyArgs r{apply_pred, apply_seen, m, u_max, q_out, U_out};
-    const int64_t ab = (m + kApplyNT - 1) / kApplyNT;
+    const int64_t ab = (m + kApplyNT * kApplyPer - 1) / (kApplyNT * kApplyPer);
     const unsigned grid = unsigned(ab < 8192 ? ab : 8192);
-    hipLaunchKernelGGL(win_apply, dim3(grid), dim3(kApplyNT), size_t(nb > 1 ? nb - 1 : 1) * 4, stream, a, r);
+    hipLaunchKernelGGL(win_apply, dim3(grid), dim3(kApplyNT), 0, stream, a, r);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }
