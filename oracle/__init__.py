@@ -72,6 +72,12 @@ def _declare(lib):
                                  c.c_int64, _i32p, _i32p, i64n, c.c_int32, c.c_int64,
                                  _i32p, _i64p, _i64p, _u8p, i64n, i64n]
     lib.oracle_place.restype = c.c_int
+    lib.oracle_rsc_state.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, c.c_int32, _i64p, _i64p,
+                                     _i64p]
+    lib.oracle_rsc_state.restype = c.c_int
+    lib.oracle_place_static.argtypes = [c.c_int32, _i64p, _i32p, c.c_int32, c.c_int64, _i32p, _i32p, c.c_int32,
+                                        c.c_int64, c.c_int32, _i32p, _i64p, _u8p, i64n, i32n]
+    lib.oracle_place_static.restype = c.c_int
     lib.oracle_local_order.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, _i64p,
                                        _i32p, _i32p, i32n, c.c_int32, c.c_int32, _i32p, _i32p]
     lib.oracle_local_order.restype = c.c_int
@@ -190,6 +196,36 @@ class Oracle:
         if rc:
             raise ValueError(f"oracle_place failed ({rc})")
         return out
+
+    # -- Algorithm 1 on block counts (Sec. 3.3, Eq. (6)) ---------------------
+    def rsc_state(self, seg_off, p, g, U, capacity, S: int):
+        """(B_free, B_res, B_eff) per decoder in blocks of S tokens."""
+        seg_off = _i64(seg_off)
+        D = seg_off.size - 1
+        out = [np.zeros(D, np.int64) for _ in range(3)]
+        rc = self.lib.oracle_rsc_state(D, seg_off, _i32(p), _i32(g), _i32(U), _i32(capacity), int(S), *out)
+        if rc:
+            raise ValueError(f"oracle_rsc_state failed ({rc})")
+        return tuple(out)
+
+    def place_static(self, b_eff, queue_len, S: int, a_p, a_U, policy=POLICY_MQ, rr_offset=0, reserve=False):
+        """Algorithm 1 per arrival; with `reserve`, each dispatch reserves its
+        B_need and joins the queue before the next.  Returns (choice, b_need,
+        flags, b_eff_after, queue_after)."""
+        b_eff = _i64(b_eff)
+        D = b_eff.size
+        a_p, a_U = _i32(a_p), _i32(a_U)
+        A = a_p.size
+        choice = np.zeros(A, np.int32)
+        need = np.zeros(A, np.int64)
+        flags = np.zeros(A, np.uint8)
+        b_after = np.zeros(D, np.int64)
+        q_after = np.zeros(D, np.int32)
+        rc = self.lib.oracle_place_static(D, b_eff, _i32(queue_len), int(S), A, a_p, a_U, int(policy),
+                                          int(rr_offset), int(bool(reserve)), choice, need, flags, b_after, q_after)
+        if rc:
+            raise ValueError(f"oracle_place_static failed ({rc})")
+        return choice, need, flags, b_after, q_after
 
     # -- local order (Sec. 3.3, Eq. (7); App. A, Eq. (10)) -------------------
     def local_order(self, seg_off, p, g, U, capacity, q_off, q_p, q_U, q_wait, max_wait_ms,

@@ -18,6 +18,9 @@
  *                maximum-capacity fallback, round-robin when no bound exists
  *                (Eq. (9)), with the static block test replaced by the
  *                projected peak of the decoder's occupancy plus the arrival.
+ *   static rule  Sec. 3.3 and Algorithm 1 as printed: block counts of the
+ *                runtime state, B_need <= B_eff, and with reservation each
+ *                dispatch reserving its B_need before the next arrival.
  *   local order  Sec. 3.3, Eq. (7): argsort of the queue by the bound, with
  *                starvation promotion, and the App. A admission rule (10)
  *                applied to the reordered queue.
@@ -340,6 +343,90 @@ int oracle_place(int32_t D, const int64_t* seg_off, const int32_t* p, const int3
         }
     }
     free(feas_d); free(feas_peak); free(fb_d); free(fb_slack); free(fb_peak);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 1 on block counts (Sec. 3.3: the runtime state, Eq. (6),        */
+/* Algorithm 1 and the atomic reservation of B_need after each dispatch)      */
+/* ------------------------------------------------------------------------ */
+
+static int64_t ceil_div(int64_t x, int64_t s) { return (x + s - 1) / s; }
+
+/* Runtime state of each decoder in blocks of S tokens: capacity floor(C/S)
+ * blocks; each resident holds ceil((p+g)/S) blocks and keeps reserved the
+ * blocks still missing to its demand ceil((p+U)/S) (none when U < 0 or when
+ * it already holds more); B_free = capacity blocks - held blocks,
+ * B_res = sum of the reservations, B_eff = B_free - B_res. */
+int oracle_rsc_state(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                     const int32_t* U, const int32_t* capacity, int32_t S,
+                     int64_t* b_free, int64_t* b_res, int64_t* b_eff)
+{
+    if (D < 1 || S < 1) return -1;
+    for (int32_t d = 0; d < D; ++d) {
+        int64_t held = 0, res = 0;
+        for (int64_t r = seg_off[d]; r < seg_off[d + 1]; ++r) {
+            int64_t now = ceil_div((int64_t)p[r] + g[r], S);
+            int64_t demand = U[r] < 0 ? now : ceil_div((int64_t)p[r] + U[r], S);
+            held += now;
+            res += max64(demand - now, 0);
+        }
+        b_free[d] = (int64_t)capacity[d] / S - held;
+        b_res[d] = res;
+        b_eff[d] = b_free[d] - res;
+    }
+    return 0;
+}
+
+/* Algorithm 1 for A arrivals in order: B_need = ceil((p+U)/S) (Eq. (6)); the
+ * feasible decoders have B_need <= B_eff; policy MQ takes the feasible one
+ * with the shortest queue (lowest index on ties), else the largest B_eff
+ * (lowest index on ties); policy MC always the largest B_eff.  An arrival
+ * without a bound (U < 0) goes round robin, (rr_offset + a) mod D, with
+ * b_need -1.  With reserve != 0 each dispatch then reserves its B_need on the
+ * chosen decoder and joins its queue (B_eff -= B_need, Q += 1; a round-robin
+ * dispatch only joins the queue), so later arrivals see the new state; with
+ * reserve == 0 every arrival sees the given state.  flags: bit0 when B_need <=
+ * B_eff of the chosen decoder (before its reservation), bit1 round robin.
+ * b_eff_out / q_out (if not NULL) receive the state after the batch. */
+int oracle_place_static(int32_t D, const int64_t* b_eff_in, const int32_t* queue_len, int32_t S,
+                        int64_t A, const int32_t* a_p, const int32_t* a_U, int32_t policy,
+                        int64_t rr_offset, int32_t reserve, int32_t* choice, int64_t* b_need,
+                        uint8_t* flags, int64_t* b_eff_out, int32_t* q_out)
+{
+    if (D < 1 || A < 0 || S < 1 || rr_offset < 0 ||
+        (policy != ORACLE_POLICY_MQ && policy != ORACLE_POLICY_MC)) return -1;
+    int64_t* B = (int64_t*)malloc((size_t)D * sizeof(int64_t));
+    int64_t* Q = (int64_t*)malloc((size_t)D * sizeof(int64_t));
+    if (!B || !Q) return -2;
+    for (int32_t d = 0; d < D; ++d) { B[d] = b_eff_in[d]; Q[d] = queue_len[d]; }
+    for (int64_t a = 0; a < A; ++a) {
+        int32_t best;
+        if (a_U[a] < 0) {
+            best = (int32_t)((rr_offset + a) % D);
+            choice[a] = best;
+            b_need[a] = -1;
+            flags[a] = 2;
+            if (reserve) Q[best] += 1;
+            continue;
+        }
+        int64_t need = ceil_div((int64_t)a_p[a] + a_U[a], S);
+        int32_t feas = -1, most = 0;
+        for (int32_t d = 0; d < D; ++d) {
+            if (need <= B[d] && (feas < 0 || Q[d] < Q[feas])) feas = d;
+            if (B[d] > B[most]) most = d;
+        }
+        best = (policy == ORACLE_POLICY_MQ && feas >= 0) ? feas : most;
+        choice[a] = best;
+        b_need[a] = need;
+        flags[a] = (uint8_t)(need <= B[best] ? 1 : 0);
+        if (reserve) { B[best] -= need; Q[best] += 1; }
+    }
+    for (int32_t d = 0; d < D; ++d) {
+        if (b_eff_out) b_eff_out[d] = B[d];
+        if (q_out) q_out[d] = (int32_t)Q[d];
+    }
+    free(B); free(Q);
     return 0;
 }
 

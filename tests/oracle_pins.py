@@ -292,6 +292,144 @@ def pin_window_coverage(o):
 
 
 # ---------------------------------------------------------------------------
+# Algorithm 1 on block counts (Sec. 3.3, Eq. (6)), with and without reservation
+# ---------------------------------------------------------------------------
+
+def py_place_static(B, Q, S, a_p, a_U, policy, rr_offset, reserve):
+    """Brute force of Algorithm 1: explicit loops, Python integers."""
+    B, Q = [int(x) for x in B], [int(x) for x in Q]
+    D = len(B)
+    out = []
+    for a, (p, U) in enumerate(zip(a_p, a_U)):
+        if U < 0:
+            d = (rr_offset + a) % D
+            out.append((d, -1, 2))
+            if reserve:
+                Q[d] += 1
+            continue
+        need = -(-(int(p) + int(U)) // S)
+        feas = [d for d in range(D) if need <= B[d]]
+        if policy == 0 and feas:
+            d = min(feas, key=lambda x: (Q[x], x))
+        else:
+            d = min(range(D), key=lambda x: (-B[x], x))
+        out.append((d, need, 1 if need <= B[d] else 0))
+        if reserve:
+            B[d] -= need
+            Q[d] += 1
+    return out, B, Q
+
+
+def pin_static_golden(o):
+    gd = golden("place_static_hand.json")
+    r = gd["rsc"]
+    bf, br, be = o.rsc_state(r["seg_off"], r["p"], r["g"], r["U"], r["capacity"], r["S"])
+    assert bf.tolist() == r["b_free"] and br.tolist() == r["b_res"] and be.tolist() == r["b_eff"], (bf, br, be)
+    pl = gd["place"]
+    for mode, reserve in (("no_reserve", False), ("reserve", True)):
+        ch, need, fl, ba, qa = o.place_static(pl["b_eff"], pl["queue_len"], pl["S"], pl["a_p"], pl["a_U"],
+                                              reserve=reserve)
+        assert ch.tolist() == pl[mode]["choice"], (mode, ch)
+        assert need.tolist() == pl["b_need"] and fl.tolist() == pl["flags"], (mode, need, fl)
+        assert ba.tolist() == pl[mode]["b_eff_after"] and qa.tolist() == pl[mode]["queue_after"], (mode, ba, qa)
+
+
+def pin_static_bruteforce(o):
+    rng = _rng(41)
+    for trial in range(60):
+        D = int(rng.integers(1, 7))
+        A = int(rng.integers(0, 40))
+        S = int(rng.choice([1, 2, 16, 33]))
+        B = rng.integers(-20, 60, size=D)
+        Q = rng.integers(0, 4, size=D)
+        a_p = rng.integers(0, 300, size=A)
+        a_U = rng.integers(-2, 300, size=A)
+        for policy in (0, 1):
+            for reserve in (False, True):
+                ch, need, fl, ba, qa = o.place_static(B, Q, S, a_p, a_U, policy, 5, reserve)
+                want, wB, wQ = py_place_static(B, Q, S, a_p, a_U, policy, 5, reserve)
+                assert [(int(c), int(n), int(f)) for c, n, f in zip(ch, need, fl)] == want, (trial, policy, reserve)
+                assert ba.tolist() == wB and qa.tolist() == wQ, (trial, policy, reserve)
+
+
+def pin_static_water_filling(o):
+    """With reservation and every decoder feasible for every arrival, the
+    shortest-queue choice fills queues level by level: arrival i takes the
+    i-th smallest slot (Q_d + m, d), m = 0, 1, ..."""
+    rng = _rng(42)
+    for trial in range(10):
+        D = int(rng.integers(1, 9))
+        A = int(rng.integers(1, 200))
+        Q = rng.integers(0, 6, size=D)
+        slots = sorted((int(Q[d]) + m, d) for d in range(D) for m in range(A))
+        ch, _, fl, _, qa = o.place_static(np.full(D, 10**12), Q, 16, rng.integers(0, 100, size=A),
+                                          rng.integers(0, 100, size=A), reserve=True)
+        assert ch.tolist() == [d for _, d in slots[:A]], trial
+        assert np.all(fl == 1) and qa.tolist() == (Q + np.bincount(ch, minlength=D)).tolist()
+
+
+def pin_static_state_and_invariants(o):
+    rng = _rng(43)
+    seg, p, g, U, cap = _static_decoders(rng)
+    for S in (1, 16):
+        bf, br, be = o.rsc_state(seg, p, g, U, cap, S)
+        for d in range(seg.size - 1):
+            sl = slice(seg[d], seg[d + 1])
+            held = sum(-(-(int(x) + int(y)) // S) for x, y in zip(p[sl], g[sl]))
+            assert bf[d] == int(cap[d]) // S - held and br[d] >= 0 and be[d] == bf[d] - br[d]
+            if S == 1:   # block size 1: B_eff = C - sum(p + max(g, U)), U < 0 counting as g
+                assert be[d] == int(cap[d]) - sum(int(x) + max(int(y), int(u)) for x, y, u in zip(p[sl], g[sl], U[sl]))
+    A = 300
+    a_p = rng.integers(0, 2000, size=A)
+    a_U = rng.integers(-1, 3000, size=A)
+    Q = rng.integers(0, 5, size=seg.size - 1)
+    ch, need, fl, ba, qa = o.place_static(be, Q, 16, a_p, a_U, reserve=True)
+    bound = a_U >= 0
+    for d in range(seg.size - 1):
+        assert be[d] - ba[d] == need[bound & (ch == d)].sum()
+        assert qa[d] - Q[d] == np.sum(ch == d)
+    ch0, _, fl0, _, _ = o.place_static(be, Q, 16, a_p[:1], a_U[:1], reserve=False)
+    assert ch0[0] == ch[0] and fl0[0] == fl[0]
+
+
+def _static_decoders(rng, D=6):
+    counts = rng.integers(0, 30, size=D)
+    seg = np.zeros(D + 1, np.int64)
+    seg[1:] = np.cumsum(counts)
+    n = int(seg[-1])
+    return (seg, rng.integers(0, 500, size=n), rng.integers(0, 400, size=n), rng.integers(-1, 600, size=n),
+            rng.integers(0, 40000, size=D))
+
+
+def pin_static_reduces_to_projection(o):
+    """Block size 1, every resident with remaining length T and every arrival
+    bound T: the projected peak test is exactly B_need <= B_eff, and the
+    largest slack is the largest B_eff (Algorithm 1 is the projected rule's
+    special case), so both oracles choose alike."""
+    rng = _rng(44)
+    for trial in range(10):
+        D = int(rng.integers(1, 6))
+        T = int(rng.integers(1, 200))
+        counts = rng.integers(0, 8, size=D)
+        seg = np.zeros(D + 1, np.int64)
+        seg[1:] = np.cumsum(counts)
+        n = int(seg[-1])
+        p = rng.integers(0, 300, size=n)
+        g = rng.integers(0, 100, size=n)
+        U = g + T
+        sums = np.add.reduceat(np.concatenate([p + U, [0]]), seg[:-1])[:D] * (counts > 0)
+        cap = (sums + rng.integers(0, 800, size=D)).astype(np.int32)
+        Q = rng.integers(0, 4, size=D)
+        A = 50
+        a_p = rng.integers(0, 400, size=A)
+        a_U = np.where(rng.random(A) < 0.1, -1, T)
+        pr = o.place(seg, p, g, U, cap, Q, a_p, a_U, want_pairs=False)
+        _, _, be = o.rsc_state(seg, p, g, U, cap, 1)
+        ch, _, fl, _, _ = o.place_static(be, Q, 1, a_p, a_U)
+        assert np.array_equal(ch, pr.choice) and np.array_equal(fl, pr.flags), trial
+
+
+# ---------------------------------------------------------------------------
 # occupancy and placement (Sec. 3.3, App. A, Algorithm 1)
 # ---------------------------------------------------------------------------
 
@@ -517,6 +655,8 @@ ALL_PINS = [
     pin_quantile_special_cases, pin_quantile_monotone_in_alpha, pin_coverage,
     pin_window_golden, pin_window_bruteforce, pin_window_closed_forms, pin_window_reduces_to_fixed_set,
     pin_window_coverage,
+    pin_static_golden, pin_static_bruteforce, pin_static_water_filling, pin_static_state_and_invariants,
+    pin_static_reduces_to_projection,
     pin_place_golden, pin_occupancy_bruteforce, pin_place_bruteforce, pin_place_closed_forms,
     pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
     pin_local_order_golden, pin_local_order_bruteforce,

@@ -60,6 +60,19 @@ MUTANTS = [
      "set[t] = (int64_t)truth[i] - (int64_t)pred[i];"),
     ("window_one_short", "int64_t nw = min64(c, window);", "int64_t nw = min64(c, window - 1);"),
     ("window_inf_gives_pred", "if (q == ORACLE_Q_INF) U_out[j] = u_max;", "if (q == ORACLE_Q_INF) U_out[j] = apply_pred[j];"),
+    ("static_need_floor", "static int64_t ceil_div(int64_t x, int64_t s) { return (x + s - 1) / s; }",
+     "static int64_t ceil_div(int64_t x, int64_t s) { return x / s; }"),
+    ("static_feasible_strict", "if (need <= B[d] && (feas < 0 || Q[d] < Q[feas])) feas = d;",
+     "if (need < B[d] && (feas < 0 || Q[d] < Q[feas])) feas = d;"),
+    ("static_mq_ties_highest", "if (need <= B[d] && (feas < 0 || Q[d] < Q[feas])) feas = d;",
+     "if (need <= B[d] && (feas < 0 || Q[d] <= Q[feas])) feas = d;"),
+    ("static_fallback_ties_highest", "if (B[d] > B[most]) most = d;", "if (B[d] >= B[most]) most = d;"),
+    ("static_no_reservation", "if (reserve) { B[best] -= need; Q[best] += 1; }", "if (reserve) { Q[best] += 1; }"),
+    ("static_no_enqueue", "if (reserve) { B[best] -= need; Q[best] += 1; }", "if (reserve) { B[best] -= need; }"),
+    ("static_rr_not_enqueued", "            if (reserve) Q[best] += 1;\n            continue;", "            continue;"),
+    ("rsc_negative_reservation", "res += max64(demand - now, 0);", "res += demand - now;"),
+    ("rsc_capacity_rounded_up", "b_free[d] = (int64_t)capacity[d] / S - held;",
+     "b_free[d] = ceil_div(capacity[d], S) - held;"),
     ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
      "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
 ]
