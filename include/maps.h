@@ -71,8 +71,10 @@ enum {
     MAPS_ERR_WAIT_TIMEOUT = 256u,   /* a workgroup's bounded wait for the other workgroups
                                        of its launch ran out (the device did not hold
                                        every workgroup of the launch at once) */
-    MAPS_ERR_SEEN_RANGE = 512u      /* a seen count outside [0, n] (sliding-window
+    MAPS_ERR_SEEN_RANGE = 512u,     /* a seen count outside [0, n] (sliding-window
                                        calibration) */
+    MAPS_ERR_BLOCK_RANGE = 1024u    /* an effective block count left [-2^52, 2^52)
+                                       during reserving placement */
 };
 
 /* Largest u_max (cap on bounds and remaining lengths) the snapshot accepts,
@@ -87,6 +89,9 @@ enum {
  * maps_calibrate_window accepts. */
 #define MAPS_MAX_WINDOW 4096
 #define MAPS_MAX_WINDOW_BUCKETS 1024
+
+/* Most decoders that maps_place_static accepts with reservation. */
+#define MAPS_MAX_RESERVE_DECODERS 1024
 
 /* Placement policies: minimum queue among feasible decoders with the largest
  * slack as fallback (Sec. 3.3 and Algorithm 1), or largest slack alone (the
@@ -221,6 +226,52 @@ maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,
                        uint8_t* flags, int32_t* pair_peak,
                        uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                        hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 3b. Algorithm 1 on block counts (Sec. 3.3: runtime state, Eq. (6),       */
+/*     Algorithm 1, the atomic reservation of B_need after a dispatch)      */
+/* ------------------------------------------------------------------------ */
+/*
+ * Runtime state of D decoders in blocks of S >= 1 tokens, from the residents
+ * of maps_project (seg_off, prompt p, generated g, bound U; U < 0: no bound)
+ * and capacity[d] in tokens: a resident holds ceil((p+g)/S) blocks and keeps
+ * reserved the blocks still missing to its demand ceil((p+U)/S) (none when
+ * U < 0 or when it holds more already);
+ *   b_free[d] = floor(capacity[d] / S) - sum of held blocks,
+ *   b_res[d]  = sum of reserved blocks,  b_eff[d] = b_free[d] - b_res[d].
+ * Outputs int64 [D], device arrays.  dev_err bits: NEG_LEN (p, g or capacity
+ * < 0), SEG_OFFSETS.  Host errors: NULL, SIZE (D < 1, n_total < 0, S < 1), HIP.
+ */
+maps_status maps_rsc_state(int32_t D, const int64_t* seg_off, int64_t n_total, const int32_t* prompt,
+                           const int32_t* generated, const int32_t* upper, const int32_t* capacity,
+                           int32_t block_size, int64_t* b_free, int64_t* b_res, int64_t* b_eff,
+                           uint32_t* dev_err, hipStream_t stream);
+
+/*
+ * Algorithm 1 for arrivals a = 0..A-1 in order against the state (b_eff[D]
+ * int64, queue_len[D]): B_need = ceil((a_prompt + a_upper) / S) (Eq. (6));
+ * decoders with B_need <= B_eff are feasible; policy MQ takes the feasible
+ * decoder with the shortest queue (lowest index on ties), else the largest
+ * B_eff (lowest index on ties); policy MC always the largest B_eff.  An
+ * arrival without a bound (a_upper < 0) goes round robin, (rr_offset + a) mod D,
+ * with b_need = -1.
+ * reserve = 0: every arrival sees the given state (independent decisions, in
+ * parallel).  reserve = 1: each dispatch reserves its B_need on its decoder
+ * and joins its queue before the next arrival (B_eff -= B_need, Q += 1; a
+ * round-robin dispatch only joins the queue), one arrival after another;
+ * D <= MAPS_MAX_RESERVE_DECODERS.
+ * Outputs [A]: choice, b_need (int64), flags (bit0: B_need <= B_eff of the
+ * chosen decoder before its reservation; bit1: round robin).  b_eff_out and
+ * queue_out [D] (may be NULL) receive the state after the batch.
+ * dev_err bits: NEG_LEN (a_prompt < 0 with a bound), BLOCK_RANGE.
+ * Host errors: NULL, SIZE (D < 1, A < 0, S < 1, rr_offset < 0, reserve with
+ * D > MAPS_MAX_RESERVE_DECODERS), POLICY, HIP.
+ */
+maps_status maps_place_static(int32_t D, const int64_t* b_eff, const int32_t* queue_len, int32_t block_size,
+                              const int32_t* a_prompt, const int32_t* a_upper, int64_t A, int32_t policy,
+                              int64_t rr_offset, int32_t reserve, int32_t* choice, int64_t* b_need,
+                              uint8_t* flags, int64_t* b_eff_out, int32_t* queue_out, uint32_t* dev_err,
+                              hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 4. Local order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10))       */

@@ -28,8 +28,9 @@ MAX_LOCAL_QUEUE = 2048
 ERR_BITS = {
     1: "NEG_LEN", 2: "EDGES_UNSORTED", 4: "INT32_RANGE", 8: "SEG_OFFSETS",
     16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG", 128: "TOO_MANY", 256: "WAIT_TIMEOUT",
-    512: "SEEN_RANGE",
+    512: "SEEN_RANGE", 1024: "BLOCK_RANGE",
 }
+MAX_RESERVE_DECODERS = 1024
 MAX_WINDOW = 4096
 MAX_WINDOW_BUCKETS = 1024
 MAX_U_MAX = (1 << 24) - 64
@@ -48,6 +49,9 @@ _SIGNATURES = {
     "maps_calibrate_window_workspace_size": (_sz, [_i64, _i32]),
     "maps_calibrate_window": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
+    "maps_rsc_state": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "maps_place_static": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp, _i64, _i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp,
+                                 _vp, _vp]),
     "maps_snapshot_bytes": (_sz, [_i32, _i64, _i32]),
     "maps_project_workspace_size": (_sz, [_i32, _i64, _i32]),
     "maps_project": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp, _vp, _sz, _vp]),
@@ -316,6 +320,58 @@ def local_order(snapshot: Snapshot, capacity, q_off, q_prompt, q_upper, q_wait_m
                                     _ptr(err), None, 0, _stream(dev))
     _check(st, "maps_local_order")
     return order, admitted, err
+
+
+# ---------------------------------------------------------------------------
+# 3b. Algorithm 1 on block counts
+# ---------------------------------------------------------------------------
+
+def rsc_state(seg_off, prompt, generated, upper, capacity, block_size: int, dev_err=None, out=None):
+    """Runtime state per decoder in blocks: (b_free, b_res, b_eff, dev_err), int64 [D]."""
+    seg_off = _dev(seg_off, torch.int64, "seg_off")
+    dev = seg_off.device
+    D = seg_off.numel() - 1
+    n = prompt.numel()
+    for name, t in (("prompt", prompt), ("generated", generated), ("upper", upper)):
+        _dev(t, torch.int32, name)
+        if t.numel() != n:
+            raise MapsError("prompt, generated and upper differ in length")
+    capacity = _dev(capacity, torch.int32, "capacity")
+    if capacity.numel() != D:
+        raise MapsError("capacity must have D entries")
+    bf, br, be = out if out is not None else [torch.empty(D, dtype=torch.int64, device=dev) for _ in range(3)]
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = library().maps_rsc_state(D, _ptr(seg_off), n, _ptr(prompt), _ptr(generated), _ptr(upper), _ptr(capacity),
+                                  int(block_size), _ptr(bf), _ptr(br), _ptr(be), _ptr(err), _stream(dev))
+    _check(st, "maps_rsc_state")
+    return bf, br, be, err
+
+
+def place_static(b_eff, queue_len, block_size: int, a_prompt, a_upper, policy: int = POLICY_MQ, rr_offset: int = 0,
+                 reserve: bool = False, dev_err=None, out=None, want_state: bool = True):
+    """Algorithm 1 per arrival against (b_eff, queue_len); with `reserve` each
+    dispatch reserves its B_need and joins its queue before the next.  Returns
+    (choice, b_need, flags, b_eff_after, queue_after, dev_err)."""
+    b_eff = _dev(b_eff, torch.int64, "b_eff")
+    dev = b_eff.device
+    queue_len = _dev(queue_len, torch.int32, "queue_len")
+    a_prompt = _dev(a_prompt, torch.int32, "a_prompt")
+    a_upper = _dev(a_upper, torch.int32, "a_upper")
+    D, A = b_eff.numel(), a_prompt.numel()
+    if queue_len.numel() != D or a_upper.numel() != A:
+        raise MapsError("queue_len must have D entries and a_upper A entries")
+    if out is None:
+        out = (torch.empty(A, dtype=torch.int32, device=dev), torch.empty(A, dtype=torch.int64, device=dev),
+               torch.empty(A, dtype=torch.uint8, device=dev),
+               torch.empty(D, dtype=torch.int64, device=dev) if want_state else None,
+               torch.empty(D, dtype=torch.int32, device=dev) if want_state else None)
+    choice, need, flags, b_after, q_after = out
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = library().maps_place_static(D, _ptr(b_eff), _ptr(queue_len), int(block_size), _ptr(a_prompt), _ptr(a_upper),
+                                     A, int(policy), int(rr_offset), int(bool(reserve)), _ptr(choice), _ptr(need),
+                                     _ptr(flags), _ptr(b_after), _ptr(q_after), _ptr(err), _stream(dev))
+    _check(st, "maps_place_static")
+    return choice, need, flags, b_after, q_after, err
 
 
 # ---------------------------------------------------------------------------

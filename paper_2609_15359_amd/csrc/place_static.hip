@@ -1,0 +1,334 @@
+// Algorithm 1 on block counts (Sec. 3.3: the runtime state of each decoder,
+// Eq. (6), Algorithm 1, and the atomic reservation of B_need after each
+// dispatch) on gfx950.
+//
+//   rsc_state           one workgroup per decoder: held and reserved blocks of
+//                       its residents summed in 64-bit integers;
+//   static_independent  every arrival against the reported state: the
+//                       decoders' (B_eff, Q) staged in LDS in tiles, each
+//                       thread scanning them for four arrivals at once (the
+//                       LDS reads are broadcasts);
+//   static_reserve      arrivals one after another, each reserving its B_need
+//                       and joining its decoder's queue before the next: one
+//                       wavefront holds the state of up to 1,024 decoders in
+//                       registers (16 per lane); per arrival a packed key per
+//                       decoder, a wavefront minimum through DPP, and the
+//                       owning lane updates its register.  The chain is serial
+//                       by definition, so this kernel runs at the latency of
+//                       one wavefront.
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace {
+
+constexpr int kRscNT = 256;
+constexpr int kIndNT = 256;
+constexpr int kIndPer = 4;           // arrivals per thread
+constexpr int kIndTile = 2048;       // decoders per LDS tile
+constexpr int kResSlots = MAPS_MAX_RESERVE_DECODERS / kWave;
+constexpr int64_t kBlockLimit = int64_t(1) << 52;
+
+__device__ inline int64_t ceil_blocks(int64_t tokens, int64_t S) { return (tokens + S - 1) / S; }
+
+// ---------------------------------------------------------------------------
+// Runtime state
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kRscNT) void rsc_state(int32_t D, const int64_t* __restrict__ seg_off,
+                                                    int64_t n_total, const int32_t* __restrict__ p,
+                                                    const int32_t* __restrict__ g, const int32_t* __restrict__ U,
+                                                    const int32_t* __restrict__ cap, int32_t S,
+                                                    int64_t* __restrict__ b_free, int64_t* __restrict__ b_res,
+                                                    int64_t* __restrict__ b_eff, uint32_t* dev_err) {
+    __shared__ int64_t tmp[kRscNT / kWave];
+    const int d = blockIdx.x;
+    int64_t lo = seg_off[d], hi = seg_off[d + 1];
+    if (!(0 <= lo && lo <= hi && hi <= n_total)) {
+        if (threadIdx.x == 0) {
+            raise_error(dev_err, MAPS_ERR_SEG_OFFSETS);
+            b_free[d] = b_res[d] = b_eff[d] = 0;
+        }
+        return;
+    }
+    int64_t held = 0, res = 0;
+    bool bad = false;
+    for (int64_t r = lo + threadIdx.x; r < hi; r += kRscNT) {
+        const int32_t pr = p[r], gr = g[r], ur = U[r];
+        bad |= (pr < 0) | (gr < 0);
+        const int64_t now = ceil_blocks(int64_t(pr) + gr, S);
+        const int64_t demand = ur < 0 ? now : ceil_blocks(int64_t(pr) + ur, S);
+        held += now;
+        res += demand > now ? demand - now : 0;
+    }
+    if (bad) raise_error(dev_err, MAPS_ERR_NEG_LEN);
+    held = block_reduce_add<kRscNT>(held, tmp);
+    res = block_reduce_add<kRscNT>(res, tmp);
+    if (threadIdx.x == 0) {
+        const int32_t c = cap[d];
+        if (c < 0) raise_error(dev_err, MAPS_ERR_NEG_LEN);
+        const int64_t fr = int64_t(c) / S - held;
+        b_free[d] = fr;
+        b_res[d] = res;
+        b_eff[d] = fr - res;
+    }
+}
+
+struct StaticArgs {
+    int32_t D;
+    const int64_t* beff;
+    const int32_t* qlen;
+    int32_t S;
+    const int32_t* ap;
+    const int32_t* aU;
+    int64_t A;
+    int32_t policy;
+    int64_t rr_offset;
+    int32_t* choice;
+    int64_t* need;
+    uint8_t* flags;
+    int64_t* beff_out;
+    int32_t* q_out;
+    uint32_t* dev_err;
+};
+
+// ---------------------------------------------------------------------------
+// Every arrival against the reported state
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kIndNT) void static_independent(StaticArgs a) {
+    __shared__ int64_t lb[kIndTile];
+    __shared__ int32_t lq[kIndTile];
+    const int64_t first = int64_t(blockIdx.x) * (kIndNT * kIndPer) + threadIdx.x;
+    int64_t need[kIndPer];
+    int32_t feas[kIndPer], most[kIndPer], fq[kIndPer];
+    int64_t mb[kIndPer];
+    bool bad = false;
+#pragma unroll
+    for (int k = 0; k < kIndPer; ++k) {
+        const int64_t i = first + k * kIndNT;
+        need[k] = -1;
+        if (i < a.A && a.aU[i] >= 0) {
+            const int32_t pr = a.ap[i];
+            bad |= pr < 0;
+            need[k] = ceil_blocks(int64_t(pr) + a.aU[i], a.S);
+        }
+        feas[k] = -1;
+        fq[k] = 0;
+        most[k] = -1;
+        mb[k] = 0;
+    }
+    if (bad) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+    for (int32_t t0 = 0; t0 < a.D; t0 += kIndTile) {
+        const int32_t n = a.D - t0 < kIndTile ? a.D - t0 : kIndTile;
+        __syncthreads();
+        for (int j = threadIdx.x; j < n; j += kIndNT) {
+            lb[j] = a.beff[t0 + j];
+            lq[j] = a.qlen[t0 + j];
+        }
+        __syncthreads();
+        for (int j = 0; j < n; ++j) {
+            const int64_t B = lb[j];
+            const int32_t Q = lq[j];
+            const int32_t d = t0 + j;
+#pragma unroll
+            for (int k = 0; k < kIndPer; ++k) {
+                // ascending decoders: strict comparisons keep the lowest index on ties
+                if (need[k] <= B && (feas[k] < 0 || Q < fq[k])) { feas[k] = d; fq[k] = Q; }
+                if (most[k] < 0 || B > mb[k]) { most[k] = d; mb[k] = B; }
+            }
+        }
+    }
+    // the feasible decoder's B_eff for the flag: feasible means need <= B_eff
+#pragma unroll
+    for (int k = 0; k < kIndPer; ++k) {
+        const int64_t i = first + k * kIndNT;
+        if (i >= a.A) continue;
+        int32_t d;
+        uint8_t f;
+        if (a.aU[i] < 0) {
+            d = int32_t((a.rr_offset + i) % a.D);
+            f = 2;
+        } else if (a.policy == MAPS_POLICY_MQ && feas[k] >= 0) {
+            d = feas[k];
+            f = 1;
+        } else {
+            d = most[k];
+            f = need[k] <= mb[k] ? 1 : 0;
+        }
+        a.choice[i] = d;
+        a.need[i] = need[k];
+        a.flags[i] = f;
+    }
+}
+
+__global__ void static_copy_state(StaticArgs a) {
+    for (int32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < a.D; d += gridDim.x * blockDim.x) {
+        if (a.beff_out) a.beff_out[d] = a.beff[d];
+        if (a.q_out) a.q_out[d] = a.qlen[d];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// One arrival after another, with reservation
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ inline T wave_min_u64(T v) {
+    return wave_last(wave_incl_scan(v, ~T(0), [](T x, T y) { return x < y ? x : y; }));
+}
+
+template <typename T>
+__device__ inline T wave_max_u64(T v) {
+    return wave_last(wave_incl_scan(v, T(0), [](T x, T y) { return x > y ? x : y; }));
+}
+
+__global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
+    const int lane = threadIdx.x;
+    int64_t B[kResSlots];
+    int64_t Q[kResSlots];
+#pragma unroll
+    for (int s = 0; s < kResSlots; ++s) {
+        const int32_t d = lane + s * kWave;
+        B[s] = d < a.D ? a.beff[d] : 0;
+        Q[s] = d < a.D ? a.qlen[d] : 0;
+    }
+    bool range_bad = false, neg = false;
+    for (int64_t c0 = 0; c0 < a.A; c0 += kWave) {
+        // 64 arrivals at a time: one per lane, read out with readlane
+        const int64_t mine = c0 + lane;
+        const int32_t my_p = mine < a.A ? a.ap[mine] : 0;
+        const int32_t my_U = mine < a.A ? a.aU[mine] : -1;
+        int32_t out_d = 0;
+        int64_t out_need = -1;
+        uint8_t out_f = 0;
+        const int cnt = a.A - c0 < kWave ? int(a.A - c0) : kWave;
+        for (int j = 0; j < cnt; ++j) {
+            const int32_t pj = __builtin_amdgcn_readlane(my_p, j);
+            const int32_t Uj = __builtin_amdgcn_readlane(my_U, j);
+            int32_t best;
+            int64_t need = -1;
+            uint8_t f;
+            if (Uj < 0) {
+                best = int32_t((a.rr_offset + c0 + j) % a.D);
+                f = 2;
+            } else {
+                neg |= pj < 0;
+                need = ceil_blocks(int64_t(pj) + Uj, a.S);
+                uint64_t kf = ~uint64_t(0);
+                if (a.policy == MAPS_POLICY_MQ) {
+                    // (Q, decoder) of the feasible decoders, the smallest first
+#pragma unroll
+                    for (int s = 0; s < kResSlots; ++s) {
+                        const int32_t d = lane + s * kWave;
+                        const uint64_t k = (uint64_t(Q[s]) << 20) | uint64_t(d);
+                        if (d < a.D && need <= B[s] && k < kf) kf = k;
+                    }
+                    kf = wave_min_u64(kf);
+                }
+                if (kf != ~uint64_t(0)) {
+                    best = int32_t(kf & 0xFFFFF);
+                    f = 1;
+                } else {
+                    // largest B_eff, lowest decoder on ties: (B + 2^52) above (1023 - d)
+                    uint64_t kb = 0;
+#pragma unroll
+                    for (int s = 0; s < kResSlots; ++s) {
+                        const int32_t d = lane + s * kWave;
+                        const uint64_t k = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
+                        if (d < a.D && k > kb) kb = k;
+                    }
+                    kb = wave_max_u64(kb);
+                    best = 1023 - int32_t(kb & 1023);
+                    const int64_t bmax = int64_t(kb >> 10) - kBlockLimit;
+                    f = need <= bmax ? 1 : 0;
+                }
+            }
+            // the owning lane reserves and enqueues
+            const int owner = best % kWave, slot = best / kWave;
+#pragma unroll
+            for (int s = 0; s < kResSlots; ++s) {
+                if (s == slot && lane == owner) {
+                    if (need >= 0) B[s] -= need;
+                    Q[s] += 1;
+                    range_bad |= B[s] < -kBlockLimit || B[s] >= kBlockLimit;
+                }
+            }
+            if (lane == j) {
+                out_d = best;
+                out_need = need;
+                out_f = f;
+            }
+        }
+        if (mine < a.A) {
+            a.choice[mine] = out_d;
+            a.need[mine] = out_need;
+            a.flags[mine] = out_f;
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < kResSlots; ++s) {
+        const int32_t d = lane + s * kWave;
+        if (d < a.D) {
+            if (a.beff_out) a.beff_out[d] = B[s];
+            if (a.q_out) a.q_out[d] = int32_t(Q[s]);
+        }
+        range_bad |= d < a.D && (B[s] < -kBlockLimit || B[s] >= kBlockLimit);
+    }
+    if (range_bad) raise_error(a.dev_err, MAPS_ERR_BLOCK_RANGE);
+    if (neg) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+}
+
+// every initial B_eff inside the packed-key range
+__global__ void static_check_range(StaticArgs a) {
+    bool bad = false;
+    for (int32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < a.D; d += gridDim.x * blockDim.x)
+        bad |= a.beff[d] < -kBlockLimit || a.beff[d] >= kBlockLimit;
+    if (bad) raise_error(a.dev_err, MAPS_ERR_BLOCK_RANGE);
+}
+
+}  // namespace
+}  // namespace maps
+
+using namespace maps;
+
+extern "C" maps_status maps_rsc_state(int32_t D, const int64_t* seg_off, int64_t n_total, const int32_t* prompt,
+                                      const int32_t* generated, const int32_t* upper, const int32_t* capacity,
+                                      int32_t block_size, int64_t* b_free, int64_t* b_res, int64_t* b_eff,
+                                      uint32_t* dev_err, hipStream_t stream) {
+    if (D < 1 || n_total < 0 || block_size < 1) return MAPS_E_SIZE;
+    if (!seg_off || !capacity || !b_free || !b_res || !b_eff || !dev_err ||
+        (n_total > 0 && (!prompt || !generated || !upper)))
+        return MAPS_E_NULL;
+    hipLaunchKernelGGL(rsc_state, dim3(unsigned(D)), dim3(kRscNT), 0, stream, D, seg_off, n_total, prompt,
+                       generated, upper, capacity, block_size, b_free, b_res, b_eff, dev_err);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+extern "C" maps_status maps_place_static(int32_t D, const int64_t* b_eff, const int32_t* queue_len,
+                                         int32_t block_size, const int32_t* a_prompt, const int32_t* a_upper,
+                                         int64_t A, int32_t policy, int64_t rr_offset, int32_t reserve,
+                                         int32_t* choice, int64_t* b_need, uint8_t* flags, int64_t* b_eff_out,
+                                         int32_t* queue_out, uint32_t* dev_err, hipStream_t stream) {
+    if (D < 1 || A < 0 || block_size < 1 || rr_offset < 0 || (reserve && D > MAPS_MAX_RESERVE_DECODERS))
+        return MAPS_E_SIZE;
+    if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
+    if (!b_eff || !queue_len || !dev_err || (A > 0 && (!a_prompt || !a_upper || !choice || !b_need || !flags)))
+        return MAPS_E_NULL;
+    StaticArgs a{D, b_eff, queue_len, block_size, a_prompt, a_upper, A, policy, rr_offset, choice, b_need, flags,
+                 b_eff_out, queue_out, dev_err};
+    if (reserve) {
+        hipLaunchKernelGGL(static_check_range, dim3(unsigned((D + 255) / 256)), dim3(256), 0, stream, a);
+        MAPS_CHECK_LAUNCH();
+        hipLaunchKernelGGL(static_reserve, dim3(1), dim3(kWave), 0, stream, a);
+        MAPS_CHECK_LAUNCH();
+        return MAPS_OK;
+    }
+    if (A > 0) {
+        const int64_t blocks = (A + kIndNT * kIndPer - 1) / (kIndNT * kIndPer);
+        hipLaunchKernelGGL(static_independent, dim3(unsigned(blocks)), dim3(kIndNT), 0, stream, a);
+        MAPS_CHECK_LAUNCH();
+    }
+    if (b_eff_out || queue_out) {
+        hipLaunchKernelGGL(static_copy_state, dim3(unsigned((D + 255) / 256)), dim3(256), 0, stream, a);
+        MAPS_CHECK_LAUNCH();
+    }
+    return MAPS_OK;
+}
