@@ -143,6 +143,74 @@ def window_calibration(b, cpu: bool, calls: int = 20):
     return out
 
 
+BLOCK = 16     # tokens per KV block for Algorithm 1 on block counts (PagedAttention's default block)
+
+
+def static_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
+    """Algorithm 1 on block counts for the batch: the runtime state from the
+    residents, then every arrival against it (independent) and one after
+    another with reservation.  HIP events around each call."""
+    import numpy as np
+    import torch
+
+    import paper_2609_15359_amd as maps
+    D, A = b.decoders, b.arrivals
+    n = int(db.seg_off[-1].item())
+    err = maps.new_error_word()
+    st = [torch.empty(D, dtype=torch.int64, device="cuda") for _ in range(3)]
+    outs = (torch.empty(A, dtype=torch.int32, device="cuda"), torch.empty(A, dtype=torch.int64, device="cuda"),
+            torch.empty(A, dtype=torch.uint8, device="cuda"), torch.empty(D, dtype=torch.int64, device="cuda"),
+            torch.empty(D, dtype=torch.int32, device="cuda"))
+    calls_of = {
+        "rsc_state": lambda: maps.rsc_state(db.seg_off, db.res_prompt, db.res_gen, U_res, db.capacity, BLOCK,
+                                            dev_err=err, out=st),
+        "independent": lambda: maps.place_static(st[2], db.queue_len, BLOCK, db.arr_prompt, U_arr, dev_err=err,
+                                                 out=outs),
+        "reserve": lambda: maps.place_static(st[2], db.queue_len, BLOCK, db.arr_prompt, U_arr, reserve=True,
+                                             dev_err=err, out=outs),
+    }
+    ms = {}
+    for name, fn in calls_of.items():
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(TimingEvent(), TimingEvent()) for _ in range(calls if name != "reserve" else 3)]
+        for e0, e1 in ev:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        ms[name] = statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
+    if int(err.item()) != 0:
+        raise SystemExit(f"static placement raised {maps.error_names(int(err.item()))}")
+    feasible = float(np.mean(outs[2].cpu().numpy() & 1))
+    out = {"block_size": BLOCK, "decoders": D, "arrivals": A, "residents": n, "ms": ms,
+           "independent_pairs_per_s": D * A / (ms["independent"] * 1e-3),
+           "reserve_arrivals_per_s": A / (ms["reserve"] * 1e-3),
+           "reserve_feasible_fraction": feasible,
+           "note": "independent: every arrival against the reported state; reserve: arrivals in order, each "
+                   "reserving its B_need and joining the queue (a serial chain, one wavefront)"}
+    if cpu:
+        import oracle
+        o = oracle.Oracle()
+        Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
+        t0 = time.perf_counter()
+        _, _, be = o.rsc_state(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, BLOCK)
+        t_rsc = time.perf_counter() - t0
+        k = min(A, 20000)
+        t0 = time.perf_counter()
+        o.place_static(be, b.queue_len, BLOCK, b.arr_prompt[:k], Ua[:k])
+        t_ind = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        o.place_static(be, b.queue_len, BLOCK, b.arr_prompt, Ua, reserve=True)
+        t_res = time.perf_counter() - t0
+        out["cpu_baseline"] = {"rsc_state_ms": t_rsc * 1e3, "independent_pairs_per_s": D * k / t_ind,
+                               "reserve_arrivals_per_s": A / t_res, "cores": 1, "kind": "oracle",
+                               "sample": f"runtime state of all {n} residents; {k} arrivals independent; all {A} "
+                                         "arrivals with reservation; single-threaded C oracle"}
+    return out
+
+
 class TimingEvent:
     """A HIP event made only for timing: created with hipEventDisableSystemFence,
     so recording it costs no system-scope cache write-back and invalidation
@@ -326,8 +394,11 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(b)
-    # the next row on the path: sliding-window calibration of the same batch
+    # the next rows on the path: sliding-window calibration and Algorithm 1 on block counts, same batch
     result["window_calibration"] = window_calibration(b, cpu=not args.no_cpu_baseline)
+    nr, na = db.n_res, db.n_arr
+    result["static_placement"] = static_placement(b, db, ws.out["U"][:nr], ws.out["U"][nr:nr + na],
+                                                  cpu=not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)
 
 

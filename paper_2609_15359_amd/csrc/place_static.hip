@@ -8,11 +8,13 @@
 //                       decoders' (B_eff, Q) staged in LDS in tiles, each
 //                       thread scanning them for four arrivals at once (the
 //                       LDS reads are broadcasts);
+//   static_need         every arrival's B_need, in parallel;
 //   static_reserve      arrivals one after another, each reserving its B_need
 //                       and joining its decoder's queue before the next: one
 //                       wavefront holds the state of up to 1,024 decoders in
-//                       registers (16 per lane); per arrival a packed key per
-//                       decoder, a wavefront minimum through DPP, and the
+//                       registers (ceil(D/64) per lane, a template parameter);
+//                       per arrival two packed keys per decoder, a wavefront
+//                       minimum and maximum through DPP side by side, and the
 //                       owning lane updates its register.  The chain is serial
 //                       by definition, so this kernel runs at the latency of
 //                       one wavefront.
@@ -179,71 +181,75 @@ __device__ inline T wave_max_u64(T v) {
     return wave_last(wave_incl_scan(v, T(0), [](T x, T y) { return x > y ? x : y; }));
 }
 
+// B_need of every arrival (-1 without a bound), in parallel before the chain
+__global__ void static_need(StaticArgs a) {
+    bool bad = false;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < a.A; i += int64_t(gridDim.x) * blockDim.x) {
+        const int32_t U = a.aU[i], p = a.ap[i];
+        bad |= U >= 0 && p < 0;
+        a.need[i] = U < 0 ? -1 : ceil_blocks(int64_t(p) + U, a.S);
+    }
+    if (bad) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+}
+
+// kSlots decoders per lane: decoder lane + 64 s in slot s
+template <int kSlots>
 __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
     const int lane = threadIdx.x;
-    int64_t B[kResSlots];
-    int64_t Q[kResSlots];
+    int64_t B[kSlots];
+    int64_t Q[kSlots];
 #pragma unroll
-    for (int s = 0; s < kResSlots; ++s) {
+    for (int s = 0; s < kSlots; ++s) {
         const int32_t d = lane + s * kWave;
         B[s] = d < a.D ? a.beff[d] : 0;
         Q[s] = d < a.D ? a.qlen[d] : 0;
     }
-    bool range_bad = false, neg = false;
+    const bool mq = a.policy == MAPS_POLICY_MQ;
+    bool range_bad = false;
     for (int64_t c0 = 0; c0 < a.A; c0 += kWave) {
         // 64 arrivals at a time: one per lane, read out with readlane
         const int64_t mine = c0 + lane;
-        const int32_t my_p = mine < a.A ? a.ap[mine] : 0;
-        const int32_t my_U = mine < a.A ? a.aU[mine] : -1;
+        const int64_t my_need = mine < a.A ? a.need[mine] : -1;
         int32_t out_d = 0;
-        int64_t out_need = -1;
         uint8_t out_f = 0;
         const int cnt = a.A - c0 < kWave ? int(a.A - c0) : kWave;
         for (int j = 0; j < cnt; ++j) {
-            const int32_t pj = __builtin_amdgcn_readlane(my_p, j);
-            const int32_t Uj = __builtin_amdgcn_readlane(my_U, j);
+            const int64_t need = (int64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(my_need) >> 32), j)))
+                                  << 32) |
+                                 uint32_t(__builtin_amdgcn_readlane(int32_t(my_need), j));
             int32_t best;
-            int64_t need = -1;
             uint8_t f;
-            if (Uj < 0) {
+            if (need < 0) {
                 best = int32_t((a.rr_offset + c0 + j) % a.D);
                 f = 2;
             } else {
-                neg |= pj < 0;
-                need = ceil_blocks(int64_t(pj) + Uj, a.S);
-                uint64_t kf = ~uint64_t(0);
-                if (a.policy == MAPS_POLICY_MQ) {
-                    // (Q, decoder) of the feasible decoders, the smallest first
+                // both keys in one pass, both reductions side by side:
+                // feasible (Q, decoder), smallest first; (B_eff + 2^52, 1023 - decoder), largest first
+                uint64_t kf = ~uint64_t(0), kb = 0;
 #pragma unroll
-                    for (int s = 0; s < kResSlots; ++s) {
-                        const int32_t d = lane + s * kWave;
-                        const uint64_t k = (uint64_t(Q[s]) << 20) | uint64_t(d);
-                        if (d < a.D && need <= B[s] && k < kf) kf = k;
+                for (int s = 0; s < kSlots; ++s) {
+                    const int32_t d = lane + s * kWave;
+                    if (d < a.D) {
+                        const uint64_t k1 = (uint64_t(Q[s]) << 20) | uint64_t(d);
+                        if (mq && need <= B[s] && k1 < kf) kf = k1;
+                        const uint64_t k2 = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
+                        if (k2 > kb) kb = k2;
                     }
-                    kf = wave_min_u64(kf);
                 }
+                kf = wave_min_u64(kf);
+                kb = wave_max_u64(kb);
                 if (kf != ~uint64_t(0)) {
                     best = int32_t(kf & 0xFFFFF);
                     f = 1;
                 } else {
-                    // largest B_eff, lowest decoder on ties: (B + 2^52) above (1023 - d)
-                    uint64_t kb = 0;
-#pragma unroll
-                    for (int s = 0; s < kResSlots; ++s) {
-                        const int32_t d = lane + s * kWave;
-                        const uint64_t k = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
-                        if (d < a.D && k > kb) kb = k;
-                    }
-                    kb = wave_max_u64(kb);
                     best = 1023 - int32_t(kb & 1023);
-                    const int64_t bmax = int64_t(kb >> 10) - kBlockLimit;
-                    f = need <= bmax ? 1 : 0;
+                    f = need <= int64_t(kb >> 10) - kBlockLimit ? 1 : 0;
                 }
             }
             // the owning lane reserves and enqueues
             const int owner = best % kWave, slot = best / kWave;
 #pragma unroll
-            for (int s = 0; s < kResSlots; ++s) {
+            for (int s = 0; s < kSlots; ++s) {
                 if (s == slot && lane == owner) {
                     if (need >= 0) B[s] -= need;
                     Q[s] += 1;
@@ -252,27 +258,23 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
             }
             if (lane == j) {
                 out_d = best;
-                out_need = need;
                 out_f = f;
             }
         }
         if (mine < a.A) {
             a.choice[mine] = out_d;
-            a.need[mine] = out_need;
             a.flags[mine] = out_f;
         }
     }
 #pragma unroll
-    for (int s = 0; s < kResSlots; ++s) {
+    for (int s = 0; s < kSlots; ++s) {
         const int32_t d = lane + s * kWave;
         if (d < a.D) {
             if (a.beff_out) a.beff_out[d] = B[s];
             if (a.q_out) a.q_out[d] = int32_t(Q[s]);
         }
-        range_bad |= d < a.D && (B[s] < -kBlockLimit || B[s] >= kBlockLimit);
     }
     if (range_bad) raise_error(a.dev_err, MAPS_ERR_BLOCK_RANGE);
-    if (neg) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
 }
 
 // every initial B_eff inside the packed-key range
@@ -317,7 +319,17 @@ extern "C" maps_status maps_place_static(int32_t D, const int64_t* b_eff, const 
     if (reserve) {
         hipLaunchKernelGGL(static_check_range, dim3(unsigned((D + 255) / 256)), dim3(256), 0, stream, a);
         MAPS_CHECK_LAUNCH();
-        hipLaunchKernelGGL(static_reserve, dim3(1), dim3(kWave), 0, stream, a);
+        if (A > 0) {
+            const int64_t nblk = (A + 255) / 256;
+            hipLaunchKernelGGL(static_need, dim3(unsigned(nblk < 4096 ? nblk : 4096)), dim3(256), 0, stream, a);
+            MAPS_CHECK_LAUNCH();
+        }
+        const int slots = (D + kWave - 1) / kWave;
+        if (slots <= 1) hipLaunchKernelGGL(static_reserve<1>, dim3(1), dim3(kWave), 0, stream, a);
+        else if (slots <= 2) hipLaunchKernelGGL(static_reserve<2>, dim3(1), dim3(kWave), 0, stream, a);
+        else if (slots <= 4) hipLaunchKernelGGL(static_reserve<4>, dim3(1), dim3(kWave), 0, stream, a);
+        else if (slots <= 8) hipLaunchKernelGGL(static_reserve<8>, dim3(1), dim3(kWave), 0, stream, a);
+        else hipLaunchKernelGGL(static_reserve<kResSlots>, dim3(1), dim3(kWave), 0, stream, a);
         MAPS_CHECK_LAUNCH();
         return MAPS_OK;
     }
