@@ -13,11 +13,14 @@
 //                       and joining its decoder's queue before the next: one
 //                       wavefront holds the state of up to 1,024 decoders in
 //                       registers (ceil(D/64) per lane, a template parameter);
-//                       per arrival two packed keys per decoder, a wavefront
-//                       minimum and maximum through DPP side by side, and the
-//                       owning lane updates its register.  The chain is serial
-//                       by definition, so this kernel runs at the latency of
-//                       one wavefront.
+//                       the largest B_eff is kept from one arrival to the next
+//                       (a wavefront maximum through DPP after each
+//                       reservation), so an arrival that fits no decoder takes
+//                       it directly; a feasible shortest-queue choice takes a
+//                       wavefront minimum over every decoder.  The owning lane
+//                       updates its register.  The chain is serial by
+//                       definition, so this kernel runs at the latency of one
+//                       wavefront.
 #include "maps_internal.hpp"
 
 namespace maps {
@@ -192,7 +195,23 @@ __global__ void static_need(StaticArgs a) {
     if (bad) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
 }
 
-// kSlots decoders per lane: decoder lane + 64 s in slot s
+// Largest-B_eff key of one lane's decoders: (B_eff + 2^52) above (1023 - decoder)
+template <int kSlots>
+__device__ inline uint64_t lane_best_b(const int64_t (&B)[kSlots], int lane, int32_t D) {
+    uint64_t kb = 0;
+#pragma unroll
+    for (int s = 0; s < kSlots; ++s) {
+        const int32_t d = lane + s * kWave;
+        const uint64_t k = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
+        if (d < D && k > kb) kb = k;
+    }
+    return kb;
+}
+
+// kSlots decoders per lane: decoder lane + 64 s in slot s.  The largest B_eff
+// over all decoders is kept between arrivals (only the chosen decoder's
+// changes): an arrival whose B_need exceeds it takes that decoder at once;
+// only a feasible shortest-queue choice scans every decoder.
 template <int kSlots>
 __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
     const int lane = threadIdx.x;
@@ -206,6 +225,7 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
     }
     const bool mq = a.policy == MAPS_POLICY_MQ;
     bool range_bad = false;
+    uint64_t kb = wave_max_u64(lane_best_b<kSlots>(B, lane, a.D));
     for (int64_t c0 = 0; c0 < a.A; c0 += kWave) {
         // 64 arrivals at a time: one per lane, read out with readlane
         const int64_t mine = c0 + lane;
@@ -223,30 +243,25 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
                 best = int32_t((a.rr_offset + c0 + j) % a.D);
                 f = 2;
             } else {
-                // both keys in one pass, both reductions side by side:
-                // feasible (Q, decoder), smallest first; (B_eff + 2^52, 1023 - decoder), largest first
-                uint64_t kf = ~uint64_t(0), kb = 0;
+                const int64_t bmax = int64_t(kb >> 10) - kBlockLimit;
+                if (mq && need <= bmax) {
+                    // feasible decoders exist: (Q, decoder) among them, smallest first
+                    uint64_t kf = ~uint64_t(0);
 #pragma unroll
-                for (int s = 0; s < kSlots; ++s) {
-                    const int32_t d = lane + s * kWave;
-                    if (d < a.D) {
+                    for (int s = 0; s < kSlots; ++s) {
+                        const int32_t d = lane + s * kWave;
                         const uint64_t k1 = (uint64_t(Q[s]) << 20) | uint64_t(d);
-                        if (mq && need <= B[s] && k1 < kf) kf = k1;
-                        const uint64_t k2 = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
-                        if (k2 > kb) kb = k2;
+                        if (d < a.D && need <= B[s] && k1 < kf) kf = k1;
                     }
-                }
-                kf = wave_min_u64(kf);
-                kb = wave_max_u64(kb);
-                if (kf != ~uint64_t(0)) {
+                    kf = wave_min_u64(kf);
                     best = int32_t(kf & 0xFFFFF);
                     f = 1;
                 } else {
                     best = 1023 - int32_t(kb & 1023);
-                    f = need <= int64_t(kb >> 10) - kBlockLimit ? 1 : 0;
+                    f = need <= bmax ? 1 : 0;
                 }
             }
-            // the owning lane reserves and enqueues
+            // the owning lane reserves and enqueues; a reservation changes the largest B_eff
             const int owner = best % kWave, slot = best / kWave;
 #pragma unroll
             for (int s = 0; s < kSlots; ++s) {
@@ -256,6 +271,7 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
                     range_bad |= B[s] < -kBlockLimit || B[s] >= kBlockLimit;
                 }
             }
+            if (need >= 0) kb = wave_max_u64(lane_best_b<kSlots>(B, lane, a.D));
             if (lane == j) {
                 out_d = best;
                 out_f = f;
