@@ -73,7 +73,7 @@ enum {
                                        every workgroup of the launch at once) */
     MAPS_ERR_SEEN_RANGE = 512u,     /* a seen count outside [0, n] (sliding-window
                                        calibration) */
-    MAPS_ERR_BLOCK_RANGE = 1024u    /* an effective block count left [-2^52, 2^52)
+    MAPS_ERR_BLOCK_RANGE = 1024u    /* an effective block count left (-2^52, 2^52)
                                        during reserving placement */
 };
 

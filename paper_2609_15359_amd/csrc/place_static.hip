@@ -268,7 +268,7 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
                 if (s == slot && lane == owner) {
                     if (need >= 0) B[s] -= need;
                     Q[s] += 1;
-                    range_bad |= B[s] < -kBlockLimit || B[s] >= kBlockLimit;
+                    range_bad |= B[s] <= -kBlockLimit || B[s] >= kBlockLimit;
                 }
             }
             if (need >= 0) kb = wave_max_u64(lane_best_b<kSlots>(B, lane, a.D));
@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
 __global__ void static_check_range(StaticArgs a) {
     bool bad = false;
     for (int32_t d = blockIdx.x * blockDim.x + threadIdx.x; d < a.D; d += gridDim.x * blockDim.x)
-        bad |= a.beff[d] < -kBlockLimit || a.beff[d] >= kBlockLimit;
+        bad |= a.beff[d] <= -kBlockLimit || a.beff[d] >= kBlockLimit;
     if (bad) raise_error(a.dev_err, MAPS_ERR_BLOCK_RANGE);
 }
 
