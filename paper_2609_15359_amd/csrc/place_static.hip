@@ -174,14 +174,20 @@ __global__ void static_copy_state(StaticArgs a) {
 // ---------------------------------------------------------------------------
 // One arrival after another, with reservation
 // ---------------------------------------------------------------------------
-template <typename T>
-__device__ inline T wave_min_u64(T v) {
-    return wave_last(wave_incl_scan(v, ~T(0), [](T x, T y) { return x < y ? x : y; }));
+// 64-bit wavefront minimum and maximum as two 32-bit reductions, high word
+// first (a 32-bit DPP step is one instruction, a 64-bit one is five)
+__device__ inline uint32_t wave_max_u32(uint32_t v) {
+    return wave_last(wave_incl_scan(v, 0u, [](uint32_t x, uint32_t y) { return x > y ? x : y; }));
 }
 
-template <typename T>
-__device__ inline T wave_max_u64(T v) {
-    return wave_last(wave_incl_scan(v, T(0), [](T x, T y) { return x > y ? x : y; }));
+__device__ inline uint64_t wave_max_u64(uint64_t v) {
+    const uint32_t hi = wave_max_u32(uint32_t(v >> 32));
+    const uint32_t lo = wave_max_u32(uint32_t(v >> 32) == hi ? uint32_t(v) : 0u);
+    return (uint64_t(hi) << 32) | lo;
+}
+
+__device__ inline uint64_t wave_min_u64(uint64_t v) {
+    return ~wave_max_u64(~v);
 }
 
 // B_need of every arrival (-1 without a bound), in parallel before the chain
