@@ -50,7 +50,7 @@ def test_hand_worked_example():
 
 # (n, nb, window): chunk and run boundaries, single entries, one bucket, windows 1 .. max
 RAGGED = [(0, 3, 500), (1, 1, 1), (5, 2, 3), (4095, 7, 500), (4096, 7, 500), (4097, 40, 1600), (9000, 2, 1),
-          (20000, 7, 4096), (30001, 64, 500), (70000, 5, 2000)]
+          (20000, 7, 4096), (30001, 64, 500), (70000, 5, 2000), (50000, 1024, 500)]
 
 
 @pytest.mark.parametrize("n,nb,window", RAGGED, ids=[f"n{r[0]}-nb{r[1]}-w{r[2]}" for r in RAGGED])
