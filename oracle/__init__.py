@@ -72,6 +72,12 @@ def _declare(lib):
                                  c.c_int64, _i32p, _i32p, i64n, c.c_int32, c.c_int64,
                                  _i32p, _i64p, _i64p, _u8p, i64n, i64n]
     lib.oracle_place.restype = c.c_int
+    lib.oracle_occupancy_blocks.argtypes = [_i32p, _i32p, _i32p, c.c_int64, c.c_int32, c.c_int64, _i64p]
+    lib.oracle_occupancy_blocks.restype = c.c_int
+    lib.oracle_place_blocks.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, _i32p, c.c_int32,
+                                        c.c_int64, _i32p, _i32p, c.c_int32, c.c_int64,
+                                        _i32p, _i64p, _i64p, _u8p, i64n, i64n]
+    lib.oracle_place_blocks.restype = c.c_int
     lib.oracle_rsc_state.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, c.c_int32, _i64p, _i64p,
                                      _i64p]
     lib.oracle_rsc_state.restype = c.c_int
@@ -195,6 +201,36 @@ class Oracle:
             None if out.pair_peak is None else out.pair_peak.reshape(-1), out.base_peak)
         if rc:
             raise ValueError(f"oracle_place failed ({rc})")
+        return out
+
+    # -- projected peak in blocks (Sec. 3.3, Eq. (6)) -------------------------
+    def occupancy_blocks(self, p, g, U, S: int, T: int):
+        OB = np.zeros(T + 1, np.int64)
+        p = _i32(p)
+        rc = self.lib.oracle_occupancy_blocks(p, _i32(g), _i32(U), p.size, int(S), int(T), OB)
+        if rc:
+            raise ValueError(f"oracle_occupancy_blocks failed ({rc})")
+        return OB
+
+    def place_blocks(self, seg_off, p, g, U, capacity, queue_len, S: int, a_p, a_U, policy=POLICY_MQ,
+                     rr_offset=0, want_pairs=True):
+        """Placement with every count in blocks of S tokens (peaks, capacities
+        floor(C/S), overflow); the same result fields as place()."""
+        seg_off = _i64(seg_off)
+        D = seg_off.size - 1
+        a_p, a_U = _i32(a_p), _i32(a_U)
+        A = a_p.size
+        out = PlaceResult(
+            choice=np.zeros(A, np.int32), chosen_peak=np.zeros(A, np.int64),
+            chosen_overflow=np.zeros(A, np.int64), flags=np.zeros(A, np.uint8),
+            pair_peak=np.zeros((D, A), np.int64) if want_pairs else None,
+            base_peak=np.zeros(D, np.int64))
+        rc = self.lib.oracle_place_blocks(
+            D, seg_off, _i32(p), _i32(g), _i32(U), _i32(capacity), _i32(queue_len), int(S), A, a_p, a_U,
+            int(policy), int(rr_offset), out.choice, out.chosen_peak, out.chosen_overflow, out.flags,
+            None if out.pair_peak is None else out.pair_peak.reshape(-1), out.base_peak)
+        if rc:
+            raise ValueError(f"oracle_place_blocks failed ({rc})")
         return out
 
     # -- Algorithm 1 on block counts (Sec. 3.3, Eq. (6)) ---------------------

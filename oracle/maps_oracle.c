@@ -431,6 +431,139 @@ int oracle_place_static(int32_t D, const int64_t* b_eff_in, const int32_t* queue
 }
 
 /* ------------------------------------------------------------------------ */
+/* Projected peak in blocks (Sec. 3.3: capacity in blocks of S tokens;       */
+/* Eq. (6) counts a request's blocks as ceil(tokens / S))                    */
+/* ------------------------------------------------------------------------ */
+
+/* OB[t], t = 0..T: KV blocks held at step t by the residents still decoding,
+ * each holding ceil((p+g+t)/S) blocks while t <= R.  Step by step: from t to
+ * t+1 a request gains a block exactly when p+g+t is a multiple of S, and the
+ * requests whose last step is t leave with their blocks. */
+int oracle_occupancy_blocks(const int32_t* p, const int32_t* g, const int32_t* U, int64_t n,
+                            int32_t S, int64_t T, int64_t* OB)
+{
+    int64_t* leave_first = (int64_t*)malloc(((size_t)T + 2) * sizeof(int64_t));
+    int64_t* next = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    int64_t* active_in = (int64_t*)calloc((size_t)S, sizeof(int64_t));   /* active requests by (p+g) mod S */
+    if (!leave_first || !next || !active_in) return -2;
+    for (int64_t t = 0; t <= T + 1; ++t) leave_first[t] = -1;
+    int64_t held = 0;
+    for (int64_t r = 0; r < n; ++r) {
+        if (p[r] < 0 || g[r] < 0 || U[r] < 0) { free(leave_first); free(next); free(active_in); return -1; }
+        int64_t R = remaining(U[r], g[r]);
+        if (R > T) { free(leave_first); free(next); free(active_in); return -3; }
+        int64_t x = (int64_t)p[r] + g[r];
+        held += (x + S - 1) / S;                 /* blocks at step 0 */
+        active_in[x % S] += 1;
+        next[r] = leave_first[R];                /* requests leaving after step R */
+        leave_first[R] = r;
+    }
+    for (int64_t t = 0; t <= T; ++t) {
+        OB[t] = held;
+        for (int64_t r = leave_first[t]; r >= 0; r = next[r]) {
+            int64_t x = (int64_t)p[r] + g[r];
+            held -= (x + t + S - 1) / S;
+            active_in[x % S] -= 1;
+        }
+        /* the requests still active gain a block when p+g+t = 0 mod S */
+        held += active_in[(S - t % S) % S];
+    }
+    free(leave_first); free(next); free(active_in);
+    return 0;
+}
+
+/* Placement in blocks: peak(a, d) = max_t [OB_d[t] + [t <= U_a] ceil((p_a+t)/S)],
+ * capacity floor(C_d / S) blocks; the choice as in oracle_place. */
+int oracle_place_blocks(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                        const int32_t* U, const int32_t* capacity, const int32_t* queue_len, int32_t S,
+                        int64_t A, const int32_t* a_p, const int32_t* a_U, int32_t policy, int64_t rr_offset,
+                        int32_t* choice, int64_t* chosen_peak, int64_t* chosen_overflow,
+                        uint8_t* flags, int64_t* pair_peak, int64_t* base_peak)
+{
+    if (D < 1 || A < 0 || S < 1 || (policy != ORACLE_POLICY_MQ && policy != ORACLE_POLICY_MC)) return -1;
+    int64_t maxU = 0;
+    for (int64_t a = 0; a < A; ++a) maxU = max64(maxU, a_U[a]);
+    int32_t* feas_d = (int32_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int32_t));
+    int64_t* feas_peak = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    int32_t* fb_d = (int32_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int32_t));
+    int64_t* fb_slack = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    int64_t* fb_peak = (int64_t*)malloc((size_t)(A > 0 ? A : 1) * sizeof(int64_t));
+    if (!feas_d || !feas_peak || !fb_d || !fb_slack || !fb_peak) return -2;
+    for (int64_t a = 0; a < A; ++a) { feas_d[a] = -1; fb_d[a] = -1; }
+
+    for (int32_t d = 0; d < D; ++d) {
+        int64_t lo = seg_off[d], hi = seg_off[d + 1];
+        int64_t T = max64(max_remaining(g, U, lo, hi), maxU);
+        int64_t* OB = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        int64_t* present = (int64_t*)malloc((size_t)S * ((size_t)T + 1) * sizeof(int64_t));
+        int64_t* after = (int64_t*)malloc(((size_t)T + 1) * sizeof(int64_t));
+        if (!OB || !present || !after) return -2;
+        int rc = oracle_occupancy_blocks(p + lo, g + lo, U + lo, hi - lo, S, T, OB);
+        if (rc) return rc;
+        int64_t peak0 = 0;
+        for (int64_t t = 0; t <= T; ++t) peak0 = max64(peak0, OB[t]);
+        if (base_peak) base_peak[d] = peak0;
+        /* present[rho][u] = max_{t<=u} (OB[t] + ceil((rho+t)/S));  after[u] = max_{t>u} OB[t] */
+        for (int32_t rho = 0; rho < S; ++rho) {
+            int64_t* pr = present + (size_t)rho * ((size_t)T + 1);
+            for (int64_t t = 0; t <= T; ++t) {
+                int64_t v = OB[t] + (rho + t + S - 1) / S;
+                pr[t] = (t == 0) ? v : max64(pr[t - 1], v);
+            }
+        }
+        after[T] = 0;
+        for (int64_t t = T - 1; t >= 0; --t) after[t] = max64(after[t + 1], OB[t + 1]);
+        int64_t capB = (int64_t)capacity[d] / S;
+
+        for (int64_t a = 0; a < A; ++a) {
+            if (a_U[a] < 0) {
+                if (pair_peak) pair_peak[(int64_t)d * A + a] = -1;
+                continue;
+            }
+            /* ceil((p+t)/S) = p div S + ceil((p mod S + t)/S) */
+            int64_t P = a_p[a] / S, rho = a_p[a] % S;
+            int64_t peak = max64(P + present[(size_t)rho * ((size_t)T + 1) + a_U[a]], after[a_U[a]]);
+            int64_t slack = capB - peak;
+            if (pair_peak) pair_peak[(int64_t)d * A + a] = peak;
+            if (policy == ORACLE_POLICY_MQ && slack >= 0) {
+                if (feas_d[a] < 0 || queue_len[d] < queue_len[feas_d[a]]) {
+                    feas_d[a] = d;
+                    feas_peak[a] = peak;
+                }
+            }
+            if (fb_d[a] < 0 || slack > fb_slack[a]) {
+                fb_d[a] = d;
+                fb_slack[a] = slack;
+                fb_peak[a] = peak;
+            }
+        }
+        free(OB); free(present); free(after);
+    }
+
+    for (int64_t a = 0; a < A; ++a) {
+        if (a_U[a] < 0) {
+            choice[a] = (int32_t)((rr_offset + a) % D);
+            chosen_peak[a] = -1;
+            chosen_overflow[a] = 0;
+            flags[a] = 2;
+        } else if (policy == ORACLE_POLICY_MQ && feas_d[a] >= 0) {
+            choice[a] = feas_d[a];
+            chosen_peak[a] = feas_peak[a];
+            chosen_overflow[a] = 0;
+            flags[a] = 1;
+        } else {
+            int64_t c = (int64_t)capacity[fb_d[a]] / S;
+            choice[a] = fb_d[a];
+            chosen_peak[a] = fb_peak[a];
+            chosen_overflow[a] = max64(0, fb_peak[a] - c);
+            flags[a] = (fb_peak[a] <= c) ? 1 : 0;
+        }
+    }
+    free(feas_d); free(feas_peak); free(fb_d); free(fb_slack); free(fb_peak);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Local order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10))           */
 /* ------------------------------------------------------------------------ */
 

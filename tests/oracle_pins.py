@@ -430,6 +430,93 @@ def pin_static_reduces_to_projection(o):
 
 
 # ---------------------------------------------------------------------------
+# projected peak in blocks (Sec. 3.3, Eq. (6))
+# ---------------------------------------------------------------------------
+
+def py_peak_blocks(p, g, U, S, extra=()):
+    """Brute force: every step t, every request's blocks ceil(tokens / S)."""
+    R = [py_remaining(u, gg) for u, gg in zip(U, g)]
+    T = max(list(R) + [int(u) for _, u in extra] + [0])
+    best = 0
+    for t in range(T + 1):
+        occ = sum(-(-(int(pp) + int(gg) + t) // S) for pp, gg, r in zip(p, g, R) if t <= r)
+        occ += sum(-(-(int(ap) + t) // S) for ap, au in extra if t <= au)
+        best = max(best, occ)
+    return best
+
+
+def pin_blocks_golden(o):
+    gd = golden("place_blocks_hand.json")
+    OB = o.occupancy_blocks(gd["p"], gd["g"], gd["U"], gd["S"], gd["occupancy_T"])
+    assert OB.tolist() == gd["occupancy"], OB
+    r = o.place_blocks(gd["seg_off"], gd["p"], gd["g"], gd["U"], gd["capacity"], gd["queue_len"], gd["S"],
+                       gd["a_p"], gd["a_U"])
+    assert r.pair_peak.tolist() == gd["pair_peak"] and r.choice.tolist() == gd["choice"], (r.pair_peak, r.choice)
+    assert r.chosen_peak.tolist() == gd["chosen_peak"] and r.chosen_overflow.tolist() == gd["chosen_overflow"]
+    assert r.flags.tolist() == gd["flags"] and r.base_peak.tolist() == gd["base_peak"]
+
+
+def pin_blocks_bruteforce(o):
+    rng = _rng(51)
+    for trial in range(40):
+        S = int(rng.choice([1, 2, 3, 16, 37]))
+        D = int(rng.integers(1, 4))
+        seg, p, g, U = _tiny_decoders(rng, D, 6, 60, 80)
+        A = int(rng.integers(1, 8))
+        a_p = rng.integers(0, 80, size=A)
+        a_U = rng.integers(-1, 70, size=A)
+        cap = rng.integers(0, 60, size=D)
+        r = o.place_blocks(seg, p, g, U, cap, np.zeros(D, np.int32), S, a_p, a_U)
+        for d in range(D):
+            sl = slice(seg[d], seg[d + 1])
+            assert r.base_peak[d] == py_peak_blocks(p[sl], g[sl], U[sl], S), (trial, d)
+            for a in range(A):
+                want = -1 if a_U[a] < 0 else py_peak_blocks(p[sl], g[sl], U[sl], S, [(a_p[a], a_U[a])])
+                assert r.pair_peak[d, a] == want, (trial, d, a, S)
+
+
+def pin_blocks_reduce_to_tokens(o):
+    """Block size 1 is the token rule, output for output."""
+    rng = _rng(52)
+    for trial in range(10):
+        D = int(rng.integers(1, 6))
+        seg, p, g, U = _tiny_decoders(rng, D, 20, 300, 400)
+        A = 40
+        a_p = rng.integers(0, 400, size=A)
+        a_U = rng.integers(-1, 300, size=A)
+        cap = rng.integers(0, 3000, size=D)
+        Q = rng.integers(0, 3, size=D)
+        for policy in (0, 1):
+            rb = o.place_blocks(seg, p, g, U, cap, Q, 1, a_p, a_U, policy, 9)
+            rt = o.place(seg, p, g, U, cap, Q, a_p, a_U, policy, 9)
+            for f in ("choice", "chosen_peak", "chosen_overflow", "flags", "pair_peak", "base_peak"):
+                assert np.array_equal(getattr(rb, f), getattr(rt, f)), (trial, policy, f)
+
+
+def pin_blocks_invariants(o):
+    """base <= peak <= base + ceil((p+U)/S); peak >= ceil((p+U)/S); peak in
+    blocks >= ceil(peak in tokens / S); monotone in p and U."""
+    rng = _rng(53)
+    seg, p, g, U = _tiny_decoders(rng, 4, 30, 500, 600)
+    A = 200
+    a_p = rng.integers(0, 600, size=A)
+    a_U = rng.integers(0, 500, size=A)
+    cap = np.full(4, 10**6)
+    Q = np.zeros(4, np.int32)
+    for S in (4, 16):
+        rb = o.place_blocks(seg, p, g, U, cap, Q, S, a_p, a_U)
+        rt = o.place(seg, p, g, U, cap, Q, a_p, a_U)
+        need = -(-(a_p.astype(np.int64) + a_U) // S)
+        for d in range(4):
+            pk = rb.pair_peak[d]
+            assert np.all(pk >= rb.base_peak[d]) and np.all(pk <= rb.base_peak[d] + need) and np.all(pk >= need)
+            assert np.all(pk >= -(-rt.pair_peak[d] // S))
+        r2 = o.place_blocks(seg, p, g, U, cap, Q, S, a_p + 5, a_U)
+        r3 = o.place_blocks(seg, p, g, U, cap, Q, S, a_p, a_U + 7)
+        assert np.all(r2.pair_peak >= rb.pair_peak) and np.all(r3.pair_peak >= rb.pair_peak)
+
+
+# ---------------------------------------------------------------------------
 # occupancy and placement (Sec. 3.3, App. A, Algorithm 1)
 # ---------------------------------------------------------------------------
 
@@ -657,6 +744,7 @@ ALL_PINS = [
     pin_window_coverage,
     pin_static_golden, pin_static_bruteforce, pin_static_water_filling, pin_static_state_and_invariants,
     pin_static_reduces_to_projection,
+    pin_blocks_golden, pin_blocks_bruteforce, pin_blocks_reduce_to_tokens, pin_blocks_invariants,
     pin_place_golden, pin_occupancy_bruteforce, pin_place_bruteforce, pin_place_closed_forms,
     pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
     pin_local_order_golden, pin_local_order_bruteforce,

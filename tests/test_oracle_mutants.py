@@ -73,6 +73,15 @@ MUTANTS = [
     ("rsc_negative_reservation", "res += max64(demand - now, 0);", "res += demand - now;"),
     ("rsc_capacity_rounded_up", "b_free[d] = (int64_t)capacity[d] / S - held;",
      "b_free[d] = ceil_div(capacity[d], S) - held;"),
+    ("blocks_gain_wrong_residue", "held += active_in[(S - t % S) % S];", "held += active_in[t % S];"),
+    ("blocks_leave_one_late", "held -= (x + t + S - 1) / S;", "held -= (x + t + S) / S;"),
+    ("blocks_start_floor", "held += (x + S - 1) / S;                 /* blocks at step 0 */",
+     "held += x / S;                 /* blocks at step 0 */"),
+    ("blocks_arrival_floor", "int64_t v = OB[t] + (rho + t + S - 1) / S;", "int64_t v = OB[t] + (rho + t) / S;"),
+    ("blocks_capacity_rounded_up", "int64_t capB = (int64_t)capacity[d] / S;",
+     "int64_t capB = ((int64_t)capacity[d] + S - 1) / S;"),
+    ("blocks_prompt_residue_dropped", "int64_t P = a_p[a] / S, rho = a_p[a] % S;",
+     "int64_t P = a_p[a] / S, rho = 0;"),
     ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
      "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
 ]
