@@ -93,6 +93,10 @@ enum {
 /* Most decoders that maps_place_static accepts with reservation. */
 #define MAPS_MAX_RESERVE_DECODERS 1024
 
+/* Largest u_max and block size of the placement in blocks. */
+#define MAPS_MAX_BLOCKS_U_MAX 131072
+#define MAPS_MAX_BLOCK_SIZE 64
+
 /* Placement policies: minimum queue among feasible decoders with the largest
  * slack as fallback (Sec. 3.3 and Algorithm 1), or largest slack alone (the
  * maximum-capacity ablation of Sec. 4). */
@@ -272,6 +276,39 @@ maps_status maps_place_static(int32_t D, const int64_t* b_eff, const int32_t* qu
                               int64_t rr_offset, int32_t reserve, int32_t* choice, int64_t* b_need,
                               uint8_t* flags, int64_t* b_eff_out, int32_t* queue_out, uint32_t* dev_err,
                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 3c. Projected placement in blocks (Sec. 3.3: capacity in blocks of S      */
+/*     tokens; Eq. (6): a request holds ceil(tokens / S) blocks)             */
+/* ------------------------------------------------------------------------ */
+/*
+ * maps_project and maps_place with every count in blocks of S tokens: a
+ * resident (p, g, U) holds ceil((p+g+t)/S) blocks at future step t while
+ * t <= R = max(U-g, 0), an arrival (p, U) ceil((p+t)/S) while t <= U, and
+ *   peak(a, d) = max_t [OB_d(t) + [t <= U_a] ceil((p_a+t)/S)]  (blocks),
+ * against floor(capacity[d] / S) blocks; the choice, outputs and flags are
+ * those of maps_place in blocks (chosen_peak, chosen_overflow, pair_peak).
+ * With S = 1 every output equals the token path's.
+ * maps_project_blocks writes the decoders' block snapshot (caller buffer of
+ * maps_blocks_snapshot_bytes(D, n_total, u_max, S) bytes, valid for
+ * maps_place_blocks with the same seg_off, D, n_total, u_max and S) and the
+ * base peaks in blocks.  maps_place_blocks writes every pair peak into
+ * pair_peak[D][A] (required) and then the choices.  1 <= S <=
+ * MAPS_MAX_BLOCK_SIZE, 0 <= u_max <= MAPS_MAX_BLOCKS_U_MAX.
+ * dev_err bits: NEG_LEN, BOUND_RANGE, SEG_OFFSETS, INT32_RANGE (as
+ * maps_project).  Host errors: NULL, SIZE, BUFFER, POLICY, HIP.
+ */
+size_t maps_blocks_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max, int32_t block_size);
+maps_status maps_project_blocks(int32_t D, const int64_t* seg_off, const int32_t* prompt,
+                                const int32_t* generated, const int32_t* upper, int64_t n_total,
+                                int32_t u_max, int32_t block_size, void* snapshot, size_t snapshot_bytes,
+                                int32_t* base_peak, uint32_t* dev_err, hipStream_t stream);
+maps_status maps_place_blocks(const void* snapshot, const int64_t* seg_off, int32_t D, int64_t n_total,
+                              int32_t u_max, int32_t block_size, const int32_t* capacity,
+                              const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
+                              int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
+                              int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
+                              int32_t* pair_peak, uint32_t* dev_err, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 4. Local order and admission (Sec. 3.3, Eq. (7); App. A, Eq. (10))       */

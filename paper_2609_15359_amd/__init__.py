@@ -31,6 +31,8 @@ ERR_BITS = {
     512: "SEEN_RANGE", 1024: "BLOCK_RANGE",
 }
 MAX_RESERVE_DECODERS = 1024
+MAX_BLOCKS_U_MAX = 131072
+MAX_BLOCK_SIZE = 64
 MAX_WINDOW = 4096
 MAX_WINDOW_BUCKETS = 1024
 MAX_U_MAX = (1 << 24) - 64
@@ -49,6 +51,10 @@ _SIGNATURES = {
     "maps_calibrate_window_workspace_size": (_sz, [_i64, _i32]),
     "maps_calibrate_window": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp,
                                      _vp, _vp, _sz, _vp]),
+    "maps_blocks_snapshot_bytes": (_sz, [_i32, _i64, _i32, _i32]),
+    "maps_project_blocks": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
+    "maps_place_blocks": (_i32, [_vp, _vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp,
+                                 _vp, _vp, _vp, _vp, _vp]),
     "maps_rsc_state": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp]),
     "maps_place_static": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp, _i64, _i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp,
                                  _vp, _vp]),
@@ -320,6 +326,72 @@ def local_order(snapshot: Snapshot, capacity, q_off, q_prompt, q_upper, q_wait_m
                                     _ptr(err), None, 0, _stream(dev))
     _check(st, "maps_local_order")
     return order, admitted, err
+
+
+# ---------------------------------------------------------------------------
+# 3c. projected placement in blocks
+# ---------------------------------------------------------------------------
+
+@dataclass
+class BlockSnapshot:
+    data: torch.Tensor      # uint8 device buffer
+    seg_off: torch.Tensor   # the residents' segment offsets it was built from
+    D: int
+    n_total: int
+    u_max: int
+    block_size: int
+
+
+def project_blocks(seg_off, prompt, generated, upper, u_max: int, block_size: int, dev_err=None, base_peak=None):
+    """Block snapshot of D decoders and their base peaks in blocks."""
+    seg_off = _dev(seg_off, torch.int64, "seg_off")
+    dev = seg_off.device
+    D = seg_off.numel() - 1
+    n = prompt.numel()
+    for name, t in (("prompt", prompt), ("generated", generated), ("upper", upper)):
+        _dev(t, torch.int32, name)
+        if t.numel() != n:
+            raise MapsError("prompt, generated and upper differ in length")
+    lib = library()
+    nbytes = lib.maps_blocks_snapshot_bytes(D, n, int(u_max), int(block_size))
+    if nbytes == 0:
+        raise MapsError("D, u_max or block_size out of range for the block snapshot")
+    snap = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    base = torch.empty(D, dtype=torch.int32, device=dev) if base_peak is None else base_peak
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = lib.maps_project_blocks(D, _ptr(seg_off), _ptr(prompt), _ptr(generated), _ptr(upper), n, int(u_max),
+                                 int(block_size), _ptr(snap), nbytes, _ptr(base), _ptr(err), _stream(dev))
+    _check(st, "maps_project_blocks")
+    return BlockSnapshot(snap, seg_off, D, n, int(u_max), int(block_size)), base, err
+
+
+def place_blocks(snapshot: BlockSnapshot, capacity, queue_len, a_prompt, a_upper, policy: int = POLICY_MQ,
+                 rr_offset: int = 0, dev_err=None, out: Placement | None = None) -> Placement:
+    """Placement with peaks, capacities floor(C/S) and overflow in blocks; the
+    pair matrix [D][A] is always written."""
+    capacity = _dev(capacity, torch.int32, "capacity")
+    dev = capacity.device
+    queue_len = _dev(queue_len, torch.int32, "queue_len")
+    a_prompt = _dev(a_prompt, torch.int32, "a_prompt")
+    a_upper = _dev(a_upper, torch.int32, "a_upper")
+    D, A = snapshot.D, a_prompt.numel()
+    if capacity.numel() != D or queue_len.numel() != D or a_upper.numel() != A:
+        raise MapsError("capacity/queue_len must have D entries and a_upper A entries")
+    if out is None:
+        out = Placement(
+            choice=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_peak=torch.empty(A, dtype=torch.int32, device=dev),
+            chosen_overflow=torch.empty(A, dtype=torch.int32, device=dev),
+            flags=torch.empty(A, dtype=torch.uint8, device=dev),
+            pair_peak=torch.empty((D, A), dtype=torch.int32, device=dev),
+            dev_err=new_error_word(dev) if dev_err is None else dev_err)
+    st = library().maps_place_blocks(_ptr(snapshot.data), _ptr(snapshot.seg_off), D, snapshot.n_total,
+                                     snapshot.u_max, snapshot.block_size, _ptr(capacity), _ptr(queue_len),
+                                     _ptr(a_prompt), _ptr(a_upper), A, int(policy), int(rr_offset), _ptr(out.choice),
+                                     _ptr(out.chosen_peak), _ptr(out.chosen_overflow), _ptr(out.flags),
+                                     _ptr(out.pair_peak), _ptr(out.dev_err), _stream(dev))
+    _check(st, "maps_place_blocks")
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -1,0 +1,440 @@
+// Projected placement in blocks of S tokens (Sec. 3.3: KV capacity counted in
+// blocks; Eq. (6): a request's blocks are ceil(tokens / S)) on gfx950.
+//
+// A resident with x = p + g tokens holds ceil((x + t)/S) blocks at step t while
+// t <= R.  With x = X S + xi and t = V S + u (0 <= xi, u < S),
+//   ceil((x + t)/S) = X + V + [xi + u >= 1] + [xi + u >= S + 1],
+// so over the residents still active at t (those with R >= t)
+//   OB(t) = sum X + N V + N - [u = 0] #{xi = 0} + #{xi >= S + 1 - u}.
+// Per event tau_e (a distinct remaining length) the snapshot keeps N_e,
+// sum X and the counts G_e[c] = #{xi >= c} of the residents with R >= tau_e.
+// Between events OB and an arrival's ceil((p + t)/S) only grow, so for an
+// arrival (p, U), p = P S + rho, with j = #{events < U}:
+//   peak = max( P + PMX_rho[j],                      events below U
+//               OB(U) + P + ceil((rho + U)/S),         U itself (active set of event j)
+//               SMX[first event above U] ),            after U
+//   PMX_rho[j] = max_{i < j} (OB(tau_i) + ceil((rho + tau_i)/S)),  SMX[j] = max_{i >= j} OB(tau_i).
+//
+//   project_blocks   one workgroup per decoder: event bitmap and ranks in LDS,
+//                    per-event counters by device atomics in the decoder's
+//                    slice, suffix scans, OB at every event, S prefix-max
+//                    scans and one suffix-max scan;
+//   blocks_pairs     one workgroup per (decoder, 1,024 arrivals): every pair's
+//                    peak from the slice (read through L2) into the matrix;
+//   blocks_finish    per arrival: the choice over the matrix column.
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace {
+
+constexpr int kPbNT = 1024;
+constexpr int kPairsNT = 256;
+constexpr int kPairsPer = 4;
+constexpr int kFinNT = 256;
+
+// Decoder slice: W rank words {bits, events before}, then per event e = 0..E
+// (E+1 records, the last one for "no resident left") the arrays
+//   tau[e] (int32), N[e] (int32), SX[e] (int64), OB[e] (int32), SMX[e] (int32),
+//   G[e][c-1] = #{xi >= c} for c = 1..S-1 (int32), PMX[e][rho] (int32),
+// each of n_d + 1 entries (E <= n_d).
+struct BlkLayout {
+    int32_t D, u_max, S, W;
+    int64_t n_total;
+    size_t rec;        // bytes per event record slot summed over the arrays
+    size_t hdr_bytes;  // decoder headers
+    size_t bytes;
+};
+
+struct BlkHeader {
+    int64_t slice;     // byte offset of the decoder's slice
+    int32_t E;
+    int32_t base;      // max_t OB(t)
+};
+
+__host__ __device__ inline BlkLayout blk_layout(int32_t D, int64_t n_total, int32_t u_max, int32_t S) {
+    BlkLayout L;
+    L.D = D;
+    L.u_max = u_max;
+    L.S = S;
+    L.W = (((u_max + 1) / 32 + 1) + 1) & ~1;
+    L.n_total = n_total;
+    L.rec = (size_t(4 + 4 + 8 + 4 + 4) + size_t(S - 1) * 4 + size_t(S) * 4 + 15) & ~size_t(15);   // 16-byte slices
+    L.hdr_bytes = align256(size_t(D) * sizeof(BlkHeader));
+    // slice d starts at hdr + d * (8 W + 8 * 16) + seg_off[d] * (rec) with room for n_d + 1 records
+    L.bytes = L.hdr_bytes + size_t(D) * (size_t(L.W) * 8 + 8 * 16 + L.rec) + size_t(n_total) * L.rec + 256;
+    return L;
+}
+
+struct BlkSlice {
+    uint2* rank;
+    int32_t* tau;
+    int32_t* N;
+    int64_t* SX;
+    int32_t* OB;
+    int32_t* SMX;
+    int32_t* G;      // [cap][S-1]
+    int32_t* PMX;    // [cap][S]
+};
+
+// Arrays of a slice with room for `cap` records (cap = n_d + 1).
+__host__ __device__ inline BlkSlice blk_slice(char* base, const BlkLayout& L, int64_t cap) {
+    BlkSlice s;
+    char* q = base;
+    s.rank = reinterpret_cast<uint2*>(q);
+    q += size_t(L.W) * 8;
+    s.SX = reinterpret_cast<int64_t*>(q);
+    q += size_t(cap) * 8;
+    s.tau = reinterpret_cast<int32_t*>(q);
+    q += size_t(cap) * 4;
+    s.N = reinterpret_cast<int32_t*>(q);
+    q += size_t(cap) * 4;
+    s.OB = reinterpret_cast<int32_t*>(q);
+    q += size_t(cap) * 4;
+    s.SMX = reinterpret_cast<int32_t*>(q);
+    q += size_t(cap) * 4;
+    s.G = reinterpret_cast<int32_t*>(q);
+    q += size_t(cap) * size_t(L.S - 1) * 4;
+    s.PMX = reinterpret_cast<int32_t*>(q);
+    return s;
+}
+
+__host__ __device__ inline int64_t blk_slice_offset(const BlkLayout& L, int32_t d, int64_t seg_lo) {
+    return int64_t(L.hdr_bytes) + int64_t(d) * (int64_t(L.W) * 8 + 8 * 16 + int64_t(L.rec)) + seg_lo * int64_t(L.rec);
+}
+
+// ceil((r + t) / S) for 0 <= r < S, t >= 0
+__device__ inline int64_t ceil_plus(int64_t r, int64_t t, int64_t S) { return (r + t + S - 1) / S; }
+
+// OB at step t from the suffix data of the active set (N, SX, G of the event
+// the step lands on); 64-bit.
+__device__ inline int64_t occupancy_at(int64_t t, int64_t S, int64_t N, int64_t SX, const int32_t* G) {
+    const int64_t V = t / S, u = t % S;
+    int64_t ob = SX + N * V + N;
+    if (u == 0) ob -= N - (S > 1 ? G[0] : 0);          // #{xi = 0} = N - #{xi >= 1}
+    if (u >= 2) ob += G[S - u];                          // #{xi >= S + 1 - u}, stored at c - 1
+    return ob;
+}
+
+// Phase boundary for the slice in HBM: every thread's stores and atomics are
+// done, and each thread's vector L1 is invalidated before it reads values
+// that other threads wrote or that device atomics produced in L2.
+__device__ inline void sync_global() {
+    __syncthreads();
+    __threadfence();
+}
+
+struct ProjArgs {
+    BlkLayout L;
+    const int64_t* seg_off;
+    const int32_t* p;
+    const int32_t* g;
+    const int32_t* U;
+    char* snap;
+    int32_t* base_peak;
+    uint32_t* dev_err;
+};
+
+__global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
+    extern __shared__ uint32_t bits[];               // W bit words, then W counts of events before each
+    __shared__ int64_t red64[kPbNT / kWave];
+    __shared__ uint32_t red32[kPbNT / kWave];
+    const BlkLayout& L = a.L;
+    uint32_t* wpre = bits + L.W;
+    const int d = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int64_t lo = a.seg_off[d], hi = a.seg_off[d + 1];
+    BlkHeader* hdr = reinterpret_cast<BlkHeader*>(a.snap);
+    if (!(0 <= lo && lo <= hi && hi <= L.n_total)) {
+        if (tid == 0) {
+            raise_error(a.dev_err, MAPS_ERR_SEG_OFFSETS);
+            hdr[d].E = 0;
+            hdr[d].base = 0;
+            hdr[d].slice = -1;
+            a.base_peak[d] = 0;
+        }
+        return;
+    }
+    const int64_t n = hi - lo, cap = n + 1;
+    const int64_t S = L.S;
+    const int64_t off = blk_slice_offset(L, d, lo);
+    BlkSlice s = blk_slice(a.snap + off, L, cap);
+
+    // 1. event bitmap over the step axis
+    for (int w = tid; w < L.W; w += kPbNT) bits[w] = 0u;
+    __syncthreads();
+    bool neg = false, range = false;
+    for (int64_t r = lo + tid; r < hi; r += kPbNT) {
+        int32_t pr = a.p[r], gr = a.g[r], ur = a.U[r];
+        neg |= (pr < 0) | (gr < 0) | (ur < 0);
+        gr = gr < 0 ? 0 : gr;
+        ur = ur < 0 ? 0 : ur;
+        int64_t R = int64_t(ur) - gr;
+        R = R > 0 ? R : 0;
+        if (R > L.u_max) { range = true; R = L.u_max; }
+        atomicOr(&bits[R >> 5], 1u << (R & 31));
+    }
+    if (neg) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+    if (range) raise_error(a.dev_err, MAPS_ERR_BOUND_RANGE);
+    __syncthreads();
+
+    // 2. ranks: events before each word; the rank words and event times
+    const uint32_t E = block_scan<kPbNT, false, false, true, uint32_t>(
+        L.W, 0u, [&](int64_t w) { return uint32_t(__popc(bits[w])); },
+        [&](int64_t w, uint32_t v) {
+            wpre[w] = v;
+            s.rank[w] = make_uint2(bits[w], v);
+        },
+        red32);
+    for (int w = tid; w < L.W; w += kPbNT) {
+        uint32_t b = bits[w], e = wpre[w];
+        while (b) {
+            s.tau[e++] = int32_t(w * 32 + (__ffs(b) - 1));
+            b &= b - 1u;
+        }
+    }
+    // counters of every record (the one past the last event stays zero)
+    for (int64_t e = tid; e <= int64_t(E); e += kPbNT) {
+        s.N[e] = 0;
+        s.SX[e] = 0;
+        for (int c = 0; c + 1 < S; ++c) s.G[e * (S - 1) + c] = 0;
+    }
+    sync_global();
+
+    // 3. each resident adds itself to its event: 1, X = x div S, and its class xi = x mod S
+    for (int64_t r = lo + tid; r < hi; r += kPbNT) {
+        int32_t pr = a.p[r], gr = a.g[r], ur = a.U[r];
+        pr = pr < 0 ? 0 : pr;
+        gr = gr < 0 ? 0 : gr;
+        ur = ur < 0 ? 0 : ur;
+        int64_t R = int64_t(ur) - gr;
+        R = R > 0 ? R : 0;
+        R = R > L.u_max ? L.u_max : R;
+        const uint32_t e = wpre[R >> 5] + __popc(bits[R >> 5] & ((1u << (R & 31)) - 1u));
+        const int64_t x = int64_t(pr) + gr;
+        atomicAdd(&s.N[e], 1);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&s.SX[e]), (unsigned long long)(x / S));
+        const int xi = int(x % S);
+        if (xi >= 1) atomicAdd(&s.G[e * (S - 1) + (xi - 1)], 1);
+    }
+    sync_global();
+
+    // 4. suffix sums over the events (record E is zero): N, SX and every class count
+    const int64_t len = int64_t(E) + 1;
+    block_scan<kPbNT, false, true, false, int32_t>(
+        len, 0, [&](int64_t e) { return s.N[e]; }, [&](int64_t e, int32_t v) { s.N[e] = v; },
+        reinterpret_cast<int32_t*>(red32));
+    block_scan<kPbNT, false, true, false, int64_t>(
+        len, int64_t(0), [&](int64_t e) { return s.SX[e]; }, [&](int64_t e, int64_t v) { s.SX[e] = v; }, red64);
+    for (int c = 0; c + 1 < S; ++c)
+        block_scan<kPbNT, false, true, false, int32_t>(
+            len, 0, [&](int64_t e) { return s.G[e * (S - 1) + c]; },
+            [&](int64_t e, int32_t v) { s.G[e * (S - 1) + c] = v; }, reinterpret_cast<int32_t*>(red32));
+    sync_global();
+    // counts by class -> counts of classes >= c
+    for (int64_t e = tid; e < len; e += kPbNT) {
+        int32_t acc = 0;
+        for (int c = int(S) - 2; c >= 0; --c) {
+            acc += s.G[e * (S - 1) + c];
+            s.G[e * (S - 1) + c] = acc;
+        }
+    }
+    sync_global();
+
+    // 5. occupancy at every event (record E: nobody left)
+    bool big = false;
+    for (int64_t e = tid; e < len; e += kPbNT) {
+        int64_t ob = 0;
+        if (e < int64_t(E)) ob = occupancy_at(s.tau[e], S, s.N[e], s.SX[e], s.G + e * (S - 1));
+        big |= ob + 2 * int64_t(L.u_max) / S + 2 > int64_t(INT32_MAX) / 2;
+        s.OB[e] = int32_t(ob > INT32_MAX ? INT32_MAX : ob);
+    }
+    if (big) raise_error(a.dev_err, MAPS_ERR_INT32_RANGE);
+    sync_global();
+
+    // 6. prefix maxima per residue class (exclusive: events below), suffix maximum
+    for (int rho = 0; rho < S; ++rho)
+        block_scan<kPbNT, true, false, true, int32_t>(
+            len, 0,
+            [&](int64_t e) {
+                return e < int64_t(E) ? int32_t(s.OB[e] + ceil_plus(rho, s.tau[e], S)) : 0;
+            },
+            [&](int64_t e, int32_t v) { s.PMX[e * S + rho] = v; }, reinterpret_cast<int32_t*>(red32));
+    const int32_t base = block_scan<kPbNT, true, true, false, int32_t>(
+        len, 0, [&](int64_t e) { return s.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
+        reinterpret_cast<int32_t*>(red32));
+    if (tid == 0) {
+        hdr[d].slice = off;
+        hdr[d].E = int32_t(E);
+        hdr[d].base = base;
+        a.base_peak[d] = base;
+    }
+}
+
+struct PairArgs {
+    BlkLayout L;
+    const char* snap;
+    const int32_t* ap;
+    const int32_t* aU;
+    int64_t A;
+    const int64_t* seg_off;
+    int32_t* pair;
+};
+
+// Every pair's peak in blocks
+__global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
+    const BlkLayout& L = a.L;
+    const int d = blockIdx.y;
+    const BlkHeader h = reinterpret_cast<const BlkHeader*>(a.snap)[d];
+    const int64_t S = L.S;
+    const int64_t first = int64_t(blockIdx.x) * (kPairsNT * kPairsPer) + threadIdx.x;
+    if (h.slice < 0) {
+        for (int k = 0; k < kPairsPer; ++k) {
+            const int64_t i = first + k * kPairsNT;
+            if (i < a.A) a.pair[int64_t(d) * a.A + i] = -1;
+        }
+        return;
+    }
+    const int64_t cap = a.seg_off[d + 1] - a.seg_off[d] + 1;
+    BlkSlice s = blk_slice(const_cast<char*>(a.snap) + h.slice, L, cap);
+    const int32_t E = h.E;
+    const int32_t tmax = 32 * L.W - 1;
+#pragma unroll
+    for (int k = 0; k < kPairsPer; ++k) {
+        const int64_t i = first + k * kPairsNT;
+        if (i >= a.A) continue;
+        const int32_t U = a.aU[i];
+        int32_t out = -1;
+        if (U >= 0) {
+            const int64_t p = a.ap[i] < 0 ? 0 : a.ap[i];
+            const int32_t tc = U < tmax ? U : tmax;
+            const uint2 w = s.rank[tc >> 5];
+            int64_t j = int64_t(w.y) + __popc(w.x & ((1u << (tc & 31)) - 1u));
+            j = j < E ? j : E;
+            const int64_t P = p / S, rho = p % S;
+            const int64_t left = P + s.PMX[j * S + rho];
+            int64_t at = P + ceil_plus(rho, U, S);
+            if (j < E) at += occupancy_at(U, S, s.N[j], s.SX[j], s.G + j * (S - 1));
+            const int64_t after = (j < E && s.tau[j] == U) ? s.SMX[j + 1] : s.SMX[j];
+            int64_t pk = left > at ? left : at;
+            pk = pk > after ? pk : after;
+            out = int32_t(pk > INT32_MAX ? INT32_MAX : pk);
+        }
+        a.pair[int64_t(d) * a.A + i] = out;
+    }
+}
+
+struct FinArgs {
+    int32_t D;
+    int32_t S;
+    const int32_t* cap;
+    const int32_t* qlen;
+    const int32_t* aU;
+    int64_t A;
+    int32_t policy;
+    int64_t rr_offset;
+    const int32_t* pair;
+    int32_t* choice;
+    int32_t* chosen_peak;
+    int32_t* chosen_overflow;
+    uint8_t* flags;
+};
+
+// Algorithm 1's choice per arrival over its column of the matrix
+__global__ __launch_bounds__(kFinNT) void blocks_finish(FinArgs a) {
+    const int64_t stride = int64_t(gridDim.x) * kFinNT;
+    for (int64_t i = int64_t(blockIdx.x) * kFinNT + threadIdx.x; i < a.A; i += stride) {
+        if (a.aU[i] < 0) {
+            a.choice[i] = int32_t((a.rr_offset + i) % a.D);
+            a.chosen_peak[i] = -1;
+            a.chosen_overflow[i] = 0;
+            a.flags[i] = 2;
+            continue;
+        }
+        int32_t feas = -1, fq = 0, fpk = 0, fb = -1, fbpk = 0;
+        int64_t fbslack = 0;
+        for (int32_t d = 0; d < a.D; ++d) {
+            const int32_t pk = a.pair[int64_t(d) * a.A + i];
+            const int64_t slack = int64_t(a.cap[d] / a.S) - pk;
+            if (a.policy == MAPS_POLICY_MQ && slack >= 0 && (feas < 0 || a.qlen[d] < fq)) {
+                feas = d;
+                fq = a.qlen[d];
+                fpk = pk;
+            }
+            if (fb < 0 || slack > fbslack) {
+                fb = d;
+                fbslack = slack;
+                fbpk = pk;
+            }
+        }
+        if (feas >= 0) {
+            a.choice[i] = feas;
+            a.chosen_peak[i] = fpk;
+            a.chosen_overflow[i] = 0;
+            a.flags[i] = 1;
+        } else {
+            a.choice[i] = fb;
+            a.chosen_peak[i] = fbpk;
+            a.chosen_overflow[i] = fbslack < 0 ? int32_t(-fbslack) : 0;
+            a.flags[i] = fbslack >= 0 ? 1 : 0;
+        }
+    }
+}
+
+}  // namespace
+}  // namespace maps
+
+using namespace maps;
+
+extern "C" size_t maps_blocks_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max, int32_t block_size) {
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max > MAPS_MAX_BLOCKS_U_MAX || block_size < 1 ||
+        block_size > MAPS_MAX_BLOCK_SIZE)
+        return 0;
+    return blk_layout(D, n_total, u_max, block_size).bytes;
+}
+
+extern "C" maps_status maps_project_blocks(int32_t D, const int64_t* seg_off, const int32_t* prompt,
+                                           const int32_t* generated, const int32_t* upper, int64_t n_total,
+                                           int32_t u_max, int32_t block_size, void* snapshot,
+                                           size_t snapshot_bytes, int32_t* base_peak, uint32_t* dev_err,
+                                           hipStream_t stream) {
+    if (D < 1 || n_total < 0 || u_max < 0 || u_max > MAPS_MAX_BLOCKS_U_MAX || block_size < 1 ||
+        block_size > MAPS_MAX_BLOCK_SIZE)
+        return MAPS_E_SIZE;
+    if (!seg_off || !snapshot || !base_peak || !dev_err || (n_total > 0 && (!prompt || !generated || !upper)))
+        return MAPS_E_NULL;
+    const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
+    if (snapshot_bytes < L.bytes) return MAPS_E_BUFFER;
+    ProjArgs a{L, seg_off, prompt, generated, upper, static_cast<char*>(snapshot), base_peak, dev_err};
+    const size_t lds = size_t(L.W) * 8;
+    allow_dynamic_lds(project_blocks, lds);
+    hipLaunchKernelGGL(project_blocks, dim3(unsigned(D)), dim3(kPbNT), lds, stream, a);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* seg_off, int32_t D, int64_t n_total,
+                                         int32_t u_max, int32_t block_size, const int32_t* capacity,
+                                         const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
+                                         int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
+                                         int32_t* chosen_peak, int32_t* chosen_overflow, uint8_t* flags,
+                                         int32_t* pair_peak, uint32_t* dev_err, hipStream_t stream) {
+    if (D < 1 || n_total < 0 || A < 0 || rr_offset < 0 || u_max < 0 || u_max > MAPS_MAX_BLOCKS_U_MAX ||
+        block_size < 1 || block_size > MAPS_MAX_BLOCK_SIZE || D > 65535)
+        return MAPS_E_SIZE;
+    if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
+    if (!snapshot || !seg_off || !capacity || !queue_len || !dev_err ||
+        (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags || !pair_peak)))
+        return MAPS_E_NULL;
+    if (A == 0) return MAPS_OK;
+    const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
+    PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak};
+    const int64_t tiles = (A + kPairsNT * kPairsPer - 1) / (kPairsNT * kPairsPer);
+    hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(tiles), unsigned(D)), dim3(kPairsNT), 0, stream, pa);
+    MAPS_CHECK_LAUNCH();
+    FinArgs fa{D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
+               chosen_overflow, flags};
+    const int64_t fb = (A + kFinNT - 1) / kFinNT;
+    hipLaunchKernelGGL(blocks_finish, dim3(unsigned(fb < 4096 ? fb : 4096)), dim3(kFinNT), 0, stream, fa);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
