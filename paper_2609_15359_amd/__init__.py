@@ -342,8 +342,10 @@ class BlockSnapshot:
     block_size: int
 
 
-def project_blocks(seg_off, prompt, generated, upper, u_max: int, block_size: int, dev_err=None, base_peak=None):
-    """Block snapshot of D decoders and their base peaks in blocks."""
+def project_blocks(seg_off, prompt, generated, upper, u_max: int, block_size: int, dev_err=None, base_peak=None,
+                   snapshot: "BlockSnapshot | None" = None):
+    """Block snapshot of D decoders and their base peaks in blocks (into the
+    buffer of `snapshot` when one is given)."""
     seg_off = _dev(seg_off, torch.int64, "seg_off")
     dev = seg_off.device
     D = seg_off.numel() - 1
@@ -356,7 +358,10 @@ def project_blocks(seg_off, prompt, generated, upper, u_max: int, block_size: in
     nbytes = lib.maps_blocks_snapshot_bytes(D, n, int(u_max), int(block_size))
     if nbytes == 0:
         raise MapsError("D, u_max or block_size out of range for the block snapshot")
-    snap = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    if snapshot is not None and snapshot.data.numel() >= nbytes:
+        snap = snapshot.data
+    else:
+        snap = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     base = torch.empty(D, dtype=torch.int32, device=dev) if base_peak is None else base_peak
     err = new_error_word(dev) if dev_err is None else dev_err
     st = lib.maps_project_blocks(D, _ptr(seg_off), _ptr(prompt), _ptr(generated), _ptr(upper), n, int(u_max),
