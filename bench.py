@@ -303,7 +303,7 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
     if cpu:
         import oracle
         o = oracle.Oracle()
-        k = min(A, 4096)
+        k = min(A, 65536)
         Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
         t0 = time.perf_counter()
         o.place_blocks(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, b.queue_len, BLOCK, b.arr_prompt[:k],

@@ -115,12 +115,15 @@ __device__ inline int64_t occupancy_at(int64_t t, int64_t S, int64_t N, int64_t 
     return ob;
 }
 
-// Phase boundary for the slice in HBM: every thread's stores and atomics are
-// done, and each thread's vector L1 is invalidated before it reads values
-// that other threads wrote or that device atomics produced in L2.
+// Phase boundary for the slice in HBM, which only this workgroup touches (one
+// CU, one L2): each thread waits until its own stores and atomics have reached
+// L2, the barrier, then each thread drops its vector-L1 lines before reading
+// what other threads wrote (atomics update L2 only).  No L2 write-back is
+// needed, unlike a device-wide fence.
 __device__ inline void sync_global() {
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    __threadfence();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
 struct ProjArgs {
