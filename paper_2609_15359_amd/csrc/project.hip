@@ -62,12 +62,15 @@ __device__ inline int64_t remaining(int32_t U, int32_t g) {
 }
 
 // Phase boundary: every thread's writes of the previous phase are visible to
-// the whole workgroup.  For arrays in HBM the vector L1 is also invalidated,
-// since values produced by L2 atomics or by other waves may be cached stale.
+// the whole workgroup.  For arrays in HBM each thread first waits until its
+// own stores and atomics have reached L2, and after the barrier drops its
+// vector-L1 lines, since values produced by L2 atomics may be cached stale
+// (the slice is this workgroup's alone: no L2 write-back is needed).
 template <bool kInLds>
 __device__ inline void phase() {
+    if constexpr (!kInLds) __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if constexpr (!kInLds) __threadfence();
+    if constexpr (!kInLds) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
 struct Scratch {
