@@ -19,6 +19,9 @@
 //                    per-event counters by device atomics in the decoder's
 //                    slice, suffix scans, OB at every event, S prefix-max
 //                    scans and one suffix-max scan;
+//   blocks_order     per tile of 1,024 arrivals: their order by bound (a
+//                    counting sort on bound ranges), so that a wavefront's
+//                    lanes read neighbouring events;
 //   blocks_pairs     one workgroup per (decoder, 1,024 arrivals): every pair's
 //                    peak from the slice (read through L2) into the matrix;
 //   blocks_finish    per arrival: the choice over the matrix column.
@@ -281,19 +284,60 @@ struct PairArgs {
     int64_t A;
     const int64_t* seg_off;
     int32_t* pair;
+    int32_t* order;   // per tile of 1,024 arrivals: their tile indices, by bound
 };
 
-// Every pair's peak in blocks
+constexpr int kTile = kPairsNT * kPairsPer;
+
+// The arrivals of each tile ordered by their bound (a counting sort on 1,024
+// bound ranges), so that the lanes of a wavefront read neighbouring events of
+// a decoder's slice.  Written once, used by every decoder's workgroup.
+__global__ __launch_bounds__(kPairsNT) void blocks_order(PairArgs a) {
+    __shared__ int32_t start[kTile];
+    __shared__ int32_t tmp[kPairsNT / kWave];
+    const int64_t base = int64_t(blockIdx.x) * kTile;
+    const int64_t left = a.A - base;
+    const int n = left < kTile ? int(left) : kTile;
+    for (int b = threadIdx.x; b < kTile; b += kPairsNT) start[b] = 0;
+    __syncthreads();
+    int key[kPairsPer];
+    const int64_t span = int64_t(a.L.u_max) + 1;
+#pragma unroll
+    for (int k = 0; k < kPairsPer; ++k) {
+        const int t = threadIdx.x + k * kPairsNT;
+        key[k] = 0;
+        if (t < n) {
+            const int64_t U = a.aU[base + t];
+            const int64_t u = U < 0 ? 0 : (U < span ? U : span - 1);
+            key[k] = int(u * kTile / span);
+            atomicAdd(&start[key[k]], 1);
+        }
+    }
+    __syncthreads();
+    block_scan<kPairsNT, false, false, true, int32_t>(
+        kTile, 0, [&](int64_t b) { return start[b]; }, [&](int64_t b, int32_t v) { start[b] = v; }, tmp);
+#pragma unroll
+    for (int k = 0; k < kPairsPer; ++k) {
+        const int t = threadIdx.x + k * kPairsNT;
+        if (t < n) a.order[base + atomicAdd(&start[key[k]], 1)] = t;
+    }
+}
+
+// Every pair's peak in blocks; the tile's arrivals taken in bound order, the
+// row of the matrix written back in arrival order from LDS
 __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
+    __shared__ int32_t row[kTile];
     const BlkLayout& L = a.L;
     const int d = blockIdx.y;
     const BlkHeader h = reinterpret_cast<const BlkHeader*>(a.snap)[d];
     const int64_t S = L.S;
-    const int64_t first = int64_t(blockIdx.x) * (kPairsNT * kPairsPer) + threadIdx.x;
+    const int64_t base = int64_t(blockIdx.x) * kTile;
+    const int64_t left = a.A - base;
+    const int n = left < kTile ? int(left) : kTile;
     if (h.slice < 0) {
         for (int k = 0; k < kPairsPer; ++k) {
-            const int64_t i = first + k * kPairsNT;
-            if (i < a.A) a.pair[int64_t(d) * a.A + i] = -1;
+            const int t = threadIdx.x + k * kPairsNT;
+            if (t < n) a.pair[int64_t(d) * a.A + base + t] = -1;
         }
         return;
     }
@@ -303,8 +347,10 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
     const int32_t tmax = 32 * L.W - 1;
 #pragma unroll
     for (int k = 0; k < kPairsPer; ++k) {
-        const int64_t i = first + k * kPairsNT;
-        if (i >= a.A) continue;
+        const int t = threadIdx.x + k * kPairsNT;
+        if (t >= n) continue;
+        const int32_t loc = a.order[base + t];
+        const int64_t i = base + loc;
         const int32_t U = a.aU[i];
         int32_t out = -1;
         if (U >= 0) {
@@ -322,8 +368,10 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
             pk = pk > after ? pk : after;
             out = int32_t(pk > INT32_MAX ? INT32_MAX : pk);
         }
-        a.pair[int64_t(d) * a.A + i] = out;
+        row[loc] = out;
     }
+    __syncthreads();
+    for (int t = threadIdx.x; t < n; t += kPairsNT) a.pair[int64_t(d) * a.A + base + t] = row[t];
 }
 
 struct FinArgs {
@@ -430,8 +478,11 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
         return MAPS_E_NULL;
     if (A == 0) return MAPS_OK;
     const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
-    PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak};
-    const int64_t tiles = (A + kPairsNT * kPairsPer - 1) / (kPairsNT * kPairsPer);
+    // chosen_overflow holds each tile's order until blocks_finish writes it
+    PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak, chosen_overflow};
+    const int64_t tiles = (A + kTile - 1) / kTile;
+    hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kPairsNT), 0, stream, pa);
+    MAPS_CHECK_LAUNCH();
     hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(tiles), unsigned(D)), dim3(kPairsNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();
     FinArgs fa{D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
