@@ -129,6 +129,58 @@ __device__ inline void sync_global() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
+// Up to kGroup scans at once over the same len elements (sum or max, forward
+// or reverse, inclusive or exclusive), each thread one contiguous chunk:
+// get(i, q) and put(i, q, v) for quantity q < nq.  One pass for the chunk
+// totals, one wavefront scan per quantity through DPP, one LDS exchange for
+// all of them, one pass to write.  `tmp` holds kGroup * NT / 64 values.
+constexpr int kGroup = 16;
+
+template <int NT, bool kMax, bool kReverse, bool kExclusive, typename T, typename Get, typename Put>
+__device__ inline void group_scan(int64_t len, int nq, T identity, Get get, Put put, T* tmp) {
+    constexpr int kWaves = NT / kWave;
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    const int64_t chunk = (len + NT - 1) / NT;
+    const int64_t b = int64_t(threadIdx.x) * chunk;
+    const int64_t e = b + chunk < len ? b + chunk : len;
+    auto idx = [&](int64_t i) { return kReverse ? len - 1 - i : i; };
+    auto op = [](T x, T y) { return kMax ? (x > y ? x : y) : x + y; };
+    T acc[kGroup];
+#pragma unroll
+    for (int q = 0; q < kGroup; ++q) acc[q] = identity;
+    for (int64_t i = b; i < e; ++i) {
+#pragma unroll
+        for (int q = 0; q < kGroup; ++q)
+            if (q < nq) acc[q] = op(acc[q], get(idx(i), q));
+    }
+    __syncthreads();   // tmp may still be read by an earlier scan
+#pragma unroll
+    for (int q = 0; q < kGroup; ++q) {
+        const T incl = kMax ? wave_incl_scan_max(acc[q]) : wave_incl_scan_add(acc[q]);
+        if (lane == kWave - 1) tmp[q * kWaves + wid] = incl;
+        acc[q] = wave_shift_up1(incl, identity);   // exclusive within the wavefront
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kGroup; ++q) {
+        T before = identity;
+        for (int w = 0; w < wid; ++w) before = op(before, tmp[q * kWaves + w]);
+        acc[q] = op(before, acc[q]);
+    }
+    for (int64_t i = b; i < e; ++i) {
+#pragma unroll
+        for (int q = 0; q < kGroup; ++q) {
+            if (q < nq) {
+                const T x = get(idx(i), q);
+                const T next = op(acc[q], x);
+                put(idx(i), q, kExclusive ? acc[q] : next);
+                acc[q] = next;
+            }
+        }
+    }
+    __syncthreads();
+}
+
 struct ProjArgs {
     BlkLayout L;
     const int64_t* seg_off;
@@ -144,6 +196,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     extern __shared__ uint32_t bits[];               // W bit words, then W counts of events before each
     __shared__ int64_t red64[kPbNT / kWave];
     __shared__ uint32_t red32[kPbNT / kWave];
+    __shared__ int32_t redg[kGroup * (kPbNT / kWave)];
     const BlkLayout& L = a.L;
     uint32_t* wpre = bits + L.W;
     const int d = blockIdx.x;
@@ -226,15 +279,17 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
 
     // 4. suffix sums over the events (record E is zero): N, SX and every class count
     const int64_t len = int64_t(E) + 1;
-    block_scan<kPbNT, false, true, false, int32_t>(
-        len, 0, [&](int64_t e) { return s.N[e]; }, [&](int64_t e, int32_t v) { s.N[e] = v; },
-        reinterpret_cast<int32_t*>(red32));
     block_scan<kPbNT, false, true, false, int64_t>(
         len, int64_t(0), [&](int64_t e) { return s.SX[e]; }, [&](int64_t e, int64_t v) { s.SX[e] = v; }, red64);
-    for (int c = 0; c + 1 < S; ++c)
-        block_scan<kPbNT, false, true, false, int32_t>(
-            len, 0, [&](int64_t e) { return s.G[e * (S - 1) + c]; },
-            [&](int64_t e, int32_t v) { s.G[e * (S - 1) + c] = v; }, reinterpret_cast<int32_t*>(red32));
+    // N (quantity 0) and the S - 1 class counts (quantity c), kGroup at a time
+    for (int q0 = 0; q0 < S; q0 += kGroup) {
+        auto cell = [&](int64_t e, int q) -> int32_t& {
+            return q0 + q == 0 ? s.N[e] : s.G[e * (S - 1) + (q0 + q - 1)];
+        };
+        group_scan<kPbNT, false, true, false, int32_t>(
+            len, int(S - q0 < kGroup ? S - q0 : kGroup), 0, [&](int64_t e, int q) { return cell(e, q); },
+            [&](int64_t e, int q, int32_t v) { cell(e, q) = v; }, redg);
+    }
     sync_global();
     // counts by class -> counts of classes >= c
     for (int64_t e = tid; e < len; e += kPbNT) {
@@ -258,13 +313,13 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     sync_global();
 
     // 6. prefix maxima per residue class (exclusive: events below), suffix maximum
-    for (int rho = 0; rho < S; ++rho)
-        block_scan<kPbNT, true, false, true, int32_t>(
-            len, 0,
-            [&](int64_t e) {
-                return e < int64_t(E) ? int32_t(s.OB[e] + ceil_plus(rho, s.tau[e], S)) : 0;
+    for (int r0 = 0; r0 < S; r0 += kGroup)
+        group_scan<kPbNT, true, false, true, int32_t>(
+            len, int(S - r0 < kGroup ? S - r0 : kGroup), 0,
+            [&](int64_t e, int q) {
+                return e < int64_t(E) ? int32_t(s.OB[e] + ceil_plus(r0 + q, s.tau[e], S)) : 0;
             },
-            [&](int64_t e, int32_t v) { s.PMX[e * S + rho] = v; }, reinterpret_cast<int32_t*>(red32));
+            [&](int64_t e, int q, int32_t v) { s.PMX[e * S + r0 + q] = v; }, redg);
     const int32_t base = block_scan<kPbNT, true, true, false, int32_t>(
         len, 0, [&](int64_t e) { return s.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
         reinterpret_cast<int32_t*>(red32));
