@@ -296,7 +296,11 @@ maps_status maps_place_static(int32_t D, const int64_t* b_eff, const int32_t* qu
  * pair_peak[D][A] (required) and then the choices.  1 <= S <=
  * MAPS_MAX_BLOCK_SIZE, 0 <= u_max <= MAPS_MAX_BLOCKS_U_MAX.
  * dev_err bits: NEG_LEN, BOUND_RANGE, SEG_OFFSETS, INT32_RANGE (as
- * maps_project).  Host errors: NULL, SIZE, BUFFER, POLICY, HIP.
+ * maps_project); SNAPSHOT from maps_place_blocks when the snapshot was not
+ * written by maps_project_blocks for these D, n_total, u_max and S, or a
+ * decoder's resident count under seg_off differs from the one it was built
+ * with (that call then reads no slice).  Host errors: NULL, SIZE, BUFFER,
+ * POLICY, HIP.
  */
 size_t maps_blocks_snapshot_bytes(int32_t D, int64_t n_total, int32_t u_max, int32_t block_size);
 maps_status maps_project_blocks(int32_t D, const int64_t* seg_off, const int32_t* prompt,

@@ -35,6 +35,21 @@ constexpr int kPairsNT = 256;
 constexpr int kPairsPer = 4;
 constexpr int kFinNT = 256;
 
+// Snapshot: a 64-byte header with the arguments it was built for, the decoder
+// headers, then the decoder slices.  Placement checks the header against its
+// own arguments and each decoder's record count against its seg_off before it
+// reads a slice, so a mismatched call raises an error instead of reading past
+// the buffer.
+constexpr uint32_t kBlkMagic = 0x4250414Du;   // "MAPB"
+
+struct BlkSnapHeader {
+    uint32_t magic;
+    int32_t D, u_max, S, W, pad0;
+    int64_t n_total;
+    int32_t pad[8];
+};
+static_assert(sizeof(BlkSnapHeader) == 64, "block snapshot header size");
+
 // Decoder slice: W rank words {bits, events before}, then per event e = 0..E
 // (E+1 records, the last one for "no resident left") the arrays
 //   tau[e] (int32), N[e] (int32), SX[e] (int64), OB[e] (int32), SMX[e] (int32),
@@ -49,7 +64,8 @@ struct BlkLayout {
 };
 
 struct BlkHeader {
-    int64_t slice;     // byte offset of the decoder's slice
+    int64_t slice;     // byte offset of the decoder's slice (-1: its seg_off entries were invalid)
+    int64_t cap;       // records in the slice: residents + 1
     int32_t E;
     int32_t base;      // max_t OB(t)
 };
@@ -62,7 +78,7 @@ __host__ __device__ inline BlkLayout blk_layout(int32_t D, int64_t n_total, int3
     L.W = (((u_max + 1) / 32 + 1) + 1) & ~1;
     L.n_total = n_total;
     L.rec = (size_t(4 + 4 + 8 + 4 + 4) + size_t(S - 1) * 4 + size_t(S) * 4 + 15) & ~size_t(15);   // 16-byte slices
-    L.hdr_bytes = align256(size_t(D) * sizeof(BlkHeader));
+    L.hdr_bytes = align256(sizeof(BlkSnapHeader) + size_t(D) * sizeof(BlkHeader));
     // slice d starts at hdr + d * (8 W + 8 * 16) + seg_off[d] * (rec) with room for n_d + 1 records
     L.bytes = L.hdr_bytes + size_t(D) * (size_t(L.W) * 8 + 8 * 16 + L.rec) + size_t(n_total) * L.rec + 256;
     return L;
@@ -103,6 +119,15 @@ __host__ __device__ inline BlkSlice blk_slice(char* base, const BlkLayout& L, in
 
 __host__ __device__ inline int64_t blk_slice_offset(const BlkLayout& L, int32_t d, int64_t seg_lo) {
     return int64_t(L.hdr_bytes) + int64_t(d) * (int64_t(L.W) * 8 + 8 * 16 + int64_t(L.rec)) + seg_lo * int64_t(L.rec);
+}
+
+__host__ __device__ inline BlkHeader* blk_headers(char* snap) {
+    return reinterpret_cast<BlkHeader*>(snap + sizeof(BlkSnapHeader));
+}
+
+__device__ inline bool blk_snapshot_ok(const BlkSnapHeader* h, const BlkLayout& L) {
+    return h->magic == kBlkMagic && h->D == L.D && h->u_max == L.u_max && h->S == L.S && h->W == L.W &&
+           h->n_total == L.n_total;
 }
 
 // ceil((r + t) / S) for 0 <= r < S, t >= 0
@@ -202,13 +227,26 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     const int d = blockIdx.x;
     const int tid = threadIdx.x;
     const int64_t lo = a.seg_off[d], hi = a.seg_off[d + 1];
-    BlkHeader* hdr = reinterpret_cast<BlkHeader*>(a.snap);
+    BlkHeader* hdr = blk_headers(a.snap);
+    if (d == 0 && tid == 0) {   // every field is known before the decoders
+        BlkSnapHeader h;
+        h.D = L.D;
+        h.u_max = L.u_max;
+        h.S = L.S;
+        h.W = L.W;
+        h.pad0 = 0;
+        h.n_total = L.n_total;
+        for (int i = 0; i < 8; ++i) h.pad[i] = 0;
+        h.magic = kBlkMagic;
+        *reinterpret_cast<BlkSnapHeader*>(a.snap) = h;
+    }
     if (!(0 <= lo && lo <= hi && hi <= L.n_total)) {
         if (tid == 0) {
             raise_error(a.dev_err, MAPS_ERR_SEG_OFFSETS);
             hdr[d].E = 0;
             hdr[d].base = 0;
             hdr[d].slice = -1;
+            hdr[d].cap = 0;
             a.base_peak[d] = 0;
         }
         return;
@@ -325,6 +363,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
         reinterpret_cast<int32_t*>(red32));
     if (tid == 0) {
         hdr[d].slice = off;
+        hdr[d].cap = cap;
         hdr[d].E = int32_t(E);
         hdr[d].base = base;
         a.base_peak[d] = base;
@@ -340,6 +379,7 @@ struct PairArgs {
     const int64_t* seg_off;
     int32_t* pair;
     int32_t* order;   // per tile of 1,024 arrivals: their tile indices, by bound
+    uint32_t* dev_err;
 };
 
 constexpr int kTile = kPairsNT * kPairsPer;
@@ -384,19 +424,24 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
     __shared__ int32_t row[kTile];
     const BlkLayout& L = a.L;
     const int d = blockIdx.y;
-    const BlkHeader h = reinterpret_cast<const BlkHeader*>(a.snap)[d];
+    if (!blk_snapshot_ok(reinterpret_cast<const BlkSnapHeader*>(a.snap), L)) {
+        if (blockIdx.x == 0 && d == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    const BlkHeader h = blk_headers(const_cast<char*>(a.snap))[d];
     const int64_t S = L.S;
     const int64_t base = int64_t(blockIdx.x) * kTile;
     const int64_t left = a.A - base;
     const int n = left < kTile ? int(left) : kTile;
-    if (h.slice < 0) {
+    const int64_t cap = a.seg_off[d + 1] - a.seg_off[d] + 1;
+    if (h.slice < 0 || h.cap != cap) {
+        if (h.slice >= 0 && blockIdx.x == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
         for (int k = 0; k < kPairsPer; ++k) {
             const int t = threadIdx.x + k * kPairsNT;
             if (t < n) a.pair[int64_t(d) * a.A + base + t] = -1;
         }
         return;
     }
-    const int64_t cap = a.seg_off[d + 1] - a.seg_off[d] + 1;
     BlkSlice s = blk_slice(const_cast<char*>(a.snap) + h.slice, L, cap);
     const int32_t E = h.E;
     const int32_t tmax = 32 * L.W - 1;
@@ -527,6 +572,7 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
     if (D < 1 || n_total < 0 || A < 0 || rr_offset < 0 || u_max < 0 || u_max > MAPS_MAX_BLOCKS_U_MAX ||
         block_size < 1 || block_size > MAPS_MAX_BLOCK_SIZE || D > 65535)
         return MAPS_E_SIZE;
+    if ((A + kTile - 1) / kTile > INT32_MAX) return MAPS_E_SIZE;
     if (policy != MAPS_POLICY_MQ && policy != MAPS_POLICY_MC) return MAPS_E_POLICY;
     if (!snapshot || !seg_off || !capacity || !queue_len || !dev_err ||
         (A > 0 && (!a_prompt || !a_upper || !choice || !chosen_peak || !chosen_overflow || !flags || !pair_peak)))
@@ -534,7 +580,8 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
     if (A == 0) return MAPS_OK;
     const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
     // chosen_overflow holds each tile's order until blocks_finish writes it
-    PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak, chosen_overflow};
+    PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak, chosen_overflow,
+                dev_err};
     const int64_t tiles = (A + kTile - 1) / kTile;
     hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kPairsNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();

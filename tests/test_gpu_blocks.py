@@ -144,3 +144,45 @@ def test_error_bits():
     assert got["err"] & 16
     got = _gpu([0, 5], [5, 1], [0, 0], [3, 3], 100, 16, [100], [0], [1], [2])
     assert got["err"] & 8
+
+
+def test_snapshot_mismatch_is_reported():
+    """maps_place_blocks called with arguments other than those the snapshot
+    was built for (block size, u_max, n_total, D, per-decoder resident counts,
+    a buffer never written) raises SNAPSHOT and reads no slice; the matching
+    call raises nothing."""
+    import dataclasses
+
+    import torch
+
+    import paper_2609_15359_amd as maps
+    rng = np.random.default_rng(5)
+    D, A, S, u_max = 4, 300, 16, 500
+    seg = np.array([0, 30, 30, 75, 120], np.int64)
+    n = int(seg[-1])
+    p = rng.integers(0, 900, size=n).astype(np.int32)
+    g = rng.integers(0, 50, size=n).astype(np.int32)
+    U = rng.integers(0, u_max, size=n).astype(np.int32) + g
+    a_p = rng.integers(0, 900, size=A).astype(np.int32)
+    a_U = rng.integers(0, u_max + 1, size=A).astype(np.int32)
+    snap, _, err = maps.project_blocks(_cuda(seg, np.int64), _cuda(p), _cuda(g), _cuda(U), u_max, S)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+
+    def place(sn, d=D):
+        e = maps.new_error_word(snap.data.device)
+        maps.place_blocks(sn, _cuda(np.full(d, 10**6)), _cuda(np.zeros(d)), _cuda(a_p), _cuda(a_U), dev_err=e)
+        torch.cuda.synchronize()
+        return int(e.item()) & 0xFFFFFFFF
+
+    assert place(snap) == 0
+    moved = seg.copy()
+    moved[2] += 1                                    # one resident moved from decoder 2 to decoder 1
+    bad = [dataclasses.replace(snap, block_size=S + 1), dataclasses.replace(snap, u_max=u_max + 1),
+           dataclasses.replace(snap, n_total=n + 1), dataclasses.replace(snap, seg_off=_cuda(moved, np.int64)),
+           dataclasses.replace(snap, data=torch.zeros_like(snap.data))]
+    for sn in bad:
+        assert place(sn) & 32, sn
+    wider = dataclasses.replace(snap, D=D + 1, seg_off=_cuda(np.append(seg, n), np.int64))
+    assert place(wider, D + 1) & 32
+    assert place(snap) == 0
