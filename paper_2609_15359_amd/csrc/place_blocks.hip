@@ -490,25 +490,29 @@ struct FinArgs {
     uint8_t* flags;
 };
 
-// Algorithm 1's choice per arrival over its column of the matrix
+// Algorithm 1's choice per arrival over its column of the matrix.  Capacities
+// in blocks and queue lengths are staged in LDS, kFinDec decoders at a time,
+// and each thread keeps kFinUnroll column loads in flight; the decoders are
+// still taken in index order, so ties go to the lowest index as before.
+constexpr int kFinDec = 1024;
+constexpr int kFinUnroll = 16;
+
 __global__ __launch_bounds__(kFinNT) void blocks_finish(FinArgs a) {
+    __shared__ int32_t lcap[kFinDec];   // floor(capacity / S)
+    __shared__ int32_t lq[kFinDec];
     const int64_t stride = int64_t(gridDim.x) * kFinNT;
-    for (int64_t i = int64_t(blockIdx.x) * kFinNT + threadIdx.x; i < a.A; i += stride) {
-        if (a.aU[i] < 0) {
-            a.choice[i] = int32_t((a.rr_offset + i) % a.D);
-            a.chosen_peak[i] = -1;
-            a.chosen_overflow[i] = 0;
-            a.flags[i] = 2;
-            continue;
-        }
+    // every thread runs the same number of rounds: the staging barriers are block-wide
+    for (int64_t i0 = int64_t(blockIdx.x) * kFinNT; i0 < a.A; i0 += stride) {
+        const int64_t i = i0 + threadIdx.x;
+        const bool live = i < a.A;
+        const int32_t U = live ? a.aU[i] : -1;
         int32_t feas = -1, fq = 0, fpk = 0, fb = -1, fbpk = 0;
         int64_t fbslack = 0;
-        for (int32_t d = 0; d < a.D; ++d) {
-            const int32_t pk = a.pair[int64_t(d) * a.A + i];
-            const int64_t slack = int64_t(a.cap[d] / a.S) - pk;
-            if (a.policy == MAPS_POLICY_MQ && slack >= 0 && (feas < 0 || a.qlen[d] < fq)) {
+        auto consider = [&](int32_t d, int32_t pk, int32_t capb, int32_t q) {
+            const int64_t slack = int64_t(capb) - pk;
+            if (a.policy == MAPS_POLICY_MQ && slack >= 0 && (feas < 0 || q < fq)) {
                 feas = d;
-                fq = a.qlen[d];
+                fq = q;
                 fpk = pk;
             }
             if (fb < 0 || slack > fbslack) {
@@ -516,8 +520,34 @@ __global__ __launch_bounds__(kFinNT) void blocks_finish(FinArgs a) {
                 fbslack = slack;
                 fbpk = pk;
             }
+        };
+        for (int32_t d0 = 0; d0 < a.D; d0 += kFinDec) {
+            const int32_t nd = a.D - d0 < kFinDec ? a.D - d0 : kFinDec;
+            __syncthreads();
+            for (int k = threadIdx.x; k < nd; k += kFinNT) {
+                lcap[k] = a.cap[d0 + k] / a.S;
+                lq[k] = a.qlen[d0 + k];
+            }
+            __syncthreads();
+            if (!live || U < 0) continue;
+            const int32_t* col = a.pair + int64_t(d0) * a.A + i;
+            int k = 0;
+            for (; k + kFinUnroll <= nd; k += kFinUnroll) {
+                int32_t pk[kFinUnroll];
+#pragma unroll
+                for (int u = 0; u < kFinUnroll; ++u) pk[u] = col[int64_t(k + u) * a.A];
+#pragma unroll
+                for (int u = 0; u < kFinUnroll; ++u) consider(d0 + k + u, pk[u], lcap[k + u], lq[k + u]);
+            }
+            for (; k < nd; ++k) consider(d0 + k, col[int64_t(k) * a.A], lcap[k], lq[k]);
         }
-        if (feas >= 0) {
+        if (!live) continue;
+        if (U < 0) {
+            a.choice[i] = int32_t((a.rr_offset + i) % a.D);
+            a.chosen_peak[i] = -1;
+            a.chosen_overflow[i] = 0;
+            a.flags[i] = 2;
+        } else if (feas >= 0) {
             a.choice[i] = feas;
             a.chosen_peak[i] = fpk;
             a.chosen_overflow[i] = 0;
