@@ -13,7 +13,9 @@
 //                   entries a round among equal buckets through ballots and
 //                   keeps running counts per bucket in LDS, then per bucket a
 //                   prefix over the wavefronts and over the buckets), and
-//                   every group's size and start;
+//                   every group's size and start; each entry's bucket in log
+//                   order, and per bucket and 64-entry sub-block of the chunk
+//                   the bucket's entries before the sub-block;
 //   win_row_scan    per bucket: the prefix over chunks of its group sizes
 //                   (where each chunk's group starts in the bucket sequence);
 //   win_scatter     every score to its place in its bucket's sequence (the
@@ -26,9 +28,11 @@
 //                   first, with popcount rank directories); then one thread per
 //                   position takes the k-th smallest score of its window, one
 //                   rank step per bit;
-//   win_apply       per request: its bucket, its position c (the chunk prefix
-//                   plus a binary search of the log indices inside one chunk's
-//                   group), the quantile and the bound (Eq. (4)).
+//   win_apply       per request: its bucket, its position c (the bucket's
+//                   entries before its chunk, then before its sub-block, then
+//                   a count of its bucket among the at most 63 entries it saw
+//                   of the sub-block: one 128-byte line of bucket ids), the
+//                   quantile and the bound (Eq. (4)).
 // Every step is integer arithmetic, so the result is deterministic.
 #include "maps_internal.hpp"
 
@@ -44,13 +48,16 @@ constexpr int kSelNT = 512;
 constexpr int kSelPer = 3;                      // positions per select thread
 constexpr int kSelC = kSelNT * kSelPer;         // positions per select workgroup
 constexpr int kLevels = 31;                     // score bits (scores are non-negative int32)
+constexpr int kSub = 64;                        // log entries per sub-block of the position table
+constexpr int kSubs = kChunk / kSub;
 constexpr int kApplyNT = 256;
-constexpr int kApplyPer = 4;                   // requests per apply thread
+constexpr int kApplyPer = 2;                   // requests per apply thread
 
 struct WinWorkspace {
     int32_t* run_s;     // [n] scores, each chunk grouped by bucket
-    int32_t* run_i;     // [n] log indices, same order
     uint16_t* run_b;    // [n] buckets, same order
+    uint16_t* lb;       // [nch * kChunk] bucket of each log entry, log order (the tail past n unused)
+    uint16_t* t64;      // [nb][nch][kSubs] entries of the bucket in the chunk before each sub-block
     int32_t* cnt;       // [nb][nch] group sizes
     int32_t* rs;        // [nb][nch] group starts inside the chunk
     int32_t* off;       // [nb][nch + 1] bucket position of each group; off[b][nch] = n_b
@@ -69,8 +76,9 @@ WinWorkspace win_carve(void* base, int64_t n, int32_t nb) {
     char* p = static_cast<char*>(base);
     auto take = [&](size_t bytes) { char* r = p ? p + off : nullptr; off += align256(bytes); return r; };
     w.run_s = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
-    w.run_i = reinterpret_cast<int32_t*>(take(size_t(n) * 4));
     w.run_b = reinterpret_cast<uint16_t*>(take(size_t(n) * 2));
+    w.lb = reinterpret_cast<uint16_t*>(take(size_t(nch) * kChunk * 2));
+    w.t64 = reinterpret_cast<uint16_t*>(take(size_t(nb) * size_t(nch) * kSubs * 2));
     w.cnt = reinterpret_cast<int32_t*>(take(size_t(nb) * size_t(nch) * 4));
     w.rs = reinterpret_cast<int32_t*>(take(size_t(nb) * size_t(nch) * 4));
     w.off = reinterpret_cast<int32_t*>(take(size_t(nb) * size_t(nch + 1) * 4));
@@ -118,6 +126,7 @@ __global__ __launch_bounds__(kSortNT) void win_chunk_sort(WinArgs a) {
     __shared__ int32_t le[kBucketsMax - 1];
     __shared__ uint16_t seg[kSegs][kBucketsMax];   // entries of each bucket in each wave's segment
     __shared__ int32_t grp[kBucketsMax];           // chunk counts, then group starts
+    __shared__ uint16_t locs[kChunk];              // chunk position of each grouped entry
     __shared__ int32_t tmp[kSortNT / kWave];
     const int ne = a.nb - 1;
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
@@ -195,9 +204,25 @@ __global__ __launch_bounds__(kSortNT) void win_chunk_sort(WinArgs a) {
         if (i < a.n) {
             const int64_t pos = base + grp[b[r]] + seg[wid][b[r]] + rank[r];
             a.w.run_s[pos] = s[r];
-            a.w.run_i[pos] = int32_t(i);
             a.w.run_b[pos] = uint16_t(b[r]);
+            a.w.lb[i] = uint16_t(b[r]);
+            locs[pos - base] = uint16_t(loc);
         }
+    }
+    __syncthreads();
+    // per bucket and sub-block: the bucket's entries at chunk positions below
+    // the sub-block (a search of the group's ascending positions)
+    const int nvalid = a.n - base < kChunk ? int(a.n - base) : kChunk;
+    for (int t = threadIdx.x; t < a.nb * kSubs; t += kSortNT) {
+        const int bb = t / kSubs, sb = t % kSubs;
+        const int g0 = grp[bb], g1 = bb + 1 < a.nb ? grp[bb + 1] : nvalid;
+        const int bound = sb * kSub;
+        int lo = g0, hi = g1;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (locs[mid] < bound) lo = mid + 1; else hi = mid;
+        }
+        a.w.t64[(int64_t(bb) * a.nch + c) * kSubs + sb] = uint16_t(lo - g0);
     }
 }
 
@@ -404,15 +429,14 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
     for (int i = threadIdx.x; i < a.nb; i += kApplyNT) lpbase[i] = a.w.pbase[i];
     __syncthreads();
     bool bad = false;
-    // kApplyPer requests per thread, their searches interleaved so that their
-    // loads are in flight together
+    // kApplyPer requests per thread; the line of bucket ids depends only on
+    // the seen count, so its loads go out before the bucket is known
     for (int64_t j0 = int64_t(blockIdx.x) * (kApplyNT * kApplyPer); j0 < r.m;
          j0 += int64_t(gridDim.x) * (kApplyNT * kApplyPer)) {
-        int32_t p[kApplyPer], b[kApplyPer], n_g[kApplyPer], pos[kApplyPer];
-        int64_t seen[kApplyPer], c[kApplyPer];
-        const int32_t* gi[kApplyPer];
+        int32_t p[kApplyPer], b[kApplyPer], rem[kApplyPer];
+        int64_t seen[kApplyPer], ch[kApplyPer];
         bool live[kApplyPer];
-        int32_t most = 0;
+        uint4 ids[kApplyPer][kSub / 8];
 #pragma unroll
         for (int k = 0; k < kApplyPer; ++k) {
             const int64_t j = j0 + threadIdx.x + k * kApplyNT;
@@ -420,33 +444,14 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
             seen[k] = j < r.m ? r.seen[j] : 0;
             live[k] = p[k] >= 0 && seen[k] >= 0 && seen[k] <= a.n;
             bad |= p[k] >= 0 && !live[k];
-            b[k] = live[k] ? win_bucket(ledges, ne, p[k]) : 0;
-            const int64_t ch = seen[k] / kChunk;
-            const int32_t* row = a.w.off + int64_t(b[k]) * (a.nch + 1);
-            n_g[k] = 0;
-            gi[k] = a.w.run_i;
-            c[k] = 0;
-            if (live[k]) {
-                if (ch >= a.nch) {
-                    c[k] = row[a.nch];
-                } else {
-                    // entries of bucket b in chunk ch logged before `seen`: a
-                    // search of the group's (ascending) log indices
-                    gi[k] = a.w.run_i + ch * kChunk + a.w.rs[int64_t(b[k]) * a.nch + ch];
-                    n_g[k] = a.w.cnt[int64_t(b[k]) * a.nch + ch];
-                    c[k] = row[ch];
-                }
-            }
-            most = most > n_g[k] ? most : n_g[k];
-            pos[k] = 0;
-        }
-        int step = 1;
-        while (step * 2 <= most) step *= 2;
-        for (; most > 0 && step > 0; step >>= 1) {
+            ch[k] = live[k] ? seen[k] / kChunk : a.nch;
+            rem[k] = 0;
+            if (ch[k] < a.nch) {
+                const int64_t sub0 = seen[k] - seen[k] % kSub;   // first entry of the sub-block
+                rem[k] = int32_t(seen[k] - sub0);
+                const uint4* line = reinterpret_cast<const uint4*>(a.w.lb + sub0);
 #pragma unroll
-            for (int k = 0; k < kApplyPer; ++k) {
-                const int np = pos[k] + step;
-                if (np <= n_g[k] && gi[k][np - 1] < seen[k]) pos[k] = np;
+                for (int v = 0; v < kSub / 8; ++v) ids[k][v] = line[v];
             }
         }
 #pragma unroll
@@ -455,7 +460,28 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
             if (j >= r.m) continue;
             int32_t q = -1, U = -1;
             if (live[k]) {
-                q = a.w.qw[lpbase[b[k]] + c[k] + pos[k]];
+                b[k] = win_bucket(ledges, ne, p[k]);
+                const int64_t bb = b[k];
+                int64_t c = a.w.off[bb * (a.nch + 1) + (ch[k] < a.nch ? ch[k] : a.nch)];
+                if (ch[k] < a.nch) {
+                    const int sb = int((seen[k] % kChunk) / kSub);
+                    c += a.w.t64[(bb * a.nch + ch[k]) * kSubs + sb];
+                    // entries of bucket b among the first rem of the sub-block
+                    const uint32_t want = uint32_t(bb) * 0x10001u;
+                    int cnt = 0;
+#pragma unroll
+                    for (int v = 0; v < kSub / 8; ++v) {
+                        const uint32_t w4[4] = {ids[k][v].x, ids[k][v].y, ids[k][v].z, ids[k][v].w};
+#pragma unroll
+                        for (int h = 0; h < 4; ++h) {
+                            const uint32_t x = w4[h] ^ want;   // a zero half: a match
+                            const int e = v * 8 + h * 2;
+                            cnt += (e < rem[k] && (x & 0xFFFFu) == 0u) + (e + 1 < rem[k] && (x >> 16) == 0u);
+                        }
+                    }
+                    c += cnt;
+                }
+                q = a.w.qw[lpbase[bb] + c];
                 U = q == MAPS_Q_INF ? r.u_max
                                     : int32_t(int64_t(p[k]) + q < r.u_max ? int64_t(p[k]) + q : r.u_max);
             }
