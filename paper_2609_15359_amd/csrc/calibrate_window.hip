@@ -31,7 +31,8 @@
 //   win_apply       per request: its bucket, its position c (the bucket's
 //                   entries before its chunk, then before its sub-block, then
 //                   a count of its bucket among the at most 63 entries it saw
-//                   of the sub-block: one 128-byte line of bucket ids), the
+//                   of the sub-block: one line of bucket ids, 64 bytes with at
+//                   most 256 buckets, else 128), the
 //                   quantile and the bound (Eq. (4)).
 // Every step is integer arithmetic, so the result is deterministic.
 #include "maps_internal.hpp"
@@ -56,7 +57,8 @@ constexpr int kApplyPer = 2;                   // requests per apply thread
 struct WinWorkspace {
     int32_t* run_s;     // [n] scores, each chunk grouped by bucket
     uint16_t* run_b;    // [n] buckets, same order
-    uint16_t* lb;       // [nch * kChunk] bucket of each log entry, log order (the tail past n unused)
+    uint16_t* lb;       // [nch * kChunk] bucket of each log entry, log order (the tail past n unused);
+                        //   one byte each when there are at most 256 buckets
     uint16_t* t64;      // [nb][nch][kSubs] entries of the bucket in the chunk before each sub-block
     int32_t* cnt;       // [nb][nch] group sizes
     int32_t* rs;        // [nb][nch] group starts inside the chunk
@@ -205,7 +207,8 @@ __global__ __launch_bounds__(kSortNT) void win_chunk_sort(WinArgs a) {
             const int64_t pos = base + grp[b[r]] + seg[wid][b[r]] + rank[r];
             a.w.run_s[pos] = s[r];
             a.w.run_b[pos] = uint16_t(b[r]);
-            a.w.lb[i] = uint16_t(b[r]);
+            if (a.nb <= 256) reinterpret_cast<uint8_t*>(a.w.lb)[i] = uint8_t(b[r]);
+            else a.w.lb[i] = uint16_t(b[r]);
             locs[pos - base] = uint16_t(loc);
         }
     }
@@ -421,7 +424,11 @@ struct ApplyArgs {
     int32_t* U_out;
 };
 
+template <bool kByteIds>
 __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
+    constexpr int kIdBytes = kByteIds ? 1 : 2;
+    constexpr int kVecs = kSub * kIdBytes / 16;    // 16-byte loads per sub-block line
+    constexpr int kPerWord = 4 / kIdBytes;
     __shared__ int32_t ledges[kBucketsMax - 1];
     __shared__ int64_t lpbase[kBucketsMax];
     const int ne = a.nb - 1;
@@ -436,7 +443,7 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
         int32_t p[kApplyPer], b[kApplyPer], rem[kApplyPer];
         int64_t seen[kApplyPer], ch[kApplyPer];
         bool live[kApplyPer];
-        uint4 ids[kApplyPer][kSub / 8];
+        uint4 ids[kApplyPer][kVecs];
 #pragma unroll
         for (int k = 0; k < kApplyPer; ++k) {
             const int64_t j = j0 + threadIdx.x + k * kApplyNT;
@@ -449,9 +456,10 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
             if (ch[k] < a.nch) {
                 const int64_t sub0 = seen[k] - seen[k] % kSub;   // first entry of the sub-block
                 rem[k] = int32_t(seen[k] - sub0);
-                const uint4* line = reinterpret_cast<const uint4*>(a.w.lb + sub0);
+                const uint4* line =
+                    reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(a.w.lb) + sub0 * kIdBytes);
 #pragma unroll
-                for (int v = 0; v < kSub / 8; ++v) ids[k][v] = line[v];
+                for (int v = 0; v < kVecs; ++v) ids[k][v] = line[v];
             }
         }
 #pragma unroll
@@ -467,16 +475,20 @@ __global__ __launch_bounds__(kApplyNT) void win_apply(WinArgs a, ApplyArgs r) {
                     const int sb = int((seen[k] % kChunk) / kSub);
                     c += a.w.t64[(bb * a.nch + ch[k]) * kSubs + sb];
                     // entries of bucket b among the first rem of the sub-block
-                    const uint32_t want = uint32_t(bb) * 0x10001u;
+                    const uint32_t want = uint32_t(bb) * (kByteIds ? 0x01010101u : 0x00010001u);
+                    constexpr uint32_t kIdMask = kByteIds ? 0xFFu : 0xFFFFu;
                     int cnt = 0;
 #pragma unroll
-                    for (int v = 0; v < kSub / 8; ++v) {
+                    for (int v = 0; v < kVecs; ++v) {
                         const uint32_t w4[4] = {ids[k][v].x, ids[k][v].y, ids[k][v].z, ids[k][v].w};
 #pragma unroll
                         for (int h = 0; h < 4; ++h) {
-                            const uint32_t x = w4[h] ^ want;   // a zero half: a match
-                            const int e = v * 8 + h * 2;
-                            cnt += (e < rem[k] && (x & 0xFFFFu) == 0u) + (e + 1 < rem[k] && (x >> 16) == 0u);
+                            const uint32_t x = w4[h] ^ want;   // a zero id field: a match
+#pragma unroll
+                            for (int f = 0; f < kPerWord; ++f) {
+                                const int e = (v * 4 + h) * kPerWord + f;
+                                cnt += e < rem[k] && ((x >> (8 * kIdBytes * f)) & kIdMask) == 0u;
+                            }
                         }
                     }
                     c += cnt;
@@ -546,7 +558,8 @@ extern "C" maps_status maps_calibrate_window(const int32_t* pred, const int32_t*
     ApplyArgs r{apply_pred, apply_seen, m, u_max, q_out, U_out};
     const int64_t ab = (m + kApplyNT * kApplyPer - 1) / (kApplyNT * kApplyPer);
     const unsigned grid = unsigned(ab < 8192 ? ab : 8192);
-    hipLaunchKernelGGL(win_apply, dim3(grid), dim3(kApplyNT), 0, stream, a, r);
+    if (nb <= 256) hipLaunchKernelGGL(win_apply<true>, dim3(grid), dim3(kApplyNT), 0, stream, a, r);
+    else hipLaunchKernelGGL(win_apply<false>, dim3(grid), dim3(kApplyNT), 0, stream, a, r);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }
