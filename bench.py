@@ -71,12 +71,14 @@ def placement_bytes(D: int, A: int, u_max: int, W: int, events) -> int:
 
 
 def cpu_baseline(batch, budget_s: float = 20.0):
+    """The single-threaded C oracle's whole step on the same batch, timed; also
+    returns its last result, which the timed GPU step is checked against."""
     import oracle
     o = oracle.Oracle()
     t0 = time.perf_counter()
     runs = 0
     while True:
-        oracle.step(batch, o, want_pairs=True)
+        ref = oracle.step(batch, o, want_pairs=True)
         runs += 1
         if time.perf_counter() - t0 > budget_s / 2 or runs >= 5:
             break
@@ -87,7 +89,35 @@ def cpu_baseline(batch, budget_s: float = 20.0):
                      f"(calibrate, bound, project, place with pair matrix, local order), "
                      f"{dt * 1e3:.1f} ms per step"}
     out["all_cores"] = cpu_placement_all_cores(batch, o)
-    return out
+    return out, ref
+
+
+def verify_step(ws, ref) -> dict:
+    """Every output of the timed GPU step against the oracle's step on the same
+    batch, element by element (all are integers): quantiles, counts, bounds,
+    base peaks, choices, chosen peaks, overflows, flags, the whole pair-peak
+    matrix, local orders and admitted prefixes.  Exits non-zero on any
+    difference."""
+    import numpy as np
+    got = {"q": ws.out["q"], "count": ws.out["count"], "U": ws.out["U"], "base_peak": ws.base_peak,
+           "choice": ws.placement.choice, "chosen_peak": ws.placement.chosen_peak,
+           "chosen_overflow": ws.placement.chosen_overflow, "flags": ws.placement.flags,
+           "pair_peak": ws.placement.pair_peak, "order": ws.order, "admitted": ws.admitted}
+    want = {"q": ref.q, "count": ref.count, "U": ref.U, "base_peak": ref.base_peak, "choice": ref.place.choice,
+            "chosen_peak": ref.place.chosen_peak, "chosen_overflow": ref.place.chosen_overflow,
+            "flags": ref.place.flags, "pair_peak": ref.place.pair_peak, "order": ref.order,
+            "admitted": ref.admitted}
+    compared = 0
+    for k, t in got.items():
+        g = t.cpu().numpy().astype(np.int64)
+        w = np.asarray(want[k]).astype(np.int64)
+        if g.shape != w.shape or not np.array_equal(g, w):
+            bad = int(np.count_nonzero(g != w)) if g.shape == w.shape else -1
+            print(f"bench.py: the timed step's {k} differs from the oracle ({bad} entries)", file=sys.stderr)
+            sys.exit(3)
+        compared += g.size
+    return {"verified": True, "entries_compared": compared,
+            "against": "the C oracle's step on the same batch (every output, the pair matrix included)"}
 
 
 def cpu_placement_all_cores(batch, o, max_threads: int = 16):
@@ -497,7 +527,12 @@ def main():
         "feasible_fraction": feasible,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(b)
+        result["cpu_baseline"], ref = cpu_baseline(b)
+    else:
+        import oracle
+        ref = oracle.step(b, oracle.Oracle(), want_pairs=True)
+    # the outputs of the last timed step (the breakdown steps rewrote the same values)
+    result.update(verify_step(ws, ref))
     # the next rows on the path: sliding-window calibration and Algorithm 1 on block counts, same batch
     result["window_calibration"] = window_calibration(b, cpu=not args.no_cpu_baseline)
     nr, na = db.n_res, db.n_arr

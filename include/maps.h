@@ -296,7 +296,9 @@ maps_status maps_place_static(int32_t D, const int64_t* b_eff, const int32_t* qu
  * pair_peak[D][A] (required) and then the choices.  1 <= S <=
  * MAPS_MAX_BLOCK_SIZE, 0 <= u_max <= MAPS_MAX_BLOCKS_U_MAX.
  * dev_err bits: NEG_LEN, BOUND_RANGE, SEG_OFFSETS, INT32_RANGE (as
- * maps_project); SNAPSHOT from maps_place_blocks when the snapshot was not
+ * maps_project); from maps_place_blocks NEG_LEN (a_prompt of an arrival with a
+ * bound, capacity or queue_len < 0), INT32_RANGE (a pair peak above INT32_MAX,
+ * stored clamped), and SNAPSHOT when the snapshot was not
  * written by maps_project_blocks for these D, n_total, u_max and S, or a
  * decoder's resident count under seg_off differs from the one it was built
  * with (that call then reads no slice).  Host errors: NULL, SIZE, BUFFER,

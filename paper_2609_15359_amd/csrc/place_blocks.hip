@@ -445,6 +445,7 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
     BlkSlice s = blk_slice(const_cast<char*>(a.snap) + h.slice, L, cap);
     const int32_t E = h.E;
     const int32_t tmax = 32 * L.W - 1;
+    bool neg = false, big = false;
 #pragma unroll
     for (int k = 0; k < kPairsPer; ++k) {
         const int t = threadIdx.x + k * kPairsNT;
@@ -454,6 +455,7 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
         const int32_t U = a.aU[i];
         int32_t out = -1;
         if (U >= 0) {
+            neg |= a.ap[i] < 0;
             const int64_t p = a.ap[i] < 0 ? 0 : a.ap[i];
             const int32_t tc = U < tmax ? U : tmax;
             const uint2 w = s.rank[tc >> 5];
@@ -466,15 +468,21 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
             const int64_t after = (j < E && s.tau[j] == U) ? s.SMX[j + 1] : s.SMX[j];
             int64_t pk = left > at ? left : at;
             pk = pk > after ? pk : after;
+            big |= pk > INT32_MAX;
             out = int32_t(pk > INT32_MAX ? INT32_MAX : pk);
         }
         row[loc] = out;
     }
+    // a negative prompt, or a peak clamped to INT32_MAX, is reported once per wavefront
+    if (__builtin_amdgcn_ballot_w64(neg) != 0 && threadIdx.x % kWave == 0) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+    if (__builtin_amdgcn_ballot_w64(big) != 0 && threadIdx.x % kWave == 0)
+        raise_error(a.dev_err, MAPS_ERR_INT32_RANGE);
     __syncthreads();
     for (int t = threadIdx.x; t < n; t += kPairsNT) a.pair[int64_t(d) * a.A + base + t] = row[t];
 }
 
 struct FinArgs {
+    uint32_t* dev_err;
     int32_t D;
     int32_t S;
     const int32_t* cap;
@@ -525,8 +533,12 @@ __global__ __launch_bounds__(kFinNT) void blocks_finish(FinArgs a) {
             const int32_t nd = a.D - d0 < kFinDec ? a.D - d0 : kFinDec;
             __syncthreads();
             for (int k = threadIdx.x; k < nd; k += kFinNT) {
-                lcap[k] = a.cap[d0 + k] / a.S;
-                lq[k] = a.qlen[d0 + k];
+                const int32_t c = a.cap[d0 + k], q = a.qlen[d0 + k];
+                // a negative capacity or queue length is an error (its block count would
+                // truncate toward zero); each workgroup checks every decoder, the first reports
+                if ((c < 0 || q < 0) && blockIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
+                lcap[k] = c < 0 ? -1 : c / a.S;
+                lq[k] = q;
             }
             __syncthreads();
             if (!live || U < 0) continue;
@@ -617,7 +629,7 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
     MAPS_CHECK_LAUNCH();
     hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(tiles), unsigned(D)), dim3(kPairsNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();
-    FinArgs fa{D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
+    FinArgs fa{dev_err, D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
                chosen_overflow, flags};
     const int64_t fb = (A + kFinNT - 1) / kFinNT;
     hipLaunchKernelGGL(blocks_finish, dim3(unsigned(fb < 4096 ? fb : 4096)), dim3(kFinNT), 0, stream, fa);

@@ -591,6 +591,24 @@ def pin_place_bruteforce(o):
                 assert r.flags[a] == (1 if slack[want] >= 0 else 0)
 
 
+def pin_bruteforce_peak(o):
+    """The oracle's term-by-term brute force (residents plus extra requests
+    that start now, each summed at every step) against the Python one, and
+    against its closed forms: no request gives 0, one extra request alone
+    gives q + V (Sec. 3.3: a request's footprint grows to p + U)."""
+    rng = _rng(23)
+    assert o.bruteforce_peak([], [], []) == 0
+    for q, V in ((0, 0), (5, 0), (3, 9), (100, 250)):
+        assert o.bruteforce_peak([], [], [], [q], [V]) == q + V
+    for trial in range(40):
+        _, p, g, U = _tiny_decoders(rng, 1, 7, 14, 25)
+        m = int(rng.integers(0, 4))
+        q = rng.integers(0, 25, size=m).astype(np.int32)
+        V = rng.integers(0, 16, size=m).astype(np.int32)
+        want = py_peak(p, g, U, [(int(a), int(b)) for a, b in zip(q, V)])
+        assert o.bruteforce_peak(p, g, U, q, V) == want, trial
+
+
 def pin_place_closed_forms(o):
     # empty decoder: peak = p_a + U_a
     seg = np.array([0, 0], np.int64)
@@ -745,7 +763,7 @@ ALL_PINS = [
     pin_static_golden, pin_static_bruteforce, pin_static_water_filling, pin_static_state_and_invariants,
     pin_static_reduces_to_projection,
     pin_blocks_golden, pin_blocks_bruteforce, pin_blocks_reduce_to_tokens, pin_blocks_invariants,
-    pin_place_golden, pin_occupancy_bruteforce, pin_place_bruteforce, pin_place_closed_forms,
+    pin_place_golden, pin_occupancy_bruteforce, pin_bruteforce_peak, pin_place_bruteforce, pin_place_closed_forms,
     pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
     pin_local_order_golden, pin_local_order_bruteforce,
 ]

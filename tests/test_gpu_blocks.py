@@ -144,6 +144,16 @@ def test_error_bits():
     assert got["err"] & 16
     got = _gpu([0, 5], [5, 1], [0, 0], [3, 3], 100, 16, [100], [0], [1], [2])
     assert got["err"] & 8
+    # placement's own inputs: a negative prompt (of an arrival with a bound), capacity or queue length
+    ok = _gpu([0, 2], [5, 1], [0, 0], [3, 3], 100, 16, [100], [0], [1], [2])
+    assert ok["err"] == 0
+    assert _gpu([0, 2], [5, 1], [0, 0], [3, 3], 100, 16, [100], [0], [-1], [2])["err"] == 1
+    assert _gpu([0, 2], [5, 1], [0, 0], [3, 3], 100, 16, [100], [0], [-1], [-1])["err"] == 0   # no bound: RR
+    assert _gpu([0, 2], [5, 1], [0, 0], [3, 3], 100, 16, [-5], [0], [1], [2])["err"] == 1
+    assert _gpu([0, 2], [5, 1], [0, 0], [3, 3], 100, 16, [100], [-2], [1], [2])["err"] == 1
+    # a pair peak beyond INT32_MAX blocks at S = 1 (prompt near INT32_MAX plus the residents)
+    big = _gpu([0, 1], [5], [0], [3], 100, 1, [100], [0], [2**31 - 8], [50])
+    assert big["err"] & 4
 
 
 def test_snapshot_mismatch_is_reported():

@@ -58,11 +58,11 @@ def test_policy_mc_and_round_robin_offset(orc, policy):
     compare_all(g, o)
 
 
-def test_xlarge_sampled(orc):
+def test_xlarge_full(orc):
     """1,024 decoders x 1,048,576 arrivals: every decision, bound, base peak,
-    order and admission compared in full; the 4 GiB pair-peak matrix compared
-    on sampled arrival columns and sampled decoder rows, which the oracle
-    computes one by one."""
+    order and admission compared in full, and every entry of the 4 GiB
+    pair-peak matrix, which the oracle computes in arrival chunks of 65,536
+    against all decoders."""
     b = workload.make("xlarge")
     say("[parity] xlarge: oracle decisions (no pair matrix)")
     o = oracle_step(b, o=orc, want_pairs=False)
@@ -70,19 +70,22 @@ def test_xlarge_sampled(orc):
     g = gpu_step(b, want_pairs=True)
     assert g["err"] == 0, g["errors"]
     compare_all(g, o, pairs=False)
-    _, U_arr, _ = b.split_bounds(o["U"])
-    U_res = b.split_bounds(o["U"])[0]
-    rng = np.random.default_rng(4)
-    cols = np.sort(rng.choice(b.arrivals, size=48, replace=False))
-    sub = orc.place(b.seg_off, b.res_prompt, b.res_gen, U_res, b.capacity, b.queue_len,
-                    b.arr_prompt[cols], U_arr[cols], a_index=cols, want_pairs=True)
-    assert_same("pair_peak[:, sampled arrivals]", g["pair_peak"][:, cols], sub.pair_peak)
-    for d in rng.choice(b.decoders, size=3, replace=False):
-        lo, hi = b.seg_off[d], b.seg_off[d + 1]
-        row = orc.place(np.array([0, hi - lo], np.int64), b.res_prompt[lo:hi], b.res_gen[lo:hi],
-                        U_res[lo:hi], b.capacity[d:d + 1], b.queue_len[d:d + 1], b.arr_prompt, U_arr,
-                        want_pairs=True)
-        assert_same(f"pair_peak[{d}, :]", g["pair_peak"][d], row.pair_peak[0])
+    U_res, U_arr, _ = b.split_bounds(o["U"])
+    chunk = 65536
+
+    def check(c0):
+        cols = np.arange(c0, min(c0 + chunk, b.arrivals))
+        sub = orc.place(b.seg_off, b.res_prompt, b.res_gen, U_res, b.capacity, b.queue_len,
+                        b.arr_prompt[cols], U_arr[cols], a_index=cols, want_pairs=True)
+        assert_same(f"pair_peak[:, {c0}:{c0 + cols.size}]", g["pair_peak"][:, c0:c0 + cols.size], sub.pair_peak)
+        assert_same(f"choice[{c0}:]", g["choice"][cols], sub.choice)
+        return c0
+
+    # chunks on 8 host threads (the oracle's C call releases the interpreter lock)
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=8) as ex:
+        for c0 in ex.map(check, range(0, b.arrivals, chunk)):
+            say(f"[parity] xlarge: pair matrix columns {c0}..{min(c0 + chunk, b.arrivals) - 1} equal")
 
 
 def test_run_to_run_bitwise_determinism():

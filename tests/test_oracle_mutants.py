@@ -82,6 +82,10 @@ MUTANTS = [
      "int64_t capB = ((int64_t)capacity[d] + S - 1) / S;"),
     ("blocks_prompt_residue_dropped", "int64_t P = a_p[a] / S, rho = a_p[a] % S;",
      "int64_t P = a_p[a] / S, rho = 0;"),
+    ("bruteforce_extra_no_growth", "            if (t <= V[k]) occ += (int64_t)q[k] + t;",
+     "            if (t <= V[k]) occ += (int64_t)q[k];"),
+    ("bruteforce_resident_leaves_early", "if (t <= remaining(U[r], g[r])) occ += (int64_t)p[r] + g[r] + t;",
+     "if (t < remaining(U[r], g[r])) occ += (int64_t)p[r] + g[r] + t;"),
     ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
      "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
 ]
