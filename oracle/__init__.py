@@ -78,12 +78,18 @@ def _declare(lib):
                                         c.c_int64, _i32p, _i32p, c.c_int32, c.c_int64,
                                         _i32p, _i64p, _i64p, _u8p, i64n, i64n]
     lib.oracle_place_blocks.restype = c.c_int
-    lib.oracle_rsc_state.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, c.c_int32, _i64p, _i64p,
+    lib.oracle_rsc_state.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, u8n, _i32p, c.c_int32, _i64p, _i64p,
                                      _i64p]
     lib.oracle_rsc_state.restype = c.c_int
     lib.oracle_place_static.argtypes = [c.c_int32, _i64p, _i32p, c.c_int32, c.c_int64, _i32p, _i32p, c.c_int32,
                                         c.c_int64, c.c_int32, _i32p, _i64p, _u8p, i64n, i32n]
     lib.oracle_place_static.restype = c.c_int
+    lib.oracle_place_commit.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, _i32p, c.c_int64,
+                                        _i32p, _i32p, c.c_int32, c.c_int64, _i32p, _i64p, _i64p, _u8p, i32n]
+    lib.oracle_place_commit.restype = c.c_int
+    lib.oracle_simulate.argtypes = [c.c_int32, c.c_int64, c.c_int32, c.c_int64, _i64p, _i32p, _i32p, _i32p,
+                                    c.c_int32, _i64p, _i32p, _i64p, _i64p, _i64p, _i64p, _i64p, _i64p]
+    lib.oracle_simulate.restype = c.c_int
     lib.oracle_local_order.argtypes = [c.c_int32, _i64p, _i32p, _i32p, _i32p, _i32p, _i64p,
                                        _i32p, _i32p, i32n, c.c_int32, c.c_int32, _i32p, _i32p]
     lib.oracle_local_order.restype = c.c_int
@@ -234,12 +240,15 @@ class Oracle:
         return out
 
     # -- Algorithm 1 on block counts (Sec. 3.3, Eq. (6)) ---------------------
-    def rsc_state(self, seg_off, p, g, U, capacity, S: int):
-        """(B_free, B_res, B_eff) per decoder in blocks of S tokens."""
+    def rsc_state(self, seg_off, p, g, U, capacity, S: int, in_flight=None):
+        """(B_free, B_res, B_eff) per decoder in blocks of S tokens; in_flight
+        (optional, one flag per request) marks requests whose prompt KV is
+        still being transferred (whole budget reserved, nothing held)."""
         seg_off = _i64(seg_off)
         D = seg_off.size - 1
         out = [np.zeros(D, np.int64) for _ in range(3)]
-        rc = self.lib.oracle_rsc_state(D, seg_off, _i32(p), _i32(g), _i32(U), _i32(capacity), int(S), *out)
+        fl = None if in_flight is None else np.ascontiguousarray(in_flight, dtype=np.uint8)
+        rc = self.lib.oracle_rsc_state(D, seg_off, _i32(p), _i32(g), _i32(U), fl, _i32(capacity), int(S), *out)
         if rc:
             raise ValueError(f"oracle_rsc_state failed ({rc})")
         return tuple(out)
@@ -262,6 +271,46 @@ class Oracle:
         if rc:
             raise ValueError(f"oracle_place_static failed ({rc})")
         return choice, need, flags, b_after, q_after
+
+    # -- placement with sequential commit (Sec. 3.3, Algorithm 1) -----------
+    def place_commit(self, seg_off, p, g, U, capacity, queue_len, a_p, a_U, policy=POLICY_MQ, rr_offset=0):
+        """Arrivals in order, each committed to its decoder's projected
+        occupancy (and queue) before the next.  Returns a PlaceResult (no pair
+        matrix, no base peaks) and the queue lengths after the batch."""
+        seg_off = _i64(seg_off)
+        D = seg_off.size - 1
+        a_p, a_U = _i32(a_p), _i32(a_U)
+        A = a_p.size
+        out = PlaceResult(choice=np.zeros(A, np.int32), chosen_peak=np.zeros(A, np.int64),
+                          chosen_overflow=np.zeros(A, np.int64), flags=np.zeros(A, np.uint8), pair_peak=None,
+                          base_peak=np.zeros(0, np.int64))
+        q_after = np.zeros(D, np.int32)
+        rc = self.lib.oracle_place_commit(D, seg_off, _i32(p), _i32(g), _i32(U), _i32(capacity), _i32(queue_len),
+                                          A, a_p, a_U, int(policy), int(rr_offset), out.choice, out.chosen_peak,
+                                          out.chosen_overflow, out.flags, q_after)
+        if rc:
+            raise ValueError(f"oracle_place_commit failed ({rc})")
+        return out, q_after
+
+    # -- App. A pressure simulation --------------------------------------------
+    def simulate(self, N: int, C: int, theta_ppm: int, arrival_ms, prompt, output, bound=None, policy: int = 0):
+        """Round-robin (policy 0) or Algorithm 1 (policy 1) routing of the
+        requests onto N decoders of C tokens, one millisecond at a time.
+        Returns a SimResult."""
+        arrival_ms = _i64(arrival_ms)
+        prompt, output = _i32(prompt), _i32(output)
+        n = prompt.size
+        bound = np.full(n, -1, np.int32) if bound is None else _i32(bound)
+        r = SimResult(finish_ms=np.zeros(n, np.int64), routed=np.zeros(n, np.int32),
+                      hp_time=np.zeros(N, np.int64), hp_max=np.zeros(N, np.int64), hp_count=np.zeros(N, np.int64),
+                      max_queue=np.zeros(N, np.int64), queue_area=np.zeros(N, np.int64),
+                      span=np.zeros(2, np.int64))
+        rc = self.lib.oracle_simulate(int(N), int(C), int(theta_ppm), n, arrival_ms, prompt, output, bound,
+                                      int(policy), r.finish_ms, r.routed, r.hp_time, r.hp_max, r.hp_count,
+                                      r.max_queue, r.queue_area, r.span)
+        if rc:
+            raise ValueError(f"oracle_simulate failed ({rc})")
+        return r
 
     # -- local order (Sec. 3.3, Eq. (7); App. A, Eq. (10)) -------------------
     def local_order(self, seg_off, p, g, U, capacity, q_off, q_p, q_U, q_wait, max_wait_ms,
@@ -295,6 +344,18 @@ class PlaceResult:
     flags: np.ndarray
     pair_peak: np.ndarray | None
     base_peak: np.ndarray
+
+
+@dataclass
+class SimResult:
+    finish_ms: np.ndarray
+    routed: np.ndarray
+    hp_time: np.ndarray
+    hp_max: np.ndarray
+    hp_count: np.ndarray
+    max_queue: np.ndarray
+    queue_area: np.ndarray
+    span: np.ndarray
 
 
 @dataclass

@@ -346,6 +346,102 @@ int oracle_place(int32_t D, const int64_t* seg_off, const int32_t* p, const int3
     return 0;
 }
 
+/*
+ * Placement with sequential commit (Sec. 3.3: each dispatch atomically
+ * reserves its demand before the next request is placed; Algorithm 1).
+ * Arrivals are taken in index order.  Arrival a is evaluated exactly as in
+ * oracle_place, but against occupancy curves that include every earlier
+ * arrival already committed to the decoder: a committed arrival (p, U) holds
+ * p + t at step t while t <= U (a resident with g = 0 and R = U).  The chosen
+ * decoder then receives the arrival (its curve grows by p + t for t <= U) and
+ * its queue grows by one; the queue lengths that MQ compares are these
+ * running ones.  An arrival without a bound goes round robin, joins that
+ * decoder's queue and commits no occupancy (its footprint is unknown).
+ * queue_out (nullable) receives the queue lengths after the batch.
+ */
+int oracle_place_commit(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
+                        const int32_t* U, const int32_t* capacity, const int32_t* queue_len,
+                        int64_t A, const int32_t* a_p, const int32_t* a_U, int32_t policy, int64_t rr_offset,
+                        int32_t* choice, int64_t* chosen_peak, int64_t* chosen_overflow, uint8_t* flags,
+                        int32_t* queue_out)
+{
+    if (D < 1 || A < 0 || rr_offset < 0 || (policy != ORACLE_POLICY_MQ && policy != ORACLE_POLICY_MC)) return -1;
+    int64_t T = 0;
+    for (int64_t a = 0; a < A; ++a) T = max64(T, a_U[a]);
+    for (int32_t d = 0; d < D; ++d) T = max64(T, max_remaining(g, U, seg_off[d], seg_off[d + 1]));
+    size_t len = (size_t)T + 1;
+    /* per decoder: the occupancy curve O, present[u] = max_{t<=u} (O[t] + t)
+     * and after[u] = max_{t>u} O[t] (0 past T), as in oracle_place */
+    int64_t* O = (int64_t*)malloc((size_t)D * len * sizeof(int64_t));
+    int64_t* present = (int64_t*)malloc((size_t)D * len * sizeof(int64_t));
+    int64_t* after = (int64_t*)malloc((size_t)D * len * sizeof(int64_t));
+    int64_t* Q = (int64_t*)malloc((size_t)D * sizeof(int64_t));
+    if (!O || !present || !after || !Q) { free(O); free(present); free(after); free(Q); return -2; }
+    int rc = 0;
+    for (int32_t d = 0; d < D && rc == 0; ++d) {
+        int64_t lo = seg_off[d], hi = seg_off[d + 1];
+        rc = oracle_occupancy(p + lo, g + lo, U + lo, hi - lo, T, O + (size_t)d * len);
+        Q[d] = queue_len[d];
+    }
+    for (int32_t d = 0; d < D && rc == 0; ++d) {   /* the derived maxima of every decoder */
+        int64_t *o = O + (size_t)d * len, *pr = present + (size_t)d * len, *af = after + (size_t)d * len;
+        for (int64_t t = 0; t <= T; ++t) pr[t] = (t == 0) ? o[0] : max64(pr[t - 1], o[t] + t);
+        af[T] = 0;
+        for (int64_t t = T - 1; t >= 0; --t) af[t] = max64(af[t + 1], o[t + 1]);
+    }
+    for (int64_t a = 0; a < A && rc == 0; ++a) {
+        if (a_U[a] < 0) {
+            int32_t d = (int32_t)((rr_offset + a) % D);
+            choice[a] = d;
+            chosen_peak[a] = -1;
+            chosen_overflow[a] = 0;
+            flags[a] = 2;
+            Q[d] += 1;
+            continue;
+        }
+        int32_t feas_d = -1, fb_d = -1;
+        int64_t feas_peak = 0, fb_slack = 0, fb_peak = 0;
+        for (int32_t d = 0; d < D; ++d) {
+            int64_t peak = max64((int64_t)a_p[a] + present[(size_t)d * len + a_U[a]], after[(size_t)d * len + a_U[a]]);
+            int64_t slack = (int64_t)capacity[d] - peak;
+            if (policy == ORACLE_POLICY_MQ && slack >= 0 && (feas_d < 0 || Q[d] < Q[feas_d])) {
+                feas_d = d;
+                feas_peak = peak;
+            }
+            if (fb_d < 0 || slack > fb_slack) {
+                fb_d = d;
+                fb_slack = slack;
+                fb_peak = peak;
+            }
+        }
+        int32_t best;
+        if (policy == ORACLE_POLICY_MQ && feas_d >= 0) {
+            best = feas_d;
+            chosen_peak[a] = feas_peak;
+            chosen_overflow[a] = 0;
+            flags[a] = 1;
+        } else {
+            best = fb_d;
+            chosen_peak[a] = fb_peak;
+            chosen_overflow[a] = max64(0, fb_peak - capacity[fb_d]);
+            flags[a] = (fb_peak <= capacity[fb_d]) ? 1 : 0;
+        }
+        choice[a] = best;
+        Q[best] += 1;
+        /* commit: the arrival joins the chosen decoder's curve, whose maxima
+         * are then derived again over the whole step axis */
+        int64_t *o = O + (size_t)best * len, *pr = present + (size_t)best * len, *af = after + (size_t)best * len;
+        for (int64_t t = 0; t <= a_U[a]; ++t) o[t] += (int64_t)a_p[a] + t;
+        for (int64_t t = 0; t <= T; ++t) pr[t] = (t == 0) ? o[0] : max64(pr[t - 1], o[t] + t);
+        af[T] = 0;
+        for (int64_t t = T - 1; t >= 0; --t) af[t] = max64(af[t + 1], o[t + 1]);
+    }
+    if (rc == 0 && queue_out)
+        for (int32_t d = 0; d < D; ++d) queue_out[d] = (int32_t)Q[d];
+    free(O); free(present); free(after); free(Q);
+    return rc;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Algorithm 1 on block counts (Sec. 3.3: the runtime state, Eq. (6),        */
 /* Algorithm 1 and the atomic reservation of B_need after each dispatch)      */
@@ -357,15 +453,26 @@ static int64_t ceil_div(int64_t x, int64_t s) { return (x + s - 1) / s; }
  * blocks; each resident holds ceil((p+g)/S) blocks and keeps reserved the
  * blocks still missing to its demand ceil((p+U)/S) (none when U < 0 or when
  * it already holds more); B_free = capacity blocks - held blocks,
- * B_res = sum of the reservations, B_eff = B_free - B_res. */
+ * B_res = sum of the reservations, B_eff = B_free - B_res.  in_flight
+ * (nullable) marks requests whose prompt KV is still in transfer. */
 int oracle_rsc_state(int32_t D, const int64_t* seg_off, const int32_t* p, const int32_t* g,
-                     const int32_t* U, const int32_t* capacity, int32_t S,
+                     const int32_t* U, const uint8_t* in_flight, const int32_t* capacity, int32_t S,
                      int64_t* b_free, int64_t* b_res, int64_t* b_eff)
 {
     if (D < 1 || S < 1) return -1;
     for (int32_t d = 0; d < D; ++d) {
         int64_t held = 0, res = 0;
         for (int64_t r = seg_off[d]; r < seg_off[d + 1]; ++r) {
+            if (in_flight && in_flight[r]) {
+                /* Staged reservation (appendix on the global algorithm): a request
+                 * dispatched here whose prompt KV has not arrived yet holds no
+                 * block and keeps its whole budget reserved, ceil((p+U)/S) (its
+                 * prompt's blocks when it has no bound).  Once the prompt is
+                 * transferred the prompt part of that reservation is released
+                 * into held blocks, the rule below. */
+                res += U[r] < 0 ? ceil_div((int64_t)p[r], S) : ceil_div((int64_t)p[r] + U[r], S);
+                continue;
+            }
             int64_t now = ceil_div((int64_t)p[r] + g[r], S);
             int64_t demand = U[r] < 0 ? now : ceil_div((int64_t)p[r] + U[r], S);
             held += now;
@@ -660,4 +767,166 @@ int64_t oracle_bruteforce_peak(int64_t n, const int32_t* p, const int32_t* g, co
         best = max64(best, occ);
     }
     return best;
+}
+
+/* ------------------------------------------------------------------------ */
+/* App. A: KV pressure of decoders under round-robin or MAPS routing,        */
+/* simulated one decoding step (t_tok = 1 ms) at a time                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * N decoders with a KV capacity of C tokens each serve n requests taken in
+ * arrival order (arrival_ms non-decreasing, whole milliseconds).  Request i
+ * has prompt L_p = prompt[i] >= 0, output L_out = output[i] >= 1 and KV demand
+ * M = L_p + L_out (Eq. (8)), held from its admission to its completion.
+ * Routing: policy 0 is round robin, d = i mod N (Eq. (9), decoders counted
+ * from 0).  Policy 1 is Algorithm 1 at block size 1 on the decoders' state:
+ * B_need = L_p + bound[i]; B_eff(d) = C - K_d - (the needs of the requests
+ * waiting in d's queue, reserved when they were dispatched); Q_d the length of
+ * d's queue; the feasible decoder (B_need <= B_eff) with the shortest queue,
+ * else the largest B_eff, lowest index on ties; a request without a bound
+ * (bound < 0) goes round robin.
+ *
+ * Every millisecond t, in this order:
+ *   1. the request whose last token a decoder decoded during [t-1, t)
+ *      completes at t and releases its M tokens;
+ *   2. every decoder admits the head of its FIFO queue while K_d + M <= C
+ *      (Eq. (10)), again and again;
+ *   3. the requests arriving at t are routed in index order; a request is
+ *      admitted at once when its decoder's queue is empty and K_d + M <= C,
+ *      else it joins the queue;
+ *   4. the state for [t, t+1) is recorded: decoder d is under high pressure
+ *      when K_d / C >= theta (the HP interval definition), and its queue
+ *      length is added up;
+ *   5. every decoder decodes one token of the request at the head of its
+ *      ready queue (processor sharing by time slices of one token: one token
+ *      per t_tok in total, the admitted requests in turn); a request with
+ *      tokens left goes to the back of the ready queue, and a newly admitted
+ *      request joins it at the back.
+ * Outputs: finish_ms[i], routed[i]; per decoder hp_time (milliseconds under
+ * pressure within [first arrival, last completion)), hp_max (longest
+ * pressure interval), hp_count (number of intervals), max_queue and
+ * queue_area (sum over milliseconds of the queue length); span[0] = first
+ * arrival, span[1] = last completion.  theta is theta_ppm / 10^6.
+ * Returns -1 for invalid arguments, M > C or L_out < 1 in a request.
+ */
+int oracle_simulate(int32_t N, int64_t C, int32_t theta_ppm, int64_t n, const int64_t* arrival_ms,
+                    const int32_t* prompt, const int32_t* output, const int32_t* bound, int32_t policy,
+                    int64_t* finish_ms, int32_t* routed, int64_t* hp_time, int64_t* hp_max, int64_t* hp_count,
+                    int64_t* max_queue, int64_t* queue_area, int64_t* span)
+{
+    if (N < 1 || C < 1 || n < 1 || theta_ppm < 1 || theta_ppm > 1000000 || (policy != 0 && policy != 1)) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        if (prompt[i] < 0 || output[i] < 1 || (int64_t)prompt[i] + output[i] > C) return -1;
+        if (i > 0 && arrival_ms[i] < arrival_ms[i - 1]) return -1;
+    }
+    /* per decoder: the ready queue and the FIFO queue as plain arrays of
+     * request indices (front at index 0, shifted on removal) */
+    int64_t* ready = (int64_t*)malloc((size_t)N * n * sizeof(int64_t));
+    int64_t* fifo = (int64_t*)malloc((size_t)N * n * sizeof(int64_t));
+    int64_t* nready = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    int64_t* nfifo = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    int64_t* K = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    int64_t* R = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    int64_t* release = (int64_t*)malloc((size_t)N * sizeof(int64_t));
+    int64_t* run = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    int64_t* left = (int64_t*)malloc((size_t)n * sizeof(int64_t));
+    if (!ready || !fifo || !nready || !nfifo || !K || !R || !release || !run || !left) {
+        free(ready); free(fifo); free(nready); free(nfifo); free(K); free(R); free(release); free(run); free(left);
+        return -2;
+    }
+    for (int32_t d = 0; d < N; ++d) {
+        release[d] = -1;
+        hp_time[d] = hp_max[d] = hp_count[d] = max_queue[d] = queue_area[d] = 0;
+    }
+    for (int64_t i = 0; i < n; ++i) left[i] = output[i];
+#define DEMAND(i) ((int64_t)prompt[i] + output[i])
+#define NEED(i) ((int64_t)prompt[i] + bound[i])
+    int64_t t = arrival_ms[0], next = 0, done = 0;
+    span[0] = t;
+    span[1] = t;
+    for (;;) {
+        /* 1. completions */
+        for (int32_t d = 0; d < N; ++d) {
+            if (release[d] < 0) continue;
+            K[d] -= DEMAND(release[d]);
+            finish_ms[release[d]] = t;
+            release[d] = -1;
+            done += 1;
+            span[1] = t;
+        }
+        if (done == n) break;
+        /* a stretch with nothing admitted, queued or arriving: every decoder
+         * idle (no pressure, empty queues) until the next arrival */
+        int idle = 1;
+        for (int32_t d = 0; d < N; ++d) if (nready[d] || nfifo[d]) idle = 0;
+        if (idle && next < n && arrival_ms[next] > t) {
+            for (int32_t d = 0; d < N; ++d) run[d] = 0;
+            t = arrival_ms[next];
+        }
+        /* 2. FIFO admission */
+        for (int32_t d = 0; d < N; ++d) {
+            while (nfifo[d] > 0 && K[d] + DEMAND(fifo[(size_t)d * n]) <= C) {
+                int64_t i = fifo[(size_t)d * n];
+                for (int64_t k = 1; k < nfifo[d]; ++k) fifo[(size_t)d * n + k - 1] = fifo[(size_t)d * n + k];
+                nfifo[d] -= 1;
+                if (policy == 1 && bound[i] >= 0) R[d] -= NEED(i);
+                K[d] += DEMAND(i);
+                ready[(size_t)d * n + nready[d]++] = i;
+            }
+        }
+        /* 3. arrivals at t */
+        while (next < n && arrival_ms[next] == t) {
+            int64_t i = next++;
+            int32_t d;
+            if (policy == 1 && bound[i] >= 0) {
+                int32_t feas = -1, most = 0;
+                for (int32_t k = 0; k < N; ++k) {
+                    int64_t beff = C - K[k] - R[k];
+                    if (NEED(i) <= beff && (feas < 0 || nfifo[k] < nfifo[feas])) feas = k;
+                    if (beff > C - K[most] - R[most]) most = k;
+                }
+                d = feas >= 0 ? feas : most;
+            } else {
+                d = (int32_t)(i % N);
+            }
+            routed[i] = d;
+            if (nfifo[d] == 0 && K[d] + DEMAND(i) <= C) {
+                K[d] += DEMAND(i);
+                ready[(size_t)d * n + nready[d]++] = i;
+            } else {
+                fifo[(size_t)d * n + nfifo[d]++] = i;
+                if (policy == 1 && bound[i] >= 0) R[d] += NEED(i);
+            }
+        }
+        /* 4. the state over [t, t+1) */
+        for (int32_t d = 0; d < N; ++d) {
+            if (K[d] * 1000000 >= (int64_t)theta_ppm * C) {
+                if (run[d] == 0) hp_count[d] += 1;
+                run[d] += 1;
+                hp_time[d] += 1;
+                hp_max[d] = max64(hp_max[d], run[d]);
+            } else {
+                run[d] = 0;
+            }
+            queue_area[d] += nfifo[d];
+            max_queue[d] = max64(max_queue[d], nfifo[d]);
+        }
+        /* 5. one token per decoder, for the head of its ready queue */
+        for (int32_t d = 0; d < N; ++d) {
+            if (nready[d] == 0) continue;
+            int64_t* rq = ready + (size_t)d * n;
+            int64_t i = rq[0];
+            for (int64_t k = 1; k < nready[d]; ++k) rq[k - 1] = rq[k];
+            nready[d] -= 1;
+            left[i] -= 1;
+            if (left[i] == 0) release[d] = i;
+            else rq[nready[d]++] = i;
+        }
+        t += 1;
+    }
+#undef DEMAND
+#undef NEED
+    free(ready); free(fifo); free(nready); free(nfifo); free(K); free(R); free(release); free(run); free(left);
+    return 0;
 }

@@ -755,6 +755,311 @@ def pin_local_order_bruteforce(o):
                 assert adm[d] == (max(k_ok) if k_ok else 0), (trial, d, peaks, cap[d])
 
 
+# ---------------------------------------------------------------------------
+# placement with sequential commit (Sec. 3.3: each dispatch reserves its
+# demand before the next request is placed; Algorithm 1)
+# ---------------------------------------------------------------------------
+
+def py_place_commit(seg, p, g, U, cap, Q, ap, aU, policy, rr):
+    """Arrivals in order; every pair peak by brute force over the residents
+    plus the arrivals already committed to the decoder plus the arrival."""
+    D = len(seg) - 1
+    Q = [int(x) for x in Q]
+    committed = [[] for _ in range(D)]
+    out = []
+    for a in range(len(ap)):
+        if aU[a] < 0:
+            d = (rr + a) % D
+            Q[d] += 1
+            out.append((d, -1, 0, 2))
+            continue
+        peaks = []
+        for d in range(D):
+            lo, hi = seg[d], seg[d + 1]
+            peaks.append(py_peak(p[lo:hi], g[lo:hi], U[lo:hi], committed[d] + [(int(ap[a]), int(aU[a]))]))
+        slack = [int(cap[d]) - peaks[d] for d in range(D)]
+        feas = [d for d in range(D) if slack[d] >= 0]
+        if policy == 0 and feas:
+            d = min(feas, key=lambda k: (Q[k], k))
+        else:
+            d = max(range(D), key=lambda k: (slack[k], -k))
+        out.append((d, peaks[d], max(0, -slack[d]), 1 if slack[d] >= 0 else 0))
+        committed[d].append((int(ap[a]), int(aU[a])))
+        Q[d] += 1
+    return out, Q
+
+
+def pin_commit_bruteforce(o):
+    rng = _rng(31)
+    for trial in range(30):
+        D = int(rng.integers(1, 5))
+        seg, p, g, U = _tiny_decoders(rng, D, 5, 10, 15)
+        A = int(rng.integers(1, 10))
+        ap = rng.integers(0, 15, size=A).astype(np.int32)
+        aU = rng.integers(-1, 12, size=A).astype(np.int32)
+        cap = rng.integers(0, 160, size=D).astype(np.int32)
+        Q = rng.integers(0, 3, size=D).astype(np.int32)
+        rr = int(rng.integers(0, 5))
+        for policy in (0, 1):
+            r, q_after = o.place_commit(seg, p, g, U, cap, Q, ap, aU, policy=policy, rr_offset=rr)
+            want, want_q = py_place_commit(seg, p, g, U, cap, Q, ap, aU, policy, rr)
+            got = list(zip(r.choice.tolist(), r.chosen_peak.tolist(), r.chosen_overflow.tolist(), r.flags.tolist()))
+            assert got == want, (trial, policy, got, want)
+            assert q_after.tolist() == want_q, (trial, policy)
+
+
+def pin_commit_reduces_to_static_reserve(o):
+    """Every resident and every arrival with the same remaining length T: the
+    projected peak is the sum of the demands plus the arrival's, so sequential
+    commit is Algorithm 1 with reservation at block size 1 (B_need = p + T <=
+    B_eff, B_eff reduced by each dispatch's need, shortest queue, else largest
+    B_eff)."""
+    rng = _rng(32)
+    for trial in range(30):
+        D = int(rng.integers(1, 6))
+        T = int(rng.integers(0, 9))
+        counts = rng.integers(0, 4, size=D)
+        seg = np.zeros(D + 1, np.int64)
+        seg[1:] = np.cumsum(counts)
+        n = int(seg[-1])
+        p = rng.integers(0, 20, size=n).astype(np.int32)
+        g = rng.integers(0, 6, size=n).astype(np.int32)
+        U = (g + T).astype(np.int32)
+        A = int(rng.integers(1, 12))
+        ap = rng.integers(0, 20, size=A).astype(np.int32)
+        aU = np.where(rng.random(A) < 0.15, -1, T).astype(np.int32)
+        cap = rng.integers(0, 200, size=D).astype(np.int32)
+        Q = rng.integers(0, 3, size=D).astype(np.int32)
+        _, _, be = o.rsc_state(seg, p, g, U, cap, 1)
+        for policy in (0, 1):
+            r, q_after = o.place_commit(seg, p, g, U, cap, Q, ap, aU, policy=policy, rr_offset=3)
+            ch, need, fl, _, q_static = o.place_static(be, Q, 1, ap, aU, policy=policy, rr_offset=3, reserve=True)
+            assert r.choice.tolist() == ch.tolist(), (trial, policy)
+            assert r.flags.tolist() == fl.tolist(), (trial, policy)
+            assert q_after.tolist() == q_static.tolist()
+
+
+def pin_commit_single_decoder_and_first_arrival(o):
+    """With one decoder every arrival lands on it, and its chosen peak is the
+    brute-force peak of the residents plus every arrival so far; the first
+    arrival of any batch sees the snapshot alone (the independent placement)."""
+    rng = _rng(33)
+    for trial in range(20):
+        seg, p, g, U = _tiny_decoders(rng, 1, 6, 10, 15)
+        A = int(rng.integers(1, 8))
+        ap = rng.integers(0, 15, size=A).astype(np.int32)
+        aU = rng.integers(0, 12, size=A).astype(np.int32)
+        r, q_after = o.place_commit(seg, p, g, U, [10**6], [0], ap, aU)
+        for a in range(A):
+            assert r.choice[a] == 0
+            assert r.chosen_peak[a] == o.bruteforce_peak(p, g, U, ap[:a + 1], aU[:a + 1]), (trial, a)
+        assert q_after.tolist() == [A]
+        D = int(rng.integers(1, 5))
+        seg, p, g, U = _tiny_decoders(rng, D, 5, 10, 15)
+        cap = rng.integers(0, 150, size=D).astype(np.int32)
+        Q = rng.integers(0, 3, size=D).astype(np.int32)
+        ind = o.place(seg, p, g, U, cap, Q, ap[:1], aU[:1])
+        r, _ = o.place_commit(seg, p, g, U, cap, Q, ap, aU)
+        assert r.choice[0] == ind.choice[0] and r.chosen_peak[0] == ind.chosen_peak[0]
+        # committing never lowers a later pair's peak below its independent value
+        ind = o.place(seg, p, g, U, cap, Q, ap, aU)
+        assert np.all(r.chosen_peak >= ind.pair_peak[r.choice, np.arange(A)])
+
+
+# ---------------------------------------------------------------------------
+# staged reservation (appendix on the global algorithm: the prompt part of a
+# dispatch's reservation is released once the prompt KV reaches the decoder)
+# ---------------------------------------------------------------------------
+
+def pin_staged_reservation(o):
+    """A request still in transfer holds nothing and reserves its whole budget
+    ceil((p+U)/S) (its prompt's blocks without a bound); once its prompt has
+    arrived (g = 0) its prompt blocks are held and only the rest stays
+    reserved, so B_eff does not move at the transfer; B_free does."""
+    rng = _rng(34)
+    for trial in range(30):
+        D = int(rng.integers(1, 4))
+        seg, p, g, U = _tiny_decoders(rng, D, 6, 40, 60)
+        U = np.where(rng.random(U.size) < 0.2, -1, U).astype(np.int32)
+        cap = rng.integers(0, 400, size=D).astype(np.int32)
+        S = int(rng.choice([1, 2, 3, 16]))
+        fl = (rng.random(U.size) < 0.5).astype(np.uint8)
+        bf, br, be = o.rsc_state(seg, p, g, U, cap, S, in_flight=fl)
+        for d in range(D):
+            held = res = 0
+            for r in range(seg[d], seg[d + 1]):
+                if fl[r]:
+                    res += -(-(int(p[r]) + max(int(U[r]), 0)) // S)
+                else:
+                    now = -(-(int(p[r]) + int(g[r])) // S)
+                    held += now
+                    if U[r] >= 0:
+                        res += max(-(-(int(p[r]) + int(U[r])) // S) - now, 0)
+            assert bf[d] == int(cap[d]) // S - held and br[d] == res and be[d] == bf[d] - br[d], (trial, d)
+        # the transfer: every in-flight request lands with g = 0; B_eff unchanged where U >= 0
+        g0 = np.where(fl == 1, 0, g).astype(np.int32)
+        bf2, br2, be2 = o.rsc_state(seg, p, g0, U, cap, S)
+        if np.all(U[fl == 1] >= 0):
+            assert be2.tolist() == be.tolist(), trial
+        # in-flight requests are exactly the dispatches of Algorithm 1 with reservation
+    seg = np.array([0, 2], np.int64)
+    bf, br, be = o.rsc_state(seg, [5, 7], [0, 0], [10, 3], [100], 4, in_flight=[1, 1])
+    assert (bf[0], br[0], be[0]) == (25, 4 + 3, 25 - 7)
+
+
+# ---------------------------------------------------------------------------
+# App. A pressure simulation
+# ---------------------------------------------------------------------------
+
+def py_simulate(N, C, theta_ppm, arr, prompt, output, bound, policy):
+    """The same millisecond-by-millisecond definition, written with Python
+    deques: release, FIFO admission, arrivals, record, one token per decoder."""
+    from collections import deque
+    n = len(arr)
+    M = [int(prompt[i]) + int(output[i]) for i in range(n)]
+    need = [int(prompt[i]) + int(bound[i]) for i in range(n)]
+    ready = [deque() for _ in range(N)]
+    fifo = [deque() for _ in range(N)]
+    K = [0] * N
+    R = [0] * N
+    left = [int(x) for x in output]
+    rel = [None] * N
+    fin = [0] * n
+    routed = [0] * n
+    hp_t, hp_m, hp_c, mq, qa, run = ([0] * N for _ in range(6))
+    t, nxt, done = int(arr[0]), 0, 0
+    last = t
+    while True:
+        for d in range(N):
+            if rel[d] is not None:
+                K[d] -= M[rel[d]]
+                fin[rel[d]] = t
+                last = t
+                rel[d] = None
+                done += 1
+        if done == n:
+            break
+        if all(not ready[d] and not fifo[d] for d in range(N)) and nxt < n and arr[nxt] > t:
+            run = [0] * N
+            t = int(arr[nxt])
+        for d in range(N):
+            while fifo[d] and K[d] + M[fifo[d][0]] <= C:
+                i = fifo[d].popleft()
+                if policy == 1 and bound[i] >= 0:
+                    R[d] -= need[i]
+                K[d] += M[i]
+                ready[d].append(i)
+        while nxt < n and arr[nxt] == t:
+            i = nxt
+            nxt += 1
+            if policy == 1 and bound[i] >= 0:
+                beff = [C - K[k] - R[k] for k in range(N)]
+                feas = [k for k in range(N) if need[i] <= beff[k]]
+                d = min(feas, key=lambda k: (len(fifo[k]), k)) if feas else max(range(N), key=lambda k: (beff[k], -k))
+            else:
+                d = i % N
+            routed[i] = d
+            if not fifo[d] and K[d] + M[i] <= C:
+                K[d] += M[i]
+                ready[d].append(i)
+            else:
+                fifo[d].append(i)
+                if policy == 1 and bound[i] >= 0:
+                    R[d] += need[i]
+        for d in range(N):
+            if K[d] * 10**6 >= theta_ppm * C:
+                hp_c[d] += run[d] == 0
+                run[d] += 1
+                hp_t[d] += 1
+                hp_m[d] = max(hp_m[d], run[d])
+            else:
+                run[d] = 0
+            qa[d] += len(fifo[d])
+            mq[d] = max(mq[d], len(fifo[d]))
+        for d in range(N):
+            if ready[d]:
+                i = ready[d].popleft()
+                left[i] -= 1
+                if left[i] == 0:
+                    rel[d] = i
+                else:
+                    ready[d].append(i)
+        t += 1
+    return dict(finish_ms=fin, routed=routed, hp_time=hp_t, hp_max=hp_m, hp_count=hp_c, max_queue=mq,
+                queue_area=qa, span=[int(arr[0]), last])
+
+
+SIM_FIELDS = ("finish_ms", "routed", "hp_time", "hp_max", "hp_count", "max_queue", "queue_area", "span")
+
+
+def pin_simulate_golden(o):
+    for c in golden("simulate_hand.json")["cases"]:
+        r = o.simulate(c["N"], c["C"], c["theta_ppm"], c["arrival_ms"], c["prompt"], c["output"], c["bound"],
+                       c["policy"])
+        for f in SIM_FIELDS:
+            assert getattr(r, f).tolist() == c[f], (c["name"], f, getattr(r, f))
+
+
+def _sim_case(rng, n_max=14):
+    N = int(rng.integers(1, 4))
+    C = int(rng.choice([16, 20, 25, 32, 40]))   # divisors of 10^6: K / C can equal theta exactly
+    n = int(rng.integers(1, n_max))
+    arr = np.cumsum(rng.integers(0, 4, size=n)).astype(np.int64) + int(rng.integers(0, 3))
+    prompt = rng.integers(0, 8, size=n).astype(np.int32)
+    output = rng.integers(1, 9, size=n).astype(np.int32)
+    output = np.minimum(output, C - prompt).astype(np.int32)
+    bound = np.where(rng.random(n) < 0.2, -1, output + rng.integers(-2, 4, size=n)).astype(np.int32)
+    bound = np.where(bound < -1, 0, bound).astype(np.int32)
+    theta = int(rng.integers(1, 10**6 + 1)) if rng.random() < 0.3 else 10**6 * int(rng.integers(1, C + 1)) // C
+    return N, C, theta, arr, prompt, output, bound
+
+
+def pin_simulate_bruteforce(o):
+    rng = _rng(41)
+    for trial in range(60):
+        N, C, theta, arr, prompt, output, bound = _sim_case(rng)
+        for policy in (0, 1):
+            r = o.simulate(N, C, theta, arr, prompt, output, bound, policy)
+            want = py_simulate(N, C, theta, arr, prompt, output, bound, policy)
+            for f in SIM_FIELDS:
+                assert getattr(r, f).tolist() == want[f], (trial, policy, f)
+
+
+def pin_simulate_closed_forms(o):
+    """One request alone completes after its output length; two requests
+    admitted together share the decoder one token at a time (the first of x
+    tokens completes at 2x - 1 when x <= y, the second at 2y when y < x, the
+    last at x + y); without memory pressure each decoder is work conserving;
+    Algorithm 1 without any bound is round robin."""
+    r = o.simulate(1, 100, 500000, [7], [30], [25])
+    assert r.finish_ms.tolist() == [32] and r.hp_time.tolist() == [25] and r.hp_count.tolist() == [1]
+    for x in range(1, 6):
+        for y in range(1, 6):
+            r = o.simulate(1, 1000, 10**6, [0, 0], [0, 0], [x, y])
+            want = [2 * x - 1, x + y] if x <= y else [x + y, 2 * y]
+            assert r.finish_ms.tolist() == want, (x, y)
+    rng = _rng(42)
+    for trial in range(20):
+        N = int(rng.integers(1, 4))
+        n = int(rng.integers(1, 12))
+        out = rng.integers(1, 9, size=n).astype(np.int32)
+        pr = rng.integers(0, 5, size=n).astype(np.int32)
+        r = o.simulate(N, 10**6, 10**6, np.zeros(n, np.int64), pr, out)
+        assert r.routed.tolist() == [i % N for i in range(n)]
+        for d in range(N):
+            mine = [i for i in range(n) if i % N == d]
+            if mine:
+                assert max(r.finish_ms[mine]) == int(out[mine].sum()), (trial, d)
+        N, C, theta, arr, prompt, output, bound = _sim_case(rng)
+        r0 = o.simulate(N, C, theta, arr, prompt, output, None, 0)
+        r1 = o.simulate(N, C, theta, arr, prompt, output, None, 1)
+        for f in SIM_FIELDS:
+            assert getattr(r0, f).tolist() == getattr(r1, f).tolist(), (trial, f)
+        assert np.all(r0.finish_ms >= arr + output)
+        assert np.all(r0.hp_max <= r0.hp_time) and np.all(r0.hp_count <= r0.hp_time)
+        assert np.all(r0.hp_time <= r0.span[1] - r0.span[0]) and r0.span[1] == r0.finish_ms.max()
+
+
 ALL_PINS = [
     pin_calibrate_golden, pin_rank_is_ceiling, pin_quantile_order_statistic,
     pin_quantile_special_cases, pin_quantile_monotone_in_alpha, pin_coverage,
@@ -766,4 +1071,7 @@ ALL_PINS = [
     pin_place_golden, pin_occupancy_bruteforce, pin_bruteforce_peak, pin_place_bruteforce, pin_place_closed_forms,
     pin_place_invariants, pin_place_reduces_to_algorithm1, pin_round_robin_and_ties,
     pin_local_order_golden, pin_local_order_bruteforce,
+    pin_commit_bruteforce, pin_commit_reduces_to_static_reserve, pin_commit_single_decoder_and_first_arrival,
+    pin_staged_reservation,
+    pin_simulate_golden, pin_simulate_bruteforce, pin_simulate_closed_forms,
 ]

@@ -86,6 +86,30 @@ MUTANTS = [
      "            if (t <= V[k]) occ += (int64_t)q[k];"),
     ("bruteforce_resident_leaves_early", "if (t <= remaining(U[r], g[r])) occ += (int64_t)p[r] + g[r] + t;",
      "if (t < remaining(U[r], g[r])) occ += (int64_t)p[r] + g[r] + t;"),
+    ("commit_no_growth", "for (int64_t t = 0; t <= a_U[a]; ++t) o[t] += (int64_t)a_p[a] + t;",
+     "for (int64_t t = 0; t <= a_U[a]; ++t) o[t] += (int64_t)a_p[a];"),
+    ("commit_not_applied", "o[t] += (int64_t)a_p[a] + t;", "o[t] += 0;"),
+    ("commit_stale_prefix_max", "o[t] += (int64_t)a_p[a] + t;\n"
+     "        for (int64_t t = 0; t <= T; ++t) pr[t] = (t == 0) ? o[0] : max64(pr[t - 1], o[t] + t);",
+     "o[t] += (int64_t)a_p[a] + t;\n"),
+    ("commit_queue_not_counted", "        choice[a] = best;\n        Q[best] += 1;", "        choice[a] = best;"),
+    ("commit_rr_not_enqueued", "            flags[a] = 2;\n            Q[d] += 1;", "            flags[a] = 2;"),
+    ("staged_in_flight_held", "res += U[r] < 0 ? ceil_div((int64_t)p[r], S) : ceil_div((int64_t)p[r] + U[r], S);",
+     "held += U[r] < 0 ? ceil_div((int64_t)p[r], S) : ceil_div((int64_t)p[r] + U[r], S);"),
+    ("staged_in_flight_prompt_only",
+     "res += U[r] < 0 ? ceil_div((int64_t)p[r], S) : ceil_div((int64_t)p[r] + U[r], S);",
+     "res += ceil_div((int64_t)p[r], S);"),
+    ("sim_serves_newest", "int64_t i = rq[0];\n            for (int64_t k = 1; k < nready[d]; ++k) rq[k - 1] = rq[k];",
+     "int64_t i = rq[nready[d] - 1];"),
+    ("sim_run_to_completion", "else rq[nready[d]++] = i;",
+     "else { for (int64_t k = nready[d]; k > 0; --k) rq[k] = rq[k - 1]; rq[0] = i; nready[d]++; }"),
+    ("sim_fifo_bypass", "if (nfifo[d] == 0 && K[d] + DEMAND(i) <= C) {", "if (K[d] + DEMAND(i) <= C) {"),
+    ("sim_pressure_strict", "if (K[d] * 1000000 >= (int64_t)theta_ppm * C) {",
+     "if (K[d] * 1000000 > (int64_t)theta_ppm * C) {"),
+    ("sim_finish_late", "finish_ms[release[d]] = t;", "finish_ms[release[d]] = t + 1;"),
+    ("sim_no_reservation", "int64_t beff = C - K[k] - R[k];", "int64_t beff = C - K[k];"),
+    ("sim_longest_queue", "(feas < 0 || nfifo[k] < nfifo[feas])", "(feas < 0 || nfifo[k] > nfifo[feas])"),
+    ("sim_rr_shifted", "d = (int32_t)(i % N);", "d = (int32_t)((i + 1) % N);"),
     ("missing_bound_zero", "int64_t Ui = q_U[qlo + i] < 0 ? u_max : q_U[qlo + i];",
      "int64_t Ui = q_U[qlo + i] < 0 ? 0 : q_U[qlo + i];"),
 ]
