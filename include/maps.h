@@ -73,8 +73,13 @@ enum {
                                        every workgroup of the launch at once) */
     MAPS_ERR_SEEN_RANGE = 512u,     /* a seen count outside [0, n] (sliding-window
                                        calibration) */
-    MAPS_ERR_BLOCK_RANGE = 1024u    /* an effective block count left (-2^52, 2^52)
+    MAPS_ERR_BLOCK_RANGE = 1024u,   /* an effective block count left (-2^52, 2^52)
                                        during reserving placement */
+    MAPS_ERR_SIM_INPUT = 2048u,     /* simulation: a request with L_p < 0, L_out < 1 or
+                                       L_p + L_out > C, or arrival times that decrease
+                                       (such a request is dropped) */
+    MAPS_ERR_SIM_READY = 4096u      /* simulation: a decoder would have held more than
+                                       MAPS_MAX_SIM_READY admitted requests */
 };
 
 /* Largest u_max (cap on bounds and remaining lengths) the snapshot accepts,
@@ -92,6 +97,14 @@ enum {
 
 /* Most decoders that maps_place_static accepts with reservation. */
 #define MAPS_MAX_RESERVE_DECODERS 1024
+
+/* Most decoders and largest u_max of placement with sequential commit. */
+#define MAPS_MAX_COMMIT_DECODERS 8192
+#define MAPS_MAX_COMMIT_U_MAX (1 << 20)
+
+/* Most decoders of one simulation and most admitted requests per decoder. */
+#define MAPS_MAX_SIM_DECODERS 8
+#define MAPS_MAX_SIM_READY 1024
 
 /* Largest u_max and block size of the placement in blocks. */
 #define MAPS_MAX_BLOCKS_U_MAX 131072
@@ -232,6 +245,44 @@ maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,
                        hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* 3a. Placement with sequential commit (Sec. 3.3: each dispatch atomically */
+/*     reserves its demand before the next request is placed; Algorithm 1)  */
+/* ------------------------------------------------------------------------ */
+/*
+ * maps_place's rule for arrivals a = 0..A-1 taken one after another, each
+ * seeing the arrivals before it: after arrival a chooses decoder d, it is
+ * committed to d -- it holds p_a + t at step t while t <= U_a, like a
+ * resident with g = 0 and R = U_a -- and d's queue length grows by one.  So
+ *   peak(a, d) = max_t [ O_d(t) + sum_{b < a, choice b = d} [t <= U_b](p_b + t)
+ *                        + [t <= U_a](p_a + t) ],
+ * and policy MQ compares the running queue lengths queue_len[d] + (arrivals
+ * already sent to d).  An arrival without a bound (a_upper < 0) goes round
+ * robin, (rr_offset + a) mod D, joins that queue and commits no occupancy.
+ * The snapshot is maps_project's for (D, u_max); every a_upper <= u_max.
+ * Outputs per arrival: choice, chosen_peak (int64, -1 for round robin),
+ * chosen_overflow (int64, max(0, peak - capacity)), flags (bit0 feasible,
+ * bit1 round robin); queue_out [D] (nullable): queue lengths after the batch.
+ * With A = 1 the outputs equal maps_place's.
+ * workspace: maps_place_commit_workspace_size(D, u_max) bytes (four dense
+ * int64 arrays over the step axis per decoder: 32 (u_max + 1) bytes per
+ * decoder), caller-owned, not shared by calls in flight.  The chain is serial:
+ * one workgroup takes the arrivals in order.
+ * dev_err bits: NEG_LEN (a_prompt of an arrival with a bound, capacity or
+ * queue_len < 0), BOUND_RANGE (a_upper > u_max: evaluated at u_max),
+ * SNAPSHOT.
+ * Host errors: NULL, SIZE (D < 1 or D > MAPS_MAX_COMMIT_DECODERS, A < 0,
+ * rr_offset < 0, u_max < 0 or u_max > MAPS_MAX_COMMIT_U_MAX), POLICY,
+ * WORKSPACE, HIP.
+ */
+size_t maps_place_commit_workspace_size(int32_t D, int32_t u_max);
+maps_status maps_place_commit(const void* snapshot, int32_t D, int32_t u_max, const int32_t* capacity,
+                              const int32_t* queue_len, const int32_t* a_prompt, const int32_t* a_upper,
+                              int64_t A, int32_t policy, int64_t rr_offset, int32_t* choice,
+                              int64_t* chosen_peak, int64_t* chosen_overflow, uint8_t* flags,
+                              int32_t* queue_out, uint32_t* dev_err, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* 3b. Algorithm 1 on block counts (Sec. 3.3: runtime state, Eq. (6),       */
 /*     Algorithm 1, the atomic reservation of B_need after a dispatch)      */
 /* ------------------------------------------------------------------------ */
@@ -243,11 +294,20 @@ maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,
  * U < 0 or when it holds more already);
  *   b_free[d] = floor(capacity[d] / S) - sum of held blocks,
  *   b_res[d]  = sum of reserved blocks,  b_eff[d] = b_free[d] - b_res[d].
+ * Staged reservation (the appendix on the global scheduling algorithm: the
+ * prompt part of a dispatch's reservation is released once the prompt KV
+ * reaches the decoder): in_flight (nullable, one byte per request) marks
+ * requests dispatched to the decoder whose prompt KV is still in transfer;
+ * such a request holds no block and reserves its whole budget
+ * ceil((p+U)/S) (ceil(p/S) without a bound); g is ignored for it.  When its
+ * transfer completes the caller clears its flag with g = 0: the prompt's
+ * blocks move from reserved to held and B_eff is unchanged.
  * Outputs int64 [D], device arrays.  dev_err bits: NEG_LEN (p, g or capacity
  * < 0), SEG_OFFSETS.  Host errors: NULL, SIZE (D < 1, n_total < 0, S < 1), HIP.
  */
 maps_status maps_rsc_state(int32_t D, const int64_t* seg_off, int64_t n_total, const int32_t* prompt,
-                           const int32_t* generated, const int32_t* upper, const int32_t* capacity,
+                           const int32_t* generated, const int32_t* upper, const uint8_t* in_flight,
+                           const int32_t* capacity,
                            int32_t block_size, int64_t* b_free, int64_t* b_res, int64_t* b_eff,
                            uint32_t* dev_err, hipStream_t stream);
 
@@ -370,6 +430,51 @@ maps_status maps_place_order(const void* snapshot, int32_t D, int32_t u_max,
                              int32_t* order, int32_t* admitted,
                              uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 5. KV pressure under round-robin or MAPS routing (App. A)                */
+/* ------------------------------------------------------------------------ */
+/*
+ * S independent simulations of N decoders with a KV capacity of C tokens
+ * each, serving the same n requests (prompt[i] = L_p >= 0, output[i] = L_out
+ * >= 1, bound[i] = calibrated bound or < 0 for none; host-side arrays are not
+ * accepted: all are device arrays) at simulation s's arrival times
+ * arrival_ms[s][i] (whole milliseconds, non-decreasing in i).  Request i holds
+ * M = L_p + L_out tokens from its admission to its completion (Eq. (8)).
+ * Routing, policy[s]: 0 round robin, d = i mod N (Eq. (9), decoders counted
+ * from 0); 1 Algorithm 1 at block size 1 with B_need = L_p + bound,
+ * B_eff(d) = C - K_d - (needs of the requests waiting in d's queue) and
+ * Q_d = d's queue length (shortest queue among B_need <= B_eff, else the
+ * largest B_eff, lowest index on ties; no bound: round robin).
+ * Each millisecond t: (1) a request whose last token was decoded during
+ * [t-1, t) completes at t and releases M; (2) every decoder admits the head
+ * of its FIFO queue while K_d + M <= C (Eq. (10)); (3) the arrivals at t are
+ * routed in index order and admitted at once when the decoder's queue is
+ * empty and K_d + M <= C, else queued; (4) the state over [t, t+1) is
+ * recorded: high pressure when K_d / C >= theta_ppm / 10^6; (5) every
+ * decoder decodes one token for the request at the head of its ready queue
+ * (t_tok = 1 ms; processor sharing by one-token time slices), which goes to
+ * the back unless it is done; admissions join the back.
+ * Outputs: finish_ms[s][i] (completion time), routed[s][i] (decoder;
+ * nullable), stats[s][5][N] = per decoder the time under high pressure
+ * within [first arrival, last completion), the longest high-pressure
+ * interval, the number of intervals, the longest FIFO queue and the sum over
+ * milliseconds of the FIFO queue length; span[s][2] = first arrival, last
+ * completion.  The high-pressure fraction of App. A is stats[s][0][d] /
+ * (span[s][1] - span[s][0]).
+ * workspace: maps_simulate_workspace_size(N, n, S) bytes (the FIFO queues).
+ * One wavefront per simulation; N <= MAPS_MAX_SIM_DECODERS and at most
+ * MAPS_MAX_SIM_READY admitted requests per decoder at a time.
+ * dev_err bits: SIM_INPUT, SIM_READY (outputs unspecified when set).
+ * Host errors: NULL, SIZE (N out of range, C < 1, n < 1 or n > INT32_MAX,
+ * S < 0, theta_ppm not in [1, 10^6]), WORKSPACE, HIP.
+ */
+size_t maps_simulate_workspace_size(int32_t N, int64_t n, int32_t S);
+maps_status maps_simulate(int32_t N, int64_t C, int32_t theta_ppm, int64_t n, int32_t S,
+                          const int64_t* arrival_ms, const int32_t* prompt, const int32_t* output,
+                          const int32_t* bound, const int32_t* policy, int64_t* finish_ms,
+                          int32_t* routed, int64_t* stats, int64_t* span, uint32_t* dev_err,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Static description of a status code (host). */
 const char* maps_status_string(maps_status status);

@@ -28,7 +28,7 @@ MAX_LOCAL_QUEUE = 2048
 ERR_BITS = {
     1: "NEG_LEN", 2: "EDGES_UNSORTED", 4: "INT32_RANGE", 8: "SEG_OFFSETS",
     16: "BOUND_RANGE", 32: "SNAPSHOT", 64: "QUEUE_TOO_LONG", 128: "TOO_MANY", 256: "WAIT_TIMEOUT",
-    512: "SEEN_RANGE", 1024: "BLOCK_RANGE",
+    512: "SEEN_RANGE", 1024: "BLOCK_RANGE", 2048: "SIM_INPUT", 4096: "SIM_READY",
 }
 MAX_RESERVE_DECODERS = 1024
 MAX_BLOCKS_U_MAX = 131072
@@ -36,6 +36,10 @@ MAX_BLOCK_SIZE = 64
 MAX_WINDOW = 4096
 MAX_WINDOW_BUCKETS = 1024
 MAX_U_MAX = (1 << 24) - 64
+MAX_SIM_DECODERS = 8
+MAX_SIM_READY = 1024
+MAX_COMMIT_DECODERS = 8192
+MAX_COMMIT_U_MAX = 1 << 20
 
 
 class MapsError(RuntimeError):
@@ -55,7 +59,7 @@ _SIGNATURES = {
     "maps_project_blocks": (_i32, [_i32, _vp, _vp, _vp, _vp, _i64, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
     "maps_place_blocks": (_i32, [_vp, _vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp]),
-    "maps_rsc_state": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "maps_rsc_state": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp]),
     "maps_place_static": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp, _i64, _i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp,
                                  _vp, _vp]),
     "maps_snapshot_bytes": (_sz, [_i32, _i64, _i32]),
@@ -69,6 +73,12 @@ _SIGNATURES = {
                                 _vp, _sz, _vp]),
     "maps_place_order": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp,
                                 _vp, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "maps_place_commit_workspace_size": (_sz, [_i32, _i32]),
+    "maps_place_commit": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _i32, _i64, _vp, _vp, _vp, _vp, _vp,
+                                 _vp, _vp, _sz, _vp]),
+    "maps_simulate_workspace_size": (_sz, [_i32, _i64, _i32]),
+    "maps_simulate": (_i32, [_i32, _i64, _i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                             _sz, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)
@@ -300,6 +310,50 @@ def place(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, policy: in
     return out
 
 
+def place_commit_workspace_bytes(D: int, u_max: int) -> int:
+    return int(library().maps_place_commit_workspace_size(int(D), int(u_max)))
+
+
+@dataclass
+class CommitPlacement:
+    choice: torch.Tensor
+    chosen_peak: torch.Tensor       # int64
+    chosen_overflow: torch.Tensor   # int64
+    flags: torch.Tensor
+    queue_out: torch.Tensor
+    dev_err: torch.Tensor
+
+
+def place_commit(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, policy: int = POLICY_MQ,
+                 rr_offset: int = 0, dev_err=None, workspace=None,
+                 out: CommitPlacement | None = None) -> CommitPlacement:
+    """Arrivals placed one after another, each committed to its decoder's
+    projected occupancy and queue before the next (Sec. 3.3, Algorithm 1)."""
+    capacity = _dev(capacity, torch.int32, "capacity")
+    dev = capacity.device
+    queue_len = _dev(queue_len, torch.int32, "queue_len")
+    a_prompt = _dev(a_prompt, torch.int32, "a_prompt")
+    a_upper = _dev(a_upper, torch.int32, "a_upper")
+    D, A = snapshot.D, a_prompt.numel()
+    if capacity.numel() != D or queue_len.numel() != D or a_upper.numel() != A:
+        raise MapsError("capacity/queue_len must have D entries and a_upper A entries")
+    if out is None:
+        out = CommitPlacement(choice=torch.empty(A, dtype=torch.int32, device=dev),
+                              chosen_peak=torch.empty(A, dtype=torch.int64, device=dev),
+                              chosen_overflow=torch.empty(A, dtype=torch.int64, device=dev),
+                              flags=torch.empty(A, dtype=torch.uint8, device=dev),
+                              queue_out=torch.empty(D, dtype=torch.int32, device=dev),
+                              dev_err=new_error_word(dev) if dev_err is None else dev_err)
+    lib = library()
+    ws = _workspace(lib.maps_place_commit_workspace_size(D, snapshot.u_max), dev, workspace)
+    st = lib.maps_place_commit(_ptr(snapshot.data), D, snapshot.u_max, _ptr(capacity), _ptr(queue_len),
+                               _ptr(a_prompt), _ptr(a_upper), A, int(policy), int(rr_offset), _ptr(out.choice),
+                               _ptr(out.chosen_peak), _ptr(out.chosen_overflow), _ptr(out.flags),
+                               _ptr(out.queue_out), _ptr(out.dev_err), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "maps_place_commit")
+    return out
+
+
 # ---------------------------------------------------------------------------
 # 4. local order (Sec. 3.3, Eq. (7); App. A, Eq. (10))
 # ---------------------------------------------------------------------------
@@ -403,8 +457,9 @@ def place_blocks(snapshot: BlockSnapshot, capacity, queue_len, a_prompt, a_upper
 # 3b. Algorithm 1 on block counts
 # ---------------------------------------------------------------------------
 
-def rsc_state(seg_off, prompt, generated, upper, capacity, block_size: int, dev_err=None, out=None):
-    """Runtime state per decoder in blocks: (b_free, b_res, b_eff, dev_err), int64 [D]."""
+def rsc_state(seg_off, prompt, generated, upper, capacity, block_size: int, dev_err=None, out=None, in_flight=None):
+    """Runtime state per decoder in blocks: (b_free, b_res, b_eff, dev_err), int64 [D].
+    in_flight (optional uint8 per request): prompt KV still in transfer."""
     seg_off = _dev(seg_off, torch.int64, "seg_off")
     dev = seg_off.device
     D = seg_off.numel() - 1
@@ -416,9 +471,14 @@ def rsc_state(seg_off, prompt, generated, upper, capacity, block_size: int, dev_
     capacity = _dev(capacity, torch.int32, "capacity")
     if capacity.numel() != D:
         raise MapsError("capacity must have D entries")
+    if in_flight is not None:
+        _dev(in_flight, torch.uint8, "in_flight")
+        if in_flight.numel() != n:
+            raise MapsError("in_flight must have one entry per request")
     bf, br, be = out if out is not None else [torch.empty(D, dtype=torch.int64, device=dev) for _ in range(3)]
     err = new_error_word(dev) if dev_err is None else dev_err
-    st = library().maps_rsc_state(D, _ptr(seg_off), n, _ptr(prompt), _ptr(generated), _ptr(upper), _ptr(capacity),
+    st = library().maps_rsc_state(D, _ptr(seg_off), n, _ptr(prompt), _ptr(generated), _ptr(upper), _ptr(in_flight),
+                                  _ptr(capacity),
                                   int(block_size), _ptr(bf), _ptr(br), _ptr(be), _ptr(err), _stream(dev))
     _check(st, "maps_rsc_state")
     return bf, br, be, err
@@ -497,3 +557,47 @@ def place_order(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, q_of
                               _ptr(out.dev_err), _ptr(ws), ws.numel(), _stream(dev))
     _check(st, "maps_place_order")
     return out, order, admitted
+
+
+# ---------------------------------------------------------------------------
+# 5. KV pressure under round-robin or MAPS routing (App. A)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Simulation:
+    finish_ms: torch.Tensor   # int64 [S][n]
+    routed: torch.Tensor      # int32 [S][n]
+    stats: torch.Tensor       # int64 [S][5][N]: hp_time, hp_max, hp_count, max_queue, queue_area
+    span: torch.Tensor        # int64 [S][2]: first arrival, last completion
+    dev_err: torch.Tensor
+
+
+def simulate(N: int, C: int, theta_ppm: int, arrival_ms, prompt, output, bound, policy, dev_err=None,
+             workspace=None, out: Simulation | None = None) -> Simulation:
+    """S simulations (rows of arrival_ms, one policy each: 0 round robin, 1
+    Algorithm 1) of the same requests on N decoders of C tokens."""
+    arrival_ms = _dev(arrival_ms, torch.int64, "arrival_ms")
+    dev = arrival_ms.device
+    if arrival_ms.dim() != 2:
+        raise MapsError("arrival_ms must be [S][n]")
+    S, n = arrival_ms.shape
+    for name, t in (("prompt", prompt), ("output", output), ("bound", bound)):
+        _dev(t, torch.int32, name)
+        if t.numel() != n:
+            raise MapsError(f"{name} must have n entries")
+    policy = _dev(policy, torch.int32, "policy")
+    if policy.numel() != S:
+        raise MapsError("policy must have S entries")
+    if out is None:
+        out = Simulation(finish_ms=torch.empty((S, n), dtype=torch.int64, device=dev),
+                         routed=torch.empty((S, n), dtype=torch.int32, device=dev),
+                         stats=torch.empty((S, 5, N), dtype=torch.int64, device=dev),
+                         span=torch.empty((S, 2), dtype=torch.int64, device=dev),
+                         dev_err=new_error_word(dev) if dev_err is None else dev_err)
+    lib = library()
+    ws = _workspace(lib.maps_simulate_workspace_size(int(N), int(n), int(S)), dev, workspace)
+    st = lib.maps_simulate(int(N), int(C), int(theta_ppm), int(n), int(S), _ptr(arrival_ms), _ptr(prompt),
+                           _ptr(output), _ptr(bound), _ptr(policy), _ptr(out.finish_ms), _ptr(out.routed),
+                           _ptr(out.stats), _ptr(out.span), _ptr(out.dev_err), _ptr(ws), ws.numel(), _stream(dev))
+    _check(st, "maps_simulate")
+    return out

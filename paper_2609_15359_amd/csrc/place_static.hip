@@ -3,7 +3,8 @@
 // dispatch) on gfx950.
 //
 //   rsc_state           one workgroup per decoder: held and reserved blocks of
-//                       its residents summed in 64-bit integers;
+//                       its residents (and of requests whose prompt KV is
+//                       still in transfer) summed in 64-bit integers;
 //   static_independent  every arrival against the reported state: the
 //                       decoders' (B_eff, Q) staged in LDS in tiles, each
 //                       thread scanning them for four arrivals at once (the
@@ -41,6 +42,7 @@ __device__ inline int64_t ceil_blocks(int64_t tokens, int64_t S) { return (token
 __global__ __launch_bounds__(kRscNT) void rsc_state(int32_t D, const int64_t* __restrict__ seg_off,
                                                     int64_t n_total, const int32_t* __restrict__ p,
                                                     const int32_t* __restrict__ g, const int32_t* __restrict__ U,
+                                                    const uint8_t* __restrict__ in_flight,
                                                     const int32_t* __restrict__ cap, int32_t S,
                                                     int64_t* __restrict__ b_free, int64_t* __restrict__ b_res,
                                                     int64_t* __restrict__ b_eff, uint32_t* dev_err) {
@@ -58,6 +60,13 @@ __global__ __launch_bounds__(kRscNT) void rsc_state(int32_t D, const int64_t* __
     bool bad = false;
     for (int64_t r = lo + threadIdx.x; r < hi; r += kRscNT) {
         const int32_t pr = p[r], gr = g[r], ur = U[r];
+        if (in_flight && in_flight[r]) {
+            // staged reservation: prompt KV still in transfer, nothing held,
+            // the whole budget (the prompt's blocks without a bound) reserved
+            bad |= pr < 0;
+            res += ceil_blocks(int64_t(pr) + (ur < 0 ? 0 : ur), S);
+            continue;
+        }
         bad |= (pr < 0) | (gr < 0);
         const int64_t now = ceil_blocks(int64_t(pr) + gr, S);
         const int64_t demand = ur < 0 ? now : ceil_blocks(int64_t(pr) + ur, S);
@@ -313,7 +322,8 @@ __global__ void static_check_range(StaticArgs a) {
 using namespace maps;
 
 extern "C" maps_status maps_rsc_state(int32_t D, const int64_t* seg_off, int64_t n_total, const int32_t* prompt,
-                                      const int32_t* generated, const int32_t* upper, const int32_t* capacity,
+                                      const int32_t* generated, const int32_t* upper, const uint8_t* in_flight,
+                                      const int32_t* capacity,
                                       int32_t block_size, int64_t* b_free, int64_t* b_res, int64_t* b_eff,
                                       uint32_t* dev_err, hipStream_t stream) {
     if (D < 1 || n_total < 0 || block_size < 1) return MAPS_E_SIZE;
@@ -321,7 +331,7 @@ extern "C" maps_status maps_rsc_state(int32_t D, const int64_t* seg_off, int64_t
         (n_total > 0 && (!prompt || !generated || !upper)))
         return MAPS_E_NULL;
     hipLaunchKernelGGL(rsc_state, dim3(unsigned(D)), dim3(kRscNT), 0, stream, D, seg_off, n_total, prompt,
-                       generated, upper, capacity, block_size, b_free, b_res, b_eff, dev_err);
+                       generated, upper, in_flight, capacity, block_size, b_free, b_res, b_eff, dev_err);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

@@ -1,0 +1,299 @@
+// KV pressure of decoders under round-robin or MAPS routing (App. A) on
+// gfx950: a batch of independent simulations, one wavefront each.
+//
+// Each simulation follows the requests of one arrival sequence through N
+// decoders of C KV tokens (App. A: demand M = L_p + L_out held from admission
+// to completion, FIFO admission while K + M <= C, one token per millisecond
+// per decoder shared by its admitted requests in one-token time slices) and
+// records the high-pressure intervals (K / C >= theta) of every decoder.
+//
+// The state only changes at arrivals and completions, so the wavefront jumps
+// from one such event to the next instead of stepping through milliseconds.
+// A decoder's ready queue is kept in LDS in service order (ids and tokens
+// left); between events it is brought up to date lazily: after m one-token
+// slices over n requests, the request at position k has received
+// m / n + [k < m mod n] tokens and the queue has rotated by m mod n (the lanes
+// read every entry, then write it back rotated).  The request at position k
+// completes after (left_k - 1) n + k + 1 slices, so the decoder's next
+// completion is a wavefront minimum; it stays valid until the decoder's queue
+// changes.  When a completion is due the completing request is the last of
+// the rotated queue, and an admission appends at the end: both O(1).  The
+// FIFO queues live in the workspace (one ring per decoder), the per-decoder
+// counters in LDS.  Every loop is bounded: an arrival or a completion is
+// consumed per event, and a simulation that could not progress reports an
+// error instead of spinning.
+#include "maps_internal.hpp"
+
+namespace maps {
+namespace {
+
+constexpr int kSimNT = kWave;      // one wavefront per simulation
+constexpr int kMaxDec = MAPS_MAX_SIM_DECODERS;
+constexpr int kReady = MAPS_MAX_SIM_READY;
+constexpr int kPerLane = kReady / kWave;
+constexpr int64_t kNever = INT64_MAX;
+
+struct SimArgs {
+    int32_t N;
+    int64_t C;
+    int32_t theta_ppm;
+    int64_t n;
+    int32_t S;
+    const int64_t* arrival;   // [S][n]
+    const int32_t* prompt;    // [n]
+    const int32_t* output;    // [n]
+    const int32_t* bound;     // [n]
+    const int32_t* policy;    // [S]
+    int64_t* finish;          // [S][n]
+    int32_t* routed;          // [S][n] (nullable)
+    int64_t* stats;           // [S][5][N]: hp_time, hp_max, hp_count, max_queue, queue_area
+    int64_t* span;            // [S][2]
+    int32_t* fifo;            // workspace [S][N][n]
+    uint32_t* dev_err;
+};
+
+struct DecState {             // per decoder, in LDS
+    int64_t K, R;             // tokens held; needs reserved by queued requests (policy 1)
+    int64_t next_done;        // time of the next completion (kNever when the ready queue is empty)
+    int64_t t_sync;           // the ready queue's tokens-left are as of this time
+    int64_t run, hp_time, hp_max, hp_count, max_queue, queue_area;
+    int32_t nready, q_head, q_count, pad;
+};
+
+__global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
+    extern __shared__ int32_t lds[];
+    __shared__ DecState st[kMaxDec];
+    const int s = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int32_t N = a.N;
+    const int64_t n = a.n, C = a.C;
+    int32_t* rid = lds;                         // [N][kReady] request ids in service order
+    int32_t* rleft = lds + N * kReady;          // [N][kReady] tokens left as of t_sync
+    const int64_t* arr = a.arrival + int64_t(s) * n;
+    int64_t* fin = a.finish + int64_t(s) * n;
+    int32_t* rout = a.routed ? a.routed + int64_t(s) * n : nullptr;
+    int32_t* fifo = a.fifo + int64_t(s) * N * n;
+    const int32_t policy = a.policy[s];
+    bool bad_input = false, ready_full = false;
+
+    if (lane < N) {
+        DecState z{};
+        z.next_done = kNever;
+        z.t_sync = arr[0];
+        st[lane] = z;
+    }
+    __syncthreads();
+
+    auto demand = [&](int64_t i) { return int64_t(a.prompt[i]) + a.output[i]; };
+    auto need = [&](int64_t i) { return int64_t(a.prompt[i]) + a.bound[i]; };
+
+    // bring decoder d's ready queue to time t: m slices since t_sync
+    auto sync = [&](int d, int64_t t) {
+        const int32_t nr = st[d].nready;
+        const int64_t m = t - st[d].t_sync;
+        __syncthreads();
+        if (nr > 0 && m > 0) {
+            const int64_t q = m / nr;
+            const int32_t r = int32_t(m % nr);
+            int32_t id[kPerLane], lf[kPerLane];
+#pragma unroll
+            for (int j = 0; j < kPerLane; ++j) {   // new position k takes old position (k + r) mod nr
+                const int32_t k = lane + j * kWave;
+                if (k < nr) {
+                    int32_t src = k + r;
+                    src = src >= nr ? src - nr : src;
+                    id[j] = rid[d * kReady + src];
+                    lf[j] = int32_t(rleft[d * kReady + src] - q - (src < r ? 1 : 0));
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kPerLane; ++j) {
+                const int32_t k = lane + j * kWave;
+                if (k < nr) {
+                    rid[d * kReady + k] = id[j];
+                    rleft[d * kReady + k] = lf[j];
+                }
+            }
+        }
+        __syncthreads();
+        if (lane == 0) st[d].t_sync = t;
+        __syncthreads();
+    };
+    // decoder d's next completion after a change of its ready queue (synced to t)
+    auto schedule = [&](int d, int64_t t) {
+        const int32_t nr = st[d].nready;
+        int64_t best = kNever;
+        for (int j = 0; j < kPerLane; ++j) {
+            const int32_t k = lane + j * kWave;
+            if (k < nr) {
+                const int64_t sk = int64_t(rleft[d * kReady + k] - 1) * nr + k + 1;
+                best = sk < best ? sk : best;
+            }
+        }
+        best = -wave_reduce_max(-best);   // the wavefront minimum (kNever = INT64_MAX negates safely)
+        __syncthreads();
+        if (lane == 0) st[d].next_done = nr > 0 ? t + best : kNever;
+        __syncthreads();
+    };
+    auto admit = [&](int d, int64_t i, int64_t t) {   // append to the ready queue (synced to t)
+        if (st[d].nready >= kReady) { ready_full = true; return false; }
+        sync(d, t);
+        if (lane == 0) {
+            const int32_t k = st[d].nready;
+            rid[d * kReady + k] = int32_t(i);
+            rleft[d * kReady + k] = a.output[i];
+            st[d].nready = k + 1;
+            st[d].K += demand(i);
+        }
+        __syncthreads();
+        return true;
+    };
+
+    int64_t t = arr[0], next = 0, done = 0, last = t;
+    uint32_t dirty = 0;   // decoders whose ready queue changed at t (bit d)
+    const int64_t max_events = 2 * n + 8;
+    for (int64_t ev = 0;; ++ev) {
+        if (ev > max_events) { bad_input = true; break; }
+        // 1. completions at t: the completing request is the last of the synced queue
+        for (int d = 0; d < N; ++d) {
+            if (st[d].next_done != t) continue;
+            sync(d, t);
+            if (lane == 0) {
+                const int32_t k = st[d].nready - 1;
+                const int64_t i = rid[d * kReady + k];
+                st[d].nready = k;
+                st[d].K -= demand(i);
+                fin[i] = t;
+            }
+            __syncthreads();
+            done += 1;
+            last = t;
+            dirty |= 1u << d;
+        }
+        if (done >= n) break;
+        // 2. FIFO admission
+        for (int d = 0; d < N; ++d) {
+            while (st[d].q_count > 0) {
+                const int64_t i = fifo[int64_t(d) * n + st[d].q_head];
+                if (st[d].K + demand(i) > C) break;
+                if (!admit(d, i, t)) break;
+                if (lane == 0) {
+                    st[d].q_head = st[d].q_head + 1 == n ? 0 : st[d].q_head + 1;
+                    st[d].q_count -= 1;
+                    if (policy == 1 && a.bound[i] >= 0) st[d].R -= need(i);
+                }
+                __syncthreads();
+                dirty |= 1u << d;
+            }
+        }
+        // 3. arrivals at t, in index order
+        while (next < n && arr[next] <= t) {
+            const int64_t i = next++;
+            if (arr[i] < t || a.prompt[i] < 0 || a.output[i] < 1 || demand(i) > C) {
+                bad_input = true;   // out of order or never admissible: dropped
+                if (lane == 0) fin[i] = t;
+                done += 1;
+                continue;
+            }
+            int d;
+            if (policy == 1 && a.bound[i] >= 0) {   // Algorithm 1 at block size 1
+                int feas = -1, most = 0;
+                for (int k = 0; k < N; ++k) {
+                    const int64_t beff = C - st[k].K - st[k].R;
+                    if (need(i) <= beff && (feas < 0 || st[k].q_count < st[feas].q_count)) feas = k;
+                    if (beff > C - st[most].K - st[most].R) most = k;
+                }
+                d = feas >= 0 ? feas : most;
+            } else {
+                d = int(i % N);
+            }
+            if (lane == 0 && rout) rout[i] = d;
+            bool queued = true;
+            if (st[d].q_count == 0 && st[d].K + demand(i) <= C) {
+                queued = !admit(d, i, t);
+                if (!queued) dirty |= 1u << d;
+            }
+            if (queued) {
+                if (lane == 0) {
+                    int64_t tail = st[d].q_head + st[d].q_count;
+                    tail = tail >= n ? tail - n : tail;
+                    fifo[int64_t(d) * n + tail] = int32_t(i);
+                    st[d].q_count += 1;
+                    if (policy == 1 && a.bound[i] >= 0) st[d].R += need(i);
+                }
+                __syncthreads();
+            }
+        }
+        if (done >= n) break;   // only dropped requests were left
+        for (int d = 0; d < N; ++d)
+            if (dirty & (1u << d)) schedule(d, t);
+        dirty = 0;
+        // the next event, and the state recorded over [t, t_next)
+        int64_t t_next = next < n ? arr[next] : kNever;
+        for (int d = 0; d < N; ++d) t_next = st[d].next_done < t_next ? st[d].next_done : t_next;
+        if (t_next == kNever || t_next <= t) { bad_input = true; break; }
+        const int64_t len = t_next - t;
+        if (lane < N) {
+            DecState& x = st[lane];
+            if (x.K * 1000000 >= int64_t(a.theta_ppm) * C) {
+                if (x.run == 0) x.hp_count += 1;
+                x.run += len;
+                x.hp_time += len;
+                x.hp_max = x.run > x.hp_max ? x.run : x.hp_max;
+            } else {
+                x.run = 0;
+            }
+            x.queue_area += int64_t(x.q_count) * len;
+            x.max_queue = x.q_count > x.max_queue ? x.q_count : x.max_queue;
+        }
+        __syncthreads();
+        t = t_next;
+    }
+    if (lane < N) {
+        int64_t* o = a.stats + int64_t(s) * 5 * N;
+        o[0 * N + lane] = st[lane].hp_time;
+        o[1 * N + lane] = st[lane].hp_max;
+        o[2 * N + lane] = st[lane].hp_count;
+        o[3 * N + lane] = st[lane].max_queue;
+        o[4 * N + lane] = st[lane].queue_area;
+    }
+    if (lane == 0) {
+        a.span[2 * int64_t(s)] = arr[0];
+        a.span[2 * int64_t(s) + 1] = last;
+        if (bad_input) raise_error(a.dev_err, MAPS_ERR_SIM_INPUT);
+        if (ready_full) raise_error(a.dev_err, MAPS_ERR_SIM_READY);
+    }
+}
+
+}  // namespace
+}  // namespace maps
+
+using namespace maps;
+
+extern "C" size_t maps_simulate_workspace_size(int32_t N, int64_t n, int32_t S) {
+    if (N < 1 || N > MAPS_MAX_SIM_DECODERS || n < 1 || S < 0) return 0;
+    return align256(size_t(S) * size_t(N) * size_t(n) * sizeof(int32_t));
+}
+
+extern "C" maps_status maps_simulate(int32_t N, int64_t C, int32_t theta_ppm, int64_t n, int32_t S,
+                                     const int64_t* arrival_ms, const int32_t* prompt, const int32_t* output,
+                                     const int32_t* bound, const int32_t* policy, int64_t* finish_ms,
+                                     int32_t* routed, int64_t* stats, int64_t* span, uint32_t* dev_err,
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (N < 1 || N > MAPS_MAX_SIM_DECODERS || C < 1 || n < 1 || n > INT32_MAX || S < 0 || theta_ppm < 1 ||
+        theta_ppm > 1000000)
+        return MAPS_E_SIZE;
+    if (S == 0) return MAPS_OK;
+    if (!arrival_ms || !prompt || !output || !bound || !policy || !finish_ms || !stats || !span || !dev_err ||
+        !workspace)
+        return MAPS_E_NULL;
+    if (workspace_bytes < maps_simulate_workspace_size(N, n, S)) return MAPS_E_WORKSPACE;
+    SimArgs a{N, C, theta_ppm, n, S, arrival_ms, prompt, output, bound, policy, finish_ms, routed, stats, span,
+              static_cast<int32_t*>(workspace), dev_err};
+    const size_t lds = size_t(N) * kReady * 2 * sizeof(int32_t);
+    allow_dynamic_lds(simulate_kernel, lds);
+    hipLaunchKernelGGL(simulate_kernel, dim3(unsigned(S)), dim3(kSimNT), lds, stream, a);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}

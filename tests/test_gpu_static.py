@@ -26,11 +26,13 @@ def _cuda(x, dtype=np.int32):
     return torch.from_numpy(np.ascontiguousarray(x, dtype=dtype)).cuda()
 
 
-def _rsc(seg, p, g, U, cap, S):
+def _rsc(seg, p, g, U, cap, S, in_flight=None):
     import torch
 
     import paper_2609_15359_amd as maps
-    bf, br, be, err = maps.rsc_state(_cuda(seg, np.int64), _cuda(p), _cuda(g), _cuda(U), _cuda(cap), S)
+    fl = None if in_flight is None else _cuda(in_flight, np.uint8)
+    bf, br, be, err = maps.rsc_state(_cuda(seg, np.int64), _cuda(p), _cuda(g), _cuda(U), _cuda(cap), S,
+                                     in_flight=fl)
     torch.cuda.synchronize()
     return bf.cpu().numpy(), br.cpu().numpy(), be.cpu().numpy(), int(err.item()) & 0xFFFFFFFF
 
@@ -140,3 +142,36 @@ def test_error_bits():
     assert got[5] & 1
     got = _static([5, 5], [0, 0], 16, [-1, 2], [3, 4], reserve=True)
     assert got[5] & 1
+
+
+@pytest.mark.parametrize("S", [1, 3, 16])
+def test_staged_reservation(orc, S):
+    """Requests whose prompt KV is still in transfer (whole budget reserved,
+    nothing held) mixed with residents: random ragged decoders and the large
+    workload with a tenth of its residents in flight."""
+    rng = np.random.default_rng(60 + S)
+    for trial in range(20):
+        D = int(rng.integers(1, 40))
+        counts = rng.integers(0, 700, size=D)
+        seg = np.zeros(D + 1, np.int64)
+        seg[1:] = np.cumsum(counts)
+        n = int(seg[-1])
+        p = rng.integers(0, 5000, size=n)
+        g = rng.integers(0, 3000, size=n)
+        U = np.where(rng.random(n) < 0.1, -1, rng.integers(0, 9000, size=n))
+        fl = (rng.random(n) < 0.3).astype(np.uint8)
+        cap = rng.integers(0, 2**31 - 1, size=D)
+        got = _rsc(seg, p, g, U, cap, S, fl)
+        assert got[3] == 0
+        want = orc.rsc_state(seg, p, g, U, cap, S, in_flight=fl)
+        for nm, gg, w in zip(("b_free", "b_res", "b_eff"), got[:3], want):
+            assert_same(f"{nm} trial {trial}", gg, w)
+    b = workload.make("large")
+    o = oracle.step(b, orc, want_pairs=False)
+    U_res, _, _ = b.split_bounds(o.U)
+    fl = (np.random.default_rng(7).random(U_res.size) < 0.1).astype(np.uint8)
+    got = _rsc(b.seg_off, b.res_prompt, b.res_gen, U_res, b.capacity, S, fl)
+    assert got[3] == 0
+    want = orc.rsc_state(b.seg_off, b.res_prompt, b.res_gen, U_res, b.capacity, S, in_flight=fl)
+    for nm, gg, w in zip(("b_free", "b_res", "b_eff"), got[:3], want):
+        assert_same(f"large {nm}", gg, w)
