@@ -79,6 +79,11 @@ _SIGNATURES = {
     "maps_simulate_workspace_size": (_sz, [_i32, _i64, _i32]),
     "maps_simulate": (_i32, [_i32, _i64, _i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                              _sz, _vp]),
+    "maps_window_state_bytes": (_sz, [_i32, _i32]),
+    "maps_window_append_workspace_size": (_sz, [_i64, _i32]),
+    "maps_window_reset": (_i32, [_vp, _sz, _i32, _i32, _vp]),
+    "maps_window_append": (_i32, [_vp, _sz, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "maps_window_bounds": (_i32, [_vp, _sz, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)
@@ -219,6 +224,60 @@ def calibrate_window(pred, truth, edges, window: int, alpha_ppm: int, apply_pred
                                    _stream(dev))
     _check(st, "maps_calibrate_window")
     return (q if want_q else None), U, err
+
+
+class WindowState:
+    """Incremental sliding-window calibration: per length bucket the count of
+    completions appended and a ring of the last `window` scores, kept in
+    device memory (Sec. 3.2; Sec. 4 uses a window of 500)."""
+
+    def __init__(self, edges: torch.Tensor, window: int, device=None):
+        self.edges = _dev(edges, torch.int32, "edges")
+        self.nb = edges.numel() + 1
+        self.window = int(window)
+        dev = edges.device if device is None else device
+        lib = library()
+        nbytes = int(lib.maps_window_state_bytes(self.nb, self.window))
+        if nbytes == 0:
+            raise MapsError("invalid (buckets, window)")
+        self.state = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self.dev_err = new_error_word(dev)
+        self.q = torch.empty(self.nb, dtype=torch.int32, device=dev)
+        self._ws = None
+        self.reset()
+
+    def reset(self):
+        _check(library().maps_window_reset(_ptr(self.state), self.state.numel(), self.nb, self.window,
+                                           _stream(self.state.device)), "maps_window_reset")
+
+    def append(self, pred, truth, workspace=None):
+        pred = _dev(pred, torch.int32, "pred")
+        truth = _dev(truth, torch.int32, "truth")
+        k = pred.numel()
+        if truth.numel() != k:
+            raise MapsError("pred and truth differ in length")
+        lib = library()
+        need = int(lib.maps_window_append_workspace_size(k, self.nb))
+        if workspace is None:
+            if self._ws is None or self._ws.numel() < need:
+                self._ws = torch.empty(max(need, 1), dtype=torch.uint8, device=self.state.device)
+            workspace = self._ws
+        st = lib.maps_window_append(_ptr(self.state), self.state.numel(), self.nb, self.window, _ptr(pred),
+                                    _ptr(truth), k, _ptr(self.edges) if self.nb > 1 else None, _ptr(self.dev_err),
+                                    _ptr(workspace), workspace.numel(), _stream(self.state.device))
+        _check(st, "maps_window_append")
+
+    def bounds(self, alpha_ppm: int, apply_pred=None, u_max: int = 0, U=None):
+        """Per-bucket quantiles of the current windows and the bounds of apply_pred."""
+        m = 0 if apply_pred is None else _dev(apply_pred, torch.int32, "apply_pred").numel()
+        if m and U is None:
+            U = torch.empty(m, dtype=torch.int32, device=self.state.device)
+        st = library().maps_window_bounds(_ptr(self.state), self.state.numel(), self.nb, self.window, int(alpha_ppm),
+                                          _ptr(self.edges) if self.nb > 1 else None, _ptr(apply_pred) if m else None,
+                                          m, int(u_max), _ptr(self.q), _ptr(U) if m else None, _ptr(self.dev_err),
+                                          _stream(self.state.device))
+        _check(st, "maps_window_bounds")
+        return self.q, U
 
 
 # ---------------------------------------------------------------------------

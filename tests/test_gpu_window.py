@@ -152,3 +152,104 @@ def test_error_bits():
     # no prediction: no bucket, no seen check
     q, U, err = _gpu(pred, truth, [], 10, 100000, [-1], [99], 100)
     assert err == 0 and q.tolist() == [-1] and U.tolist() == [-1]
+
+
+# ---------------------------------------------------------------------------
+# incremental window state (maps_window_reset / append / bounds)
+# ---------------------------------------------------------------------------
+
+def _bucket_reps(edges):
+    """One prediction per non-empty bucket range: 0 for bucket 0 (when the
+    first edge is above 0), each distinct edge for the bucket it opens."""
+    reps, buckets = [], []
+    e = list(int(x) for x in edges)
+    if not e or e[0] > 0:
+        reps.append(0)
+        buckets.append(0)
+    for j, x in enumerate(e):
+        if j + 1 < len(e) and e[j + 1] == x:
+            continue           # duplicated edge: the bucket it opens is empty
+        reps.append(x)
+        buckets.append(j + 1)
+    return np.array(reps, np.int32), buckets
+
+
+def _check_state(orc, st, pred, truth, edges, window, alpha, ap, u_max, tag):
+    import torch
+    n = len(pred)
+    q, U = st.bounds(alpha, _cuda(ap), u_max)
+    torch.cuda.synchronize()
+    assert int(st.dev_err.item()) == 0, tag
+    _, want_U = orc.calibrate_window(pred, truth, edges, window, alpha, ap, np.full(len(ap), n), u_max)
+    assert_same(f"{tag} U", U.cpu().numpy(), want_U)
+    reps, buckets = _bucket_reps(edges)
+    want_q, _ = orc.calibrate_window(pred, truth, edges, window, alpha, reps, np.full(len(reps), n), u_max)
+    assert_same(f"{tag} q", q.cpu().numpy()[buckets], want_q)
+
+
+@pytest.mark.parametrize("nb,window", [(1, 1), (3, 7), (8, 500), (64, 500), (200, 4096)])
+def test_incremental_window(orc, nb, window):
+    """Completions appended in batches of 0 to 3 windows (chunk edges, a
+    bucket wrapping its ring within one batch and across batches); after each
+    append every bucket's quantile and a batch of bounds equal the window
+    calibration of the whole log so far."""
+    import paper_2609_15359_amd as maps
+    rng = np.random.default_rng(nb * 31 + window)
+    total = 40000 if window < 4096 else 60000
+    pred = rng.integers(0, 5000, size=total).astype(np.int32)
+    truth = (pred + rng.integers(-900, 3000, size=total)).clip(0).astype(np.int32)
+    edges = np.sort(rng.integers(0, 5000, size=nb - 1)).astype(np.int32)
+    if nb > 3:
+        edges[1] = edges[2]   # a duplicated edge: an empty bucket
+    ap = np.concatenate([rng.integers(-1, 6000, size=3000 if window <= 500 else 300), [-1, 0]]).astype(np.int32)
+    st = maps.WindowState(_cuda(edges), window)
+    _check_state(orc, st, pred[:0], truth[:0], edges, window, 100000, ap, 8000, "empty log")
+    n = 0
+    sizes = [0, 1, 1023, 1024, 1025, window - 1, window, window + 1, 3 * window, 4096, 5000]
+    for step, k in enumerate(sizes + list(rng.integers(0, 3 * window + 2, size=8))):
+        k = int(min(k, total - n))
+        st.append(_cuda(pred[n:n + k]), _cuda(truth[n:n + k]))
+        n += k
+        for alpha in (50000, 100000):
+            _check_state(orc, st, pred[:n], truth[:n], edges, window, alpha, ap, 8000, f"nb={nb} w={window} n={n}")
+    say(f"[window-state] nb={nb} window={window}: {n} completions appended in {step + 1} batches")
+
+
+def test_incremental_window_large(orc):
+    """The large workload's 1,000,000 calibration pairs as the completion log,
+    appended in 16 batches, window 500, 64 buckets; the bounds of every
+    resident, arrival and queued request after the last batch (the state
+    calibration of the batch, against the oracle with every request having
+    seen the whole log) and sampled requests after each batch."""
+    import paper_2609_15359_amd as maps
+    b = workload.make("large")
+    ap = b.apply_pred()
+    st = maps.WindowState(_cuda(b.edges), 500)
+    n_all = b.cal_pred.size
+    cuts = np.linspace(0, n_all, 17).astype(np.int64)
+    idx = np.arange(0, ap.size, 97)
+    for j in range(16):
+        st.append(_cuda(b.cal_pred[cuts[j]:cuts[j + 1]]), _cuda(b.cal_truth[cuts[j]:cuts[j + 1]]))
+        n = int(cuts[j + 1])
+        _check_state(orc, st, b.cal_pred[:n], b.cal_truth[:n], b.edges, 500, b.alpha_ppm, ap[idx], b.u_max,
+                     f"large after {n}")
+    _check_state(orc, st, b.cal_pred, b.cal_truth, b.edges, 500, b.alpha_ppm, ap, b.u_max, "large all")
+
+
+def test_incremental_window_errors():
+    import torch
+
+    import paper_2609_15359_amd as maps
+    st = maps.WindowState(_cuda([10, 20]), 5)
+    st.append(_cuda([1, -2]), _cuda([3, 4]))
+    torch.cuda.synchronize()
+    assert int(st.dev_err.item()) & 1
+    st = maps.WindowState(_cuda([20, 10]), 5)
+    st.append(_cuda([1, 2]), _cuda([3, 4]))
+    torch.cuda.synchronize()
+    assert int(st.dev_err.item()) & 2
+    st = maps.WindowState(_cuda([10, 20]), 5)
+    st.state[:4] = 0    # not a reset state
+    st.bounds(100000)
+    torch.cuda.synchronize()
+    assert int(st.dev_err.item()) & 32
