@@ -68,9 +68,9 @@ enum {
     MAPS_ERR_SNAPSHOT = 32u,        /* snapshot was not built for this (D, u_max) */
     MAPS_ERR_QUEUE_TOO_LONG = 64u,  /* a local queue longer than MAPS_MAX_LOCAL_QUEUE */
     MAPS_ERR_TOO_MANY = 128u,       /* a decoder with MAPS_MAX_RESIDENTS or more residents */
-    MAPS_ERR_WAIT_TIMEOUT = 256u,   /* a workgroup's bounded wait for the other workgroups
-                                       of its launch ran out (the device did not hold
-                                       every workgroup of the launch at once) */
+    MAPS_ERR_WAIT_TIMEOUT = 256u,   /* reserved: no entry point raises it any more (a
+                                       bounded wait on another workgroup now falls back
+                                       to computing the value itself) */
     MAPS_ERR_SEEN_RANGE = 512u,     /* a seen count outside [0, n] (sliding-window
                                        calibration) */
     MAPS_ERR_BLOCK_RANGE = 1024u,   /* an effective block count left (-2^52, 2^52)
@@ -131,7 +131,11 @@ enum { MAPS_POLICY_MQ = 0, MAPS_POLICY_MC = 1 };
  *   U_out[i] = -1                          if apply_pred[i] < 0 (no prediction)
  *            = u_max                       if q of its bucket is MAPS_Q_INF
  *            = min(apply_pred[i] + q, u_max) otherwise.
- * dev_err bits: NEG_LEN (pred or truth < 0), EDGES_UNSORTED, WAIT_TIMEOUT.
+ * dev_err bits: NEG_LEN (pred or truth < 0), EDGES_UNSORTED.  (The bounds
+ * may be written by workgroups of the selection's own launch; such a workgroup
+ * waits a bounded time for each quantile and otherwise selects it itself, so
+ * the call neither needs its workgroups to run at the same time nor raises
+ * WAIT_TIMEOUT.)
  * Host errors: NULL, SIZE (n < 0, m < 0, nb < 1 or nb > 65536, u_max < 0),
  * ALPHA, WORKSPACE, HIP.
  */
@@ -177,6 +181,46 @@ maps_status maps_calibrate_window(const int32_t* pred, const int32_t* truth, int
                                   int32_t u_max, int32_t* q_out, int32_t* U_out,
                                   uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                                   hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 1c. Incremental sliding-window calibration (Sec. 3.2: the calibration    */
+/*     set holds the most recent completed requests; Sec. 4: window 500)    */
+/* ------------------------------------------------------------------------ */
+/*
+ * A caller-owned device state of maps_window_state_bytes(nb, window) bytes
+ * keeps, per length bucket b (b(i) = #{j : edges[j] <= pred[i]}, as for
+ * maps_calibrate), the number of completions appended so far and the scores
+ * s = max(0, truth - pred) (Eq. (2)) of its last `window` ones.
+ *   maps_window_reset   empties the state (enqueued on stream).
+ *   maps_window_append  appends k completions (pred[k], truth[k] >= 0, in
+ *                       completion order) to the log: only the newest `window`
+ *                       entries of each bucket are written, the rest of the
+ *                       state is untouched.  workspace of
+ *                       maps_window_append_workspace_size(k, nb) bytes.
+ *   maps_window_bounds  for the log as it stands (n entries appended in all):
+ *                       q_out[b] = the k-th smallest of bucket b's last
+ *                       n_w = min(count_b, window) scores, k = ceil((1 -
+ *                       alpha)(n_w + 1)) (Eq. (3)), MAPS_Q_INF when k > n_w;
+ *                       and for m predictions U_out[j] = -1 (apply_pred < 0),
+ *                       u_max (infinite q) or min(apply_pred + q, u_max)
+ *                       (Eq. (4)).  This is maps_calibrate_window with every
+ *                       apply_seen = n.
+ * dev_err bits: NEG_LEN, EDGES_UNSORTED (append); SNAPSHOT when the state was
+ * not reset for these (nb, window).
+ * Host errors: NULL, SIZE (nb < 1 or nb > MAPS_MAX_WINDOW_BUCKETS, window < 1
+ * or window > MAPS_MAX_WINDOW, k < 0 or k > INT32_MAX, m < 0, u_max < 0),
+ * ALPHA, BUFFER (state smaller than maps_window_state_bytes), WORKSPACE, HIP.
+ */
+size_t maps_window_state_bytes(int32_t nb, int32_t window);
+size_t maps_window_append_workspace_size(int64_t k, int32_t nb);
+maps_status maps_window_reset(void* state, size_t state_bytes, int32_t nb, int32_t window, hipStream_t stream);
+maps_status maps_window_append(void* state, size_t state_bytes, int32_t nb, int32_t window,
+                               const int32_t* pred, const int32_t* truth, int64_t k, const int32_t* edges,
+                               uint32_t* dev_err, void* workspace, size_t workspace_bytes, hipStream_t stream);
+maps_status maps_window_bounds(const void* state, size_t state_bytes, int32_t nb, int32_t window,
+                               int32_t alpha_ppm, const int32_t* edges, const int32_t* apply_pred, int64_t m,
+                               int32_t u_max, int32_t* q_out, int32_t* U_out, uint32_t* dev_err,
+                               hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 2. Projection of KV occupancy per decoder (Sec. 3.3; App. A, Eq. (8))    */

@@ -21,6 +21,8 @@
 // pass and one selection kernel per 8-bit digit (cal_score, cal_rank,
 // cal_hist, cal_select, cal_finish), histograms in LDS for up to 128 buckets.
 // All reductions are integer additions, so the result is deterministic.
+#include <cstdlib>
+
 #include "maps_internal.hpp"
 
 namespace maps {
@@ -480,7 +482,7 @@ struct SelectArgs {
 // bucket of at most kSelNT * kKeep scores is gathered once (runs into LDS,
 // then into registers) and kept across passes; a larger one is read from its
 // runs on every pass.
-__device__ void select_bucket(const SelectArgs& A, int b) {
+__device__ int32_t select_bucket(const SelectArgs& A, int b) {
     const int nb = A.nb;
     const int64_t chunks = A.chunks;
     const int32_t alpha_ppm = A.alpha_ppm;
@@ -516,7 +518,7 @@ __device__ void select_bucket(const SelectArgs& A, int b) {
     if (k64 > int64_t(nbk)) {
         if (t == 0) q_out[b] = MAPS_Q_INF;
         publish_q(A.qflag, b, MAPS_Q_INF);
-        return;
+        return MAPS_Q_INF;
     }
     int32_t k = int32_t(k64);
     const int top = mx >> 24 ? 24 : (mx >> 16 ? 16 : (mx >> 8 ? 8 : 0));
@@ -592,10 +594,11 @@ __device__ void select_bucket(const SelectArgs& A, int b) {
     }
     if (t == 0) q_out[b] = int32_t(prefix);
     publish_q(A.qflag, b, int32_t(prefix));
+    return int32_t(prefix);
 }
 
 // The selection alone: one workgroup per bucket.
-__global__ __launch_bounds__(kSelNT) void cal_bucket_select(SelectArgs A) { select_bucket(A, int(blockIdx.x)); }
+__global__ __launch_bounds__(kSelNT) void cal_bucket_select(SelectArgs A) { (void)select_bucket(A, int(blockIdx.x)); }
 
 struct ApplyArgs {
     const int32_t* edges;
@@ -604,18 +607,26 @@ struct ApplyArgs {
     int32_t u_max;
     int32_t* U;
     uint32_t* dev_err;
+    uint32_t max_spins;   // polls of a quantile before the apply workgroup selects it itself
 };
 
 constexpr int kApplyFusedPer = 8;              // bounds per thread of a fused apply workgroup
-constexpr uint32_t kMaxSpins = 1u << 17;       // polls of the ready count before giving up (tens of ms)
+constexpr uint32_t kMaxSpins = 1u << 14;       // polls of a quantile before selecting it locally (about 1 ms)
 static_assert(2 * kSelStageBytes > 160 * 1024, "one workgroup of the fused launch per CU");
+static_assert(kFastBuckets <= kSelNT, "one waiting thread per bucket");
 
 // Apply workgroup j of ga in the fused launch (Eq. (4)): its first
 // predictions are loaded and their buckets found while the selection runs;
 // then thread i < nb waits (bounded) for bucket i's published quantile, and
-// the workgroup writes its bounds, then the rest of its share.
+// the workgroup writes its bounds, then the rest of its share.  A quantile
+// still missing after the bounded wait (its selecting workgroup not yet
+// resident: the device is shared, or did not hold the whole launch) is
+// selected by this workgroup itself from the same sorted runs -- the same
+// deterministic computation, so the same value -- so the launch completes
+// and is exact whether or not its workgroups run at the same time.
 __device__ void apply_after_select(const SelectArgs& S, const ApplyArgs& A, int j, int ga) {
     extern __shared__ __align__(16) uint32_t stage[];
+    __shared__ uint32_t missing[kFastBuckets / 32];   // buckets whose quantile did not arrive
     const int nb = S.nb, ne = nb - 1;
     const int t = threadIdx.x;
     int32_t* le = reinterpret_cast<int32_t*>(stage);   // [ne] edges
@@ -650,23 +661,35 @@ __device__ void apply_after_select(const SelectArgs& S, const ApplyArgs& A, int 
     for (int i = t; i < ne; i += kSelNT) le[i] = A.edges[i];
     __syncthreads();
     buckets_of<kA>(le, ne, p, bk);
-    for (int i0 = 0; i0 < nb; i0 += kSelNT) {   // uniform across the workgroup
-        const int i = i0 + t;
-        if (i0 + (t & ~(kWave - 1)) >= nb) continue;   // wavefronts past nb: nothing to wait for
-        uint64_t v = 0;
+    if (t < kFastBuckets / 32) missing[t] = 0;
+    __syncthreads();
+    // nb <= kFastBuckets = kSelNT: thread i waits for bucket i
+    uint64_t v = uint64_t(1) << 32;
+    if ((t & ~(kWave - 1)) < nb) {   // wavefronts past nb: nothing to wait for
         uint32_t spins = 0;
         for (;;) {   // device-coherent polls, no cache invalidation
-            v = i < nb ? __hip_atomic_load(&S.qflag[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+            v = t < nb ? __hip_atomic_load(&S.qflag[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                        : (uint64_t(1) << 32);
             if (__all(int(v >> 32) != 0)) break;
-            if (++spins > kMaxSpins) {
-                if (t % kWave == 0) raise_error(A.dev_err, MAPS_ERR_WAIT_TIMEOUT);
-                break;
-            }
+            if (++spins > A.max_spins) break;
             __builtin_amdgcn_s_sleep(8);
         }
-        if (i < nb) lq[i] = int32_t(uint32_t(v));
+        if (t < nb && (v >> 32) == 0) atomicOr(&missing[t / 32], 1u << (t % 32));
     }
+    __syncthreads();
+    int32_t q_own = int32_t(uint32_t(v));   // thread i < nb: bucket i's quantile
+    bool any = false;
+    for (int w = 0; w < kFastBuckets / 32; ++w) any |= missing[w] != 0;
+    if (any) {   // uniform: every thread read the same bitmap
+        for (int b = 0; b < nb; ++b) {
+            if (!((missing[b / 32] >> (b % 32)) & 1u)) continue;
+            const int32_t qb = select_bucket(S, b);   // overwrites `stage`: edges reloaded below
+            if (t == b) q_own = qb;
+        }
+        __syncthreads();
+        for (int i = t; i < ne; i += kSelNT) le[i] = A.edges[i];
+    }
+    if (t < nb) lq[t] = q_own;
     __syncthreads();
     emit(c0);
     for (c0 += stride; c0 < A.m; c0 += stride) {
@@ -678,8 +701,10 @@ __device__ void apply_after_select(const SelectArgs& S, const ApplyArgs& A, int 
 
 // Selection and bounds in one launch: workgroups [0, nb) select, the rest
 // apply.  Every workgroup holds more than half of a CU's LDS and the grid is
-// at most the CU count, so all of them are resident at once and the apply
-// workgroups' wait ends.
+// at most the CU count, so normally all of them are resident at once and the
+// apply workgroups find every quantile published; when not, they select the
+// missing ones themselves after a bounded wait (no workgroup waits without
+// bound on another).
 __global__ __launch_bounds__(kSelNT) void cal_select_apply(SelectArgs S, ApplyArgs A) {
     if (int(blockIdx.x) < S.nb) select_bucket(S, int(blockIdx.x));
     else apply_after_select(S, A, int(blockIdx.x) - S.nb, int(gridDim.x) - S.nb);
@@ -808,7 +833,11 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     const int ne = nb - 1;
     bool applied = false;
     if (fast_path(n, nb)) {
-        const ApplyArgs apply{edges, apply_pred, m, u_max, U_out, dev_err};
+        // MAPS_CAL_SPIN_LIMIT (tests only) lowers the bounded wait, so that the
+        // local selection of missing quantiles is exercised
+        const char* spin_env = getenv("MAPS_CAL_SPIN_LIMIT");
+        const uint32_t spins = spin_env ? uint32_t(strtoul(spin_env, nullptr, 10)) : kMaxSpins;
+        const ApplyArgs apply{edges, apply_pred, m, u_max, U_out, dev_err, spins};
         const maps_status st = calibrate_fast(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, apply, dev_err,
                                               workspace, stream, &applied);
         if (st != MAPS_OK) return st;
@@ -830,5 +859,3 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
     }
     return MAPS_OK;
 }
-
-

@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
+import workload
 from tests.gpu_common import assert_same, compare_all, custom_batch, gpu_step, oracle_step, say
 
 pytestmark = pytest.mark.gpu
@@ -458,3 +459,21 @@ def test_empty_arrival_batch_with_queues(orc):
                                            np.array(U, np.int32), cap, qoff, qp, qU, None, 2**31 - 1, 100)
     assert_same("order", order.cpu().numpy(), want_order)
     assert_same("admitted", admitted.cpu().numpy(), want_adm)
+
+
+@pytest.mark.parametrize("spins", ["0", "3"])
+def test_calibrate_fused_launch_selects_missing_quantiles(orc, spins, monkeypatch):
+    """The bounds written by workgroups of the selection's own launch: with the
+    bounded wait cut to almost nothing (set from the host), the apply
+    workgroups find quantiles not yet published and select them themselves;
+    every quantile, count and bound is still the oracle's."""
+    monkeypatch.setenv("MAPS_CAL_SPIN_LIMIT", spins)
+    for name in ("small", "large"):
+        b = workload.make(name)
+        ap = b.apply_pred()
+        q, cnt, U, err = _calib_gpu(b.cal_pred, b.cal_truth, b.edges, b.alpha_ppm, ap, b.u_max)
+        assert err == 0
+        qo, co = orc.calibrate(b.cal_pred, b.cal_truth, b.edges, b.alpha_ppm)
+        assert_same(f"{name} q", q, qo)
+        assert_same(f"{name} count", cnt, co)
+        assert_same(f"{name} U", U, orc.apply_bounds(ap, b.edges, qo, b.u_max))
