@@ -49,6 +49,7 @@ class Workload:
     bytes_per_token: int | None = None   # KV bytes per token (App. A note)
     wait_mean_ms: float = 250.0          # queue wait ~ floor(Exp(mean)) (reading)
     max_wait_ms: int = 1000              # starvation threshold (Sec. 4)
+    gen_frac: float = 1.0                # residents generated g = floor(f * gen_frac * true), f ~ U[0,1)
     notes: dict = field(default_factory=dict)
 
     @property
@@ -89,6 +90,16 @@ WORKLOADS = {
         prompt=_LONG_MIX, output=LogNormal(7.0, 1.8, 1, 65536), pred_sigma=0.5,
         n_cal=4000000, buckets=128, alphas_ppm=(100000,), queue_fixed=512, seed=4),
 }
+
+# Not one of the five: the large shape with residents early in long outputs
+# (short prompts, few tokens generated, outputs of thousands of tokens), so
+# that every decoder's occupancy keeps growing long after its first events
+# and placement needs the event records of the hot and full walks instead of
+# the flat region that every decoder of `large` reaches at once.
+WORKLOADS["large_growing"] = Workload(
+    name="large_growing", decoders=256, residents=4096, arrivals=262144, capacities=_HETERO,
+    prompt=PromptMix(LogNormal(4.0, 1.0, 1, 512)), output=LogNormal(8.5, 1.0, 1, 32768), pred_sigma=0.5,
+    n_cal=1000000, buckets=64, alphas_ppm=(50000,), queue_fixed=None, seed=13, gen_frac=0.05)
 
 # Workloads in size order; index i is the i-th workload of the scheduler-core
 # benchmark statement (tiny .. xlarge).

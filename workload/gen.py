@@ -115,7 +115,7 @@ def make(name_or_workload, alpha_ppm: int | None = None, seed: int | None = None
     res_prompt = _prompts(rng, D * n, w.prompt)
     res_true = _lognormal(rng, D * n, w.output)
     res_pred = _predict(rng, res_true, w.pred_sigma)
-    res_gen = np.floor(rng.random(D * n) * res_true).astype(np.int32)
+    res_gen = np.floor(rng.random(D * n) * w.gen_frac * res_true).astype(np.int32)
     seg_off = np.arange(D + 1, dtype=np.int64) * n
 
     rng = np.random.Generator(np.random.PCG64(s_arr))
