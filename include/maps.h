@@ -147,6 +147,24 @@ maps_status maps_calibrate(const int32_t* pred, const int32_t* truth, int64_t n,
                            uint32_t* dev_err, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/*
+ * maps_calibrate for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, outputs and errors without the workspace.  Its scratch
+ * is a library-owned device array of MAPS_CALIBRATE_NOALLOC_BYTES per GPU
+ * (held until the process ends), enough for n <= 1,048,576 residuals and
+ * nb <= 1,024 buckets; a call needing more returns MAPS_E_SIZE.  The call
+ * allocates nothing.  Every call on one GPU shares that array, so calls that
+ * overlap on one GPU (different streams, or host threads) race: serialize
+ * them on one stream.
+ */
+#define MAPS_CALIBRATE_NOALLOC_BYTES (8u << 20)
+maps_status maps_calibrate_noalloc(const int32_t* pred, const int32_t* truth, int64_t n,
+                                   const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                                   int32_t* q_out, int32_t* count_out,
+                                   const int32_t* apply_pred, int64_t m, int32_t u_max, int32_t* U_out,
+                                   uint32_t* dev_err, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* 1b. Sliding-window calibration (Sec. 3.2: the calibration set holds the  */
 /*     most recent completed requests; Sec. 4: a window of the last 500)    */

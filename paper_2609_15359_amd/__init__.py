@@ -84,6 +84,7 @@ _SIGNATURES = {
     "maps_window_reset": (_i32, [_vp, _sz, _i32, _i32, _vp]),
     "maps_window_append": (_i32, [_vp, _sz, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "maps_window_bounds": (_i32, [_vp, _sz, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
+    "maps_calibrate_noalloc": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)

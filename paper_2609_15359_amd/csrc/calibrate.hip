@@ -22,6 +22,8 @@
 // cal_hist, cal_select, cal_finish), histograms in LDS for up to 128 buckets.
 // All reductions are integer additions, so the result is deterministic.
 #include <cstdlib>
+#include <mutex>
+#include <unordered_map>
 
 #include "maps_internal.hpp"
 
@@ -858,4 +860,50 @@ extern "C" maps_status maps_calibrate(const int32_t* pred, const int32_t* truth,
         MAPS_CHECK_LAUNCH();
     }
     return MAPS_OK;
+}
+
+
+
+// ---------------------------------------------------------------------------
+// Calibration without a caller workspace: the scratch lives in a file-scope
+// device array (one per GPU, held until the process ends).  Host code never
+// passes the array's name to a kernel: its device address is looked up once
+// per device with hipGetSymbolAddress.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = MAPS_CALIBRATE_NOALLOC_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device (nullptr on failure).
+void* scratch_address() {
+    static std::mutex mu;
+    static std::unordered_map<int, void*> addr;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = addr.find(dev);
+    if (it != addr.end()) return it->second;
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    addr[dev] = p;
+    return p;
+}
+
+}  // namespace
+
+extern "C" maps_status maps_calibrate_noalloc(const int32_t* pred, const int32_t* truth, int64_t n,
+                                              const int32_t* edges, int32_t nb, int32_t alpha_ppm,
+                                              int32_t* q_out, int32_t* count_out, const int32_t* apply_pred,
+                                              int64_t m, int32_t u_max, int32_t* U_out, uint32_t* dev_err,
+                                              hipStream_t stream) {
+    if (n < 0 || m < 0 || nb < 1 || nb > 65536 || u_max < 0) return MAPS_E_SIZE;
+    if (maps_calibrate_workspace_size(n, nb) > kScratchBytes) return MAPS_E_SIZE;
+    void* ws = scratch_address();
+    if (!ws) return MAPS_E_HIP;
+    return maps_calibrate(pred, truth, n, edges, nb, alpha_ppm, q_out, count_out, apply_pred, m, u_max, U_out,
+                          dev_err, ws, kScratchBytes, stream);
 }
