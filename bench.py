@@ -345,6 +345,273 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
     return res
 
 
+def _median_ms(fn, calls: int, warm: int = 2) -> float:
+    """Median over `calls` of fence-free HIP events around fn() on the current stream."""
+    import torch
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(TimingEvent(), TimingEvent()) for _ in range(calls)]
+    for e0, e1 in ev:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
+
+
+def _walks(hdr, A: int, U_arr, groups: int = 8, tile: int = 8192):
+    """How the placement kernel walks each (arrival tile, decoder group) of a
+    launch with 8 groups and tiles of 8,192 arrivals, from the decoder headers
+    (hot window, flat region start) and the tile's bound range: 'flat' needs
+    no event data, 'hot' reads the rank word and PMX, 'full' also tests the
+    thresholds (the rule of the kernel's tile choice, restated on the host)."""
+    import numpy as np
+    D = hdr.shape[0]
+    Dg = (D + groups - 1) // groups
+    out = {"flat": 0, "hot": 0, "full": 0}
+    for g in range(groups):
+        h = hdr[g * Dg:(g + 1) * Dg]
+        if h.shape[0] == 0:
+            continue
+        lo, hi, fl = int(h[:, 6].max()), int(h[:, 7].min()), max(int(h[:, 8].max()), int(h[:, 6].max()))
+        for a0 in range(0, A, tile):
+            u = U_arr[a0:a0 + tile]
+            if (u < 0).any():
+                out["full"] += 1
+                continue
+            t_lo, t_hi = int(u.min()), int(u.max())
+            if t_lo >= fl and t_hi <= hi:
+                out["flat"] += 1
+            elif t_lo >= lo and t_hi <= hi:
+                out["hot"] += 1
+            else:
+                out["full"] += 1
+    return out
+
+
+def record_path(cpu: bool, calls: int = 20):
+    """The general placement path at the headline shape: workload
+    large_growing (256 decoders x 4,096 residents, 262,144 arrivals, the pair
+    matrix written), whose decoders' occupancy peaks mid-horizon, so that
+    tiles take the event-record walks.  The placement pass (maps_place_order)
+    timed alone with HIP events on inputs already projected; its outputs are
+    checked against the oracle's step on the same batch."""
+    import numpy as np
+    import torch
+
+    import workload
+    from paper_2609_15359_amd import pipeline
+    b = workload.make("large_growing")
+    D, A = b.decoders, b.arrivals
+    db = pipeline.to_device(b)
+    ws = pipeline.Workspaces(db, want_pairs=True)
+    phases = pipeline.step_phases(db, ws, fused="project")
+    for fn in phases:
+        fn()
+    torch.cuda.synchronize()
+    if int(ws.dev_err.item()) != 0:
+        raise SystemExit("large_growing raised device errors")
+    ms = _median_ms(phases[2], calls)
+    hdr = ws.snapshot[256:256 + 64 * D].view(torch.int32).view(D, 16).cpu().numpy()
+    W = (((db.u_max + 1) // 32 + 1) + 1) & ~1
+    nbytes = placement_bytes(D, A, db.u_max, W, hdr[:, 4])
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    U_arr = ws.out["U"][db.n_res:db.n_res + db.n_arr].cpu().numpy()
+    out = {"workload": f"large_growing: {workload.describe(b.workload)}; residents early in outputs of "
+                       f"LN(8.5, 1.0) tokens, prompts LN(4, 1)", "decoders": D, "arrivals": A, "pairs": D * A,
+           "place_ms": ms, "pairs_per_s": D * A / (ms * 1e-3),
+           "mean_events_per_decoder": float(np.mean(hdr[:, 4])),
+           "walks": _walks(hdr, A, U_arr),
+           "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes,
+                        "kernel": "maps_place (place_records, then place_finish)"}}
+    import oracle
+    o = oracle.Oracle()
+    t0 = time.perf_counter()
+    ref = oracle.step(b, o, want_pairs=True)
+    dt = time.perf_counter() - t0
+    out.update({k: v for k, v in verify_step(ws, ref).items() if k != "against"})
+    if cpu:
+        out["cpu_baseline"] = {"value": D * A / dt, "unit": "pair-evaluations/s", "cores": 1, "kind": "oracle",
+                               "sample": f"one whole step of the single-threaded C oracle on the same batch, "
+                                         f"{dt:.2f} s"}
+    return out
+
+
+def sequential_commit(b, db, snap, U_arr, ref, cpu: bool, k: int = 65536, check: int = 3000):
+    """Placement with sequential commit on the headline batch: the first k
+    arrivals in order, each committed to its decoder's projected occupancy
+    and queue before the next (a serial chain: one workgroup).  The first
+    `check` outputs are compared with the oracle, given the oracle's own
+    bounds (later arrivals never change earlier ones)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2609_15359_amd as maps
+    D = b.decoders
+    ap = db.arr_prompt[:k].contiguous()
+    aU = U_arr[:k].contiguous()
+    err = maps.new_error_word()
+    out = maps.CommitPlacement(choice=torch.empty(k, dtype=torch.int32, device="cuda"),
+                               chosen_peak=torch.empty(k, dtype=torch.int64, device="cuda"),
+                               chosen_overflow=torch.empty(k, dtype=torch.int64, device="cuda"),
+                               flags=torch.empty(k, dtype=torch.uint8, device="cuda"),
+                               queue_out=torch.empty(D, dtype=torch.int32, device="cuda"), dev_err=err)
+    wsb = torch.empty(maps.place_commit_workspace_bytes(D, db.u_max), dtype=torch.uint8, device="cuda")
+    fn = lambda: maps.place_commit(snap, db.capacity, db.queue_len, ap, aU, workspace=wsb, out=out)  # noqa: E731
+    ms = _median_ms(fn, 3, warm=1)
+    if int(err.item()) != 0:
+        raise SystemExit(f"sequential commit raised {maps.error_names(int(err.item()))}")
+    o = oracle.Oracle()
+    Ur, Ua, _ = b.split_bounds(ref.U)
+    t0 = time.perf_counter()
+    r, _ = o.place_commit(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, b.queue_len, b.arr_prompt[:check],
+                          Ua[:check])
+    dt = time.perf_counter() - t0
+    got = {"choice": out.choice, "chosen_peak": out.chosen_peak, "chosen_overflow": out.chosen_overflow,
+           "flags": out.flags}
+    for name, t in got.items():
+        if not np.array_equal(t[:check].cpu().numpy().astype(np.int64), getattr(r, name).astype(np.int64)):
+            print(f"bench.py: sequential commit's {name} differs from the oracle", file=sys.stderr)
+            sys.exit(3)
+    res = {"decoders": D, "arrivals": k, "ms": ms, "arrivals_per_s": k / (ms * 1e-3),
+           "workspace_mb": wsb.numel() / 1e6, "verified": True,
+           "verified_note": f"the first {check} arrivals' choices, peaks, overflows and flags against the oracle",
+           "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
+           "note": "arrivals in order; per arrival one peak lookup per decoder (dense curves plus Fenwick floors), "
+                   "a workgroup argmin, then the commit on [0, U] of the chosen decoder: a serial chain"}
+    if cpu:
+        res["cpu_baseline"] = {"value": check / dt, "unit": "arrivals/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the first {check} arrivals of the same batch (dense curves rebuilt over "
+                                         f"the whole step axis at every commit), single-threaded C oracle, "
+                                         f"{dt:.2f} s"}
+    return res
+
+
+def appa_simulation(cpu: bool, rhos: int = 64):
+    """App. A: 10,000 synthetic requests on N = 4 decoders of C = 50,000
+    tokens, theta = 0.85, t_tok = 1 ms, round robin and Algorithm 1 routing
+    at `rhos` utilisations from 0.5 to 1.3, all in one call (one wavefront
+    per simulation); bounds from maps_calibrate on the workload's calibration
+    pairs.  Four simulations are checked against the oracle."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2609_15359_amd as maps
+    import workload.appa as appa
+    w = appa.make()
+    dev = lambda x, t=torch.int32: torch.from_numpy(np.ascontiguousarray(x)).to(t).cuda()  # noqa: E731
+    q, _, U, err = maps.calibrate(dev(w.cal_pred), dev(w.cal_truth), dev(w.edges), appa.ALPHA_PPM, dev(w.pred),
+                                  appa.U_MAX)
+    grid = np.linspace(0.5, 1.3, rhos)
+    arr = np.stack([w.arrivals(r) for r in grid for _ in (0, 1)])
+    pol = np.array([p for _ in grid for p in (0, 1)], np.int32)
+    arr_d, pol_d, pr, ou = dev(arr, torch.int64), dev(pol), dev(w.prompt), dev(w.output)
+    S = arr.shape[0]
+    sim = maps.simulate(appa.N_DECODERS, appa.CAPACITY, appa.THETA_PPM, arr_d, pr, ou, U, pol_d, dev_err=err)
+    wsb = torch.empty(maps.library().maps_simulate_workspace_size(appa.N_DECODERS, w.n, S), dtype=torch.uint8,
+                      device="cuda")
+    fn = lambda: maps.simulate(appa.N_DECODERS, appa.CAPACITY, appa.THETA_PPM, arr_d, pr, ou, U, pol_d,  # noqa
+                               dev_err=err, workspace=wsb, out=sim)
+    ms = _median_ms(fn, 3, warm=1)
+    if int(err.item()) != 0:
+        raise SystemExit(f"simulation raised {maps.error_names(int(err.item()))}")
+    o = oracle.Oracle()
+    qo, _ = o.calibrate(w.cal_pred, w.cal_truth, w.edges, appa.ALPHA_PPM)
+    Uo = o.apply_bounds(w.pred, w.edges, qo, appa.U_MAX)
+    fin = sim.finish_ms.cpu().numpy()
+    st = sim.stats.cpu().numpy()
+    span = sim.span.cpu().numpy()
+    checked = [int(np.argmin(np.abs(grid - r))) * 2 + p for r in (0.96, 1.05) for p in (0, 1)]
+    t0 = time.perf_counter()
+    for s in checked:
+        r = o.simulate(appa.N_DECODERS, appa.CAPACITY, appa.THETA_PPM, arr[s], w.prompt, w.output, Uo, int(pol[s]))
+        ok = (np.array_equal(fin[s], r.finish_ms) and np.array_equal(st[s, 0], r.hp_time)
+              and np.array_equal(st[s, 1], r.hp_max) and np.array_equal(st[s, 2], r.hp_count)
+              and np.array_equal(st[s, 3], r.max_queue) and np.array_equal(st[s, 4], r.queue_area)
+              and np.array_equal(span[s], r.span))
+        if not ok:
+            print(f"bench.py: simulation {s} differs from the oracle", file=sys.stderr)
+            sys.exit(3)
+    dt = (time.perf_counter() - t0) / len(checked)
+
+    def summary(s):
+        T = int(span[s, 1] - span[s, 0])
+        lat = fin[s] - arr[s]
+        return {"rho": round(float(grid[s // 2]), 3), "policy": ["round_robin", "algorithm1"][int(pol[s])],
+                "f_hp": [round(float(x) / T, 4) for x in st[s, 0]], "B_hp_ms": st[s, 1].tolist(),
+                "C_hp": st[s, 2].tolist(), "max_queue": st[s, 3].tolist(),
+                "mean_e2e_ms": float(lat.mean()), "p99_e2e_ms": float(np.percentile(lat, 99))}
+    res = {"simulations": S, "requests": w.n, "decoders": appa.N_DECODERS, "capacity": appa.CAPACITY,
+           "theta": appa.THETA_PPM / 1e6, "ms": ms, "simulations_per_s": S / (ms * 1e-3),
+           "simulated_requests_per_s": S * w.n / (ms * 1e-3), "verified": True,
+           "verified_note": f"simulations {checked} (rho 0.96 and 1.05, both policies) against the oracle in full",
+           "at": [summary(s) for s in checked],
+           "note": "synthetic lognormal lengths stand in for BurstGPT; event to event per wavefront"}
+    if cpu:
+        res["cpu_baseline"] = {"value": 1.0 / dt, "unit": "simulations/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{len(checked)} of the simulations, one millisecond at a time, "
+                                         f"single-threaded C oracle, {dt:.3f} s each"}
+    return res
+
+
+def incremental_window(b, ref, cpu: bool, batches: int = 64, window: int = 500):
+    """The headline batch's 1,000,000 calibration pairs appended as a
+    completion log in `batches` batches to the incremental window state
+    (64 buckets, window 500), then the bounds of every resident, arrival and
+    queued request from the state: each append and the bound call timed with
+    HIP events.  The final bounds of a sample of requests are checked against
+    the oracle's window calibration with every request having seen the log."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2609_15359_amd as maps
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(torch.int32).cuda()  # noqa: E731
+    pred, truth, ap = dev(b.cal_pred), dev(b.cal_truth), dev(b.apply_pred())
+    n = pred.numel()
+    cuts = np.linspace(0, n, batches + 1).astype(np.int64)
+    st = maps.WindowState(dev(b.edges), window)
+    U = torch.empty(ap.numel(), dtype=torch.int32, device="cuda")
+    ws = torch.empty(maps.library().maps_window_append_workspace_size(int(cuts[1] - cuts[0]) + 1, st.nb),
+                     dtype=torch.uint8, device="cuda")
+    ev = [(TimingEvent(), TimingEvent()) for _ in range(batches)]
+    st.reset()
+    torch.cuda.synchronize()
+    for j, (e0, e1) in enumerate(ev):
+        e0.record()
+        st.append(pred[cuts[j]:cuts[j + 1]], truth[cuts[j]:cuts[j + 1]], workspace=ws)
+        e1.record()
+    torch.cuda.synchronize()
+    append_ms = statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
+    bounds_ms = _median_ms(lambda: st.bounds(b.alpha_ppm, ap, b.u_max, U=U), 10)
+    if int(st.dev_err.item()) != 0:
+        raise SystemExit("incremental window raised device errors")
+    o = oracle.Oracle()
+    apn = b.apply_pred()
+    idx = np.arange(0, apn.size, max(1, apn.size // 20000))
+    t0 = time.perf_counter()
+    _, Uo = o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, window, b.alpha_ppm, apn[idx],
+                               np.full(idx.size, n), b.u_max)
+    dt = time.perf_counter() - t0
+    if not np.array_equal(U.cpu().numpy()[idx], Uo):
+        print("bench.py: incremental window bounds differ from the oracle", file=sys.stderr)
+        sys.exit(3)
+    m = apn.size
+    res = {"log": n, "batches": batches, "batch_size": int(cuts[1] - cuts[0]), "buckets": st.nb, "window": window,
+           "append_ms": append_ms, "appended_per_s": (cuts[1] - cuts[0]) / (append_ms * 1e-3),
+           "bounds_ms": bounds_ms, "requests": m, "bounds_per_s": m / (bounds_ms * 1e-3), "verified": True,
+           "verified_note": f"{idx.size} evenly spaced requests' bounds after the last batch against the oracle"}
+    if cpu:
+        res["cpu_baseline"] = {"value": idx.size / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{idx.size} requests, each calibrated on the last {window} completions of "
+                                         f"its bucket (a sort per request), single-threaded C oracle, {dt:.2f} s"}
+    return res
+
+
 class TimingEvent:
     """A HIP event made only for timing: created with hipEventDisableSystemFence,
     so recording it costs no system-scope cache write-back and invalidation
@@ -428,16 +695,16 @@ def main():
     D, A = b.decoders, b.arrivals
     db = pipeline.to_device(b)
     ws = pipeline.Workspaces(db, want_pairs=True)
-    # placement and local order in one call: the final selection and the
-    # local orders share a launch
-    phases = pipeline.step_phases(db, ws, fused=True)
-    names = pipeline.PHASES_FUSED
+    # projection and local order in one call (each decoder's workgroup orders
+    # its queue after projecting it), then placement
+    phases = pipeline.step_phases(db, ws, fused="project")
+    names = pipeline.PHASES_PROJECT_ORDER
 
     ws.dev_err.zero_()
     for fn in phases:   # one eager step: the reference for the replayed graphs
         fn()
     eager = (ws.placement.choice.clone(), ws.placement.pair_peak.sum(dtype=torch.int64), ws.order.clone())
-    graphs = pipeline.StepGraphs(db, ws, fused=True) if args.graph else None
+    graphs = pipeline.StepGraphs(db, ws, fused="project") if args.graph else None
 
     def one_step(ev=None, place_ev=None):
         """One step; `ev` brackets every phase, `place_ev` only placement.
@@ -516,8 +783,8 @@ def main():
                    "launch": "one HIP graph per phase" if args.graph else "host launches"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(args.workload),
-                     "kernel": "maps_place_order (place_records, then place_finish_order: placement's final "
-                               "selection and every local order in one launch)",
+                     "kernel": "maps_place (place_records, then place_finish: each arrival's best group); "
+                               "the local orders run inside the projection's launch (maps_project_order)",
                      "algorithmic_bytes": nbytes, "place_ms": place_ms},
         "breakdown_ms": parts,
         "breakdown_note": f"median of {BREAKDOWN_STEPS} untimed steps with a timing event (no system "
@@ -540,6 +807,12 @@ def main():
                                                   cpu=not args.no_cpu_baseline)
     result["block_placement"] = block_placement(b, db, ws.out["U"][:nr], ws.out["U"][nr:nr + na],
                                                 cpu=not args.no_cpu_baseline)
+    snap = maps.Snapshot(data=ws.snapshot, D=D, n_total=nr, u_max=db.u_max)
+    result["sequential_commit"] = sequential_commit(b, db, snap, ws.out["U"][nr:nr + na], ref,
+                                                    cpu=not args.no_cpu_baseline)
+    result["incremental_window"] = incremental_window(b, ref, cpu=not args.no_cpu_baseline)
+    result["appa_simulation"] = appa_simulation(cpu=not args.no_cpu_baseline)
+    result["record_path"] = record_path(cpu=not args.no_cpu_baseline)
     print(json.dumps(result), flush=True)
 
 

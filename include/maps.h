@@ -538,6 +538,28 @@ maps_status maps_simulate(int32_t N, int64_t C, int32_t theta_ppm, int64_t n, in
                           int32_t* routed, int64_t* stats, int64_t* span, uint32_t* dev_err,
                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------ */
+/* 2 + 4. Projection and local order in one launch (Sec. 3.3; Eq. (7);      */
+/*        App. A, Eq. (10))                                                  */
+/* ------------------------------------------------------------------------ */
+/*
+ * Exactly maps_project followed by maps_local_order on the snapshot it
+ * writes (same D and u_max; capacity, q_off, q_total, q_prompt, q_upper,
+ * q_wait_ms, max_wait_ms, order and admitted as for maps_local_order), with
+ * the same outputs bit for bit.  Each decoder's workgroup orders the
+ * decoder's queue right after projecting it, so the order costs no launch
+ * or pass of its own.  dev_err bits: those of both calls.  Host errors:
+ * those of both calls; nothing is enqueued when either argument set is
+ * rejected.
+ */
+maps_status maps_project_order(int32_t D, const int64_t* seg_off, int64_t n_total,
+                               const int32_t* prompt, const int32_t* generated, const int32_t* upper,
+                               int32_t u_max, void* snapshot, size_t snapshot_bytes, int32_t* base_peak,
+                               const int32_t* capacity, const int64_t* q_off, int64_t q_total,
+                               const int32_t* q_prompt, const int32_t* q_upper, const int32_t* q_wait_ms,
+                               int32_t max_wait_ms, int32_t* order, int32_t* admitted,
+                               uint32_t* dev_err, hipStream_t stream);
+
 /* Static description of a status code (host). */
 const char* maps_status_string(maps_status status);
 

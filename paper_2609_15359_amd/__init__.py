@@ -85,6 +85,8 @@ _SIGNATURES = {
     "maps_window_append": (_i32, [_vp, _sz, _i32, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "maps_window_bounds": (_i32, [_vp, _sz, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
     "maps_calibrate_noalloc": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
+    "maps_project_order": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
+                                  _i32, _vp, _vp, _vp, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)
@@ -412,6 +414,42 @@ def place_commit(snapshot: Snapshot, capacity, queue_len, a_prompt, a_upper, pol
                                _ptr(out.queue_out), _ptr(out.dev_err), _ptr(ws), ws.numel(), _stream(dev))
     _check(st, "maps_place_commit")
     return out
+
+
+def project_order(seg_off, prompt, generated, upper, u_max: int, capacity, q_off, q_prompt, q_upper, q_wait_ms=None,
+                  max_wait_ms: int = 2**31 - 1, snapshot=None, dev_err=None, base_peak=None, order=None,
+                  admitted=None):
+    """maps_project then maps_local_order in one launch: (snapshot, base_peak,
+    order, admitted, dev_err)."""
+    seg_off = _dev(seg_off, torch.int64, "seg_off")
+    dev = seg_off.device
+    D = seg_off.numel() - 1
+    n = prompt.numel()
+    for name, t in (("prompt", prompt), ("generated", generated), ("upper", upper)):
+        _dev(t, torch.int32, name)
+        if t.numel() != n:
+            raise MapsError("prompt, generated and upper differ in length")
+    capacity = _dev(capacity, torch.int32, "capacity")
+    q_off = _dev(q_off, torch.int64, "q_off")
+    q_prompt = _dev(q_prompt, torch.int32, "q_prompt")
+    q_upper = _dev(q_upper, torch.int32, "q_upper")
+    if q_wait_ms is not None:
+        _dev(q_wait_ms, torch.int32, "q_wait_ms")
+    total = q_prompt.numel()
+    if capacity.numel() != D or q_off.numel() != D + 1 or q_upper.numel() != total:
+        raise MapsError("capacity must have D entries, q_off D+1 and q_upper as many as q_prompt")
+    nbytes = snapshot_bytes(D, n, u_max)
+    snap = snapshot if snapshot is not None else torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    bp = torch.empty(D, dtype=torch.int32, device=dev) if base_peak is None else base_peak
+    order = torch.empty(total, dtype=torch.int32, device=dev) if order is None else order
+    admitted = torch.empty(D, dtype=torch.int32, device=dev) if admitted is None else admitted
+    err = new_error_word(dev) if dev_err is None else dev_err
+    st = library().maps_project_order(D, _ptr(seg_off), n, _ptr(prompt), _ptr(generated), _ptr(upper), int(u_max),
+                                      _ptr(snap), snap.numel(), _ptr(bp), _ptr(capacity), _ptr(q_off), total,
+                                      _ptr(q_prompt), _ptr(q_upper), _ptr(q_wait_ms), int(max_wait_ms), _ptr(order),
+                                      _ptr(admitted), _ptr(err), _stream(dev))
+    _check(st, "maps_project_order")
+    return Snapshot(data=snap, D=D, n_total=n, u_max=int(u_max)), bp, order, admitted, err
 
 
 # ---------------------------------------------------------------------------

@@ -140,17 +140,24 @@ __device__ inline int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* ra
 }
 
 // The whole local order of decoder d by one workgroup of kOrderNT threads.
-__device__ inline void order_queue(const LocalArgs& g, int32_t d) {
+// built_n_total >= 0: the snapshot's decoder d was written by this workgroup
+// (the projection's launch), whose header the workgroup cannot read back
+// reliably; the resident count is then given.
+__device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_n_total = -1) {
     __shared__ LocalLds s;
     const SnapLayout& L = g.L;
     const SnapView V = snap_view(const_cast<void*>(g.snap), L);
-    const SnapHeader hdr = *V.hdr;
-    if (!(hdr.magic == kSnapMagic && hdr.D == L.D && hdr.u_max == L.u_max && hdr.W == L.W)) {
-        if (d == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
-        return;
+    int64_t n_total = built_n_total;
+    if (built_n_total < 0) {
+        const SnapHeader hdr = *V.hdr;
+        if (!(hdr.magic == kSnapMagic && hdr.D == L.D && hdr.u_max == L.u_max && hdr.W == L.W)) {
+            if (d == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
+            return;
+        }
+        n_total = hdr.n_total;
     }
     const DecHeader h = V.dec[d];
-    if (!slice_ok(h, hdr.n_total, L)) {
+    if (!slice_ok(h, n_total, L)) {
         if (threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         return;
     }

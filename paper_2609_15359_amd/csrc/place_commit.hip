@@ -166,14 +166,21 @@ __global__ __launch_bounds__(kCommitNT) void commit_init(CommitArgs a) {
 // 1..u+1.  The positions are known up front, so the loads are independent.
 constexpr int kFenwickSteps = 21;   // positions up to 2^21 > MAPS_MAX_COMMIT_U_MAX + 1
 __device__ inline int64_t floor_at(const int64_t* F, int32_t u) {
-    int64_t m = 0;
+    // every position of the path first (ALU only), then all loads, then the maximum:
+    // the loads are in flight together instead of one round trip each
+    int32_t pos[kFenwickSteps];
     int32_t i = u + 1;
 #pragma unroll
     for (int k = 0; k < kFenwickSteps; ++k) {
-        const int64_t x = i > 0 ? F[i] : 0;
-        m = max64(m, x);
+        pos[k] = i;
         i -= i & -i;
     }
+    int64_t x[kFenwickSteps];
+#pragma unroll
+    for (int k = 0; k < kFenwickSteps; ++k) x[k] = pos[k] > 0 ? F[pos[k]] : 0;
+    int64_t m = 0;
+#pragma unroll
+    for (int k = 0; k < kFenwickSteps; ++k) m = max64(m, x[k]);
     return m;
 }
 
@@ -302,14 +309,15 @@ __global__ __launch_bounds__(kCommitNT) void commit_serial(CommitArgs a) {
             after = max64(after, O[t]);
         }
         // the new PF(Uc) = v is a floor for every step above Uc
-        if (threadIdx.x == 0) {
-            // 64-bit position: after passing L it keeps doubling and would wrap a 32-bit
-            // integer to a negative index that passes the bound test
-            int64_t* Fd = a.F + int64_t(bd) * (L + 1);
+        if (threadIdx.x < kFenwickSteps) {
+            // lane k updates the k-th position of the path (no two lanes share one, so the
+            // read-modify-writes run side by side); 64-bit positions: past L a position keeps
+            // doubling and would wrap a 32-bit integer to a negative index
             int64_t j = int64_t(Uc) + 2;
-            for (int k = 0; k < kFenwickSteps && j <= L; ++k) {
+            for (int k = 0; k < int(threadIdx.x) && j <= L; ++k) j += j & -j;
+            if (j <= L) {
+                int64_t* Fd = a.F + int64_t(bd) * (L + 1);
                 Fd[j] = max64(Fd[j], v);
-                j += j & -j;
             }
         }
         __syncthreads();

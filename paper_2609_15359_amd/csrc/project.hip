@@ -14,6 +14,7 @@
 // Small decoders keep every array in LDS; decoders that do not fit run the
 // same steps on their own slice of the snapshot in HBM.
 #include "maps_internal.hpp"
+#include "order_core.hpp"
 
 namespace maps {
 namespace {
@@ -393,15 +394,14 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     }
 }
 
-__global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t* __restrict__ seg_off,
-                                                        int64_t n_total, const int32_t* __restrict__ p,
-                                                        const int32_t* __restrict__ g,
-                                                        const int32_t* __restrict__ U, int32_t u_max,
-                                                        SnapLayout L, void* snap, int32_t* __restrict__ base_peak,
-                                                        int64_t lds_cap, uint32_t* dev_err) {
-    extern __shared__ uint32_t lds[];
+// Decoder d's projection (the slice, its header and base peak) by one
+// workgroup of kNT threads; `lds` is the launch's dynamic LDS.
+__device__ inline void project_decoder(int32_t d, int32_t D, const int64_t* __restrict__ seg_off, int64_t n_total,
+                                       const int32_t* __restrict__ p, const int32_t* __restrict__ g,
+                                       const int32_t* __restrict__ U, int32_t u_max, const SnapLayout& L,
+                                       void* snap, int32_t* __restrict__ base_peak, int64_t lds_cap,
+                                       uint32_t* dev_err, uint32_t* lds) {
     __shared__ Scratch sc;
-    const int32_t d = blockIdx.x;
     const int32_t W = L.W;
     SnapView V = snap_view(snap, L);
     int64_t lo = seg_off[d], hi = seg_off[d + 1];
@@ -446,6 +446,36 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
     }
 }
 
+__global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t* __restrict__ seg_off,
+                                                        int64_t n_total, const int32_t* __restrict__ p,
+                                                        const int32_t* __restrict__ g,
+                                                        const int32_t* __restrict__ U, int32_t u_max,
+                                                        SnapLayout L, void* snap, int32_t* __restrict__ base_peak,
+                                                        int64_t lds_cap, uint32_t* dev_err) {
+    extern __shared__ uint32_t lds[];
+    project_decoder(int32_t(blockIdx.x), D, seg_off, n_total, p, g, U, u_max, L, snap, base_peak, lds_cap, dev_err,
+                    lds);
+}
+
+// Projection and local order in one launch: workgroup d projects decoder d,
+// then (once its slice and header are stored) orders d's queue against that
+// slice, in the same dynamic LDS.  The order's latency-bound work then costs
+// no launch and no pass of its own.
+static_assert(order::kOrderNT == kNT, "one workgroup size for both steps");
+__global__ __launch_bounds__(kNT) void project_order_decoders(int32_t D, const int64_t* __restrict__ seg_off,
+                                                              int64_t n_total, const int32_t* __restrict__ p,
+                                                              const int32_t* __restrict__ g,
+                                                              const int32_t* __restrict__ U, int32_t u_max,
+                                                              SnapLayout L, void* snap,
+                                                              int32_t* __restrict__ base_peak, int64_t lds_cap,
+                                                              uint32_t* dev_err, order::LocalArgs o) {
+    extern __shared__ uint32_t lds[];
+    const int32_t d = int32_t(blockIdx.x);
+    project_decoder(d, D, seg_off, n_total, p, g, U, u_max, L, snap, base_peak, lds_cap, dev_err, lds);
+    __syncthreads();   // the slice and header stores of this workgroup are done
+    order::order_queue(o, d, n_total);
+}
+
 }  // namespace
 }  // namespace maps
 
@@ -478,6 +508,46 @@ extern "C" maps_status maps_project(int32_t D, const int64_t* seg_off, int64_t n
     allow_dynamic_lds(project_decoders, lds);
     hipLaunchKernelGGL(project_decoders, dim3(D), dim3(kNT), lds, stream, D, seg_off, n_total, prompt, generated,
                        upper, u_max, L, snapshot, base_peak, cap, dev_err);
+    MAPS_CHECK_LAUNCH();
+    return MAPS_OK;
+}
+
+extern "C" maps_status maps_project_order(int32_t D, const int64_t* seg_off, int64_t n_total,
+                                          const int32_t* prompt, const int32_t* generated, const int32_t* upper,
+                                          int32_t u_max, void* snapshot, size_t snapshot_bytes, int32_t* base_peak,
+                                          const int32_t* capacity, const int64_t* q_off, int64_t q_total,
+                                          const int32_t* q_prompt, const int32_t* q_upper, const int32_t* q_wait_ms,
+                                          int32_t max_wait_ms, int32_t* order, int32_t* admitted,
+                                          uint32_t* dev_err, hipStream_t stream) {
+    if (D < 1 || n_total < 0 || q_total < 0 || u_max < 0 || u_max > MAPS_MAX_U_MAX) return MAPS_E_SIZE;
+    if (!seg_off || !snapshot || !base_peak || !dev_err || !capacity || !q_off || !admitted ||
+        (n_total > 0 && (!prompt || !generated || !upper)) || (q_total > 0 && (!q_prompt || !q_upper || !order)))
+        return MAPS_E_NULL;
+    const SnapLayout L = snap_layout(D, n_total, u_max);
+    if (snapshot_bytes < L.bytes) return MAPS_E_BUFFER;
+    // the local order's LDS is static, beside the projection's: a smaller
+    // budget for the projection's arrays (larger decoders run from HBM)
+    constexpr size_t kFusedBudget = kLdsBudget - sizeof(order::LocalLds);
+    const size_t fixed = size_t(2) * L.W * 4;
+    int64_t cap = fixed < kFusedBudget ? int64_t((kFusedBudget - fixed) / 16) : 0;
+    if (cap > int64_t(kNT) * kEvPer) cap = int64_t(kNT) * kEvPer;
+    const size_t lds = cap > 0 ? fixed + size_t(cap) * 16 : 0;
+    order::LocalArgs o;
+    o.L = L;
+    o.snap = snapshot;
+    o.cap = capacity;
+    o.q_off = q_off;
+    o.total = q_total;
+    o.qp = q_prompt;
+    o.qU = q_upper;
+    o.qwait = q_wait_ms;
+    o.max_wait = max_wait_ms;
+    o.order = order;
+    o.admitted = admitted;
+    o.dev_err = dev_err;
+    allow_dynamic_lds(project_order_decoders, lds);
+    hipLaunchKernelGGL(project_order_decoders, dim3(D), dim3(kNT), lds, stream, D, seg_off, n_total, prompt,
+                       generated, upper, u_max, L, snapshot, base_peak, cap, dev_err, o);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

@@ -10,7 +10,7 @@ import numpy as np
 import torch
 
 from . import (POLICY_MQ, Placement, Snapshot, calibrate, local_order, new_error_word, place, place_order,
-               place_workspace_bytes, project)
+               place_workspace_bytes, project, project_order)
 
 
 @dataclass
@@ -107,14 +107,20 @@ class Workspaces:
 PHASES = ("calibrate", "project", "place", "local_order")
 # with placement and local order in one call (maps_place_order)
 PHASES_FUSED = ("calibrate", "project", "place+local_order")
+# with projection and local order in one call (maps_project_order), then placement
+PHASES_PROJECT_ORDER = ("calibrate", "project+local_order", "place")
+
+
+def phase_names(fused) -> tuple:
+    return {False: PHASES, True: PHASES_FUSED, "project": PHASES_PROJECT_ORDER}[fused]
 
 
 def step_phases(db: DeviceBatch, ws: Workspaces, want_pairs: bool = True, capacity=None,
                 policy: int = POLICY_MQ, rr_offset: int = 0, fused: bool = False):
-    """The step as one callable per phase (PHASES order, or PHASES_FUSED with
-    `fused`).  Each enqueues its library calls on the current stream and
-    writes only into `ws`, so a phase can also be captured into a graph and
-    replayed."""
+    """The step as one callable per phase (PHASES order; PHASES_FUSED with
+    fused=True, PHASES_PROJECT_ORDER with fused="project").  Each enqueues its
+    library calls on the current stream and writes only into `ws`, so a phase
+    can also be captured into a graph and replayed."""
     cap = db.capacity if capacity is None else capacity
     err = ws.dev_err
     nr, na = db.n_res, db.n_arr
@@ -142,6 +148,13 @@ def step_phases(db: DeviceBatch, ws: Workspaces, want_pairs: bool = True, capaci
                     db.q_wait_ms, db.max_wait_ms, policy=policy, rr_offset=rr_offset, want_pairs=want_pairs,
                     workspace=ws.place, out=ws.placement, order=ws.order, admitted=ws.admitted)
 
+    def proj_loc():
+        project_order(db.seg_off, db.res_prompt, db.res_gen, U[:nr], db.u_max, cap, db.q_off, db.q_prompt,
+                      U[nr + na:], db.q_wait_ms, db.max_wait_ms, snapshot=ws.snapshot, dev_err=err,
+                      base_peak=ws.base_peak, order=ws.order, admitted=ws.admitted)
+
+    if fused == "project":
+        return [cal, proj_loc, pla]
     return [cal, proj, pla_loc] if fused else [cal, proj, pla, loc]
 
 

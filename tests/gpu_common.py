@@ -19,8 +19,9 @@ def say(*a):
 
 
 def gpu_step(b: Batch, capacity=None, want_pairs=True, policy=0, rr_offset=0, fused=False):
-    """The whole step on the GPU; `fused` makes placement and local order one
-    call (maps_place_order), as the benchmark does."""
+    """The whole step on the GPU; fused=True makes placement and local order
+    one call (maps_place_order); fused="project" makes projection and local
+    order one call (maps_project_order), as the benchmark does."""
     import torch
 
     import paper_2609_15359_amd as maps

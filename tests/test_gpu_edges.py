@@ -140,7 +140,7 @@ def test_ragged_shapes(orc, D, nmax, A, qmax, policy):
     cap = (o0["base_peak"] + rng.integers(0, 20000, size=D)).astype(np.int32)
     for capacity in (None, cap):
         o = oracle_step(b, capacity=capacity, policy=policy, rr_offset=2**40 + 3, o=orc)
-        for fused in (False, True):
+        for fused in (False, True, "project"):
             gg = gpu_step(b, capacity=capacity, policy=policy, rr_offset=2**40 + 3, fused=fused)
             assert gg["err"] == 0, gg["errors"]
             compare_all(gg, o)

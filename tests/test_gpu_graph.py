@@ -17,7 +17,7 @@ def _snapshot_all(db, ws):
             "flags": pl.flags, "pair_peak": pl.pair_peak, "order": ws.order, "admitted": ws.admitted}
 
 
-@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("fused", [False, True, "project"])
 @pytest.mark.parametrize("name", ["small", "medium"])
 def test_graph_replays_match_eager(name, fused):
     import torch

@@ -23,7 +23,7 @@ def test_workload_bit_exact(orc, name, alpha):
     b = workload.make(name, alpha_ppm=alpha)
     say(f"[parity] {name} alpha_ppm={b.alpha_ppm} D={b.decoders} A={b.arrivals}")
     o = oracle_step(b, o=orc)
-    g = gpu_step(b, fused=True)   # the benchmark's launch configuration
+    g = gpu_step(b, fused="project")   # the benchmark's launch configuration
     assert g["err"] == 0, g["errors"]
     compare_all(g, o)
     # the literal workloads overload the decoders; the fit variant below takes both branches
@@ -58,6 +58,27 @@ def test_policy_mc_and_round_robin_offset(orc, policy):
     compare_all(g, o)
 
 
+def test_large_growing_bit_exact(orc):
+    """The headline shape with occupancy that peaks mid-horizon: tiles take
+    the event-record walks (hot and full) rather than the flat region; every
+    output and the whole pair matrix, literal capacities and with room."""
+    b = workload.make("large_growing")
+    say("[parity] large_growing")
+    o = oracle_step(b, o=orc)
+    g = gpu_step(b, fused="project")
+    assert g["err"] == 0, g["errors"]
+    compare_all(g, o)
+    hdr = g["dec_hdr"]
+    say(f"[parity] large_growing: events per decoder {int(hdr[:, 4].min())}..{int(hdr[:, 4].max())}, "
+        f"flat region from {int(hdr[:, 8].min())}..{int(hdr[:, 8].max())}")
+    cap = fit_capacity(b, o)
+    o = oracle_step(b, capacity=cap, o=orc)
+    g = gpu_step(b, capacity=cap, fused=True)
+    assert g["err"] == 0, g["errors"]
+    compare_all(g, o)
+    say(f"[parity] large_growing with room: feasible fraction {np.mean(o['flags'] & 1):.4f}")
+
+
 def test_xlarge_full(orc):
     """1,024 decoders x 1,048,576 arrivals: every decision, bound, base peak,
     order and admission compared in full, and every entry of the 4 GiB
@@ -67,7 +88,7 @@ def test_xlarge_full(orc):
     say("[parity] xlarge: oracle decisions (no pair matrix)")
     o = oracle_step(b, o=orc, want_pairs=False)
     say("[parity] xlarge: gpu step")
-    g = gpu_step(b, want_pairs=True)
+    g = gpu_step(b, want_pairs=True, fused="project")
     assert g["err"] == 0, g["errors"]
     compare_all(g, o, pairs=False)
     U_res, U_arr, _ = b.split_bounds(o["U"])
