@@ -249,14 +249,15 @@ __device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, 
 // the LDS address of the bound's rank word in buffer 0 and the mask of the
 // bits below it (bound clamped to [0, 32 W - 1]), and the running best.
 // The workgroup walks its decoders with two LDS buffers: while decoder d is
-// evaluated from one buffer, the rank words and PMX values (and thresholds,
-// unless the tile lies in every decoder's hot window) of decoder d+1 are
-// already on their way into registers, and they are written to the other
-// buffer before the single barrier of the next step.  Cold records, needed
-// only past an event's threshold, stay in the snapshot (read through L2).  A
-// slice whose staged part exceeds a buffer is read from HBM altogether.
+// evaluated from one buffer, the rank words and PMX values of decoder d+1
+// (and its cold records {S_e, N_e + 1}, unless the tile lies in every
+// decoder's hot window) are already on their way into registers, and they
+// are written to the other buffer before the single barrier of the next
+// step.  Every lookup then stays in LDS.  A slice whose staged part exceeds
+// a buffer is read from HBM altogether (with the thresholds, so that only
+// lanes past one read a cold record).
 // ---------------------------------------------------------------------------
-constexpr int kStage = 6;   // 16-byte units per thread staged in registers: a whole LDS buffer
+constexpr int kStage = 7;   // 16-byte units per thread staged in registers: a whole LDS buffer
 
 template <int kAPT>
 struct RecArrivals {
@@ -356,17 +357,69 @@ __device__ __forceinline__ void eval_flat(RecArrivals<kAPT>& s, int32_t pmx_end,
     }
 }
 
-// Load this thread's units of a slice of `units` units into registers: rows
-// j of kNT units that hold part of the slice (a uniform test), with the units
-// past the end of the last one read as 0.
-__device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* src, int32_t units) {
-    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, uint32_t(units) * 16u);
+// Load this thread's units of `units` staged units of a slice into
+// registers: rows j of kNT units that hold part of them (a uniform test).
+// Staged unit u comes from slice unit u below `split` and from u + skip at
+// or above it (the cold records follow the PMX values once the thresholds
+// are skipped); units past the slice's end read as 0.
+__device__ __forceinline__ void stage_slice(v4i (&stage)[kStage], const int4* src, int32_t units, int32_t split,
+                                            int32_t skip) {
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, uint32_t(units + skip) * 16u);
 #pragma unroll
     for (int j = 0; j < kStage; ++j)
-        if (j * kNT < units)
-            stage[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
-                                                   rs, int(threadIdx.x) * 16 + j * kNT * 16, 0, 0));
+        if (j * kNT < units) {
+            const int32_t u = int32_t(threadIdx.x) + j * kNT;
+            stage[j] = __builtin_bit_cast(
+                v4i, __builtin_amdgcn_raw_buffer_load_b128(rs, (u + (u >= split ? skip : 0)) * 16, 0, 0));
+        }
 }
+
+// Evaluate the thread's arrivals against one decoder whose rank words, PMX
+// values and cold records are all in LDS: PF(U) = max(PMX_e, S_e + U (N_e +
+// 1), U) for every lane, with no threshold test (see event_peak for why the
+// low 24 bits of U suffice in the product).
+template <int kAPT, bool kFull, bool kPairs, int kPolicy>
+__device__ __forceinline__ void eval_cold(RecArrivals<kAPT>& s, uint32_t rank_lds, const int32_t* pmx,
+                                          const int2* cold, uint32_t E, int32_t base, int32_t C, int32_t Q,
+                                          int32_t d, __amdgpu_buffer_rsrc_t row) {
+    constexpr int kChunk = kAPT < 4 ? kAPT : 4;
+    int32_t Qm = int32_t(uint32_t(Q) + 0x80000000u);
+    asm("" : "+s"(Qm));
+#pragma unroll
+    for (int c = 0; c < kAPT; c += kChunk) {
+        uint32_t e[kChunk];
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            const uint64_t x =
+                *reinterpret_cast<const __attribute__((address_space(3))) uint64_t*>(size_t(s.roff[c + i] + rank_lds));
+            e[i] = uint32_t(x >> 32) + __popc(uint32_t(x) & s.mask[c + i]);
+            e[i] = e[i] < E ? e[i] : E;   // stays inside the decoder's records
+        }
+        int32_t m[kChunk];
+        int2 cr[kChunk];
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            m[i] = pmx[e[i]];
+            cr[i] = cold[e[i]];
+        }
+#pragma unroll
+        for (int i = 0; i < kChunk; ++i) {
+            const int k = c + i;
+            const int32_t U = s.U[k];
+            const int32_t lin = cr[i].x + int32_t(__umul24(uint32_t(U), uint32_t(cr[i].y)));
+            const int32_t pf = imax(imax(m[i], lin), U);
+            const int32_t peak = imax(s.p[k] + pf, base);
+            if constexpr (kPairs) store_pair<kFull>(row, k, peak | s.neg[k]);
+            const int32_t key = select_key<kPolicy>(peak, C, Qm);
+            const bool take = key < s.best_key[k];
+            s.best_key[k] = take ? key : s.best_key[k];
+            s.best_d[k] = take ? d : s.best_d[k];
+        }
+    }
+}
+
+// 16-byte units of a decoder's cold records {S_e, N_e + 1}, e = 0..E.
+__device__ __forceinline__ int64_t cold_units(int64_t E) { return (E + 2) / 2; }
 
 // One arrival tile against the decoders of group grp.  kMixed: some slices
 // may exceed an LDS buffer and are then read from HBM; otherwise every slice
@@ -448,14 +501,22 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                 asm("" : "+v"(s.pU[k]));   // opaque: keeps max(p + PMX, p + U, base) a single three-way max
             }
         }
-        auto staged = [&](const DecHeader& h) { return int64_t(half_w) + (kHot ? 1 : 2) * event_units(h.E); };
+        // staged units: rank words and PMX, and (full walk) the cold records after them
+        auto staged = [&](const DecHeader& h) {
+            return int64_t(half_w) + event_units(h.E) + (kHot ? 0 : cold_units(h.E));
+        };
         auto fits = [&](const DecHeader& h) { return staged(h) <= buf_units; };
+        auto stage_next = [&](v4i (&st)[kStage], const DecHeader& h) {
+            const int32_t split = half_w + int32_t(event_units(h.E));
+            stage_slice(st, V.slices + h.slice_off, int32_t(staged(h)), split,
+                        kHot ? 0 : int32_t(event_units(h.E)));   // the cold records skip the thresholds
+        };
         DecLanes lanes = load_lanes(g, V, d_begin, d_end);
         int32_t lanes0 = d_begin;
         v4i stage[kStage];
         DecHeader h = lane_header(lanes, 0);
         bool h_ok = d_begin < d_end && slice_ok(h, n_total, L) && (kMixed || fits(h));
-        if (h_ok && fits(h)) stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
+        if (h_ok && fits(h)) stage_next(stage, h);
         // one step per decoder; unrolled by two so that the buffer is a
         // compile-time offset where every slice is staged in LDS
         auto step = [&](int32_t d, auto par_tag) {
@@ -485,7 +546,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
                 h = lane_header(lanes, d + 1 - lanes0);
                 h_ok = slice_ok(h, n_total, L) && (kMixed || fits(h));
                 if (h_ok && fits(h))   // overlaps the evaluation
-                    stage_slice(stage, V.slices + h.slice_off, int32_t(staged(h)));
+                    stage_next(stage, h);
             }
             __syncthreads();
             if (!valid) return;
@@ -494,9 +555,13 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             if (!kMixed || in_lds) {
                 const int32_t* pmx = reinterpret_cast<const int32_t*>(slice + half_w);
                 const uint32_t rank_lds = kOdd ? uint32_t(kMixed ? buf_units : kStage * kNT) * 16u : 0u;
-                eval_records<kAPT, kFull, kPairs, kPolicy, kHot, true>(
-                    s, nullptr, rank_lds, pmx, pmx + 4 * event_units(cur.E), slice_cold(V, cur, L), uint32_t(cur.E),
-                    cur.base_peak, C, Q, d, row);
+                if constexpr (kHot)
+                    eval_records<kAPT, kFull, kPairs, kPolicy, true, true>(
+                        s, nullptr, rank_lds, pmx, nullptr, nullptr, uint32_t(cur.E), cur.base_peak, C, Q, d, row);
+                else
+                    eval_cold<kAPT, kFull, kPairs, kPolicy>(
+                        s, rank_lds, pmx, reinterpret_cast<const int2*>(slice + half_w + event_units(cur.E)),
+                        uint32_t(cur.E), cur.base_peak, C, Q, d, row);
             } else if constexpr (kMixed) {
                 eval_records<kAPT, kFull, kPairs, kPolicy, false, false>(
                     s, reinterpret_cast<const char*>(slice_rank(V, cur)) - lds_off, 0u, slice_pmx(V, cur, L),
@@ -554,7 +619,8 @@ __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
     const int32_t d_begin = grp * g.Dg;
     const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
-    if (g.L.W / 2 + 2 * ((int64_t(gm.records) + 3) / 4) <= g.buf_units) {
+    // the full walk stages rank words, PMX values and cold records: (E + 1) records of 4 + 8 bytes
+    if (g.L.W / 2 + (int64_t(gm.records) + 3) / 4 + (int64_t(gm.records) + 1) / 2 <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
             records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
         else
