@@ -36,6 +36,7 @@ namespace {
 constexpr int kCommitNT = 1024;
 constexpr int kWaves = kCommitNT / kWave;
 constexpr int64_t kFeasibleBias = int64_t(1) << 62;
+constexpr int kBatch = 8;   // dense entries a thread loads at once in a commit
 
 struct CommitLayout {
     int32_t D, L;          // decoders, steps per decoder (u_max + 1)
@@ -271,19 +272,28 @@ __global__ __launch_bounds__(kCommitNT) void commit_serial(CommitArgs a) {
             Q[bd] += 1;
         }
         // commit (p, Uc) to decoder bd: O += p + t on [0, Uc], then PF and SA there
-        int64_t* O = a.O + int64_t(bd) * L;
-        int64_t* PF = a.PF + int64_t(bd) * L;
-        int64_t* SA = a.SA + int64_t(bd) * L;
+        int64_t* __restrict__ O = a.O + int64_t(bd) * L;
+        int64_t* __restrict__ PF = a.PF + int64_t(bd) * L;
+        int64_t* __restrict__ SA = a.SA + int64_t(bd) * L;
         const int32_t n = Uc + 1;
         const int32_t chunk = (n + kCommitNT - 1) / kCommitNT;
         const int32_t b = threadIdx.x * chunk, e = b + chunk < n ? b + chunk : n;
         const int64_t sa_top = SA[Uc];   // max of O beyond Uc: unchanged by the commit
         int64_t mpre = 0, msuf = 0;
-        for (int32_t t = b; t < e; ++t) {
-            const int64_t o = O[t] + p + t;
-            O[t] = o;
-            mpre = max64(mpre, o + t);
-            msuf = max64(msuf, o);
+        // kBatch loads in flight at a time, then their updates
+        for (int32_t t0 = b; t0 < e; t0 += kBatch) {
+            int64_t o[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) o[j] = t0 + j < e ? O[t0 + j] : 0;
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int32_t t = t0 + j;
+                if (t >= e) break;
+                o[j] += p + t;
+                O[t] = o[j];
+                mpre = max64(mpre, o[j] + t);
+                msuf = max64(msuf, o[j]);
+            }
         }
         int64_t v;
         int64_t run = block_excl_scan<kCommitNT, true>(mpre, int64_t(0), scan_tmp, &v);
@@ -300,13 +310,28 @@ __global__ __launch_bounds__(kCommitNT) void commit_serial(CommitArgs a) {
         for (int w = wid + 1; w < kWaves; ++w) after = max64(after, scan_tmp[w]);
         const int64_t next = __shfl_down(incl, 1, kWave);
         if (lane + 1 < kWave) after = max64(after, next);
-        for (int32_t t = b; t < e; ++t) {
-            run = max64(run, O[t] + t);
-            PF[t] = run;
+        for (int32_t t0 = b; t0 < e; t0 += kBatch) {
+            int64_t o[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) o[j] = t0 + j < e ? O[t0 + j] : 0;
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (t0 + j >= e) break;
+                run = max64(run, o[j] + t0 + j);
+                PF[t0 + j] = run;
+            }
         }
-        for (int32_t t = e - 1; t >= b; --t) {
-            if (t < Uc) SA[t] = after;
-            after = max64(after, O[t]);
+        for (int32_t t1 = e; t1 > b; t1 -= kBatch) {   // [t1 - kBatch, t1) from the top down
+            int64_t o[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) o[j] = t1 - 1 - j >= b ? O[t1 - 1 - j] : 0;
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int32_t t = t1 - 1 - j;
+                if (t < b) break;
+                if (t < Uc) SA[t] = after;
+                after = max64(after, o[j]);
+            }
         }
         // the new PF(Uc) = v is a floor for every step above Uc
         if (threadIdx.x < kFenwickSteps) {
