@@ -27,6 +27,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
 DEFAULT_WORKLOAD = "large"     # 256 decoders x 4096 residents, 262,144 arrivals
 PLACE_SAMPLE = 5               # placement bracketed by timing events on every 5th timed step
+LEGS = ("window", "static", "blocks", "commit", "incremental", "appa", "record")
 BREAKDOWN_STEPS = 10           # untimed steps with an event at every phase boundary
 PLACEMENT_SOURCES = ("paper_2609_15359_amd/csrc/place.hip", "paper_2609_15359_amd/csrc/maps_internal.hpp",
                      "paper_2609_15359_amd/csrc/order_core.hpp")
@@ -672,7 +673,12 @@ def main():
                                                                "(for profiling its kernels)")
     ap.add_argument("--graph", action="store_true", help="replay one HIP graph per phase instead of "
                                                          "launching every kernel from the host")
+    ap.add_argument("--legs", default="all", help="comma-separated legs to run after the step ("
+                    + ", ".join(LEGS) + "), 'all' or 'none' (for profiling the step alone)")
     args = ap.parse_args()
+    legs = set(LEGS) if args.legs == "all" else set() if args.legs == "none" else set(args.legs.split(","))
+    if legs - set(LEGS):
+        ap.error(f"unknown legs: {sorted(legs - set(LEGS))}")
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (--gpus {args.gpus} requested); "
               "the multi-GPU split is described in DESIGN.md", file=sys.stderr)
@@ -800,19 +806,25 @@ def main():
         ref = oracle.step(b, oracle.Oracle(), want_pairs=True)
     # the outputs of the last timed step (the breakdown steps rewrote the same values)
     result.update(verify_step(ws, ref))
-    # the next rows on the path: sliding-window calibration and Algorithm 1 on block counts, same batch
-    result["window_calibration"] = window_calibration(b, cpu=not args.no_cpu_baseline)
+    # the next rows on the path, on the same batch
+    cpu = not args.no_cpu_baseline
     nr, na = db.n_res, db.n_arr
-    result["static_placement"] = static_placement(b, db, ws.out["U"][:nr], ws.out["U"][nr:nr + na],
-                                                  cpu=not args.no_cpu_baseline)
-    result["block_placement"] = block_placement(b, db, ws.out["U"][:nr], ws.out["U"][nr:nr + na],
-                                                cpu=not args.no_cpu_baseline)
-    snap = maps.Snapshot(data=ws.snapshot, D=D, n_total=nr, u_max=db.u_max)
-    result["sequential_commit"] = sequential_commit(b, db, snap, ws.out["U"][nr:nr + na], ref,
-                                                    cpu=not args.no_cpu_baseline)
-    result["incremental_window"] = incremental_window(b, ref, cpu=not args.no_cpu_baseline)
-    result["appa_simulation"] = appa_simulation(cpu=not args.no_cpu_baseline)
-    result["record_path"] = record_path(cpu=not args.no_cpu_baseline)
+    U_res, U_arr = ws.out["U"][:nr], ws.out["U"][nr:nr + na]
+    if "window" in legs:
+        result["window_calibration"] = window_calibration(b, cpu=cpu)
+    if "static" in legs:
+        result["static_placement"] = static_placement(b, db, U_res, U_arr, cpu=cpu)
+    if "blocks" in legs:
+        result["block_placement"] = block_placement(b, db, U_res, U_arr, cpu=cpu)
+    if "commit" in legs:
+        snap = maps.Snapshot(data=ws.snapshot, D=D, n_total=nr, u_max=db.u_max)
+        result["sequential_commit"] = sequential_commit(b, db, snap, U_arr, ref, cpu=cpu)
+    if "incremental" in legs:
+        result["incremental_window"] = incremental_window(b, ref, cpu=cpu)
+    if "appa" in legs:
+        result["appa_simulation"] = appa_simulation(cpu=cpu)
+    if "record" in legs:
+        result["record_path"] = record_path(cpu=cpu)
     print(json.dumps(result), flush=True)
 
 

@@ -116,6 +116,20 @@ enum {
 enum { MAPS_POLICY_MQ = 0, MAPS_POLICY_MC = 1 };
 
 /* ------------------------------------------------------------------------ */
+/* 0. Capacities in bytes (App. A: KV tokens and bytes are related by model  */
+/*    constants)                                                             */
+/* ------------------------------------------------------------------------ */
+/*
+ * capacity_tokens[d] = floor(capacity_bytes[d] / bytes_per_token) for the D
+ * decoders (device arrays; int64 in, int32 out), the token capacities the
+ * other calls take.  dev_err bits: NEG_LEN (a negative byte count: 0 tokens),
+ * INT32_RANGE (more than INT32_MAX tokens: clamped).
+ * Host errors: NULL, SIZE (D < 1, bytes_per_token < 1), HIP.
+ */
+maps_status maps_capacity_tokens(const int64_t* capacity_bytes, int32_t D, int64_t bytes_per_token,
+                                 int32_t* capacity_tokens, uint32_t* dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* 1. Uncertainty-aware calibration (Sec. 3.2, Eqs. (2)-(4))                */
 /* ------------------------------------------------------------------------ */
 /*

@@ -87,6 +87,7 @@ _SIGNATURES = {
     "maps_calibrate_noalloc": (_i32, [_vp, _vp, _i64, _vp, _i32, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "maps_project_order": (_i32, [_i32, _vp, _i64, _vp, _vp, _vp, _i32, _vp, _sz, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
                                   _i32, _vp, _vp, _vp, _vp]),
+    "maps_capacity_tokens": (_i32, [_vp, _i32, _i64, _vp, _vp, _vp]),
     "maps_status_string": (_c.c_char_p, [_i32]),
 }
 EXPORTS = tuple(_SIGNATURES)
@@ -161,10 +162,18 @@ def check_errors(dev_err: torch.Tensor):
         raise MapsError("device value error: " + ", ".join(error_names(bits)))
 
 
-def capacity_tokens(capacity_bytes: torch.Tensor, bytes_per_token: int) -> torch.Tensor:
-    """KV capacity in bytes -> tokens (App. A: tokens map to bytes by model
-    constants).  floor(C / b) is exact for the test peak * b <= C."""
-    return torch.div(capacity_bytes, int(bytes_per_token), rounding_mode="floor").to(torch.int32)
+def capacity_tokens(capacity_bytes: torch.Tensor, bytes_per_token: int, dev_err=None) -> torch.Tensor:
+    """KV capacity in bytes -> tokens, floor(C / b) (App. A: tokens map to
+    bytes by model constants); int64 device tensor in, int32 out."""
+    capacity_bytes = _dev(capacity_bytes, torch.int64, "capacity_bytes")
+    dev = capacity_bytes.device
+    out = torch.empty(capacity_bytes.numel(), dtype=torch.int32, device=dev)
+    err = new_error_word(dev) if dev_err is None else dev_err
+    _check(library().maps_capacity_tokens(_ptr(capacity_bytes), capacity_bytes.numel(), int(bytes_per_token),
+                                          _ptr(out), _ptr(err), _stream(dev)), "maps_capacity_tokens")
+    if dev_err is None:
+        check_errors(err)
+    return out
 
 
 # ---------------------------------------------------------------------------

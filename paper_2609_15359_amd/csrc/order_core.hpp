@@ -139,16 +139,44 @@ __device__ inline int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* ra
     return block_reduce_max<kOrderNT>(best, s.red64);
 }
 
+// Decoder d's queue bounds and capacity, and, when the queue holds at most
+// one wavefront of requests, request i's prompt, bound and wait in thread i
+// (0 elsewhere).  Called early by a launch that has other work first, so
+// that these loads are in flight during it.
+struct QueueFetch {
+    int64_t qlo, qhi;
+    int32_t C, pr, u, wait;
+};
+
+__device__ inline QueueFetch fetch_queue(const LocalArgs& g, int32_t d) {
+    QueueFetch f;
+    f.qlo = g.q_off[d];
+    f.qhi = g.q_off[d + 1];
+    f.C = g.cap[d];
+    f.pr = 0;
+    f.u = 0;
+    f.wait = 0;
+    const int64_t i = f.qlo + int64_t(threadIdx.x);
+    if (0 <= f.qlo && f.qlo <= f.qhi && f.qhi <= g.total && f.qhi - f.qlo <= kWave && i < f.qhi) {
+        f.pr = g.qp[i];
+        f.u = g.qU[i];
+        f.wait = g.qwait != nullptr ? g.qwait[i] : 0;
+    }
+    return f;
+}
+
 // The whole local order of decoder d by one workgroup of kOrderNT threads.
-// built_n_total >= 0: the snapshot's decoder d was written by this workgroup
-// (the projection's launch), whose header the workgroup cannot read back
-// reliably; the resident count is then given.
-__device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_n_total = -1) {
+// built != nullptr: the snapshot's decoder d was written by this workgroup
+// (the projection's launch), which passes the header it wrote (the
+// snapshot's own header, written by another workgroup, cannot be read back
+// reliably) and the resident count.  pre (nullable): fetch_queue's values.
+__device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_n_total = -1,
+                                   const DecHeader* built = nullptr, const QueueFetch* pre = nullptr) {
     __shared__ LocalLds s;
     const SnapLayout& L = g.L;
     const SnapView V = snap_view(const_cast<void*>(g.snap), L);
     int64_t n_total = built_n_total;
-    if (built_n_total < 0) {
+    if (built == nullptr) {
         const SnapHeader hdr = *V.hdr;
         if (!(hdr.magic == kSnapMagic && hdr.D == L.D && hdr.u_max == L.u_max && hdr.W == L.W)) {
             if (d == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
@@ -156,12 +184,13 @@ __device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_
         }
         n_total = hdr.n_total;
     }
-    const DecHeader h = V.dec[d];
+    const DecHeader h = built != nullptr ? *built : V.dec[d];
     if (!slice_ok(h, n_total, L)) {
         if (threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         return;
     }
-    int64_t qlo = g.q_off[d], qhi = g.q_off[d + 1];
+    const QueueFetch f = pre != nullptr ? *pre : fetch_queue(g, d);
+    const int64_t qlo = f.qlo, qhi = f.qhi;
     if (!(0 <= qlo && qlo <= qhi && qhi <= g.total)) {
         if (threadIdx.x == 0) { raise_error(g.dev_err, MAPS_ERR_SEG_OFFSETS); g.admitted[d] = 0; }
         return;
@@ -172,7 +201,7 @@ __device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_
         return;
     }
     const int n = int(n64);
-    const int32_t C = g.cap[d];
+    const int32_t C = f.C;
     if (threadIdx.x == 0 && C < 0) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
     int n2 = 1;
     while (n2 < n) n2 <<= 1;
@@ -185,12 +214,12 @@ __device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_
             uint64_t key = ~0ull, key2 = ~0ull;
             bool neg = false;
             if (i < n) {
-                const int32_t pr = g.qp[qlo + i], u = g.qU[qlo + i];
+                const int32_t pr = f.pr, u = f.u;   // fetch_queue's: the queue fits one wavefront
                 neg = pr < 0;
                 s.pp[i] = pr < 0 ? 0 : pr;
                 const int32_t ue = u < 0 ? L.u_max : u;
                 s.ue[i] = ue;
-                const bool promoted = g.qwait != nullptr && g.qwait[qlo + i] >= g.max_wait;
+                const bool promoted = g.qwait != nullptr && f.wait >= g.max_wait;
                 const uint64_t cls = promoted ? 0ull : (1ull << 63);
                 const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
                 key = cls | (val << 32) | uint64_t(uint32_t(i));

@@ -208,17 +208,30 @@ __device__ __forceinline__ int32_t event_peak(const int32_t* pmx, const int32_t*
     return imax(p + pf, base);
 }
 
-// Arrival k of the thread's tile with its prompt clamped at 0, reporting the
-// error bits of the tile's arrivals.
-template <int kAPT, bool kFull>
-__device__ __forceinline__ void load_arrivals(const PlaceArgs& g, int64_t a0, int64_t max_tot, int32_t (&p)[kAPT],
-                                              int32_t (&U)[kAPT]) {
-    bool neg = false, range = false;
+// Raw prompt and bound of arrival k of the thread's tile (bound -1 past the
+// batch).  Issued first in a workgroup: nothing else is needed to address
+// them, so their latency overlaps the snapshot's header reads.
+template <int kAPT>
+__device__ __forceinline__ void fetch_arrivals(const PlaceArgs& g, int64_t a0, int32_t (&p)[kAPT],
+                                               int32_t (&U)[kAPT]) {
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
-        int32_t pk = 0, Uk = -1;
-        if (kFull || a < g.A) { pk = g.ap[a]; Uk = g.aU[a]; }
+        p[k] = 0;
+        U[k] = -1;
+        if (a < g.A) { p[k] = g.ap[a]; U[k] = g.aU[a]; }
+    }
+}
+
+// The fetched arrivals with their prompts clamped at 0, reporting the error
+// bits of the tile's arrivals.
+template <int kAPT>
+__device__ __forceinline__ void check_arrivals(const PlaceArgs& g, int64_t max_tot, const int32_t (&rp)[kAPT],
+                                               const int32_t (&rU)[kAPT], int32_t (&p)[kAPT], int32_t (&U)[kAPT]) {
+    bool neg = false, range = false;
+#pragma unroll
+    for (int k = 0; k < kAPT; ++k) {
+        const int32_t pk = rp[k], Uk = rU[k];
         neg |= pk < 0;
         if (Uk >= 0 && int64_t(pk) + Uk + max_tot + g.L.u_max > int64_t(INT32_MAX)) range = true;
         p[k] = pk < 0 ? 0 : pk;
@@ -426,7 +439,8 @@ __device__ __forceinline__ int64_t cold_units(int64_t E) { return (E + 2) / 2; }
 // fits (a header claiming more is reported and skipped).
 template <int kAPT, bool kFull, bool kPairs, int kPolicy, bool kMixed>
 __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView& V, int4* lds, int32_t grp,
-                                             int64_t a0, const GroupMax& gm) {
+                                             int64_t a0, const GroupMax& gm, const int32_t (&rp)[kAPT],
+                                             const int32_t (&rU)[kAPT], const DecLanes& first_lanes) {
     const SnapLayout& L = g.L;
     const int32_t half_w = L.W / 2;                // rank words in 16-byte units
     const int32_t d_begin = grp * g.Dg;
@@ -439,7 +453,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
     // LDS address of buffer 0 (where the dynamic LDS starts)
     const uint32_t lds_off = uint32_t(size_t((__attribute__((address_space(3))) char*)lds));
     RecArrivals<kAPT> s;
-    load_arrivals<kAPT, kFull>(g, a0, gm.tot, s.p, s.U);
+    check_arrivals<kAPT>(g, gm.tot, rp, rU, s.p, s.U);
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int32_t U = s.U[k];
@@ -511,6 +525,8 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             stage_slice(st, V.slices + h.slice_off, int32_t(staged(h)), split,
                         kHot ? 0 : int32_t(event_units(h.E)));   // the cold records skip the thresholds
         };
+        // loaded here rather than with the tile's first loads: holding them
+        // across the preamble costs this walk registers and time
         DecLanes lanes = load_lanes(g, V, d_begin, d_end);
         int32_t lanes0 = d_begin;
         v4i stage[kStage];
@@ -580,7 +596,7 @@ __device__ __forceinline__ void records_tile(const PlaceArgs& g, const SnapView&
             s.pU[k] = s.p[k] + s.U[k];
             asm("" : "+v"(s.pU[k]));   // opaque: keeps max(p + PMX_E, p + U, base) a single three-way max
         }
-        DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+        DecLanes lanes = first_lanes;
         int32_t lanes0 = d_begin;
         for (int32_t d = d_begin; d < d_end; ++d) {
             if (d - lanes0 == kWave) {
@@ -611,25 +627,37 @@ template <int kAPT, bool kPairs, int kPolicy>
 __global__ __launch_bounds__(kNT) void place_records(PlaceArgs g) {
     extern __shared__ int4 lds[];
     const SnapView V = snap_view(const_cast<void*>(g.snap), g.L);
+    const int32_t grp = blockIdx.x % g.G;
+    const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
+    const int32_t d_begin = grp * g.Dg;
+    const int32_t d_end = d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D;
+    // The tile's arrivals go out first (they need nothing but the arguments),
+    // so their latency overlaps the snapshot header's check; the decoder
+    // headers are read only once the header shows that the buffer holds them,
+    // the first 64 decoders' values (for the flat walk) and the group's
+    // maxima together.
+    int32_t rp[kAPT], rU[kAPT];
+    fetch_arrivals<kAPT>(g, a0, rp, rU);
     if (!snapshot_ok(V.hdr, g.L)) {
         if (blockIdx.x == 0 && threadIdx.x == 0) raise_error(g.dev_err, MAPS_ERR_SNAPSHOT);
         return;
     }
-    const int32_t grp = blockIdx.x % g.G;
-    const int64_t a0 = int64_t(blockIdx.x / g.G) * (kNT * kAPT);
-    const int32_t d_begin = grp * g.Dg;
-    const GroupMax gm = group_max(V, d_begin, d_begin + g.Dg < g.L.D ? d_begin + g.Dg : g.L.D);
+    const DecLanes lanes = load_lanes(g, V, d_begin, d_end);
+    const GroupMax gm = group_max(V, d_begin, d_end);
     // the full walk stages rank words, PMX values and cold records: (E + 1) records of 4 + 8 bytes
     if (g.L.W / 2 + (int64_t(gm.records) + 3) / 4 + (int64_t(gm.records) + 1) / 2 <= g.buf_units) {
         if (a0 + kNT * kAPT <= g.A)
-            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
+            records_tile<kAPT, true, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm, rp, rU, lanes);
         else
-            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm);
+            records_tile<kAPT, false, kPairs, kPolicy, false>(g, V, lds, grp, a0, gm, rp, rU, lanes);
     } else {
         constexpr int kSub = kAPT < 4 ? kAPT : 4;
         for (int t = 0; t < kAPT / kSub; ++t) {
             const int64_t b0 = a0 + int64_t(t) * kNT * kSub;
-            if (b0 < g.A) records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0, gm);
+            if (b0 >= g.A) continue;
+            int32_t sp[kSub], sU[kSub];
+            fetch_arrivals<kSub>(g, b0, sp, sU);
+            records_tile<kSub, false, kPairs, kPolicy, true>(g, V, lds, grp, b0, gm, sp, sU, lanes);
         }
     }
 }
@@ -690,7 +718,11 @@ __device__ __forceinline__ void prof_tile(const PlaceArgs& g, const SnapView& V,
     const int64_t tile_n = g.A - a0 < kNT * kAPT ? g.A - a0 : kNT * kAPT;
 
     ProfArrivals<kAPT> s;
-    load_arrivals<kAPT, kFull>(g, a0, group_max(V, d_begin, d_end).tot, s.p, s.U);
+    {
+        int32_t rp[kAPT], rU[kAPT];
+        fetch_arrivals<kAPT>(g, a0, rp, rU);
+        check_arrivals<kAPT>(g, group_max(V, d_begin, d_end).tot, rp, rU, s.p, s.U);
+    }
 #pragma unroll
     for (int k = 0; k < kAPT; ++k) {
         const int32_t U = s.U[k];

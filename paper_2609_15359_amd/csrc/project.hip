@@ -120,7 +120,7 @@ template <bool kInLds, typename Arr>
 __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int32_t* __restrict__ p,
                             const int32_t* __restrict__ g, const int32_t* __restrict__ U, int32_t u_max, int32_t W,
                             int32_t P, SnapView V, int64_t slice_off, int32_t* __restrict__ base_peak, uint32_t* dev_err,
-                            Scratch& sc) {
+                            Scratch& sc, DecHeader* hdr_out) {
     const int tid = threadIdx.x;
     for (int64_t w = tid; w < W; w += kNT) a.B(w) = 0u;
     if constexpr (kInLds) {   // the event counters too: E <= residents <= the LDS capacity
@@ -390,21 +390,23 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         h.pmx_end = pmx_end;
         for (int i = 0; i < 6; ++i) h.pad[i] = 0;
         V.dec[d] = h;
+        if (hdr_out != nullptr) *hdr_out = h;
         base_peak[d] = base;
     }
 }
 
 // Decoder d's projection (the slice, its header and base peak) by one
 // workgroup of kNT threads; `lds` is the launch's dynamic LDS.
-__device__ inline void project_decoder(int32_t d, int32_t D, const int64_t* __restrict__ seg_off, int64_t n_total,
+// [lo, hi): the decoder's residents (seg_off[d], seg_off[d + 1], loaded by the
+// caller); hdr_out (nullable, LDS): receives the decoder header written.
+__device__ inline void project_decoder(int32_t d, int32_t D, int64_t lo, int64_t hi, int64_t n_total,
                                        const int32_t* __restrict__ p, const int32_t* __restrict__ g,
                                        const int32_t* __restrict__ U, int32_t u_max, const SnapLayout& L,
                                        void* snap, int32_t* __restrict__ base_peak, int64_t lds_cap,
-                                       uint32_t* dev_err, uint32_t* lds) {
+                                       uint32_t* dev_err, uint32_t* lds, DecHeader* hdr_out = nullptr) {
     __shared__ Scratch sc;
     const int32_t W = L.W;
     SnapView V = snap_view(snap, L);
-    int64_t lo = seg_off[d], hi = seg_off[d + 1];
     if (!(0 <= lo && lo <= hi && hi <= n_total)) {
         if (threadIdx.x == 0) raise_error(dev_err, MAPS_ERR_SEG_OFFSETS);
         lo = lo < 0 ? 0 : (lo > n_total ? n_total : lo);
@@ -435,14 +437,14 @@ __device__ inline void project_decoder(int32_t d, int32_t D, const int64_t* __re
         a.wsum = a.cnt + lds_cap;
         a.tau = a.wsum + lds_cap;
         a.pmx = a.tau + lds_cap;
-        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
+        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc, hdr_out);
     } else {
         HbmArrays a;
         a.rank = reinterpret_cast<uint32_t*>(V.slices + slice_off);
         a.pmx = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
         a.thr = nullptr;
         a.cold = nullptr;
-        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc);
+        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc, hdr_out);
     }
 }
 
@@ -453,8 +455,9 @@ __global__ __launch_bounds__(kNT) void project_decoders(int32_t D, const int64_t
                                                         SnapLayout L, void* snap, int32_t* __restrict__ base_peak,
                                                         int64_t lds_cap, uint32_t* dev_err) {
     extern __shared__ uint32_t lds[];
-    project_decoder(int32_t(blockIdx.x), D, seg_off, n_total, p, g, U, u_max, L, snap, base_peak, lds_cap, dev_err,
-                    lds);
+    const int32_t d = int32_t(blockIdx.x);
+    project_decoder(d, D, seg_off[d], seg_off[d + 1], n_total, p, g, U, u_max, L, snap, base_peak, lds_cap,
+                    dev_err, lds);
 }
 
 // Projection and local order in one launch: workgroup d projects decoder d,
@@ -470,10 +473,15 @@ __global__ __launch_bounds__(kNT) void project_order_decoders(int32_t D, const i
                                                               int32_t* __restrict__ base_peak, int64_t lds_cap,
                                                               uint32_t* dev_err, order::LocalArgs o) {
     extern __shared__ uint32_t lds[];
+    __shared__ DecHeader hdr;
     const int32_t d = int32_t(blockIdx.x);
-    project_decoder(d, D, seg_off, n_total, p, g, U, u_max, L, snap, base_peak, lds_cap, dev_err, lds);
-    __syncthreads();   // the slice and header stores of this workgroup are done
-    order::order_queue(o, d, n_total);
+    // the residents' offsets and the queue's inputs are loaded together
+    // first, so the queue's loads are in flight during the projection
+    const int64_t lo = seg_off[d], hi = seg_off[d + 1];
+    const order::QueueFetch qf = order::fetch_queue(o, d);
+    project_decoder(d, D, lo, hi, n_total, p, g, U, u_max, L, snap, base_peak, lds_cap, dev_err, lds, &hdr);
+    __syncthreads();   // the slice and header stores of this workgroup are done; hdr holds the header
+    order::order_queue(o, d, n_total, &hdr, &qf);
 }
 
 }  // namespace

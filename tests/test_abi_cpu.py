@@ -125,6 +125,11 @@ def test_host_argument_errors_without_gpu(lib):
     # the workspace holds the scores three times over (grouped, by bucket, and their
     # log indices) plus a quantile per position of every bucket
     assert lib.maps_calibrate_window_workspace_size(100000, 64) >= 100000 * 18
+    # byte capacities: D < 1, bytes per token < 1, NULL
+    assert lib.maps_capacity_tokens(fake, 0, 131072, fake, fake, None) == -2
+    assert lib.maps_capacity_tokens(fake, 4, 0, fake, fake, None) == -2
+    assert lib.maps_capacity_tokens(None, 4, 131072, fake, fake, None) == -1
+    assert lib.maps_capacity_tokens(fake, 4, 131072, fake, None, None) == -1
 
 
 def test_binding_refuses_host_tensors(lib):

@@ -130,6 +130,15 @@ def test_byte_capacity_boundary(orc):
     cap_bytes = b.capacity.astype(np.int64) * bpt + 12345
     cap = maps.capacity_tokens(torch.from_numpy(cap_bytes).cuda(), bpt).cpu().numpy()
     assert np.array_equal(cap, b.capacity)
+    # floor division at the edges, and the value errors of the conversion
+    edge = np.array([0, bpt - 1, bpt, 2 * bpt - 1, (2**31 - 1) * bpt, (2**31 - 1) * bpt + bpt - 1], np.int64)
+    got = maps.capacity_tokens(torch.from_numpy(edge).cuda(), bpt).cpu().numpy()
+    assert got.tolist() == (edge // bpt).tolist()
+    err = maps.new_error_word()
+    bad = np.array([-1, 2**31 * bpt, 5 * bpt], np.int64)
+    got = maps.capacity_tokens(torch.from_numpy(bad).cuda(), bpt, dev_err=err).cpu().numpy()
+    assert got.tolist() == [0, 2**31 - 1, 5]
+    assert set(maps.error_names(int(err.item()) & 0xFFFFFFFF)) == {"NEG_LEN", "INT32_RANGE"}
     o0 = oracle_step(b, o=orc, want_pairs=False)
     fit = fit_capacity(b, o0)
     g = gpu_step(b, capacity=fit, want_pairs=False)
