@@ -496,11 +496,12 @@ __device__ int32_t select_bucket(const SelectArgs& A, int b) {
     __shared__ uint32_t roff[kSortMaxChunks];           // where each run starts among the bucket's scores
     __shared__ uint32_t rcnt[kSortMaxChunks];           // its size
     __shared__ uint32_t rsrc[kSortMaxChunks];           // its first score's index in `sorted`
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[2][256];                   // digit histograms of alternate passes
     __shared__ uint32_t red[kSelWaves];
-    __shared__ uint32_t pick[2];
+    __shared__ uint32_t pick[2][2];                     // digit and remaining rank of alternate passes
     const int t = threadIdx.x;
     const int lane = t % kWave, w = t / kWave;
+    if (t < 256) hist[0][t] = 0;   // published by the barriers of the scans below
     uint32_t c = 0, m = 0, src = 0;
     if (t < chunks) {
         c = A.run_cnt[int64_t(b) * chunks + t];
@@ -529,10 +530,14 @@ __device__ int32_t select_bucket(const SelectArgs& A, int b) {
     // bucket (16-byte LDS reads); groups past n_b are skipped whole.
     uint32_t x[kKeep] = {};
     auto slot = [&](int j) { return uint32_t(j / 4) * (4 * kSelNT) + 4 * uint32_t(t) + uint32_t(j % 4); };
+    uint32_t zeros = 0;   // the first pass's digit-0 count of this wavefront
     if (in_regs) {
         // wavefront w gathers runs w, w + kSelWaves, ...: the first 128
         // scores of kGatherRuns runs in flight per lane, longer runs' rest
         // after.  Lane q reads run q's table entry; the wavefront shares it.
+        // Every score also enters the first pass's histogram (its top digit:
+        // every score lies below 256 << top) as it arrives, so that pass
+        // needs no loop of its own.
         for (int64_t r0 = w; r0 < chunks; r0 += int64_t(kSelWaves) * kGatherRuns) {
             const int64_t rq = r0 + int64_t(lane) * kSelWaves;
             const bool has = lane < kGatherRuns && rq < chunks;
@@ -550,9 +555,17 @@ __device__ int32_t select_bucket(const SelectArgs& A, int b) {
                 const uint32_t d0 = __builtin_amdgcn_readlane(to, q);
                 if (uint32_t(lane) < cn) stage[d0 + lane] = v0[q];
                 if (uint32_t(lane) + kWave < cn) stage[d0 + kWave + lane] = v1[q];
-                for (uint32_t i = 2 * kWave + lane; i < cn; i += kWave) stage[d0 + i] = uint32_t(sorted[s0 + i]);
+                hist_add(hist[0], uint32_t(lane) < cn, v0[q] >> top, zeros);
+                hist_add(hist[0], uint32_t(lane) + kWave < cn, v1[q] >> top, zeros);
+                for (uint32_t i0 = 2 * kWave; i0 < cn; i0 += kWave) {   // bounds uniform across the wavefront
+                    const uint32_t i = i0 + lane;
+                    const uint32_t v = i < cn ? uint32_t(sorted[s0 + i]) : 0u;
+                    if (i < cn) stage[d0 + i] = v;
+                    hist_add(hist[0], i < cn, v >> top, zeros);
+                }
             }
         }
+        hist_flush_zeros(hist[0], zeros);
         __syncthreads();
 #pragma unroll
         for (int g = 0; g < kKeep / 4; ++g) {
@@ -564,35 +577,41 @@ __device__ int32_t select_bucket(const SelectArgs& A, int b) {
             x[4 * g + 3] = v.w;
         }
     }
+    // Pass p builds hist[p & 1] and picks into pick[p & 1]; the other
+    // histogram is cleared meanwhile for the next pass.  Two barriers a pass:
+    // after the histogram (before the pick) and after the pick (before
+    // everyone reads it); a buffer is reused two passes later, past both.
     uint32_t prefix = 0;
-    for (int shift = top; shift >= 0; shift -= 8) {
-        if (t < 256) hist[t] = 0;
-        __syncthreads();
-        uint32_t zeros = 0;
-        if (in_regs) {
+    int pass = 0;
+    for (int shift = top; shift >= 0; shift -= 8, ++pass) {
+        const int cur = pass & 1;
+        if (t < 256) hist[cur ^ 1][t] = 0;   // last read by the pick of the previous pass
+        if (!(in_regs && pass == 0)) {       // the gather built the first in-register pass
+            zeros = 0;
+            if (in_regs) {
 #pragma unroll
-            for (int j = 0; j < kKeep; ++j) {
-                if (j % 4 == 0 && uint32_t(j / 4) * (4 * kSelNT) >= nbk) break;
-                const uint32_t y = x[j] >> shift;
-                hist_add(hist, slot(j) < nbk && (y >> 8) == prefix, y & 255u, zeros);
-            }
-        } else {
-            for (int64_t r = w; r < chunks; r += kSelWaves) {
-                const uint32_t cn = rcnt[r], s0 = rsrc[r];
-                for (uint32_t i0 = 0; i0 < cn; i0 += kWave) {   // bounds uniform across the wavefront
-                    const uint32_t i = i0 + lane;
-                    const uint32_t y = i < cn ? uint32_t(sorted[s0 + i]) >> shift : 0u;
-                    hist_add(hist, i < cn && (y >> 8) == prefix, y & 255u, zeros);
+                for (int j = 0; j < kKeep; ++j) {
+                    if (j % 4 == 0 && uint32_t(j / 4) * (4 * kSelNT) >= nbk) break;
+                    const uint32_t y = x[j] >> shift;
+                    hist_add(hist[cur], slot(j) < nbk && (y >> 8) == prefix, y & 255u, zeros);
+                }
+            } else {
+                for (int64_t r = w; r < chunks; r += kSelWaves) {
+                    const uint32_t cn = rcnt[r], s0 = rsrc[r];
+                    for (uint32_t i0 = 0; i0 < cn; i0 += kWave) {   // bounds uniform across the wavefront
+                        const uint32_t i = i0 + lane;
+                        const uint32_t y = i < cn ? uint32_t(sorted[s0 + i]) >> shift : 0u;
+                        hist_add(hist[cur], i < cn && (y >> 8) == prefix, y & 255u, zeros);
+                    }
                 }
             }
+            hist_flush_zeros(hist[cur], zeros);
+            __syncthreads();
         }
-        hist_flush_zeros(hist, zeros);
+        if (t < kWave) pick_digit(hist[cur], k, pick[cur]);
         __syncthreads();
-        if (t < kWave) pick_digit(hist, k, pick);
-        __syncthreads();
-        prefix = (prefix << 8) | pick[0];
-        k = int32_t(pick[1]);
-        __syncthreads();
+        prefix = (prefix << 8) | pick[cur][0];
+        k = int32_t(pick[cur][1]);
     }
     if (t == 0) q_out[b] = int32_t(prefix);
     publish_q(A.qflag, b, int32_t(prefix));

@@ -116,7 +116,10 @@ __device__ inline int4 block_reduce_max4(int4 v, int4* tmp, int64_t* sum = nullp
     return r;
 }
 
-template <bool kInLds, typename Arr>
+// kRP residents and kEP events per thread in registers: (4, 4) for decoders
+// of at most 4 * kNT residents (fewer instructions in every unrolled loop),
+// (8, 8) otherwise.
+template <bool kInLds, int kRP, int kEP, typename Arr>
 __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int32_t* __restrict__ p,
                             const int32_t* __restrict__ g, const int32_t* __restrict__ U, int32_t u_max, int32_t W,
                             int32_t P, SnapView V, int64_t slice_off, int32_t* __restrict__ base_peak, uint32_t* dev_err,
@@ -129,13 +132,13 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     phase<kInLds>();
 
     // 1. event bitmap and total demand sum_r (p + g + R).  A decoder of at
-    // most kNT * kResPer residents is read once, every load in flight
+    // most kNT * kRP residents is read once, every load in flight
     // together, and keeps R and p + g in registers for step 3.
     int64_t tot = 0;
     bool neg = false, range = false;
     const int64_t n = hi - lo;
-    const bool in_regs = n <= int64_t(kNT) * kResPer;
-    uint32_t Rk[kResPer], PGk[kResPer];
+    const bool in_regs = n <= int64_t(kNT) * kRP;
+    uint32_t Rk[kRP], PGk[kRP];
     auto resident = [&](int32_t pr, int32_t gr, int32_t ur, uint32_t& Rout, uint32_t& PGout) {
         neg |= (pr < 0) | (gr < 0) | (ur < 0);
         pr = pr < 0 ? 0 : pr;
@@ -148,16 +151,16 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         PGout = uint32_t(pr) + uint32_t(gr);
     };
     if (in_regs) {
-        int32_t pr[kResPer], gr[kResPer], ur[kResPer];
+        int32_t pr[kRP], gr[kRP], ur[kRP];
 #pragma unroll
-        for (int j = 0; j < kResPer; ++j) {
+        for (int j = 0; j < kRP; ++j) {
             const int64_t i = int64_t(j) * kNT + tid;
             pr[j] = i < n ? p[lo + i] : 0;
             gr[j] = i < n ? g[lo + i] : 0;
             ur[j] = i < n ? U[lo + i] : 0;
         }
 #pragma unroll
-        for (int j = 0; j < kResPer; ++j) {
+        for (int j = 0; j < kRP; ++j) {
             Rk[j] = 0u;
             PGk[j] = 0u;
             if (int64_t(j) * kNT + tid < n) resident(pr[j], gr[j], ur[j], Rk[j], PGk[j]);
@@ -204,7 +207,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     };
     if (in_regs) {
 #pragma unroll
-        for (int j = 0; j < kResPer; ++j)
+        for (int j = 0; j < kRP; ++j)
             if (int64_t(j) * kNT + tid < n) count(Rk[j], PGk[j]);
     } else {
         for (int64_t r = lo + tid; r < hi; r += kNT) {
@@ -236,16 +239,16 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
     // register chunks of the LDS path: after the pass below, per event the
     // suffix count N_e (cN), the suffix sum S_e (cS), the threshold T_e (cT)
     // and PMX_e (cM)
-    uint32_t cN[kEvPer], cS[kEvPer], cT[kEvPer];
-    int32_t cM[kEvPer];
-    bool ok[kEvPer];
+    uint32_t cN[kEP], cS[kEP], cT[kEP];
+    int32_t cM[kEP];
+    bool ok[kEP];
     const int chunk = int((int64_t(E) + kNT - 1) / kNT);
     const int e0 = kInLds ? tid * chunk : 0;
     if constexpr (kInLds) {
-        // E <= residents <= kNT * kEvPer: each thread keeps its contiguous
+        // E <= residents <= kNT * kEP: each thread keeps its contiguous
         // chunk of events in registers through both scans and the thresholds
 #pragma unroll
-        for (int j = 0; j < kEvPer; ++j) {
+        for (int j = 0; j < kEP; ++j) {
             const int e = e0 + j;
             ok[j] = j < chunk && e < int(E);
             cN[j] = ok[j] ? a.C(e) : 0u;
@@ -254,15 +257,15 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         }
         uint64_t loc = 0;
 #pragma unroll
-        for (int j = 0; j < kEvPer; ++j) loc += (uint64_t(cN[j]) << 32) | cS[j];
+        for (int j = 0; j < kEP; ++j) loc += (uint64_t(cN[j]) << 32) | cS[j];
         uint64_t all;
         const uint64_t before =
             block_excl_scan<kNT, false, uint64_t, false>(loc, uint64_t(0), reinterpret_cast<uint64_t*>(sc.red64), &all);
         uint64_t run = all - before - loc;   // the events after this chunk
-        int32_t v[kEvPer];
+        int32_t v[kEP];
         int32_t lmax = 0;
 #pragma unroll
-        for (int j = kEvPer - 1; j >= 0; --j) {
+        for (int j = kEP - 1; j >= 0; --j) {
             run += (uint64_t(cN[j]) << 32) | cS[j];
             cN[j] = uint32_t(run >> 32);
             cS[j] = uint32_t(run);
@@ -275,7 +278,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         pmx_end = mall;
         uint32_t prev_tau = e0 >= 1 && e0 - 1 < int(E) ? a.T(e0 - 1) : 0u;
 #pragma unroll
-        for (int j = 0; j < kEvPer; ++j) {
+        for (int j = 0; j < kEP; ++j) {
             cM[j] = m;
             if (!ok[j]) continue;
             const int e = e0 + j;
@@ -360,7 +363,7 @@ __device__ void project_one(Arr a, int32_t d, int64_t lo, int64_t hi, const int3
         // the event arrays from the registers, after the last barrier (a
         // barrier waits for every store in flight)
 #pragma unroll
-        for (int j = 0; j < kEvPer; ++j) {
+        for (int j = 0; j < kEP; ++j) {
             if (!ok[j]) continue;
             const int e = e0 + j;
             pmx[e] = cM[j];
@@ -437,14 +440,20 @@ __device__ inline void project_decoder(int32_t d, int32_t D, int64_t lo, int64_t
         a.wsum = a.cnt + lds_cap;
         a.tau = a.wsum + lds_cap;
         a.pmx = a.tau + lds_cap;
-        project_one<true>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc, hdr_out);
+        if (hi - lo <= int64_t(kNT) * 4)
+            project_one<true, 4, 4>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc,
+                                    hdr_out);
+        else
+            project_one<true, kResPer, kEvPer>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak,
+                                               dev_err, sc, hdr_out);
     } else {
         HbmArrays a;
         a.rank = reinterpret_cast<uint32_t*>(V.slices + slice_off);
         a.pmx = reinterpret_cast<uint32_t*>(V.slices + slice_off + W / 2);
         a.thr = nullptr;
         a.cold = nullptr;
-        project_one<false>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err, sc, hdr_out);
+        project_one<false, kResPer, kEvPer>(a, d, lo, hi, p, g, U, u_max, W, L.P, V, slice_off, base_peak, dev_err,
+                                            sc, hdr_out);
     }
 }
 
