@@ -200,13 +200,18 @@ def window_calibration(b, cpu: bool, calls: int = 20):
            "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes},
            "note": "median of per-call HIP events over the five launches of one call"}
+    import oracle
+    o = oracle.Oracle()
+    idx = np.arange(0, m, max(1, m // 30000))
+    t0 = time.perf_counter()
+    _, U_ref = o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, WINDOW, b.alpha_ppm, ap[idx], seen[idx],
+                                  b.u_max)
+    dt = time.perf_counter() - t0
+    if not np.array_equal(U.cpu().numpy()[idx], U_ref):
+        raise SystemExit("window calibration differs from the oracle")
+    out["verified"] = True
+    out["verified_note"] = f"{idx.size} evenly spaced requests' bounds against the oracle"
     if cpu:
-        import oracle
-        o = oracle.Oracle()
-        idx = np.arange(0, m, max(1, m // 30000))
-        t0 = time.perf_counter()
-        o.calibrate_window(b.cal_pred, b.cal_truth, b.edges, WINDOW, b.alpha_ppm, ap[idx], seen[idx], b.u_max)
-        dt = time.perf_counter() - t0
         out["cpu_baseline"] = {"value": idx.size / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
                                "sample": f"{idx.size} evenly spaced requests of the same batch, single-threaded C "
                                          f"oracle (each request's window sorted), {dt:.2f} s"}
@@ -260,20 +265,27 @@ def static_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
            "reserve_feasible_fraction": feasible,
            "note": "independent: every arrival against the reported state; reserve: arrivals in order, each "
                    "reserving its B_need and joining the queue (a serial chain, one wavefront)"}
+    import oracle
+    o = oracle.Oracle()
+    Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
+    t0 = time.perf_counter()
+    state_ref = o.rsc_state(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, BLOCK)
+    t_rsc = time.perf_counter() - t0
+    be = state_ref[2]
+    k = min(A, 20000)
+    t0 = time.perf_counter()
+    o.place_static(be, b.queue_len, BLOCK, b.arr_prompt[:k], Ua[:k])
+    t_ind = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    res_ref = o.place_static(be, b.queue_len, BLOCK, b.arr_prompt, Ua, reserve=True)
+    t_res = time.perf_counter() - t0
+    # the last call made was the reserving one: its outputs, and the state, against the oracle
+    for got, want in zip(list(st) + list(outs), list(state_ref) + list(res_ref)):
+        if not np.array_equal(got.cpu().numpy().astype(np.int64), np.asarray(want).astype(np.int64)):
+            raise SystemExit("Algorithm 1 on block counts differs from the oracle")
+    out["verified"] = True
+    out["verified_note"] = "the runtime state and every arrival of the reserving chain against the oracle"
     if cpu:
-        import oracle
-        o = oracle.Oracle()
-        Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
-        t0 = time.perf_counter()
-        _, _, be = o.rsc_state(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, BLOCK)
-        t_rsc = time.perf_counter() - t0
-        k = min(A, 20000)
-        t0 = time.perf_counter()
-        o.place_static(be, b.queue_len, BLOCK, b.arr_prompt[:k], Ua[:k])
-        t_ind = time.perf_counter() - t0
-        t0 = time.perf_counter()
-        o.place_static(be, b.queue_len, BLOCK, b.arr_prompt, Ua, reserve=True)
-        t_res = time.perf_counter() - t0
         out["cpu_baseline"] = {"rsc_state_ms": t_rsc * 1e3, "independent_pairs_per_s": D * k / t_ind,
                                "reserve_arrivals_per_s": A / t_res, "cores": 1, "kind": "oracle",
                                "sample": f"runtime state of all {n} residents; {k} arrivals independent; all {A} "
@@ -331,15 +343,24 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
            "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
            "note": "peaks, capacities and overflow in blocks; the pair matrix always written; the block snapshot "
                    "is read through L2 (about 150 B per event at 16 tokens per block)"}
+    import oracle
+    o = oracle.Oracle()
+    k = min(A, 65536)
+    Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
+    t0 = time.perf_counter()
+    ref = o.place_blocks(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, b.queue_len, BLOCK, b.arr_prompt[:k],
+                         Ua[:k], want_pairs=True)
+    dt = time.perf_counter() - t0
+    checks = ((out.choice[:k], ref.choice), (out.chosen_peak[:k], ref.chosen_peak),
+              (out.chosen_overflow[:k], ref.chosen_overflow), (out.flags[:k], ref.flags),
+              (out.pair_peak[:, :k], ref.pair_peak), (state["base"], ref.base_peak))
+    for got, want in checks:
+        if not np.array_equal(got.cpu().numpy().astype(np.int64), want.astype(np.int64)):
+            raise SystemExit("placement in blocks differs from the oracle")
+    res["verified"] = True
+    res["verified_note"] = f"every output of the first {k} arrivals (their pair-matrix columns included) and the " \
+                           "base peaks against the oracle"
     if cpu:
-        import oracle
-        o = oracle.Oracle()
-        k = min(A, 65536)
-        Ur, Ua = U_res.cpu().numpy(), U_arr.cpu().numpy()
-        t0 = time.perf_counter()
-        o.place_blocks(b.seg_off, b.res_prompt, b.res_gen, Ur, b.capacity, b.queue_len, BLOCK, b.arr_prompt[:k],
-                       Ua[:k], want_pairs=True)
-        dt = time.perf_counter() - t0
         res["cpu_baseline"] = {"value": D * k / dt, "unit": "pair-evaluations/s", "cores": 1, "kind": "oracle",
                                "sample": f"every decoder against the first {k} arrivals (dense occupancy in blocks "
                                          f"per decoder, then each pair), single-threaded C oracle, {dt:.2f} s"}
@@ -425,7 +446,8 @@ def record_path(cpu: bool, calls: int = 20):
            "mean_events_per_decoder": float(np.mean(hdr[:, 4])),
            "walks": _walks(hdr, A, U_arr),
            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes,
+                        "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic("large_growing"),
+                        "algorithmic_bytes": nbytes,
                         "kernel": "maps_place (place_records, then place_finish)"}}
     import oracle
     o = oracle.Oracle()
