@@ -262,6 +262,7 @@ def static_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
     out = {"block_size": BLOCK, "decoders": D, "arrivals": A, "residents": n, "ms": ms,
            "independent_pairs_per_s": D * A / (ms["independent"] * 1e-3),
            "reserve_arrivals_per_s": A / (ms["reserve"] * 1e-3),
+           "reserve_bound": "latency: a serial chain, each arrival's choice waits on the state its predecessors left",
            "reserve_feasible_fraction": feasible,
            "note": "independent: every arrival against the reported state; reserve: arrivals in order, each "
                    "reserving its B_need and joining the queue (a serial chain, one wavefront)"}
@@ -340,6 +341,9 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
     res = {"block_size": BLOCK, "decoders": D, "arrivals": A, "ms": ms,
            "pairs_per_s": D * A / (ms["place_blocks"] * 1e-3),
            "snapshot_mb": snap.data.numel() / 1e6,
+           # the pair matrix written once, the block snapshot read once, 21 B per arrival in and out
+           "roofline": _hbm_roofline(4 * D * A + snap.data.numel() + 21 * A, ms["place_blocks"],
+                                     "maps_place_blocks (blocks_order, blocks_pairs, blocks_finish)"),
            "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
            "note": "peaks, capacities and overflow in blocks; the pair matrix always written; the block snapshot "
                    "is read through L2 (about 150 B per event at 16 tokens per block)"}
@@ -365,6 +369,12 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
                                "sample": f"every decoder against the first {k} arrivals (dense occupancy in blocks "
                                          f"per decoder, then each pair), single-threaded C oracle, {dt:.2f} s"}
     return res
+
+
+def _hbm_roofline(nbytes: int, ms: float, kernel: str) -> dict:
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes": nbytes, "kernel": kernel}
 
 
 def _median_ms(fn, calls: int, warm: int = 2) -> float:
@@ -501,6 +511,7 @@ def sequential_commit(b, db, snap, U_arr, ref, cpu: bool, k: int = 65536, check:
             sys.exit(3)
     res = {"decoders": D, "arrivals": k, "ms": ms, "arrivals_per_s": k / (ms * 1e-3),
            "workspace_mb": wsb.numel() / 1e6, "verified": True,
+           "bound": "latency: a serial chain, each arrival is evaluated against the curves its predecessors left",
            "verified_note": f"the first {check} arrivals' choices, peaks, overflows and flags against the oracle",
            "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
            "note": "arrivals in order; per arrival one peak lookup per decoder (dense curves plus Fenwick floors), "
@@ -570,6 +581,7 @@ def appa_simulation(cpu: bool, rhos: int = 64):
                 "mean_e2e_ms": float(lat.mean()), "p99_e2e_ms": float(np.percentile(lat, 99))}
     res = {"simulations": S, "requests": w.n, "decoders": appa.N_DECODERS, "capacity": appa.CAPACITY,
            "theta": appa.THETA_PPM / 1e6, "ms": ms, "simulations_per_s": S / (ms * 1e-3),
+           "bound": "latency: one wavefront per simulation, event after event",
            "simulated_requests_per_s": S * w.n / (ms * 1e-3), "verified": True,
            "verified_note": f"simulations {checked} (rho 0.96 and 1.05, both policies) against the oracle in full",
            "at": [summary(s) for s in checked],
@@ -626,7 +638,11 @@ def incremental_window(b, ref, cpu: bool, batches: int = 64, window: int = 500):
     m = apn.size
     res = {"log": n, "batches": batches, "batch_size": int(cuts[1] - cuts[0]), "buckets": st.nb, "window": window,
            "append_ms": append_ms, "appended_per_s": (cuts[1] - cuts[0]) / (append_ms * 1e-3),
-           "bounds_ms": bounds_ms, "requests": m, "bounds_per_s": m / (bounds_ms * 1e-3), "verified": True,
+           "bounds_ms": bounds_ms, "requests": m, "bounds_per_s": m / (bounds_ms * 1e-3),
+           # the bounds call: prediction in, bound out per request, every ring slot read once
+           "roofline": _hbm_roofline(8 * m + 4 * st.nb * window, bounds_ms,
+                                     "maps_window_bounds (win_select, win_bounds)"),
+           "verified": True,
            "verified_note": f"{idx.size} evenly spaced requests' bounds after the last batch against the oracle"}
     if cpu:
         res["cpu_baseline"] = {"value": idx.size / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
