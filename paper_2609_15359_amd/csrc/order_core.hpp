@@ -8,7 +8,8 @@
 //      bound, index) -- unique keys, so the order is the stable one;
 //   2. a second bitonic sort of (bound, index) gives the queue by bound, with
 //      the start of each run of equal bounds;
-//   (a queue of at most 64 requests is sorted in the lanes of one wavefront);
+//   (a queue of at most 64 requests is ordered by counting instead, each
+//   wavefront counting against 4 of its requests);
 //   3. admitted = the largest k whose prefix keeps the projected peak within
 //      the capacity, by binary search over k (the peak never decreases when a
 //      request is added).  For a prefix, residents plus admitted requests form
@@ -74,23 +75,6 @@ __device__ inline void bitonic_sort(uint64_t* keys, int n2) {
     }
 }
 
-// Ascending sort of one key per lane across a wavefront (bitonic network
-// through lane shuffles: no LDS, no barrier).
-__device__ inline uint64_t wave_bitonic(uint64_t key) {
-    const int lane = threadIdx.x % kWave;
-#pragma unroll
-    for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            const uint64_t other = __shfl_xor(key, j, kWave);
-            const bool ascending = (lane & k) == 0;
-            const bool lower = (lane & j) == 0;
-            key = (lower == ascending) ? (key < other ? key : other) : (key > other ? key : other);
-        }
-    }
-    return key;
-}
-
 // Largest projected peak of the residents plus the first k requests of the new order.
 __device__ inline int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* rank, const int2* cold, int32_t E,
                                int32_t W) {
@@ -140,8 +124,8 @@ __device__ inline int64_t prefix_peak(LocalLds& s, int n, int k, const uint2* ra
 }
 
 // Decoder d's queue bounds and capacity, and, when the queue holds at most
-// one wavefront of requests, request i's prompt, bound and wait in thread i
-// (0 elsewhere).  Called early by a launch that has other work first, so
+// one wavefront of requests, request i's prompt, bound and wait in lane i of
+// every wavefront (0 elsewhere).  Called early by a launch that has other work first, so
 // that these loads are in flight during it.
 struct QueueFetch {
     int64_t qlo, qhi;
@@ -156,7 +140,7 @@ __device__ inline QueueFetch fetch_queue(const LocalArgs& g, int32_t d) {
     f.pr = 0;
     f.u = 0;
     f.wait = 0;
-    const int64_t i = f.qlo + int64_t(threadIdx.x);
+    const int64_t i = f.qlo + int64_t(threadIdx.x % kWave);   // every wavefront holds the short queue
     if (0 <= f.qlo && f.qlo <= f.qhi && f.qhi <= g.total && f.qhi - f.qlo <= kWave && i < f.qhi) {
         f.pr = g.qp[i];
         f.u = g.qU[i];
@@ -207,38 +191,55 @@ __device__ inline void order_queue(const LocalArgs& g, int32_t d, int64_t built_
     while (n2 < n) n2 <<= 1;
 
     if (n2 <= kWave) {
-        // a queue of at most one wavefront: both sorts and the runs of equal
-        // bounds in the lanes of wave 0 (key i in lane i)
-        if (threadIdx.x < kWave) {
-            const int i = threadIdx.x;
-            uint64_t key = ~0ull, key2 = ~0ull;
-            bool neg = false;
-            if (i < n) {
-                const int32_t pr = f.pr, u = f.u;   // fetch_queue's: the queue fits one wavefront
-                neg = pr < 0;
-                s.pp[i] = pr < 0 ? 0 : pr;
-                const int32_t ue = u < 0 ? L.u_max : u;
-                s.ue[i] = ue;
-                const bool promoted = g.qwait != nullptr && f.wait >= g.max_wait;
-                const uint64_t cls = promoted ? 0ull : (1ull << 63);
-                const uint64_t val = promoted ? uint64_t(i) : uint64_t(ue);
-                key = cls | (val << 32) | uint64_t(uint32_t(i));
-                key2 = (uint64_t(uint32_t(ue)) << 32) | uint64_t(uint32_t(i));
+        // A queue of at most one wavefront: request i in lane i of every
+        // wavefront.  Both orders by counting: the new position of i is the
+        // number of requests before it by (class and key, index), its place
+        // by bound the number before it by (bound, index), and the start of
+        // its run of equal bounds the number with a smaller bound.  Wavefront
+        // w counts against requests [4w, 4w + 4); wave 0 adds the counts.
+        constexpr int kWaves = kOrderNT / kWave;
+        constexpr int kPer = kWave / kWaves;   // requests each wavefront counts against
+        const int i = int(threadIdx.x % kWave), w = int(threadIdx.x / kWave);
+        bool neg = false;
+        uint32_t h = ~0u, ue = ~0u;   // past the queue: after every request
+        if (i < n) {
+            neg = f.pr < 0;
+            ue = uint32_t(f.u < 0 ? L.u_max : f.u);
+            const bool promoted = g.qwait != nullptr && f.wait >= g.max_wait;
+            h = promoted ? uint32_t(i) : (0x80000000u | ue);   // class bit, then index or bound
+            if (w == 0) {
+                s.pp[i] = f.pr < 0 ? 0 : f.pr;
+                s.ue[i] = int32_t(ue);
             }
-            if (neg) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
-            key = wave_bitonic(key);
-            key2 = wave_bitonic(key2);
-            if (i < n) {
-                const int idx = int(uint32_t(key));
-                g.order[qlo + i] = idx;
-                s.pos[idx] = i;
-                s.uidx[i] = int(uint32_t(key2));
+        }
+        if (neg && w == 0) raise_error(g.dev_err, MAPS_ERR_NEG_LEN);
+        uint32_t r1 = 0, r2 = 0, r3 = 0;
+#pragma unroll
+        for (int jj = 0; jj < kPer; ++jj) {
+            const int j = w * kPer + jj;
+            if (j >= n) break;   // uniform
+            const uint32_t hj = __builtin_amdgcn_readlane(h, j), uj = __builtin_amdgcn_readlane(ue, j);
+            r1 += (hj < h) | ((hj == h) & (j < i));
+            r2 += (uj < ue) | ((uj == ue) & (j < i));
+            r3 += uj < ue;
+        }
+        uint32_t* part = reinterpret_cast<uint32_t*>(s.keys);   // [3][kWaves][kWave], free until step 3
+        part[(0 * kWaves + w) * kWave + i] = r1;
+        part[(1 * kWaves + w) * kWave + i] = r2;
+        part[(2 * kWaves + w) * kWave + i] = r3;
+        __syncthreads();
+        if (w == 0 && i < n) {
+            uint32_t a1 = 0, a2 = 0, a3 = 0;
+#pragma unroll
+            for (int v = 0; v < kWaves; ++v) {
+                a1 += part[(0 * kWaves + v) * kWave + i];
+                a2 += part[(1 * kWaves + v) * kWave + i];
+                a3 += part[(2 * kWaves + v) * kWave + i];
             }
-            const uint32_t b = uint32_t(key2 >> 32);
-            const uint32_t prev = __shfl_up(b, 1, kWave);
-            const int32_t start = (i == 0 || prev != b) ? i : 0;
-            const int32_t run = wave_incl_scan_max(start);
-            if (i < n) s.grp[i] = run;
+            g.order[qlo + a1] = i;
+            s.pos[i] = int32_t(a1);
+            s.uidx[a2] = i;
+            s.grp[a2] = int32_t(a3);
         }
         __syncthreads();
     } else {
