@@ -419,23 +419,32 @@ __global__ __launch_bounds__(kPairsNT) void blocks_order(PairArgs a) {
 }
 
 // Every pair's peak in blocks; the tile's arrivals taken in bound order, the
-// row of the matrix written back in arrival order from LDS
-__global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a) {
+// row of the matrix written back in arrival order from LDS.  One workgroup
+// per (decoder, tile), numbered so that the workgroups of one decoder are
+// consecutive among those of one XCD (workgroup b runs on XCD b mod 8): XCD x
+// takes decoders x, x + 8, ... one after another, every tile of a decoder
+// while its slice is in that XCD's L2, instead of each of the 8 L2s fetching
+// every slice.
+constexpr int kXcds = 8;
+__global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t tiles) {
     __shared__ int32_t row[kTile];
     const BlkLayout& L = a.L;
-    const int d = blockIdx.y;
+    const int64_t k = int64_t(blockIdx.x) / kXcds;   // the k-th workgroup of its XCD
+    const int d = int(blockIdx.x % kXcds) + kXcds * int(k / tiles);
+    const int64_t tile = k % tiles;
+    if (d >= L.D) return;   // the last round of decoders when D is not a multiple of 8
     if (!blk_snapshot_ok(reinterpret_cast<const BlkSnapHeader*>(a.snap), L)) {
-        if (blockIdx.x == 0 && d == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
+        if (tile == 0 && d == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
         return;
     }
     const BlkHeader h = blk_headers(const_cast<char*>(a.snap))[d];
     const int64_t S = L.S;
-    const int64_t base = int64_t(blockIdx.x) * kTile;
+    const int64_t base = tile * kTile;
     const int64_t left = a.A - base;
     const int n = left < kTile ? int(left) : kTile;
     const int64_t cap = a.seg_off[d + 1] - a.seg_off[d] + 1;
     if (h.slice < 0 || h.cap != cap) {
-        if (h.slice >= 0 && blockIdx.x == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
+        if (h.slice >= 0 && tile == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
         for (int k = 0; k < kPairsPer; ++k) {
             const int t = threadIdx.x + k * kPairsNT;
             if (t < n) a.pair[int64_t(d) * a.A + base + t] = -1;
@@ -627,7 +636,8 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
     const int64_t tiles = (A + kTile - 1) / kTile;
     hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kPairsNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();
-    hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(tiles), unsigned(D)), dim3(kPairsNT), 0, stream, pa);
+    const int64_t rounds = (int64_t(D) + kXcds - 1) / kXcds;   // decoders per XCD
+    hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(rounds * kXcds * tiles)), dim3(kPairsNT), 0, stream, pa, tiles);
     MAPS_CHECK_LAUNCH();
     FinArgs fa{dev_err, D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
                chosen_overflow, flags};
