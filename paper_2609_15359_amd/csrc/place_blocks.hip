@@ -215,7 +215,136 @@ struct ProjArgs {
     char* snap;
     int32_t* base_peak;
     uint32_t* dev_err;
+    int64_t lds_cap;   // event records that fit the LDS arrays past the bitmap (0: every decoder in HBM)
 };
+
+// The per-event arrays of one decoder in LDS (past the W bitmap words and the
+// W rank counts), every count of a record summed with LDS atomics, the scans
+// done in LDS, and the slice written to HBM once at the end.
+struct LdsRecs {
+    uint32_t* tau;
+    uint32_t* N;
+    unsigned long long* SX;
+    int32_t* OB;
+    uint32_t* G;   // [cap][Gw]: class c (c = 0..S-2, for xi = c + 1) in half (c & 1) of word c / 2
+    int64_t Gw;
+    __device__ uint32_t g(int64_t e, int c) const { return (G[e * Gw + c / 2] >> (16 * (c & 1))) & 0xFFFFu; }
+    __device__ void set_g(int64_t e, int c, uint32_t v) const {
+        uint32_t& w = G[e * Gw + c / 2];
+        const int sh = 16 * (c & 1);
+        w = (w & ~(0xFFFFu << sh)) | (v << sh);
+    }
+};
+
+__device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int64_t lo, int64_t hi, uint32_t E, const uint32_t* bits,
+                                   const uint32_t* wpre, const BlkSlice& s, int64_t off, int64_t cap, int64_t* red64,
+                                   uint32_t* red32, int32_t* redg) {
+    const BlkLayout& L = a.L;
+    const int tid = threadIdx.x;
+    const int64_t S = L.S;
+    const int64_t len = int64_t(E) + 1;   // the events and the record past the last one
+    LdsRecs r;
+    uint32_t* base = const_cast<uint32_t*>(wpre) + L.W;
+    r.Gw = S / 2;   // ceil((S - 1) / 2) halves
+    r.tau = base;
+    r.N = r.tau + len;
+    r.SX = reinterpret_cast<unsigned long long*>(r.N + len);   // 8-byte aligned: 8 W + 8 len bytes in
+    r.OB = reinterpret_cast<int32_t*>(r.SX + len);
+    r.G = reinterpret_cast<uint32_t*>(r.OB + len);
+    // 3'. event times; counters zeroed
+    for (int64_t e = tid; e < len; e += kPbNT) {
+        r.tau[e] = 0;
+        r.N[e] = 0;
+        r.SX[e] = 0;
+        for (int64_t c = 0; c < r.Gw; ++c) r.G[e * r.Gw + c] = 0;
+    }
+    __syncthreads();
+    for (int w = tid; w < L.W; w += kPbNT) {
+        uint32_t b = bits[w], e = wpre[w];
+        while (b) {
+            r.tau[e++] = uint32_t(w * 32 + (__ffs(b) - 1));
+            b &= b - 1u;
+        }
+    }
+    // each resident adds itself to its event: 1, X = x div S, and its class xi = x mod S
+    for (int64_t i = lo + tid; i < hi; i += kPbNT) {
+        int32_t pr = a.p[i], gr = a.g[i], ur = a.U[i];
+        pr = pr < 0 ? 0 : pr;
+        gr = gr < 0 ? 0 : gr;
+        ur = ur < 0 ? 0 : ur;
+        int64_t R = int64_t(ur) - gr;
+        R = R > 0 ? R : 0;
+        R = R > L.u_max ? L.u_max : R;
+        const uint32_t e = wpre[R >> 5] + __popc(bits[R >> 5] & ((1u << (R & 31)) - 1u));
+        const int64_t x = int64_t(pr) + gr;
+        atomicAdd(&r.N[e], 1u);
+        atomicAdd(&r.SX[e], (unsigned long long)(x / S));
+        const int xi = int(x % S);
+        if (xi >= 1) atomicAdd(&r.G[e * r.Gw + (xi - 1) / 2], ((xi - 1) & 1) ? 0x10000u : 1u);
+    }
+    __syncthreads();
+    // 4'. suffix sums over the events (record E is zero): SX, then N and every class count
+    block_scan<kPbNT, false, true, false, int64_t>(
+        len, int64_t(0), [&](int64_t e) { return int64_t(r.SX[e]); },
+        [&](int64_t e, int64_t v) { r.SX[e] = (unsigned long long)v; }, red64);
+    for (int q0 = 0; q0 < S; q0 += kGroup)
+        group_scan<kPbNT, false, true, false, int32_t>(
+            len, int(S - q0 < kGroup ? S - q0 : kGroup), 0,
+            [&](int64_t e, int q) { return q0 + q == 0 ? int32_t(r.N[e]) : int32_t(r.g(e, q0 + q - 1)); },
+            [&](int64_t e, int q, int32_t v) {
+                if (q0 + q == 0) r.N[e] = uint32_t(v);
+                else r.set_g(e, q0 + q - 1, uint32_t(v));
+            },
+            redg);   // ends with a barrier
+    // counts by class -> counts of classes >= c, and the occupancy at every event
+    bool big = false;
+    for (int64_t e = tid; e < len; e += kPbNT) {
+        uint32_t acc = 0;
+        for (int c = int(S) - 2; c >= 0; --c) {
+            acc += r.g(e, c);
+            r.set_g(e, c, acc);
+        }
+        int64_t ob = 0;
+        if (e < int64_t(E)) {
+            // occupancy_at with the class counts read from the halves
+            const int64_t t = r.tau[e], V = t / S, u = t % S, N = r.N[e];
+            ob = int64_t(r.SX[e]) + N * V + N;
+            if (u == 0) ob -= N - (S > 1 ? int64_t(r.g(e, 0)) : 0);
+            if (u >= 2) ob += r.g(e, int(S - u));   // #{xi >= S + 1 - u}: class S - u
+        }
+        big |= ob + 2 * int64_t(L.u_max) / S + 2 > int64_t(INT32_MAX) / 2;
+        r.OB[e] = int32_t(ob > INT32_MAX ? INT32_MAX : ob);
+    }
+    if (big) raise_error(a.dev_err, MAPS_ERR_INT32_RANGE);
+    __syncthreads();
+    // 6'. prefix maxima per residue class (exclusive: events below) into the
+    // slice, the suffix maximum, then the slice's event arrays
+    for (int r0 = 0; r0 < S; r0 += kGroup)
+        group_scan<kPbNT, true, false, true, int32_t>(
+            len, int(S - r0 < kGroup ? S - r0 : kGroup), 0,
+            [&](int64_t e, int q) {
+                return e < int64_t(E) ? int32_t(r.OB[e] + ceil_plus(r0 + q, r.tau[e], S)) : 0;
+            },
+            [&](int64_t e, int q, int32_t v) { s.PMX[e * S + r0 + q] = v; }, redg);
+    const int32_t base_pk = block_scan<kPbNT, true, true, false, int32_t>(
+        len, 0, [&](int64_t e) { return r.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
+        reinterpret_cast<int32_t*>(red32));
+    for (int64_t e = tid; e < len; e += kPbNT) {
+        s.tau[e] = e < int64_t(E) ? int32_t(r.tau[e]) : 0;
+        s.N[e] = int32_t(r.N[e]);
+        s.SX[e] = int64_t(r.SX[e]);
+        s.OB[e] = r.OB[e];
+        for (int c = 0; c + 1 < S; ++c) s.G[e * (S - 1) + c] = int32_t(r.g(e, c));
+    }
+    if (tid == 0) {
+        BlkHeader* hdr = blk_headers(a.snap);
+        hdr[d].slice = off;
+        hdr[d].cap = cap;
+        hdr[d].E = int32_t(E);
+        hdr[d].base = base_pk;
+        a.base_peak[d] = base_pk;
+    }
+}
 
 __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     extern __shared__ uint32_t bits[];               // W bit words, then W counts of events before each
@@ -282,6 +411,10 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
             s.rank[w] = make_uint2(bits[w], v);
         },
         red32);
+    if (int64_t(E) + 1 <= a.lds_cap && n < 65536) {   // the same in every thread
+        project_blocks_lds(a, d, lo, hi, E, bits, wpre, s, off, cap, red64, red32, redg);
+        return;
+    }
     for (int w = tid; w < L.W; w += kPbNT) {
         uint32_t b = bits[w], e = wpre[w];
         while (b) {
@@ -606,8 +739,13 @@ extern "C" maps_status maps_project_blocks(int32_t D, const int64_t* seg_off, co
         return MAPS_E_NULL;
     const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
     if (snapshot_bytes < L.bytes) return MAPS_E_BUFFER;
-    ProjArgs a{L, seg_off, prompt, generated, upper, static_cast<char*>(snapshot), base_peak, dev_err};
-    const size_t lds = size_t(L.W) * 8;
+    // the bitmap and its rank counts, then as many LDS event records as fit 152 KB
+    const size_t fixed = size_t(L.W) * 8;
+    const size_t per_rec = size_t(4 + 4 + 8 + 4) + size_t(block_size / 2) * 4;
+    constexpr size_t kBudget = 152 * 1024;
+    int64_t lds_cap = fixed + 64 < kBudget ? int64_t((kBudget - fixed - 64) / per_rec) : 0;
+    ProjArgs a{L, seg_off, prompt, generated, upper, static_cast<char*>(snapshot), base_peak, dev_err, lds_cap};
+    const size_t lds = fixed + (lds_cap > 0 ? size_t(lds_cap) * per_rec + 64 : 0);
     allow_dynamic_lds(project_blocks, lds);
     hipLaunchKernelGGL(project_blocks, dim3(unsigned(D)), dim3(kPbNT), lds, stream, a);
     MAPS_CHECK_LAUNCH();

@@ -58,6 +58,10 @@ def test_hand_worked_example(orc):
 CASES = [  # (D, max residents, A, u_max, S)
     (1, 40, 700, 50, 1), (3, 200, 1025, 4096, 16), (5, 300, 3000, 4096, 2), (17, 120, 5000, 20000, 37),
     (9, 64, 4097, 300, 64), (4, 0, 100, 100, 16),
+    # decoders with more distinct remaining lengths than the projection's LDS records hold (about
+    # 1,000 at S = 64, 2,700 at S = 16 with u_max 60,000), or with 65,536 residents or more: their
+    # arrays stay in HBM, beside decoders that fit
+    (3, 4000, 2000, 30000, 64), (4, 10000, 1200, 60000, 16), (1, 200000, 300, 1000, 16),
 ]
 
 
