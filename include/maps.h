@@ -339,10 +339,10 @@ maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max,
  * chosen_overflow (int64, max(0, peak - capacity)), flags (bit0 feasible,
  * bit1 round robin); queue_out [D] (nullable): queue lengths after the batch.
  * With A = 1 the outputs equal maps_place's.
- * workspace: maps_place_commit_workspace_size(D, u_max) bytes (four dense
- * int64 arrays over the step axis per decoder: 32 (u_max + 1) bytes per
- * decoder), caller-owned, not shared by calls in flight.  The chain is serial:
- * one workgroup takes the arrivals in order.
+ * workspace: maps_place_commit_workspace_size(D, u_max) bytes (three dense
+ * int64 arrays over the step axis and one int64 per 1,024 steps per decoder:
+ * about 24 (u_max + 1) bytes per decoder), caller-owned, not shared by calls
+ * in flight.  The chain is serial: one workgroup takes the arrivals in order.
  * dev_err bits: NEG_LEN (a_prompt of an arrival with a bound, capacity or
  * queue_len < 0), BOUND_RANGE (a_upper > u_max: evaluated at u_max),
  * SNAPSHOT.

@@ -1,5 +1,6 @@
-// Host-side caches shared by the entry points: kernel LDS attributes and the
-// compute-unit count of each device, each looked up once per process.
+// Host-side caches shared by the entry points: kernel LDS attributes, each
+// kernel's static LDS and the compute-unit count of each device, each looked
+// up once per process.
 #include <mutex>
 #include <unordered_map>
 
@@ -29,6 +30,20 @@ int device_compute_units() {
     int v = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
     cus[dev] = v;
+    return v;
+}
+
+size_t kernel_static_lds(const void* fn) {
+    static std::mutex mu;
+    static std::unordered_map<const void*, size_t> sizes;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = sizes.find(fn);
+    if (it != sizes.end()) return it->second;
+    hipFuncAttributes fa{};
+    // unknown: assume the whole workgroup's LDS is taken, so that no dynamic LDS is planned
+    const size_t v = hipFuncGetAttributes(&fa, fn) == hipSuccess ? fa.sharedSizeBytes : kLdsPerWorkgroup;
+    (void)hipGetLastError();
+    sizes[fn] = v;
     return v;
 }
 

@@ -351,6 +351,16 @@ inline void allow_dynamic_lds(Kernel* fn, size_t bytes) {
 // Host: compute units of the current device, queried once per device.
 int device_compute_units();
 
+// LDS of one workgroup on gfx950, static and dynamic together.
+constexpr size_t kLdsPerWorkgroup = 160 * 1024;
+
+// Host: a kernel's static LDS in bytes, queried once per kernel.
+size_t kernel_static_lds(const void* fn);
+template <typename Kernel>
+inline size_t kernel_static_lds(Kernel* fn) {
+    return kernel_static_lds(reinterpret_cast<const void*>(fn));
+}
+
 }  // namespace maps
 
 // Host-side launch check: returns MAPS_E_HIP from the enclosing function when

@@ -57,7 +57,11 @@ def _random_case(rng, D, nmax, A, u_max):
 
 
 @pytest.mark.parametrize("D,nmax,A,u_max", [(1, 5, 40, 50), (3, 30, 300, 2000), (17, 200, 700, 9000),
-                                            (64, 40, 2100, 1023), (300, 8, 900, 70)])
+                                            (64, 40, 2100, 1023), (300, 8, 900, 70),
+                                            # ranges longer than the chain's LDS stage, many floor blocks
+                                            (4, 60, 500, 40000),
+                                            # more decoders than threads: no lookups ahead
+                                            (1100, 3, 250, 2500)])
 def test_random(orc, D, nmax, A, u_max):
     rng = np.random.default_rng(D * 1000 + A)
     seg, p, g, U, a_p, a_U = _random_case(rng, D, nmax, A, u_max)
