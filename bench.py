@@ -514,7 +514,7 @@ def sequential_commit(b, db, snap, U_arr, ref, cpu: bool, k: int = 65536, check:
            "bound": "latency: a serial chain, each arrival is evaluated against the curves its predecessors left",
            "verified_note": f"the first {check} arrivals' choices, peaks, overflows and flags against the oracle",
            "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
-           "note": "arrivals in order; per arrival one peak lookup per decoder (dense curves plus Fenwick floors), "
+           "note": "arrivals in order; per arrival one peak lookup per decoder (dense curves plus block floors), "
                    "a workgroup argmin, then the commit on [0, U] of the chosen decoder: a serial chain"}
     if cpu:
         res["cpu_baseline"] = {"value": check / dt, "unit": "arrivals/s", "cores": 1, "kind": "oracle",
