@@ -794,15 +794,34 @@ __global__ __launch_bounds__(kNT) void place_prof(PlaceArgs g) {
 // the peak back; a feasible MQ choice evaluates its pair once more from the
 // snapshot's records.
 // ---------------------------------------------------------------------------
-// The final selection for arrivals first, first + stride, ...
-__device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_t stride) {
+// The final selection for arrivals first, first + stride, ...  `scap`
+// (nullable): LDS for the D capacities, staged by the workgroup while its
+// first arrival's keys are on their way; every thread of the workgroup calls
+// this with the same stride.
+__device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_t stride, int32_t* scap) {
     const SnapLayout& L = g.L;
     const SnapView V = snap_view(const_cast<void*>(g.snap), L);
-    if (!snapshot_ok(V.hdr, L)) return;
-    const int64_t n_total = load_uniform(&V.hdr->n_total);
     const int32_t ucl_max = 32 * L.W - 1;
+    // the first arrival's bound and keys go out before anything that waits
+    int32_t U = first < g.A ? g.aU[first] : -1;
+    int32_t keys[kMaxGroups];
+#pragma unroll
+    for (int gi = 0; gi < kMaxGroups; ++gi)
+        keys[gi] = first < g.A && gi < g.G ? g.pkey[int64_t(gi) * g.A + first] : INT32_MAX;
+    if (!snapshot_ok(V.hdr, L)) return;   // uniform
+    const int64_t n_total = load_uniform(&V.hdr->n_total);
+    const int32_t* cap = g.cap;
+    if (scap != nullptr) {
+        for (int32_t d = threadIdx.x; d < L.D; d += blockDim.x) scap[d] = g.cap[d];
+        __syncthreads();
+        cap = scap;
+    }
     for (int64_t a = first; a < g.A; a += stride) {
-        const int32_t U = g.aU[a];
+        if (a != first) {
+            U = g.aU[a];
+#pragma unroll
+            for (int gi = 0; gi < kMaxGroups; ++gi) keys[gi] = gi < g.G ? g.pkey[int64_t(gi) * g.A + a] : INT32_MAX;
+        }
         if (U < 0) {
             g.choice[a] = int32_t((g.rr_offset + a) % L.D);
             g.chosen_peak[a] = -1;
@@ -810,16 +829,13 @@ __device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_
             g.flags[a] = 2;
             continue;
         }
-        int32_t keys[kMaxGroups];
-#pragma unroll
-        for (int gi = 0; gi < kMaxGroups; ++gi) keys[gi] = gi < g.G ? g.pkey[int64_t(gi) * g.A + a] : INT32_MAX;
         int32_t key = keys[0], best = 0;
 #pragma unroll
         for (int gi = 1; gi < kMaxGroups; ++gi)
             if (keys[gi] < key) { key = keys[gi]; best = gi; }
         int32_t d = g.pdec[int64_t(best) * g.A + a];
         d = d < 0 || d >= L.D ? 0 : d;
-        const int32_t C = g.cap[d];
+        const int32_t C = cap[d];
         int32_t peak = 0;
         if (g.policy == MAPS_POLICY_MC) {
             peak = int32_t(key_peak<MAPS_POLICY_MC>(key, C));
@@ -843,8 +859,13 @@ __device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_
     }
 }
 
+// Capacities staged in LDS for up to kFinishLdsDecoders decoders.
+constexpr int32_t kFinishLdsDecoders = 16384;
+
 __global__ __launch_bounds__(256) void place_finish(PlaceArgs g) {
-    finish_arrivals(g, int64_t(blockIdx.x) * blockDim.x + threadIdx.x, int64_t(gridDim.x) * blockDim.x);
+    extern __shared__ int32_t scap[];
+    finish_arrivals(g, int64_t(blockIdx.x) * blockDim.x + threadIdx.x, int64_t(gridDim.x) * blockDim.x,
+                    g.L.D <= kFinishLdsDecoders ? scap : nullptr);
 }
 
 // The end of placement and every decoder's local order in one launch:
@@ -859,7 +880,7 @@ __global__ __launch_bounds__(order::kOrderNT) void place_finish_order(PlaceArgs 
         order::order_queue(o, int32_t(blockIdx.x));
     else
         finish_arrivals(g, int64_t(int32_t(blockIdx.x) - D) * order::kOrderNT + threadIdx.x,
-                        int64_t(fin_blocks) * order::kOrderNT);
+                        int64_t(fin_blocks) * order::kOrderNT, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -1023,7 +1044,9 @@ extern "C" maps_status maps_place(const void* snapshot, int32_t D, int32_t u_max
                                                  &launched);
     if (st != MAPS_OK || !launched) return st;
     const int64_t blocks = (A + 255) / 256;
-    hipLaunchKernelGGL(place_finish, dim3(unsigned(blocks < 4096 ? blocks : 4096)), dim3(256), 0, stream, a);
+    const size_t lds = D <= kFinishLdsDecoders ? size_t(D) * sizeof(int32_t) : 0;
+    allow_dynamic_lds(place_finish, lds);
+    hipLaunchKernelGGL(place_finish, dim3(unsigned(blocks < 4096 ? blocks : 4096)), dim3(256), lds, stream, a);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

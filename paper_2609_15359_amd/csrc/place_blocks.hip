@@ -236,9 +236,12 @@ struct LdsRecs {
     }
 };
 
-__device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int64_t lo, int64_t hi, uint32_t E, const uint32_t* bits,
-                                   const uint32_t* wpre, const BlkSlice& s, int64_t off, int64_t cap, int64_t* red64,
-                                   uint32_t* red32, int32_t* redg) {
+// The 16-bit class counts hold because a decoder on this path has fewer than
+// 65,536 residents: no count, sum of counts or suffix sum reaches 2^16.
+__device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int64_t lo, int64_t hi, uint32_t E,
+                                                   const uint32_t* bits, const uint32_t* wpre, const BlkSlice& s,
+                                                   int64_t off, int64_t cap, int64_t* red64, uint32_t* red32,
+                                                   int32_t* redg) {
     const BlkLayout& L = a.L;
     const int tid = threadIdx.x;
     const int64_t S = L.S;

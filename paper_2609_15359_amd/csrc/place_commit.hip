@@ -65,7 +65,8 @@ CommitLayout commit_layout(int32_t D, int32_t u_max) {
     return c;
 }
 // the blocks after a commit's own: at most NB - 1
-static_assert((MAPS_MAX_COMMIT_U_MAX + kFloorBlock) / kFloorBlock - 1 <= kFloorPer * kSerialNT, "block floors per thread");
+static_assert((MAPS_MAX_COMMIT_U_MAX + kFloorBlock) / kFloorBlock - 1 <= kFloorPer * kSerialNT,
+              "block floors per thread");
 static_assert(kTailPer * kSerialNT >= kFloorBlock - 1, "steps of a block above a commit per thread");
 
 struct CommitArgs {
@@ -229,7 +230,8 @@ __device__ inline int64_t commit_key(const PeakIn& in, int64_t p, int32_t C, int
 __device__ inline void block_argmin(int64_t& key, int32_t& d, int64_t* skey, int32_t* sd) {
     const int64_t wk = wave_last(wave_incl_scan(key, INT64_MAX, [](int64_t x, int64_t y) { return x < y ? x : y; }));
     const int32_t wd =
-        wave_last(wave_incl_scan(key == wk ? d : INT32_MAX, INT32_MAX, [](int32_t x, int32_t y) { return x < y ? x : y; }));
+        wave_last(wave_incl_scan(key == wk ? d : INT32_MAX, INT32_MAX,
+                                 [](int32_t x, int32_t y) { return x < y ? x : y; }));
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
     if (lane == 0) { skey[wid] = wk; sd[wid] = wd; }
     lds_barrier();
@@ -488,7 +490,8 @@ __global__ __launch_bounds__(kSerialNT) void commit_serial(CommitArgs a) {
         int32_t un = -1;
         if constexpr (kPre) {
             const int64_t j = i + 1;
-            const int32_t Un = j < a.A ? __builtin_amdgcn_readfirstlane(tile_U[(j / kSerialNT) & 1][j % kSerialNT]) : -1;
+            const int32_t Un =
+                j < a.A ? __builtin_amdgcn_readfirstlane(tile_U[(j / kSerialNT) & 1][j % kSerialNT]) : -1;
             if (Un >= 0) un = Un < T ? Un : T;
         }
         const int32_t pre_d = kPre && tid < D ? tid : -1;
