@@ -718,8 +718,8 @@ def main():
     if legs - set(LEGS):
         ap.error(f"unknown legs: {sorted(legs - set(LEGS))}")
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (--gpus {args.gpus} requested); "
-              "the multi-GPU split is described in DESIGN.md", file=sys.stderr)
+        print(f"bench.py: one GPU only (--gpus {args.gpus} requested); placement would shard by arrivals, "
+              "each GPU holding a replica of the snapshot, but no multi-GPU path is built", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
