@@ -50,13 +50,14 @@ struct PlaceArgs {
     uint8_t* flags;
     int32_t* pair;
     int32_t* pkey;     // [G][A] best key of each group
-    int32_t* pdec;     // [G][A] best decoder of each group
+    int32_t* pdec;     // [G][A] best decoder of each group (16-bit entries when dec16)
     int32_t G;
     int32_t policy;
     int32_t Dg;        // decoders per group
     int32_t buf_units; // record path: 16-byte units per LDS buffer (0: slices stay in HBM)
     int32_t nb;        // profile path: profiles per LDS batch
     uint32_t* dev_err;
+    bool dec16;        // D <= 65,536: the groups' decoders are written as 16-bit indices
 };
 
 template <bool B>
@@ -250,8 +251,10 @@ __device__ __forceinline__ void write_partials(const PlaceArgs& g, int32_t grp, 
         const int64_t a = a0 + int64_t(k) * kNT + threadIdx.x;
         if (!kFull && a >= g.A) continue;
         const int64_t o = int64_t(grp) * g.A + a;
+        const int32_t d = dec[k] < g.L.D ? dec[k] : 0;
         g.pkey[o] = key[k];
-        g.pdec[o] = dec[k] < g.L.D ? dec[k] : 0;
+        if (g.dec16) reinterpret_cast<uint16_t*>(g.pdec)[o] = uint16_t(d);
+        else g.pdec[o] = d;
     }
 }
 
@@ -833,7 +836,8 @@ __device__ inline void finish_arrivals(const PlaceArgs& g, int64_t first, int64_
 #pragma unroll
         for (int gi = 1; gi < kMaxGroups; ++gi)
             if (keys[gi] < key) { key = keys[gi]; best = gi; }
-        int32_t d = g.pdec[int64_t(best) * g.A + a];
+        const int64_t od = int64_t(best) * g.A + a;
+        int32_t d = g.dec16 ? int32_t(reinterpret_cast<const uint16_t*>(g.pdec)[od]) : g.pdec[od];
         d = d < 0 || d >= L.D ? 0 : d;
         const int32_t C = cap[d];
         int32_t peak = 0;
@@ -994,6 +998,7 @@ maps_status place_records_enqueue(const void* snapshot, int32_t D, int32_t u_max
     a.pair = pair_peak;
     a.pkey = w.key;
     a.pdec = w.dec;
+    a.dec16 = D <= 65536;
     a.G = G;
     a.policy = policy;
     a.Dg = (D + G - 1) / G;
