@@ -210,37 +210,41 @@ __global__ void static_need(StaticArgs a) {
     if (bad) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
 }
 
-// Largest-B_eff key of one lane's decoders: (B_eff + 2^52) above (1023 - decoder)
-template <int kSlots>
-__device__ inline uint64_t lane_best_b(const int64_t (&B)[kSlots], int lane, int32_t D) {
-    uint64_t kb = 0;
-#pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-        const int32_t d = lane + s * kWave;
-        const uint64_t k = (uint64_t(B[s] + kBlockLimit) << 10) | uint64_t(1023 - d);
-        if (d < D && k > kb) kb = k;
-    }
-    return kb;
+// Largest-B_eff key of one decoder: (B_eff + 2^52) above (1023 - decoder);
+// 0 (below every key) for a slot past the last decoder.
+__device__ inline uint64_t best_b_key(int64_t B, int32_t d, int32_t D) {
+    return d < D ? (uint64_t(B + kBlockLimit) << 10) | uint64_t(1023 - d) : 0;
 }
 
-// kSlots decoders per lane: decoder lane + 64 s in slot s.  The largest B_eff
-// over all decoders is kept between arrivals (only the chosen decoder's
-// changes): an arrival whose B_need exceeds it takes that decoder at once;
-// only a feasible shortest-queue choice scans every decoder.
+// kSlots decoders per lane: decoder lane + 64 s in slot s, with its B_eff,
+// queue length and largest-B_eff key in registers.  The largest key over all
+// decoders is kept between arrivals (only the chosen decoder's changes): an
+// arrival whose B_need exceeds it takes that decoder at once; only a
+// feasible shortest-queue choice scans every decoder.  The chosen decoder's
+// lane and slot are the same in every lane, so its update is one scalar
+// branch to one slot's code.
 template <int kSlots>
 __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
     const int lane = threadIdx.x;
     int64_t B[kSlots];
     int64_t Q[kSlots];
+    uint64_t K[kSlots];
 #pragma unroll
     for (int s = 0; s < kSlots; ++s) {
         const int32_t d = lane + s * kWave;
         B[s] = d < a.D ? a.beff[d] : 0;
         Q[s] = d < a.D ? a.qlen[d] : 0;
+        K[s] = best_b_key(B[s], d, a.D);
     }
+    auto lane_best = [&]() {
+        uint64_t m = K[0];
+#pragma unroll
+        for (int s = 1; s < kSlots; ++s) m = K[s] > m ? K[s] : m;
+        return m;
+    };
     const bool mq = a.policy == MAPS_POLICY_MQ;
     bool range_bad = false;
-    uint64_t kb = wave_max_u64(lane_best_b<kSlots>(B, lane, a.D));
+    uint64_t kb = wave_max_u64(lane_best());
     for (int64_t c0 = 0; c0 < a.A; c0 += kWave) {
         // 64 arrivals at a time: one per lane, read out with readlane
         const int64_t mine = c0 + lane;
@@ -278,15 +282,20 @@ __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
             }
             // the owning lane reserves and enqueues; a reservation changes the largest B_eff
             const int owner = best % kWave, slot = best / kWave;
+            if (lane == owner) {
 #pragma unroll
-            for (int s = 0; s < kSlots; ++s) {
-                if (s == slot && lane == owner) {
-                    if (need >= 0) B[s] -= need;
-                    Q[s] += 1;
-                    range_bad |= B[s] <= -kBlockLimit || B[s] >= kBlockLimit;
+                for (int s = 0; s < kSlots; ++s) {
+                    if (s == slot) {   // uniform: a scalar branch
+                        if (need >= 0) {
+                            B[s] -= need;
+                            K[s] = best_b_key(B[s], best, a.D);
+                        }
+                        Q[s] += 1;
+                        range_bad |= B[s] <= -kBlockLimit || B[s] >= kBlockLimit;
+                    }
                 }
             }
-            if (need >= 0) kb = wave_max_u64(lane_best_b<kSlots>(B, lane, a.D));
+            if (need >= 0) kb = wave_max_u64(lane_best());
             if (lane == j) {
                 out_d = best;
                 out_f = f;
