@@ -115,8 +115,9 @@ def _queues(rng, D, qmax, u_max):
 
 SHAPES = [  # (D, max residents, A, max queue)
     (1, 50, 1, 3), (3, 200, 1025, 40), (9, 300, 5000, 64), (17, 100, 9000, 0), (64, 40, 70000, 10),
-    # more decoders than the final selection stages capacities for in LDS (16,384)
-    (16500, 2, 300, 1),
+    # more decoders than the final selection stages capacities for in LDS (16,384), and more than a
+    # 16-bit decoder index holds in the groups' partial choices (65,536)
+    (16500, 2, 300, 1), (70000, 1, 100, 0),
 ]
 
 
