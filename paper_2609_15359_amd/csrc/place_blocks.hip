@@ -143,6 +143,23 @@ __device__ inline int64_t occupancy_at(int64_t t, int64_t S, int64_t N, int64_t 
     return ob;
 }
 
+// Quotient and remainder by the block size S for the pair kernel, whose
+// operands are below 2^32 (prompts and bounds are 32-bit, residues below S):
+// shifts when S is a power of two, else 32-bit division (a 64-bit division
+// is a software routine of about a hundred instructions, several per pair).
+template <bool kPow2>
+struct BlockDiv {
+    uint32_t S, sh;
+    __device__ uint32_t div(uint32_t n) const {
+        if constexpr (kPow2) return n >> sh;
+        else return n / S;
+    }
+    __device__ uint32_t mod(uint32_t n) const {
+        if constexpr (kPow2) return n & (S - 1u);
+        else return n - div(n) * S;
+    }
+};
+
 // Phase boundary for the slice in HBM, which only this workgroup touches (one
 // CU, one L2): each thread waits until its own stores and atomics have reached
 // L2, the barrier, then each thread drops its vector-L1 lines before reading
@@ -562,6 +579,7 @@ __global__ __launch_bounds__(kPairsNT) void blocks_order(PairArgs a) {
 // while its slice is in that XCD's L2, instead of each of the 8 L2s fetching
 // every slice.
 constexpr int kXcds = 8;
+template <bool kPow2>
 __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t tiles) {
     __shared__ int32_t row[kTile];
     const BlkLayout& L = a.L;
@@ -590,6 +608,7 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t til
     BlkSlice s = blk_slice(const_cast<char*>(a.snap) + h.slice, L, cap);
     const int32_t E = h.E;
     const int32_t tmax = 32 * L.W - 1;
+    const BlockDiv<kPow2> dv{uint32_t(S), uint32_t(__builtin_ctzll(uint64_t(S)))};
     bool neg = false, big = false;
 #pragma unroll
     for (int k = 0; k < kPairsPer; ++k) {
@@ -606,10 +625,18 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t til
             const uint2 w = s.rank[tc >> 5];
             int64_t j = int64_t(w.y) + __popc(w.x & ((1u << (tc & 31)) - 1u));
             j = j < E ? j : E;
-            const int64_t P = p / S, rho = p % S;
+            const int64_t P = dv.div(uint32_t(p)), rho = dv.mod(uint32_t(p));
             const int64_t left = P + s.PMX[j * S + rho];
-            int64_t at = P + ceil_plus(rho, U, S);
-            if (j < E) at += occupancy_at(U, S, s.N[j], s.SX[j], s.G + j * (S - 1));
+            int64_t at = P + dv.div(uint32_t(rho + U + S - 1));   // ceil((rho + U) / S)
+            if (j < E) {
+                // occupancy at U (as occupancy_at, with the quotient and remainder of U taken here)
+                const int64_t V = dv.div(uint32_t(U)), u = dv.mod(uint32_t(U)), N = s.N[j];
+                const int32_t* Gj = s.G + j * (S - 1);
+                int64_t ob = s.SX[j] + N * V + N;
+                if (u == 0) ob -= N - (S > 1 ? Gj[0] : 0);
+                if (u >= 2) ob += Gj[S - u];
+                at += ob;
+            }
             const int64_t after = (j < E && s.tau[j] == U) ? s.SMX[j + 1] : s.SMX[j];
             int64_t pk = left > at ? left : at;
             pk = pk > after ? pk : after;
@@ -778,7 +805,12 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
     hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kPairsNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();
     const int64_t rounds = (int64_t(D) + kXcds - 1) / kXcds;   // decoders per XCD
-    hipLaunchKernelGGL(blocks_pairs, dim3(unsigned(rounds * kXcds * tiles)), dim3(kPairsNT), 0, stream, pa, tiles);
+    if ((block_size & (block_size - 1)) == 0)
+        hipLaunchKernelGGL(blocks_pairs<true>, dim3(unsigned(rounds * kXcds * tiles)), dim3(kPairsNT), 0, stream, pa,
+                           tiles);
+    else
+        hipLaunchKernelGGL(blocks_pairs<false>, dim3(unsigned(rounds * kXcds * tiles)), dim3(kPairsNT), 0, stream, pa,
+                           tiles);
     MAPS_CHECK_LAUNCH();
     FinArgs fa{dev_err, D, block_size, capacity, queue_len, a_upper, A, policy, rr_offset, pair_peak, choice, chosen_peak,
                chosen_overflow, flags};
