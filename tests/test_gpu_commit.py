@@ -61,7 +61,9 @@ def _random_case(rng, D, nmax, A, u_max):
                                             # ranges longer than the chain's LDS stage, many floor blocks
                                             (4, 60, 500, 40000),
                                             # more decoders than threads: no lookups ahead
-                                            (1100, 3, 250, 2500)])
+                                            (1100, 3, 250, 2500),
+                                            # the most decoders the chain takes: the smallest LDS stage
+                                            (8192, 2, 60, 100)])
 def test_random(orc, D, nmax, A, u_max):
     rng = np.random.default_rng(D * 1000 + A)
     seg, p, g, U, a_p, a_U = _random_case(rng, D, nmax, A, u_max)
