@@ -10,18 +10,20 @@
 //   win_hist     one workgroup per chunk of 1,024 new completions: bucket of
 //                each (edges in LDS, binary search), kept as a 16-bit id, and
 //                the chunk's count per bucket (LDS atomics on nb counters).
-//   win_place    one workgroup per bucket: the bucket's new entries counted
-//                over the chunks (scan), then only the chunks that hold its
-//                last `window` new entries are walked, newest first; in each,
-//                the entries of the bucket are ranked in log order (ballots
-//                and a scan over the wavefronts) and written to their ring
-//                slots (count + rank) mod window; finally the count grows.
-//                Entries that a later entry of the same append would
-//                overwrite are not written, so no slot is written twice.
+//   win_place    one workgroup per bucket: the bucket's new entries before
+//                each chunk (a scan over the chunks, kept in LDS for appends
+//                of up to 1,024 chunks), then only the chunks
+//                that hold its last `window` new entries are visited, 16 at a
+//                time: the entries of the bucket are ranked in log order
+//                (ballots and a prefix over the wavefronts) and written to
+//                their ring slots (count + rank) mod window; finally the
+//                count grows.  Entries that a later entry of the same append
+//                would overwrite are not written, so no slot is written twice.
 //   win_select   one workgroup per bucket: the k-th smallest of its min(count,
 //                window) scores, k = ceil((1 - alpha)(n_w + 1)) (Eq. (3)), by an
-//                MSB-first radix select over LDS histograms; infinite when
-//                k > n_w.
+//                MSB-first radix select over LDS histograms, from the highest
+//                byte the largest score uses, each pass's digit found by one
+//                wavefront's scan of the 256 bins; infinite when k > n_w.
 //   win_bounds   grid-stride: the bound of Eq. (4) for every request from the
 //                quantile of its prediction's bucket.
 #include "maps_internal.hpp"
@@ -123,51 +125,132 @@ __global__ __launch_bounds__(kHistNT) void win_hist(AppendArgs a) {
     for (int32_t j = threadIdx.x; j < nb; j += kHistNT) a.ccount[int64_t(blockIdx.x) * nb + j] = cnt[j];
 }
 
+// Bucket b's workgroup.  The bucket's entries before each chunk come from a
+// scan over the chunks of its column of ccount: held in LDS when the append
+// has at most kPlaceNT chunks (kLds), else written over the column itself
+// (the column is the workgroup's alone).  Only the chunks that hold one of
+// the bucket's last `window` new entries are visited, kPlaceGroup of them at
+// a time: thread t takes entry t of each, the wavefronts' ballots rank the
+// entries inside each chunk, and a prefix over the wavefronts (one row of 16
+// lanes per chunk) places them.  Every load of a group is issued before the
+// group's first wait.
+constexpr int kPlaceGroup = 16;   // chunks ranked together
+constexpr int kPlaceWaves = kPlaceNT / kWave;
+static_assert(kPlaceWaves == 16, "one DPP row of 16 lanes holds a chunk's wavefront counts");
+static_assert(kPlaceGroup * kPlaceWaves <= kPlaceNT, "one thread per (chunk, wavefront) of a group");
+
+template <bool kLds>
 __global__ __launch_bounds__(kPlaceNT) void win_place(AppendArgs a) {
-    __shared__ int32_t tmp[kPlaceNT / kWave];
-    __shared__ int32_t wcount[kPlaceNT / kWave];
+    __shared__ int32_t tmp[kPlaceWaves];
+    __shared__ int32_t wcnt[kPlaceGroup * kPlaceWaves];   // bucket entries per (chunk of the group, wavefront)
+    __shared__ int32_t spre[kLds ? kPlaceNT : 1];         // kLds: the bucket's entries before chunk c
+    __shared__ int32_t first_active;
     const int32_t b = blockIdx.x, nb = a.nb, W = a.window;
-    if (!state_ok(a.state, nb, W)) {   // not reset for these (nb, window)
-        if (b == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
-        return;
-    }
+    const int tid = threadIdx.x, lane = tid % kWave, wid = tid / kWave;
     const WinLayout l = win_layout(nb, W);
     int64_t* count = reinterpret_cast<int64_t*>(a.state + l.off_count);
     int32_t* ring = reinterpret_cast<int32_t*>(a.state + l.off_ring) + int64_t(b) * W;
-    // new entries of bucket b, in total
-    int32_t mine = 0;
-    for (int32_t c = threadIdx.x; c < a.chunks; c += kPlaceNT) mine += a.ccount[int64_t(c) * nb + b];
-    const int32_t total = block_reduce_add<kPlaceNT>(mine, tmp);
+    int32_t* pre = a.ccount + b;   // chunk c at pre[c * nb]
+    // the header, the bucket's count and (kLds) this thread's chunk count are loaded together
     const int64_t c0 = count[b];
+    const int32_t mine = kLds && tid < a.chunks ? pre[int64_t(tid) * nb] : 0;
+    if (!state_ok(a.state, nb, W)) {   // not reset for these (nb, window)
+        if (b == 0 && tid == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
+        return;
+    }
+    int32_t total;
+    if constexpr (kLds) {
+        const int32_t run = block_excl_scan<kPlaceNT, false>(mine, 0, tmp, &total);
+        spre[tid] = run;
+    } else {
+        total = block_scan<kPlaceNT, false, false, true, int32_t>(
+            a.chunks, 0, [&](int64_t c) { return pre[c * nb]; }, [&](int64_t c, int32_t v) { pre[c * nb] = v; },
+            tmp);
+    }
+    auto start_of = [&](int32_t c) { return kLds ? spre[c] : pre[int64_t(c) * nb]; };
+    const int32_t keep = total - W;   // entries ranked below keep are overwritten within this append
+    // ring slot of rank r: (c0 + r) mod W, with c0 reduced once; base + r < W + 2^31 fits 32 unsigned bits
+    const uint32_t base = uint32_t(c0 % W);
+    // the first chunk holding an entry of rank >= keep: the first c whose next chunk starts above keep
+    if (tid == 0) first_active = a.chunks;
     __syncthreads();
-    // walk the chunks newest first while fewer than W of the newest entries are placed
-    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
-    int32_t after = 0;   // entries of bucket b in the chunks after the current one
-    for (int32_t c = a.chunks - 1; c >= 0 && after < W; --c) {
-        const int32_t in_chunk = a.ccount[int64_t(c) * nb + b];
-        if (in_chunk == 0) continue;
-        const int64_t i = int64_t(c) * kChunk + threadIdx.x;
-        const bool hit = i < a.k && a.bid[i] == b;
-        const uint64_t bal = __builtin_amdgcn_ballot_w64(hit);
-        const int32_t before_lane = __popcll(bal & ((uint64_t(1) << lane) - 1));
-        if (lane == 0) wcount[wid] = __popcll(bal);
-        __syncthreads();
-        int32_t before_wave = 0;
-        for (int w = 0; w < wid; ++w) before_wave += wcount[w];
-        // rank among all new entries of the bucket (0-based, log order)
-        const int32_t r = total - after - in_chunk + before_wave + before_lane;
-        if (hit && r >= total - W) {
-            const int32_t s = a.truth[i] > a.pred[i] ? a.truth[i] - a.pred[i] : 0;
-            ring[(c0 + r) % W] = s;
+    for (int32_t c = tid; c < a.chunks; c += kPlaceNT) {
+        const int32_t next = c + 1 < a.chunks ? start_of(c + 1) : total;
+        if (next > keep && next > start_of(c)) atomicMin(&first_active, c);
+    }
+    __syncthreads();
+    for (int32_t g0 = first_active; g0 < a.chunks; g0 += kPlaceGroup) {
+        bool hit[kPlaceGroup];
+        int32_t before_lane[kPlaceGroup], t[kPlaceGroup], p[kPlaceGroup], start[kPlaceGroup];
+#pragma unroll
+        for (int j = 0; j < kPlaceGroup; ++j) {
+            const int64_t i = int64_t(g0 + j) * kChunk + tid;
+            hit[j] = g0 + j < a.chunks && i < a.k && a.bid[i] == b;
+        }
+#pragma unroll
+        for (int j = 0; j < kPlaceGroup; ++j) {
+            const int64_t i = int64_t(g0 + j) * kChunk + tid;
+            t[j] = hit[j] ? a.truth[i] : 0;
+            p[j] = hit[j] ? a.pred[i] : 0;
+            start[j] = g0 + j < a.chunks ? start_of(g0 + j) : 0;
+            const uint64_t bal = __builtin_amdgcn_ballot_w64(hit[j]);
+            before_lane[j] = __popcll(bal & ((uint64_t(1) << lane) - 1));
+            if (lane == 0) wcnt[j * kPlaceWaves + wid] = __popcll(bal);
         }
         __syncthreads();
-        after += in_chunk;
+        // exclusive prefix over the wavefronts of each chunk: thread (j, w) scans row j's 16 counts
+        if (tid < kPlaceGroup * kPlaceWaves) {
+            const int32_t v = wcnt[tid];
+            int32_t incl = v;
+            incl += dpp_move<kDppRowShr1, 0xf>(0, incl);
+            incl += dpp_move<kDppRowShr2, 0xf>(0, incl);
+            incl += dpp_move<kDppRowShr4, 0xf>(0, incl);
+            incl += dpp_move<kDppRowShr8, 0xf>(0, incl);
+            wcnt[tid] = incl - v;   // each thread rewrites only its own entry
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPlaceGroup; ++j) {
+            // rank among all new entries of the bucket (0-based, log order)
+            const int32_t r = start[j] + wcnt[j * kPlaceWaves + wid] + before_lane[j];
+            if (hit[j] && r >= keep) ring[(base + uint32_t(r)) % uint32_t(W)] = t[j] > p[j] ? t[j] - p[j] : 0;
+        }
+        __syncthreads();   // wcnt is reused by the next group
     }
-    if (threadIdx.x == 0) count[b] = c0 + total;
+    if (tid == 0) count[b] = c0 + total;
 }
 
 __device__ inline int64_t conformal_rank(int64_t n, int32_t alpha_ppm) {
     return ((int64_t(1000000) - alpha_ppm) * (n + 1) + 999999) / 1000000;
+}
+
+// The digit of the next radix pass, found by wavefront 0: lane l holds bins
+// 4l .. 4l + 3, a wavefront scan gives the count below each lane, and the one
+// lane whose range holds `rank` walks its four bins.  sel = {digit, rank
+// within the digit}.
+__device__ inline void pick_digit(const int32_t* hist, int32_t rank, int32_t* sel) {
+    const int lane = threadIdx.x % kWave;
+    const int32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
+    const int32_t sum = h0 + h1 + h2 + h3;
+    const int32_t incl = wave_incl_scan_add(sum);
+    int32_t acc = incl - sum;
+    if (acc < rank && rank <= incl) {
+        int32_t d = 4 * lane;
+        if (acc + h0 < rank) {
+            acc += h0;
+            ++d;
+            if (acc + h1 < rank) {
+                acc += h1;
+                ++d;
+                if (acc + h2 < rank) {
+                    acc += h2;
+                    ++d;
+                }
+            }
+        }
+        sel[0] = d;
+        sel[1] = rank - acc;
+    }
 }
 
 __global__ __launch_bounds__(kSelNT) void win_select(const char* state, int32_t nb, int32_t W, int32_t alpha_ppm,
@@ -175,6 +258,7 @@ __global__ __launch_bounds__(kSelNT) void win_select(const char* state, int32_t 
     extern __shared__ int32_t vals[];   // W
     __shared__ int32_t hist[256];
     __shared__ int32_t sel[2];          // digit, remaining rank
+    __shared__ uint32_t vmax;
     const int32_t b = blockIdx.x;
     if (!state_ok(state, nb, W)) {
         if (threadIdx.x == 0) {
@@ -192,11 +276,24 @@ __global__ __launch_bounds__(kSelNT) void win_select(const char* state, int32_t 
         return;
     }
     const int32_t* ring = reinterpret_cast<const int32_t*>(state + l.off_ring) + int64_t(b) * W;
-    // the window is the ring's first nw slots (all W once the bucket has wrapped)
-    for (int32_t j = threadIdx.x; j < nw; j += kSelNT) vals[j] = ring[j];
-    uint32_t prefix = 0, mask = 0;
+    if (threadIdx.x == 0) vmax = 0;
+    __syncthreads();
+    // the window is the ring's first nw slots (all W once the bucket has wrapped); scores are >= 0
+    uint32_t m = 0;
+    for (int32_t j = threadIdx.x; j < nw; j += kSelNT) {
+        const int32_t v = ring[j];
+        vals[j] = v;
+        m = m > uint32_t(v) ? m : uint32_t(v);
+    }
+    m = wave_reduce_max(m);
+    if (threadIdx.x % kWave == 0) atomicMax(&vmax, m);
+    __syncthreads();
+    // passes start at the highest byte the largest score uses: the bytes above it are 0 in every score
+    const uint32_t top = vmax;
+    const int first = top >> 24 ? 24 : top >> 16 ? 16 : top >> 8 ? 8 : 0;
+    uint32_t prefix = 0, mask = first == 24 ? 0u : ~0u << (first + 8);
     int32_t rank = int32_t(k);   // 1-indexed among the values matching prefix under mask
-    for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int shift = first; shift >= 0; shift -= 8) {
         for (int j = threadIdx.x; j < 256; j += kSelNT) hist[j] = 0;
         __syncthreads();
         for (int32_t j = threadIdx.x; j < nw; j += kSelNT) {
@@ -204,12 +301,7 @@ __global__ __launch_bounds__(kSelNT) void win_select(const char* state, int32_t 
             if ((v & mask) == prefix) atomicAdd(&hist[(v >> shift) & 255], 1);
         }
         __syncthreads();
-        if (threadIdx.x == 0) {
-            int32_t acc = 0, d = 0;
-            for (; d < 255 && acc + hist[d] < rank; ++d) acc += hist[d];
-            sel[0] = d;
-            sel[1] = rank - acc;
-        }
+        if (threadIdx.x < kWave) pick_digit(hist, rank, sel);
         __syncthreads();
         prefix |= uint32_t(sel[0]) << shift;
         mask |= 255u << shift;
@@ -292,7 +384,8 @@ extern "C" maps_status maps_window_append(void* state, size_t state_bytes, int32
     allow_dynamic_lds(win_hist, lds);
     hipLaunchKernelGGL(win_hist, dim3(unsigned(chunks)), dim3(kHistNT), lds, stream, a);
     MAPS_CHECK_LAUNCH();
-    hipLaunchKernelGGL(win_place, dim3(unsigned(nb)), dim3(kPlaceNT), 0, stream, a);
+    if (chunks <= kPlaceNT) hipLaunchKernelGGL(win_place<true>, dim3(unsigned(nb)), dim3(kPlaceNT), 0, stream, a);
+    else hipLaunchKernelGGL(win_place<false>, dim3(unsigned(nb)), dim3(kPlaceNT), 0, stream, a);
     MAPS_CHECK_LAUNCH();
     return MAPS_OK;
 }

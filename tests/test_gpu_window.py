@@ -215,6 +215,77 @@ def test_incremental_window(orc, nb, window):
     say(f"[window-state] nb={nb} window={window}: {n} completions appended in {step + 1} batches")
 
 
+@pytest.mark.parametrize("top", [0, 255, 65535, 2**24 - 1, 2**24, 2**31 - 1])
+def test_incremental_window_score_range(orc, top):
+    """Scores from 0 up to `top` (all zero; the largest in the lowest, second,
+    third and top byte): the selection starts at the highest byte the largest
+    score uses, and every start gives the oracle's quantiles."""
+    import paper_2609_15359_amd as maps
+    rng = np.random.default_rng(top % 1000003)
+    n, window = 6000, 37
+    pred = rng.integers(0, 5000, size=n).astype(np.int32)
+    score = rng.integers(0, top + 1, size=n, dtype=np.int64)
+    score[rng.integers(0, n, size=50)] = top   # the largest score is present
+    truth = np.minimum(pred.astype(np.int64) + score, 2**31 - 1).astype(np.int32)
+    edges = np.array([1000, 3000], np.int32)
+    ap = np.concatenate([rng.integers(-1, 6000, size=500), [-1, 0]]).astype(np.int32)
+    st = maps.WindowState(_cuda(edges), window)
+    done = 0
+    for k in (1000, 37, 4963):
+        st.append(_cuda(pred[done:done + k]), _cuda(truth[done:done + k]))
+        done += k
+        for alpha in (50000, 500000):
+            _check_state(orc, st, pred[:done], truth[:done], edges, window, alpha, ap, 2**31 - 1,
+                         f"top={top} n={done}")
+
+
+def test_incremental_window_chunk_prefix_paths(orc):
+    """Appends of exactly 1,024 chunks of 1,024 completions (the largest whose
+    per-chunk prefix stays in LDS), of one completion more (the prefix written
+    over the workspace column) and a small one after them."""
+    import paper_2609_15359_amd as maps
+    rng = np.random.default_rng(1025)
+    sizes = [1024 * 1024, 1024 * 1024 + 1, 3000]
+    total = sum(sizes)
+    pred = rng.integers(0, 5000, size=total).astype(np.int32)
+    truth = (pred + rng.integers(-900, 3000, size=total)).clip(0).astype(np.int32)
+    edges = np.array([300, 800, 1500, 2500, 2600, 4000, 4900], np.int32)
+    ap = np.concatenate([rng.integers(-1, 6000, size=300), [-1, 0]]).astype(np.int32)
+    st = maps.WindowState(_cuda(edges), 500)
+    n = 0
+    for k in sizes:
+        st.append(_cuda(pred[n:n + k]), _cuda(truth[n:n + k]))
+        n += k
+        _check_state(orc, st, pred[:n], truth[:n], edges, 500, 100000, ap, 8000, f"chunks n={n}")
+
+
+def test_incremental_window_bounds_past_one_pass(orc):
+    """A bound call on more requests than one pass of the bound kernel's grid
+    covers (2,048 workgroups x 256 requests, three passes and a ragged tail):
+    the quantiles against the oracle's window calibration and every bound
+    against the oracle's Eq. (4) from those quantiles."""
+    import torch
+
+    import paper_2609_15359_amd as maps
+    rng = np.random.default_rng(8192)
+    n, window = 20000, 500
+    pred = rng.integers(0, 5000, size=n).astype(np.int32)
+    truth = (pred + rng.integers(-900, 3000, size=n)).clip(0).astype(np.int32)
+    edges = np.array([700, 1400, 2900, 4100], np.int32)
+    st = maps.WindowState(_cuda(edges), window)
+    st.append(_cuda(pred), _cuda(truth))
+    m = 3 * 2048 * 256 + 777
+    ap = rng.integers(-2, 7000, size=m).astype(np.int32)
+    q, U = st.bounds(50000, _cuda(ap), 6000)
+    torch.cuda.synchronize()
+    assert int(st.dev_err.item()) == 0
+    reps, buckets = _bucket_reps(edges)
+    want_q, _ = orc.calibrate_window(pred, truth, edges, window, 50000, reps, np.full(len(reps), n), 6000)
+    got_q = q.cpu().numpy()
+    assert_same("q", got_q[buckets], want_q)
+    assert_same("U", U.cpu().numpy(), orc.apply_bounds(ap, edges, got_q, 6000))
+
+
 def test_incremental_window_large(orc):
     """The large workload's 1,000,000 calibration pairs as the completion log,
     appended in 16 batches, window 500, 64 buckets; the bounds of every
