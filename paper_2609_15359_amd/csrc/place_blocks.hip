@@ -19,11 +19,14 @@
 //                    per-event counters by device atomics in the decoder's
 //                    slice, suffix scans, OB at every event, S prefix-max
 //                    scans and one suffix-max scan;
-//   blocks_order     per tile of 1,024 arrivals: their order by bound (a
-//                    counting sort on bound ranges), so that a wavefront's
-//                    lanes read neighbouring events;
-//   blocks_pairs     one workgroup per (decoder, 1,024 arrivals): every pair's
-//                    peak from the slice (read through L2) into the matrix;
+//   blocks_order     per tile of 8,192 arrivals: their positions, bounds and
+//                    prompts in bound order (a counting sort on 32,768 bound
+//                    ranges), so that a wavefront's lanes read the same or
+//                    neighbouring events;
+//   blocks_pairs     one workgroup per (decoder, tile), the tile in passes of
+//                    1,024 pairs, four a thread, each pass's loads issued in
+//                    three rounds: every pair's peak from the slice (read
+//                    through L2) into the matrix;
 //   blocks_finish    per arrival: the choice over the matrix column.
 #include "maps_internal.hpp"
 
@@ -33,6 +36,7 @@ namespace {
 constexpr int kPbNT = 1024;
 constexpr int kPairsNT = 256;
 constexpr int kPairsPer = 4;
+constexpr int kOrdNT = 1024;
 constexpr int kFinNT = 256;
 
 // Snapshot: a 64-byte header with the arguments it was built for, the decoder
@@ -531,43 +535,81 @@ struct PairArgs {
     int64_t A;
     const int64_t* seg_off;
     int32_t* pair;
-    int32_t* order;   // per tile of 1,024 arrivals: their tile indices, by bound
+    int32_t* order;   // per tile of kTile arrivals: their tile indices, by bound
+    int32_t* sU;      // the same tile's bounds in that order
+    int32_t* sp;      // and prompts
     uint32_t* dev_err;
 };
 
-constexpr int kTile = kPairsNT * kPairsPer;
+// A tile of kTile arrivals is sorted by bound once; each decoder's workgroup
+// takes it in passes of kPass pairs, kPairsPer per thread.  The larger the
+// tile, the fewer distinct events the 64 sorted arrivals of a wavefront land
+// on, so the fewer cache lines each of the pair kernel's loads touches.
+constexpr int kPass = kPairsNT * kPairsPer;
+constexpr int kTile = 8192;
+constexpr int kOrdPer = kTile / kOrdNT;
+constexpr int kOrdBins = 32768;   // bound ranges of the counting sort, a power of two
+static_assert(kTile % kPass == 0 && kTile % kOrdNT == 0, "whole passes and order rounds per tile");
+constexpr int kOrdBinsPer = kOrdBins / kOrdNT;
+static_assert(kOrdBins % kOrdNT == 0, "whole bins a thread in the scan");
 
-// The arrivals of each tile ordered by their bound (a counting sort on 1,024
-// bound ranges), so that the lanes of a wavefront read neighbouring events of
-// a decoder's slice.  Written once, used by every decoder's workgroup.
-__global__ __launch_bounds__(kPairsNT) void blocks_order(PairArgs a) {
-    __shared__ int32_t start[kTile];
-    __shared__ int32_t tmp[kPairsNT / kWave];
+// The arrivals of each tile ordered by their bound (a counting sort on
+// kOrdBins bound ranges of 2^sh steps, sh the least that covers 0..u_max), so
+// that the lanes of a wavefront read neighbouring events of a decoder's slice.
+// Written once, used by every decoder's workgroup.
+__global__ __launch_bounds__(kOrdNT) void blocks_order(PairArgs a) {
+    __shared__ int32_t start[kOrdBins];
+    __shared__ int32_t tmp[kOrdNT / kWave];
     const int64_t base = int64_t(blockIdx.x) * kTile;
     const int64_t left = a.A - base;
     const int n = left < kTile ? int(left) : kTile;
-    for (int b = threadIdx.x; b < kTile; b += kPairsNT) start[b] = 0;
-    __syncthreads();
-    int key[kPairsPer];
-    const int64_t span = int64_t(a.L.u_max) + 1;
+    for (int b = threadIdx.x; b < kOrdBins; b += kOrdNT) start[b] = 0;
+    int32_t Uv[kOrdPer], pv[kOrdPer];
 #pragma unroll
-    for (int k = 0; k < kPairsPer; ++k) {
-        const int t = threadIdx.x + k * kPairsNT;
-        key[k] = 0;
-        if (t < n) {
-            const int64_t U = a.aU[base + t];
-            const int64_t u = U < 0 ? 0 : (U < span ? U : span - 1);
-            key[k] = int(u * kTile / span);
-            atomicAdd(&start[key[k]], 1);
-        }
+    for (int k = 0; k < kOrdPer; ++k) {
+        const int t = threadIdx.x + k * kOrdNT;
+        Uv[k] = t < n ? a.aU[base + t] : 0;
+        pv[k] = t < n ? a.ap[base + t] : 0;
+    }
+    const int32_t top = a.L.u_max;   // bounds above u_max share the last range
+    int sh = 0;
+    while ((top >> sh) >= kOrdBins) ++sh;
+    __syncthreads();
+    int key[kOrdPer];
+#pragma unroll
+    for (int k = 0; k < kOrdPer; ++k) {
+        const int t = threadIdx.x + k * kOrdNT;
+        const int32_t u = Uv[k] < 0 ? 0 : (Uv[k] < top ? Uv[k] : top);
+        key[k] = u >> sh;
+        if (t < n) atomicAdd(&start[key[k]], 1);
     }
     __syncthreads();
-    block_scan<kPairsNT, false, false, true, int32_t>(
-        kTile, 0, [&](int64_t b) { return start[b]; }, [&](int64_t b, int32_t v) { start[b] = v; }, tmp);
+    {
+        // exclusive prefix over the bins, kOrdBinsPer consecutive ones a thread
+        int32_t c[kOrdBinsPer], sum = 0;
 #pragma unroll
-    for (int k = 0; k < kPairsPer; ++k) {
-        const int t = threadIdx.x + k * kPairsNT;
-        if (t < n) a.order[base + atomicAdd(&start[key[k]], 1)] = t;
+        for (int q = 0; q < kOrdBinsPer; ++q) {
+            c[q] = start[kOrdBinsPer * threadIdx.x + q];
+            sum += c[q];
+        }
+        int32_t total;
+        int32_t run = block_excl_scan<kOrdNT, false>(sum, 0, tmp, &total);
+#pragma unroll
+        for (int q = 0; q < kOrdBinsPer; ++q) {
+            start[kOrdBinsPer * threadIdx.x + q] = run;
+            run += c[q];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int k = 0; k < kOrdPer; ++k) {
+        const int t = threadIdx.x + k * kOrdNT;
+        if (t < n) {
+            const int64_t o = base + atomicAdd(&start[key[k]], 1);
+            a.order[o] = t;
+            a.sU[o] = Uv[k];
+            a.sp[o] = pv[k];
+        }
     }
 }
 
@@ -599,51 +641,85 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t til
     const int64_t cap = a.seg_off[d + 1] - a.seg_off[d] + 1;
     if (h.slice < 0 || h.cap != cap) {
         if (h.slice >= 0 && tile == 0 && threadIdx.x == 0) raise_error(a.dev_err, MAPS_ERR_SNAPSHOT);
-        for (int k = 0; k < kPairsPer; ++k) {
-            const int t = threadIdx.x + k * kPairsNT;
-            if (t < n) a.pair[int64_t(d) * a.A + base + t] = -1;
-        }
+        for (int t = threadIdx.x; t < n; t += kPairsNT) a.pair[int64_t(d) * a.A + base + t] = -1;
         return;
     }
     BlkSlice s = blk_slice(const_cast<char*>(a.snap) + h.slice, L, cap);
     const int32_t E = h.E;
     const int32_t tmax = 32 * L.W - 1;
     const BlockDiv<kPow2> dv{uint32_t(S), uint32_t(__builtin_ctzll(uint64_t(S)))};
+    // The kPairsPer pairs of a thread go through three rounds of loads together:
+    // the tile's (position, bound, prompt) in bound order, the rank words, then
+    // the event's entries; a pair without a bound (or past the tile) reads event 0
+    // and is written as -1.
     bool neg = false, big = false;
+    for (int p0 = 0; p0 < n; p0 += kPass) {
+        int32_t loc[kPairsPer], Uv[kPairsPer], pv[kPairsPer];
 #pragma unroll
-    for (int k = 0; k < kPairsPer; ++k) {
-        const int t = threadIdx.x + k * kPairsNT;
-        if (t >= n) continue;
-        const int32_t loc = a.order[base + t];
-        const int64_t i = base + loc;
-        const int32_t U = a.aU[i];
-        int32_t out = -1;
-        if (U >= 0) {
-            neg |= a.ap[i] < 0;
-            const int64_t p = a.ap[i] < 0 ? 0 : a.ap[i];
-            const int32_t tc = U < tmax ? U : tmax;
-            const uint2 w = s.rank[tc >> 5];
-            int64_t j = int64_t(w.y) + __popc(w.x & ((1u << (tc & 31)) - 1u));
-            j = j < E ? j : E;
-            const int64_t P = dv.div(uint32_t(p)), rho = dv.mod(uint32_t(p));
-            const int64_t left = P + s.PMX[j * S + rho];
-            int64_t at = P + dv.div(uint32_t(rho + U + S - 1));   // ceil((rho + U) / S)
-            if (j < E) {
-                // occupancy at U (as occupancy_at, with the quotient and remainder of U taken here)
-                const int64_t V = dv.div(uint32_t(U)), u = dv.mod(uint32_t(U)), N = s.N[j];
-                const int32_t* Gj = s.G + j * (S - 1);
-                int64_t ob = s.SX[j] + N * V + N;
-                if (u == 0) ob -= N - (S > 1 ? Gj[0] : 0);
-                if (u >= 2) ob += Gj[S - u];
-                at += ob;
-            }
-            const int64_t after = (j < E && s.tau[j] == U) ? s.SMX[j + 1] : s.SMX[j];
-            int64_t pk = left > at ? left : at;
-            pk = pk > after ? pk : after;
-            big |= pk > INT32_MAX;
-            out = int32_t(pk > INT32_MAX ? INT32_MAX : pk);
+        for (int k = 0; k < kPairsPer; ++k) {
+            const int t = p0 + threadIdx.x + k * kPairsNT;
+            const bool in = t < n;
+            loc[k] = in ? a.order[base + t] : -1;
+            Uv[k] = in ? a.sU[base + t] : -1;
+            pv[k] = in ? a.sp[base + t] : 0;
         }
-        row[loc] = out;
+        uint2 w[kPairsPer];
+#pragma unroll
+        for (int k = 0; k < kPairsPer; ++k) {
+            const int32_t tc = Uv[k] < 0 ? 0 : (Uv[k] < tmax ? Uv[k] : tmax);
+            w[k] = s.rank[tc >> 5];
+        }
+        int32_t pmx[kPairsPer], nj[kPairsPer], gj[kPairsPer], tj[kPairsPer], sm0[kPairsPer], sm1[kPairsPer];
+        int64_t sx[kPairsPer];
+        int32_t jj[kPairsPer];
+#pragma unroll
+        for (int k = 0; k < kPairsPer; ++k) {
+            const int32_t U = Uv[k] < 0 ? 0 : Uv[k];
+            const int32_t tc = U < tmax ? U : tmax;
+            int32_t j = int32_t(w[k].y) + __popc(w[k].x & ((1u << (tc & 31)) - 1u));
+            j = j < E ? j : E;
+            jj[k] = j;
+            const uint32_t p = uint32_t(pv[k] < 0 ? 0 : pv[k]);
+            const uint32_t u = dv.mod(uint32_t(U));
+            // G index: Gj[0] when u = 0, Gj[S - u] when u >= 2, unused otherwise (read at 0)
+            const int64_t gi = u >= 2 ? int64_t(S) - u : 0;
+            const int32_t jr = j < E ? j : 0;   // the entries of a real event; E has none
+            pmx[k] = s.PMX[int64_t(j) * S + dv.mod(p)];
+            nj[k] = s.N[jr];
+            gj[k] = S > 1 ? s.G[int64_t(jr) * (S - 1) + gi] : 0;
+            sx[k] = s.SX[jr];
+            tj[k] = s.tau[jr];
+            sm0[k] = s.SMX[j];
+            sm1[k] = s.SMX[j < E ? j + 1 : j];
+        }
+#pragma unroll
+        for (int k = 0; k < kPairsPer; ++k) {
+            if (loc[k] < 0) continue;
+            const int32_t U = Uv[k];
+            int32_t out = -1;
+            if (U >= 0) {
+                neg |= pv[k] < 0;
+                const int64_t p = pv[k] < 0 ? 0 : pv[k];
+                const int32_t j = jj[k];
+                const int64_t P = dv.div(uint32_t(p)), rho = dv.mod(uint32_t(p));
+                const int64_t left = P + pmx[k];
+                int64_t at = P + dv.div(uint32_t(rho + U + S - 1));   // ceil((rho + U) / S)
+                if (j < E) {
+                    // occupancy at U (as occupancy_at, with the quotient and remainder of U taken here)
+                    const int64_t V = dv.div(uint32_t(U)), u = dv.mod(uint32_t(U)), N = nj[k];
+                    int64_t ob = sx[k] + N * V + N;
+                    if (u == 0) ob -= N - gj[k];
+                    if (u >= 2) ob += gj[k];
+                    at += ob;
+                }
+                const int64_t after = (j < E && tj[k] == U) ? sm1[k] : sm0[k];
+                int64_t pk = left > at ? left : at;
+                pk = pk > after ? pk : after;
+                big |= pk > INT32_MAX;
+                out = int32_t(pk > INT32_MAX ? INT32_MAX : pk);
+            }
+            row[loc[k]] = out;
+        }
     }
     // a negative prompt, or a peak clamped to INT32_MAX, is reported once per wavefront
     if (__builtin_amdgcn_ballot_w64(neg) != 0 && threadIdx.x % kWave == 0) raise_error(a.dev_err, MAPS_ERR_NEG_LEN);
@@ -798,11 +874,12 @@ extern "C" maps_status maps_place_blocks(const void* snapshot, const int64_t* se
         return MAPS_E_NULL;
     if (A == 0) return MAPS_OK;
     const BlkLayout L = blk_layout(D, n_total, u_max, block_size);
-    // chosen_overflow holds each tile's order until blocks_finish writes it
+    // chosen_overflow, chosen_peak and choice hold each tile's order, bounds and prompts until blocks_finish
+    // writes them
     PairArgs pa{L, static_cast<const char*>(snapshot), a_prompt, a_upper, A, seg_off, pair_peak, chosen_overflow,
-                dev_err};
+                chosen_peak, choice, dev_err};
     const int64_t tiles = (A + kTile - 1) / kTile;
-    hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kPairsNT), 0, stream, pa);
+    hipLaunchKernelGGL(blocks_order, dim3(unsigned(tiles)), dim3(kOrdNT), 0, stream, pa);
     MAPS_CHECK_LAUNCH();
     const int64_t rounds = (int64_t(D) + kXcds - 1) / kXcds;   // decoders per XCD
     if ((block_size & (block_size - 1)) == 0)

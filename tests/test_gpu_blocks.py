@@ -62,6 +62,9 @@ CASES = [  # (D, max residents, A, u_max, S)
     # 1,000 at S = 64, 2,700 at S = 16 with u_max 60,000), or with 65,536 residents or more: their
     # arrays stay in HBM, beside decoders that fit
     (3, 4000, 2000, 30000, 64), (4, 10000, 1200, 60000, 16), (1, 200000, 300, 1000, 16),
+    # two whole sort tiles of 8,192 arrivals and a ragged third, bounds up to the largest u_max (sorted in
+    # ranges of four steps)
+    (6, 150, 16461, 131072, 16),
 ]
 
 
