@@ -56,9 +56,12 @@ static_assert(sizeof(BlkSnapHeader) == 64, "block snapshot header size");
 
 // Decoder slice: W rank words {bits, events before}, then per event e = 0..E
 // (E+1 records, the last one for "no resident left") the arrays
-//   tau[e] (int32), N[e] (int32), SX[e] (int64), OB[e] (int32), SMX[e] (int32),
-//   G[e][c-1] = #{xi >= c} for c = 1..S-1 (int32), PMX[e][rho] (int32),
-// each of n_d + 1 entries (E <= n_d).
+//   PMX[e][rho] (int32), G[e][c-1] = #{xi >= c} for c = 1..S-1 (int32, rows of
+//   Sg = S - 1 rounded up to a multiple of 4), SX[e] (int64), tau[e], N[e],
+//   OB[e], SMX[e] (int32),
+// each with room for capA = n_d + 1 rounded up to a multiple of 4 records, so
+// that every array starts 16-byte aligned (and, when S is a multiple of 4,
+// every PMX row: the projection writes them 16 bytes at a time).
 struct BlkLayout {
     int32_t D, u_max, S, W;
     int64_t n_total;
@@ -74,6 +77,9 @@ struct BlkHeader {
     int32_t base;      // max_t OB(t)
 };
 
+// Entries per G row: the S - 1 class counts, rounded up to a multiple of 4.
+__host__ __device__ inline int64_t blk_gw(int64_t S) { return (S - 1 + 3) & ~int64_t(3); }
+
 __host__ __device__ inline BlkLayout blk_layout(int32_t D, int64_t n_total, int32_t u_max, int32_t S) {
     BlkLayout L;
     L.D = D;
@@ -81,10 +87,11 @@ __host__ __device__ inline BlkLayout blk_layout(int32_t D, int64_t n_total, int3
     L.S = S;
     L.W = (((u_max + 1) / 32 + 1) + 1) & ~1;
     L.n_total = n_total;
-    L.rec = (size_t(4 + 4 + 8 + 4 + 4) + size_t(S - 1) * 4 + size_t(S) * 4 + 15) & ~size_t(15);   // 16-byte slices
+    // bytes per record, a multiple of 16 so that every slice starts 16-byte aligned
+    L.rec = (size_t(4 + 4 + 8 + 4 + 4) + size_t(blk_gw(S)) * 4 + size_t(S) * 4 + 15) & ~size_t(15);
     L.hdr_bytes = align256(sizeof(BlkSnapHeader) + size_t(D) * sizeof(BlkHeader));
-    // slice d starts at hdr + d * (8 W + 8 * 16) + seg_off[d] * (rec) with room for n_d + 1 records
-    L.bytes = L.hdr_bytes + size_t(D) * (size_t(L.W) * 8 + 8 * 16 + L.rec) + size_t(n_total) * L.rec + 256;
+    // slice d starts at hdr + d * (8 W + 4 rec) + seg_off[d] * rec with room for capA <= n_d + 4 records
+    L.bytes = L.hdr_bytes + size_t(D) * (size_t(L.W) * 8 + 4 * L.rec) + size_t(n_total) * L.rec + 256;
     return L;
 }
 
@@ -95,34 +102,38 @@ struct BlkSlice {
     int64_t* SX;
     int32_t* OB;
     int32_t* SMX;
-    int32_t* G;      // [cap][S-1]
-    int32_t* PMX;    // [cap][S]
+    int32_t* G;      // [capA][Gw]: class c of event e at G[e * Gw + c]
+    int32_t* PMX;    // [capA][S]
+    int64_t Gw;
 };
 
-// Arrays of a slice with room for `cap` records (cap = n_d + 1).
+// Arrays of a slice with room for `cap` records (cap = n_d + 1), each array
+// capA = cap rounded up to a multiple of 4 entries long.
 __host__ __device__ inline BlkSlice blk_slice(char* base, const BlkLayout& L, int64_t cap) {
     BlkSlice s;
+    const size_t capA = size_t((cap + 3) & ~int64_t(3));
+    s.Gw = blk_gw(L.S);
     char* q = base;
     s.rank = reinterpret_cast<uint2*>(q);
     q += size_t(L.W) * 8;
-    s.SX = reinterpret_cast<int64_t*>(q);
-    q += size_t(cap) * 8;
-    s.tau = reinterpret_cast<int32_t*>(q);
-    q += size_t(cap) * 4;
-    s.N = reinterpret_cast<int32_t*>(q);
-    q += size_t(cap) * 4;
-    s.OB = reinterpret_cast<int32_t*>(q);
-    q += size_t(cap) * 4;
-    s.SMX = reinterpret_cast<int32_t*>(q);
-    q += size_t(cap) * 4;
-    s.G = reinterpret_cast<int32_t*>(q);
-    q += size_t(cap) * size_t(L.S - 1) * 4;
     s.PMX = reinterpret_cast<int32_t*>(q);
+    q += capA * size_t(L.S) * 4;
+    s.G = reinterpret_cast<int32_t*>(q);
+    q += capA * size_t(s.Gw) * 4;
+    s.SX = reinterpret_cast<int64_t*>(q);
+    q += capA * 8;
+    s.tau = reinterpret_cast<int32_t*>(q);
+    q += capA * 4;
+    s.N = reinterpret_cast<int32_t*>(q);
+    q += capA * 4;
+    s.OB = reinterpret_cast<int32_t*>(q);
+    q += capA * 4;
+    s.SMX = reinterpret_cast<int32_t*>(q);
     return s;
 }
 
 __host__ __device__ inline int64_t blk_slice_offset(const BlkLayout& L, int32_t d, int64_t seg_lo) {
-    return int64_t(L.hdr_bytes) + int64_t(d) * (int64_t(L.W) * 8 + 8 * 16 + int64_t(L.rec)) + seg_lo * int64_t(L.rec);
+    return int64_t(L.hdr_bytes) + int64_t(d) * (int64_t(L.W) * 8 + 4 * int64_t(L.rec)) + seg_lo * int64_t(L.rec);
 }
 
 __host__ __device__ inline BlkHeader* blk_headers(char* snap) {
@@ -177,12 +188,14 @@ __device__ inline void sync_global() {
 
 // Up to kGroup scans at once over the same len elements (sum or max, forward
 // or reverse, inclusive or exclusive), each thread one contiguous chunk:
-// get(i, q) and put(i, q, v) for quantity q < nq.  One pass for the chunk
+// get(i, q) and put(i, q, v) for quantity q < nq (kRowPut: put(i, v[kGroup])
+// once per element, entries past nq unused).  One pass for the chunk
 // totals, one wavefront scan per quantity through DPP, one LDS exchange for
 // all of them, one pass to write.  `tmp` holds kGroup * NT / 64 values.
 constexpr int kGroup = 16;
 
-template <int NT, bool kMax, bool kReverse, bool kExclusive, typename T, typename Get, typename Put>
+template <int NT, bool kMax, bool kReverse, bool kExclusive, typename T, bool kRowPut = false, typename Get,
+          typename Put>
 __device__ inline void group_scan(int64_t len, int nq, T identity, Get get, Put put, T* tmp) {
     constexpr int kWaves = NT / kWave;
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
@@ -207,22 +220,43 @@ __device__ inline void group_scan(int64_t len, int nq, T identity, Get get, Put 
         acc[q] = wave_shift_up1(incl, identity);   // exclusive within the wavefront
     }
     __syncthreads();
+    if constexpr (kWaves == 16) {
+        // every quantity's prefix over the wavefronts at once: thread (q, w) of the first kGroup
+        // wavefront-rows holds tmp[q][w], one DPP row of 16 lanes scans it, and the row shifted by one
+        // is the exclusive prefix (each thread rewrites only its own entry)
+        if (threadIdx.x < kGroup * kWaves) {
+            T incl = tmp[threadIdx.x];
+            incl = op(incl, dpp_move<kDppRowShr1, 0xf>(identity, incl));
+            incl = op(incl, dpp_move<kDppRowShr2, 0xf>(identity, incl));
+            incl = op(incl, dpp_move<kDppRowShr4, 0xf>(identity, incl));
+            incl = op(incl, dpp_move<kDppRowShr8, 0xf>(identity, incl));
+            tmp[threadIdx.x] = dpp_move<kDppRowShr1, 0xf>(identity, incl);
+        }
+        __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kGroup; ++q) {
-        T before = identity;
-        for (int w = 0; w < wid; ++w) before = op(before, tmp[q * kWaves + w]);
-        acc[q] = op(before, acc[q]);
-    }
-    for (int64_t i = b; i < e; ++i) {
+        for (int q = 0; q < kGroup; ++q) acc[q] = op(tmp[q * kWaves + wid], acc[q]);
+    } else {
 #pragma unroll
         for (int q = 0; q < kGroup; ++q) {
+            T before = identity;
+            for (int w = 0; w < wid; ++w) before = op(before, tmp[q * kWaves + w]);
+            acc[q] = op(before, acc[q]);
+        }
+    }
+    for (int64_t i = b; i < e; ++i) {
+        T out[kGroup];
+#pragma unroll
+        for (int q = 0; q < kGroup; ++q) {
+            out[q] = identity;
             if (q < nq) {
                 const T x = get(idx(i), q);
                 const T next = op(acc[q], x);
-                put(idx(i), q, kExclusive ? acc[q] : next);
+                out[q] = kExclusive ? acc[q] : next;
+                if constexpr (!kRowPut) put(idx(i), q, out[q]);
                 acc[q] = next;
             }
         }
+        if constexpr (kRowPut) put(idx(i), out);   // all nq results of element i at once
     }
     __syncthreads();
 }
@@ -343,13 +377,29 @@ __device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int
     __syncthreads();
     // 6'. prefix maxima per residue class (exclusive: events below) into the
     // slice, the suffix maximum, then the slice's event arrays
-    for (int r0 = 0; r0 < S; r0 += kGroup)
-        group_scan<kPbNT, true, false, true, int32_t>(
-            len, int(S - r0 < kGroup ? S - r0 : kGroup), 0,
+    // with S a multiple of 4 every row, and every group of kGroup residues in it, starts 16-byte aligned
+    const bool vec = S % 4 == 0 && (reinterpret_cast<uintptr_t>(s.PMX) & 15) == 0;
+    for (int r0 = 0; r0 < S; r0 += kGroup) {
+        const int nq = int(S - r0 < kGroup ? S - r0 : kGroup);
+        group_scan<kPbNT, true, false, true, int32_t, true>(
+            len, nq, 0,
             [&](int64_t e, int q) {
                 return e < int64_t(E) ? int32_t(r.OB[e] + ceil_plus(r0 + q, r.tau[e], S)) : 0;
             },
-            [&](int64_t e, int q, int32_t v) { s.PMX[e * S + r0 + q] = v; }, redg);
+            [&](int64_t e, const int32_t (&v)[kGroup]) {
+                int32_t* dst = s.PMX + e * S + r0;
+                if (vec) {
+#pragma unroll
+                    for (int q = 0; q < kGroup; q += 4)
+                        if (q < nq) *reinterpret_cast<int4*>(dst + q) = make_int4(v[q], v[q + 1], v[q + 2], v[q + 3]);
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kGroup; ++q)
+                        if (q < nq) dst[q] = v[q];
+                }
+            },
+            redg);
+    }
     const int32_t base_pk = block_scan<kPbNT, true, true, false, int32_t>(
         len, 0, [&](int64_t e) { return r.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
         reinterpret_cast<int32_t*>(red32));
@@ -358,7 +408,13 @@ __device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int
         s.N[e] = int32_t(r.N[e]);
         s.SX[e] = int64_t(r.SX[e]);
         s.OB[e] = r.OB[e];
-        for (int c = 0; c + 1 < S; ++c) s.G[e * (S - 1) + c] = int32_t(r.g(e, c));
+    }
+    // the class rows in address order, Gw entries an event (the padding past S - 1 classes zero): each
+    // wavefront stores whole lines (len Gw is below 2^31 here: fewer than 65,536 records)
+    const uint32_t gw = uint32_t(s.Gw);
+    for (uint32_t k = tid; k < uint32_t(len) * gw; k += kPbNT) {
+        const uint32_t e = k / gw, c = k - e * gw;
+        s.G[k] = c + 1 < uint32_t(S) ? int32_t(r.g(e, int(c))) : 0;
     }
     if (tid == 0) {
         BlkHeader* hdr = blk_headers(a.snap);
@@ -450,7 +506,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     for (int64_t e = tid; e <= int64_t(E); e += kPbNT) {
         s.N[e] = 0;
         s.SX[e] = 0;
-        for (int c = 0; c + 1 < S; ++c) s.G[e * (S - 1) + c] = 0;
+        for (int c = 0; c + 1 < S; ++c) s.G[e * s.Gw + c] = 0;
     }
     sync_global();
 
@@ -468,7 +524,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
         atomicAdd(&s.N[e], 1);
         atomicAdd(reinterpret_cast<unsigned long long*>(&s.SX[e]), (unsigned long long)(x / S));
         const int xi = int(x % S);
-        if (xi >= 1) atomicAdd(&s.G[e * (S - 1) + (xi - 1)], 1);
+        if (xi >= 1) atomicAdd(&s.G[e * s.Gw + (xi - 1)], 1);
     }
     sync_global();
 
@@ -479,7 +535,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     // N (quantity 0) and the S - 1 class counts (quantity c), kGroup at a time
     for (int q0 = 0; q0 < S; q0 += kGroup) {
         auto cell = [&](int64_t e, int q) -> int32_t& {
-            return q0 + q == 0 ? s.N[e] : s.G[e * (S - 1) + (q0 + q - 1)];
+            return q0 + q == 0 ? s.N[e] : s.G[e * s.Gw + (q0 + q - 1)];
         };
         group_scan<kPbNT, false, true, false, int32_t>(
             len, int(S - q0 < kGroup ? S - q0 : kGroup), 0, [&](int64_t e, int q) { return cell(e, q); },
@@ -490,8 +546,8 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     for (int64_t e = tid; e < len; e += kPbNT) {
         int32_t acc = 0;
         for (int c = int(S) - 2; c >= 0; --c) {
-            acc += s.G[e * (S - 1) + c];
-            s.G[e * (S - 1) + c] = acc;
+            acc += s.G[e * s.Gw + c];
+            s.G[e * s.Gw + c] = acc;
         }
     }
     sync_global();
@@ -500,7 +556,7 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     bool big = false;
     for (int64_t e = tid; e < len; e += kPbNT) {
         int64_t ob = 0;
-        if (e < int64_t(E)) ob = occupancy_at(s.tau[e], S, s.N[e], s.SX[e], s.G + e * (S - 1));
+        if (e < int64_t(E)) ob = occupancy_at(s.tau[e], S, s.N[e], s.SX[e], s.G + e * s.Gw);
         big |= ob + 2 * int64_t(L.u_max) / S + 2 > int64_t(INT32_MAX) / 2;
         s.OB[e] = int32_t(ob > INT32_MAX ? INT32_MAX : ob);
     }
@@ -686,7 +742,7 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t til
             const int32_t jr = j < E ? j : 0;   // the entries of a real event; E has none
             pmx[k] = s.PMX[int64_t(j) * S + dv.mod(p)];
             nj[k] = s.N[jr];
-            gj[k] = S > 1 ? s.G[int64_t(jr) * (S - 1) + gi] : 0;
+            gj[k] = S > 1 ? s.G[int64_t(jr) * s.Gw + gi] : 0;
             sx[k] = s.SX[jr];
             tj[k] = s.tau[jr];
             sm0[k] = s.SMX[j];
