@@ -613,8 +613,7 @@ constexpr int kTile = 8192;
 constexpr int kOrdPer = kTile / kOrdNT;
 constexpr int kOrdBins = 32768;   // bound ranges of the counting sort, a power of two
 static_assert(kTile % kPass == 0 && kTile % kOrdNT == 0, "whole passes and order rounds per tile");
-constexpr int kOrdBinsPer = kOrdBins / kOrdNT;
-static_assert(kOrdBins % kOrdNT == 0, "whole bins a thread in the scan");
+static_assert(kOrdBins % kOrdNT == 0, "whole rounds of 64 bins per wavefront in the scan");
 
 // The arrivals of each tile ordered by their bound (a counting sort on
 // kOrdBins bound ranges of 2^sh steps, sh the least that covers 0..u_max), so
@@ -648,19 +647,27 @@ __global__ __launch_bounds__(kOrdNT) void blocks_order(PairArgs a) {
     }
     __syncthreads();
     {
-        // exclusive prefix over the bins, kOrdBinsPer consecutive ones a thread
-        int32_t c[kOrdBinsPer], sum = 0;
+        // exclusive prefix over the bins: wavefront w takes the contiguous bins [w kSeg, (w + 1) kSeg), 64 at a
+        // time (lane l reads bin 64 r + l of round r, so no two lanes share an LDS bank), once for its total
+        // and, after the totals are exchanged, once more for the prefix
+        constexpr int kWaves = kOrdNT / kWave;
+        constexpr int kSeg = kOrdBins / kWaves;
+        const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+        int32_t* seg = start + wid * kSeg;
+        int32_t part = 0;
+        for (int r = 0; r < kSeg; r += kWave) part += seg[r + lane];
+        part = wave_reduce_add(part);
+        if (lane == 0) tmp[wid] = part;
+        __syncthreads();
+        int32_t carry = 0;
 #pragma unroll
-        for (int q = 0; q < kOrdBinsPer; ++q) {
-            c[q] = start[kOrdBinsPer * threadIdx.x + q];
-            sum += c[q];
-        }
-        int32_t total;
-        int32_t run = block_excl_scan<kOrdNT, false>(sum, 0, tmp, &total);
-#pragma unroll
-        for (int q = 0; q < kOrdBinsPer; ++q) {
-            start[kOrdBinsPer * threadIdx.x + q] = run;
-            run += c[q];
+        for (int w = 0; w < kWaves; ++w)
+            if (w < wid) carry += tmp[w];
+        for (int r = 0; r < kSeg; r += kWave) {
+            const int32_t v = seg[r + lane];
+            const int32_t incl = wave_incl_scan_add(v);
+            seg[r + lane] = carry + incl - v;
+            carry += wave_last(incl);
         }
         __syncthreads();
     }
