@@ -22,6 +22,8 @@
 //                       updates its register.  The chain is serial by
 //                       definition, so this kernel runs at the latency of one
 //                       wavefront.
+#include <type_traits>
+
 #include "maps_internal.hpp"
 
 namespace maps {
@@ -216,91 +218,147 @@ __device__ inline uint64_t best_b_key(int64_t B, int32_t d, int32_t D) {
     return d < D ? (uint64_t(B + kBlockLimit) << 10) | uint64_t(1023 - d) : 0;
 }
 
+// The same order in 32 bits for a run of arrivals whose needs sum to less
+// than 2^21 blocks: B_eff relative to the largest one at the run's start,
+// `top` (B - top + 2^21, at least 1 for every B the largest can still reach,
+// 0 for the lower ones, which cannot become the largest within the run).
+constexpr int64_t kNarrowSpan = int64_t(1) << 21;
+__device__ inline uint32_t best_b_key32(int64_t B, int64_t top, int32_t d, int32_t D) {
+    if (d >= D) return 0;
+    const int64_t r = B - top + kNarrowSpan;
+    return (uint32_t(r > 0 ? r : 0) << 10) | uint32_t(1023 - d);
+}
+
 // kSlots decoders per lane: decoder lane + 64 s in slot s, with its B_eff,
 // queue length and largest-B_eff key in registers.  The largest key over all
 // decoders is kept between arrivals (only the chosen decoder's changes): an
 // arrival whose B_need exceeds it takes that decoder at once; only a
 // feasible shortest-queue choice scans every decoder.  The chosen decoder's
 // lane and slot are the same in every lane, so its update is one scalar
-// branch to one slot's code.
+// branch to one slot's code.  The arrivals go 64 at a time (one per lane,
+// read out with readlane); a run of 64 whose needs sum to less than 2^21
+// blocks and whose queues stay below 2^21 keeps its keys in 32 bits (one DPP
+// reduction per arrival instead of two), any other run in 64 bits.
+template <int kSlots, bool kNarrow>
+__device__ __forceinline__ void reserve_run(const StaticArgs& a, int64_t c0, int cnt, int64_t my_need,
+                                            int64_t (&B)[kSlots], int64_t (&Q)[kSlots], int64_t& bmax_all,
+                                            bool& range_bad, int32_t& out_d, uint8_t& out_f) {
+    using Key = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
+    const int lane = threadIdx.x;
+    const bool mq = a.policy == MAPS_POLICY_MQ;
+    const int64_t top = bmax_all;   // the largest B_eff at the run's start
+    Key K[kSlots];
+    auto key_of = [&](int64_t b, int32_t d) -> Key {
+        if constexpr (kNarrow) return best_b_key32(b, top, d, a.D);
+        else return best_b_key(b, d, a.D);
+    };
+    auto wave_max = [&](Key v) -> Key {
+        if constexpr (kNarrow) return wave_max_u32(v);
+        else return wave_max_u64(v);
+    };
+    auto lane_best = [&]() {
+        Key m = K[0];
+#pragma unroll
+        for (int s = 1; s < kSlots; ++s) m = K[s] > m ? K[s] : m;
+        return m;
+    };
+#pragma unroll
+    for (int s = 0; s < kSlots; ++s) K[s] = key_of(B[s], lane + s * kWave);
+    Key kb = wave_max(lane_best());
+    auto largest = [&](Key k) -> int64_t {
+        if constexpr (kNarrow) return top + int64_t(k >> 10) - kNarrowSpan;
+        else return int64_t(k >> 10) - kBlockLimit;
+    };
+    for (int j = 0; j < cnt; ++j) {
+        const int64_t need = (int64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(my_need) >> 32), j)))
+                              << 32) |
+                             uint32_t(__builtin_amdgcn_readlane(int32_t(my_need), j));
+        int32_t best;
+        uint8_t f;
+        if (need < 0) {
+            best = int32_t((a.rr_offset + c0 + j) % a.D);
+            f = 2;
+        } else {
+            const int64_t bmax = largest(kb);
+            if (mq && need <= bmax) {
+                // feasible decoders exist: (Q, decoder) among them, smallest first
+                Key kf = ~Key(0);
+#pragma unroll
+                for (int s = 0; s < kSlots; ++s) {
+                    const int32_t d = lane + s * kWave;
+                    const Key k1 = kNarrow ? Key((uint64_t(Q[s]) << 10) | uint64_t(d))
+                                           : Key((uint64_t(Q[s]) << 20) | uint64_t(d));
+                    if (d < a.D && need <= B[s] && k1 < kf) kf = k1;
+                }
+                kf = ~wave_max(~kf);
+                best = int32_t(kf & (kNarrow ? 0x3FF : 0xFFFFF));
+                f = 1;
+            } else {
+                best = 1023 - int32_t(kb & 1023);
+                f = need <= bmax ? 1 : 0;
+            }
+        }
+        // the owning lane reserves and enqueues; a reservation changes the largest B_eff
+        const int owner = best % kWave, slot = best / kWave;
+        if (lane == owner) {
+#pragma unroll
+            for (int s = 0; s < kSlots; ++s) {
+                if (s == slot) {   // uniform: a scalar branch
+                    if (need >= 0) {
+                        B[s] -= need;
+                        K[s] = key_of(B[s], best);
+                    }
+                    Q[s] += 1;
+                    if constexpr (!kNarrow) range_bad |= B[s] <= -kBlockLimit || B[s] >= kBlockLimit;
+                }
+            }
+        }
+        if (need >= 0) kb = wave_max(lane_best());
+        if (lane == j) {
+            out_d = best;
+            out_f = f;
+        }
+    }
+    bmax_all = largest(kb);
+    if constexpr (kNarrow) {
+        // B only decreases: the run's end shows whether any left the packed-key range
+#pragma unroll
+        for (int s = 0; s < kSlots; ++s) range_bad |= B[s] <= -kBlockLimit;
+    }
+}
+
 template <int kSlots>
 __global__ __launch_bounds__(kWave) void static_reserve(StaticArgs a) {
     const int lane = threadIdx.x;
     int64_t B[kSlots];
     int64_t Q[kSlots];
-    uint64_t K[kSlots];
+    uint64_t k0 = 0;
 #pragma unroll
     for (int s = 0; s < kSlots; ++s) {
         const int32_t d = lane + s * kWave;
         B[s] = d < a.D ? a.beff[d] : 0;
         Q[s] = d < a.D ? a.qlen[d] : 0;
-        K[s] = best_b_key(B[s], d, a.D);
+        const uint64_t k = best_b_key(B[s], d, a.D);
+        k0 = k > k0 ? k : k0;
     }
-    auto lane_best = [&]() {
-        uint64_t m = K[0];
-#pragma unroll
-        for (int s = 1; s < kSlots; ++s) m = K[s] > m ? K[s] : m;
-        return m;
-    };
-    const bool mq = a.policy == MAPS_POLICY_MQ;
+    int64_t bmax_all = int64_t(wave_max_u64(k0) >> 10) - kBlockLimit;   // the largest B_eff
     bool range_bad = false;
-    uint64_t kb = wave_max_u64(lane_best());
     for (int64_t c0 = 0; c0 < a.A; c0 += kWave) {
-        // 64 arrivals at a time: one per lane, read out with readlane
         const int64_t mine = c0 + lane;
         const int64_t my_need = mine < a.A ? a.need[mine] : -1;
         int32_t out_d = 0;
         uint8_t out_f = 0;
         const int cnt = a.A - c0 < kWave ? int(a.A - c0) : kWave;
-        for (int j = 0; j < cnt; ++j) {
-            const int64_t need = (int64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(my_need) >> 32), j)))
-                                  << 32) |
-                                 uint32_t(__builtin_amdgcn_readlane(int32_t(my_need), j));
-            int32_t best;
-            uint8_t f;
-            if (need < 0) {
-                best = int32_t((a.rr_offset + c0 + j) % a.D);
-                f = 2;
-            } else {
-                const int64_t bmax = int64_t(kb >> 10) - kBlockLimit;
-                if (mq && need <= bmax) {
-                    // feasible decoders exist: (Q, decoder) among them, smallest first
-                    uint64_t kf = ~uint64_t(0);
+        // the run's needs and the longest queue after it decide the key width (the same in every lane)
+        int64_t qmax = 0;
 #pragma unroll
-                    for (int s = 0; s < kSlots; ++s) {
-                        const int32_t d = lane + s * kWave;
-                        const uint64_t k1 = (uint64_t(Q[s]) << 20) | uint64_t(d);
-                        if (d < a.D && need <= B[s] && k1 < kf) kf = k1;
-                    }
-                    kf = wave_min_u64(kf);
-                    best = int32_t(kf & 0xFFFFF);
-                    f = 1;
-                } else {
-                    best = 1023 - int32_t(kb & 1023);
-                    f = need <= bmax ? 1 : 0;
-                }
-            }
-            // the owning lane reserves and enqueues; a reservation changes the largest B_eff
-            const int owner = best % kWave, slot = best / kWave;
-            if (lane == owner) {
-#pragma unroll
-                for (int s = 0; s < kSlots; ++s) {
-                    if (s == slot) {   // uniform: a scalar branch
-                        if (need >= 0) {
-                            B[s] -= need;
-                            K[s] = best_b_key(B[s], best, a.D);
-                        }
-                        Q[s] += 1;
-                        range_bad |= B[s] <= -kBlockLimit || B[s] >= kBlockLimit;
-                    }
-                }
-            }
-            if (need >= 0) kb = wave_max_u64(lane_best());
-            if (lane == j) {
-                out_d = best;
-                out_f = f;
-            }
-        }
+        for (int s = 0; s < kSlots; ++s) qmax = Q[s] > qmax ? Q[s] : qmax;
+        qmax = int64_t(wave_max_u64(uint64_t(qmax)));
+        const int64_t need_sum = wave_reduce_add(my_need > 0 ? my_need : int64_t(0));
+        if (need_sum < kNarrowSpan - 1 && qmax + kWave < kNarrowSpan)
+            reserve_run<kSlots, true>(a, c0, cnt, my_need, B, Q, bmax_all, range_bad, out_d, out_f);
+        else
+            reserve_run<kSlots, false>(a, c0, cnt, my_need, B, Q, bmax_all, range_bad, out_d, out_f);
         if (mine < a.A) {
             a.choice[mine] = out_d;
             a.flags[mine] = out_f;

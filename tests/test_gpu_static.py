@@ -91,6 +91,43 @@ def test_ragged_shapes(orc, D, A, policy):
         _compare(got, want, f"D{D} A{A} reserve={reserve}")
 
 
+@pytest.mark.parametrize("case", ["wide", "alternating", "long_queues", "spread"])
+@pytest.mark.parametrize("policy", [0, 1])
+def test_reserve_key_widths(orc, case, policy):
+    """The reserving chain takes each run of 64 arrivals with 32-bit keys when
+    its needs sum to less than 2^21 blocks and the queues stay below 2^21,
+    else with 64-bit keys: runs of huge needs only, narrow and wide runs in
+    turn, queues past 2^21, and decoders 2^21 blocks or more below the largest
+    B_eff (their 32-bit keys saturate) with some decoders feasible."""
+    rng = np.random.default_rng(len(case) * 7 + policy)
+    D, A, S = 200, 1000, 1
+    B = rng.integers(-3000, 6000, size=D)
+    Q = rng.integers(0, 8, size=D)
+    a_p = rng.integers(0, 20000, size=A)
+    a_U = rng.integers(-3, 40000, size=A)
+    if case == "wide":
+        a_p = rng.integers(10**6, 10**8, size=A)
+    elif case == "alternating":
+        huge = (np.arange(A) // 64) % 2 == 1
+        a_p = np.where(huge, rng.integers(10**6, 10**8, size=A), rng.integers(0, 200, size=A))
+        a_U = np.where(huge, a_U, rng.integers(-1, 300, size=A))
+    elif case == "long_queues":
+        Q = rng.integers(2**21 - 40, 2**21 + 40, size=D)
+        a_p = rng.integers(0, 200, size=A)
+        a_U = rng.integers(-1, 300, size=A)
+    else:   # spread: half the decoders near the largest B_eff, the rest 2^21 or more below, a few at the edge
+        B = np.concatenate([rng.integers(10**9, 10**9 + 5000, size=D // 2),
+                            rng.integers(-10**9, 10**9 - 10**7, size=D - D // 2)])
+        B[-5:] = B[: D // 2].max() - 2**21 + np.arange(-2, 3)
+        a_p = rng.integers(0, 300, size=A)
+        a_U = rng.integers(-1, 1000, size=A)
+    a_p, a_U = a_p.astype(np.int32), a_U.astype(np.int32)
+    want = orc.place_static(B, Q, S, a_p, a_U, policy, 7, True)
+    got = _static(B, Q, S, a_p, a_U, policy, 7, True)
+    assert got[5] == 0
+    _compare(got, want, f"key widths {case} policy={policy}")
+
+
 def test_water_filling_with_reservation(orc):
     """Every decoder feasible throughout: shortest queues fill level by level."""
     D, A = 37, 5000
