@@ -538,7 +538,8 @@ maps_status maps_place_order(const void* snapshot, int32_t D, int32_t u_max,
  * milliseconds of the FIFO queue length; span[s][2] = first arrival, last
  * completion.  The high-pressure fraction of App. A is stats[s][0][d] /
  * (span[s][1] - span[s][0]).
- * workspace: maps_simulate_workspace_size(N, n, S) bytes (the FIFO queues).
+ * workspace: maps_simulate_workspace_size(N, n, S) bytes (the FIFO queues:
+ * 16 bytes per request slot, S N n slots).
  * One wavefront per simulation; N <= MAPS_MAX_SIM_DECODERS and at most
  * MAPS_MAX_SIM_READY admitted requests per decoder at a time.
  * dev_err bits: SIM_INPUT, SIM_READY (outputs unspecified when set).

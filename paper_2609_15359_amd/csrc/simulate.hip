@@ -18,8 +18,12 @@
 // completion is a wavefront minimum; it stays valid until the decoder's queue
 // changes.  When a completion is due the completing request is the last of
 // the rotated queue, and an admission appends at the end: both O(1).  The
-// FIFO queues live in the workspace (one ring per decoder), the per-decoder
-// counters in LDS.  Every loop is bounded: an arrival or a completion is
+// ready queue keeps each request's demand beside it, and the next 64
+// arrivals (time, prompt, output, bound) sit in the lanes' registers, so
+// neither a completion nor an arrival waits on a global load.  The FIFO
+// queues live in the workspace (one ring per decoder, 16 bytes an entry:
+// id, prompt, output, bound), the head's entry and the per-decoder counters
+// in LDS, so only an admission from a queue loads (its successor's entry).  Every loop is bounded: an arrival or a completion is
 // consumed per event, and a simulation that could not progress reports an
 // error instead of spinning.
 #include "maps_internal.hpp"
@@ -48,7 +52,7 @@ struct SimArgs {
     int32_t* routed;          // [S][n] (nullable)
     int64_t* stats;           // [S][5][N]: hp_time, hp_max, hp_count, max_queue, queue_area
     int64_t* span;            // [S][2]
-    int32_t* fifo;            // workspace [S][N][n]
+    int4* fifo;               // workspace [S][N][n]: {id, prompt, output, bound}
     uint32_t* dev_err;
 };
 
@@ -58,6 +62,7 @@ struct DecState {             // per decoder, in LDS
     int64_t t_sync;           // the ready queue's tokens-left are as of this time
     int64_t run, hp_time, hp_max, hp_count, max_queue, queue_area;
     int32_t nready, q_head, q_count, pad;
+    int4 head;                // the FIFO head's {id, prompt, output, bound} while q_count > 0
 };
 
 __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
@@ -69,10 +74,11 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
     const int64_t n = a.n, C = a.C;
     int32_t* rid = lds;                         // [N][kReady] request ids in service order
     int32_t* rleft = lds + N * kReady;          // [N][kReady] tokens left as of t_sync
+    uint32_t* rdem = reinterpret_cast<uint32_t*>(lds + 2 * N * kReady);   // [N][kReady] demands L_p + L_out
     const int64_t* arr = a.arrival + int64_t(s) * n;
     int64_t* fin = a.finish + int64_t(s) * n;
     int32_t* rout = a.routed ? a.routed + int64_t(s) * n : nullptr;
-    int32_t* fifo = a.fifo + int64_t(s) * N * n;
+    int4* fifo = a.fifo + int64_t(s) * N * n;
     const int32_t policy = a.policy[s];
     bool bad_input = false, ready_full = false;
 
@@ -84,8 +90,30 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
     }
     __syncthreads();
 
-    auto demand = [&](int64_t i) { return int64_t(a.prompt[i]) + a.output[i]; };
-    auto need = [&](int64_t i) { return int64_t(a.prompt[i]) + a.bound[i]; };
+    // The next 64 arrivals in lane registers (lane k: request wbase + k), refilled by one coalesced load
+    // when the arrivals pass them; read with readlane at a uniform index.
+    int64_t wbase = 0, w_arr = kNever;
+    int32_t w_p = 0, w_o = 0, w_b = -1;
+    auto refill = [&](int64_t base) {
+        wbase = base;
+        const int64_t i = base + lane;
+        w_arr = i < n ? arr[i] : kNever;
+        w_p = i < n ? a.prompt[i] : 0;
+        w_o = i < n ? a.output[i] : 0;
+        w_b = i < n ? a.bound[i] : -1;
+    };
+    auto rl32 = [](int32_t v, int j) { return __builtin_amdgcn_readlane(v, j); };
+    auto rl64 = [](int64_t v, int j) {
+        return int64_t((uint64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(v) >> 32), j))) << 32) |
+                       uint32_t(__builtin_amdgcn_readlane(int32_t(v), j)));
+    };
+    // arrival time of request `next` (kNever past the last), the window moved up to it when passed
+    auto arrival_of_next = [&](int64_t nx) -> int64_t {
+        if (nx >= n) return kNever;
+        if (nx >= wbase + kWave) refill(nx);
+        return rl64(w_arr, int(nx - wbase));
+    };
+    refill(0);
 
     // bring decoder d's ready queue to time t: m slices since t_sync
     auto sync = [&](int d, int64_t t) {
@@ -96,23 +124,28 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             const int64_t q = m / nr;
             const int32_t r = int32_t(m % nr);
             int32_t id[kPerLane], lf[kPerLane];
+            uint32_t dm[kPerLane];
 #pragma unroll
             for (int j = 0; j < kPerLane; ++j) {   // new position k takes old position (k + r) mod nr
+                if (j * kWave >= nr) break;         // uniform: only the rows of 64 that hold entries
                 const int32_t k = lane + j * kWave;
                 if (k < nr) {
                     int32_t src = k + r;
                     src = src >= nr ? src - nr : src;
                     id[j] = rid[d * kReady + src];
                     lf[j] = int32_t(rleft[d * kReady + src] - q - (src < r ? 1 : 0));
+                    dm[j] = rdem[d * kReady + src];
                 }
             }
             __syncthreads();
 #pragma unroll
             for (int j = 0; j < kPerLane; ++j) {
+                if (j * kWave >= nr) break;
                 const int32_t k = lane + j * kWave;
                 if (k < nr) {
                     rid[d * kReady + k] = id[j];
                     rleft[d * kReady + k] = lf[j];
+                    rdem[d * kReady + k] = dm[j];
                 }
             }
         }
@@ -125,6 +158,7 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         const int32_t nr = st[d].nready;
         int64_t best = kNever;
         for (int j = 0; j < kPerLane; ++j) {
+            if (j * kWave >= nr) break;
             const int32_t k = lane + j * kWave;
             if (k < nr) {
                 const int64_t sk = int64_t(rleft[d * kReady + k] - 1) * nr + k + 1;
@@ -136,21 +170,23 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         if (lane == 0) st[d].next_done = nr > 0 ? t + best : kNever;
         __syncthreads();
     };
-    auto admit = [&](int d, int64_t i, int64_t t) {   // append to the ready queue (synced to t)
+    // append request i (output o, demand dem) to the ready queue (synced to t)
+    auto admit = [&](int d, int64_t i, int32_t o, int64_t dem, int64_t t) {
         if (st[d].nready >= kReady) { ready_full = true; return false; }
         sync(d, t);
         if (lane == 0) {
             const int32_t k = st[d].nready;
             rid[d * kReady + k] = int32_t(i);
-            rleft[d * kReady + k] = a.output[i];
+            rleft[d * kReady + k] = o;
+            rdem[d * kReady + k] = uint32_t(dem);
             st[d].nready = k + 1;
-            st[d].K += demand(i);
+            st[d].K += dem;
         }
         __syncthreads();
         return true;
     };
 
-    int64_t t = arr[0], next = 0, done = 0, last = t;
+    int64_t t = arrival_of_next(0), next = 0, done = 0, last = t;
     uint32_t dirty = 0;   // decoders whose ready queue changed at t (bit d)
     const int64_t max_events = 2 * n + 8;
     for (int64_t ev = 0;; ++ev) {
@@ -163,7 +199,7 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
                 const int32_t k = st[d].nready - 1;
                 const int64_t i = rid[d * kReady + k];
                 st[d].nready = k;
-                st[d].K -= demand(i);
+                st[d].K -= int64_t(rdem[d * kReady + k]);
                 fin[i] = t;
             }
             __syncthreads();
@@ -175,33 +211,41 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         // 2. FIFO admission
         for (int d = 0; d < N; ++d) {
             while (st[d].q_count > 0) {
-                const int64_t i = fifo[int64_t(d) * n + st[d].q_head];
-                if (st[d].K + demand(i) > C) break;
-                if (!admit(d, i, t)) break;
+                const int4 h = st[d].head;
+                const int64_t dem = int64_t(h.y) + h.z;
+                if (st[d].K + dem > C) break;
+                if (!admit(d, h.x, h.z, dem, t)) break;
                 if (lane == 0) {
                     st[d].q_head = st[d].q_head + 1 == n ? 0 : st[d].q_head + 1;
                     st[d].q_count -= 1;
-                    if (policy == 1 && a.bound[i] >= 0) st[d].R -= need(i);
+                    if (policy == 1 && h.w >= 0) st[d].R -= int64_t(h.y) + h.w;
+                    // the next head's entry: one 16-byte load, only after an admission
+                    if (st[d].q_count > 0) st[d].head = fifo[int64_t(d) * n + st[d].q_head];
                 }
                 __syncthreads();
                 dirty |= 1u << d;
             }
         }
         // 3. arrivals at t, in index order
-        while (next < n && arr[next] <= t) {
+        while (next < n) {
+            const int64_t ai = arrival_of_next(next);
+            if (ai > t) break;
+            const int j = int(next - wbase);
+            const int32_t pi = rl32(w_p, j), oi = rl32(w_o, j), bi = rl32(w_b, j);
             const int64_t i = next++;
-            if (arr[i] < t || a.prompt[i] < 0 || a.output[i] < 1 || demand(i) > C) {
+            const int64_t dem = int64_t(pi) + oi, nd = int64_t(pi) + bi;
+            if (ai < t || pi < 0 || oi < 1 || dem > C) {
                 bad_input = true;   // out of order or never admissible: dropped
                 if (lane == 0) fin[i] = t;
                 done += 1;
                 continue;
             }
             int d;
-            if (policy == 1 && a.bound[i] >= 0) {   // Algorithm 1 at block size 1
+            if (policy == 1 && bi >= 0) {   // Algorithm 1 at block size 1
                 int feas = -1, most = 0;
                 for (int k = 0; k < N; ++k) {
                     const int64_t beff = C - st[k].K - st[k].R;
-                    if (need(i) <= beff && (feas < 0 || st[k].q_count < st[feas].q_count)) feas = k;
+                    if (nd <= beff && (feas < 0 || st[k].q_count < st[feas].q_count)) feas = k;
                     if (beff > C - st[most].K - st[most].R) most = k;
                 }
                 d = feas >= 0 ? feas : most;
@@ -210,17 +254,19 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             }
             if (lane == 0 && rout) rout[i] = d;
             bool queued = true;
-            if (st[d].q_count == 0 && st[d].K + demand(i) <= C) {
-                queued = !admit(d, i, t);
+            if (st[d].q_count == 0 && st[d].K + dem <= C) {
+                queued = !admit(d, i, oi, dem, t);
                 if (!queued) dirty |= 1u << d;
             }
             if (queued) {
                 if (lane == 0) {
                     int64_t tail = st[d].q_head + st[d].q_count;
                     tail = tail >= n ? tail - n : tail;
-                    fifo[int64_t(d) * n + tail] = int32_t(i);
+                    const int4 e = make_int4(int32_t(i), pi, oi, bi);
+                    fifo[int64_t(d) * n + tail] = e;
+                    if (st[d].q_count == 0) st[d].head = e;
                     st[d].q_count += 1;
-                    if (policy == 1 && a.bound[i] >= 0) st[d].R += need(i);
+                    if (policy == 1 && bi >= 0) st[d].R += nd;
                 }
                 __syncthreads();
             }
@@ -230,7 +276,7 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             if (dirty & (1u << d)) schedule(d, t);
         dirty = 0;
         // the next event, and the state recorded over [t, t_next)
-        int64_t t_next = next < n ? arr[next] : kNever;
+        int64_t t_next = arrival_of_next(next);
         for (int d = 0; d < N; ++d) t_next = st[d].next_done < t_next ? st[d].next_done : t_next;
         if (t_next == kNever || t_next <= t) { bad_input = true; break; }
         const int64_t len = t_next - t;
@@ -273,7 +319,7 @@ using namespace maps;
 
 extern "C" size_t maps_simulate_workspace_size(int32_t N, int64_t n, int32_t S) {
     if (N < 1 || N > MAPS_MAX_SIM_DECODERS || n < 1 || S < 0) return 0;
-    return align256(size_t(S) * size_t(N) * size_t(n) * sizeof(int32_t));
+    return align256(size_t(S) * size_t(N) * size_t(n) * sizeof(int4));
 }
 
 extern "C" maps_status maps_simulate(int32_t N, int64_t C, int32_t theta_ppm, int64_t n, int32_t S,
@@ -290,8 +336,8 @@ extern "C" maps_status maps_simulate(int32_t N, int64_t C, int32_t theta_ppm, in
         return MAPS_E_NULL;
     if (workspace_bytes < maps_simulate_workspace_size(N, n, S)) return MAPS_E_WORKSPACE;
     SimArgs a{N, C, theta_ppm, n, S, arrival_ms, prompt, output, bound, policy, finish_ms, routed, stats, span,
-              static_cast<int32_t*>(workspace), dev_err};
-    const size_t lds = size_t(N) * kReady * 2 * sizeof(int32_t);
+              static_cast<int4*>(workspace), dev_err};
+    const size_t lds = size_t(N) * kReady * 3 * sizeof(int32_t);
     allow_dynamic_lds(simulate_kernel, lds);
     hipLaunchKernelGGL(simulate_kernel, dim3(unsigned(S)), dim3(kSimNT), lds, stream, a);
     MAPS_CHECK_LAUNCH();
