@@ -33,6 +33,7 @@ namespace {
 
 constexpr int kSimNT = kWave;      // one wavefront per simulation
 constexpr int kMaxDec = MAPS_MAX_SIM_DECODERS;
+static_assert(kMaxDec <= kWave, "each decoder's state lives in one lane");
 constexpr int kReady = MAPS_MAX_SIM_READY;
 constexpr int kPerLane = kReady / kWave;
 constexpr int64_t kNever = INT64_MAX;
@@ -56,18 +57,25 @@ struct SimArgs {
     uint32_t* dev_err;
 };
 
-struct DecState {             // per decoder, in LDS
+// Decoder d's state lives in lane d's registers (N <= 8 < 64): every lane
+// reads it with readlane at the uniform index d, lane d alone writes it.
+struct DecRegs {
     int64_t K, R;             // tokens held; needs reserved by queued requests (policy 1)
     int64_t next_done;        // time of the next completion (kNever when the ready queue is empty)
     int64_t t_sync;           // the ready queue's tokens-left are as of this time
     int64_t run, hp_time, hp_max, hp_count, max_queue, queue_area;
-    int32_t nready, q_head, q_count, pad;
+    int32_t nready, q_head, q_count;
     int4 head;                // the FIFO head's {id, prompt, output, bound} while q_count > 0
 };
 
+__device__ inline int32_t rl32(int32_t v, int j) { return __builtin_amdgcn_readlane(v, j); }
+__device__ inline int64_t rl64(int64_t v, int j) {
+    return int64_t((uint64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(v) >> 32), j))) << 32) |
+                   uint32_t(__builtin_amdgcn_readlane(int32_t(v), j)));
+}
+
 __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
     extern __shared__ int32_t lds[];
-    __shared__ DecState st[kMaxDec];
     const int s = blockIdx.x;
     const int lane = threadIdx.x;
     const int32_t N = a.N;
@@ -82,14 +90,6 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
     const int32_t policy = a.policy[s];
     bool bad_input = false, ready_full = false;
 
-    if (lane < N) {
-        DecState z{};
-        z.next_done = kNever;
-        z.t_sync = arr[0];
-        st[lane] = z;
-    }
-    __syncthreads();
-
     // The next 64 arrivals in lane registers (lane k: request wbase + k), refilled by one coalesced load
     // when the arrivals pass them; read with readlane at a uniform index.
     int64_t wbase = 0, w_arr = kNever;
@@ -102,11 +102,6 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         w_o = i < n ? a.output[i] : 0;
         w_b = i < n ? a.bound[i] : -1;
     };
-    auto rl32 = [](int32_t v, int j) { return __builtin_amdgcn_readlane(v, j); };
-    auto rl64 = [](int64_t v, int j) {
-        return int64_t((uint64_t(uint32_t(__builtin_amdgcn_readlane(int32_t(uint64_t(v) >> 32), j))) << 32) |
-                       uint32_t(__builtin_amdgcn_readlane(int32_t(v), j)));
-    };
     // arrival time of request `next` (kNever past the last), the window moved up to it when passed
     auto arrival_of_next = [&](int64_t nx) -> int64_t {
         if (nx >= n) return kNever;
@@ -115,11 +110,14 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
     };
     refill(0);
 
+    DecRegs me{};   // this lane's decoder (lanes < N)
+    me.next_done = kNever;
+    me.t_sync = rl64(w_arr, 0);   // the first arrival
+
     // bring decoder d's ready queue to time t: m slices since t_sync
     auto sync = [&](int d, int64_t t) {
-        const int32_t nr = st[d].nready;
-        const int64_t m = t - st[d].t_sync;
-        __syncthreads();
+        const int32_t nr = rl32(me.nready, d);
+        const int64_t m = t - rl64(me.t_sync, d);
         if (nr > 0 && m > 0) {
             const int64_t q = m / nr;
             const int32_t r = int32_t(m % nr);
@@ -148,14 +146,13 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
                     rdem[d * kReady + k] = dm[j];
                 }
             }
+            __syncthreads();
         }
-        __syncthreads();
-        if (lane == 0) st[d].t_sync = t;
-        __syncthreads();
+        if (lane == d) me.t_sync = t;
     };
     // decoder d's next completion after a change of its ready queue (synced to t)
     auto schedule = [&](int d, int64_t t) {
-        const int32_t nr = st[d].nready;
+        const int32_t nr = rl32(me.nready, d);
         int64_t best = kNever;
         for (int j = 0; j < kPerLane; ++j) {
             if (j * kWave >= nr) break;
@@ -166,21 +163,21 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             }
         }
         best = -wave_reduce_max(-best);   // the wavefront minimum (kNever = INT64_MAX negates safely)
-        __syncthreads();
-        if (lane == 0) st[d].next_done = nr > 0 ? t + best : kNever;
-        __syncthreads();
+        if (lane == d) me.next_done = nr > 0 ? t + best : kNever;
     };
     // append request i (output o, demand dem) to the ready queue (synced to t)
     auto admit = [&](int d, int64_t i, int32_t o, int64_t dem, int64_t t) {
-        if (st[d].nready >= kReady) { ready_full = true; return false; }
+        if (rl32(me.nready, d) >= kReady) { ready_full = true; return false; }
         sync(d, t);
+        const int32_t k = rl32(me.nready, d);
         if (lane == 0) {
-            const int32_t k = st[d].nready;
             rid[d * kReady + k] = int32_t(i);
             rleft[d * kReady + k] = o;
             rdem[d * kReady + k] = uint32_t(dem);
-            st[d].nready = k + 1;
-            st[d].K += dem;
+        }
+        if (lane == d) {
+            me.nready = k + 1;
+            me.K += dem;
         }
         __syncthreads();
         return true;
@@ -193,16 +190,16 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         if (ev > max_events) { bad_input = true; break; }
         // 1. completions at t: the completing request is the last of the synced queue
         for (int d = 0; d < N; ++d) {
-            if (st[d].next_done != t) continue;
+            if (rl64(me.next_done, d) != t) continue;
             sync(d, t);
-            if (lane == 0) {
-                const int32_t k = st[d].nready - 1;
-                const int64_t i = rid[d * kReady + k];
-                st[d].nready = k;
-                st[d].K -= int64_t(rdem[d * kReady + k]);
-                fin[i] = t;
+            const int32_t k = rl32(me.nready, d) - 1;
+            const int64_t i = rid[d * kReady + k];
+            const int64_t dem = int64_t(rdem[d * kReady + k]);
+            if (lane == d) {
+                me.nready = k;
+                me.K -= dem;
             }
-            __syncthreads();
+            if (lane == 0) fin[i] = t;
             done += 1;
             last = t;
             dirty |= 1u << d;
@@ -210,19 +207,21 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         if (done >= n) break;
         // 2. FIFO admission
         for (int d = 0; d < N; ++d) {
-            while (st[d].q_count > 0) {
-                const int4 h = st[d].head;
+            while (rl32(me.q_count, d) > 0) {
+                const int4 h = make_int4(rl32(me.head.x, d), rl32(me.head.y, d), rl32(me.head.z, d),
+                                         rl32(me.head.w, d));
                 const int64_t dem = int64_t(h.y) + h.z;
-                if (st[d].K + dem > C) break;
+                if (rl64(me.K, d) + dem > C) break;
                 if (!admit(d, h.x, h.z, dem, t)) break;
-                if (lane == 0) {
-                    st[d].q_head = st[d].q_head + 1 == n ? 0 : st[d].q_head + 1;
-                    st[d].q_count -= 1;
-                    if (policy == 1 && h.w >= 0) st[d].R -= int64_t(h.y) + h.w;
-                    // the next head's entry: one 16-byte load, only after an admission
-                    if (st[d].q_count > 0) st[d].head = fifo[int64_t(d) * n + st[d].q_head];
+                const int32_t qh = rl32(me.q_head, d), qc = rl32(me.q_count, d) - 1;
+                const int32_t nh = qh + 1 == n ? 0 : qh + 1;
+                if (lane == d) {
+                    me.q_head = nh;
+                    me.q_count = qc;
+                    if (policy == 1 && h.w >= 0) me.R -= int64_t(h.y) + h.w;
+                    // the next head's entry: one 16-byte load, only after an admission (lane d wrote it)
+                    if (qc > 0) me.head = fifo[int64_t(d) * n + nh];
                 }
-                __syncthreads();
                 dirty |= 1u << d;
             }
         }
@@ -243,10 +242,19 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             int d;
             if (policy == 1 && bi >= 0) {   // Algorithm 1 at block size 1
                 int feas = -1, most = 0;
+                int32_t fq = 0;
+                int64_t most_beff = 0;
                 for (int k = 0; k < N; ++k) {
-                    const int64_t beff = C - st[k].K - st[k].R;
-                    if (nd <= beff && (feas < 0 || st[k].q_count < st[feas].q_count)) feas = k;
-                    if (beff > C - st[most].K - st[most].R) most = k;
+                    const int64_t beff = C - rl64(me.K, k) - rl64(me.R, k);
+                    const int32_t qk = rl32(me.q_count, k);
+                    if (nd <= beff && (feas < 0 || qk < fq)) {
+                        feas = k;
+                        fq = qk;
+                    }
+                    if (k == 0 || beff > most_beff) {
+                        most = k;
+                        most_beff = beff;
+                    }
                 }
                 d = feas >= 0 ? feas : most;
             } else {
@@ -254,21 +262,21 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
             }
             if (lane == 0 && rout) rout[i] = d;
             bool queued = true;
-            if (st[d].q_count == 0 && st[d].K + dem <= C) {
+            if (rl32(me.q_count, d) == 0 && rl64(me.K, d) + dem <= C) {
                 queued = !admit(d, i, oi, dem, t);
                 if (!queued) dirty |= 1u << d;
             }
             if (queued) {
-                if (lane == 0) {
-                    int64_t tail = st[d].q_head + st[d].q_count;
-                    tail = tail >= n ? tail - n : tail;
-                    const int4 e = make_int4(int32_t(i), pi, oi, bi);
+                const int32_t qh = rl32(me.q_head, d), qc = rl32(me.q_count, d);
+                int64_t tail = int64_t(qh) + qc;
+                tail = tail >= n ? tail - n : tail;
+                const int4 e = make_int4(int32_t(i), pi, oi, bi);
+                if (lane == d) {   // the lane that reads the ring writes it
                     fifo[int64_t(d) * n + tail] = e;
-                    if (st[d].q_count == 0) st[d].head = e;
-                    st[d].q_count += 1;
-                    if (policy == 1 && bi >= 0) st[d].R += nd;
+                    if (qc == 0) me.head = e;
+                    me.q_count = qc + 1;
+                    if (policy == 1 && bi >= 0) me.R += nd;
                 }
-                __syncthreads();
             }
         }
         if (done >= n) break;   // only dropped requests were left
@@ -277,32 +285,33 @@ __global__ __launch_bounds__(kSimNT) void simulate_kernel(SimArgs a) {
         dirty = 0;
         // the next event, and the state recorded over [t, t_next)
         int64_t t_next = arrival_of_next(next);
-        for (int d = 0; d < N; ++d) t_next = st[d].next_done < t_next ? st[d].next_done : t_next;
+        for (int d = 0; d < N; ++d) {
+            const int64_t nd = rl64(me.next_done, d);
+            t_next = nd < t_next ? nd : t_next;
+        }
         if (t_next == kNever || t_next <= t) { bad_input = true; break; }
         const int64_t len = t_next - t;
         if (lane < N) {
-            DecState& x = st[lane];
-            if (x.K * 1000000 >= int64_t(a.theta_ppm) * C) {
-                if (x.run == 0) x.hp_count += 1;
-                x.run += len;
-                x.hp_time += len;
-                x.hp_max = x.run > x.hp_max ? x.run : x.hp_max;
+            if (me.K * 1000000 >= int64_t(a.theta_ppm) * C) {
+                if (me.run == 0) me.hp_count += 1;
+                me.run += len;
+                me.hp_time += len;
+                me.hp_max = me.run > me.hp_max ? me.run : me.hp_max;
             } else {
-                x.run = 0;
+                me.run = 0;
             }
-            x.queue_area += int64_t(x.q_count) * len;
-            x.max_queue = x.q_count > x.max_queue ? x.q_count : x.max_queue;
+            me.queue_area += int64_t(me.q_count) * len;
+            me.max_queue = me.q_count > me.max_queue ? me.q_count : me.max_queue;
         }
-        __syncthreads();
         t = t_next;
     }
     if (lane < N) {
         int64_t* o = a.stats + int64_t(s) * 5 * N;
-        o[0 * N + lane] = st[lane].hp_time;
-        o[1 * N + lane] = st[lane].hp_max;
-        o[2 * N + lane] = st[lane].hp_count;
-        o[3 * N + lane] = st[lane].max_queue;
-        o[4 * N + lane] = st[lane].queue_area;
+        o[0 * N + lane] = me.hp_time;
+        o[1 * N + lane] = me.hp_max;
+        o[2 * N + lane] = me.hp_count;
+        o[3 * N + lane] = me.max_queue;
+        o[4 * N + lane] = me.queue_area;
     }
     if (lane == 0) {
         a.span[2 * int64_t(s)] = arr[0];
