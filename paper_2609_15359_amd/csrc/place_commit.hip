@@ -262,8 +262,8 @@ __device__ inline void pin(int64_t& x) { asm volatile("" : "+v"(x)); }
 // peak inputs at un into *pre_out, issued with the range's loads.  Returns
 // the new PF(Uc), the same in every thread.  Ends with a barrier after which
 // every store of the commit is visible to the workgroup.
-template <bool kStaged>
-__device__ inline int64_t commit_range(const CommitArgs& a, int64_t* stage, int32_t bd, int64_t p, int32_t Uc,
+template <bool kStaged, typename SType = int64_t>
+__device__ inline int64_t commit_range(const CommitArgs& a, SType* stage, int32_t bd, int64_t p, int32_t Uc,
                                        int32_t un, int32_t pre_d, PeakIn* pre_out, Capture* cap,
                                        int64_t* scan_tmp) {
     const int32_t L = a.L;
@@ -320,7 +320,7 @@ __device__ inline int64_t commit_range(const CommitArgs& a, int64_t* stage, int3
             if (t < e) {
                 o[j] += p + t;
                 O[t] = o[j];
-                if constexpr (kStaged) stage[t] = o[j];
+                if constexpr (kStaged) stage[t] = SType(o[j]);
                 mpre = max64(mpre, o[j] + t);
                 msuf = max64(msuf, o[j]);
             }
@@ -339,14 +339,16 @@ __device__ inline int64_t commit_range(const CommitArgs& a, int64_t* stage, int3
     if (lane == 0) scan_tmp[wid] = incl;
     lds_barrier();
     int64_t after = sa_top;
-    for (int w = wid + 1; w < kSerialWaves; ++w) after = max64(after, scan_tmp[w]);
+#pragma unroll
+    for (int w = 0; w < kSerialWaves; ++w)   // independent reads, one LDS round trip
+        if (w > wid) after = max64(after, scan_tmp[w]);
     const int64_t below = __shfl_down(incl, 1, kWave);
     if (lane + 1 < kWave) after = max64(after, below);
     // the new O of the thread's entries [t0, t0 + kBatch), from LDS or HBM
     auto fetch = [&](int32_t t0, int64_t (&o)[kBatch]) {
         if constexpr (kStaged) {
 #pragma unroll
-            for (int j = 0; j < kBatch; ++j) o[j] = t0 + j < e ? stage[t0 + j] : 0;
+            for (int j = 0; j < kBatch; ++j) o[j] = t0 + j < e ? int64_t(stage[t0 + j]) : 0;
         } else {
 #pragma unroll
             for (int j = 0; j < kBatch; ++j) o[j] = t0 + j < e ? O[t0 + j] : 0;
@@ -495,9 +497,15 @@ __global__ __launch_bounds__(kSerialNT) void commit_serial(CommitArgs a) {
             if (Un >= 0) un = Un < T ? Un : T;
         }
         const int32_t pre_d = kPre && tid < D ? tid : -1;
-        const int64_t v = Uc < a.stage_cap
-                              ? commit_range<true>(a, ostage, bd, p, Uc, un, pre_d, &cur, &cap, scan_tmp)
-                              : commit_range<false>(a, ostage, bd, p, Uc, un, pre_d, &cur, &cap, scan_tmp);
+        // the new O values are at most peak + Uc (O(t) <= O(t) + t <= PF(Uc) <= peak - p, plus p + t): below
+        // 2^31 they fit the stage as 32-bit values, twice as many of them
+        const bool narrow = peak + Uc < int64_t(INT32_MAX);
+        const int64_t v =
+            Uc < a.stage_cap ? commit_range<true>(a, ostage, bd, p, Uc, un, pre_d, &cur, &cap, scan_tmp)
+            : narrow && Uc < 2 * int64_t(a.stage_cap)
+                ? commit_range<true, int32_t>(a, reinterpret_cast<int32_t*>(ostage), bd, p, Uc, un, pre_d, &cur,
+                                              &cap, scan_tmp)
+                : commit_range<false>(a, ostage, bd, p, Uc, un, pre_d, &cur, &cap, scan_tmp);
         if constexpr (kPre) {
             if (un >= 0) {
                 if (tid < D) {
