@@ -90,7 +90,7 @@ __host__ __device__ inline BlkLayout blk_layout(int32_t D, int64_t n_total, int3
     L.W = (((u_max + 1) / 32 + 1) + 1) & ~1;
     L.n_total = n_total;
     // bytes per record, a multiple of 16 so that every slice starts 16-byte aligned
-    L.rec = (size_t(4 + 4 + 8 + 4 + 4) + size_t(blk_gw(S)) * 4 + size_t(S) * 4 + 15) & ~size_t(15);
+    L.rec = (size_t(4 + 4 + 8 + 4 + 4 + 16) + size_t(blk_gw(S)) * 4 + size_t(S) * 4 + 15) & ~size_t(15);
     L.hdr_bytes = align256(sizeof(BlkSnapHeader) + size_t(D) * sizeof(BlkHeader));
     // slice d starts at hdr + d * (8 W + 4 rec + 64) + seg_off[d] * rec with room for capA <= n_d + 4
     // records after at most 48 bytes of padding
@@ -107,6 +107,7 @@ struct BlkSlice {
     int32_t* SMX;
     int32_t* G;      // [capA][Gw]: class c of event e at G[e * Gw + c]
     int32_t* PMX;    // [capA][S]
+    int4* rec;       // [capA]: {tau[e], N[e], SMX[e], SMX[min(e + 1, E)]}, what the pair kernel reads of event e
     int64_t Gw;
 };
 
@@ -135,6 +136,8 @@ __host__ __device__ inline BlkSlice blk_slice(char* snap, int64_t off, const Blk
     s.OB = reinterpret_cast<int32_t*>(q);
     q += capA * 4;
     s.SMX = reinterpret_cast<int32_t*>(q);
+    q += capA * 4;
+    s.rec = reinterpret_cast<int4*>(q);
     return s;
 }
 
@@ -407,15 +410,25 @@ __device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int
             },
             redg);
     }
-    const int32_t base_pk = block_scan<kPbNT, true, true, false, int32_t>(
-        len, 0, [&](int64_t e) { return r.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
-        reinterpret_cast<int32_t*>(red32));
     for (int64_t e = tid; e < len; e += kPbNT) {
         s.tau[e] = e < int64_t(E) ? int32_t(r.tau[e]) : 0;
         s.N[e] = int32_t(r.N[e]);
         s.SX[e] = int64_t(r.SX[e]);
         s.OB[e] = r.OB[e];
     }
+    __syncthreads();   // SX is out: its LDS array takes the suffix maxima
+    int32_t* smx = reinterpret_cast<int32_t*>(r.SX);
+    const int32_t base_pk = block_scan<kPbNT, true, true, false, int32_t>(
+        len, 0, [&](int64_t e) { return r.OB[e]; },
+        [&](int64_t e, int32_t v) {
+            s.SMX[e] = v;
+            smx[e] = v;
+        },
+        reinterpret_cast<int32_t*>(red32));   // ends with a barrier
+    // the pair kernel's record of every event
+    for (int64_t e = tid; e < len; e += kPbNT)
+        s.rec[e] = make_int4(e < int64_t(E) ? int32_t(r.tau[e]) : 0, int32_t(r.N[e]), smx[e],
+                             smx[e + 1 < len ? e + 1 : e]);
     // the class rows in address order, Gw entries an event (the padding past S - 1 classes zero): each
     // wavefront stores whole lines (len Gw is below 2^31 here: fewer than 65,536 records)
     const uint32_t gw = uint32_t(s.Gw);
@@ -581,6 +594,9 @@ __global__ __launch_bounds__(kPbNT) void project_blocks(ProjArgs a) {
     const int32_t base = block_scan<kPbNT, true, true, false, int32_t>(
         len, 0, [&](int64_t e) { return s.OB[e]; }, [&](int64_t e, int32_t v) { s.SMX[e] = v; },
         reinterpret_cast<int32_t*>(red32));
+    sync_global();
+    for (int64_t e = tid; e < len; e += kPbNT)
+        s.rec[e] = make_int4(e < int64_t(E) ? s.tau[e] : 0, s.N[e], s.SMX[e], s.SMX[e + 1 < len ? e + 1 : e]);
     if (tid == 0) {
         hdr[d].slice = off;
         hdr[d].cap = cap;
@@ -755,12 +771,13 @@ __global__ __launch_bounds__(kPairsNT) void blocks_pairs(PairArgs a, int64_t til
             const int64_t gi = u >= 2 ? int64_t(S) - u : 0;
             const int32_t jr = j < E ? j : 0;   // the entries of a real event; E has none
             pmx[k] = s.PMX[int64_t(j) * S + dv.mod(p)];
-            nj[k] = s.N[jr];
+            const int4 rc = s.rec[j];   // tau, N, SMX(j), SMX(j + 1) of event j: one 16-byte load
+            nj[k] = rc.y;
             gj[k] = S > 1 ? s.G[int64_t(jr) * s.Gw + gi] : 0;
             sx[k] = s.SX[jr];
-            tj[k] = s.tau[jr];
-            sm0[k] = s.SMX[j];
-            sm1[k] = s.SMX[j < E ? j + 1 : j];
+            tj[k] = rc.x;
+            sm0[k] = rc.z;
+            sm1[k] = rc.w;
         }
 #pragma unroll
         for (int k = 0; k < kPairsPer; ++k) {
