@@ -338,15 +338,20 @@ def block_placement(b, db, U_res, U_arr, cpu: bool, calls: int = 10):
         ms[name] = statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
     if int(err.item()) != 0:
         raise SystemExit(f"block placement raised {maps.error_names(int(err.item()))}")
+    # the slice arrays placement reads (rank words, residue maxima, class counts, sums, event records), not the
+    # projection's own copies of tau, N, OB and the suffix maxima: 16 B per record slot, a decoder's slots
+    # being its residents + 1 rounded up to a multiple of 4
+    slots = ((np.diff(np.asarray(b.seg_off, dtype=np.int64)) + 1 + 3) // 4) * 4
+    snap_read = snap.data.numel() - 16 * int(slots.sum())
     res = {"block_size": BLOCK, "decoders": D, "arrivals": A, "ms": ms,
            "pairs_per_s": D * A / (ms["place_blocks"] * 1e-3),
            "snapshot_mb": snap.data.numel() / 1e6,
-           # the pair matrix written once, the block snapshot read once, 21 B per arrival in and out
-           "roofline": _hbm_roofline(4 * D * A + snap.data.numel() + 21 * A, ms["place_blocks"],
+           # the pair matrix written once, the snapshot arrays placement reads read once, 21 B per arrival in and out
+           "roofline": _hbm_roofline(4 * D * A + snap_read + 21 * A, ms["place_blocks"],
                                      "maps_place_blocks (blocks_order, blocks_pairs, blocks_finish)"),
            "feasible_fraction": float(np.mean(out.flags.cpu().numpy() & 1)),
            "note": "peaks, capacities and overflow in blocks; the pair matrix always written; the block snapshot "
-                   "is read through L2 (about 150 B per event at 16 tokens per block)"}
+                   "is read through L2 (about 160 B per event at 16 tokens per block)"}
     import oracle
     o = oracle.Oracle()
     k = min(A, 65536)
