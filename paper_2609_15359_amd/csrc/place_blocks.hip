@@ -58,7 +58,9 @@ static_assert(sizeof(BlkSnapHeader) == 64, "block snapshot header size");
 // (E+1 records, the last one for "no resident left") the arrays
 //   PMX[e][rho] (int32), G[e][c-1] = #{xi >= c} for c = 1..S-1 (int32, rows of
 //   Sg = S - 1 rounded up to a multiple of 4), SX[e] (int64), tau[e], N[e],
-//   OB[e], SMX[e] (int32),
+//   OB[e], SMX[e] (int32; the projection's working arrays when the records do
+//   not fit LDS), rec[e] = {tau[e], N[e], SMX[e], SMX[min(e + 1, E)]} (what
+//   placement reads of them),
 // each with room for capA = n_d + 1 rounded up to a multiple of 4 records.
 // PMX starts on a 64-byte boundary and every array is a multiple of 16 bytes
 // long, so every array starts 16-byte aligned; when S is a multiple of 4 so
@@ -410,20 +412,13 @@ __device__ __forceinline__ void project_blocks_lds(const ProjArgs& a, int d, int
             },
             redg);
     }
-    for (int64_t e = tid; e < len; e += kPbNT) {
-        s.tau[e] = e < int64_t(E) ? int32_t(r.tau[e]) : 0;
-        s.N[e] = int32_t(r.N[e]);
-        s.SX[e] = int64_t(r.SX[e]);
-        s.OB[e] = r.OB[e];
-    }
+    // placement reads SX and the event records; tau, N, OB and the suffix maxima as arrays of their own are
+    // the HBM path's working copies and are not written here
+    for (int64_t e = tid; e < len; e += kPbNT) s.SX[e] = int64_t(r.SX[e]);
     __syncthreads();   // SX is out: its LDS array takes the suffix maxima
     int32_t* smx = reinterpret_cast<int32_t*>(r.SX);
     const int32_t base_pk = block_scan<kPbNT, true, true, false, int32_t>(
-        len, 0, [&](int64_t e) { return r.OB[e]; },
-        [&](int64_t e, int32_t v) {
-            s.SMX[e] = v;
-            smx[e] = v;
-        },
+        len, 0, [&](int64_t e) { return r.OB[e]; }, [&](int64_t e, int32_t v) { smx[e] = v; },
         reinterpret_cast<int32_t*>(red32));   // ends with a barrier
     // the pair kernel's record of every event
     for (int64_t e = tid; e < len; e += kPbNT)
