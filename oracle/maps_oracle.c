@@ -25,7 +25,7 @@
  *                starvation promotion, and the App. A admission rule (10)
  *                applied to the reordered queue.
  *
- * Readings of points the paper leaves open (all listed in the design doc):
+ * Readings of points the paper leaves open:
  *   - alpha is an integer in parts per million; the rank is an exact integer
  *     ceiling.  A rank above the bucket size gives an infinite quantile, and
  *     the bound is then the cap u_max.  Bounds are capped at u_max.

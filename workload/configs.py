@@ -4,7 +4,7 @@ Every length is an integer token count.  The length model is the heavy-tailed
 lognormal family the paper's workloads motivate (Sec. 1 and App. A: skewed,
 heavy-tailed output lengths); prompts of the two largest workloads mix in a
 long-context share.  Values not fixed by the workload statement are marked
-"reading" and listed in DESIGN.md.
+"reading".
 """
 from __future__ import annotations
 
